@@ -1,0 +1,716 @@
+/*
+ * lamp_oracle.c -- plain, slow CPU oracle for the LampAttention forward pass.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the independent reference that the
+ * GPU library is checked against.  It shares no code, header, table or
+ * constant generator with the GPU library, and nothing in the product path may
+ * call it: only the test suite, the smoke check and the benchmark's
+ * cpu_baseline leg load it.
+ *
+ * What it computes follows the paper (LampAttention: look-ahead mixed-precision
+ * FlashAttention) section by section:
+ *   - online softmax state (mu, omega) and its update: Sec. 2 (opening);
+ *   - block threat T_theta, descending sort, safety-margin test: Sec. 3.1,
+ *     Eq. (7) ("stage 1");
+ *   - block-LAMP multidimensional knapsack: Sec. 3.1, Eq. (8) ("stage 2");
+ *   - the kernel as a whole: Sec. 3.2, Algorithm 1;
+ *   - number formats e4m3 / ue5m3 / e4m11 / ue5m11 and the 8-bit exp LUT:
+ *     Sec. 3.3, "Floating-point formats";
+ *   - recursive FMA accumulation in FP32 with rounding after every step:
+ *     Sec. 4.1.
+ * Where the paper is silent the readings listed in DESIGN.md ("Readings of the
+ * paper") are taken; each is restated at the place it is used.
+ *
+ * Everything is fp64 except where the method fixes another precision (the
+ * fp32 FMA of the 8-bit accumulation, the formats above).  Build with
+ * -ffp-contract=off: every fused multiply-add below is an explicit fma().
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <float.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* ------------------------------------------------------------------------ */
+/* Number formats (Sec. 3.3).                                                */
+/* ------------------------------------------------------------------------ */
+
+/* A binary floating-point format with `mbits` stored mantissa bits, exponent
+ * bias `bias`, gradual underflow (subnormals) and a largest finite value
+ * `maxval`.  Rounding is round-to-nearest-even; values beyond maxval saturate
+ * to +-maxval (reading: no QK-Norm is assumed, so overflow saturates). */
+typedef struct {
+    int ebits, mbits, bias, is_signed;
+    double maxval;
+} ofmt_t;
+
+/* e4m3 accumulator: OCP E4M3FN, bias 7, largest finite 448 (Sec. 3.3). */
+static const ofmt_t F_E4M3 = {4, 3, 7, 1, 448.0};
+/* e4m11 high-precision accumulator: bias 7, all codes finite,
+ * largest (2 - 2^-11) * 2^8 = 511.875 (Sec. 3.3). */
+static const ofmt_t F_E4M11 = {4, 11, 7, 1, 511.875};
+/* ue5m3 / ue5m11 shifted logits mu_hat - y >= 0 (Sec. 3.3); the paper does
+ * not state a bias, reading: 15. */
+static const ofmt_t F_UE5M3_SHIFT = {5, 3, 15, 0, 122880.0};
+static const ofmt_t F_UE5M11_SHIFT = {5, 11, 15, 0, 131040.0};
+/* ue5m3 / ue5m11 exponentials: bias 31 so that code 11111000 is 1.0, smallest
+ * normal 2^-30, smallest subnormal 2^-33 resp. 2^-41 (Sec. 3.3). */
+static const ofmt_t F_UE5M3_EXP = {5, 3, 31, 0, 1.875};
+static const ofmt_t F_UE5M11_EXP = {5, 11, 31, 0, 2.0 - 0x1p-11};
+
+/* Round an exact double to the format grid (RNE, subnormals, saturation). */
+static double round_to_fmt(double x, const ofmt_t *f)
+{
+    if (isnan(x)) return x;
+    if (x == 0.0) return x;                       /* keeps the sign of zero */
+    double ax = fabs(x);
+    if (isinf(ax)) return copysign(f->maxval, x);
+    int E;
+    (void)frexp(ax, &E);                          /* ax = fr * 2^E, fr in [0.5,1) */
+    int e = E - 1;                                /* ax in [2^e, 2^(e+1)) */
+    int emin = 1 - f->bias;                       /* smallest normal exponent */
+    if (e < emin) e = emin;
+    double quantum = ldexp(1.0, e - f->mbits);
+    double r = nearbyint(ax / quantum) * quantum; /* default mode: ties to even */
+    if (r > f->maxval) r = f->maxval;
+    return copysign(r, x);
+}
+
+/* Code of a value that already lies on the grid. */
+static uint32_t encode_fmt(double v, const ofmt_t *f)
+{
+    uint32_t sign = (f->is_signed && signbit(v)) ? 1u : 0u;
+    double a = fabs(v);
+    int emin = 1 - f->bias;
+    uint32_t e, m;
+    if (a < ldexp(1.0, emin)) {
+        e = 0;
+        m = (uint32_t)(a / ldexp(1.0, emin - f->mbits));
+    } else {
+        int E;
+        (void)frexp(a, &E);
+        int eu = E - 1;
+        e = (uint32_t)(eu + f->bias);
+        m = (uint32_t)(a / ldexp(1.0, eu - f->mbits)) - (1u << f->mbits);
+    }
+    return (sign << (f->ebits + f->mbits)) | (e << f->mbits) | m;
+}
+
+static double decode_fmt(uint32_t code, const ofmt_t *f)
+{
+    uint32_t m = code & ((1u << f->mbits) - 1u);
+    uint32_t e = (code >> f->mbits) & ((1u << f->ebits) - 1u);
+    int sign = f->is_signed ? (int)((code >> (f->ebits + f->mbits)) & 1u) : 0;
+    double v;
+    if (e == 0) v = ldexp((double)m, 1 - f->bias - f->mbits);
+    else v = ldexp((double)((1u << f->mbits) | m), (int)e - f->bias - f->mbits);
+    return sign ? -v : v;
+}
+
+static const ofmt_t *fmt_by_id(int id)
+{
+    switch (id) {
+    case 0: return &F_E4M3;
+    case 1: return &F_E4M11;
+    case 2: return &F_UE5M3_SHIFT;
+    case 3: return &F_UE5M11_SHIFT;
+    case 4: return &F_UE5M3_EXP;
+    case 5: return &F_UE5M11_EXP;
+    default: return NULL;
+    }
+}
+
+/* Exported codec entry points (used by the tests to pin the codecs). */
+int oracle_round_fmt(int fmt_id, const double *x, double *y, int64_t n)
+{
+    const ofmt_t *f = fmt_by_id(fmt_id);
+    if (!f) return -1;
+    for (int64_t i = 0; i < n; ++i) y[i] = round_to_fmt(x[i], f);
+    return 0;
+}
+
+int oracle_encode_fmt(int fmt_id, const double *x, uint32_t *c, int64_t n)
+{
+    const ofmt_t *f = fmt_by_id(fmt_id);
+    if (!f) return -1;
+    for (int64_t i = 0; i < n; ++i) c[i] = encode_fmt(round_to_fmt(x[i], f), f);
+    return 0;
+}
+
+int oracle_decode_fmt(int fmt_id, const uint32_t *c, double *y, int64_t n)
+{
+    const ofmt_t *f = fmt_by_id(fmt_id);
+    if (!f) return -1;
+    for (int64_t i = 0; i < n; ++i) y[i] = decode_fmt(c[i], f);
+    return 0;
+}
+
+/* e4m3 code of every fp32 bit pattern in [start, start+count): used to check
+ * the GPU's rounding exhaustively.  NaN patterns give 0xFF. */
+int oracle_e4m3_of_f32_bits(uint64_t start, int64_t count, uint8_t *out, int nthreads)
+{
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(static)
+#endif
+    for (int64_t i = 0; i < count; ++i) {
+        uint32_t b = (uint32_t)(start + (uint64_t)i);
+        float x;
+        memcpy(&x, &b, 4);
+        if (isnan(x)) { out[i] = 0xFF; continue; }
+        out[i] = (uint8_t)encode_fmt(round_to_fmt((double)x, &F_E4M3), &F_E4M3);
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* exp_doc: the one documented fp64 exponential used for the rescale factor  */
+/* lambda_hat = exp(mu - mu_hat).  The paper takes alpha_hat in high          */
+/* precision (Sec. 2.2, last paragraph); both the oracle and the GPU library  */
+/* evaluate it with the same operations in the same order so that the        */
+/* stage-2 decisions, which depend on omega_hat, agree bit for bit:           */
+/*   x < -700 -> 0;                                                          */
+/*   n = rint(RN(x * LOG2E));  r = fma(-n, LN2_HI, x);  r = fma(-n, LN2_LO, r) */
+/*   p = Horner in fma of sum_{k=0}^{13} r^k / k!  (coefficients RN64(1/k!)) */
+/*   result = ldexp(p, n).                                                   */
+/* LN2_HI is ln 2 truncated to 32 significant bits (so n*LN2_HI is exact),   */
+/* LN2_LO = RN64(ln 2 - LN2_HI), LOG2E = RN64(1/ln 2).                        */
+/* ------------------------------------------------------------------------ */
+static const double ED_LOG2E = 0x1.71547652b82fep+0;
+static const double ED_LN2_HI = 0x1.62e42fee00000p-1;
+static const double ED_LN2_LO = 0x1.a39ef35793c76p-33;
+static const double ED_C[14] = {
+    0x1.0000000000000p+0, 0x1.0000000000000p+0, 0x1.0000000000000p-1,
+    0x1.5555555555555p-3, 0x1.5555555555555p-5, 0x1.1111111111111p-7,
+    0x1.6c16c16c16c17p-10, 0x1.a01a01a01a01ap-13, 0x1.a01a01a01a01ap-16,
+    0x1.71de3a556c734p-19, 0x1.27e4fb7789f5cp-22, 0x1.ae64567f544e4p-26,
+    0x1.1eed8eff8d898p-29, 0x1.6124613a86d09p-33};
+
+static double exp_doc(double x)
+{
+    if (x < -700.0) return 0.0;
+    double n = nearbyint(x * ED_LOG2E);
+    double r = fma(-n, ED_LN2_HI, x);
+    r = fma(-n, ED_LN2_LO, r);
+    double p = ED_C[13];
+    for (int k = 12; k >= 0; --k) p = fma(p, r, ED_C[k]);
+    return ldexp(p, (int)n);
+}
+
+int oracle_exp_doc(const double *x, double *y, int64_t n)
+{
+    for (int64_t i = 0; i < n; ++i) y[i] = exp_doc(x[i]);
+    return 0;
+}
+
+int oracle_exp_doc_constants(double *out /* 17 */)
+{
+    out[0] = ED_LOG2E;
+    out[1] = ED_LN2_HI;
+    out[2] = ED_LN2_LO;
+    for (int k = 0; k < 14; ++k) out[3 + k] = ED_C[k];
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Exponential tables (Sec. 3.3): the 8-bit exp is a look-up table from the  */
+/* ue5m3 shift code to the ue5m3 exp code, E = RN(exp(-s)), correctly         */
+/* rounded (Sec. 4.1 models the exponentials as correctly rounded); the       */
+/* 16-bit exp uses the same rule on ue5m11.  exp is evaluated in long double  */
+/* and every entry is checked to lie clearly away from a rounding midpoint;  */
+/* an entry that does not is reported as an error (never seen for these     */
+/* inputs; the test suite re-derives every entry in 60-digit arithmetic).     */
+/* ------------------------------------------------------------------------ */
+static uint8_t g_lut8[256];
+static uint16_t g_exp16[65536];
+static int g_tables_ok = 0;
+
+static int cr_exp_neg(double s, const ofmt_t *f, uint32_t *code)
+{
+    long double e = expl(-(long double)s);
+    long double elo = e * (1.0L - 0x1p-60L), ehi = e * (1.0L + 0x1p-60L);
+    double r = round_to_fmt((double)e, f);
+    uint32_t c = encode_fmt(r, f);
+    uint32_t cmax = (1u << (f->ebits + f->mbits)) - 1u;
+    /* The enclosure [elo, ehi] of exp(-s) must lie strictly between the
+     * midpoints to the neighbouring grid values; then the exact value rounds
+     * to r as well. */
+    if (c > 0) {
+        long double mb = ((long double)decode_fmt(c - 1, f) + (long double)r) / 2;
+        if (!(elo > mb)) return -1;
+    }
+    if (c < cmax) {
+        long double ma = ((long double)r + (long double)decode_fmt(c + 1, f)) / 2;
+        if (!(ehi < ma)) return -1;
+    }
+    *code = c;
+    return 0;
+}
+
+static int build_tables(void)
+{
+    if (g_tables_ok) return 0;
+    for (uint32_t c = 0; c < 256; ++c) {
+        uint32_t e;
+        if (cr_exp_neg(decode_fmt(c, &F_UE5M3_SHIFT), &F_UE5M3_EXP, &e)) return -1;
+        g_lut8[c] = (uint8_t)e;
+    }
+    for (uint32_t c = 0; c < 65536; ++c) {
+        uint32_t e;
+        if (cr_exp_neg(decode_fmt(c, &F_UE5M11_SHIFT), &F_UE5M11_EXP, &e)) return -1;
+        g_exp16[c] = (uint16_t)e;
+    }
+    g_tables_ok = 1;
+    return 0;
+}
+
+int oracle_tables(uint8_t *lut8, uint16_t *exp16)
+{
+    int rc = build_tables();
+    if (rc) return rc;
+    if (lut8) memcpy(lut8, g_lut8, sizeof g_lut8);
+    if (exp16) memcpy(exp16, g_exp16, sizeof g_exp16);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Logits.                                                                   */
+/* ------------------------------------------------------------------------ */
+
+static float bf16_to_f32(uint16_t b)
+{
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return f;
+}
+
+/* Scale applied to Q before accumulation (Sec. 3.3: the 1/sqrt(d) scaling
+ * is applied before the product is accumulated): s = RN32(1/sqrt(d)). */
+static float scale_of(int d)
+{
+    return (float)(1.0 / sqrt((double)d));
+}
+
+float oracle_scale(int d) { return scale_of(d); }
+
+/* q_tilde = RN32(q * s). */
+static void prescale(const uint16_t *q, int d, float s, float *qt)
+{
+    for (int c = 0; c < d; ++c) qt[c] = (float)((double)bf16_to_f32(q[c]) * (double)s);
+}
+
+/* Low-precision logit (Sec. 4.1 and Alg. 1): recursive summation with one
+ * FP32 FMA per step, the running sum rounded to e4m3 after every step,
+ * channels in ascending order, starting from +0. */
+static double logit8(const float *qt, const uint16_t *k, int d)
+{
+    float acc = 0.0f;
+    for (int c = 0; c < d; ++c) {
+        float t = fmaf(qt[c], bf16_to_f32(k[c]), acc);
+        acc = (float)round_to_fmt((double)t, &F_E4M3);
+    }
+    return (double)acc;
+}
+
+/* High-precision logit (Alg. 1, recompute steps; Sec. 3.3 gives e4m11 as the
+ * 16-bit accumulator format).  Reading: the dot product is accumulated in
+ * fp64 by a sequential FMA chain in ascending channel order (every product
+ * q_tilde*k is exact in fp64) and the sum is rounded once to e4m11. */
+static double logit16(const float *qt, const uint16_t *k, int d)
+{
+    double acc = 0.0;
+    for (int c = 0; c < d; ++c) acc = fma((double)qt[c], (double)bf16_to_f32(k[c]), acc);
+    return round_to_fmt(acc, &F_E4M11);
+}
+
+static int visible(int64_t i, int64_t j, int causal, int window)
+{
+    if (causal && i > j) return 0;
+    if (window > 0 && i <= j - window) return 0;
+    return 1;
+}
+
+/* Y8 codes of rows [row0, row0+nrows) of every (b, h): out[B][Hq][nrows][N],
+ * invisible entries 0xFF. */
+int oracle_logits8(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv, int N, int d,
+                   int causal, int window, int row0, int nrows, uint8_t *out, int nthreads)
+{
+    if (Hq % Hkv) return -1;
+    int G = Hq / Hkv;
+    float s = scale_of(d);
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for collapse(3) schedule(dynamic)
+#endif
+    for (int b = 0; b < B; ++b)
+        for (int h = 0; h < Hq; ++h)
+            for (int r = 0; r < nrows; ++r) {
+                int64_t j = row0 + r;
+                float qt[1024];
+                prescale(q + (((int64_t)b * Hq + h) * N + j) * d, d, s, qt);
+                const uint16_t *kb = k + ((int64_t)b * Hkv + h / G) * N * d;
+                uint8_t *o = out + (((int64_t)b * Hq + h) * nrows + r) * N;
+                for (int64_t i = 0; i < N; ++i) {
+                    if (!visible(i, j, causal, window)) { o[i] = 0xFF; continue; }
+                    o[i] = (uint8_t)encode_fmt(logit8(qt, kb + i * d, d), &F_E4M3);
+                }
+            }
+    return 0;
+}
+
+/* Y16 codes, same layout; invisible entries 0xFFFF (never compared). */
+int oracle_logits16(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv, int N, int d,
+                    int causal, int window, int row0, int nrows, uint16_t *out, int nthreads)
+{
+    if (Hq % Hkv) return -1;
+    int G = Hq / Hkv;
+    float s = scale_of(d);
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for collapse(3) schedule(dynamic)
+#endif
+    for (int b = 0; b < B; ++b)
+        for (int h = 0; h < Hq; ++h)
+            for (int r = 0; r < nrows; ++r) {
+                int64_t j = row0 + r;
+                float qt[1024];
+                prescale(q + (((int64_t)b * Hq + h) * N + j) * d, d, s, qt);
+                const uint16_t *kb = k + ((int64_t)b * Hkv + h / G) * N * d;
+                uint16_t *o = out + (((int64_t)b * Hq + h) * nrows + r) * N;
+                for (int64_t i = 0; i < N; ++i) {
+                    if (!visible(i, j, causal, window)) { o[i] = 0xFFFF; continue; }
+                    o[i] = (uint16_t)encode_fmt(logit16(qt, kb + i * d, d), &F_E4M11);
+                }
+            }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* The forward pass (Algorithm 1).                                           */
+/* ------------------------------------------------------------------------ */
+
+enum { MASK_LOW = 0, MASK_STAGE1 = 1, MASK_STAGE2 = 2, MASK_INACTIVE = 3 };
+
+/* Shifted exponential of one logit y against the running maximum mu_hat
+ * (Alg. 1, exponential steps; Sec. 3.3): s = RN_shift(max(0, mu_hat - y)),
+ * E = table[s].  The difference is exact in fp64 (both operands are
+ * multiples of 2^-17 of magnitude <= 512).  Reading: the shift is clamped at
+ * 0 (a stage-2 16-bit logit may exceed mu_hat, which stage 2 does not
+ * update), so every E <= 1. */
+static double shifted_exp(double mu_hat, double y, int high)
+{
+    double x = mu_hat - y;
+    if (x < 0.0) x = 0.0;
+    if (high) {
+        uint32_t sc = encode_fmt(round_to_fmt(x, &F_UE5M11_SHIFT), &F_UE5M11_SHIFT);
+        return decode_fmt(g_exp16[sc], &F_UE5M11_EXP);
+    } else {
+        uint32_t sc = encode_fmt(round_to_fmt(x, &F_UE5M3_SHIFT), &F_UE5M3_SHIFT);
+        return decode_fmt(g_lut8[sc], &F_UE5M3_EXP);
+    }
+}
+
+typedef struct {
+    const uint16_t *q, *k, *v;
+    int B, Hq, Hkv, N, d, causal, window, bq, bk, nk;
+    double delta, tau;
+    double *o, *lse;
+    uint8_t *mask;
+} fwd_args_t;
+
+/* One query block (Alg. 1, body of the outer parallel loop). */
+static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
+{
+    const int d = A->d, N = A->N, bq = A->bq, bk = A->bk, nk = A->nk;
+    const int T = bk * nk;                       /* keys per tile */
+    const int G = A->Hq / A->Hkv;
+    const int nkb = N / bk;                      /* key sub-blocks per row */
+    const int ntiles = N / T;
+    const int64_t q0 = (int64_t)qb * bq;
+    const float s = scale_of(d);
+    const uint16_t *kbase = A->k + ((int64_t)b * A->Hkv + h / G) * (int64_t)N * d;
+    const uint16_t *vbase = A->v + ((int64_t)b * A->Hkv + h / G) * (int64_t)N * d;
+    const int pure8 = isinf(A->tau) && A->tau > 0;
+    const int all16 = (A->tau == 0.0);
+
+    float *qt = (float *)malloc(sizeof(float) * (size_t)bq * d);
+    double *mu = (double *)malloc(sizeof(double) * bq);
+    double *om = (double *)malloc(sizeof(double) * bq);
+    double *O = (double *)calloc((size_t)bq * d, sizeof(double));
+    double *muh = (double *)malloc(sizeof(double) * bq);
+    double *lam = (double *)malloc(sizeof(double) * bq);
+    double *omh = (double *)malloc(sizeof(double) * bq);
+    double *Y = (double *)malloc(sizeof(double) * (size_t)T * bq);   /* [i][j] */
+    double *E = (double *)malloc(sizeof(double) * (size_t)T * bq);   /* [i][j] */
+    unsigned char *vis = (unsigned char *)malloc((size_t)T * bq);
+    double *m8 = (double *)malloc(sizeof(double) * (size_t)nk * bq);
+    double *cost = (double *)malloc(sizeof(double) * (size_t)nk * bq);
+    int *prec = (int *)malloc(sizeof(int) * nk);  /* 0 low, 1 stage1, 2 stage2, 3 inactive */
+    int *order = (int *)malloc(sizeof(int) * nk);
+    double *thr = (double *)malloc(sizeof(double) * nk);
+
+    for (int j = 0; j < bq; ++j) {
+        prescale(A->q + (((int64_t)b * A->Hq + h) * N + q0 + j) * d, d, s, qt + (size_t)j * d);
+        mu[j] = -INFINITY;
+        om[j] = 0.0;
+    }
+    uint8_t *mrow = A->mask + (((int64_t)b * A->Hq + h) * (N / bq) + qb) * nkb;
+    for (int t = 0; t < nkb; ++t) mrow[t] = MASK_INACTIVE;
+
+    for (int tile = 0; tile < ntiles; ++tile) {
+        const int64_t k0 = (int64_t)tile * T;
+        int any_active = 0;
+        for (int th = 0; th < nk; ++th) {
+            int act = 0;
+            for (int ii = th * bk; ii < (th + 1) * bk && !act; ++ii)
+                for (int j = 0; j < bq; ++j)
+                    if (visible(k0 + ii, q0 + j, A->causal, A->window)) { act = 1; break; }
+            prec[th] = act ? MASK_LOW : MASK_INACTIVE;
+            any_active |= act;
+        }
+        if (!any_active) continue;               /* no state change */
+        for (int ii = 0; ii < T; ++ii)
+            for (int j = 0; j < bq; ++j)
+                vis[(size_t)ii * bq + j] = (unsigned char)visible(k0 + ii, q0 + j, A->causal, A->window);
+
+        /* Low-precision logits of the tile (Alg. 1: accumulate Y in low
+         * precision).  In the all-16-bit mode they are never used. */
+        if (!all16) {
+            for (int ii = 0; ii < T; ++ii)
+                for (int j = 0; j < bq; ++j)
+                    Y[(size_t)ii * bq + j] = vis[(size_t)ii * bq + j]
+                        ? logit8(qt + (size_t)j * d, kbase + (k0 + ii) * d, d) : NAN;
+        }
+        /* Column maxima per sub-block: m8[theta][j] (Sec. 3.1, C and T). */
+        for (int th = 0; th < nk; ++th)
+            for (int j = 0; j < bq; ++j) {
+                double m = -INFINITY;
+                if (!all16)
+                    for (int ii = th * bk; ii < (th + 1) * bk; ++ii)
+                        if (vis[(size_t)ii * bq + j] && Y[(size_t)ii * bq + j] > m) m = Y[(size_t)ii * bq + j];
+                m8[(size_t)th * bq + j] = m;
+            }
+        for (int j = 0; j < bq; ++j) muh[j] = mu[j];
+
+        if (pure8) {
+            /* The paper's 8-bit baseline (Sec. 4.1): no recomputation, the
+             * running maximum is taken over the 8-bit logits. */
+            for (int th = 0; th < nk; ++th)
+                if (prec[th] != MASK_INACTIVE)
+                    for (int j = 0; j < bq; ++j)
+                        if (m8[(size_t)th * bq + j] > muh[j]) muh[j] = m8[(size_t)th * bq + j];
+        } else if (all16) {
+            /* Threshold 0: every active sub-block is recomputed in 16 bits
+             * (16-bit FlashAttention in the paper's formats). */
+            for (int th = 0; th < nk; ++th) {
+                if (prec[th] == MASK_INACTIVE) continue;
+                prec[th] = MASK_STAGE1;
+                for (int ii = th * bk; ii < (th + 1) * bk; ++ii)
+                    for (int j = 0; j < bq; ++j) {
+                        size_t ix = (size_t)ii * bq + j;
+                        if (!vis[ix]) continue;
+                        Y[ix] = logit16(qt + (size_t)j * d, kbase + (k0 + ii) * d, d);
+                        if (Y[ix] > muh[j]) muh[j] = Y[ix];
+                    }
+            }
+        } else {
+            /* Stage 1 (Sec. 3.1, Eq. (7); Alg. 1): threats
+             * T_theta = max_j (m8[theta][j] - mu_j) over columns with a
+             * visible entry (exact in fp64, +inf when mu_j = -inf). */
+            int na = 0;
+            for (int th = 0; th < nk; ++th) {
+                if (prec[th] == MASK_INACTIVE) continue;
+                double tv = -INFINITY;
+                for (int j = 0; j < bq; ++j) {
+                    double m = m8[(size_t)th * bq + j];
+                    if (m == -INFINITY) continue;
+                    double dlt = m - mu[j];
+                    if (dlt > tv) tv = dlt;
+                }
+                thr[th] = tv;
+                order[na++] = th;
+            }
+            /* Sort by threat, descending; reading: ties by ascending theta
+             * (insertion sort is stable). */
+            for (int a = 1; a < na; ++a) {
+                int x = order[a], p = a - 1;
+                while (p >= 0 && thr[order[p]] < thr[x]) { order[p + 1] = order[p]; --p; }
+                order[p + 1] = x;
+            }
+            /* Sequential safety-margin test against the running mu_hat.
+             * Reading: mu_hat_j > fma(|mu_hat_j|, delta, m8) (exact for the
+             * paper's power-of-two delta); columns without a visible entry
+             * are not tested; mu_hat = -inf fails. */
+            for (int a = 0; a < na; ++a) {
+                int th = order[a];
+                int pass = 1;
+                for (int j = 0; j < bq && pass; ++j) {
+                    double m = m8[(size_t)th * bq + j];
+                    if (m == -INFINITY) continue;
+                    if (!(muh[j] > fma(fabs(muh[j]), A->delta, m))) pass = 0;
+                }
+                if (pass) continue;
+                prec[th] = MASK_STAGE1;
+                for (int ii = th * bk; ii < (th + 1) * bk; ++ii)
+                    for (int j = 0; j < bq; ++j) {
+                        size_t ix = (size_t)ii * bq + j;
+                        if (!vis[ix]) continue;
+                        Y[ix] = logit16(qt + (size_t)j * d, kbase + (k0 + ii) * d, d);
+                        if (Y[ix] > muh[j]) muh[j] = Y[ix];
+                    }
+            }
+        }
+
+        /* Exponentials against the final mu_hat: 16-bit for stage-1
+         * sub-blocks, 8-bit LUT for the rest (Alg. 1). */
+        for (int th = 0; th < nk; ++th)
+            for (int ii = th * bk; ii < (th + 1) * bk; ++ii)
+                for (int j = 0; j < bq; ++j) {
+                    size_t ix = (size_t)ii * bq + j;
+                    E[ix] = (prec[th] == MASK_INACTIVE || !vis[ix]) ? 0.0
+                            : shifted_exp(muh[j], Y[ix], prec[th] == MASK_STAGE1);
+                }
+        /* lambda_hat = exp(mu - mu_hat) in high precision (Sec. 2.2):
+         * 1 when mu_hat = -inf (no mass yet), 0 when mu = -inf < mu_hat. */
+        for (int j = 0; j < bq; ++j) {
+            if (muh[j] == -INFINITY) lam[j] = 1.0;
+            else if (mu[j] == -INFINITY) lam[j] = 0.0;
+            else lam[j] = exp_doc(mu[j] - muh[j]);
+            /* S_j = sum_i E_ij is exact in fp64 (every E is a multiple of
+             * 2^-41 in [0,1] and a tile holds at most 2^9 of them). */
+            double S = 0.0;
+            for (int ii = 0; ii < T; ++ii) S += E[(size_t)ii * bq + j];
+            omh[j] = fma(lam[j], om[j], S);
+        }
+
+        if (!pure8 && !all16) {
+            /* Stage 2 (Sec. 3.1, Eq. (8)): per sub-block and column
+             * c = sum_{i in theta, ascending} E (omega_hat - E), each
+             * operation rounded in fp64. */
+            int F = 0;
+            for (int th = 0; th < nk; ++th) {
+                if (prec[th] != MASK_LOW) continue;
+                F |= 1 << th;
+                for (int j = 0; j < bq; ++j) {
+                    double c = 0.0;
+                    for (int ii = th * bk; ii < (th + 1) * bk; ++ii) {
+                        size_t ix = (size_t)ii * bq + j;
+                        if (!vis[ix]) continue;
+                        double tt = omh[j] - E[ix];
+                        double pp = E[ix] * tt;
+                        c = c + pp;
+                    }
+                    cost[(size_t)th * bq + j] = c;
+                }
+            }
+            /* Maximise the number of 8-bit sub-blocks: enumerate the
+             * recompute set R (a subset of F) by size, then (reading) by
+             * ascending bitmask, and take the first R whose complement
+             * satisfies xi_j <= (tau*omega_hat_j)*omega_hat_j for every j,
+             * xi_j = sum over kept sub-blocks, ascending, in fp64. */
+            int R = F;
+            int nF = __builtin_popcount((unsigned)F);
+            int found = 0;
+            for (int sz = 0; sz <= nF && !found; ++sz) {
+                for (int msk = 0; msk < (1 << nk) && !found; ++msk) {
+                    if ((msk & ~F) || __builtin_popcount((unsigned)msk) != sz) continue;
+                    int ok = 1;
+                    for (int j = 0; j < bq && ok; ++j) {
+                        double xi = 0.0;
+                        for (int th = 0; th < nk; ++th)
+                            if ((F >> th & 1) && !(msk >> th & 1)) xi = xi + cost[(size_t)th * bq + j];
+                        double lim = (A->tau * omh[j]) * omh[j];
+                        if (!(xi <= lim)) ok = 0;
+                    }
+                    if (ok) { R = msk; found = 1; }
+                }
+            }
+            /* Stage-2 recompute (Alg. 1): 16-bit logits and exponentials
+             * against the same mu_hat, which is not updated. */
+            for (int th = 0; th < nk; ++th) {
+                if (!(R >> th & 1)) continue;
+                prec[th] = MASK_STAGE2;
+                for (int ii = th * bk; ii < (th + 1) * bk; ++ii)
+                    for (int j = 0; j < bq; ++j) {
+                        size_t ix = (size_t)ii * bq + j;
+                        if (!vis[ix]) continue;
+                        Y[ix] = logit16(qt + (size_t)j * d, kbase + (k0 + ii) * d, d);
+                        E[ix] = shifted_exp(muh[j], Y[ix], 1);
+                    }
+            }
+        }
+
+        /* State update (Alg. 1): omega, O, mu. */
+        for (int j = 0; j < bq; ++j) {
+            double S = 0.0;
+            for (int ii = 0; ii < T; ++ii) S += E[(size_t)ii * bq + j];
+            om[j] = fma(lam[j], om[j], S);
+            double *oj = O + (size_t)j * d;
+            for (int c = 0; c < d; ++c) oj[c] *= lam[j];
+            for (int ii = 0; ii < T; ++ii) {
+                double e = E[(size_t)ii * bq + j];
+                if (e == 0.0) continue;
+                const uint16_t *vr = vbase + (k0 + ii) * d;
+                for (int c = 0; c < d; ++c) oj[c] += e * (double)bf16_to_f32(vr[c]);
+            }
+            mu[j] = muh[j];
+        }
+        for (int th = 0; th < nk; ++th) mrow[tile * nk + th] = (uint8_t)prec[th];
+    }
+
+    /* Epilogue (Alg. 1): O / omega; lse = mu + ln(omega). */
+    for (int j = 0; j < bq; ++j) {
+        double *dst = A->o + (((int64_t)b * A->Hq + h) * N + q0 + j) * d;
+        for (int c = 0; c < d; ++c) dst[c] = O[(size_t)j * d + c] / om[j];
+        A->lse[((int64_t)b * A->Hq + h) * N + q0 + j] = mu[j] + log(om[j]);
+    }
+    free(qt); free(mu); free(om); free(O); free(muh); free(lam); free(omh);
+    free(Y); free(E); free(vis); free(m8); free(cost); free(prec); free(order); free(thr);
+}
+
+/* lamp_oracle_fwd: Q,K,V bf16 bit patterns [B,H,N,d] (host memory),
+ * outputs o [B,Hq,N,d] fp64, lse [B,Hq,N] fp64, mask [B,Hq,N/bq,N/bk] u8.
+ * If qblocks != NULL only the listed query blocks (flat index
+ * (b*Hq + h)*(N/bq) + qb) are computed; other outputs are left untouched.
+ * Returns 0, or -1 on invalid arguments / -2 on a table failure. */
+int lamp_oracle_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                    int B, int Hq, int Hkv, int N, int d, int causal, int window,
+                    int bq, int bk, int nk, double delta, double tau,
+                    double *o, double *lse, uint8_t *mask,
+                    const int64_t *qblocks, int64_t nqblocks, int nthreads)
+{
+    if (B <= 0 || Hq <= 0 || Hkv <= 0 || N <= 0 || d <= 0 || d > 1024) return -1;
+    if (Hq % Hkv || bq <= 0 || bk <= 0 || nk <= 0 || nk > 16) return -1;
+    if (N % bq || N % (bk * nk)) return -1;
+    if (window < 0 || (window > 0 && !causal)) return -1;
+    if (!(tau >= 0.0) || !(delta >= 0.0)) return -1;
+    if (build_tables()) return -2;
+    fwd_args_t A = {q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, o, lse, mask};
+    int64_t nqb = (int64_t)B * Hq * (N / bq);
+    int64_t count = qblocks ? nqblocks : nqb;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+#endif
+    for (int64_t t = 0; t < count; ++t) {
+        int64_t f = qblocks ? qblocks[t] : t;
+        int qb = (int)(f % (N / bq));
+        int h = (int)((f / (N / bq)) % Hq);
+        int b = (int)(f / ((int64_t)(N / bq) * Hq));
+        fwd_qblock(&A, b, h, qb);
+    }
+    return 0;
+}
+
+int oracle_max_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

@@ -1,0 +1,186 @@
+"""ctypes wrapper around the CPU oracle (oracle/lamp_oracle.c).
+
+TEST INFRASTRUCTURE ONLY: imported by the test suite, the smoke check and the
+benchmark's cpu_baseline leg, never by the product path.  It shares no code
+with the GPU library.
+
+All functions take numpy arrays on the host.  Q, K and V are passed as bf16 bit
+patterns (uint16); see `bf16_bits` for the conversion from a torch tensor.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liblamp_oracle.so")
+
+# Format ids understood by the oracle's codec entry points.
+E4M3, E4M11, UE5M3_SHIFT, UE5M11_SHIFT, UE5M3_EXP, UE5M11_EXP = range(6)
+
+MASK_LOW, MASK_STAGE1, MASK_STAGE2, MASK_INACTIVE = 0, 1, 2, 3
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            import importlib.util
+            spec = importlib.util.spec_from_file_location("_oracle_build", os.path.join(HERE, "build.py"))
+            mod = importlib.util.module_from_spec(spec)
+            spec.loader.exec_module(mod)
+            mod.build()
+        _lib = ctypes.CDLL(LIB_PATH)
+        P = ctypes.c_void_p
+        i32, i64, f64 = ctypes.c_int, ctypes.c_int64, ctypes.c_double
+        _lib.lamp_oracle_fwd.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32,
+                                         f64, f64, P, P, P, P, i64, i32]
+        _lib.lamp_oracle_fwd.restype = i32
+        for name in ("oracle_logits8", "oracle_logits16"):
+            fn = getattr(_lib, name)
+            fn.argtypes = [P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, i32]
+            fn.restype = i32
+        for name in ("oracle_round_fmt", "oracle_encode_fmt", "oracle_decode_fmt"):
+            fn = getattr(_lib, name)
+            fn.argtypes = [i32, P, P, i64]
+            fn.restype = i32
+        _lib.oracle_e4m3_of_f32_bits.argtypes = [ctypes.c_uint64, i64, P, i32]
+        _lib.oracle_e4m3_of_f32_bits.restype = i32
+        _lib.oracle_exp_doc.argtypes = [P, P, i64]
+        _lib.oracle_exp_doc.restype = i32
+        _lib.oracle_exp_doc_constants.argtypes = [P]
+        _lib.oracle_exp_doc_constants.restype = i32
+        _lib.oracle_tables.argtypes = [P, P]
+        _lib.oracle_tables.restype = i32
+        _lib.oracle_scale.argtypes = [i32]
+        _lib.oracle_scale.restype = ctypes.c_float
+        _lib.oracle_max_threads.argtypes = []
+        _lib.oracle_max_threads.restype = i32
+    return _lib
+
+
+def _ptr(a):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def bf16_bits(t):
+    """uint16 numpy array of the bf16 bit patterns of a torch bf16 tensor."""
+    import torch
+    assert t.dtype == torch.bfloat16
+    return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+# ---------------------------------------------------------------- codecs
+def round_fmt(fmt, x):
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    y = np.empty_like(x)
+    assert lib().oracle_round_fmt(fmt, _ptr(x), _ptr(y), x.size) == 0
+    return y
+
+
+def encode_fmt(fmt, x):
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    c = np.empty(x.shape, dtype=np.uint32)
+    assert lib().oracle_encode_fmt(fmt, _ptr(x), _ptr(c), x.size) == 0
+    return c
+
+
+def decode_fmt(fmt, c):
+    c = np.ascontiguousarray(c, dtype=np.uint32)
+    y = np.empty(c.shape, dtype=np.float64)
+    assert lib().oracle_decode_fmt(fmt, _ptr(c), _ptr(y), c.size) == 0
+    return y
+
+
+def e4m3_of_f32_bits(start, count, nthreads=0):
+    out = np.empty(count, dtype=np.uint8)
+    assert lib().oracle_e4m3_of_f32_bits(start, count, _ptr(out), nthreads) == 0
+    return out
+
+
+def exp_doc(x):
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    y = np.empty_like(x)
+    assert lib().oracle_exp_doc(_ptr(x), _ptr(y), x.size) == 0
+    return y
+
+
+def exp_doc_constants():
+    c = np.empty(17, dtype=np.float64)
+    lib().oracle_exp_doc_constants(_ptr(c))
+    return c
+
+
+def tables():
+    lut8 = np.empty(256, dtype=np.uint8)
+    exp16 = np.empty(65536, dtype=np.uint16)
+    rc = lib().oracle_tables(_ptr(lut8), _ptr(exp16))
+    if rc != 0:
+        raise RuntimeError("oracle table construction failed (%d)" % rc)
+    return lut8, exp16
+
+
+def scale(d):
+    return lib().oracle_scale(d)
+
+
+# ---------------------------------------------------------------- logits
+def logits8(q, k, causal, window, row0, nrows, nthreads=0):
+    """e4m3 codes of the 8-bit logits of rows [row0, row0+nrows): [B,Hq,nrows,N], 0xFF = invisible."""
+    q = np.ascontiguousarray(q, dtype=np.uint16)
+    k = np.ascontiguousarray(k, dtype=np.uint16)
+    B, Hq, N, d = q.shape
+    Hkv = k.shape[1]
+    out = np.empty((B, Hq, nrows, N), dtype=np.uint8)
+    rc = lib().oracle_logits8(_ptr(q), _ptr(k), B, Hq, Hkv, N, d, int(causal), int(window),
+                              row0, nrows, _ptr(out), nthreads)
+    assert rc == 0
+    return out
+
+
+def logits16(q, k, causal, window, row0, nrows, nthreads=0):
+    """e4m11 codes of the 16-bit logits, same layout; invisible entries hold 0xFFFF."""
+    q = np.ascontiguousarray(q, dtype=np.uint16)
+    k = np.ascontiguousarray(k, dtype=np.uint16)
+    B, Hq, N, d = q.shape
+    Hkv = k.shape[1]
+    out = np.empty((B, Hq, nrows, N), dtype=np.uint16)
+    rc = lib().oracle_logits16(_ptr(q), _ptr(k), B, Hq, Hkv, N, d, int(causal), int(window),
+                               row0, nrows, _ptr(out), nthreads)
+    assert rc == 0
+    return out
+
+
+# ---------------------------------------------------------------- forward
+def fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, qblocks=None, nthreads=0):
+    """The LampAttention forward pass on the CPU.
+
+    Returns (o [B,Hq,N,d] fp64, lse [B,Hq,N] fp64, mask [B,Hq,N/bq,N/bk] u8).
+    With `qblocks` (flat indices (b*Hq+h)*(N/bq)+qb) only those query blocks
+    are computed; the other rows of o/lse hold NaN and their mask bytes 0xFE.
+    """
+    q = np.ascontiguousarray(q, dtype=np.uint16)
+    k = np.ascontiguousarray(k, dtype=np.uint16)
+    v = np.ascontiguousarray(v, dtype=np.uint16)
+    B, Hq, N, d = q.shape
+    Hkv = k.shape[1]
+    o = np.full((B, Hq, N, d), np.nan, dtype=np.float64)
+    lse = np.full((B, Hq, N), np.nan, dtype=np.float64)
+    mask = np.full((B, Hq, N // bq, N // bk), 0xFE, dtype=np.uint8)
+    if qblocks is not None:
+        qbl = np.ascontiguousarray(qblocks, dtype=np.int64)
+        qp, nq = _ptr(qbl), qbl.size
+    else:
+        qp, nq = None, 0
+    rc = lib().lamp_oracle_fwd(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(causal), int(window),
+                               bq, bk, nk, float(delta), float(tau), _ptr(o), _ptr(lse), _ptr(mask),
+                               qp, nq, nthreads)
+    if rc != 0:
+        raise ValueError("lamp_oracle_fwd failed with %d" % rc)
+    return o, lse, mask
+
+
+def max_threads():
+    return lib().oracle_max_threads()

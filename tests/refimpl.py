@@ -1,0 +1,202 @@
+"""A second, independent implementation of LampAttention (paper Sec. 3.1-3.2,
+Algorithm 1) for tiny inputs, used to pin the C oracle.
+
+Written separately from the oracle with different methods:
+  * numpy vectorised over a whole tile instead of scalar loops;
+  * the FP32 FMA of the 8-bit accumulation is emulated exactly from fp64
+    products and a TwoSum correction instead of calling fmaf;
+  * rounding to the formats with the integer model of fpmodel.py;
+  * exponential tables from mpmath, lambda_hat from math.exp;
+  * the stage-2 knapsack by brute force over every g in {0,1}^N_k.
+It asserts the stage-1 invariant (every 8-bit sub-block passes the margin test
+against the final running maximum) on every tile.
+"""
+import math
+
+import numpy as np
+
+import fpmodel as M
+
+
+def _two_sum(a, b):
+    s = a + b
+    bb = s - a
+    e = (a - (s - bb)) + (b - bb)
+    return s, e
+
+
+def rn32_sum(p, c):
+    """RN32(p + c) for fp64 arrays p (exact products) and c (fp32 values)."""
+    s, e = _two_sum(p, c)
+    r = s.astype(np.float32).astype(np.float64)
+    inexact = r != s
+    # neighbour on the other side of s
+    toward = np.where(s > r, np.inf, -np.inf).astype(np.float32)
+    r2 = np.nextafter(r.astype(np.float32), toward).astype(np.float64)
+    mid = (r + r2) / 2
+    # Only when s is exactly an fp32 midpoint can the exact sum s + e round
+    # differently from s (any other midpoint is an fp64 number strictly closer
+    # to s + e than s, impossible).  Then the sign of e decides.
+    tie = inexact & (s == mid) & (e != 0)
+    go_r2 = tie & (np.sign(e) == np.sign(r2 - r))
+    return np.where(go_r2, r2, r)
+
+
+def y8_tile(qt, kf):
+    """qt [bq, d] fp32 values (as fp64), kf [T, d] -> Y8 values [T, bq]."""
+    acc = np.zeros((kf.shape[0], qt.shape[0]))
+    for c in range(qt.shape[1]):
+        p = kf[:, c][:, None] * qt[:, c][None, :]          # exact in fp64
+        t = rn32_sum(p, acc)
+        acc = M.np_round(t, "e4m3")
+    return acc
+
+
+def y16_tile(qt, kf):
+    acc = np.zeros((kf.shape[0], qt.shape[0]))
+    for c in range(qt.shape[1]):
+        acc = acc + kf[:, c][:, None] * qt[:, c][None, :]   # exact product, one rounding
+    return M.np_round(acc, "e4m11")
+
+
+def _shift_exp(muh, y, high, tabs):
+    x = np.maximum(muh[None, :] - y, 0.0)
+    if high:
+        code = M.np_encode(M.np_round(x, "ue5m11_shift"), "ue5m11_shift")
+        e = tabs[1][code]
+        return M.np_decode(e, "ue5m11_exp")
+    code = M.np_encode(M.np_round(x, "ue5m3_shift"), "ue5m3_shift")
+    return M.np_decode(tabs[0][code], "ue5m3_exp")
+
+
+def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale):
+    """q [B,Hq,N,d], k/v [B,Hkv,N,d] bf16 bit patterns.  Returns o, lse, mask."""
+    B, Hq, N, d = q.shape
+    Hkv = k.shape[1]
+    G = Hq // Hkv
+    T = bk * nk
+    o = np.zeros((B, Hq, N, d))
+    lse = np.zeros((B, Hq, N))
+    mask = np.full((B, Hq, N // bq, N // bk), 3, dtype=np.uint8)
+    pure8 = math.isinf(tau)
+    all16 = tau == 0.0
+    for b in range(B):
+        for h in range(Hq):
+            kf_all = M.bf16_to_float(k[b, h // G])
+            vf_all = M.bf16_to_float(v[b, h // G])
+            for qb in range(N // bq):
+                q0 = qb * bq
+                qf = M.bf16_to_float(q[b, h, q0:q0 + bq])
+                qt = (qf * np.float64(scale)).astype(np.float32).astype(np.float64)
+                mu = np.full(bq, -np.inf)
+                om = np.zeros(bq)
+                O = np.zeros((bq, d))
+                jj = q0 + np.arange(bq)
+                for t in range(N // T):
+                    ii = t * T + np.arange(T)
+                    vis = np.ones((T, bq), dtype=bool)
+                    if causal:
+                        vis &= ii[:, None] <= jj[None, :]
+                    if window > 0:
+                        vis &= ii[:, None] > jj[None, :] - window
+                    act = np.array([vis[th * bk:(th + 1) * bk].any() for th in range(nk)])
+                    if not act.any():
+                        continue
+                    kf = kf_all[ii]
+                    prec = np.where(act, 0, 3)
+                    Y = np.full((T, bq), np.nan)
+                    if not all16:
+                        Y = y8_tile(qt, kf)
+                    Yv = np.where(vis, Y, -np.inf)
+                    m8 = np.array([Yv[th * bk:(th + 1) * bk].max(axis=0) for th in range(nk)])
+                    muh = mu.copy()
+                    Y16 = None
+
+                    def y16():
+                        nonlocal Y16
+                        if Y16 is None:
+                            Y16 = y16_tile(qt, kf)
+                        return Y16
+
+                    if pure8:
+                        for th in range(nk):
+                            if act[th]:
+                                muh = np.maximum(muh, m8[th])
+                    elif all16:
+                        for th in range(nk):
+                            if act[th]:
+                                prec[th] = 1
+                                sl = slice(th * bk, (th + 1) * bk)
+                                Y[sl] = y16()[sl]
+                                muh = np.maximum(muh, np.where(vis[sl], Y[sl], -np.inf).max(axis=0))
+                    else:
+                        thr = {}
+                        for th in range(nk):
+                            if act[th]:
+                                m = m8[th]
+                                ok = m > -np.inf
+                                thr[th] = (m[ok] - mu[ok]).max()
+                        order = sorted(thr, key=lambda th: (-thr[th], th))
+                        for th in order:
+                            m = m8[th]
+                            ok = m > -np.inf
+                            margin = muh[ok] > m[ok] + np.abs(muh[ok]) * delta
+                            if margin.all():
+                                continue
+                            prec[th] = 1
+                            sl = slice(th * bk, (th + 1) * bk)
+                            Y[sl] = y16()[sl]
+                            muh = np.maximum(muh, np.where(vis[sl], Y[sl], -np.inf).max(axis=0))
+                        # stage-1 invariant against the final mu_hat
+                        for th in range(nk):
+                            if act[th] and prec[th] == 0:
+                                m = m8[th]
+                                ok = m > -np.inf
+                                assert np.all(muh[ok] > m[ok] + np.abs(muh[ok]) * delta)
+                    E = np.zeros((T, bq))
+                    for th in range(nk):
+                        if prec[th] == 3:
+                            continue
+                        sl = slice(th * bk, (th + 1) * bk)
+                        e = _shift_exp(muh, np.where(vis[sl], Y[sl], 0.0), prec[th] == 1, tabs)
+                        E[sl] = np.where(vis[sl], e, 0.0)
+                    lam = np.where(muh == -np.inf, 1.0,
+                                   np.where(mu == -np.inf, 0.0,
+                                            np.exp(np.where(np.isfinite(mu) & np.isfinite(muh), mu - muh, 0.0))))
+                    omh = lam * om + E.sum(axis=0)
+                    if not pure8 and not all16:
+                        F = [th for th in range(nk) if prec[th] == 0]
+                        cost = {}
+                        for th in F:
+                            c = np.zeros(bq)
+                            for r in range(th * bk, (th + 1) * bk):
+                                c = c + np.where(vis[r], E[r] * (omh - E[r]), 0.0)
+                            cost[th] = c
+                        lim = (tau * omh) * omh
+                        best = None
+                        for g in range(1 << len(F)):           # g: kept (8-bit) subset of F
+                            keep = [F[a] for a in range(len(F)) if g >> a & 1]
+                            xi = np.zeros(bq)
+                            for th in sorted(keep):
+                                xi = xi + cost[th]
+                            if not np.all(xi <= lim):
+                                continue
+                            rmask = sum(1 << th for th in F if th not in keep)
+                            key = (len(keep), -rmask)
+                            if best is None or key > best[0]:
+                                best = (key, rmask)
+                        rmask = best[1]
+                        for th in range(nk):
+                            if rmask >> th & 1:
+                                prec[th] = 2
+                                sl = slice(th * bk, (th + 1) * bk)
+                                Y[sl] = y16()[sl]
+                                e = _shift_exp(muh, np.where(vis[sl], Y[sl], 0.0), True, tabs)
+                                E[sl] = np.where(vis[sl], e, 0.0)
+                    om = lam * om + E.sum(axis=0)
+                    O = O * lam[:, None] + E.T @ vf_all[ii]
+                    mu = muh
+                    mask[b, h, qb, t * nk:(t + 1) * nk] = prec
+                o[b, h, q0:q0 + bq] = O / om[:, None]
+                lse[b, h, q0:q0 + bq] = mu + np.log(om)
+    return o, lse, mask

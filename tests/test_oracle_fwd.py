@@ -1,0 +1,227 @@
+"""Pins of the oracle's forward pass (paper Sec. 3.1-3.2, Algorithm 1).
+
+* an independent implementation (tests/refimpl.py) reproduces the masks
+  exactly and O / lse to 1e-9 on tiny problems, including a brute-force
+  solution of the stage-2 knapsack and the stage-1 invariant;
+* threshold +inf is the pure 8-bit path and, on one tile, equals a naive
+  softmax of the identically rounded 8-bit logits;
+* threshold 0 is 16-bit FlashAttention (a plain tile loop written here) and
+  lies within the ue5m11 rounding bound of an fp64 softmax of Y16;
+* threshold 1 never triggers stage 2 (Sec. 4.2);
+* larger safety margins give more stage-1 recomputes (App. C);
+* rows of the attention matrix sum to one, O is a convex combination of V.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+import fpmodel as M
+import refimpl as R
+from paper_2609_39361_amd import workloads as W
+
+
+@pytest.fixture(scope="session")
+def mp_tables():
+    return M.mp_exp_tables()
+
+
+def _bits(w):
+    q, k, v = W.make_inputs(w)
+    return O.bf16_bits(q), O.bf16_bits(k), O.bf16_bits(v)
+
+
+CASES = [
+    # (workload, tau, delta)
+    (W.small("nc_d16", N=64, d=16, Hq=1, Hkv=1, bq=32, bk=8, nk=4, causal=0, seed=11), 0.5, 2 ** -8),
+    (W.small("causal_gqa", N=96, d=16, Hq=2, Hkv=1, bq=32, bk=8, nk=4, causal=1, seed=12), 0.5, 2 ** -8),
+    (W.small("causal_tau_small", N=64, d=16, Hq=2, Hkv=2, bq=16, bk=4, nk=4, causal=1, seed=13), 2 ** -5, 2 ** -8),
+    (W.small("window", N=96, d=8, Hq=1, Hkv=1, bq=16, bk=4, nk=4, causal=1, window=20, seed=14), 0.5, 2 ** -4),
+    (W.small("outlier", N=64, d=32, Hq=1, Hkv=1, bq=32, bk=16, nk=2, causal=0, seed=15, kind="outlier",
+             n_outlier=2, outlier_gain=16.0), 0.5, 2 ** -8),
+    (W.small("tau1", N=64, d=16, Hq=1, Hkv=1, bq=32, bk=8, nk=4, causal=1, seed=16), 1.0, 2 ** -8),
+    (W.small("pure8", N=64, d=16, Hq=1, Hkv=1, bq=32, bk=8, nk=4, causal=1, seed=17), math.inf, 2 ** -8),
+    (W.small("all16", N=64, d=16, Hq=1, Hkv=1, bq=32, bk=8, nk=4, causal=1, seed=18), 0.0, 2 ** -8),
+    (W.small("nk3", N=96, d=8, Hq=1, Hkv=1, bq=32, bk=8, nk=3, causal=1, seed=19), 0.25, 2 ** -8),
+]
+
+
+@pytest.mark.parametrize("w,tau,delta", CASES, ids=[c[0].name for c in CASES])
+def test_oracle_matches_independent_implementation(w, tau, delta, mp_tables):
+    q, k, v = _bits(w)
+    o, lse, mask = O.fwd(q, k, v, w.causal, w.window, w.bq, w.bk, w.nk, delta, tau)
+    ro, rlse, rmask = R.ref_fwd(q, k, v, w.causal, w.window, w.bq, w.bk, w.nk, delta, tau,
+                                mp_tables, O.scale(w.d))
+    assert np.array_equal(mask, rmask)
+    np.testing.assert_allclose(o, ro, rtol=1e-9, atol=1e-12)
+    np.testing.assert_allclose(lse, rlse, rtol=1e-12, atol=1e-12)
+
+
+def test_pure8_single_tile_is_naive_softmax_of_rounded_logits(mp_tables):
+    """Threshold +inf, one key tile (N = b_k N_k): O = softmax(Y8) V where
+    each exponential is the LUT value of the rounded shift max(Y8) - Y8."""
+    w = W.CONFIGS[1]
+    q, k, v = _bits(w)
+    o, lse, mask = O.fwd(q, k, v, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, math.inf)
+    assert np.all(mask == 0)
+    y8 = M.np_decode(O.logits8(q, k, 0, 0, 0, w.N)[0, 0].astype(np.int64), "e4m3")   # [j, i]
+    mx = y8.max(axis=1, keepdims=True)
+    sc = M.np_encode(M.np_round(mx - y8, "ue5m3_shift"), "ue5m3_shift")
+    E = M.np_decode(mp_tables[0][sc], "ue5m3_exp")
+    vf = M.bf16_to_float(v[0, 0])
+    ref = (E @ vf) / E.sum(axis=1, keepdims=True)
+    np.testing.assert_allclose(o[0, 0], ref, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(lse[0, 0], mx[:, 0] + np.log(E.sum(axis=1)), rtol=0, atol=1e-12)
+
+
+def _flash16(q, k, v, causal, window, T, tabs, scale):
+    """16-bit FlashAttention in the paper's formats: Y16 logits, ue5m11 shift
+    and exp, running max/sum over key tiles of T keys."""
+    B, Hq, N, d = q.shape
+    G = Hq // k.shape[1]
+    o = np.zeros((B, Hq, N, d))
+    for b in range(B):
+        for h in range(Hq):
+            qt = (M.bf16_to_float(q[b, h]) * np.float64(scale)).astype(np.float32).astype(np.float64)
+            kf = M.bf16_to_float(k[b, h // G])
+            vf = M.bf16_to_float(v[b, h // G])
+            y = R.y16_tile(qt, kf).T                     # [j, i]
+            j = np.arange(N)[:, None]
+            i = np.arange(N)[None, :]
+            vis = np.ones((N, N), dtype=bool)
+            if causal:
+                vis &= i <= j
+            if window:
+                vis &= i > j - window
+            mu = np.full(N, -np.inf)
+            om = np.zeros(N)
+            acc = np.zeros((N, d))
+            for t in range(N // T):
+                sl = slice(t * T, (t + 1) * T)
+                yv = np.where(vis[:, sl], y[:, sl], -np.inf)
+                muh = np.maximum(mu, yv.max(axis=1))
+                rows = muh > -np.inf
+                x = np.maximum(np.where(rows[:, None], muh[:, None], 0.0) - np.where(vis[:, sl], y[:, sl], 0.0), 0)
+                sc = M.np_encode(M.np_round(x, "ue5m11_shift"), "ue5m11_shift")
+                E = np.where(vis[:, sl], M.np_decode(tabs[1][sc], "ue5m11_exp"), 0.0)
+                lam = np.where(~rows, 1.0, np.where(mu == -np.inf, 0.0,
+                                                    np.exp(np.where(rows & (mu > -np.inf), mu - muh, 0.0))))
+                om = lam * om + E.sum(axis=1)
+                acc = acc * lam[:, None] + E @ vf[sl]
+                mu = muh
+            o[b, h] = acc / om[:, None]
+    return o
+
+
+def test_tau0_is_16bit_flash_attention(mp_tables):
+    w = W.small("f16", N=128, d=32, Hq=2, Hkv=1, bq=32, bk=8, nk=4, causal=1, seed=21)
+    q, k, v = _bits(w)
+    o, lse, mask = O.fwd(q, k, v, 1, 0, w.bq, w.bk, w.nk, w.delta, 0.0)
+    assert set(np.unique(mask)) <= {1, 3}
+    ref = _flash16(q, k, v, 1, 0, w.bk * w.nk, mp_tables, O.scale(w.d))
+    np.testing.assert_allclose(o, ref, rtol=1e-9, atol=1e-12)
+    # and within the ue5m11 rounding bound of an exact softmax of Y16: each E
+    # carries relative error <= 2^-12 (exp rounding) * exp(2^-12 * s) from the
+    # shift rounding, |s| <= 2^-12 * s relative; the normalised weights shift by
+    # at most twice the largest relative error.
+    qt = (M.bf16_to_float(q) * np.float64(O.scale(w.d))).astype(np.float32).astype(np.float64)
+    for h in range(2):
+        y = R.y16_tile(qt[0, h], M.bf16_to_float(k[0, 0])).T
+        j = np.arange(w.N)[:, None]
+        i = np.arange(w.N)[None, :]
+        y = np.where(i <= j, y, -np.inf)
+        p = torch.softmax(torch.from_numpy(y), dim=1).numpy()
+        exact = p @ M.bf16_to_float(v[0, 0])
+        span = (y.max(axis=1) - np.where(np.isfinite(y), y, np.inf).min(axis=1))
+        rel = 2.0 ** -12 + np.expm1(2.0 ** -12 * span) + 2.0 ** -12
+        bound = 2 * rel[:, None] * np.abs(M.bf16_to_float(v[0, 0])).max() + 1e-12
+        assert np.all(np.abs(o[0, h] - exact) <= bound)
+
+
+def test_tau1_never_recomputes_in_stage2():
+    """Sec. 4.2: at threshold 1 the block-LAMP solution never reroutes."""
+    for seed, kind in ((31, "rope_lognormal"), (32, "outlier")):
+        w = W.small("t1", N=256, d=32, Hq=2, Hkv=1, bq=64, bk=16, nk=4, causal=1, seed=seed, kind=kind,
+                    n_outlier=2, outlier_gain=12.0)
+        q, k, v = _bits(w)
+        _, _, mask = O.fwd(q, k, v, 1, 0, w.bq, w.bk, w.nk, w.delta, 1.0)
+        assert not np.any(mask == 2)
+        assert np.any(mask == 1)        # the first tile of every block always reroutes
+
+
+def test_threshold_monotonicity_and_extremes():
+    """Fewer recomputes as tau grows (Sec. 4.2); tau = inf none, tau = 0 all."""
+    w = W.small("mono", N=256, d=32, Hq=4, Hkv=2, bq=64, bk=16, nk=4, causal=1, seed=41)
+    q, k, v = _bits(w)
+    counts = []
+    for tau in (0.0, 2 ** -5, 2 ** -3, 0.5, 1.0, math.inf):
+        _, _, mask = O.fwd(q, k, v, 1, 0, w.bq, w.bk, w.nk, w.delta, tau)
+        counts.append(int(np.isin(mask, (1, 2)).sum()))
+        if tau == 0:
+            assert np.all((mask == 1) | (mask == 3))
+        if math.isinf(tau):
+            assert np.all((mask == 0) | (mask == 3))
+    assert counts == sorted(counts, reverse=True), counts
+    assert counts[-1] == 0 and counts[0] > counts[-2]
+
+
+def test_larger_safety_margin_more_stage1():
+    """App. C: delta = 2^-4 initiates more stage-1 recomputes than 2^-8."""
+    w = W.small("delta", N=512, d=32, Hq=2, Hkv=1, bq=64, bk=16, nk=4, causal=1, seed=51)
+    q, k, v = _bits(w)
+    _, _, m8 = O.fwd(q, k, v, 1, 0, w.bq, w.bk, w.nk, 2 ** -8, 1.0)
+    _, _, m4 = O.fwd(q, k, v, 1, 0, w.bq, w.bk, w.nk, 2 ** -4, 1.0)
+    assert (m4 == 1).sum() >= (m8 == 1).sum()
+    # with the larger margin every stage-1 reroute of the small margin remains
+    assert (m4 == 1).sum() > (m8 == 1).sum() or np.array_equal(m4, m8)
+
+
+def test_rows_sum_to_one_and_convexity():
+    w = W.small("cvx", N=128, d=32, Hq=2, Hkv=1, bq=32, bk=8, nk=4, causal=1, seed=61)
+    q, k, v = _bits(w)
+    ones = np.full_like(v, 0x3F80)                   # bf16 1.0
+    o1, _, _ = O.fwd(q, k, ones, 1, 0, w.bq, w.bk, w.nk, w.delta, 0.5)
+    assert np.abs(o1 - 1.0).max() < 1e-12
+    o, _, _ = O.fwd(q, k, v, 1, 0, w.bq, w.bk, w.nk, w.delta, 0.5)
+    vf = M.bf16_to_float(v)
+    for h in range(2):
+        for j in range(w.N):
+            lo = vf[0, 0, :j + 1].min(axis=0)
+            hi = vf[0, 0, :j + 1].max(axis=0)
+            assert np.all(o[0, h, j] >= lo - 1e-12) and np.all(o[0, h, j] <= hi + 1e-12)
+
+
+def test_subset_equals_full_rows():
+    w = W.small("sub", N=128, d=16, Hq=2, Hkv=2, bq=32, bk=8, nk=4, causal=1, seed=71)
+    q, k, v = _bits(w)
+    o, lse, mask = O.fwd(q, k, v, 1, 0, w.bq, w.bk, w.nk, w.delta, 0.5)
+    sub = [1, 3, 6]                                  # flat (b*Hq + h)*(N/bq) + qb
+    so, slse, smask = O.fwd(q, k, v, 1, 0, w.bq, w.bk, w.nk, w.delta, 0.5, qblocks=sub)
+    nqb = w.N // w.bq
+    for f in sub:
+        h, qb = f // nqb, f % nqb
+        rows = slice(qb * w.bq, (qb + 1) * w.bq)
+        assert np.array_equal(so[0, h, rows], o[0, h, rows])
+        assert np.array_equal(smask[0, h, qb], mask[0, h, qb])
+    assert np.isnan(so[0, 0, :w.bq]).all()
+
+
+def test_window_one_is_diagonal_only():
+    """Window 1 leaves only the diagonal visible: O = V row by row."""
+    w = W.small("diag", N=64, d=16, Hq=1, Hkv=1, bq=16, bk=8, nk=2, causal=1, window=1, seed=81)
+    q, k, v = _bits(w)
+    o, lse, mask = O.fwd(q, k, v, 1, 1, w.bq, w.bk, w.nk, w.delta, 0.5)
+    np.testing.assert_allclose(o[0, 0], M.bf16_to_float(v[0, 0]), rtol=0, atol=0)
+
+
+def test_invalid_arguments_rejected():
+    w = W.small("bad", N=64, d=16, Hq=3, Hkv=2, bq=16, bk=8, nk=2)
+    q, k, v = _bits(W.small("ok", N=64, d=16, Hq=2, Hkv=1, bq=16, bk=8, nk=2))
+    with pytest.raises(ValueError):
+        O.fwd(q, k, v, 1, 0, 24, 8, 2, 2 ** -8, 0.5)          # N % bq != 0
+    with pytest.raises(ValueError):
+        O.fwd(q, k, v, 0, 8, 16, 8, 2, 2 ** -8, 0.5)          # window without causal
+    with pytest.raises(ValueError):
+        O.fwd(q, k, v, 1, 0, 16, 8, 2, 2 ** -8, -1.0)         # negative threshold
