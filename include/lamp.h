@@ -1,0 +1,132 @@
+/*
+ * lamp.h -- C ABI of liblamp.so, the MI355X (gfx950) LampAttention forward pass.
+ *
+ * LampAttention (look-ahead mixed-precision FlashAttention) computes every
+ * QK^T logit with 8-bit (e4m3) accumulation, flags the numerically sensitive
+ * (query block x key sub-block) sub-blocks in two stages -- a running-maximum
+ * look-ahead with a safety margin, then a block-LAMP knapsack on an analytical
+ * round-off bound -- recomputes only those in 16 bits (e4m11), and finishes
+ * with the online-softmax rescale and the P.V accumulation.  Paper: Sec. 3.1
+ * (block LAMP, Eqs. (7) and (8)), Sec. 3.2 (Algorithm 1), Sec. 3.3 (formats).
+ *
+ * Conventions shared by every entry point:
+ *   - Pointers named q, k, v, o, lse, mask, y8, y16 are DEVICE pointers to
+ *     memory the caller owns; the library never frees or retains them.
+ *   - Tensors are dense row-major: q [B][Hq][N][d], k and v [B][Hkv][N][d]
+ *     (bf16 bit patterns, uint16_t), o [B][Hq][N][d] fp32, lse [B][Hq][N]
+ *     fp32, mask [B][Hq][N/bq][N/bk] uint8.  Query head h reads kv head
+ *     h / (Hq/Hkv) (grouped-query attention).
+ *   - Visibility: key i is visible to query j unless causal and i > j, or
+ *     window > 0 and i <= j - window (window requires causal).
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
+ *     stream).  Results are valid after the stream has been synchronised.
+ *   - Every function returns a lamp_status; nothing aborts or throws across
+ *     the ABI.  lamp_last_error() describes the last failure of the calling
+ *     thread.
+ *   - Inputs must be finite; non-finite inputs give unspecified results.
+ */
+#ifndef LAMP_H
+#define LAMP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    LAMP_OK = 0,
+    LAMP_ERR_INVALID_ARG = 1,   /* null pointer, negative size, bad parameter */
+    LAMP_ERR_UNSUPPORTED = 2,   /* valid but not built: shape or block sizes */
+    LAMP_ERR_HIP = 3,           /* a HIP runtime call failed */
+    LAMP_ERR_INIT = 4           /* device tables could not be built */
+} lamp_status;
+
+/* Mask codes, one byte per (query block, key sub-block). */
+enum {
+    LAMP_MASK_LOW = 0,      /* kept in 8 bits */
+    LAMP_MASK_STAGE1 = 1,   /* recomputed in 16 bits by the running-max test, Eq. (7) */
+    LAMP_MASK_STAGE2 = 2,   /* recomputed in 16 bits by the block-LAMP knapsack, Eq. (8) */
+    LAMP_MASK_INACTIVE = 3  /* no visible (query, key) pair: never computed */
+};
+
+/*
+ * lamp_attn_fwd -- the LampAttention forward pass (Algorithm 1).
+ *
+ * Inputs q, k, v: bf16, layouts above.  bq = queries per block (b_q), bk =
+ * keys per sub-block (b_k), nk = sub-blocks per key tile (N_k); the paper's
+ * tiles hold bq queries x bk*nk keys.  delta >= 0: safety margin of Eq. (7).
+ * tau >= 0: threshold of Eq. (8); tau = +INFINITY is the pure 8-bit path (no
+ * recomputation, the paper's 8-bit baseline) and tau = 0 recomputes every
+ * active sub-block (16-bit FlashAttention in the paper's formats).
+ *
+ * Outputs: o (normalised attention output), lse (mu + ln omega per query row,
+ * natural log), mask (codes above).  Every mask byte of the rows is written.
+ *
+ * Built configurations (LAMP_ERR_UNSUPPORTED otherwise): d in {64, 128, 256};
+ * bq in {64, 128}; (bk, nk) in {(16, 4), (64, 4)}; N a multiple of bq and of
+ * bk * nk; N <= 2^20.
+ *
+ * The first call on a device builds the library's exponential tables; the
+ * library also keeps a grow-only per-device workspace (fp32 copies of the
+ * pre-scaled Q and of K, an fp64 copy of K), allocated with hipMalloc when a
+ * call needs more than it holds.
+ */
+int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                  int B, int Hq, int Hkv, int N, int d,
+                  int causal, int window, int bq, int bk, int nk,
+                  double delta, double tau,
+                  float *o, float *lse, uint8_t *mask, void *stream);
+
+/*
+ * lamp_attn_logits8 -- the 8-bit logits alone (Alg. 1, first accumulation;
+ * Sec. 4.1 recursive FMA summation rounded to e4m3 after every step).
+ * Writes the e4m3 codes of rows [row0, row0 + nrows) of every (b, h):
+ * y8 [B][Hq][nrows][N]; invisible entries hold 0xFF.  d in {64, 128, 256},
+ * N a multiple of 16, 0 <= row0, row0 + nrows <= N.
+ */
+int lamp_attn_logits8(const uint16_t *q, const uint16_t *k,
+                      int B, int Hq, int Hkv, int N, int d, int causal, int window,
+                      int row0, int nrows, uint8_t *y8, void *stream);
+
+/*
+ * lamp_attn_logits16 -- the 16-bit logits of the recompute steps (Alg. 1):
+ * the dot product of the pre-scaled query and the key accumulated in fp64 in
+ * ascending channel order, rounded once to e4m11 (saturating).  Codes
+ * [B][Hq][nrows][N] uint16; invisible entries hold 0xFFFF.
+ */
+int lamp_attn_logits16(const uint16_t *q, const uint16_t *k,
+                       int B, int Hq, int Hkv, int N, int d, int causal, int window,
+                       int row0, int nrows, uint16_t *y16, void *stream);
+
+/* Build the device tables of `device` now (otherwise done by the first call). */
+int lamp_init(int device);
+
+/* Release every device table and workspace the library holds. */
+void lamp_shutdown(void);
+
+/*
+ * Diagnostics used by the test suite.
+ *
+ * lamp_selftest_e4m3: e4m3 codes of fp32 values, in[n] -> out[n] (device
+ * pointers), by the same rounding sequence as the 8-bit accumulation (the
+ * hardware conversion, saturating at +-448); raw (device, may be NULL)
+ * receives the codes of the non-saturating hardware conversion alone.
+ * lamp_selftest_exp_doc: the fp64 exponential used for the rescale factor
+ * exp(mu - mu_hat), x[n] -> y[n] (device pointers).
+ * lamp_get_tables: copies the device exponential tables to HOST memory:
+ * lut8[256] (ue5m3 shift code -> ue5m3 exp code) and exp16[65536] (ue5m11
+ * shift code -> ue5m11 exp code); either pointer may be NULL.
+ */
+int lamp_selftest_e4m3(const float *in, uint8_t *out, uint8_t *raw, size_t n, void *stream);
+int lamp_selftest_exp_doc(const double *x, double *y, size_t n, void *stream);
+int lamp_get_tables(int device, uint8_t *lut8, uint16_t *exp16);
+
+const char *lamp_status_str(int status);
+const char *lamp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LAMP_H */

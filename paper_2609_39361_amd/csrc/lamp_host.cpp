@@ -1,0 +1,334 @@
+// lamp_host.cpp -- the C ABI of liblamp.so (declared in include/lamp.h):
+// argument validation, per-device tables and workspace, kernel launches.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "lamp.h"
+#include "lamp_kernels.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int status, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+#define HIP_TRY(expr)                                                                              \
+    do {                                                                                           \
+        hipError_t e_ = (expr);                                                                    \
+        if (e_ != hipSuccess) return fail(LAMP_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_));  \
+    } while (0)
+
+struct DeviceState {
+    bool ready = false;
+    uint8_t *lut8 = nullptr;
+    uint16_t *lut8e = nullptr;
+    uint16_t *exp16 = nullptr;
+    void *ws = nullptr;
+    size_t ws_bytes = 0;
+};
+
+std::mutex g_mu;
+std::vector<DeviceState> g_dev;
+
+DeviceState *state_of(int dev)
+{
+    if (dev < 0) return nullptr;
+    if ((size_t)dev >= g_dev.size()) g_dev.resize((size_t)dev + 1);
+    return &g_dev[(size_t)dev];
+}
+
+// Build the exponential tables of the current device (lock held).
+int init_locked(int dev)
+{
+    DeviceState *st = state_of(dev);
+    if (st->ready) return LAMP_OK;
+    HIP_TRY(hipMalloc(&st->lut8, 256));
+    HIP_TRY(hipMalloc(&st->lut8e, 256 * sizeof(uint16_t)));
+    HIP_TRY(hipMalloc(&st->exp16, 65536 * sizeof(uint16_t)));
+    unsigned *amb = nullptr;
+    HIP_TRY(hipMalloc(&amb, sizeof(unsigned)));
+    HIP_TRY(hipMemset(amb, 0, sizeof(unsigned)));
+    HIP_TRY(lamp::launch_build_tables(st->lut8, st->lut8e, st->exp16, amb, nullptr));
+    unsigned h_amb = 0;
+    HIP_TRY(hipMemcpy(&h_amb, amb, sizeof(unsigned), hipMemcpyDeviceToHost));
+    HIP_TRY(hipFree(amb));
+    if (h_amb != 0) return fail(LAMP_ERR_INIT, "%u exponential table entries could not be rounded with certainty", h_amb);
+    st->ready = true;
+    return LAMP_OK;
+}
+
+int current_device(int *dev)
+{
+    HIP_TRY(hipGetDevice(dev));
+    return LAMP_OK;
+}
+
+// Scale applied to Q before accumulation, RN32(1/sqrt(d)).
+float scale_of(int d)
+{
+    switch (d) {
+    case 64: return 0.125f;
+    case 256: return 0.0625f;
+    case 128: {
+        uint32_t b = 0x3DB504F3u;   // RN32(1/sqrt(128))
+        float f;
+        std::memcpy(&f, &b, 4);
+        return f;
+    }
+    default: return 0.0f;
+    }
+}
+
+struct Workspace {
+    float *qt;
+    float *kt32;
+    double *kt64;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Grow-only workspace for the pre-scaled Q and the regrouped K (lock held).
+int workspace_locked(int dev, int B, int Hq, int Hkv, int N, int d, Workspace *w)
+{
+    DeviceState *st = state_of(dev);
+    size_t nq = (size_t)B * Hq * N * d, nk = (size_t)B * Hkv * N * d;
+    size_t bq = align256(nq * 4), bk32 = align256(nk * 4), bk64 = align256(nk * 8);
+    size_t need = bq + bk32 + bk64;
+    if (need > st->ws_bytes) {
+        if (st->ws) {
+            HIP_TRY(hipDeviceSynchronize());
+            HIP_TRY(hipFree(st->ws));
+            st->ws = nullptr;
+            st->ws_bytes = 0;
+        }
+        HIP_TRY(hipMalloc(&st->ws, need));
+        st->ws_bytes = need;
+    }
+    char *base = static_cast<char *>(st->ws);
+    w->qt = reinterpret_cast<float *>(base);
+    w->kt32 = reinterpret_cast<float *>(base + bq);
+    w->kt64 = reinterpret_cast<double *>(base + bq + bk32);
+    return LAMP_OK;
+}
+
+int check_common(const void *q, const void *k, int B, int Hq, int Hkv, int N, int d, int causal, int window)
+{
+    if (!q || !k) return fail(LAMP_ERR_INVALID_ARG, "null input pointer");
+    if (B <= 0 || Hq <= 0 || Hkv <= 0 || N <= 0 || d <= 0)
+        return fail(LAMP_ERR_INVALID_ARG, "sizes must be positive (B=%d Hq=%d Hkv=%d N=%d d=%d)", B, Hq, Hkv, N, d);
+    if (Hq % Hkv) return fail(LAMP_ERR_INVALID_ARG, "Hq=%d is not a multiple of Hkv=%d", Hq, Hkv);
+    if (causal != 0 && causal != 1) return fail(LAMP_ERR_INVALID_ARG, "causal must be 0 or 1");
+    if (window < 0) return fail(LAMP_ERR_INVALID_ARG, "window must be >= 0");
+    if (window > 0 && !causal) return fail(LAMP_ERR_INVALID_ARG, "a sliding window requires causal=1");
+    if (d != 64 && d != 128 && d != 256) return fail(LAMP_ERR_UNSUPPORTED, "head dimension %d not built (64, 128, 256)", d);
+    if (N > (1 << 20)) return fail(LAMP_ERR_UNSUPPORTED, "N=%d above 2^20", N);
+    if ((size_t)B * Hq * (size_t)N > (size_t)1 << 31) return fail(LAMP_ERR_UNSUPPORTED, "B*Hq*N above 2^31");
+    return LAMP_OK;
+}
+
+} // namespace
+
+extern "C" {
+
+const char *lamp_status_str(int s)
+{
+    switch (s) {
+    case LAMP_OK: return "ok";
+    case LAMP_ERR_INVALID_ARG: return "invalid argument";
+    case LAMP_ERR_UNSUPPORTED: return "unsupported configuration";
+    case LAMP_ERR_HIP: return "HIP runtime error";
+    case LAMP_ERR_INIT: return "device table initialisation failed";
+    default: return "unknown status";
+    }
+}
+
+const char *lamp_last_error(void) { return g_err; }
+
+int lamp_init(int device)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    int prev = 0;
+    HIP_TRY(hipGetDevice(&prev));
+    HIP_TRY(hipSetDevice(device));
+    int rc = init_locked(device);
+    HIP_TRY(hipSetDevice(prev));
+    return rc;
+}
+
+void lamp_shutdown(void)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    int prev = 0;
+    if (hipGetDevice(&prev) != hipSuccess) return;
+    for (size_t i = 0; i < g_dev.size(); ++i) {
+        DeviceState &st = g_dev[i];
+        if (!st.ready && !st.ws) continue;
+        if (hipSetDevice((int)i) != hipSuccess) continue;
+        (void)hipDeviceSynchronize();
+        (void)hipFree(st.lut8);
+        (void)hipFree(st.lut8e);
+        (void)hipFree(st.exp16);
+        (void)hipFree(st.ws);
+        st = DeviceState();
+    }
+    (void)hipSetDevice(prev);
+}
+
+int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B, int Hq, int Hkv, int N, int d,
+                  int causal, int window, int bq, int bk, int nk, double delta, double tau, float *o, float *lse,
+                  uint8_t *mask, void *stream)
+{
+    int rc = check_common(q, k, B, Hq, Hkv, N, d, causal, window);
+    if (rc) return rc;
+    if (!v || !o || !lse || !mask) return fail(LAMP_ERR_INVALID_ARG, "null pointer among v, o, lse, mask");
+    if (!(delta >= 0.0) || std::isinf(delta)) return fail(LAMP_ERR_INVALID_ARG, "delta must be finite and >= 0");
+    if (!(tau >= 0.0)) return fail(LAMP_ERR_INVALID_ARG, "tau must be >= 0 (or +inf)");
+    if (bq <= 0 || bk <= 0 || nk <= 0) return fail(LAMP_ERR_INVALID_ARG, "block sizes must be positive");
+    if (N % bq || N % (bk * nk))
+        return fail(LAMP_ERR_INVALID_ARG, "N=%d must be a multiple of bq=%d and of bk*nk=%d", N, bq, bk * nk);
+    int dev = 0;
+    rc = current_device(&dev);
+    if (rc) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    lamp::FwdParams p{};
+    Workspace w{};
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        rc = init_locked(dev);
+        if (rc) return rc;
+        rc = workspace_locked(dev, B, Hq, Hkv, N, d, &w);
+        if (rc) return rc;
+        DeviceState *st = state_of(dev);
+        p.exp16 = st->exp16;
+        p.lut8e = st->lut8e;
+    }
+    p.qt = w.qt;
+    p.kt32 = w.kt32;
+    p.kt64 = w.kt64;
+    p.v = v;
+    p.o = o;
+    p.lse = lse;
+    p.mask = mask;
+    p.B = B;
+    p.Hq = Hq;
+    p.Hkv = Hkv;
+    p.N = N;
+    p.causal = causal;
+    p.window = window;
+    p.delta = delta;
+    p.tau = tau;
+    p.mode = std::isinf(tau) ? lamp::MODE_PURE8 : (tau == 0.0 ? lamp::MODE_ALL16 : lamp::MODE_LAMP);
+    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, w.kt64, B, Hq, Hkv, N, d, scale_of(d), s));
+    bool found = false;
+    HIP_TRY(lamp::dispatch_fwd(d, bq, bk, nk, p, s, &found));
+    if (!found)
+        return fail(LAMP_ERR_UNSUPPORTED, "block sizes (bq=%d, bk=%d, nk=%d) not built for d=%d", bq, bk, nk, d);
+    return LAMP_OK;
+}
+
+static int logits_common(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv, int N, int d, int causal,
+                         int window, int row0, int nrows, void *out, lamp::LogitsParams *p, Workspace *w)
+{
+    int rc = check_common(q, k, B, Hq, Hkv, N, d, causal, window);
+    if (rc) return rc;
+    if (!out) return fail(LAMP_ERR_INVALID_ARG, "null output pointer");
+    if (N % 16) return fail(LAMP_ERR_UNSUPPORTED, "N=%d is not a multiple of 16", N);
+    if (row0 < 0 || nrows <= 0 || row0 + nrows > N) return fail(LAMP_ERR_INVALID_ARG, "row range outside [0, N)");
+    int dev = 0;
+    rc = current_device(&dev);
+    if (rc) return rc;
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        rc = init_locked(dev);
+        if (rc) return rc;
+        rc = workspace_locked(dev, B, Hq, Hkv, N, d, w);
+        if (rc) return rc;
+    }
+    *p = lamp::LogitsParams{};
+    p->qt = w->qt;
+    p->kt32 = w->kt32;
+    p->kt64 = w->kt64;
+    p->B = B;
+    p->Hq = Hq;
+    p->Hkv = Hkv;
+    p->N = N;
+    p->causal = causal;
+    p->window = window;
+    p->row0 = row0;
+    p->nrows = nrows;
+    return LAMP_OK;
+}
+
+int lamp_attn_logits8(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv, int N, int d, int causal,
+                      int window, int row0, int nrows, uint8_t *y8, void *stream)
+{
+    lamp::LogitsParams p;
+    Workspace w;
+    int rc = logits_common(q, k, B, Hq, Hkv, N, d, causal, window, row0, nrows, y8, &p, &w);
+    if (rc) return rc;
+    p.y8 = y8;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, w.kt64, B, Hq, Hkv, N, d, scale_of(d), s));
+    HIP_TRY(lamp::launch_logits8(p, d, s));
+    return LAMP_OK;
+}
+
+int lamp_attn_logits16(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv, int N, int d, int causal,
+                       int window, int row0, int nrows, uint16_t *y16, void *stream)
+{
+    lamp::LogitsParams p;
+    Workspace w;
+    int rc = logits_common(q, k, B, Hq, Hkv, N, d, causal, window, row0, nrows, y16, &p, &w);
+    if (rc) return rc;
+    p.y16 = y16;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, w.kt64, B, Hq, Hkv, N, d, scale_of(d), s));
+    HIP_TRY(lamp::launch_logits16(p, d, s));
+    return LAMP_OK;
+}
+
+int lamp_selftest_e4m3(const float *in, uint8_t *out, uint8_t *raw, size_t n, void *stream)
+{
+    if (!in || !out) return fail(LAMP_ERR_INVALID_ARG, "null pointer");
+    if (n == 0) return LAMP_OK;
+    HIP_TRY(lamp::launch_selftest_e4m3(in, out, raw, n, static_cast<hipStream_t>(stream)));
+    return LAMP_OK;
+}
+
+int lamp_selftest_exp_doc(const double *x, double *y, size_t n, void *stream)
+{
+    if (!x || !y) return fail(LAMP_ERR_INVALID_ARG, "null pointer");
+    if (n == 0) return LAMP_OK;
+    HIP_TRY(lamp::launch_selftest_exp_doc(x, y, n, static_cast<hipStream_t>(stream)));
+    return LAMP_OK;
+}
+
+int lamp_get_tables(int device, uint8_t *lut8, uint16_t *exp16)
+{
+    int rc = lamp_init(device);
+    if (rc) return rc;
+    std::lock_guard<std::mutex> lk(g_mu);
+    int prev = 0;
+    HIP_TRY(hipGetDevice(&prev));
+    HIP_TRY(hipSetDevice(device));
+    DeviceState *st = state_of(device);
+    if (lut8) HIP_TRY(hipMemcpy(lut8, st->lut8, 256, hipMemcpyDeviceToHost));
+    if (exp16) HIP_TRY(hipMemcpy(exp16, st->exp16, 65536 * sizeof(uint16_t), hipMemcpyDeviceToHost));
+    HIP_TRY(hipSetDevice(prev));
+    return LAMP_OK;
+}
+
+} // extern "C"

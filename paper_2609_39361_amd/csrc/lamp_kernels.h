@@ -1,0 +1,45 @@
+// lamp_kernels.h -- kernel parameter blocks and launchers (library-internal).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace lamp {
+
+enum { MODE_LAMP = 0, MODE_PURE8 = 1, MODE_ALL16 = 2 };
+
+struct FwdParams {
+    const float *qt;          // [B][Hq][N][D] pre-scaled queries, fp32
+    const float *kt32;        // [B][Hkv][N/16][D][16] keys, fp32
+    const double *kt64;       // same layout, fp64
+    const uint16_t *v;        // [B][Hkv][N][D] bf16
+    const uint16_t *exp16;    // ue5m11 shift code -> ue5m11 exp code
+    const uint16_t *lut8e;    // ue5m3 shift code -> bf16 bits of the ue5m3 exp
+    float *o;                 // [B][Hq][N][D]
+    float *lse;               // [B][Hq][N]
+    uint8_t *mask;            // [B][Hq][N/BQ][N/BK]
+    int B, Hq, Hkv, N;
+    int causal, window, mode;
+    double delta, tau;
+};
+
+struct LogitsParams {
+    const float *qt;
+    const float *kt32;
+    const double *kt64;
+    uint8_t *y8;
+    uint16_t *y16;
+    int B, Hq, Hkv, N, causal, window, row0, nrows;
+};
+
+hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found);
+hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float *kt32, double *kt64,
+                          int B, int Hq, int Hkv, int N, int D, float scale, hipStream_t s);
+hipError_t launch_logits8(const LogitsParams &p, int D, hipStream_t s);
+hipError_t launch_logits16(const LogitsParams &p, int D, hipStream_t s);
+hipError_t launch_build_tables(uint8_t *lut8, uint16_t *lut8e, uint16_t *exp16, unsigned *ambiguous,
+                               hipStream_t s);
+hipError_t launch_selftest_e4m3(const float *in, uint8_t *out, uint8_t *raw, size_t n, hipStream_t s);
+hipError_t launch_selftest_exp_doc(const double *x, double *y, size_t n, hipStream_t s);
+
+} // namespace lamp

@@ -1,0 +1,185 @@
+"""Python binding of liblamp.so (the C ABI declared in include/lamp.h).
+
+Argument marshalling only: every step of the forward pass runs in the HIP
+kernels of the library.  PyTorch provides device memory and the stream.  The
+library must have been built (python -m paper_2609_39361_amd.build); there is
+no fallback path.
+"""
+import ctypes
+import math
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liblamp.so")
+
+LAMP_OK = 0
+MASK_LOW, MASK_STAGE1, MASK_STAGE2, MASK_INACTIVE = 0, 1, 2, 3
+
+
+class LampError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__("lamp status %d: %s" % (status, msg))
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """The loaded C library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("liblamp.so is not built; run `python -m paper_2609_39361_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, f64, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_double, ctypes.c_size_t
+        L.lamp_attn_fwd.argtypes = [P, P, P] + [i32] * 5 + [i32] * 5 + [f64, f64, P, P, P, P]
+        L.lamp_attn_fwd.restype = i32
+        L.lamp_attn_logits8.argtypes = [P, P] + [i32] * 9 + [P, P]
+        L.lamp_attn_logits8.restype = i32
+        L.lamp_attn_logits16.argtypes = [P, P] + [i32] * 9 + [P, P]
+        L.lamp_attn_logits16.restype = i32
+        L.lamp_init.argtypes = [i32]
+        L.lamp_init.restype = i32
+        L.lamp_shutdown.argtypes = []
+        L.lamp_shutdown.restype = None
+        L.lamp_selftest_e4m3.argtypes = [P, P, P, sz, P]
+        L.lamp_selftest_e4m3.restype = i32
+        L.lamp_selftest_exp_doc.argtypes = [P, P, sz, P]
+        L.lamp_selftest_exp_doc.restype = i32
+        L.lamp_get_tables.argtypes = [i32, P, P]
+        L.lamp_get_tables.restype = i32
+        L.lamp_status_str.argtypes = [i32]
+        L.lamp_status_str.restype = ctypes.c_char_p
+        L.lamp_last_error.argtypes = []
+        L.lamp_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(rc):
+    if rc != LAMP_OK:
+        L = lib()
+        raise LampError(rc, "%s: %s" % (L.lamp_status_str(rc).decode(), L.lamp_last_error().decode()))
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _check_inputs(q, k, v=None):
+    for t in (q, k) + ((v,) if v is not None else ()):
+        if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous() or t.dim() != 4:
+            raise ValueError("q, k, v must be contiguous 4-d bf16 CUDA tensors [B,H,N,d]")
+    B, Hq, N, d = q.shape
+    if k.shape[0] != B or k.shape[2] != N or k.shape[3] != d:
+        raise ValueError("k shape %s does not match q %s" % (tuple(k.shape), tuple(q.shape)))
+    if v is not None and v.shape != k.shape:
+        raise ValueError("v shape %s differs from k %s" % (tuple(v.shape), tuple(k.shape)))
+    if q.device != k.device or (v is not None and v.device != q.device):
+        raise ValueError("q, k, v must be on one device")
+    return B, Hq, k.shape[1], N, d
+
+
+def attn_fwd(q, k, v, causal=True, window=0, bq=128, bk=16, nk=4, delta=2.0 ** -8, tau=0.5, out=None):
+    """LampAttention forward pass.  Returns (o fp32 [B,Hq,N,d], lse fp32
+    [B,Hq,N], mask uint8 [B,Hq,N/bq,N/bk]).  `out` may supply those three
+    tensors to write into."""
+    B, Hq, Hkv, N, d = _check_inputs(q, k, v)
+    dev = q.device
+    if out is None:
+        o = torch.empty((B, Hq, N, d), dtype=torch.float32, device=dev)
+        lse = torch.empty((B, Hq, N), dtype=torch.float32, device=dev)
+        mask = torch.empty((B, Hq, N // bq, N // bk), dtype=torch.uint8, device=dev)
+    else:
+        o, lse, mask = out
+    with torch.cuda.device(dev):
+        rc = lib().lamp_attn_fwd(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(causal), int(window),
+                                 bq, bk, nk, float(delta), float(tau), _ptr(o), _ptr(lse), _ptr(mask),
+                                 _stream(dev))
+    _check(rc)
+    return o, lse, mask
+
+
+def logits8(q, k, causal=True, window=0, row0=0, nrows=None):
+    """e4m3 codes of the 8-bit logits of rows [row0, row0+nrows): uint8 [B,Hq,nrows,N], 0xFF invisible."""
+    B, Hq, Hkv, N, d = _check_inputs(q, k)
+    nrows = N - row0 if nrows is None else nrows
+    y = torch.empty((B, Hq, nrows, N), dtype=torch.uint8, device=q.device)
+    with torch.cuda.device(q.device):
+        rc = lib().lamp_attn_logits8(_ptr(q), _ptr(k), B, Hq, Hkv, N, d, int(causal), int(window), row0, nrows,
+                                     _ptr(y), _stream(q.device))
+    _check(rc)
+    return y
+
+
+def logits16(q, k, causal=True, window=0, row0=0, nrows=None):
+    """e4m11 codes of the 16-bit logits: int16 bit patterns [B,Hq,nrows,N] (0xFFFF invisible)."""
+    B, Hq, Hkv, N, d = _check_inputs(q, k)
+    nrows = N - row0 if nrows is None else nrows
+    y = torch.empty((B, Hq, nrows, N), dtype=torch.int16, device=q.device)
+    with torch.cuda.device(q.device):
+        rc = lib().lamp_attn_logits16(_ptr(q), _ptr(k), B, Hq, Hkv, N, d, int(causal), int(window), row0, nrows,
+                                      _ptr(y), _stream(q.device))
+    _check(rc)
+    return y
+
+
+def selftest_e4m3(x):
+    """(codes, raw codes) of fp32 CUDA tensor x by the device rounding sequence."""
+    assert x.dtype == torch.float32 and x.is_cuda and x.is_contiguous()
+    out = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
+    raw = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
+    with torch.cuda.device(x.device):
+        _check(lib().lamp_selftest_e4m3(_ptr(x), _ptr(out), _ptr(raw), x.numel(), _stream(x.device)))
+    return out, raw
+
+
+def selftest_exp_doc(x):
+    assert x.dtype == torch.float64 and x.is_cuda and x.is_contiguous()
+    y = torch.empty_like(x)
+    with torch.cuda.device(x.device):
+        _check(lib().lamp_selftest_exp_doc(_ptr(x), _ptr(y), x.numel(), _stream(x.device)))
+    return y
+
+
+def get_tables(device=0):
+    """(lut8 uint8[256], exp16 uint16[65536]) numpy copies of the device tables."""
+    import numpy as np
+    lut8 = np.empty(256, dtype=np.uint8)
+    exp16 = np.empty(65536, dtype=np.uint16)
+    _check(lib().lamp_get_tables(int(device), lut8.ctypes.data_as(ctypes.c_void_p),
+                                 exp16.ctypes.data_as(ctypes.c_void_p)))
+    return lut8, exp16
+
+
+def init(device=0):
+    _check(lib().lamp_init(int(device)))
+
+
+def shutdown():
+    lib().lamp_shutdown()
+
+
+def mask_stats(mask, nk):
+    """Recompute statistics from a mask [B,Hq,N/bq,N/bk]: per key tile (nk
+    sub-blocks, at least one active) the number of 16-bit sub-blocks, as a
+    histogram 0..nk, plus counts per code.  Reporting only."""
+    m = mask.reshape(-1, nk)
+    active = (m != MASK_INACTIVE)
+    tiles = active.any(dim=1)
+    rec = ((m == MASK_STAGE1) | (m == MASK_STAGE2)).sum(dim=1)[tiles]
+    hist = torch.bincount(rec.to(torch.int64), minlength=nk + 1).cpu().tolist()
+    counts = torch.bincount(mask.reshape(-1).to(torch.int64), minlength=4).cpu().tolist()
+    n_active = counts[0] + counts[1] + counts[2]
+    return {
+        "tile_hist": hist,
+        "low": counts[0], "stage1": counts[1], "stage2": counts[2], "inactive": counts[3],
+        "recompute_fraction": (counts[1] + counts[2]) / n_active if n_active else math.nan,
+    }

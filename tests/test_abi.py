@@ -1,0 +1,70 @@
+"""The C-ABI library loads on the CPU and exports every function that
+include/lamp.h declares (no compute calls: there is no GPU here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lamp.h")
+LIB = os.path.join(ROOT, "paper_2609_39361_amd", "liblamp.so")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(lamp_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for n in ("lamp_attn_fwd", "lamp_attn_logits8", "lamp_attn_logits16", "lamp_init", "lamp_shutdown",
+              "lamp_status_str", "lamp_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    if not os.path.exists(LIB):
+        pytest.skip("liblamp.so not built")
+    lib = ctypes.CDLL(LIB)
+    missing = [n for n in _declared() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_status_strings_without_gpu():
+    if not os.path.exists(LIB):
+        pytest.skip("liblamp.so not built")
+    lib = ctypes.CDLL(LIB)
+    lib.lamp_status_str.restype = ctypes.c_char_p
+    lib.lamp_status_str.argtypes = [ctypes.c_int]
+    assert lib.lamp_status_str(0) == b"ok"
+    assert lib.lamp_status_str(2) == b"unsupported configuration"
+
+
+def test_binding_rejects_bad_arguments_without_gpu():
+    """Host-side validation runs before any device call."""
+    if not os.path.exists(LIB):
+        pytest.skip("liblamp.so not built")
+    lib = ctypes.CDLL(LIB)
+    lib.lamp_attn_fwd.restype = ctypes.c_int
+    P = ctypes.c_void_p
+    lib.lamp_attn_fwd.argtypes = [P, P, P] + [ctypes.c_int] * 10 + [ctypes.c_double] * 2 + [P, P, P, P]
+    lib.lamp_last_error.restype = ctypes.c_char_p
+    dummy = P(16)
+    # Hq not a multiple of Hkv
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 3, 2, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5,
+                           dummy, dummy, dummy, None)
+    assert rc == 1 and b"multiple" in lib.lamp_last_error()
+    # unsupported head dimension
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 96, 1, 0, 128, 16, 4, 2 ** -8, 0.5,
+                           dummy, dummy, dummy, None)
+    assert rc == 2
+    # window without causal
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 0, 16, 128, 16, 4, 2 ** -8, 0.5,
+                           dummy, dummy, dummy, None)
+    assert rc == 1
+    # negative threshold
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, -1.0,
+                           dummy, dummy, dummy, None)
+    assert rc == 1

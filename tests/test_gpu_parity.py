@@ -1,0 +1,209 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Bar: e4m3 / e4m11 logit codes, exponential tables, the fp64 rescale
+exponential and the recompute masks bit-exact; O within 2e-3 * max|O|
+(fp32 matrix-core accumulation vs the oracle's fp64); lse within 1e-4.
+"""
+import math
+import sys
+import time
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2609_39361_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+O_TOL = 2e-3
+LSE_TOL = 1e-4
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+@pytest.fixture(scope="module")
+def L():
+    _need_gpu()
+    from paper_2609_39361_amd import lamp
+    lamp.init(0)
+    return lamp
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+# ------------------------------------------------------------------ codecs
+def test_e4m3_exhaustive_vs_oracle(L):
+    """Every fp32 bit pattern: the device rounding sequence equals the oracle.
+    The emulator relies on two facts about the non-saturating hardware
+    conversion, checked here as well: it returns either the correct code or a
+    NaN code (never a wrong finite code), and a NaN input gives a NaN code."""
+    chunk = 1 << 28
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    nan_lo = np.inf
+    for c in range(16):
+        start = c * chunk
+        bits = (torch.arange(chunk, dtype=torch.int64, device=dev) + start).to(torch.int32)
+        x = bits.view(torch.float32)
+        out, raw = L.selftest_e4m3(x)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        rawh = raw.cpu().numpy()
+        ref = O.e4m3_of_f32_bits(start, chunk)
+        xf = x.cpu().numpy()
+        isnan = np.isnan(xf)
+        mism = (got != ref) & ~isnan
+        assert not mism.any(), "chunk %d: %d mismatches, first at bits 0x%08x" % (
+            c, mism.sum(), start + int(np.argmax(mism)))
+        rawnan = (rawh & 0x7F) == 0x7F
+        assert np.all(rawnan[isnan]), "chunk %d: a NaN input gave a finite code" % c
+        bad = ~rawnan & ~isnan & (rawh != ref)
+        assert not bad.any(), "chunk %d: raw conversion gave a wrong finite code at 0x%08x" % (
+            c, start + int(np.argmax(bad)))
+        fin = rawnan & ~isnan
+        if fin.any():
+            nan_lo = min(nan_lo, float(np.abs(xf[fin]).min()))
+        _say("e4m3 chunk %d/16 ok (%.1fs)" % (c + 1, time.time() - t0))
+        del bits, x, out, raw
+    _say("smallest |x| whose raw conversion is NaN: %r" % nan_lo)
+    assert nan_lo > 448.0
+
+def test_tables_match_oracle(L):
+    lut8, exp16 = L.get_tables(0)
+    olut8, oexp16 = O.tables()
+    assert np.array_equal(lut8, olut8)
+    assert np.array_equal(exp16, oexp16)
+
+
+def test_exp_doc_bitexact(L):
+    rng = np.random.default_rng(5)
+    x = np.concatenate([-rng.uniform(0, 720, 500_000), -rng.uniform(0, 2, 200_000),
+                        -np.ldexp(1.0, -rng.integers(1, 60, 10_000)), [0.0, -700.0, -700.0000001, -1e-300]])
+    y = L.selftest_exp_doc(torch.from_numpy(x).cuda()).cpu().numpy()
+    ref = O.exp_doc(x)
+    assert np.array_equal(y.view(np.uint64), ref.view(np.uint64))
+
+
+# ------------------------------------------------------------------ logits
+LOGIT_CASES = [
+    W.small("l_nc_d64", N=128, d=64, Hq=2, Hkv=1, causal=0, seed=101),
+    W.small("l_causal_d128", N=192, d=128, Hq=4, Hkv=2, causal=1, seed=102),
+    W.small("l_window_d128", N=256, d=128, Hq=1, Hkv=1, causal=1, window=40, seed=103),
+    W.small("l_outlier_d64", N=128, d=64, Hq=1, Hkv=1, causal=0, seed=104, kind="outlier",
+            n_outlier=2, outlier_gain=16.0),
+    W.small("l_saturate_d128", N=64, d=128, Hq=1, Hkv=1, causal=0, seed=105, extra={"gain": 12.0}),
+    W.small("l_d256", N=64, d=256, Hq=2, Hkv=2, causal=1, seed=106),
+]
+
+
+@pytest.mark.parametrize("w", LOGIT_CASES, ids=[w.name for w in LOGIT_CASES])
+def test_logits8_bitexact(L, w):
+    q, k, v = W.make_inputs(w)
+    ref = O.logits8(O.bf16_bits(q), O.bf16_bits(k), w.causal, w.window, 0, w.N)
+    got = L.logits8(q.cuda(), k.cuda(), w.causal, w.window, 0, w.N).cpu().numpy()
+    assert np.array_equal(got, ref), "%d mismatching codes" % (got != ref).sum()
+
+
+@pytest.mark.parametrize("w", LOGIT_CASES[:4] + LOGIT_CASES[5:], ids=[w.name for w in LOGIT_CASES[:4] + LOGIT_CASES[5:]])
+def test_logits16_bitexact(L, w):
+    q, k, v = W.make_inputs(w)
+    ref = O.logits16(O.bf16_bits(q), O.bf16_bits(k), w.causal, w.window, 0, w.N)
+    got = L.logits16(q.cuda(), k.cuda(), w.causal, w.window, 0, w.N).cpu().numpy().view(np.uint16)
+    vis = ref != 0xFFFF
+    assert np.array_equal(got[vis], ref[vis])
+
+
+def test_logits8_row_range_and_ragged_rows(L):
+    w = W.small("rows", N=256, d=128, Hq=2, Hkv=1, causal=1, seed=107)
+    q, k, v = W.make_inputs(w)
+    ref = O.logits8(O.bf16_bits(q), O.bf16_bits(k), 1, 0, 37, 91)
+    got = L.logits8(q.cuda(), k.cuda(), 1, 0, 37, 91).cpu().numpy()
+    assert np.array_equal(got, ref)
+
+
+# ------------------------------------------------------------------ forward
+def _compare_fwd(L, w, tau, delta=None, qblocks=None):
+    delta = w.delta if delta is None else delta
+    q, k, v = W.make_inputs(w)
+    qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
+    o, lse, mask = L.attn_fwd(qd, kd, vd, w.causal, w.window, w.bq, w.bk, w.nk, delta, tau)
+    torch.cuda.synchronize()
+    ro, rlse, rmask = O.fwd(O.bf16_bits(q), O.bf16_bits(k), O.bf16_bits(v), w.causal, w.window,
+                            w.bq, w.bk, w.nk, delta, tau, qblocks=qblocks)
+    o, lse, mask = o.cpu().numpy(), lse.cpu().numpy(), mask.cpu().numpy()
+    if qblocks is not None:
+        nqb = w.N // w.bq
+        sel = np.zeros((w.B, w.Hq, nqb), dtype=bool)
+        for f in qblocks:
+            sel.reshape(-1)[f] = True
+        rows = np.repeat(sel, w.bq, axis=2)
+        o, ro = o[rows], ro[rows]
+        lse, rlse = lse[rows], rlse[rows]
+        mask, rmask = mask[sel], rmask[sel]
+    assert np.array_equal(mask, rmask), "%d mask bytes differ" % (mask != rmask).sum()
+    scale = np.abs(ro).max()
+    err = np.abs(o - ro).max() / scale
+    assert err <= O_TOL, "O max-abs error %.3g of max|O| %.3g" % (err, scale)
+    assert np.abs(lse - rlse).max() <= LSE_TOL
+    return err, mask
+
+
+FWD_CASES = [
+    W.small("f_causal_d128_bq128", N=256, d=128, Hq=2, Hkv=1, bq=128, bk=16, nk=4, causal=1, seed=201),
+    W.small("f_causal_d64_bq64", N=256, d=64, Hq=2, Hkv=2, bq=64, bk=16, nk=4, causal=1, seed=202),
+    W.small("f_noncausal_d64_bk64", N=256, d=64, Hq=1, Hkv=1, bq=64, bk=64, nk=4, causal=0, seed=203,
+            kind="outlier", n_outlier=2, outlier_gain=16.0),
+    W.small("f_window_d128", N=512, d=128, Hq=1, Hkv=1, bq=128, bk=16, nk=4, causal=1, window=100, seed=204),
+    W.small("f_gqa_d128_bk64", N=512, d=128, Hq=4, Hkv=2, bq=128, bk=64, nk=4, causal=1, seed=205),
+    W.small("f_d256", N=256, d=256, Hq=2, Hkv=1, bq=128, bk=16, nk=4, causal=1, seed=206),
+]
+
+
+@pytest.mark.parametrize("tau", [math.inf, 1.0, 0.5, 2.0 ** -5, 0.0])
+@pytest.mark.parametrize("w", FWD_CASES, ids=[w.name for w in FWD_CASES])
+def test_fwd_parity_small(L, w, tau):
+    _compare_fwd(L, w, tau)
+
+
+def test_fwd_delta_variant(L):
+    _compare_fwd(L, FWD_CASES[0], 0.5, delta=2.0 ** -4)
+
+
+def test_fwd_config1_full(L):
+    w = W.CONFIGS[1]
+    err, mask = _compare_fwd(L, w, w.tau)
+    _say("config 1: O err %.2e, mask %s" % (err, np.bincount(mask.ravel(), minlength=4)))
+
+
+def test_fwd_config2_full(L):
+    w = W.CONFIGS[2]
+    err, mask = _compare_fwd(L, w, w.tau)
+    _say("config 2: O err %.2e, mask %s" % (err, np.bincount(mask.ravel(), minlength=4)))
+
+
+def _sample_blocks(w, n_per_head=2, heads=(0,)):
+    nqb = w.N // w.bq
+    out = []
+    for b in range(w.B):
+        for h in heads:
+            for qb in (nqb - 1, nqb // 3)[:n_per_head]:
+                out.append((b * w.Hq + h) * nqb + qb)
+    return out
+
+
+def test_fwd_config3_sampled(L):
+    """Qwen3-8B-shaped prefill at full size; the oracle computes sampled query
+    blocks (the last block of heads 0 and 31, and a middle one of head 0)."""
+    w = W.CONFIGS[3]
+    nqb = w.N // w.bq
+    qbl = [0 * nqb + nqb - 1, 0 * nqb + 21, 31 * nqb + nqb - 1]
+    err, mask = _compare_fwd(L, w, w.tau, qblocks=qbl)
+    _say("config 3 sampled: O err %.2e, mask %s" % (err, np.bincount(mask.ravel(), minlength=4)))
