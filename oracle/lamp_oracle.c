@@ -317,14 +317,15 @@ static double logit8(const float *qt, const uint16_t *k, int d)
 }
 
 /* High-precision logit (Alg. 1, recompute steps; Sec. 3.3 gives e4m11 as the
- * 16-bit accumulator format).  Reading: the dot product is accumulated in
- * fp64 by a sequential FMA chain in ascending channel order (every product
- * q_tilde*k is exact in fp64) and the sum is rounded once to e4m11. */
+ * 16-bit accumulator format).  Reading: as in the paper's simulation (Sec.
+ * 4.1: FP32 storage, recursive summation with FP32 FMA), the dot product is
+ * accumulated by a sequential FP32 FMA chain in ascending channel order,
+ * starting from +0, and the sum is rounded once to e4m11 (saturating). */
 static double logit16(const float *qt, const uint16_t *k, int d)
 {
-    double acc = 0.0;
-    for (int c = 0; c < d; ++c) acc = fma((double)qt[c], (double)bf16_to_f32(k[c]), acc);
-    return round_to_fmt(acc, &F_E4M11);
+    float acc = 0.0f;
+    for (int c = 0; c < d; ++c) acc = fmaf(qt[c], bf16_to_f32(k[c]), acc);
+    return round_to_fmt((double)acc, &F_E4M11);
 }
 
 static int visible(int64_t i, int64_t j, int causal, int window)

@@ -3,8 +3,8 @@ Algorithm 1) for tiny inputs, used to pin the C oracle.
 
 Written separately from the oracle with different methods:
   * numpy vectorised over a whole tile instead of scalar loops;
-  * the FP32 FMA of the 8-bit accumulation is emulated exactly from fp64
-    products and a TwoSum correction instead of calling fmaf;
+  * the FP32 FMAs of the 8- and 16-bit accumulations are emulated exactly
+    from fp64 products and a TwoSum correction instead of calling fmaf;
   * rounding to the formats with the integer model of fpmodel.py;
   * exponential tables from mpmath, lambda_hat from math.exp;
   * the stage-2 knapsack by brute force over every g in {0,1}^N_k.
@@ -55,7 +55,8 @@ def y8_tile(qt, kf):
 def y16_tile(qt, kf):
     acc = np.zeros((kf.shape[0], qt.shape[0]))
     for c in range(qt.shape[1]):
-        acc = acc + kf[:, c][:, None] * qt[:, c][None, :]   # exact product, one rounding
+        p = kf[:, c][:, None] * qt[:, c][None, :]           # exact in fp64
+        acc = rn32_sum(p, acc)                               # FP32 FMA step
     return M.np_round(acc, "e4m11")
 
 
