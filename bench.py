@@ -1,0 +1,184 @@
+#!/usr/bin/env python3
+"""Benchmark of the LampAttention forward pass on one MI355X.
+
+One step is one full forward pass (lamp_attn_fwd: prepass + the forward
+kernel) over the Qwen3-8B-shaped causal prefill (B=1, 32 query heads / 8 KV
+heads, d=128, N=8192, b_q=128, b_k=16, N_k=4, delta=2^-8, tau=2^-1) with
+synthetic inputs resident in HBM.  Prints one JSON line with the effective
+attention TFLOP/s (4*B*H*N^2*d, halved for causal), the recomputed-sub-block
+fraction, the VALU roofline of the forward kernel and the CPU oracle timed on
+a bounded sample of the same workload.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# MI355X peaks (public figures): 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz of
+# VALU issue (one fp32 FMA or conversion per lane per cycle).
+VALU_LANE_OPS = 256 * 4 * 16 * 2.4e9          # 39.3e12 lane-instructions / s
+# Fewest VALU lane-instructions per emulated 8-bit multiply-add on gfx950: one
+# fp32 FMA, half a packed round-to-e4m3 and half a packed decode.
+OPS_PER_MAC8 = 2.0
+# 16-bit recompute: one fp32 FMA per multiply-add.
+OPS_PER_MAC16 = 1.0
+
+
+def visible_in_mask(w, mask):
+    """Visible (query, key) pairs inside the recomputed sub-blocks."""
+    m = mask.reshape(w.B * w.Hq, w.N // w.bq, w.N // w.bk)
+    rec = (m == 1) | (m == 2)
+    qb = np.arange(w.N // w.bq)[:, None]
+    kb = np.arange(w.N // w.bk)[None, :]
+    # count visible pairs of each (query block, key sub-block) in closed form
+    j0 = qb * w.bq
+    i0 = kb * w.bk
+    cnt = np.zeros((w.N // w.bq, w.N // w.bk), dtype=np.int64)
+    for dj in range(w.bq):
+        j = j0 + dj
+        lo = np.maximum(i0, (j - w.window + 1) if w.window > 0 else i0)
+        hi = np.minimum(i0 + w.bk - 1, j if w.causal else i0 + w.bk - 1)
+        cnt += np.maximum(hi - lo + 1, 0)
+    return int((rec * cnt[None]).sum())
+
+
+def cpu_baseline(w, tau, q, k, v, budget_s=15.0, seed=0):
+    """The CPU oracle on a bounded, stated sample of query blocks."""
+    from oracle import oracle as O
+    rng = np.random.default_rng(seed)
+    nqb = w.N // w.bq
+    qbits, kbits, vbits = O.bf16_bits(q), O.bf16_bits(k), O.bf16_bits(v)
+    threads = O.max_threads()
+    # calibrate: one block of the median position, then as many as fit the budget
+    order = rng.permutation(w.B * w.Hq * nqb)
+    picked, spent, flops = [], 0.0, 0.0
+    first = True
+    while spent < budget_s and len(picked) < len(order):
+        n = 1 if first else max(1, min(threads, int((budget_s - spent) / max(spent / len(picked), 1e-3))))
+        batch = [int(x) for x in order[len(picked):len(picked) + n]]
+        t0 = time.perf_counter()
+        O.fwd(qbits, kbits, vbits, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau, qblocks=batch,
+              nthreads=threads)
+        spent += time.perf_counter() - t0
+        for f in batch:
+            qb = f % nqb
+            vis = 0
+            for dj in range(w.bq):
+                j = qb * w.bq + dj
+                lo = max(0, j - w.window + 1) if w.window > 0 else 0
+                hi = j if w.causal else w.N - 1
+                vis += hi - lo + 1
+            flops += 4.0 * vis * w.d
+        picked += batch
+        first = False
+    return {
+        "value": flops / spent / 1e12,
+        "unit": "TFLOP/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": "%d of %d query blocks (seeded random over heads and positions), %.1f s, "
+                  "effective FLOP counted over the sampled blocks' visible pairs" % (
+                      len(picked), w.B * w.Hq * nqb, spent),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", type=int, default=3, help="config id (1, 2, 3, 4, 40, 5)")
+    ap.add_argument("--tau", type=float, default=None)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: the forward pass is not sharded across GPUs "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_39361_amd import lamp, workloads as W
+
+    w = W.CONFIGS[args.workload]
+    tau = w.tau if args.tau is None else args.tau
+    dev = torch.device("cuda:0")
+    q, k, v = W.make_inputs(w)
+    qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
+    o = torch.empty((w.B, w.Hq, w.N, w.d), dtype=torch.float32, device=dev)
+    lse = torch.empty((w.B, w.Hq, w.N), dtype=torch.float32, device=dev)
+    mask = torch.empty((w.B, w.Hq, w.N // w.bq, w.N // w.bk), dtype=torch.uint8, device=dev)
+    out = (o, lse, mask)
+
+    def step():
+        lamp.attn_fwd(qd, kd, vd, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau, out=out)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        starts[i].record(stream)
+        step()
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    ms = float(np.mean(ev_ms))
+
+    st = lamp.mask_stats(mask, w.nk)
+    mask_np = mask.cpu().numpy()
+    mac8 = 0 if tau == 0 else w.macs
+    mac16 = visible_in_mask(w, mask_np) * w.d
+    alg_ops = OPS_PER_MAC8 * mac8 + OPS_PER_MAC16 * mac16
+    achieved = alg_ops / (ms * 1e-3) / 1e12
+    peak = VALU_LANE_OPS / 1e12
+    result = {
+        "metric": "effective attention TFLOP/s (4*B*H*N^2*d, halved for causal), 1 GPU",
+        "value": w.eff_flops / (ms * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "e4m3/e4m11 emulated (fp32 FMA + fp8 conversions), bf16 inputs, fp32 output",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "N": w.N, "d": w.d,
+                   "causal": w.causal, "window": w.window, "bq": w.bq, "bk": w.bk, "nk": w.nk,
+                   "delta": w.delta, "tau": tau},
+        "recompute_fraction": st["recompute_fraction"],
+        "tile_hist": st["tile_hist"],
+        "roofline": {
+            "bound": "alu",
+            "achieved": achieved,
+            "peak": peak,
+            "unit": "T VALU lane-ops/s",
+            "frac": achieved / peak,
+            "traffic": None,
+            "kernel": "lamp_fwd_kernel (events span the whole call: prepass + forward kernel)",
+            "ops_per_launch": alg_ops,
+            "algorithmic_frac_one_op_per_mac": mac8 / (ms * 1e-3) / VALU_LANE_OPS,
+        },
+        "wall_s_timed_region": wall,
+    }
+    if not args.no_cpu:
+        result["cpu_baseline"] = cpu_baseline(w, tau, q, k, v, budget_s=args.cpu_budget)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -70,8 +70,8 @@ enum {
  *
  * The first call on a device builds the library's exponential tables; the
  * library also keeps a grow-only per-device workspace (fp32 copies of the
- * pre-scaled Q and of K, an fp64 copy of K), allocated with hipMalloc when a
- * call needs more than it holds.
+ * pre-scaled Q and of K), allocated with hipMalloc when a call needs more
+ * than it holds.  Calls that overlap on one device race on that workspace.
  */
 int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                   int B, int Hq, int Hkv, int N, int d,
@@ -92,8 +92,8 @@ int lamp_attn_logits8(const uint16_t *q, const uint16_t *k,
 
 /*
  * lamp_attn_logits16 -- the 16-bit logits of the recompute steps (Alg. 1):
- * the dot product of the pre-scaled query and the key accumulated in fp64 in
- * ascending channel order, rounded once to e4m11 (saturating).  Codes
+ * the dot product of the pre-scaled query and the key accumulated by FP32
+ * FMAs in ascending channel order, rounded once to e4m11 (saturating).  Codes
  * [B][Hq][nrows][N] uint16; invisible entries hold 0xFFFF.
  */
 int lamp_attn_logits16(const uint16_t *q, const uint16_t *k,

@@ -18,7 +18,7 @@ LIB = os.path.join(HERE, "liblamp.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["lamp_kernels.hip", "lamp_host.cpp"]
+SOURCES = ["lamp_kernels.hip", "lamp_fwd.hip", "lamp_host.cpp"]
 
 
 def build(verbose=False, extra=()):

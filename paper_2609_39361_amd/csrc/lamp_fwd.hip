@@ -1,0 +1,695 @@
+// lamp_fwd.hip -- the LampAttention forward kernel for gfx950 (paper Alg. 1).
+//
+// One workgroup handles one (batch, query head, query block of BQ rows) and
+// walks its key tiles (KPT = BK*NK keys) in order.  Work split:
+//   * every lane holds QPL = BQ/64 query rows (rows lane and lane+64), and
+//     every wave keeps the running state (mu, omega) of all BQ rows -- the
+//     state is small and every wave derives it from the same shared data, so
+//     it stays identical across waves without extra traffic;
+//   * wave w owns SPW = NK/NW consecutive key sub-blocks of each tile: it
+//     computes their 8-bit logits, their 16-bit recomputes and their
+//     exponentials, and publishes per-row partial results in LDS;
+//   * wave w owns the channel slice [w*CPW, (w+1)*CPW) of the output and
+//     accumulates O^T = V^T E for that slice on the bf16 matrix cores.
+// Per tile (Alg. 1 inner loop):
+//   1. 8-bit logits of the own sub-blocks, column maxima m8 -> LDS;
+//   2. stage 1 (Sec. 3.1, Eq. (7)): threats, sort, sequential margin tests on
+//      the shared m8; a failing sub-block is recomputed in 16 bits by its
+//      owner and raises mu_hat;
+//   3. exponentials of the own sub-blocks against mu_hat (8-bit LUT in LDS,
+//      16-bit table in global memory), written in place of the logit codes;
+//      partial row sums -> LDS; lambda_hat, omega_hat;
+//   4. stage 2 (Eq. (8)): per-sub-block costs -> LDS, feasibility of every
+//      candidate recompute set evaluated identically by every wave, 16-bit
+//      recompute of the chosen sub-blocks by their owners;
+//   5. omega, mu update; O^T <- O^T diag(lambda_hat) + V^T E.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "lamp_device.h"
+#include "lamp_kernels.h"
+#include "lamp_loops.h"
+
+#ifndef LAMP_MIN_WAVES
+#define LAMP_MIN_WAVES 2   // minimum waves per SIMD requested from the register allocator
+#endif
+
+namespace lamp {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+enum { PREC_LOW = 0, PREC_S1 = 1, PREC_S2 = 2, PREC_INACTIVE = 3 };
+
+template <int D, int BQ, int BK, int NK>
+struct Cfg {
+    static constexpr int QPL = BQ / 64;                    // query rows per lane
+    static constexpr int KPT = BK * NK;                    // keys per tile
+    static constexpr int NCH = KPT / 16;                   // 16-key chunks per tile
+    static constexpr int NW = NK < D / 32 ? NK : D / 32;   // waves
+    static constexpr int SPW = NK / NW;                    // sub-blocks per wave
+    static constexpr int CPW = D / NW;                     // output channels per wave
+    static constexpr int CT = CPW / 32;                    // 32-channel MFMA tiles per wave
+    static constexpr int QG = BQ / 32;                     // 32-row MFMA groups
+    static constexpr int YP = KPT + 8;                     // LDS pitch (u16) of the code rows
+    static constexpr int VP = KPT + 8;                     // LDS pitch (u16) of V^T
+    static constexpr size_t OFF_Y = 0;
+    static constexpr size_t OFF_V = OFF_Y + (size_t)BQ * YP * 2;
+    static constexpr size_t OFF_LUT = OFF_V + (size_t)D * VP * 2;
+    static constexpr size_t OFF_M8 = OFF_LUT + 512;                       // f32 [NK][BQ]
+    static constexpr size_t OFF_CM = OFF_M8 + (size_t)NK * BQ * 4;       // f32 [NK][BQ]
+    static constexpr size_t OFF_SP = OFF_CM + (size_t)NK * BQ * 4;       // f64 [NW][BQ]
+    static constexpr size_t OFF_CO = OFF_SP + (size_t)NW * BQ * 8;       // f64 [NK][BQ]
+    static constexpr size_t LDS = OFF_CO + (size_t)NK * BQ * 8;
+    static_assert(BQ == 64 || BQ == 128, "64 or 128 query rows per block");
+    static_assert(BK % 16 == 0 && NK <= 4 && NK % NW == 0, "sub-blocks of 16-key chunks, at most 4 per tile");
+    static_assert(CPW % 32 == 0, "whole 32-channel tiles per wave");
+};
+
+template <int D, int BQ, int BK, int NK>
+__global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) void lamp_fwd_kernel(FwdParams p)
+{
+    using C = Cfg<D, BQ, BK, NK>;
+    constexpr int QPL = C::QPL, KPT = C::KPT, NCH = C::NCH, NW = C::NW, SPW = C::SPW, CPW = C::CPW;
+    constexpr int CT = C::CT, QG = C::QG, YP = C::YP, VP = C::VP;
+    constexpr int CPS = BK / 16;   // chunks per sub-block
+
+    extern __shared__ __align__(16) unsigned char smem[];
+    uint16_t *ycode = reinterpret_cast<uint16_t *>(smem + C::OFF_Y);   // [BQ][YP] logit / exp codes
+    uint16_t *vt = reinterpret_cast<uint16_t *>(smem + C::OFF_V);      // [D][VP] V^T of the tile
+    uint16_t *lut = reinterpret_cast<uint16_t *>(smem + C::OFF_LUT);   // [256] 8-bit exp (bf16 bits)
+    float *m8s = reinterpret_cast<float *>(smem + C::OFF_M8);          // [NK][BQ] 8-bit column maxima
+    float *cms = reinterpret_cast<float *>(smem + C::OFF_CM);          // [NK][BQ] 16-bit column maxima
+    double *sps = reinterpret_cast<double *>(smem + C::OFF_SP);        // [NW][BQ] partial row sums
+    double *cst_lds = reinterpret_cast<double *>(smem + C::OFF_CO);    // [NK][BQ] stage-2 costs
+
+    const int tid = threadIdx.x;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;   // w is wave-uniform
+    const int nqb = p.N / BQ;
+    const int BH = p.B * p.Hq;
+    const int qb = nqb - 1 - (int)(blockIdx.x / BH);   // longest blocks first under causality
+    const int bh = blockIdx.x % BH;
+    const int b = bh / p.Hq, h = bh % p.Hq;
+    const int hk = h / (p.Hq / p.Hkv);
+    const int q0 = qb * BQ;
+    const float NEG_INF = -__builtin_inff();
+
+    // per-slot row, query index and visible key range [vlo, vhi]
+    int row[QPL], vlo[QPL], vhi[QPL];
+    const float *qrow[QPL];
+#pragma unroll
+    for (int s = 0; s < QPL; ++s) {
+        row[s] = s * 64 + lane;
+        const int j = q0 + row[s];
+        vlo[s] = p.window > 0 ? (j - p.window + 1 > 0 ? j - p.window + 1 : 0) : 0;
+        vhi[s] = p.causal ? j : p.N - 1;
+        qrow[s] = p.qt + (((size_t)b * p.Hq + h) * p.N + j) * D;
+    }
+    // visible key range of the whole block
+    const int bv_lo = p.window > 0 ? (q0 - p.window + 1 > 0 ? q0 - p.window + 1 : 0) : 0;
+    const int bv_hi = p.causal ? q0 + BQ - 1 : p.N - 1;
+    const int t_begin = bv_lo / KPT, t_end = bv_hi / KPT;
+
+    const float *kt32 = p.kt32 + ((size_t)b * p.Hkv + hk) * (size_t)(p.N / 16) * D * 16;
+    const uint16_t *vbase = p.v + ((size_t)b * p.Hkv + hk) * (size_t)p.N * D;
+    uint8_t *mrow = p.mask + (((size_t)b * p.Hq + h) * nqb + qb) * (size_t)(p.N / BK);
+
+    for (int i = tid; i < 256; i += 64 * NW) lut[i] = p.lut8e[i];
+
+    float mu[QPL];     // running maxima (e4m11 or e4m3 values)
+    double om[QPL];    // running sums omega
+#pragma unroll
+    for (int s = 0; s < QPL; ++s) {
+        mu[s] = NEG_INF;
+        om[s] = 0.0;
+    }
+    floatx16 acc[QG][CT];
+#pragma unroll
+    for (int g = 0; g < QG; ++g)
+#pragma unroll
+        for (int t = 0; t < CT; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[g][t][r] = 0.0f;
+
+    auto visible = [&](int s, int key) { return key >= vlo[s] && key <= vhi[s]; };
+
+    for (int tile = t_begin; tile <= t_end; ++tile) {
+        const int k0 = tile * KPT;
+        __syncthreads();   // readers of vt / ycode / LDS partials of the previous tile are done
+
+        // ---- V^T of the tile into LDS: vt[c][i] = v[k0 + i][c]
+        for (int e = tid; e < (KPT / 2) * (D / 8); e += 64 * NW) {
+            const int i = 2 * (e % (KPT / 2)), c8 = (e / (KPT / 2)) * 8;
+            const u32x4 r0 = *reinterpret_cast<const u32x4 *>(vbase + (size_t)(k0 + i) * D + c8);
+            const u32x4 r1 = *reinterpret_cast<const u32x4 *>(vbase + (size_t)(k0 + i + 1) * D + c8);
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                *reinterpret_cast<uint32_t *>(vt + (c8 + 2 * t) * VP + i) = (r0[t] & 0xFFFFu) | (r1[t] << 16);
+                *reinterpret_cast<uint32_t *>(vt + (c8 + 2 * t + 1) * VP + i) = (r0[t] >> 16) | (r1[t] & 0xFFFF0000u);
+            }
+        }
+
+        // ---- active sub-blocks (a visible pair anywhere in the block), uniform
+        uint32_t active = 0;
+#pragma unroll
+        for (int th = 0; th < NK; ++th) {
+            const int a = k0 + th * BK, z = a + BK - 1;
+            bool any = false;
+#pragma unroll
+            for (int s = 0; s < QPL; ++s) any |= (a <= vhi[s] && z >= vlo[s]);
+            if (wave_any(any)) active |= 1u << th;
+        }
+        if (active == 0) {   // no visible pair in the tile: no state change
+            if (tid == 0)
+                for (int th = 0; th < NK; ++th) mrow[tile * NK + th] = PREC_INACTIVE;
+            continue;
+        }
+
+        // ---- 1. 8-bit logits of the own sub-blocks (unused at threshold 0)
+        if (p.mode != MODE_ALL16) {
+#pragma unroll
+            for (int u = 0; u < SPW; ++u) {
+                const int th = w * SPW + u;
+                float mx[QPL];
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) mx[s] = NEG_INF;
+                if (active >> th & 1u) {
+                    for (int ch = 0; ch < CPS; ++ch) {
+                        const int c16 = th * CPS + ch;
+                        const int ck0 = k0 + c16 * 16;
+                        if (ck0 > bv_hi || ck0 + 15 < bv_lo) continue;   // nothing visible in the block
+                        uint32_t a8[QPL][8];
+                        emu8_chunk<D, QPL>(qrow, kt32 + (size_t)(ck0 / 16) * D * 16, a8);
+#pragma unroll
+                        for (int s = 0; s < QPL; ++s) {
+                            const bool full = ck0 >= vlo[s] && ck0 + 15 <= vhi[s];
+                            uint32_t packed[8];
+#pragma unroll
+                            for (int pp = 0; pp < 8; ++pp) {
+                                const float2 yv = unpk_e4m3(a8[s][pp]);
+                                const int i0 = ck0 + 2 * pp;
+                                if (full || visible(s, i0)) mx[s] = yv.x > mx[s] ? yv.x : mx[s];
+                                if (full || visible(s, i0 + 1)) mx[s] = yv.y > mx[s] ? yv.y : mx[s];
+                                packed[pp] = (a8[s][pp] & 0xFFu) | ((a8[s][pp] & 0xFF00u) << 8);
+                            }
+                            u32x4 *dst = reinterpret_cast<u32x4 *>(ycode + row[s] * YP + c16 * 16);
+                            dst[0] = u32x4{packed[0], packed[1], packed[2], packed[3]};
+                            dst[1] = u32x4{packed[4], packed[5], packed[6], packed[7]};
+                        }
+                    }
+                }
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) m8s[th * BQ + row[s]] = mx[s];
+            }
+        }
+        __syncthreads();   // m8s and vt complete
+
+        // ---- 2. running maximum mu_hat and stage 1
+        float muh[QPL];
+        float m8[NK][QPL];
+#pragma unroll
+        for (int s = 0; s < QPL; ++s) {
+            muh[s] = mu[s];
+#pragma unroll
+            for (int th = 0; th < NK; ++th) m8[th][s] = (p.mode != MODE_ALL16) ? m8s[th * BQ + row[s]] : NEG_INF;
+        }
+        uint32_t prec16 = 0;   // stage-1 (or threshold-0) sub-blocks
+        if (p.mode == MODE_PURE8) {
+#pragma unroll
+            for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                for (int th = 0; th < NK; ++th) muh[s] = m8[th][s] > muh[s] ? m8[th][s] : muh[s];
+        } else if (p.mode == MODE_ALL16) {
+            prec16 = active;
+#pragma unroll
+            for (int u = 0; u < SPW; ++u) {
+                const int th = w * SPW + u;
+                float cm[QPL];
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) cm[s] = NEG_INF;
+                if (active >> th & 1u) {
+                    for (int ch = 0; ch < CPS; ++ch) {
+                        const int c16 = th * CPS + ch;
+                        const int ck0 = k0 + c16 * 16;
+                        if (ck0 > bv_hi || ck0 + 15 < bv_lo) continue;
+                        uint32_t yc[QPL][8];
+                        rec16_chunk<D, QPL>(qrow, kt32 + (size_t)(ck0 / 16) * D * 16, yc);
+#pragma unroll
+                        for (int s = 0; s < QPL; ++s) {
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) {
+                                const float yv = e4m11_value((yc[s][i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
+                                if (visible(s, ck0 + i)) cm[s] = yv > cm[s] ? yv : cm[s];
+                            }
+                            u32x4 *dst = reinterpret_cast<u32x4 *>(ycode + row[s] * YP + c16 * 16);
+                            dst[0] = u32x4{yc[s][0], yc[s][1], yc[s][2], yc[s][3]};
+                            dst[1] = u32x4{yc[s][4], yc[s][5], yc[s][6], yc[s][7]};
+                        }
+                    }
+                }
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) cms[th * BQ + row[s]] = cm[s];
+            }
+            __syncthreads();
+#pragma unroll
+            for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                for (int th = 0; th < NK; ++th) {
+                    const float c = cms[th * BQ + row[s]];
+                    muh[s] = c > muh[s] ? c : muh[s];
+                }
+        } else {
+            // threats T_theta = max_j (m8 - mu_j), exact in fp64 (+inf when mu_j = -inf)
+            double T[NK];
+#pragma unroll
+            for (int th = 0; th < NK; ++th) {
+                double t = -__builtin_inf();
+#pragma unroll
+                for (int s = 0; s < QPL; ++s)
+                    if (m8[th][s] > NEG_INF) {
+                        const double d = (double)m8[th][s] - (double)mu[s];
+                        t = d > t ? d : t;
+                    }
+                T[th] = wave_max_f64(t);
+            }
+            // descending threat, ties by index; order packed 4 bits per rank
+            uint32_t order = 0, taken = 0;
+            int na = 0;
+#pragma unroll
+            for (int r = 0; r < NK; ++r) {
+                int best = -1;
+                double bt = 0.0;
+#pragma unroll
+                for (int th = 0; th < NK; ++th) {
+                    const bool cand = (active >> th & 1u) && !(taken >> th & 1u);
+                    if (cand && (best < 0 || T[th] > bt)) {
+                        best = th;
+                        bt = T[th];
+                    }
+                }
+                if (best >= 0) {
+                    order |= (uint32_t)best << (4 * na);
+                    ++na;
+                    taken |= 1u << best;
+                }
+            }
+            // margin test of every sub-block against the current mu_hat:
+            // mu_hat_j > fma(|mu_hat_j|, delta, m8); columns without a visible
+            // entry are not tested; mu_hat = -inf fails
+            auto fails = [&]() {
+                uint32_t f = 0;
+#pragma unroll
+                for (int th = 0; th < NK; ++th) {
+                    bool bad = false;
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s)
+                        if (m8[th][s] > NEG_INF) {
+                            const double mh = (double)muh[s];
+                            bad |= !(mh > __builtin_fma(__builtin_fabs(mh), p.delta, (double)m8[th][s]));
+                        }
+                    if (wave_any(bad)) f |= 1u << th;
+                }
+                return f;
+            };
+            uint32_t fail = fails();
+            int pos = 0;
+            while (true) {
+                while (pos < na && !(fail >> ((order >> (4 * pos)) & 15u) & 1u)) ++pos;
+                if (pos >= na) break;
+                const int th = (int)((order >> (4 * pos)) & 15u);
+                ++pos;
+                prec16 |= 1u << th;
+                if (th / SPW == w) {   // the owner recomputes the sub-block in 16 bits
+                    float cm[QPL];
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) cm[s] = NEG_INF;
+                    for (int ch = 0; ch < CPS; ++ch) {
+                        const int c16 = th * CPS + ch;
+                        const int ck0 = k0 + c16 * 16;
+                        if (ck0 > bv_hi || ck0 + 15 < bv_lo) continue;
+                        uint32_t yc[QPL][8];
+                        rec16_chunk<D, QPL>(qrow, kt32 + (size_t)(ck0 / 16) * D * 16, yc);
+#pragma unroll
+                        for (int s = 0; s < QPL; ++s) {
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) {
+                                const float yv = e4m11_value((yc[s][i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
+                                if (visible(s, ck0 + i)) cm[s] = yv > cm[s] ? yv : cm[s];
+                            }
+                            u32x4 *dst = reinterpret_cast<u32x4 *>(ycode + row[s] * YP + c16 * 16);
+                            dst[0] = u32x4{yc[s][0], yc[s][1], yc[s][2], yc[s][3]};
+                            dst[1] = u32x4{yc[s][4], yc[s][5], yc[s][6], yc[s][7]};
+                        }
+                    }
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) cms[th * BQ + row[s]] = cm[s];
+                }
+                __syncthreads();
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) {
+                    const float c = cms[th * BQ + row[s]];
+                    muh[s] = c > muh[s] ? c : muh[s];
+                }
+                if (pos < na) fail = fails();
+            }
+        }
+
+        // ---- 3. exponentials of the own sub-blocks against mu_hat
+        {
+            double sp[QPL];
+#pragma unroll
+            for (int s = 0; s < QPL; ++s) sp[s] = 0.0;
+#pragma unroll
+            for (int u = 0; u < SPW; ++u) {
+                const int th = w * SPW + u;
+                if (!(active >> th & 1u)) {
+                    // inactive: zero exponentials so the P.V pass may read them
+                    for (int ch = 0; ch < CPS; ++ch)
+#pragma unroll
+                        for (int s = 0; s < QPL; ++s) {
+                            u32x4 *d = reinterpret_cast<u32x4 *>(ycode + row[s] * YP + (th * CPS + ch) * 16);
+                            d[0] = u32x4{0u, 0u, 0u, 0u};
+                            d[1] = u32x4{0u, 0u, 0u, 0u};
+                        }
+                    continue;
+                }
+                const bool hi16 = prec16 >> th & 1u;
+                for (int ch = 0; ch < CPS; ++ch) {
+                    const int c16 = th * CPS + ch;
+                    const int ck0 = k0 + c16 * 16;
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) {
+                        u32x4 *rp = reinterpret_cast<u32x4 *>(ycode + row[s] * YP + c16 * 16);
+                        if (ck0 > vhi[s] || ck0 + 15 < vlo[s]) {
+                            rp[0] = u32x4{0u, 0u, 0u, 0u};
+                            rp[1] = u32x4{0u, 0u, 0u, 0u};
+                            continue;
+                        }
+                        const u32x4 c0 = rp[0], c1 = rp[1];
+                        const uint32_t in[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
+                        uint32_t outw[8];
+#pragma unroll
+                        for (int pp = 0; pp < 8; ++pp) {
+                            uint32_t res = 0;
+#pragma unroll
+                            for (int t = 0; t < 2; ++t) {
+                                const int key = ck0 + 2 * pp + t;
+                                const uint32_t yc = (in[pp] >> (16 * t)) & 0xFFFFu;
+                                uint32_t ec = 0;
+                                float ev = 0.0f;
+                                if (visible(s, key)) {
+                                    if (hi16) {
+                                        ec = p.exp16[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))];
+                                        ev = ue5m11e_value(ec);
+                                    } else {
+                                        ec = lut[ue5m3_code(shift_of(muh[s], e4m3_value(yc)))];
+                                        ev = bf16_value(ec);
+                                    }
+                                }
+                                sp[s] += (double)ev;   // exact: multiples of 2^-41 below 2^9
+                                res |= ec << (16 * t);
+                            }
+                            outw[pp] = res;
+                        }
+                        rp[0] = u32x4{outw[0], outw[1], outw[2], outw[3]};
+                        rp[1] = u32x4{outw[4], outw[5], outw[6], outw[7]};
+                    }
+                }
+            }
+#pragma unroll
+            for (int s = 0; s < QPL; ++s) sps[w * BQ + row[s]] = sp[s];
+        }
+        __syncthreads();
+
+        // ---- 4. lambda_hat, omega_hat, stage 2
+        double S[QPL], lam[QPL], omh[QPL];
+#pragma unroll
+        for (int s = 0; s < QPL; ++s) {
+            double t = 0.0;
+#pragma unroll
+            for (int ww = 0; ww < NW; ++ww) t += sps[ww * BQ + row[s]];
+            S[s] = t;
+            if (muh[s] == NEG_INF) lam[s] = 1.0;
+            else if (mu[s] == NEG_INF) lam[s] = 0.0;
+            else lam[s] = exp_doc((double)mu[s] - (double)muh[s]);
+            omh[s] = __builtin_fma(lam[s], om[s], t);
+        }
+        uint32_t prec2 = 0;
+        if (p.mode == MODE_LAMP) {
+            const uint32_t F = active & ~prec16;
+            if (F) {
+                // costs c_theta,j = sum_{i in theta, ascending} E (omega_hat - E)
+#pragma unroll
+                for (int u = 0; u < SPW; ++u) {
+                    const int th = w * SPW + u;
+                    if (!(F >> th & 1u)) continue;
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) {
+                        double cth = 0.0;
+                        for (int ch = 0; ch < CPS; ++ch) {
+                            const int c16 = th * CPS + ch;
+                            const u32x4 *rp = reinterpret_cast<const u32x4 *>(ycode + row[s] * YP + c16 * 16);
+                            const u32x4 c0 = rp[0], c1 = rp[1];
+                            const uint32_t in[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) {
+                                const double e = (double)bf16_value((in[i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
+                                const double tt = omh[s] - e;
+                                const double pr = e * tt;
+                                cth = cth + pr;   // invisible entries hold E = 0 and add +0
+                            }
+                        }
+                        cst_lds[th * BQ + row[s]] = cth;
+                    }
+                }
+                __syncthreads();
+                // feasibility of every recompute set R within F, identical in every wave
+                double cst[NK][QPL], lim[QPL];
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) {
+                    lim[s] = (p.tau * omh[s]) * omh[s];
+#pragma unroll
+                    for (int th = 0; th < NK; ++th) cst[th][s] = (F >> th & 1u) ? cst_lds[th * BQ + row[s]] : 0.0;
+                }
+                uint32_t feas = 0;
+                for (int R = 0; R < (1 << NK); ++R) {
+                    if (R & ~(int)F) continue;
+                    bool bad = false;
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) {
+                        double xi = 0.0;
+#pragma unroll
+                        for (int th = 0; th < NK; ++th)
+                            if ((F >> th & 1u) && !(R >> th & 1)) xi = xi + cst[th][s];
+                        bad |= !(xi <= lim[s]);
+                    }
+                    if (!wave_any(bad)) feas |= 1u << R;
+                }
+                // smallest recompute set first, then ascending bitmask
+                int chosen = (int)F;
+                bool found = false;
+                for (int sz = 0; sz <= NK && !found; ++sz)
+                    for (int R = 0; R < (1 << NK) && !found; ++R) {
+                        if ((R & ~(int)F) || __builtin_popcount(R) != sz) continue;
+                        if (feas >> R & 1u) {
+                            chosen = R;
+                            found = true;
+                        }
+                    }
+                prec2 = (uint32_t)chosen;
+                if (prec2) {
+                    // stage-2 recompute by the owners: 16-bit logits and
+                    // exponentials against the unchanged mu_hat
+                    double ds[QPL];
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) ds[s] = 0.0;
+#pragma unroll
+                    for (int u = 0; u < SPW; ++u) {
+                        const int th = w * SPW + u;
+                        if (!(prec2 >> th & 1u)) continue;
+                        for (int ch = 0; ch < CPS; ++ch) {
+                            const int c16 = th * CPS + ch;
+                            const int ck0 = k0 + c16 * 16;
+                            if (ck0 > bv_hi || ck0 + 15 < bv_lo) continue;
+                            uint32_t yc[QPL][8];
+                            rec16_chunk<D, QPL>(qrow, kt32 + (size_t)(ck0 / 16) * D * 16, yc);
+#pragma unroll
+                            for (int s = 0; s < QPL; ++s) {
+                                u32x4 *rp = reinterpret_cast<u32x4 *>(ycode + row[s] * YP + c16 * 16);
+                                const u32x4 c0 = rp[0], c1 = rp[1];
+                                const uint32_t in[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
+                                uint32_t outw[8];
+#pragma unroll
+                                for (int pp = 0; pp < 8; ++pp) {
+                                    uint32_t res = 0;
+#pragma unroll
+                                    for (int t = 0; t < 2; ++t) {
+                                        const int key = ck0 + 2 * pp + t;
+                                        uint32_t ec = 0;
+                                        if (visible(s, key)) {
+                                            const float old = bf16_value((in[pp] >> (16 * t)) & 0xFFFFu);
+                                            const float y = e4m11_value((yc[s][pp] >> (16 * t)) & 0xFFFFu);
+                                            ec = p.exp16[ue5m11_code(shift_of(muh[s], y))];
+                                            ds[s] = ds[s] - (double)old;
+                                            ds[s] = ds[s] + (double)ue5m11e_value(ec);
+                                        }
+                                        res |= ec << (16 * t);
+                                    }
+                                    outw[pp] = res;
+                                }
+                                rp[0] = u32x4{outw[0], outw[1], outw[2], outw[3]};
+                                rp[1] = u32x4{outw[4], outw[5], outw[6], outw[7]};
+                            }
+                        }
+                    }
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) sps[w * BQ + row[s]] = ds[s];
+                    __syncthreads();
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) {
+                        double t = S[s];
+#pragma unroll
+                        for (int ww = 0; ww < NW; ++ww) t += sps[ww * BQ + row[s]];   // exact
+                        S[s] = t;
+                    }
+                }
+            }
+        }
+
+        // ---- 5. state update; O^T <- O^T diag(lambda_hat) + V^T E
+#pragma unroll
+        for (int s = 0; s < QPL; ++s) {
+            om[s] = __builtin_fma(lam[s], om[s], S[s]);
+            mu[s] = muh[s];
+        }
+        if (tid == 0)
+#pragma unroll
+            for (int th = 0; th < NK; ++th)
+                mrow[tile * NK + th] = !(active >> th & 1u) ? PREC_INACTIVE
+                                     : (prec16 >> th & 1u) ? PREC_S1
+                                     : (prec2 >> th & 1u) ? PREC_S2 : PREC_LOW;
+        const uint32_t p16 = prec16 | prec2;
+        const int half = lane >> 5, l32 = lane & 31;
+        {
+            // lambda_hat of row 32g + l32 lives in lane (32g + l32) % 64, slot (32g + l32) / 64
+            float lamf[QPL];
+            bool scale = false;
+#pragma unroll
+            for (int s = 0; s < QPL; ++s) {
+                lamf[s] = (float)lam[s];
+                scale |= lamf[s] != 1.0f;
+            }
+            if (wave_any(scale)) {
+#pragma unroll
+                for (int g = 0; g < QG; ++g) {
+                    const float lg = __shfl(lamf[g / 2 < QPL ? g / 2 : 0], ((g & 1) << 5) + l32, 64);
+#pragma unroll
+                    for (int t = 0; t < CT; ++t)
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) acc[g][t][r] *= lg;
+                }
+            }
+        }
+        for (int c16 = 0; c16 < NCH; ++c16) {
+            const int ck0 = k0 + c16 * 16;
+            const int th = c16 / CPS;
+            if (!(active >> th & 1u) || ck0 > bv_hi || ck0 + 15 < bv_lo) continue;
+            const bool hi16 = p16 >> th & 1u;
+            u32x4 av[CT];
+#pragma unroll
+            for (int t = 0; t < CT; ++t)
+                av[t] = *reinterpret_cast<const u32x4 *>(vt + (w * CPW + t * 32 + l32) * VP + c16 * 16 + half * 8);
+#pragma unroll
+            for (int g = 0; g < QG; ++g) {
+                const u32x4 e = *reinterpret_cast<const u32x4 *>(ycode + (g * 32 + l32) * YP + c16 * 16 + half * 8);
+                if (!hi16) {
+                    const bf16x8 bb = __builtin_bit_cast(bf16x8, e);
+#pragma unroll
+                    for (int t = 0; t < CT; ++t)
+                        acc[g][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av[t]), bb,
+                                                                            acc[g][t], 0, 0, 0);
+                } else {
+                    u32x4 hw, lw;
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        const float e0 = ue5m11e_value(e[t] & 0xFFFFu), e1 = ue5m11e_value(e[t] >> 16);
+                        const uint32_t h0 = bf16_bits(e0), h1 = bf16_bits(e1);
+                        hw[t] = h0 | (h1 << 16);
+                        lw[t] = bf16_bits(e0 - bf16_value(h0)) | (bf16_bits(e1 - bf16_value(h1)) << 16);
+                    }
+                    const bf16x8 bh = __builtin_bit_cast(bf16x8, hw), bl = __builtin_bit_cast(bf16x8, lw);
+#pragma unroll
+                    for (int t = 0; t < CT; ++t) {
+                        const bf16x8 a = __builtin_bit_cast(bf16x8, av[t]);
+                        acc[g][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bh, acc[g][t], 0, 0, 0);
+                        acc[g][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bl, acc[g][t], 0, 0, 0);
+                    }
+                }
+            }
+        }
+    }
+
+    // ---- epilogue: O / omega, lse = mu + ln(omega), mask bytes of skipped tiles
+    {
+        const int half = lane >> 5, l32 = lane & 31;
+#pragma unroll
+        for (int g = 0; g < QG; ++g) {
+            const double og = __shfl(om[g / 2 < QPL ? g / 2 : 0], ((g & 1) << 5) + l32, 64);
+            const float inv = (float)(1.0 / og);
+            const int jq = q0 + g * 32 + l32;
+            float *orow = p.o + (((size_t)b * p.Hq + h) * p.N + jq) * D + w * CPW;
+#pragma unroll
+            for (int t = 0; t < CT; ++t)
+#pragma unroll
+                for (int r4 = 0; r4 < 4; ++r4) {
+                    const int c = t * 32 + r4 * 8 + half * 4;
+                    const float4 v4 = make_float4(acc[g][t][r4 * 4 + 0] * inv, acc[g][t][r4 * 4 + 1] * inv,
+                                                  acc[g][t][r4 * 4 + 2] * inv, acc[g][t][r4 * 4 + 3] * inv);
+                    *reinterpret_cast<float4 *>(orow + c) = v4;
+                }
+        }
+        if (w == 0)
+#pragma unroll
+            for (int s = 0; s < QPL; ++s)
+                p.lse[((size_t)b * p.Hq + h) * p.N + q0 + row[s]] = (float)((double)mu[s] + ::log(om[s]));
+        const int ntiles = p.N / KPT;
+        for (int t = tid; t < ntiles; t += 64 * NW)
+            if (t < t_begin || t > t_end)
+                for (int th = 0; th < NK; ++th) mrow[t * NK + th] = PREC_INACTIVE;
+    }
+}
+
+// ------------------------------------------------------------------ launcher
+template <int D, int BQ, int BK, int NK>
+static hipError_t launch_fwd(const FwdParams &p, hipStream_t s)
+{
+    using C = Cfg<D, BQ, BK, NK>;
+    auto kern = lamp_fwd_kernel<D, BQ, BK, NK>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
+    if (e != hipSuccess) return e;
+    dim3 grid((unsigned)(p.B * p.Hq * (p.N / BQ)));
+    hipLaunchKernelGGL(kern, grid, dim3(64 * C::NW), C::LDS, s, p);
+    return hipGetLastError();
+}
+
+#define LAMP_FWD_CASE(D_, BQ_, BK_, NK_) \
+    if (D == D_ && BQ == BQ_ && BK == BK_ && NK == NK_) return launch_fwd<D_, BQ_, BK_, NK_>(p, s);
+
+hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found)
+{
+    *found = true;
+    // configurations built: d in {64,128,256}, bq in {64,128}, (bk, nk) in {(16,4), (64,4)}
+#define LAMP_FWD_D(D_)                                                           \
+    LAMP_FWD_CASE(D_, 64, 16, 4) LAMP_FWD_CASE(D_, 128, 16, 4)                     \
+    LAMP_FWD_CASE(D_, 64, 64, 4) LAMP_FWD_CASE(D_, 128, 64, 4)
+    LAMP_FWD_D(64)
+    LAMP_FWD_D(128)
+    LAMP_FWD_D(256)
+#undef LAMP_FWD_D
+    *found = false;
+    return hipSuccess;
+}
+
+} // namespace lamp

@@ -95,7 +95,6 @@ float scale_of(int d)
 struct Workspace {
     float *qt;
     float *kt32;
-    double *kt64;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -105,8 +104,8 @@ int workspace_locked(int dev, int B, int Hq, int Hkv, int N, int d, Workspace *w
 {
     DeviceState *st = state_of(dev);
     size_t nq = (size_t)B * Hq * N * d, nk = (size_t)B * Hkv * N * d;
-    size_t bq = align256(nq * 4), bk32 = align256(nk * 4), bk64 = align256(nk * 8);
-    size_t need = bq + bk32 + bk64;
+    size_t bq = align256(nq * 4), bk32 = align256(nk * 4);
+    size_t need = bq + bk32;
     if (need > st->ws_bytes) {
         if (st->ws) {
             HIP_TRY(hipDeviceSynchronize());
@@ -120,7 +119,6 @@ int workspace_locked(int dev, int B, int Hq, int Hkv, int N, int d, Workspace *w
     char *base = static_cast<char *>(st->ws);
     w->qt = reinterpret_cast<float *>(base);
     w->kt32 = reinterpret_cast<float *>(base + bq);
-    w->kt64 = reinterpret_cast<double *>(base + bq + bk32);
     return LAMP_OK;
 }
 
@@ -217,7 +215,6 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
     }
     p.qt = w.qt;
     p.kt32 = w.kt32;
-    p.kt64 = w.kt64;
     p.v = v;
     p.o = o;
     p.lse = lse;
@@ -231,7 +228,7 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
     p.delta = delta;
     p.tau = tau;
     p.mode = std::isinf(tau) ? lamp::MODE_PURE8 : (tau == 0.0 ? lamp::MODE_ALL16 : lamp::MODE_LAMP);
-    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, w.kt64, B, Hq, Hkv, N, d, scale_of(d), s));
+    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, d, scale_of(d), s));
     bool found = false;
     HIP_TRY(lamp::dispatch_fwd(d, bq, bk, nk, p, s, &found));
     if (!found)
@@ -260,7 +257,6 @@ static int logits_common(const uint16_t *q, const uint16_t *k, int B, int Hq, in
     *p = lamp::LogitsParams{};
     p->qt = w->qt;
     p->kt32 = w->kt32;
-    p->kt64 = w->kt64;
     p->B = B;
     p->Hq = Hq;
     p->Hkv = Hkv;
@@ -281,7 +277,7 @@ int lamp_attn_logits8(const uint16_t *q, const uint16_t *k, int B, int Hq, int H
     if (rc) return rc;
     p.y8 = y8;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, w.kt64, B, Hq, Hkv, N, d, scale_of(d), s));
+    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, d, scale_of(d), s));
     HIP_TRY(lamp::launch_logits8(p, d, s));
     return LAMP_OK;
 }
@@ -295,7 +291,7 @@ int lamp_attn_logits16(const uint16_t *q, const uint16_t *k, int B, int Hq, int 
     if (rc) return rc;
     p.y16 = y16;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, w.kt64, B, Hq, Hkv, N, d, scale_of(d), s));
+    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, d, scale_of(d), s));
     HIP_TRY(lamp::launch_logits16(p, d, s));
     return LAMP_OK;
 }

@@ -11,7 +11,6 @@ enum { MODE_LAMP = 0, MODE_PURE8 = 1, MODE_ALL16 = 2 };
 struct FwdParams {
     const float *qt;          // [B][Hq][N][D] pre-scaled queries, fp32
     const float *kt32;        // [B][Hkv][N/16][D][16] keys, fp32
-    const double *kt64;       // same layout, fp64
     const uint16_t *v;        // [B][Hkv][N][D] bf16
     const uint16_t *exp16;    // ue5m11 shift code -> ue5m11 exp code
     const uint16_t *lut8e;    // ue5m3 shift code -> bf16 bits of the ue5m3 exp
@@ -26,14 +25,13 @@ struct FwdParams {
 struct LogitsParams {
     const float *qt;
     const float *kt32;
-    const double *kt64;
     uint8_t *y8;
     uint16_t *y16;
     int B, Hq, Hkv, N, causal, window, row0, nrows;
 };
 
 hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found);
-hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float *kt32, double *kt64,
+hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float *kt32,
                           int B, int Hq, int Hkv, int N, int D, float scale, hipStream_t s);
 hipError_t launch_logits8(const LogitsParams &p, int D, hipStream_t s);
 hipError_t launch_logits16(const LogitsParams &p, int D, hipStream_t s);
