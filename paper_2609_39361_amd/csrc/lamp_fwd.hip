@@ -52,6 +52,7 @@ struct Cfg {
     static constexpr int CPW = D / NW;                     // output channels per wave
     static constexpr int CT = CPW / 32;                    // 32-channel MFMA tiles per wave
     static constexpr int QG = BQ / 32;                     // 32-row MFMA groups
+    static constexpr int KPW = BK / NW;                    // keys per wave in a shared 16-bit recompute
     static constexpr int YP = KPT + 8;                     // LDS pitch (u16) of the code rows
     static constexpr int VP = KPT + 8;                     // LDS pitch (u16) of V^T
     static constexpr size_t OFF_Y = 0;
@@ -65,6 +66,7 @@ struct Cfg {
     static_assert(BQ == 64 || BQ == 128, "64 or 128 query rows per block");
     static_assert(BK % 16 == 0 && NK <= 4 && NK % NW == 0, "sub-blocks of 16-key chunks, at most 4 per tile");
     static_assert(CPW % 32 == 0, "whole 32-channel tiles per wave");
+    static_assert(KPW == 4 || KPW == 8 || KPW % 16 == 0, "recompute split in 4, 8 or multiples of 16 keys");
 };
 
 template <int D, int BQ, int BK, int NK>
@@ -72,7 +74,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
 {
     using C = Cfg<D, BQ, BK, NK>;
     constexpr int QPL = C::QPL, KPT = C::KPT, NCH = C::NCH, NW = C::NW, SPW = C::SPW, CPW = C::CPW;
-    constexpr int CT = C::CT, QG = C::QG, YP = C::YP, VP = C::VP;
+    constexpr int CT = C::CT, QG = C::QG, YP = C::YP, VP = C::VP, KPW = C::KPW;
     constexpr int CPS = BK / 16;   // chunks per sub-block
 
     extern __shared__ __align__(16) unsigned char smem[];
@@ -111,7 +113,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
     const int bv_hi = p.causal ? q0 + BQ - 1 : p.N - 1;
     const int t_begin = bv_lo / KPT, t_end = bv_hi / KPT;
 
-    const float *kt32 = p.kt32 + ((size_t)b * p.Hkv + hk) * (size_t)(p.N / 16) * D * 16;
+    const float *kt32 = p.kt32 + ((size_t)b * p.Hkv + hk) * (size_t)p.N * D;   // fp32 keys [N][D]
     const uint16_t *vbase = p.v + ((size_t)b * p.Hkv + hk) * (size_t)p.N * D;
     uint8_t *mrow = p.mask + (((size_t)b * p.Hq + h) * nqb + qb) * (size_t)(p.N / BK);
 
@@ -133,6 +135,36 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
             for (int r = 0; r < 16; ++r) acc[g][t][r] = 0.0f;
 
     auto visible = [&](int s, int key) { return key >= vlo[s] && key <= vhi[s]; };
+
+    // 16-bit recompute of sub-block th shared by all waves: wave w takes keys
+    // [key0, key0 + KPW) with key0 = k0 + th*BK + w*KPW.  For every 16-key
+    // group (or the 4 / 8 keys) fn(key, nk, codes) receives the e4m11 codes.
+    auto shared16 = [&](int k0, int th, auto fn) {
+        const int key0 = k0 + th * BK + w * KPW;
+        if (key0 > bv_hi || key0 + KPW - 1 < bv_lo) return;   // nothing visible in the block
+        if constexpr (KPW >= 16) {
+            for (int ch = 0; ch < KPW / 16; ++ch) {
+                const int kc = key0 + ch * 16;
+                uint32_t yc[QPL][8];
+                rec16_keys<D, QPL, 16>(qrow, kt32 + (size_t)kc * D, yc);
+                fn(kc, yc);
+            }
+        } else {
+            uint32_t yc[QPL][KPW / 2];
+            rec16_keys<D, QPL, KPW>(qrow, kt32 + (size_t)key0 * D, yc);
+            fn(key0, yc);
+        }
+    };
+    // write n = 4, 8 or 16 u16 codes (packed two per word) at row r, key offset ko
+    auto put_codes = [&](int r, int ko, const uint32_t *cw, int nw) {
+        uint16_t *dst = ycode + r * YP + ko;
+        if (nw == 2) {
+            *reinterpret_cast<uint2 *>(dst) = make_uint2(cw[0], cw[1]);
+        } else {
+            for (int t = 0; t < nw; t += 4)
+                *reinterpret_cast<u32x4 *>(dst + 2 * t) = u32x4{cw[t], cw[t + 1], cw[t + 2], cw[t + 3]};
+        }
+    };
 
     for (int tile = t_begin; tile <= t_end; ++tile) {
         const int k0 = tile * KPT;
@@ -180,7 +212,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                         const int ck0 = k0 + c16 * 16;
                         if (ck0 > bv_hi || ck0 + 15 < bv_lo) continue;   // nothing visible in the block
                         uint32_t a8[QPL][8];
-                        emu8_chunk<D, QPL>(qrow, kt32 + (size_t)(ck0 / 16) * D * 16, a8);
+                        emu8_chunk<D, QPL>(qrow, kt32 + (size_t)ck0 * D, a8);
 #pragma unroll
                         for (int s = 0; s < QPL; ++s) {
                             const bool full = ck0 >= vlo[s] && ck0 + 15 <= vhi[s];
@@ -234,7 +266,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                         const int ck0 = k0 + c16 * 16;
                         if (ck0 > bv_hi || ck0 + 15 < bv_lo) continue;
                         uint32_t yc[QPL][8];
-                        rec16_chunk<D, QPL>(qrow, kt32 + (size_t)(ck0 / 16) * D * 16, yc);
+                        rec16_chunk<D, QPL>(qrow, kt32 + (size_t)ck0 * D, yc);
 #pragma unroll
                         for (int s = 0; s < QPL; ++s) {
 #pragma unroll
@@ -320,36 +352,33 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                 const int th = (int)((order >> (4 * pos)) & 15u);
                 ++pos;
                 prec16 |= 1u << th;
-                if (th / SPW == w) {   // the owner recomputes the sub-block in 16 bits
+                {   // all waves recompute the sub-block in 16 bits, KPW keys each
                     float cm[QPL];
 #pragma unroll
                     for (int s = 0; s < QPL; ++s) cm[s] = NEG_INF;
-                    for (int ch = 0; ch < CPS; ++ch) {
-                        const int c16 = th * CPS + ch;
-                        const int ck0 = k0 + c16 * 16;
-                        if (ck0 > bv_hi || ck0 + 15 < bv_lo) continue;
-                        uint32_t yc[QPL][8];
-                        rec16_chunk<D, QPL>(qrow, kt32 + (size_t)(ck0 / 16) * D * 16, yc);
+                    shared16(k0, th, [&](int kc, const auto &yc) {
+                        constexpr int NWD = sizeof(yc[0]) / sizeof(uint32_t);   // words per slot
 #pragma unroll
                         for (int s = 0; s < QPL; ++s) {
 #pragma unroll
-                            for (int i = 0; i < 16; ++i) {
+                            for (int i = 0; i < 2 * NWD; ++i) {
                                 const float yv = e4m11_value((yc[s][i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
-                                if (visible(s, ck0 + i)) cm[s] = yv > cm[s] ? yv : cm[s];
+                                if (visible(s, kc + i)) cm[s] = yv > cm[s] ? yv : cm[s];
                             }
-                            u32x4 *dst = reinterpret_cast<u32x4 *>(ycode + row[s] * YP + c16 * 16);
-                            dst[0] = u32x4{yc[s][0], yc[s][1], yc[s][2], yc[s][3]};
-                            dst[1] = u32x4{yc[s][4], yc[s][5], yc[s][6], yc[s][7]};
+                            put_codes(row[s], kc - k0, yc[s], NWD);
                         }
-                    }
+                    });
 #pragma unroll
-                    for (int s = 0; s < QPL; ++s) cms[th * BQ + row[s]] = cm[s];
+                    for (int s = 0; s < QPL; ++s) cms[w * BQ + row[s]] = cm[s];
                 }
                 __syncthreads();
 #pragma unroll
                 for (int s = 0; s < QPL; ++s) {
-                    const float c = cms[th * BQ + row[s]];
-                    muh[s] = c > muh[s] ? c : muh[s];
+#pragma unroll
+                    for (int ww = 0; ww < NW; ++ww) {
+                        const float c = cms[ww * BQ + row[s]];
+                        muh[s] = c > muh[s] ? c : muh[s];
+                    }
                 }
                 if (pos < na) fail = fails();
             }
@@ -499,36 +528,28 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                     }
                 prec2 = (uint32_t)chosen;
                 if (prec2) {
-                    // stage-2 recompute by the owners: 16-bit logits and
+                    // stage-2 recompute shared by all waves: 16-bit logits and
                     // exponentials against the unchanged mu_hat
                     double ds[QPL];
 #pragma unroll
                     for (int s = 0; s < QPL; ++s) ds[s] = 0.0;
-#pragma unroll
-                    for (int u = 0; u < SPW; ++u) {
-                        const int th = w * SPW + u;
+                    for (int th = 0; th < NK; ++th) {
                         if (!(prec2 >> th & 1u)) continue;
-                        for (int ch = 0; ch < CPS; ++ch) {
-                            const int c16 = th * CPS + ch;
-                            const int ck0 = k0 + c16 * 16;
-                            if (ck0 > bv_hi || ck0 + 15 < bv_lo) continue;
-                            uint32_t yc[QPL][8];
-                            rec16_chunk<D, QPL>(qrow, kt32 + (size_t)(ck0 / 16) * D * 16, yc);
+                        shared16(k0, th, [&](int kc, const auto &yc) {
+                            constexpr int NWD = sizeof(yc[0]) / sizeof(uint32_t);
 #pragma unroll
                             for (int s = 0; s < QPL; ++s) {
-                                u32x4 *rp = reinterpret_cast<u32x4 *>(ycode + row[s] * YP + c16 * 16);
-                                const u32x4 c0 = rp[0], c1 = rp[1];
-                                const uint32_t in[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
-                                uint32_t outw[8];
+                                const uint16_t *src = ycode + row[s] * YP + (kc - k0);
+                                uint32_t outw[NWD];
 #pragma unroll
-                                for (int pp = 0; pp < 8; ++pp) {
+                                for (int pp = 0; pp < NWD; ++pp) {
                                     uint32_t res = 0;
 #pragma unroll
                                     for (int t = 0; t < 2; ++t) {
-                                        const int key = ck0 + 2 * pp + t;
+                                        const int key = kc + 2 * pp + t;
                                         uint32_t ec = 0;
                                         if (visible(s, key)) {
-                                            const float old = bf16_value((in[pp] >> (16 * t)) & 0xFFFFu);
+                                            const float old = bf16_value(src[2 * pp + t]);
                                             const float y = e4m11_value((yc[s][pp] >> (16 * t)) & 0xFFFFu);
                                             ec = p.exp16[ue5m11_code(shift_of(muh[s], y))];
                                             ds[s] = ds[s] - (double)old;
@@ -538,10 +559,9 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                                     }
                                     outw[pp] = res;
                                 }
-                                rp[0] = u32x4{outw[0], outw[1], outw[2], outw[3]};
-                                rp[1] = u32x4{outw[4], outw[5], outw[6], outw[7]};
+                                put_codes(row[s], kc - k0, outw, NWD);
                             }
-                        }
+                        });
                     }
 #pragma unroll
                     for (int s = 0; s < QPL; ++s) sps[w * BQ + row[s]] = ds[s];

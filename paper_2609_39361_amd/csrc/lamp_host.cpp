@@ -99,7 +99,7 @@ struct Workspace {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Grow-only workspace for the pre-scaled Q and the regrouped K (lock held).
+// Grow-only workspace for the pre-scaled Q and the fp32 K (lock held).
 int workspace_locked(int dev, int B, int Hq, int Hkv, int N, int d, Workspace *w)
 {
     DeviceState *st = state_of(dev);

@@ -10,7 +10,7 @@ enum { MODE_LAMP = 0, MODE_PURE8 = 1, MODE_ALL16 = 2 };
 
 struct FwdParams {
     const float *qt;          // [B][Hq][N][D] pre-scaled queries, fp32
-    const float *kt32;        // [B][Hkv][N/16][D][16] keys, fp32
+    const float *kt32;        // [B][Hkv][N][D] keys, fp32
     const uint16_t *v;        // [B][Hkv][N][D] bf16
     const uint16_t *exp16;    // ue5m11 shift code -> ue5m11 exp code
     const uint16_t *lut8e;    // ue5m3 shift code -> bf16 bits of the ue5m3 exp

@@ -1,5 +1,5 @@
 // lamp_kernels.hip -- auxiliary HIP kernels of liblamp.so for gfx950: the
-// prepass (pre-scaled Q, K regrouped for scalar loads), the exponential
+// prepass (pre-scaled Q, K in fp32), the exponential
 // tables, the stand-alone logit kernels and the self tests.  The forward
 // kernel is in lamp_fwd.hip, the logit loops in lamp_loops.h.
 #include <hip/hip_runtime.h>
@@ -24,18 +24,12 @@ __global__ void prescale_q_kernel(const uint16_t *__restrict__ q, float *__restr
     for (; i < n; i += stride) qt[i] = bf16_value(q[i]) * s;
 }
 
-// K regrouped per 16 keys, channel-major: kt[B][Hkv][N/16][D][16], fp32, so
-// that one scalar load brings 16 keys of one channel.
-__global__ void regroup_k_kernel(const uint16_t *__restrict__ k, float *__restrict__ kt32, int D, size_t n)
+// K in fp32, same layout [B][Hkv][N][D] (bf16 -> fp32 is exact).
+__global__ void convert_k_kernel(const uint16_t *__restrict__ k, float *__restrict__ k32, size_t n)
 {
-    size_t o = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     size_t stride = (size_t)gridDim.x * blockDim.x;
-    for (; o < n; o += stride) {
-        size_t kk = o & 15;
-        size_t c = (o >> 4) % (size_t)D;
-        size_t grp = (o >> 4) / (size_t)D;       // (b*Hkv + h) * N/16 + key group
-        kt32[o] = bf16_value(k[(grp * 16 + kk) * (size_t)D + c]);
-    }
+    for (; i < n; i += stride) k32[i] = bf16_value(k[i]);
 }
 
 // ------------------------------------------------------------------ tables
@@ -107,7 +101,7 @@ __global__ __launch_bounds__(64) void logits8_kernel(LogitsParams p)
     const float *qrow[1] = {p.qt + (((size_t)b * p.Hq + h) * p.N + j) * D};
     for (int g = 0; g < NC; ++g) {
         const int key0 = (blockIdx.y * NC + g) * 16;
-        const float *kt = p.kt32 + (((size_t)b * p.Hkv + hk) * (p.N / 16) + key0 / 16) * (size_t)D * 16;
+        const float *kt = p.kt32 + (((size_t)b * p.Hkv + hk) * p.N + key0) * (size_t)D;
         uint32_t acc[1][8];
         emu8_chunk<D, 1>(qrow, kt, acc);
         if (r < p.nrows) {
@@ -138,7 +132,7 @@ __global__ __launch_bounds__(64) void logits16_kernel(LogitsParams p)
     const int j = p.row0 + rr;
     const int key0 = blockIdx.y * 16;
     const float *qrow[1] = {p.qt + (((size_t)b * p.Hq + h) * p.N + j) * D};
-    const float *kt = p.kt32 + (((size_t)b * p.Hkv + hk) * (p.N / 16) + key0 / 16) * (size_t)D * 16;
+    const float *kt = p.kt32 + (((size_t)b * p.Hkv + hk) * p.N + key0) * (size_t)D;
     uint32_t codes[1][8];
     rec16_chunk<D, 1>(qrow, kt, codes);
     if (r >= p.nrows) return;
@@ -185,7 +179,7 @@ hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float
     unsigned gq = (unsigned)((nq + 255) / 256 < 65536 ? (nq + 255) / 256 : 65536);
     unsigned gk = (unsigned)((nk + 255) / 256 < 65536 ? (nk + 255) / 256 : 65536);
     hipLaunchKernelGGL(prescale_q_kernel, dim3(gq), dim3(256), 0, s, q, qt, scale, nq);
-    hipLaunchKernelGGL(regroup_k_kernel, dim3(gk), dim3(256), 0, s, k, kt32, D, nk);
+    hipLaunchKernelGGL(convert_k_kernel, dim3(gk), dim3(256), 0, s, k, kt32, nk);
     return hipGetLastError();
 }
 

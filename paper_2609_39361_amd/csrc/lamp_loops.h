@@ -1,178 +1,173 @@
 // lamp_loops.h -- the two logit loops of the LampAttention forward pass.
 //
-// Both loops give each lane QPL query rows and run over the D channels of a
-// 16-key chunk.  The key value of (key, channel) is the same for every lane of
-// a wave, so it is read with scalar loads into scalar registers and used as
-// the scalar operand of the FMAs.  Scalar loads complete out of order and can
-// only be waited for all at once, so they are issued in batches of two
-// channels (32 values): wait for every load, issue the next batch, then run
-// the arithmetic of the current batch while the next one is in flight.
+// Both loops give each lane QPL query rows and accumulate over the D channels
+// of a group of NKEY <= 16 keys.  Lane l of every 16-lane row of the wave
+// holds the key value of key (l mod NKEY) for the current channel; the FMA
+// reads it through a DPP row broadcast (row_newbcast:i hands lane i of each
+// row to all 16 lanes of that row), so every lane multiplies its own query
+// value by the value of key i without scalar registers or LDS.  Keys and
+// queries are fp32 and arrive with ordinary vector loads one 4-channel group
+// ahead of their use.  A DPP read of a VGPR written by a VALU instruction less
+// than two instructions earlier is a hardware hazard; the key registers are
+// only written by loads, and the build scans the generated code for the
+// pattern (see build.py).
 #pragma once
+#include <utility>
+
 #include "lamp_device.h"
 
 namespace lamp {
 
-// Every outstanding scalar/LDS load has completed; the scheduler may not move
-// instructions across this point.
-__device__ __forceinline__ void smem_fence()
+// acc + bcast_i(kv) * q with one rounding (v_fmac_f32 is a fused multiply-add).
+template <int I>
+__device__ __forceinline__ float fmac_bc(float acc, float kv, float q)
 {
-    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0); vmcnt, expcnt unchanged
-    __builtin_amdgcn_sched_barrier(0);
+    asm("v_fmac_f32_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf" : "+v"(acc) : "v"(kv), "v"(q), "n"(I));
+    return acc;
 }
 
-__device__ __forceinline__ void kload2(float (&a)[16], float (&b)[16], kptr32_t kt, int c, int D)
+// Loads of a 4-channel group: this lane's key row and query rows.
+template <int QPL>
+__device__ __forceinline__ void load_group(const float *krow, const float *const (&qrow)[QPL], int c, float4 &k4,
+                                           float4 (&q4)[QPL])
 {
-    const int c1 = c + 1 < D ? c + 1 : D - 1;   // past the end: a harmless repeat
-    const int c0 = c < D ? c : D - 1;
-    kptr32_t p0 = kt + (size_t)c0 * 16, p1 = kt + (size_t)c1 * 16;
+    k4 = *reinterpret_cast<const float4 *>(krow + c);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) a[i] = p0[i];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) b[i] = p1[i];
+    for (int s = 0; s < QPL; ++s) q4[s] = *reinterpret_cast<const float4 *>(qrow[s] + c);
 }
 
-// One channel of the 8-bit accumulation: acc <- RN_e4m3(RN32(q * k + acc)).
-template <int QPL, bool SAT>
-__device__ __forceinline__ void emu8_step(const float (&kv)[16], const float (&q)[QPL], uint32_t (&acc)[QPL][8])
+__device__ __forceinline__ float f4_at(const float4 &v, int i)
+{
+    return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
+}
+
+// One channel of the 8-bit accumulation for key pair (2P, 2P+1) of every
+// slot: acc <- RN_e4m3(RN32(q * k + acc)).
+template <int QPL, bool SAT, int P>
+__device__ __forceinline__ void emu8_pair(float kv, const float (&q)[QPL], uint32_t (&acc)[QPL][8])
 {
 #pragma unroll
-    for (int s = 0; s < QPL; ++s)
-#pragma unroll
-        for (int p = 0; p < 8; ++p) {
-            float2 a = unpk_e4m3(acc[s][p]);
-            float x = __builtin_fmaf(q[s], kv[2 * p], a.x);
-            float y = __builtin_fmaf(q[s], kv[2 * p + 1], a.y);
-            acc[s][p] = SAT ? pk_e4m3_sat(x, y, acc[s][p]) : pk_e4m3(x, y, acc[s][p]);
-        }
+    for (int s = 0; s < QPL; ++s) {
+        const float2 a = unpk_e4m3(acc[s][P]);
+        const float x = fmac_bc<2 * P>(a.x, kv, q[s]);
+        const float y = fmac_bc<2 * P + 1>(a.y, kv, q[s]);
+        acc[s][P] = SAT ? pk_e4m3_sat(x, y, acc[s][P]) : pk_e4m3(x, y, acc[s][P]);
+    }
+}
+
+template <int QPL, bool SAT, int... P>
+__device__ __forceinline__ void emu8_channel(float kv, const float (&q)[QPL], uint32_t (&acc)[QPL][8],
+                                             std::integer_sequence<int, P...>)
+{
+    (emu8_pair<QPL, SAT, P>(kv, q, acc), ...);
 }
 
 // Y8 of one 16-key chunk for QPL query rows of this lane (Sec. 4.1:
 // acc <- RN_e4m3(RN32(q_tilde * k + acc)), channels ascending, from +0).
-// qrow[s] is the fp32 pre-scaled query row of slot s; kt the chunk's keys,
-// [D][16] fp32.  acc[s][p] receives the codes of keys 2p, 2p+1 in bits [15:0].
+// k32 is the fp32 key matrix at the chunk's first key ([key][D]); qrow[s] the
+// fp32 pre-scaled query row of slot s.  acc[s][p] receives the codes of keys
+// 2p, 2p+1 in bits [15:0].
 template <int D, int QPL, bool SAT>
-__device__ __forceinline__ void emu8_pass(const float *const (&qrow)[QPL], kptr32_t kt, uint32_t (&acc)[QPL][8])
+__device__ __forceinline__ void emu8_pass(const float *const (&qrow)[QPL], const float *k32, uint32_t (&acc)[QPL][8])
 {
-    static_assert(D % 4 == 0, "channels in groups of 4");
+    static_assert(D % 8 == 0, "channels in pairs of 4-channel groups");
 #pragma unroll
     for (int s = 0; s < QPL; ++s)
 #pragma unroll
         for (int p = 0; p < 8; ++p) acc[s][p] = 0u;
-    float ka0[16], ka1[16], kb0[16], kb1[16];
-    kload2(ka0, ka1, kt, 0, D);
-    float4 qc[QPL];
+    const float *krow = k32 + (size_t)(__lane_id() & 15) * D;
+    // Two alternating load buffers: the key registers feeding the DPP
+    // broadcast are only ever written by vector loads, never copied.
+    float4 ka, kb, qa[QPL], qb[QPL];
+    auto run = [&](const float4 &k4, const float4 (&q4)[QPL]) {
 #pragma unroll
-    for (int s = 0; s < QPL; ++s) qc[s] = reinterpret_cast<const float4 *>(qrow[s])[0];
-    for (int c = 0; c < D; c += 4) {
-        float4 qn[QPL];
-        const int cn = c + 4 < D ? c + 4 : c;
+        for (int cc = 0; cc < 4; ++cc) {
+            float q[QPL];
 #pragma unroll
-        for (int s = 0; s < QPL; ++s) qn[s] = reinterpret_cast<const float4 *>(qrow[s])[cn / 4];
-        float q0[QPL], q1[QPL], q2[QPL], q3[QPL];
-#pragma unroll
-        for (int s = 0; s < QPL; ++s) {
-            q0[s] = qc[s].x;
-            q1[s] = qc[s].y;
-            q2[s] = qc[s].z;
-            q3[s] = qc[s].w;
+            for (int s = 0; s < QPL; ++s) q[s] = f4_at(q4[s], cc);
+            emu8_channel<QPL, SAT>(f4_at(k4, cc), q, acc, std::make_integer_sequence<int, 8>());
         }
-        smem_fence();
-        kload2(kb0, kb1, kt, c + 2, D);
-        __builtin_amdgcn_sched_barrier(0);
-        emu8_step<QPL, SAT>(ka0, q0, acc);
-        emu8_step<QPL, SAT>(ka1, q1, acc);
-        smem_fence();
-        kload2(ka0, ka1, kt, c + 4, D);
-        __builtin_amdgcn_sched_barrier(0);
-        emu8_step<QPL, SAT>(kb0, q2, acc);
-        emu8_step<QPL, SAT>(kb1, q3, acc);
-#pragma unroll
-        for (int s = 0; s < QPL; ++s) qc[s] = qn[s];
+    };
+    load_group<QPL>(krow, qrow, 0, ka, qa);
+    for (int c = 0; c < D; c += 8) {
+        load_group<QPL>(krow, qrow, c + 4, kb, qb);
+        run(ka, qa);
+        load_group<QPL>(krow, qrow, c + 8 < D ? c + 8 : c, ka, qa);
+        run(kb, qb);
     }
-    smem_fence();   // drain the last (unused) batch
 }
 
 // The fast pass uses the non-saturating conversion; if any lane of the wave
 // overflowed somewhere (a NaN code at the end of a chain), the chunk is
 // recomputed with the saturating conversion.
 template <int D, int QPL>
-__device__ __forceinline__ void emu8_chunk(const float *const (&qrow)[QPL], const float *kt_generic,
-                                           uint32_t (&acc)[QPL][8])
+__device__ __forceinline__ void emu8_chunk(const float *const (&qrow)[QPL], const float *k32, uint32_t (&acc)[QPL][8])
 {
-    kptr32_t kt = (kptr32_t)kt_generic;
-    emu8_pass<D, QPL, false>(qrow, kt, acc);
+    emu8_pass<D, QPL, false>(qrow, k32, acc);
     uint32_t nan = 0;
 #pragma unroll
     for (int s = 0; s < QPL; ++s)
 #pragma unroll
         for (int p = 0; p < 8; ++p) nan |= e4m3_nan_bits(acc[s][p]);
-    if (wave_any(nan != 0)) emu8_pass<D, QPL, true>(qrow, kt, acc);
+    if (wave_any(nan != 0)) emu8_pass<D, QPL, true>(qrow, k32, acc);
 }
 
-// One channel of the 16-bit accumulation: acc <- RN32(q * k + acc).
-template <int QPL>
-__device__ __forceinline__ void rec16_step(const float (&kv)[16], const float (&q)[QPL], float (&acc)[QPL][16])
+// One channel of the 16-bit accumulation for every key and slot.
+template <int QPL, int NKEY, int... I>
+__device__ __forceinline__ void rec16_channel(float kv, const float (&q)[QPL], float (&acc)[QPL][NKEY],
+                                              std::integer_sequence<int, I...>)
 {
+#pragma unroll
+    for (int s = 0; s < QPL; ++s) ((acc[s][I] = fmac_bc<I>(acc[s][I], kv, q[s])), ...);
+}
+
+// Y16 of NKEY keys (NKEY in {4, 8, 16}) starting at k32 ([key][D] fp32) for
+// QPL query rows: the FP32 FMA chain over the channels in ascending order
+// from +0, rounded once to e4m11 (saturating).  codes[s][p] receives the
+// e4m11 codes of keys 2p (bits [15:0]) and 2p+1.
+template <int D, int QPL, int NKEY>
+__device__ __forceinline__ void rec16_keys(const float *const (&qrow)[QPL], const float *k32,
+                                           uint32_t (&codes)[QPL][NKEY / 2])
+{
+    static_assert(NKEY == 4 || NKEY == 8 || NKEY == 16, "4, 8 or 16 keys");
+    float acc[QPL][NKEY];
 #pragma unroll
     for (int s = 0; s < QPL; ++s)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) acc[s][i] = __builtin_fmaf(q[s], kv[i], acc[s][i]);
-}
-
-// Y16 of one 16-key chunk for QPL query rows: the FP32 FMA chain over the
-// channels in ascending order from +0, rounded once to e4m11 (saturating).
-// codes[s][p] receives the e4m11 codes of keys 2p (bits [15:0]) and 2p+1.
-template <int D, int QPL>
-__device__ __forceinline__ void rec16_chunk(const float *const (&qrow)[QPL], const float *kt_generic,
-                                            uint32_t (&codes)[QPL][8])
-{
-    kptr32_t kt = (kptr32_t)kt_generic;
-    float acc[QPL][16];
+        for (int i = 0; i < NKEY; ++i) acc[s][i] = 0.0f;
+    const float *krow = k32 + (size_t)((__lane_id() & 15) % NKEY) * D;
+    float4 ka, kb, qa[QPL], qb[QPL];   // alternating buffers, see emu8_pass
+    auto run = [&](const float4 &k4, const float4 (&q4)[QPL]) {
 #pragma unroll
-    for (int s = 0; s < QPL; ++s)
+        for (int cc = 0; cc < 4; ++cc) {
+            float q[QPL];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) acc[s][i] = 0.0f;
-    float ka0[16], ka1[16], kb0[16], kb1[16];
-    kload2(ka0, ka1, kt, 0, D);
-    float4 qc[QPL];
-#pragma unroll
-    for (int s = 0; s < QPL; ++s) qc[s] = reinterpret_cast<const float4 *>(qrow[s])[0];
-    for (int c = 0; c < D; c += 4) {
-        float4 qn[QPL];
-        const int cn = c + 4 < D ? c + 4 : c;
-#pragma unroll
-        for (int s = 0; s < QPL; ++s) qn[s] = reinterpret_cast<const float4 *>(qrow[s])[cn / 4];
-        float q0[QPL], q1[QPL], q2[QPL], q3[QPL];
-#pragma unroll
-        for (int s = 0; s < QPL; ++s) {
-            q0[s] = qc[s].x;
-            q1[s] = qc[s].y;
-            q2[s] = qc[s].z;
-            q3[s] = qc[s].w;
+            for (int s = 0; s < QPL; ++s) q[s] = f4_at(q4[s], cc);
+            rec16_channel<QPL, NKEY>(f4_at(k4, cc), q, acc, std::make_integer_sequence<int, NKEY>());
         }
-        smem_fence();
-        kload2(kb0, kb1, kt, c + 2, D);
-        __builtin_amdgcn_sched_barrier(0);
-        rec16_step<QPL>(ka0, q0, acc);
-        rec16_step<QPL>(ka1, q1, acc);
-        smem_fence();
-        kload2(ka0, ka1, kt, c + 4, D);
-        __builtin_amdgcn_sched_barrier(0);
-        rec16_step<QPL>(kb0, q2, acc);
-        rec16_step<QPL>(kb1, q3, acc);
-#pragma unroll
-        for (int s = 0; s < QPL; ++s) qc[s] = qn[s];
+    };
+    load_group<QPL>(krow, qrow, 0, ka, qa);
+    for (int c = 0; c < D; c += 8) {
+        load_group<QPL>(krow, qrow, c + 4, kb, qb);
+        run(ka, qa);
+        load_group<QPL>(krow, qrow, c + 8 < D ? c + 8 : c, ka, qa);
+        run(kb, qb);
     }
-    smem_fence();
 #pragma unroll
     for (int s = 0; s < QPL; ++s)
 #pragma unroll
-        for (int p = 0; p < 8; ++p) {
+        for (int p = 0; p < NKEY / 2; ++p) {
             uint32_t c0, c1;
             (void)rn_e4m11((double)acc[s][2 * p], &c0);
             (void)rn_e4m11((double)acc[s][2 * p + 1], &c1);
             codes[s][p] = c0 | (c1 << 16);
         }
+}
+
+template <int D, int QPL>
+__device__ __forceinline__ void rec16_chunk(const float *const (&qrow)[QPL], const float *k32, uint32_t (&codes)[QPL][8])
+{
+    rec16_keys<D, QPL, 16>(qrow, k32, codes);
 }
 
 } // namespace lamp
