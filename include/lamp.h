@@ -100,6 +100,19 @@ int lamp_attn_logits16(const uint16_t *q, const uint16_t *k,
                        int B, int Hq, int Hkv, int N, int d, int causal, int window,
                        int row0, int nrows, uint16_t *y16, void *stream);
 
+/*
+ * Kernel timing, for measurement.  While enabled (lamp_timing_enable(1)),
+ * each lamp_attn_fwd call records three HIP events on its own stream: before
+ * the prepass (query scaling, key conversion), between it and the forward
+ * kernel, and after the forward kernel.  lamp_timing_read waits for the
+ * events of every call recorded since the previous read, stores the number
+ * of calls and the summed durations (milliseconds) of the forward kernel and
+ * of the prepass (any output pointer may be NULL), destroys the events and
+ * forgets the calls.  Calls made while disabled record nothing.
+ */
+int lamp_timing_enable(int on);
+int lamp_timing_read(int *launches, double *fwd_ms, double *prepass_ms);
+
 /* Build the device tables of `device` now (otherwise done by the first call). */
 int lamp_init(int device);
 

@@ -697,6 +697,12 @@ static hipError_t launch_fwd(const FwdParams &p, hipStream_t s)
 #define LAMP_FWD_CASE(D_, BQ_, BK_, NK_) \
     if (D == D_ && BQ == BQ_ && BK == BK_ && NK == NK_) return launch_fwd<D_, BQ_, BK_, NK_>(p, s);
 
+bool fwd_supported(int D, int BQ, int BK, int NK)
+{
+    // configurations built: d in {64,128,256}, bq in {64,128}, (bk, nk) in {(16,4), (64,4)}
+    return (D == 64 || D == 128 || D == 256) && (BQ == 64 || BQ == 128) && (BK == 16 || BK == 64) && NK == 4;
+}
+
 hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found)
 {
     *found = true;

@@ -43,6 +43,15 @@ struct DeviceState {
 std::mutex g_mu;
 std::vector<DeviceState> g_dev;
 
+// Kernel timing (lamp_timing_enable / lamp_timing_read): event triples
+// around the prepass and the forward kernel of each lamp_attn_fwd call.
+struct TimedCall {
+    hipEvent_t e[3];
+};
+std::mutex g_tmu;
+bool g_timing = false;
+std::vector<TimedCall> g_timed;
+
 DeviceState *state_of(int dev)
 {
     if (dev < 0) return nullptr;
@@ -197,6 +206,8 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
     if (bq <= 0 || bk <= 0 || nk <= 0) return fail(LAMP_ERR_INVALID_ARG, "block sizes must be positive");
     if (N % bq || N % (bk * nk))
         return fail(LAMP_ERR_INVALID_ARG, "N=%d must be a multiple of bq=%d and of bk*nk=%d", N, bq, bk * nk);
+    if (!lamp::fwd_supported(d, bq, bk, nk))
+        return fail(LAMP_ERR_UNSUPPORTED, "block sizes (bq=%d, bk=%d, nk=%d) not built for d=%d", bq, bk, nk, d);
     int dev = 0;
     rc = current_device(&dev);
     if (rc) return rc;
@@ -228,12 +239,62 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
     p.delta = delta;
     p.tau = tau;
     p.mode = std::isinf(tau) ? lamp::MODE_PURE8 : (tau == 0.0 ? lamp::MODE_ALL16 : lamp::MODE_LAMP);
+    bool timed = false;
+    TimedCall tc{};
+    {
+        std::lock_guard<std::mutex> lk(g_tmu);
+        timed = g_timing;
+    }
+    if (timed) {
+        for (int i = 0; i < 3; ++i) HIP_TRY(hipEventCreate(&tc.e[i]));
+        HIP_TRY(hipEventRecord(tc.e[0], s));
+    }
     HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, d, scale_of(d), s));
+    if (timed) HIP_TRY(hipEventRecord(tc.e[1], s));
     bool found = false;
     HIP_TRY(lamp::dispatch_fwd(d, bq, bk, nk, p, s, &found));
     if (!found)
         return fail(LAMP_ERR_UNSUPPORTED, "block sizes (bq=%d, bk=%d, nk=%d) not built for d=%d", bq, bk, nk, d);
+    if (timed) {
+        HIP_TRY(hipEventRecord(tc.e[2], s));
+        std::lock_guard<std::mutex> lk(g_tmu);
+        g_timed.push_back(tc);
+    }
     return LAMP_OK;
+}
+
+int lamp_timing_enable(int on)
+{
+    std::lock_guard<std::mutex> lk(g_tmu);
+    g_timing = on != 0;
+    return LAMP_OK;
+}
+
+int lamp_timing_read(int *launches, double *fwd_ms, double *prepass_ms)
+{
+    std::vector<TimedCall> calls;
+    {
+        std::lock_guard<std::mutex> lk(g_tmu);
+        calls.swap(g_timed);
+    }
+    double tf = 0.0, tp = 0.0;
+    int rc = LAMP_OK;
+    for (TimedCall &c : calls) {
+        float a = 0.f, b = 0.f;
+        if (rc == LAMP_OK) {
+            hipError_t e = hipEventSynchronize(c.e[2]);
+            if (e == hipSuccess) e = hipEventElapsedTime(&a, c.e[0], c.e[1]);
+            if (e == hipSuccess) e = hipEventElapsedTime(&b, c.e[1], c.e[2]);
+            if (e != hipSuccess) rc = fail(LAMP_ERR_HIP, "kernel timing events: %s", hipGetErrorString(e));
+        }
+        tp += a;
+        tf += b;
+        for (int i = 0; i < 3; ++i) (void)hipEventDestroy(c.e[i]);
+    }
+    if (launches) *launches = (int)calls.size();
+    if (fwd_ms) *fwd_ms = tf;
+    if (prepass_ms) *prepass_ms = tp;
+    return rc;
 }
 
 static int logits_common(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv, int N, int d, int causal,

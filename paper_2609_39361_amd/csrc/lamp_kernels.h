@@ -30,6 +30,7 @@ struct LogitsParams {
     int B, Hq, Hkv, N, causal, window, row0, nrows;
 };
 
+bool fwd_supported(int D, int BQ, int BK, int NK);
 hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found);
 hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float *kt32,
                           int B, int Hq, int Hkv, int N, int D, float scale, hipStream_t s);

@@ -51,6 +51,10 @@ def lib():
         L.lamp_selftest_exp_doc.restype = i32
         L.lamp_get_tables.argtypes = [i32, P, P]
         L.lamp_get_tables.restype = i32
+        L.lamp_timing_enable.argtypes = [i32]
+        L.lamp_timing_enable.restype = i32
+        L.lamp_timing_read.argtypes = [P, P, P]
+        L.lamp_timing_read.restype = i32
         L.lamp_status_str.argtypes = [i32]
         L.lamp_status_str.restype = ctypes.c_char_p
         L.lamp_last_error.argtypes = []
@@ -165,6 +169,20 @@ def init(device=0):
 
 def shutdown():
     lib().lamp_shutdown()
+
+
+def timing_enable(on=True):
+    """Record HIP events around the prepass and forward kernel of each
+    attn_fwd call (on the call's stream) until disabled."""
+    _check(lib().lamp_timing_enable(1 if on else 0))
+
+
+def timing_read():
+    """(calls, forward-kernel ms summed, prepass ms summed) of the calls
+    recorded since the previous read; waits for their events."""
+    n, tf, tp = ctypes.c_int(0), ctypes.c_double(0.0), ctypes.c_double(0.0)
+    _check(lib().lamp_timing_read(ctypes.byref(n), ctypes.byref(tf), ctypes.byref(tp)))
+    return n.value, tf.value, tp.value
 
 
 def mask_stats(mask, nk):

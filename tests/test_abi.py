@@ -68,3 +68,20 @@ def test_binding_rejects_bad_arguments_without_gpu():
     rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, -1.0,
                            dummy, dummy, dummy, None)
     assert rc == 1
+    # block sizes that are not built
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 32, 16, 4, 2 ** -8, 0.5,
+                           dummy, dummy, dummy, None)
+    assert rc == 2 and b"not built" in lib.lamp_last_error()
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 128, 32, 4, 2 ** -8, 0.5,
+                           dummy, dummy, dummy, None)
+    assert rc == 2
+
+
+def test_timing_read_without_calls():
+    """Timing bookkeeping is host-only: nothing recorded reads as zero."""
+    if not os.path.exists(LIB):
+        pytest.skip("liblamp.so not built")
+    from paper_2609_39361_amd import lamp
+    lamp.timing_enable(True)
+    lamp.timing_enable(False)
+    assert lamp.timing_read() == (0, 0.0, 0.0)
