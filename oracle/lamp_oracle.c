@@ -18,8 +18,8 @@
  *     Sec. 3.3, "Floating-point formats";
  *   - recursive FMA accumulation in FP32 with rounding after every step:
  *     Sec. 4.1.
- * Where the paper is silent the readings listed in DESIGN.md ("Readings of the
- * paper") are taken; each is restated at the place it is used.
+ * Where the paper is silent or ambiguous, the reading taken is stated at the
+ * place it is used (marked "reading:").
  *
  * Everything is fp64 except where the method fixes another precision (the
  * fp32 FMA of the 8-bit accumulation, the formats above).  Build with
