@@ -150,30 +150,34 @@ __device__ __forceinline__ float bf16_value(uint32_t b)
 // 32-significant-bit head and an fp64 tail, then the degree-13 Taylor
 // polynomial in Horner form with fma and coefficients RN64(1/k!), then an
 // exact scaling by 2^n.  Arguments below -700 give 0.
-__device__ __forceinline__ double exp_doc(double x)
+//
+// EXPDOC_K: log2(e), ln2 head, ln2 tail, then 1/13!, 1/12!, ..., 1/0!.
+constexpr int EXPDOC_NK = 17;
+__device__ constexpr double EXPDOC_K[EXPDOC_NK] = {
+    0x1.71547652b82fep+0, 0x1.62e42fee00000p-1, 0x1.a39ef35793c76p-33,
+    0x1.6124613a86d09p-33, 0x1.1eed8eff8d898p-29, 0x1.ae64567f544e4p-26, 0x1.27e4fb7789f5cp-22,
+    0x1.71de3a556c734p-19, 0x1.a01a01a01a01ap-16, 0x1.a01a01a01a01ap-13, 0x1.6c16c16c16c17p-10,
+    0x1.1111111111111p-7,  0x1.5555555555555p-5,  0x1.5555555555555p-3,  0x1.0000000000000p-1,
+    1.0, 1.0};
+
+// k(i) returns EXPDOC_K[i]; the forward kernel reads them from LDS so that the
+// compiler does not keep 17 fp64 constants in registers across its main loop.
+template <class K>
+__device__ __forceinline__ double exp_doc_k(double x, K k)
 {
     if (x < -700.0) return 0.0;
-    const double log2e = 0x1.71547652b82fep+0;
-    const double ln2_hi = 0x1.62e42fee00000p-1;
-    const double ln2_lo = 0x1.a39ef35793c76p-33;
-    double n = __builtin_rint(x * log2e);
-    double r = __builtin_fma(-n, ln2_hi, x);
-    r = __builtin_fma(-n, ln2_lo, r);
-    double p = 0x1.6124613a86d09p-33;                // 1/13!
-    p = __builtin_fma(p, r, 0x1.1eed8eff8d898p-29);  // 1/12!
-    p = __builtin_fma(p, r, 0x1.ae64567f544e4p-26);  // 1/11!
-    p = __builtin_fma(p, r, 0x1.27e4fb7789f5cp-22);  // 1/10!
-    p = __builtin_fma(p, r, 0x1.71de3a556c734p-19);  // 1/9!
-    p = __builtin_fma(p, r, 0x1.a01a01a01a01ap-16);  // 1/8!
-    p = __builtin_fma(p, r, 0x1.a01a01a01a01ap-13);  // 1/7!
-    p = __builtin_fma(p, r, 0x1.6c16c16c16c17p-10);  // 1/6!
-    p = __builtin_fma(p, r, 0x1.1111111111111p-7);   // 1/5!
-    p = __builtin_fma(p, r, 0x1.5555555555555p-5);   // 1/4!
-    p = __builtin_fma(p, r, 0x1.5555555555555p-3);   // 1/3!
-    p = __builtin_fma(p, r, 0x1.0000000000000p-1);   // 1/2!
-    p = __builtin_fma(p, r, 1.0);                    // 1/1!
-    p = __builtin_fma(p, r, 1.0);                    // 1/0!
+    double n = __builtin_rint(x * k(0));
+    double r = __builtin_fma(-n, k(1), x);
+    r = __builtin_fma(-n, k(2), r);
+    double p = k(3);
+#pragma unroll
+    for (int i = 4; i < EXPDOC_NK; ++i) p = __builtin_fma(p, r, k(i));
     return __builtin_amdgcn_ldexp(p, (int)n);
+}
+
+__device__ __forceinline__ double exp_doc(double x)
+{
+    return exp_doc_k(x, [](int i) { return EXPDOC_K[i]; });
 }
 
 // --- wave helpers ------------------------------------------------------------

@@ -59,10 +59,11 @@ struct Cfg {
     static constexpr size_t OFF_V = OFF_Y + (size_t)BQ * YP * 2;
     static constexpr size_t OFF_LUT = OFF_V + (size_t)D * VP * 2;
     static constexpr size_t OFF_M8 = OFF_LUT + 512;                       // f32 [NK][BQ]
-    static constexpr size_t OFF_CM = OFF_M8 + (size_t)NK * BQ * 4;       // f32 [NK][BQ]
-    static constexpr size_t OFF_SP = OFF_CM + (size_t)NK * BQ * 4;       // f64 [NW][BQ]
+    static constexpr size_t OFF_CM = OFF_M8 + (size_t)NK * BQ * 4;       // f32 [NK + 2][NW][BQ]
+    static constexpr size_t OFF_SP = OFF_CM + (size_t)(NK + 2) * NW * BQ * 4;   // f64 [NW][BQ]
     static constexpr size_t OFF_CO = OFF_SP + (size_t)NW * BQ * 8;       // f64 [NK][BQ]
-    static constexpr size_t LDS = OFF_CO + (size_t)NK * BQ * 8;
+    static constexpr size_t OFF_ED = OFF_CO + (size_t)NK * BQ * 8;       // f64 [EXPDOC_NK]
+    static constexpr size_t LDS = OFF_ED + (size_t)EXPDOC_NK * 8;
     static_assert(BQ == 64 || BQ == 128, "64 or 128 query rows per block");
     static_assert(BK % 16 == 0 && NK <= 4 && NK % NW == 0, "sub-blocks of 16-key chunks, at most 4 per tile");
     static_assert(CPW % 32 == 0, "whole 32-channel tiles per wave");
@@ -76,15 +77,20 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
     constexpr int QPL = C::QPL, KPT = C::KPT, NCH = C::NCH, NW = C::NW, SPW = C::SPW, CPW = C::CPW;
     constexpr int CT = C::CT, QG = C::QG, YP = C::YP, VP = C::VP, KPW = C::KPW;
     constexpr int CPS = BK / 16;   // chunks per sub-block
+    // Stage-1 recomputes in one batch (4 keys of every sub-block per wave),
+    // codes kept in registers; otherwise one shared recompute per failure.
+    constexpr bool BATCH = KPW == 4;
 
     extern __shared__ __align__(16) unsigned char smem[];
     uint16_t *ycode = reinterpret_cast<uint16_t *>(smem + C::OFF_Y);   // [BQ][YP] logit / exp codes
     uint16_t *vt = reinterpret_cast<uint16_t *>(smem + C::OFF_V);      // [D][VP] V^T of the tile
     uint16_t *lut = reinterpret_cast<uint16_t *>(smem + C::OFF_LUT);   // [256] 8-bit exp (bf16 bits)
     float *m8s = reinterpret_cast<float *>(smem + C::OFF_M8);          // [NK][BQ] 8-bit column maxima
-    float *cms = reinterpret_cast<float *>(smem + C::OFF_CM);          // [NK][BQ] 16-bit column maxima
+    float *cms = reinterpret_cast<float *>(smem + C::OFF_CM);          // [NK][NW][BQ] 16-bit column maxima
+    float *cmf = cms + NK * NW * BQ;   // [2][NW][BQ] the same for the one-at-a-time path, by iteration parity
     double *sps = reinterpret_cast<double *>(smem + C::OFF_SP);        // [NW][BQ] partial row sums
     double *cst_lds = reinterpret_cast<double *>(smem + C::OFF_CO);    // [NK][BQ] stage-2 costs
+    double *edk = reinterpret_cast<double *>(smem + C::OFF_ED);        // exp_doc constants
 
     const int tid = threadIdx.x;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;   // w is wave-uniform
@@ -118,6 +124,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
     uint8_t *mrow = p.mask + (((size_t)b * p.Hq + h) * nqb + qb) * (size_t)(p.N / BK);
 
     for (int i = tid; i < 256; i += 64 * NW) lut[i] = p.lut8e[i];
+    if (tid < EXPDOC_NK) edk[tid] = EXPDOC_K[tid];
 
     float mu[QPL];     // running maxima (e4m11 or e4m3 values)
     double om[QPL];    // running sums omega
@@ -146,12 +153,12 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
             for (int ch = 0; ch < KPW / 16; ++ch) {
                 const int kc = key0 + ch * 16;
                 uint32_t yc[QPL][8];
-                rec16_keys<D, QPL, 16>(qrow, kt32 + (size_t)kc * D, yc);
+                rec16_keys<D, QPL, 16>(qrow, kt32 + (size_t)(kc + (lane & 15)) * D, yc);
                 fn(kc, yc);
             }
         } else {
             uint32_t yc[QPL][KPW / 2];
-            rec16_keys<D, QPL, KPW>(qrow, kt32 + (size_t)key0 * D, yc);
+            rec16_keys<D, QPL, KPW>(qrow, kt32 + (size_t)(key0 + (lane & 15) % KPW) * D, yc);
             fn(key0, yc);
         }
     };
@@ -247,6 +254,8 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
             for (int th = 0; th < NK; ++th) m8[th][s] = (p.mode != MODE_ALL16) ? m8s[th * BQ + row[s]] : NEG_INF;
         }
         uint32_t prec16 = 0;   // stage-1 (or threshold-0) sub-blocks
+        uint32_t F0 = 0;       // sub-blocks whose 16-bit codes this wave holds in y16r (batched stage 1)
+        uint32_t y16r[QPL][8]; // e4m11 codes of keys th*BK + w*4 + {0..3} of the members of F0, 2 per word
         if (p.mode == MODE_PURE8) {
 #pragma unroll
             for (int s = 0; s < QPL; ++s)
@@ -345,13 +354,106 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                 return f;
             };
             uint32_t fail = fails();
-            int pos = 0;
+            float cm16[NK][QPL];   // batched: 16-bit column maxima of the members of F0
+            if constexpr (BATCH) if (fail) {   // fail is identical in every wave: the barrier below is uniform
+                // Speculation: the margin test is monotone in mu_hat and mu_hat
+                // only grows, so every sub-block that stage 1 will recompute
+                // fails against mu already.  Recompute all of those at once,
+                // 4 keys of each per wave; the sequential test below then needs
+                // only their column maxima.  A sub-block outside this set that
+                // still fails takes the one-at-a-time path.
+                F0 = fail;
+                const int nf = __builtin_popcount(F0);
+                // lane key slot kk = lane%16 mod 4nf: member g = kk/4, key w*4 + kk%4 of it
+                const int kk = (lane & 15) % (4 * nf);
+                int thg = 0;
+                {
+                    uint32_t m = F0;
+                    for (int g = 0; g < kk / 4; ++g) m &= m - 1;
+                    thg = __builtin_ctz(m);
+                }
+                const float *krow = kt32 + (size_t)(k0 + thg * BK + w * 4 + (kk & 3)) * D;
+                if (nf == 1) {
+                    uint32_t c[QPL][2];
+                    rec16_keys<D, QPL, 4>(qrow, krow, c);
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                        for (int pp = 0; pp < 2; ++pp) y16r[s][pp] = c[s][pp];
+                } else if (nf == 2) {
+                    uint32_t c[QPL][4];
+                    rec16_keys<D, QPL, 8>(qrow, krow, c);
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                        for (int pp = 0; pp < 4; ++pp) y16r[s][pp] = c[s][pp];
+                } else if (nf == 3) {
+                    uint32_t c[QPL][6];
+                    rec16_keys<D, QPL, 12>(qrow, krow, c);
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                        for (int pp = 0; pp < 6; ++pp) y16r[s][pp] = c[s][pp];
+                } else if (nf == 4) {
+                    rec16_keys<D, QPL, 16>(qrow, krow, y16r);
+                }
+                // partial column maxima over this wave's 4 keys of every member
+                {
+                    uint32_t m = F0;
+#pragma unroll
+                    for (int g = 0; g < NK; ++g) {
+                        if (!m) break;
+                        const int th = __builtin_ctz(m);
+                        m &= m - 1;
+                        const int key0 = k0 + th * BK + w * 4;
+#pragma unroll
+                        for (int s = 0; s < QPL; ++s) {
+                            float cm = NEG_INF;
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) {
+                                const uint32_t word = g == 0 ? y16r[s][i >> 1] : g == 1 ? y16r[s][2 + (i >> 1)]
+                                                    : g == 2 ? y16r[s][4 + (i >> 1)] : y16r[s][6 + (i >> 1)];
+                                const float yv = e4m11_value((word >> (16 * (i & 1))) & 0xFFFFu);
+                                if (visible(s, key0 + i)) cm = yv > cm ? yv : cm;
+                            }
+                            cms[(th * NW + w) * BQ + row[s]] = cm;
+                        }
+                    }
+                }
+                __syncthreads();
+#pragma unroll
+                for (int th = 0; th < NK; ++th)
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) {
+                        float c = NEG_INF;
+                        if (F0 >> th & 1u)
+#pragma unroll
+                            for (int ww = 0; ww < NW; ++ww) {
+                                const float x = cms[(th * NW + ww) * BQ + row[s]];
+                                c = x > c ? x : c;
+                            }
+                        cm16[th][s] = c;
+                    }
+            }
+            int pos = 0, par = 0;
             while (true) {
                 while (pos < na && !(fail >> ((order >> (4 * pos)) & 15u) & 1u)) ++pos;
                 if (pos >= na) break;
                 const int th = (int)((order >> (4 * pos)) & 15u);
                 ++pos;
                 prec16 |= 1u << th;
+                if (BATCH && (F0 >> th & 1u)) {
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) {
+                        float c = muh[s];
+#pragma unroll
+                        for (int t2 = 0; t2 < NK; ++t2)
+                            if (t2 == th) c = cm16[t2][s] > c ? cm16[t2][s] : c;
+                        muh[s] = c;
+                    }
+                    if (pos < na) fail = fails();
+                    continue;
+                }
                 {   // all waves recompute the sub-block in 16 bits, KPW keys each
                     float cm[QPL];
 #pragma unroll
@@ -369,17 +471,18 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                         }
                     });
 #pragma unroll
-                    for (int s = 0; s < QPL; ++s) cms[w * BQ + row[s]] = cm[s];
+                    for (int s = 0; s < QPL; ++s) cmf[(par * NW + w) * BQ + row[s]] = cm[s];
                 }
                 __syncthreads();
 #pragma unroll
                 for (int s = 0; s < QPL; ++s) {
 #pragma unroll
                     for (int ww = 0; ww < NW; ++ww) {
-                        const float c = cms[ww * BQ + row[s]];
+                        const float c = cmf[(par * NW + ww) * BQ + row[s]];
                         muh[s] = c > muh[s] ? c : muh[s];
                     }
                 }
+                par ^= 1;   // the next write goes to the other half: readers of this one may lag
                 if (pos < na) fail = fails();
             }
         }
@@ -403,6 +506,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                         }
                     continue;
                 }
+                if (BATCH && ((prec16 & F0) >> th & 1u)) continue;   // from registers by every wave, below
                 const bool hi16 = prec16 >> th & 1u;
                 for (int ch = 0; ch < CPS; ++ch) {
                     const int c16 = th * CPS + ch;
@@ -446,6 +550,43 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                     }
                 }
             }
+            if constexpr (BATCH) {
+                // 16-bit exponentials of this wave's 4 keys of every batched
+                // stage-1 sub-block, from the codes held in registers
+                const uint32_t mine = prec16 & F0;
+                uint32_t m = F0;
+#pragma unroll
+                for (int g = 0; g < NK; ++g) {
+                    if (!m) break;
+                    const int th = __builtin_ctz(m);
+                    m &= m - 1;
+                    if (!(mine >> th & 1u)) continue;
+                    const int key0 = k0 + th * BK + w * 4;
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) {
+                        uint32_t outw[2];
+#pragma unroll
+                        for (int pp = 0; pp < 2; ++pp) {
+                            uint32_t res = 0;
+#pragma unroll
+                            for (int t = 0; t < 2; ++t) {
+                                const int key = key0 + 2 * pp + t;
+                                uint32_t ec = 0;
+                                float ev = 0.0f;
+                                if (visible(s, key)) {
+                                    const uint32_t yc = (y16r[s][2 * g + pp] >> (16 * t)) & 0xFFFFu;
+                                    ec = p.exp16[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))];
+                                    ev = ue5m11e_value(ec);
+                                }
+                                sp[s] += (double)ev;
+                                res |= ec << (16 * t);
+                            }
+                            outw[pp] = res;
+                        }
+                        *reinterpret_cast<uint2 *>(ycode + row[s] * YP + (key0 - k0)) = make_uint2(outw[0], outw[1]);
+                    }
+                }
+            }
 #pragma unroll
             for (int s = 0; s < QPL; ++s) sps[w * BQ + row[s]] = sp[s];
         }
@@ -461,7 +602,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
             S[s] = t;
             if (muh[s] == NEG_INF) lam[s] = 1.0;
             else if (mu[s] == NEG_INF) lam[s] = 0.0;
-            else lam[s] = exp_doc((double)mu[s] - (double)muh[s]);
+            else lam[s] = exp_doc_k((double)mu[s] - (double)muh[s], [&](int i) { return edk[i]; });
             omh[s] = __builtin_fma(lam[s], om[s], t);
         }
         uint32_t prec2 = 0;
@@ -533,35 +674,55 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                     double ds[QPL];
 #pragma unroll
                     for (int s = 0; s < QPL; ++s) ds[s] = 0.0;
+                    auto s2fn = [&](int kc, const auto &yc) {
+                        constexpr int NWD = sizeof(yc[0]) / sizeof(uint32_t);
+#pragma unroll
+                        for (int s = 0; s < QPL; ++s) {
+                            const uint16_t *src = ycode + row[s] * YP + (kc - k0);
+                            uint32_t outw[NWD];
+#pragma unroll
+                            for (int pp = 0; pp < NWD; ++pp) {
+                                uint32_t res = 0;
+#pragma unroll
+                                for (int t = 0; t < 2; ++t) {
+                                    const int key = kc + 2 * pp + t;
+                                    uint32_t ec = 0;
+                                    if (visible(s, key)) {
+                                        const float old = bf16_value(src[2 * pp + t]);
+                                        const float y = e4m11_value((yc[s][pp] >> (16 * t)) & 0xFFFFu);
+                                        ec = p.exp16[ue5m11_code(shift_of(muh[s], y))];
+                                        ds[s] = ds[s] - (double)old;
+                                        ds[s] = ds[s] + (double)ue5m11e_value(ec);
+                                    }
+                                    res |= ec << (16 * t);
+                                }
+                                outw[pp] = res;
+                            }
+                            put_codes(row[s], kc - k0, outw, NWD);
+                        }
+                    };
                     for (int th = 0; th < NK; ++th) {
                         if (!(prec2 >> th & 1u)) continue;
-                        shared16(k0, th, [&](int kc, const auto &yc) {
-                            constexpr int NWD = sizeof(yc[0]) / sizeof(uint32_t);
+                        if (BATCH && (F0 >> th & 1u)) {
+                            // the codes of this wave's keys are already in registers
+                            const uint32_t below = F0 & ((1u << th) - 1u);
+                            const int gi = __builtin_popcount(below);
+                            uint32_t yc[QPL][2];
 #pragma unroll
                             for (int s = 0; s < QPL; ++s) {
-                                const uint16_t *src = ycode + row[s] * YP + (kc - k0);
-                                uint32_t outw[NWD];
+                                yc[s][0] = y16r[s][0];
+                                yc[s][1] = y16r[s][1];
 #pragma unroll
-                                for (int pp = 0; pp < NWD; ++pp) {
-                                    uint32_t res = 0;
-#pragma unroll
-                                    for (int t = 0; t < 2; ++t) {
-                                        const int key = kc + 2 * pp + t;
-                                        uint32_t ec = 0;
-                                        if (visible(s, key)) {
-                                            const float old = bf16_value(src[2 * pp + t]);
-                                            const float y = e4m11_value((yc[s][pp] >> (16 * t)) & 0xFFFFu);
-                                            ec = p.exp16[ue5m11_code(shift_of(muh[s], y))];
-                                            ds[s] = ds[s] - (double)old;
-                                            ds[s] = ds[s] + (double)ue5m11e_value(ec);
-                                        }
-                                        res |= ec << (16 * t);
+                                for (int g = 1; g < NK; ++g)
+                                    if (g == gi) {
+                                        yc[s][0] = y16r[s][2 * g];
+                                        yc[s][1] = y16r[s][2 * g + 1];
                                     }
-                                    outw[pp] = res;
-                                }
-                                put_codes(row[s], kc - k0, outw, NWD);
                             }
-                        });
+                            s2fn(k0 + th * BK + w * 4, yc);
+                        } else {
+                            shared16(k0, th, s2fn);
+                        }
                     }
 #pragma unroll
                     for (int s = 0; s < QPL; ++s) sps[w * BQ + row[s]] = ds[s];

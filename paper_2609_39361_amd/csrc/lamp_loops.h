@@ -88,13 +88,18 @@ __device__ __forceinline__ void emu8_pass(const float *const (&qrow)[QPL], const
             emu8_channel<QPL, SAT>(f4_at(k4, cc), q, acc, std::make_integer_sequence<int, 8>());
         }
     };
+    // steady state, then the last pair of groups without further loads (the
+    // offsets stay affine in c, so they fold into the loads' immediates)
     load_group<QPL>(krow, qrow, 0, ka, qa);
-    for (int c = 0; c < D; c += 8) {
+    for (int c = 0; c < D - 8; c += 8) {
         load_group<QPL>(krow, qrow, c + 4, kb, qb);
         run(ka, qa);
-        load_group<QPL>(krow, qrow, c + 8 < D ? c + 8 : c, ka, qa);
+        load_group<QPL>(krow, qrow, c + 8, ka, qa);
         run(kb, qb);
     }
+    load_group<QPL>(krow, qrow, D - 4, kb, qb);
+    run(ka, qa);
+    run(kb, qb);
 }
 
 // The fast pass uses the non-saturating conversion; if any lane of the wave
@@ -121,38 +126,48 @@ __device__ __forceinline__ void rec16_channel(float kv, const float (&q)[QPL], f
     for (int s = 0; s < QPL; ++s) ((acc[s][I] = fmac_bc<I>(acc[s][I], kv, q[s])), ...);
 }
 
-// Y16 of NKEY keys (NKEY in {4, 8, 16}) starting at k32 ([key][D] fp32) for
-// QPL query rows: the FP32 FMA chain over the channels in ascending order
-// from +0, rounded once to e4m11 (saturating).  codes[s][p] receives the
-// e4m11 codes of keys 2p (bits [15:0]) and 2p+1.
+// Y16 of NKEY keys (NKEY in {4, 8, 12, 16}) for QPL query rows: the FP32 FMA
+// chain over the channels in ascending order from +0, rounded once to e4m11
+// (saturating).  krow is this lane's key row ([D] fp32): lane l of every
+// 16-lane row supplies key (l mod 16) and must hold key (l mod NKEY) (lanes
+// past NKEY duplicate the first keys and are not read).  codes[s][p] receives
+// the e4m11 codes of keys 2p (bits [15:0]) and 2p+1.  With few keys per
+// channel the loop is latency-bound, so the loads run PD 4-channel groups
+// ahead in a ring of buffers written only by loads.
 template <int D, int QPL, int NKEY>
-__device__ __forceinline__ void rec16_keys(const float *const (&qrow)[QPL], const float *k32,
+__device__ __forceinline__ void rec16_keys(const float *const (&qrow)[QPL], const float *krow,
                                            uint32_t (&codes)[QPL][NKEY / 2])
 {
-    static_assert(NKEY == 4 || NKEY == 8 || NKEY == 16, "4, 8 or 16 keys");
+    static_assert(NKEY == 4 || NKEY == 8 || NKEY == 12 || NKEY == 16, "4, 8, 12 or 16 keys");
+    constexpr int PD0 = NKEY <= 8 ? 4 : 2;
+    constexpr int PD = (D / 4) % PD0 == 0 ? PD0 : 2;
+    static_assert((D / 4) % PD == 0, "whole rings of 4-channel groups");
     float acc[QPL][NKEY];
 #pragma unroll
     for (int s = 0; s < QPL; ++s)
 #pragma unroll
         for (int i = 0; i < NKEY; ++i) acc[s][i] = 0.0f;
-    const float *krow = k32 + (size_t)((__lane_id() & 15) % NKEY) * D;
-    float4 ka, kb, qa[QPL], qb[QPL];   // alternating buffers, see emu8_pass
-    auto run = [&](const float4 &k4, const float4 (&q4)[QPL]) {
+    float4 kb[PD], qb[PD][QPL];
+    auto run = [&](int r) {
 #pragma unroll
         for (int cc = 0; cc < 4; ++cc) {
             float q[QPL];
 #pragma unroll
-            for (int s = 0; s < QPL; ++s) q[s] = f4_at(q4[s], cc);
-            rec16_channel<QPL, NKEY>(f4_at(k4, cc), q, acc, std::make_integer_sequence<int, NKEY>());
+            for (int s = 0; s < QPL; ++s) q[s] = f4_at(qb[r][s], cc);
+            rec16_channel<QPL, NKEY>(f4_at(kb[r], cc), q, acc, std::make_integer_sequence<int, NKEY>());
         }
     };
-    load_group<QPL>(krow, qrow, 0, ka, qa);
-    for (int c = 0; c < D; c += 8) {
-        load_group<QPL>(krow, qrow, c + 4, kb, qb);
-        run(ka, qa);
-        load_group<QPL>(krow, qrow, c + 8 < D ? c + 8 : c, ka, qa);
-        run(kb, qb);
+#pragma unroll
+    for (int r = 0; r < PD; ++r) load_group<QPL>(krow, qrow, 4 * r, kb[r], qb[r]);
+    for (int c = 0; c < D - 4 * PD; c += 4 * PD) {
+#pragma unroll
+        for (int r = 0; r < PD; ++r) {
+            run(r);
+            load_group<QPL>(krow, qrow, c + 4 * (r + PD), kb[r], qb[r]);
+        }
     }
+#pragma unroll
+    for (int r = 0; r < PD; ++r) run(r);   // the last ring, no further loads
 #pragma unroll
     for (int s = 0; s < QPL; ++s)
 #pragma unroll
@@ -164,10 +179,11 @@ __device__ __forceinline__ void rec16_keys(const float *const (&qrow)[QPL], cons
         }
 }
 
+// Y16 of the 16 keys starting at k32 ([key][D] fp32).
 template <int D, int QPL>
 __device__ __forceinline__ void rec16_chunk(const float *const (&qrow)[QPL], const float *k32, uint32_t (&codes)[QPL][8])
 {
-    rec16_keys<D, QPL, 16>(qrow, k32, codes);
+    rec16_keys<D, QPL, 16>(qrow, k32 + (size_t)(__lane_id() & 15) * D, codes);
 }
 
 } // namespace lamp
