@@ -26,14 +26,26 @@ __device__ __forceinline__ float fmac_bc(float acc, float kv, float q)
     return acc;
 }
 
+// Query rows come either from global memory (const float *) or from LDS
+// (lds_cfptr, so that the loads are ds_read_b128 rather than flat loads).
+typedef const __attribute__((address_space(3))) float *lds_cfptr;
+
+__device__ __forceinline__ float4 load4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float4 load4(lds_cfptr p)
+{
+    const f32x4_t v = *reinterpret_cast<const __attribute__((address_space(3))) f32x4_t *>(p);
+    return make_float4(v.x, v.y, v.z, v.w);
+}
+
 // Loads of a 4-channel group: this lane's key row and query rows.
-template <int QPL>
-__device__ __forceinline__ void load_group(const float *krow, const float *const (&qrow)[QPL], int c, float4 &k4,
+template <int QPL, class QP>
+__device__ __forceinline__ void load_group(const float *krow, const QP (&qrow)[QPL], int c, float4 &k4,
                                            float4 (&q4)[QPL])
 {
     k4 = *reinterpret_cast<const float4 *>(krow + c);
 #pragma unroll
-    for (int s = 0; s < QPL; ++s) q4[s] = *reinterpret_cast<const float4 *>(qrow[s] + c);
+    for (int s = 0; s < QPL; ++s) q4[s] = load4(qrow[s] + c);
 }
 
 __device__ __forceinline__ float f4_at(const float4 &v, int i)
@@ -67,8 +79,8 @@ __device__ __forceinline__ void emu8_channel(float kv, const float (&q)[QPL], ui
 // k32 is the fp32 key matrix at the chunk's first key ([key][D]); qrow[s] the
 // fp32 pre-scaled query row of slot s.  acc[s][p] receives the codes of keys
 // 2p, 2p+1 in bits [15:0].
-template <int D, int QPL, bool SAT>
-__device__ __forceinline__ void emu8_pass(const float *const (&qrow)[QPL], const float *k32, uint32_t (&acc)[QPL][8])
+template <int D, int QPL, bool SAT, class QP>
+__device__ __forceinline__ void emu8_pass(const QP (&qrow)[QPL], const float *k32, uint32_t (&acc)[QPL][8])
 {
     static_assert(D % 8 == 0, "channels in pairs of 4-channel groups");
 #pragma unroll
@@ -105,8 +117,8 @@ __device__ __forceinline__ void emu8_pass(const float *const (&qrow)[QPL], const
 // The fast pass uses the non-saturating conversion; if any lane of the wave
 // overflowed somewhere (a NaN code at the end of a chain), the chunk is
 // recomputed with the saturating conversion.
-template <int D, int QPL>
-__device__ __forceinline__ void emu8_chunk(const float *const (&qrow)[QPL], const float *k32, uint32_t (&acc)[QPL][8])
+template <int D, int QPL, class QP>
+__device__ __forceinline__ void emu8_chunk(const QP (&qrow)[QPL], const float *k32, uint32_t (&acc)[QPL][8])
 {
     emu8_pass<D, QPL, false>(qrow, k32, acc);
     uint32_t nan = 0;
@@ -134,8 +146,8 @@ __device__ __forceinline__ void rec16_channel(float kv, const float (&q)[QPL], f
 // the e4m11 codes of keys 2p (bits [15:0]) and 2p+1.  With few keys per
 // channel the loop is latency-bound, so the loads run PD 4-channel groups
 // ahead in a ring of buffers written only by loads.
-template <int D, int QPL, int NKEY>
-__device__ __forceinline__ void rec16_keys(const float *const (&qrow)[QPL], const float *krow,
+template <int D, int QPL, int NKEY, class QP>
+__device__ __forceinline__ void rec16_keys(const QP (&qrow)[QPL], const float *krow,
                                            uint32_t (&codes)[QPL][NKEY / 2])
 {
     static_assert(NKEY == 4 || NKEY == 8 || NKEY == 12 || NKEY == 16, "4, 8, 12 or 16 keys");
@@ -180,8 +192,8 @@ __device__ __forceinline__ void rec16_keys(const float *const (&qrow)[QPL], cons
 }
 
 // Y16 of the 16 keys starting at k32 ([key][D] fp32).
-template <int D, int QPL>
-__device__ __forceinline__ void rec16_chunk(const float *const (&qrow)[QPL], const float *k32, uint32_t (&codes)[QPL][8])
+template <int D, int QPL, class QP>
+__device__ __forceinline__ void rec16_chunk(const QP (&qrow)[QPL], const float *k32, uint32_t (&codes)[QPL][8])
 {
     rec16_keys<D, QPL, 16>(qrow, k32 + (size_t)(__lane_id() & 15) * D, codes);
 }

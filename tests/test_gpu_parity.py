@@ -130,14 +130,28 @@ def test_logits8_row_range_and_ragged_rows(L):
 
 
 # ------------------------------------------------------------------ forward
-def _compare_fwd(L, w, tau, delta=None, qblocks=None):
-    delta = w.delta if delta is None else delta
+_INPUTS = {}
+
+
+def _inputs(w, keep=False):
+    """(q, k, v) on the GPU and their bf16 bit patterns on the host; kept for
+    reuse across thresholds when `keep`."""
+    if w.name in _INPUTS:
+        return _INPUTS[w.name]
     q, k, v = W.make_inputs(w)
-    qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
+    r = (q.cuda(), k.cuda(), v.cuda(), O.bf16_bits(q), O.bf16_bits(k), O.bf16_bits(v))
+    if keep:
+        _INPUTS.clear()
+        _INPUTS[w.name] = r
+    return r
+
+
+def _compare_fwd(L, w, tau, delta=None, qblocks=None, keep=False):
+    delta = w.delta if delta is None else delta
+    qd, kd, vd, qb, kb, vb = _inputs(w, keep)
     o, lse, mask = L.attn_fwd(qd, kd, vd, w.causal, w.window, w.bq, w.bk, w.nk, delta, tau)
     torch.cuda.synchronize()
-    ro, rlse, rmask = O.fwd(O.bf16_bits(q), O.bf16_bits(k), O.bf16_bits(v), w.causal, w.window,
-                            w.bq, w.bk, w.nk, delta, tau, qblocks=qblocks)
+    ro, rlse, rmask = O.fwd(qb, kb, vb, w.causal, w.window, w.bq, w.bk, w.nk, delta, tau, qblocks=qblocks)
     o, lse, mask = o.cpu().numpy(), lse.cpu().numpy(), mask.cpu().numpy()
     if qblocks is not None:
         nqb = w.N // w.bq
@@ -207,3 +221,32 @@ def test_fwd_config3_sampled(L):
     qbl = [0 * nqb + nqb - 1, 0 * nqb + 21, 31 * nqb + nqb - 1]
     err, mask = _compare_fwd(L, w, w.tau, qblocks=qbl)
     _say("config 3 sampled: O err %.2e, mask %s" % (err, np.bincount(mask.ravel(), minlength=4)))
+
+
+@pytest.mark.parametrize("cfg", [4, 40])
+def test_fwd_config4_sampled(L, cfg):
+    """Gemma-3-shaped d=256 layers at full size (N=16384): the sliding-window
+    (1024) local layer and the global causal layer; the oracle computes the
+    last query block and an early one of the first and last query head."""
+    w = W.CONFIGS[cfg]
+    nqb = w.N // w.bq
+    qbl = [nqb - 1, 9, (w.Hq - 1) * nqb + nqb - 1, (w.Hq - 1) * nqb + nqb // 2]
+    t0 = time.time()
+    err, mask = _compare_fwd(L, w, w.tau, qblocks=qbl)
+    _say("config %d sampled: O err %.2e, mask %s (%.1f s)" % (cfg, err, np.bincount(mask.ravel(), minlength=4),
+                                                              time.time() - t0))
+
+
+@pytest.mark.parametrize("tau", W.TAU_SWEEP)
+def test_fwd_config5_sampled(L, tau):
+    """Long-context batch (B=4, 32/8 heads, N=32768, Student-t channel scales)
+    at full size for every threshold of the sweep; the oracle computes the
+    last query block of batch 0 head 0 and of batch 3 head 31, and an early
+    block of batch 1 head 7 and batch 2 head 20."""
+    w = W.CONFIGS[5]
+    nqb = w.N // w.bq
+    qbl = [nqb - 1, (3 * w.Hq + 31) * nqb + nqb - 1, (1 * w.Hq + 7) * nqb + 5, (2 * w.Hq + 20) * nqb + nqb // 4]
+    t0 = time.time()
+    err, mask = _compare_fwd(L, w, tau, qblocks=qbl, keep=True)
+    _say("config 5 tau %s sampled: O err %.2e, mask %s (%.1f s)" % (tau, err, np.bincount(mask.ravel(), minlength=4),
+                                                                   time.time() - t0))
