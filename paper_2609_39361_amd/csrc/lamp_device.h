@@ -143,6 +143,16 @@ __device__ __forceinline__ float bf16_value(uint32_t b)
     return __builtin_bit_cast(float, b << 16);
 }
 
+// A ue5m11 exponential (12 significant bits, at least 2^-41) as the exact sum
+// of two bf16 values: hi keeps the top 8 significant bits (the fp32 pattern
+// with its low half cleared), lo = ev - hi holds the remaining 4 and is exact.
+__device__ __forceinline__ void split_bf16(float ev, uint32_t &hi, uint32_t &lo)
+{
+    const uint32_t bits = __builtin_bit_cast(uint32_t, ev);
+    hi = bits >> 16;
+    lo = __builtin_bit_cast(uint32_t, ev - __builtin_bit_cast(float, bits & 0xFFFF0000u)) >> 16;
+}
+
 // --- exp_doc ----------------------------------------------------------------
 // The fp64 exponential of the rescale factor lambda_hat = exp(mu - mu_hat)
 // (Sec. 2.2: alpha_hat in high precision), fixed operation by operation so

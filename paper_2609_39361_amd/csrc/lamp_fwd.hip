@@ -54,10 +54,9 @@ struct Cfg {
     static constexpr int QG = BQ / 32;                     // 32-row MFMA groups
     static constexpr int KPW = BK / NW;                    // keys per wave in a shared 16-bit recompute
     static constexpr int YP = KPT + 8;                     // LDS pitch (u16) of the code rows
-    static constexpr int VP = KPT + 8;                     // LDS pitch (u16) of V^T
     static constexpr size_t OFF_Y = 0;
-    static constexpr size_t OFF_V = OFF_Y + (size_t)BQ * YP * 2;
-    static constexpr size_t OFF_LUT = OFF_V + (size_t)D * VP * 2;
+    static constexpr size_t OFF_YL = OFF_Y + (size_t)BQ * YP * 2;        // low bf16 parts of E16
+    static constexpr size_t OFF_LUT = OFF_YL + (size_t)BQ * YP * 2;
     static constexpr size_t OFF_M8 = OFF_LUT + 512;                       // f32 [NK][BQ]
     static constexpr size_t OFF_CM = OFF_M8 + (size_t)NK * BQ * 4;       // f32 [NK + 2][NW][BQ]
     static constexpr size_t OFF_SP = OFF_CM + (size_t)(NK + 2) * NW * BQ * 4;   // f64 [NW][BQ]
@@ -75,15 +74,16 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
 {
     using C = Cfg<D, BQ, BK, NK>;
     constexpr int QPL = C::QPL, KPT = C::KPT, NCH = C::NCH, NW = C::NW, SPW = C::SPW, CPW = C::CPW;
-    constexpr int CT = C::CT, QG = C::QG, YP = C::YP, VP = C::VP, KPW = C::KPW;
+    constexpr int CT = C::CT, QG = C::QG, YP = C::YP, KPW = C::KPW;
     constexpr int CPS = BK / 16;   // chunks per sub-block
     // Stage-1 recomputes in one batch (4 keys of every sub-block per wave),
     // codes kept in registers; otherwise one shared recompute per failure.
     constexpr bool BATCH = KPW == 4;
 
     extern __shared__ __align__(16) unsigned char smem[];
-    uint16_t *ycode = reinterpret_cast<uint16_t *>(smem + C::OFF_Y);   // [BQ][YP] logit / exp codes
-    uint16_t *vt = reinterpret_cast<uint16_t *>(smem + C::OFF_V);      // [D][VP] V^T of the tile
+    uint16_t *ycode = reinterpret_cast<uint16_t *>(smem + C::OFF_Y);   // [BQ][YP] logit codes, then E (bf16 bits;
+                                                                       // 16-bit sub-blocks: high part)
+    uint16_t *ylo = reinterpret_cast<uint16_t *>(smem + C::OFF_YL);    // [BQ][YP] low bf16 part of E16
     uint16_t *lut = reinterpret_cast<uint16_t *>(smem + C::OFF_LUT);   // [256] 8-bit exp (bf16 bits)
     float *m8s = reinterpret_cast<float *>(smem + C::OFF_M8);          // [NK][BQ] 8-bit column maxima
     float *cms = reinterpret_cast<float *>(smem + C::OFF_CM);          // [NK][NW][BQ] 16-bit column maxima
@@ -120,7 +120,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
     const int t_begin = bv_lo / KPT, t_end = bv_hi / KPT;
 
     const float *kt32 = p.kt32 + ((size_t)b * p.Hkv + hk) * (size_t)p.N * D;   // fp32 keys [N][D]
-    const uint16_t *vbase = p.v + ((size_t)b * p.Hkv + hk) * (size_t)p.N * D;
+    const uint16_t *vtbase = p.vt + ((size_t)b * p.Hkv + hk) * (size_t)D * p.N;   // V^T [D][N]
     uint8_t *mrow = p.mask + (((size_t)b * p.Hq + h) * nqb + qb) * (size_t)(p.N / BK);
 
     for (int i = tid; i < 256; i += 64 * NW) lut[i] = p.lut8e[i];
@@ -163,8 +163,8 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
         }
     };
     // write n = 4, 8 or 16 u16 codes (packed two per word) at row r, key offset ko
-    auto put_codes = [&](int r, int ko, const uint32_t *cw, int nw) {
-        uint16_t *dst = ycode + r * YP + ko;
+    auto put_codes = [&](uint16_t *arr, int r, int ko, const uint32_t *cw, int nw) {
+        uint16_t *dst = arr + r * YP + ko;
         if (nw == 2) {
             *reinterpret_cast<uint2 *>(dst) = make_uint2(cw[0], cw[1]);
         } else {
@@ -175,19 +175,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
 
     for (int tile = t_begin; tile <= t_end; ++tile) {
         const int k0 = tile * KPT;
-        __syncthreads();   // readers of vt / ycode / LDS partials of the previous tile are done
-
-        // ---- V^T of the tile into LDS: vt[c][i] = v[k0 + i][c]
-        for (int e = tid; e < (KPT / 2) * (D / 8); e += 64 * NW) {
-            const int i = 2 * (e % (KPT / 2)), c8 = (e / (KPT / 2)) * 8;
-            const u32x4 r0 = *reinterpret_cast<const u32x4 *>(vbase + (size_t)(k0 + i) * D + c8);
-            const u32x4 r1 = *reinterpret_cast<const u32x4 *>(vbase + (size_t)(k0 + i + 1) * D + c8);
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                *reinterpret_cast<uint32_t *>(vt + (c8 + 2 * t) * VP + i) = (r0[t] & 0xFFFFu) | (r1[t] << 16);
-                *reinterpret_cast<uint32_t *>(vt + (c8 + 2 * t + 1) * VP + i) = (r0[t] >> 16) | (r1[t] & 0xFFFF0000u);
-            }
-        }
+        __syncthreads();   // readers of ycode / ylo / LDS partials of the previous tile are done
 
         // ---- active sub-blocks (a visible pair anywhere in the block), uniform
         uint32_t active = 0;
@@ -242,7 +230,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                 for (int s = 0; s < QPL; ++s) m8s[th * BQ + row[s]] = mx[s];
             }
         }
-        __syncthreads();   // m8s and vt complete
+        __syncthreads();   // m8s complete
 
         // ---- 2. running maximum mu_hat and stage 1
         float muh[QPL];
@@ -467,7 +455,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                                 const float yv = e4m11_value((yc[s][i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
                                 if (visible(s, kc + i)) cm[s] = yv > cm[s] ? yv : cm[s];
                             }
-                            put_codes(row[s], kc - k0, yc[s], NWD);
+                            put_codes(ycode, row[s], kc - k0, yc[s], NWD);
                         }
                     });
 #pragma unroll
@@ -514,39 +502,50 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
 #pragma unroll
                     for (int s = 0; s < QPL; ++s) {
                         u32x4 *rp = reinterpret_cast<u32x4 *>(ycode + row[s] * YP + c16 * 16);
+                        u32x4 *lp = reinterpret_cast<u32x4 *>(ylo + row[s] * YP + c16 * 16);
                         if (ck0 > vhi[s] || ck0 + 15 < vlo[s]) {
                             rp[0] = u32x4{0u, 0u, 0u, 0u};
                             rp[1] = u32x4{0u, 0u, 0u, 0u};
+                            if (hi16) {
+                                lp[0] = u32x4{0u, 0u, 0u, 0u};
+                                lp[1] = u32x4{0u, 0u, 0u, 0u};
+                            }
                             continue;
                         }
                         const u32x4 c0 = rp[0], c1 = rp[1];
                         const uint32_t in[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
-                        uint32_t outw[8];
+                        uint32_t outw[8], outl[8];
 #pragma unroll
                         for (int pp = 0; pp < 8; ++pp) {
-                            uint32_t res = 0;
+                            uint32_t res = 0, rlo = 0;
 #pragma unroll
                             for (int t = 0; t < 2; ++t) {
                                 const int key = ck0 + 2 * pp + t;
                                 const uint32_t yc = (in[pp] >> (16 * t)) & 0xFFFFu;
-                                uint32_t ec = 0;
+                                uint32_t eh = 0, el = 0;
                                 float ev = 0.0f;
                                 if (visible(s, key)) {
                                     if (hi16) {
-                                        ec = p.exp16[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))];
-                                        ev = ue5m11e_value(ec);
+                                        ev = ue5m11e_value(p.exp16[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))]);
+                                        split_bf16(ev, eh, el);
                                     } else {
-                                        ec = lut[ue5m3_code(shift_of(muh[s], e4m3_value(yc)))];
-                                        ev = bf16_value(ec);
+                                        eh = lut[ue5m3_code(shift_of(muh[s], e4m3_value(yc)))];
+                                        ev = bf16_value(eh);
                                     }
                                 }
                                 sp[s] += (double)ev;   // exact: multiples of 2^-41 below 2^9
-                                res |= ec << (16 * t);
+                                res |= eh << (16 * t);
+                                rlo |= el << (16 * t);
                             }
                             outw[pp] = res;
+                            outl[pp] = rlo;
                         }
                         rp[0] = u32x4{outw[0], outw[1], outw[2], outw[3]};
                         rp[1] = u32x4{outw[4], outw[5], outw[6], outw[7]};
+                        if (hi16) {
+                            lp[0] = u32x4{outl[0], outl[1], outl[2], outl[3]};
+                            lp[1] = u32x4{outl[4], outl[5], outl[6], outl[7]};
+                        }
                     }
                 }
             }
@@ -564,26 +563,29 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                     const int key0 = k0 + th * BK + w * 4;
 #pragma unroll
                     for (int s = 0; s < QPL; ++s) {
-                        uint32_t outw[2];
+                        uint32_t outw[2], outl[2];
 #pragma unroll
                         for (int pp = 0; pp < 2; ++pp) {
-                            uint32_t res = 0;
+                            uint32_t res = 0, rlo = 0;
 #pragma unroll
                             for (int t = 0; t < 2; ++t) {
                                 const int key = key0 + 2 * pp + t;
-                                uint32_t ec = 0;
+                                uint32_t eh = 0, el = 0;
                                 float ev = 0.0f;
                                 if (visible(s, key)) {
                                     const uint32_t yc = (y16r[s][2 * g + pp] >> (16 * t)) & 0xFFFFu;
-                                    ec = p.exp16[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))];
-                                    ev = ue5m11e_value(ec);
+                                    ev = ue5m11e_value(p.exp16[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))]);
+                                    split_bf16(ev, eh, el);
                                 }
                                 sp[s] += (double)ev;
-                                res |= ec << (16 * t);
+                                res |= eh << (16 * t);
+                                rlo |= el << (16 * t);
                             }
                             outw[pp] = res;
+                            outl[pp] = rlo;
                         }
                         *reinterpret_cast<uint2 *>(ycode + row[s] * YP + (key0 - k0)) = make_uint2(outw[0], outw[1]);
+                        *reinterpret_cast<uint2 *>(ylo + row[s] * YP + (key0 - k0)) = make_uint2(outl[0], outl[1]);
                     }
                 }
             }
@@ -679,26 +681,30 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
 #pragma unroll
                         for (int s = 0; s < QPL; ++s) {
                             const uint16_t *src = ycode + row[s] * YP + (kc - k0);
-                            uint32_t outw[NWD];
+                            uint32_t outw[NWD], outl[NWD];
 #pragma unroll
                             for (int pp = 0; pp < NWD; ++pp) {
-                                uint32_t res = 0;
+                                uint32_t res = 0, rlo = 0;
 #pragma unroll
                                 for (int t = 0; t < 2; ++t) {
                                     const int key = kc + 2 * pp + t;
-                                    uint32_t ec = 0;
+                                    uint32_t eh = 0, el = 0;
                                     if (visible(s, key)) {
                                         const float old = bf16_value(src[2 * pp + t]);
                                         const float y = e4m11_value((yc[s][pp] >> (16 * t)) & 0xFFFFu);
-                                        ec = p.exp16[ue5m11_code(shift_of(muh[s], y))];
+                                        const float ev = ue5m11e_value(p.exp16[ue5m11_code(shift_of(muh[s], y))]);
+                                        split_bf16(ev, eh, el);
                                         ds[s] = ds[s] - (double)old;
-                                        ds[s] = ds[s] + (double)ue5m11e_value(ec);
+                                        ds[s] = ds[s] + (double)ev;
                                     }
-                                    res |= ec << (16 * t);
+                                    res |= eh << (16 * t);
+                                    rlo |= el << (16 * t);
                                 }
                                 outw[pp] = res;
+                                outl[pp] = rlo;
                             }
-                            put_codes(row[s], kc - k0, outw, NWD);
+                            put_codes(ycode, row[s], kc - k0, outw, NWD);
+                            put_codes(ylo, row[s], kc - k0, outl, NWD);
                         }
                     };
                     for (int th = 0; th < NK; ++th) {
@@ -752,6 +758,39 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                                      : (prec2 >> th & 1u) ? PREC_S2 : PREC_LOW;
         const uint32_t p16 = prec16 | prec2;
         const int half = lane >> 5, l32 = lane & 31;
+        // V^T operands from global memory, one chunk ahead of the matrix-core
+        // work (every chunk's keys lie below N, so the loads stay in bounds
+        // even for chunks without a visible pair, whose products are skipped)
+        auto load_v = [&](int c16, u32x4 (&a)[CT]) {
+#pragma unroll
+            for (int t = 0; t < CT; ++t)
+                a[t] = *reinterpret_cast<const u32x4 *>(vtbase + (size_t)(w * CPW + t * 32 + l32) * p.N + k0 + c16 * 16 +
+                                                        half * 8);
+        };
+        auto pv_chunk = [&](int c16, const u32x4 (&a)[CT]) {
+            const int ck0 = k0 + c16 * 16;
+            const int th = c16 / CPS;
+            if (!(active >> th & 1u) || ck0 > bv_hi || ck0 + 15 < bv_lo) return;
+            const bool hi16 = p16 >> th & 1u;
+#pragma unroll
+            for (int g = 0; g < QG; ++g) {
+                const int off = (g * 32 + l32) * YP + c16 * 16 + half * 8;
+                const bf16x8 bh = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(ycode + off));
+#pragma unroll
+                for (int t = 0; t < CT; ++t)
+                    acc[g][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[t]), bh, acc[g][t],
+                                                                        0, 0, 0);
+                if (hi16) {   // E16 = hi + lo exactly
+                    const bf16x8 bl = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(ylo + off));
+#pragma unroll
+                    for (int t = 0; t < CT; ++t)
+                        acc[g][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[t]), bl,
+                                                                            acc[g][t], 0, 0, 0);
+                }
+            }
+        };
+        u32x4 va[CT], vb[CT];
+        load_v(0, va);
         {
             // lambda_hat of row 32g + l32 lives in lane (32g + l32) % 64, slot (32g + l32) / 64
             float lamf[QPL];
@@ -772,42 +811,12 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                 }
             }
         }
-        for (int c16 = 0; c16 < NCH; ++c16) {
-            const int ck0 = k0 + c16 * 16;
-            const int th = c16 / CPS;
-            if (!(active >> th & 1u) || ck0 > bv_hi || ck0 + 15 < bv_lo) continue;
-            const bool hi16 = p16 >> th & 1u;
-            u32x4 av[CT];
-#pragma unroll
-            for (int t = 0; t < CT; ++t)
-                av[t] = *reinterpret_cast<const u32x4 *>(vt + (w * CPW + t * 32 + l32) * VP + c16 * 16 + half * 8);
-#pragma unroll
-            for (int g = 0; g < QG; ++g) {
-                const u32x4 e = *reinterpret_cast<const u32x4 *>(ycode + (g * 32 + l32) * YP + c16 * 16 + half * 8);
-                if (!hi16) {
-                    const bf16x8 bb = __builtin_bit_cast(bf16x8, e);
-#pragma unroll
-                    for (int t = 0; t < CT; ++t)
-                        acc[g][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av[t]), bb,
-                                                                            acc[g][t], 0, 0, 0);
-                } else {
-                    u32x4 hw, lw;
-#pragma unroll
-                    for (int t = 0; t < 4; ++t) {
-                        const float e0 = ue5m11e_value(e[t] & 0xFFFFu), e1 = ue5m11e_value(e[t] >> 16);
-                        const uint32_t h0 = bf16_bits(e0), h1 = bf16_bits(e1);
-                        hw[t] = h0 | (h1 << 16);
-                        lw[t] = bf16_bits(e0 - bf16_value(h0)) | (bf16_bits(e1 - bf16_value(h1)) << 16);
-                    }
-                    const bf16x8 bh = __builtin_bit_cast(bf16x8, hw), bl = __builtin_bit_cast(bf16x8, lw);
-#pragma unroll
-                    for (int t = 0; t < CT; ++t) {
-                        const bf16x8 a = __builtin_bit_cast(bf16x8, av[t]);
-                        acc[g][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bh, acc[g][t], 0, 0, 0);
-                        acc[g][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bl, acc[g][t], 0, 0, 0);
-                    }
-                }
-            }
+        static_assert(NCH % 2 == 0, "chunks in pairs");
+        for (int c16 = 0; c16 < NCH; c16 += 2) {
+            load_v(c16 + 1, vb);
+            pv_chunk(c16, va);
+            if (c16 + 2 < NCH) load_v(c16 + 2, va);
+            pv_chunk(c16 + 1, vb);
         }
     }
 

@@ -104,17 +104,19 @@ float scale_of(int d)
 struct Workspace {
     float *qt;
     float *kt32;
+    uint16_t *vt;   // only when asked for (the forward pass)
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Grow-only workspace for the pre-scaled Q and the fp32 K (lock held).
-int workspace_locked(int dev, int B, int Hq, int Hkv, int N, int d, Workspace *w)
+// Grow-only workspace for the pre-scaled Q, the fp32 K and (with_vt) the
+// transposed V (lock held).
+int workspace_locked(int dev, int B, int Hq, int Hkv, int N, int d, Workspace *w, bool with_vt = false)
 {
     DeviceState *st = state_of(dev);
     size_t nq = (size_t)B * Hq * N * d, nk = (size_t)B * Hkv * N * d;
-    size_t bq = align256(nq * 4), bk32 = align256(nk * 4);
-    size_t need = bq + bk32;
+    size_t bq = align256(nq * 4), bk32 = align256(nk * 4), bvt = with_vt ? align256(nk * 2) : 0;
+    size_t need = bq + bk32 + bvt;
     if (need > st->ws_bytes) {
         if (st->ws) {
             HIP_TRY(hipDeviceSynchronize());
@@ -128,6 +130,7 @@ int workspace_locked(int dev, int B, int Hq, int Hkv, int N, int d, Workspace *w
     char *base = static_cast<char *>(st->ws);
     w->qt = reinterpret_cast<float *>(base);
     w->kt32 = reinterpret_cast<float *>(base + bq);
+    w->vt = with_vt ? reinterpret_cast<uint16_t *>(base + bq + bk32) : nullptr;
     return LAMP_OK;
 }
 
@@ -218,7 +221,7 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
         std::lock_guard<std::mutex> lk(g_mu);
         rc = init_locked(dev);
         if (rc) return rc;
-        rc = workspace_locked(dev, B, Hq, Hkv, N, d, &w);
+        rc = workspace_locked(dev, B, Hq, Hkv, N, d, &w, true);
         if (rc) return rc;
         DeviceState *st = state_of(dev);
         p.exp16 = st->exp16;
@@ -226,7 +229,7 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
     }
     p.qt = w.qt;
     p.kt32 = w.kt32;
-    p.v = v;
+    p.vt = w.vt;
     p.o = o;
     p.lse = lse;
     p.mask = mask;
@@ -250,6 +253,7 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
         HIP_TRY(hipEventRecord(tc.e[0], s));
     }
     HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, d, scale_of(d), s));
+    HIP_TRY(lamp::launch_transpose_v(v, w.vt, B, Hkv, N, d, s));
     if (timed) HIP_TRY(hipEventRecord(tc.e[1], s));
     bool found = false;
     HIP_TRY(lamp::dispatch_fwd(d, bq, bk, nk, p, s, &found));

@@ -11,7 +11,7 @@ enum { MODE_LAMP = 0, MODE_PURE8 = 1, MODE_ALL16 = 2 };
 struct FwdParams {
     const float *qt;          // [B][Hq][N][D] pre-scaled queries, fp32
     const float *kt32;        // [B][Hkv][N][D] keys, fp32
-    const uint16_t *v;        // [B][Hkv][N][D] bf16
+    const uint16_t *vt;       // [B][Hkv][D][N] bf16, V transposed
     const uint16_t *exp16;    // ue5m11 shift code -> ue5m11 exp code
     const uint16_t *lut8e;    // ue5m3 shift code -> bf16 bits of the ue5m3 exp
     float *o;                 // [B][Hq][N][D]
@@ -32,6 +32,7 @@ struct LogitsParams {
 
 bool fwd_supported(int D, int BQ, int BK, int NK);
 hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found);
+hipError_t launch_transpose_v(const uint16_t *v, uint16_t *vt, int B, int Hkv, int N, int D, hipStream_t s);
 hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float *kt32,
                           int B, int Hq, int Hkv, int N, int D, float scale, hipStream_t s);
 hipError_t launch_logits8(const LogitsParams &p, int D, hipStream_t s);

@@ -32,6 +32,27 @@ __global__ void convert_k_kernel(const uint16_t *__restrict__ k, float *__restri
     for (; i < n; i += stride) k32[i] = bf16_value(k[i]);
 }
 
+// V^T [B*Hkv][D][N] from V [B*Hkv][N][D] (bf16): 64x64 tiles through LDS.
+// grid (N/64, D/64, B*Hkv); N and D are multiples of 64.
+__global__ __launch_bounds__(256) void transpose_v_kernel(const uint16_t *__restrict__ v, uint16_t *__restrict__ vt,
+                                                          int N, int D)
+{
+    __shared__ uint16_t tile[64][66];
+    const size_t bh = blockIdx.z;
+    const int n0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+    const uint16_t *src = v + bh * (size_t)N * D;
+    uint16_t *dst = vt + bh * (size_t)D * N;
+    for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+        const int r = e / 64, c = e % 64;
+        tile[r][c] = src[(size_t)(n0 + r) * D + c0 + c];
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+        const int c = e / 64, r = e % 64;
+        dst[(size_t)(c0 + c) * N + n0 + r] = tile[r][c];
+    }
+}
+
 // ------------------------------------------------------------------ tables
 // Exponential tables: E = RN(exp(-s)) for every shift code s, correctly
 // rounded (Sec. 3.3 LUT exp; Sec. 4.1 exponentials correctly rounded).  exp
@@ -180,6 +201,13 @@ hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float
     unsigned gk = (unsigned)((nk + 255) / 256 < 65536 ? (nk + 255) / 256 : 65536);
     hipLaunchKernelGGL(prescale_q_kernel, dim3(gq), dim3(256), 0, s, q, qt, scale, nq);
     hipLaunchKernelGGL(convert_k_kernel, dim3(gk), dim3(256), 0, s, k, kt32, nk);
+    return hipGetLastError();
+}
+
+hipError_t launch_transpose_v(const uint16_t *v, uint16_t *vt, int B, int Hkv, int N, int D, hipStream_t s)
+{
+    hipLaunchKernelGGL(transpose_v_kernel, dim3((unsigned)(N / 64), (unsigned)(D / 64), (unsigned)(B * Hkv)), dim3(256),
+                       0, s, v, vt, N, D);
     return hipGetLastError();
 }
 
