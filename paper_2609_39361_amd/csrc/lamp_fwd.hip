@@ -59,8 +59,8 @@ struct Cfg {
     static constexpr size_t OFF_LUT = OFF_YL + (size_t)BQ * YP * 2;
     static constexpr size_t OFF_M8 = OFF_LUT + 512;                       // f32 [NK][BQ]
     static constexpr size_t OFF_CM = OFF_M8 + (size_t)NK * BQ * 4;       // f32 [NK + 2][NW][BQ]
-    static constexpr size_t OFF_SP = OFF_CM + (size_t)(NK + 2) * NW * BQ * 4;   // f64 [NW][BQ]
-    static constexpr size_t OFF_CO = OFF_SP + (size_t)NW * BQ * 8;       // f64 [NK][BQ]
+    static constexpr size_t OFF_SP = OFF_CM + (size_t)(NK + 2) * NW * BQ * 4;   // f64 [2][NW][BQ]
+    static constexpr size_t OFF_CO = OFF_SP + (size_t)2 * NW * BQ * 8;   // f64 [NK][BQ]
     static constexpr size_t OFF_ED = OFF_CO + (size_t)NK * BQ * 8;       // f64 [EXPDOC_NK]
     static constexpr size_t LDS = OFF_ED + (size_t)EXPDOC_NK * 8;
     static_assert(BQ == 64 || BQ == 128, "64 or 128 query rows per block");
@@ -88,7 +88,8 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
     float *m8s = reinterpret_cast<float *>(smem + C::OFF_M8);          // [NK][BQ] 8-bit column maxima
     float *cms = reinterpret_cast<float *>(smem + C::OFF_CM);          // [NK][NW][BQ] 16-bit column maxima
     float *cmf = cms + NK * NW * BQ;   // [2][NW][BQ] the same for the one-at-a-time path, by iteration parity
-    double *sps = reinterpret_cast<double *>(smem + C::OFF_SP);        // [NW][BQ] partial row sums
+    double *sps = reinterpret_cast<double *>(smem + C::OFF_SP);        // [NW][BQ] partial row sums of E
+    double *spf = sps + NW * BQ;                                       // [NW][BQ] the same over 8-bit sub-blocks
     double *cst_lds = reinterpret_cast<double *>(smem + C::OFF_CO);    // [NK][BQ] stage-2 costs
     double *edk = reinterpret_cast<double *>(smem + C::OFF_ED);        // exp_doc constants
 
@@ -477,9 +478,9 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
 
         // ---- 3. exponentials of the own sub-blocks against mu_hat
         {
-            double sp[QPL];
+            double sp[QPL], spF[QPL];   // all exponentials / those of 8-bit sub-blocks
 #pragma unroll
-            for (int s = 0; s < QPL; ++s) sp[s] = 0.0;
+            for (int s = 0; s < QPL; ++s) sp[s] = spF[s] = 0.0;
 #pragma unroll
             for (int u = 0; u < SPW; ++u) {
                 const int th = w * SPW + u;
@@ -534,6 +535,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                                     }
                                 }
                                 sp[s] += (double)ev;   // exact: multiples of 2^-41 below 2^9
+                                if (!hi16) spF[s] += (double)ev;
                                 res |= eh << (16 * t);
                                 rlo |= el << (16 * t);
                             }
@@ -590,12 +592,19 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                 }
             }
 #pragma unroll
-            for (int s = 0; s < QPL; ++s) sps[w * BQ + row[s]] = sp[s];
+            for (int s = 0; s < QPL; ++s) {
+                sps[w * BQ + row[s]] = sp[s];
+                spf[w * BQ + row[s]] = spF[s];
+            }
         }
         __syncthreads();
 
         // ---- 4. lambda_hat, omega_hat, stage 2
         double S[QPL], lam[QPL], omh[QPL];
+        bool moved = false;   // exp_doc(0) is exactly 1: skip the exponentials when no maximum moved
+#pragma unroll
+        for (int s = 0; s < QPL; ++s) moved |= muh[s] != mu[s];
+        moved = wave_any(moved);
 #pragma unroll
         for (int s = 0; s < QPL; ++s) {
             double t = 0.0;
@@ -604,13 +613,31 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
             S[s] = t;
             if (muh[s] == NEG_INF) lam[s] = 1.0;
             else if (mu[s] == NEG_INF) lam[s] = 0.0;
-            else lam[s] = exp_doc_k((double)mu[s] - (double)muh[s], [&](int i) { return edk[i]; });
+            else lam[s] = moved ? exp_doc_k((double)mu[s] - (double)muh[s], [&](int i) { return edk[i]; }) : 1.0;
             omh[s] = __builtin_fma(lam[s], om[s], t);
         }
         uint32_t prec2 = 0;
         if (p.mode == MODE_LAMP) {
             const uint32_t F = active & ~prec16;
+            // Quick feasibility of the empty recompute set.  Every cost term
+            // E (omega_hat - E) is at most E omega_hat, so the computed xi_j
+            // stays below omega_hat_j S_F,j (1 + 2^-40) (at most a few hundred
+            // fp64 roundings), S_F,j being the exact mass of the 8-bit
+            // sub-blocks; the computed limit is at least tau omega_hat_j^2
+            // (1 - 2^-52).  S_F,j <= tau omega_hat_j (1 - 2^-38) on every row
+            // therefore implies that the exact test accepts R = {} as well.
+            bool need = false;
             if (F) {
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) {
+                    double sf = 0.0;
+#pragma unroll
+                    for (int ww = 0; ww < NW; ++ww) sf += spf[ww * BQ + row[s]];
+                    need |= !(sf <= (p.tau * omh[s]) * (1.0 - 0x1p-38));
+                }
+                need = wave_any(need);
+            }
+            if (need) {
                 // costs c_theta,j = sum_{i in theta, ascending} E (omega_hat - E)
 #pragma unroll
                 for (int u = 0; u < SPW; ++u) {
