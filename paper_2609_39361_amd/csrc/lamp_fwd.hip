@@ -902,11 +902,12 @@ bool fwd_supported(int D, int BQ, int BK, int NK)
 
 hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found)
 {
+    // 16-key sub-blocks with d >= 128: the kernel pipelined across key tiles
+    if (BK == 16 && NK == 4 && D >= 128) return dispatch_fwd16(D, BQ, p, s, found);
     *found = true;
-    // configurations built: d in {64,128,256}, bq in {64,128}, (bk, nk) in {(16,4), (64,4)}
-#define LAMP_FWD_D(D_)                                                           \
-    LAMP_FWD_CASE(D_, 64, 16, 4) LAMP_FWD_CASE(D_, 128, 16, 4)                     \
-    LAMP_FWD_CASE(D_, 64, 64, 4) LAMP_FWD_CASE(D_, 128, 64, 4)
+    LAMP_FWD_CASE(64, 64, 16, 4)
+    LAMP_FWD_CASE(64, 128, 16, 4)
+#define LAMP_FWD_D(D_) LAMP_FWD_CASE(D_, 64, 64, 4) LAMP_FWD_CASE(D_, 128, 64, 4)
     LAMP_FWD_D(64)
     LAMP_FWD_D(128)
     LAMP_FWD_D(256)

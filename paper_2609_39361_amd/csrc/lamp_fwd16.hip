@@ -1,0 +1,865 @@
+// lamp_fwd16.hip -- the LampAttention forward kernel for 16-key sub-blocks
+// (b_k = 16, N_k = 4, d in {128, 256}), software-pipelined across key tiles.
+//
+// Work split as in the general kernel: one workgroup of 4 waves per (batch,
+// query head, query block of BQ rows); every lane holds QPL = BQ/64 query rows
+// and every wave the running state of all BQ rows; wave w owns sub-block w of
+// every 64-key tile and the output channel slice [w*D/4, (w+1)*D/4).
+//
+// Pipelining.  The 8-bit logits of tile t+1 do not depend on any decision
+// taken in tile t.  Stage 1 of tile t needs the 16-bit logits of the
+// sub-blocks that fail the margin test against the running maximum mu after
+// tile t-1 (the set F0; the test is monotone in mu_hat and mu_hat only grows,
+// so every sub-block stage 1 recomputes is in F0; one that is not takes the
+// one-at-a-time path).  So one fused pass over the channels computes the
+// 16-bit logits of F0(t) (4 keys of each member per wave, codes kept in
+// registers) together with the 8-bit logits of this wave's sub-block of tile
+// t+1 (codes to the other half of a double-buffered LDS array).  Per tile:
+//   A. fused pass: 16-bit logits of F0(t), 8-bit logits of tile t+1;
+//      16-bit column maxima merged with LDS atomic max (exact fixed point:
+//      e4m11 values are multiples of 2^-17 below 2^9);
+//   B. barrier;
+//   C. stage 1 of tile t (Sec. 3.1, Eq. (7)) on the column maxima;
+//   D. exponentials of tile t (8-bit LUT in LDS, 16-bit table in global
+//      memory), 16-bit ones split into exact bf16 high and low parts;
+//   E. barrier; lambda_hat, omega_hat, stage 2 (Eq. (8));
+//   G. state update, P.V on the bf16 matrix cores, F0(t+1);
+//   I. barrier (the code buffer of tile t is reused by tile t+2).
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <climits>
+#include <type_traits>
+
+#include "lamp_device.h"
+#include "lamp_kernels.h"
+#include "lamp_loops.h"
+
+#ifndef LAMP_MIN_WAVES
+#define LAMP_MIN_WAVES 2
+#endif
+
+namespace lamp {
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+enum { PREC_LOW = 0, PREC_S1 = 1, PREC_S2 = 2, PREC_INACTIVE = 3 };
+
+template <int D, int BQ>
+struct Cfg16 {
+    static constexpr int NK = 4, BK = 16, KPT = 64, NW = 4;
+    static constexpr int QPL = BQ / 64;       // query rows per lane
+    static constexpr int CPW = D / NW;        // output channels per wave
+    static constexpr int CT = CPW / 32;       // 32-channel MFMA tiles per wave
+    static constexpr int QG = BQ / 32;        // 32-row MFMA groups
+    static constexpr int YP = KPT + 8;        // LDS pitch (u16) of the code rows
+    static constexpr size_t YB = (size_t)BQ * YP * 2;
+    static constexpr size_t OFF_Y = 0;                                  // u16 [2][BQ][YP]
+    static constexpr size_t OFF_YL = OFF_Y + 2 * YB;                    // u16 [BQ][YP]
+    static constexpr size_t OFF_LUT = OFF_YL + YB;                      // u16 [256]
+    static constexpr size_t OFF_M8 = OFF_LUT + 512;                     // f32 [2][NK][BQ]
+    static constexpr size_t OFF_CMI = OFF_M8 + (size_t)2 * NK * BQ * 4;  // i32 [2][NK][BQ]
+    static constexpr size_t CMF = (size_t)2 * NW * BQ * 4 > (size_t)NK * BQ * 8 ? (size_t)2 * NW * BQ * 4
+                                                                                  : (size_t)NK * BQ * 8;
+    static constexpr size_t OFF_CMF = OFF_CMI + (size_t)2 * NK * BQ * 4;  // f32 [2][NW][BQ] | f64 [NK][BQ]
+    static constexpr size_t OFF_SP = OFF_CMF + CMF;                     // f64 [2][NW][BQ]
+    static constexpr size_t OFF_ED = OFF_SP + (size_t)2 * NW * BQ * 8;  // f64 [EXPDOC_NK]
+    static constexpr size_t LDS = OFF_ED + (size_t)EXPDOC_NK * 8;
+    static_assert(BQ == 64 || BQ == 128, "64 or 128 query rows per block");
+    static_assert(CPW % 32 == 0, "whole 32-channel tiles per wave");
+};
+
+// e4m11 / e4m3 values as exact fixed point in units of 2^-17 (|y| < 2^9).
+__device__ __forceinline__ int fx_of(float y) { return (int)(y * 131072.0f); }
+__device__ __forceinline__ float fx_value(int f) { return (float)f * (1.0f / 131072.0f); }
+
+} // namespace
+
+template <int D, int BQ>
+__global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdParams p)
+{
+    using C = Cfg16<D, BQ>;
+    constexpr int NK = C::NK, BK = C::BK, KPT = C::KPT, NW = C::NW, QPL = C::QPL, CPW = C::CPW;
+    constexpr int CT = C::CT, QG = C::QG, YP = C::YP;
+
+    extern __shared__ __align__(16) unsigned char smem[];
+    uint16_t *ycode2 = reinterpret_cast<uint16_t *>(smem + C::OFF_Y);   // [2][BQ][YP] logit codes, then E
+    uint16_t *ylo = reinterpret_cast<uint16_t *>(smem + C::OFF_YL);     // [BQ][YP] low bf16 part of E16
+    uint16_t *lut = reinterpret_cast<uint16_t *>(smem + C::OFF_LUT);    // [256] 8-bit exp (bf16 bits)
+    float *m8s2 = reinterpret_cast<float *>(smem + C::OFF_M8);          // [2][NK][BQ] 8-bit column maxima
+    int *cmi2 = reinterpret_cast<int *>(smem + C::OFF_CMI);             // [2][NK][BQ] 16-bit column maxima
+    float *cmf = reinterpret_cast<float *>(smem + C::OFF_CMF);          // [2][NW][BQ] one-at-a-time maxima
+    double *cst_lds = reinterpret_cast<double *>(smem + C::OFF_CMF);    // [NK][BQ] stage-2 costs (same space)
+    double *sps = reinterpret_cast<double *>(smem + C::OFF_SP);         // [NW][BQ] partial row sums of E
+    double *spf = sps + NW * BQ;                                        // [NW][BQ] over 8-bit sub-blocks
+    double *edk = reinterpret_cast<double *>(smem + C::OFF_ED);         // exp_doc constants
+
+    const int tid = threadIdx.x;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;   // w is wave-uniform
+    const int nqb = p.N / BQ;
+    const int BH = p.B * p.Hq;
+    const int qb = nqb - 1 - (int)(blockIdx.x / BH);   // longest blocks first under causality
+    const int bh = blockIdx.x % BH;
+    const int b = bh / p.Hq, h = bh % p.Hq;
+    const int hk = h / (p.Hq / p.Hkv);
+    const int q0 = qb * BQ;
+    const float NEG_INF = -__builtin_inff();
+    const int mode = p.mode;
+
+    int row[QPL], vlo[QPL], vhi[QPL];
+    const float *qrow[QPL];
+#pragma unroll
+    for (int s = 0; s < QPL; ++s) {
+        row[s] = s * 64 + lane;
+        const int j = q0 + row[s];
+        vlo[s] = p.window > 0 ? (j - p.window + 1 > 0 ? j - p.window + 1 : 0) : 0;
+        vhi[s] = p.causal ? j : p.N - 1;
+        qrow[s] = p.qt + (((size_t)b * p.Hq + h) * p.N + j) * D;
+    }
+    const int bv_lo = p.window > 0 ? (q0 - p.window + 1 > 0 ? q0 - p.window + 1 : 0) : 0;
+    const int bv_hi = p.causal ? q0 + BQ - 1 : p.N - 1;
+    const int t_begin = bv_lo / KPT, t_end = bv_hi / KPT;   // every tile in between has a visible pair
+
+    const float *kt32 = p.kt32 + ((size_t)b * p.Hkv + hk) * (size_t)p.N * D;       // fp32 keys [N][D]
+    const uint16_t *vtbase = p.vt + ((size_t)b * p.Hkv + hk) * (size_t)D * p.N;    // V^T [D][N]
+    uint8_t *mrow = p.mask + (((size_t)b * p.Hq + h) * nqb + qb) * (size_t)(p.N / BK);
+
+    for (int i = tid; i < 256; i += 256) lut[i] = p.lut8e[i];
+    if (tid < EXPDOC_NK) edk[tid] = EXPDOC_K[tid];
+    for (int i = tid; i < 2 * NK * BQ; i += 256) cmi2[i] = INT_MIN;
+
+    float mu[QPL];
+    double om[QPL];
+#pragma unroll
+    for (int s = 0; s < QPL; ++s) {
+        mu[s] = NEG_INF;
+        om[s] = 0.0;
+    }
+    floatx16 acc[QG][CT];
+#pragma unroll
+    for (int g = 0; g < QG; ++g)
+#pragma unroll
+        for (int t = 0; t < CT; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[g][t][r] = 0.0f;
+
+    auto visible = [&](int s, int key) { return key >= vlo[s] && key <= vhi[s]; };
+    auto ycode_of = [&](int tile) { return ycode2 + (size_t)(tile & 1) * BQ * YP; };
+    auto m8s_of = [&](int tile) { return m8s2 + (size_t)(tile & 1) * NK * BQ; };
+    auto cmi_of = [&](int tile) { return cmi2 + (size_t)(tile & 1) * NK * BQ; };
+
+    // active sub-blocks of a tile (a visible pair anywhere in the block), uniform
+    auto active_of = [&](int tile) {
+        uint32_t a = 0;
+#pragma unroll
+        for (int th = 0; th < NK; ++th) {
+            const int k = tile * KPT + th * BK, z = k + BK - 1;
+            bool any = false;
+#pragma unroll
+            for (int s = 0; s < QPL; ++s) any |= (k <= vhi[s] && z >= vlo[s]);
+            if (wave_any(any)) a |= 1u << th;
+        }
+        return a;
+    };
+    // does this wave's sub-block of `tile` have a visible pair (then it is emulated)?
+    auto own_emulated = [&](int tile, uint32_t act) {
+        const int ck0 = tile * KPT + w * BK;
+        return (act >> w & 1u) && !(ck0 > bv_hi || ck0 + 15 < bv_lo);
+    };
+    // 8-bit codes of this wave's sub-block of `tile` into its code buffer, the
+    // column maxima over visible keys into m8s (NEG_INF for a sub-block that
+    // was not emulated)
+    auto emit8 = [&](int tile, const uint32_t (&a8)[QPL][8], bool done) {
+        const int ck0 = tile * KPT + w * BK;
+        uint16_t *yc = ycode_of(tile);
+        float *m8s = m8s_of(tile);
+#pragma unroll
+        for (int s = 0; s < QPL; ++s) {
+            float mx = NEG_INF;
+            if (done) {
+                const bool full = ck0 >= vlo[s] && ck0 + 15 <= vhi[s];
+                uint32_t packed[8];
+#pragma unroll
+                for (int pp = 0; pp < 8; ++pp) {
+                    const float2 yv = unpk_e4m3(a8[s][pp]);
+                    const int i0 = ck0 + 2 * pp;
+                    if (full || visible(s, i0)) mx = yv.x > mx ? yv.x : mx;
+                    if (full || visible(s, i0 + 1)) mx = yv.y > mx ? yv.y : mx;
+                    packed[pp] = (a8[s][pp] & 0xFFu) | ((a8[s][pp] & 0xFF00u) << 8);
+                }
+                u32x4 *dst = reinterpret_cast<u32x4 *>(yc + row[s] * YP + w * BK);
+                dst[0] = u32x4{packed[0], packed[1], packed[2], packed[3]};
+                dst[1] = u32x4{packed[4], packed[5], packed[6], packed[7]};
+            }
+            m8s[w * BQ + row[s]] = mx;
+        }
+    };
+    // the margin test of every sub-block of `tile` against mu_hat (Eq. (7)):
+    // mu_hat_j > fma(|mu_hat_j|, delta, m8); columns without a visible entry
+    // are not tested; mu_hat = -inf fails.  m8 from LDS, identical in every wave.
+    auto fails_of = [&](const float (&m8)[NK][QPL], const float (&mh)[QPL]) {
+        uint32_t f = 0;
+#pragma unroll
+        for (int th = 0; th < NK; ++th) {
+            bool bad = false;
+#pragma unroll
+            for (int s = 0; s < QPL; ++s)
+                if (m8[th][s] > NEG_INF) {
+                    const double m = (double)mh[s];
+                    bad |= !(m > __builtin_fma(__builtin_fabs(m), p.delta, (double)m8[th][s]));
+                }
+            if (wave_any(bad)) f |= 1u << th;
+        }
+        return f;
+    };
+    auto load_m8 = [&](int tile, float (&m8)[NK][QPL]) {
+        const float *m8s = m8s_of(tile);
+#pragma unroll
+        for (int th = 0; th < NK; ++th)
+#pragma unroll
+            for (int s = 0; s < QPL; ++s) m8[th][s] = m8s[th * BQ + row[s]];
+    };
+    // the set of sub-blocks whose 16-bit logits the next fused pass computes
+    auto f0_of = [&](int tile, uint32_t act) -> uint32_t {
+        if (mode == MODE_ALL16) return act;
+        if (mode == MODE_PURE8) return 0u;
+        float m8[NK][QPL];
+        load_m8(tile, m8);
+        return fails_of(m8, mu);
+    };
+    // one-at-a-time 16-bit recompute of sub-block th of the tile at k0 shared
+    // by all waves (4 keys each); fn(key0, codes[QPL][2]) receives the codes
+    auto shared16 = [&](int k0, int th, auto fn) {
+        const int key0 = k0 + th * BK + w * 4;
+        if (key0 > bv_hi || key0 + 3 < bv_lo) return;   // nothing visible in the block
+        uint32_t yc[QPL][2];
+        rec16_keys<D, QPL, 4>(qrow, kt32 + (size_t)(key0 + (lane & 3)) * D, yc);
+        fn(key0, yc);
+    };
+
+    // ---- prologue: 8-bit logits of the first tile, its F0
+    int t = t_begin;
+    uint32_t act = active_of(t);
+    if (mode != MODE_ALL16) {
+        const bool done = own_emulated(t, act);
+        uint32_t a8[QPL][8];
+        if (done) emu8_chunk<D, QPL>(qrow, kt32 + (size_t)(t * KPT + w * BK) * D, a8);
+        emit8(t, a8, done);
+    }
+    __syncthreads();
+    uint32_t F0 = f0_of(t, act);
+
+    for (; t <= t_end; ++t) {
+        const int k0 = t * KPT;
+        const bool has_next = t < t_end;
+        const uint32_t act_next = has_next ? active_of(t + 1) : 0u;
+        uint16_t *ycode = ycode_of(t);
+
+        // ---- A. fused pass: 16-bit logits of F0 (4 keys of each member per
+        // wave), 8-bit logits of this wave's sub-block of the next tile
+        uint32_t y16r[QPL][8];   // codes of keys th*16 + w*4 + {0..3} of the g-th member of F0, 2 per word
+        {
+            const int nf = __builtin_popcount(F0);
+            const int kk = nf ? (lane & 15) % (4 * nf) : 0;
+            int thg = 0;
+            if (nf) {
+                uint32_t m = F0;
+                for (int g = 0; g < kk / 4; ++g) m &= m - 1;
+                thg = __builtin_ctz(m);
+            }
+            const float *krowr = kt32 + (size_t)(k0 + thg * BK + w * 4 + (kk & 3)) * D;
+            const bool emu = mode != MODE_ALL16 && has_next && own_emulated(t + 1, act_next);
+            const float *k32e = kt32 + (size_t)(k0 + KPT + w * BK) * D;   // read only when emu (then below N)
+            uint32_t a8[QPL][8];
+            auto run = [&](auto nkey_c, auto emu_c) {
+                constexpr int NKEY = decltype(nkey_c)::value;
+                constexpr bool EMU = decltype(emu_c)::value;
+                uint32_t c[QPL][NKEY > 0 ? NKEY / 2 : 1];
+                fused_pass<D, QPL, NKEY, EMU>(qrow, k32e, krowr, a8, c);
+                if constexpr (NKEY > 0)
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                        for (int pp = 0; pp < NKEY / 2; ++pp) y16r[s][pp] = c[s][pp];
+            };
+            using T_ = std::true_type;
+            using F_ = std::false_type;
+            using std::integral_constant;
+            if (emu) {
+                switch (nf) {
+                case 0: run(integral_constant<int, 0>(), T_()); break;
+                case 1: run(integral_constant<int, 4>(), T_()); break;
+                case 2: run(integral_constant<int, 8>(), T_()); break;
+                case 3: run(integral_constant<int, 12>(), T_()); break;
+                default: run(integral_constant<int, 16>(), T_()); break;
+                }
+            } else {
+                switch (nf) {
+                case 0: break;
+                case 1: run(integral_constant<int, 4>(), F_()); break;
+                case 2: run(integral_constant<int, 8>(), F_()); break;
+                case 3: run(integral_constant<int, 12>(), F_()); break;
+                default: run(integral_constant<int, 16>(), F_()); break;
+                }
+            }
+            if (has_next && mode != MODE_ALL16) emit8(t + 1, a8, emu);
+            // 16-bit column maxima over this wave's 4 keys of every member of F0
+            int *cmi = cmi_of(t);
+            uint32_t m = F0;
+#pragma unroll
+            for (int g = 0; g < NK; ++g) {
+                if (!m) break;
+                const int th = __builtin_ctz(m);
+                m &= m - 1;
+                const int key0 = k0 + th * BK + w * 4;
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) {
+                    int cm = INT_MIN;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const uint32_t word = y16r[s][2 * g + (i >> 1)];
+                        const int f = fx_of(e4m11_value((word >> (16 * (i & 1))) & 0xFFFFu));
+                        if (visible(s, key0 + i)) cm = f > cm ? f : cm;
+                    }
+                    if (cm != INT_MIN) atomicMax(&cmi[th * BQ + row[s]], cm);
+                }
+            }
+        }
+        __syncthreads();   // B: codes, m8 of the next tile and the 16-bit maxima are complete
+
+        // ---- C. running maximum mu_hat and stage 1 of tile t
+        float muh[QPL];
+#pragma unroll
+        for (int s = 0; s < QPL; ++s) muh[s] = mu[s];
+        uint32_t prec16 = 0;   // stage-1 (or threshold-0) sub-blocks
+        float cm16[NK][QPL];   // 16-bit column maxima of the members of F0
+        {
+            const int *cmi = cmi_of(t);
+#pragma unroll
+            for (int th = 0; th < NK; ++th)
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) {
+                    const int f = (F0 >> th & 1u) ? cmi[th * BQ + row[s]] : INT_MIN;
+                    cm16[th][s] = f == INT_MIN ? NEG_INF : fx_value(f);
+                }
+        }
+        if (mode == MODE_PURE8) {
+            float m8[NK][QPL];
+            load_m8(t, m8);
+#pragma unroll
+            for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                for (int th = 0; th < NK; ++th) muh[s] = m8[th][s] > muh[s] ? m8[th][s] : muh[s];
+        } else if (mode == MODE_ALL16) {
+            prec16 = act;
+#pragma unroll
+            for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                for (int th = 0; th < NK; ++th) muh[s] = cm16[th][s] > muh[s] ? cm16[th][s] : muh[s];
+        } else {
+            float m8[NK][QPL];
+            load_m8(t, m8);
+            // threats T_theta = max_j (m8 - mu_j), exact in fp64 (+inf when mu_j = -inf)
+            double T[NK];
+#pragma unroll
+            for (int th = 0; th < NK; ++th) {
+                double tv = -__builtin_inf();
+#pragma unroll
+                for (int s = 0; s < QPL; ++s)
+                    if (m8[th][s] > NEG_INF) {
+                        const double d = (double)m8[th][s] - (double)mu[s];
+                        tv = d > tv ? d : tv;
+                    }
+                T[th] = wave_max_f64(tv);
+            }
+            // descending threat, ties by index; order packed 4 bits per rank
+            uint32_t order = 0, taken = 0;
+            int na = 0;
+#pragma unroll
+            for (int r = 0; r < NK; ++r) {
+                int best = -1;
+                double bt = 0.0;
+#pragma unroll
+                for (int th = 0; th < NK; ++th) {
+                    const bool cand = (act >> th & 1u) && !(taken >> th & 1u);
+                    if (cand && (best < 0 || T[th] > bt)) {
+                        best = th;
+                        bt = T[th];
+                    }
+                }
+                if (best >= 0) {
+                    order |= (uint32_t)best << (4 * na);
+                    ++na;
+                    taken |= 1u << best;
+                }
+            }
+            uint32_t fail = F0;   // the test against mu_hat = mu
+            int pos = 0, par = 0;
+            while (true) {
+                while (pos < na && !(fail >> ((order >> (4 * pos)) & 15u) & 1u)) ++pos;
+                if (pos >= na) break;
+                const int th = (int)((order >> (4 * pos)) & 15u);
+                ++pos;
+                prec16 |= 1u << th;
+                if (F0 >> th & 1u) {
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) {
+                        float c = muh[s];
+#pragma unroll
+                        for (int t2 = 0; t2 < NK; ++t2)
+                            if (t2 == th) c = cm16[t2][s] > c ? cm16[t2][s] : c;
+                        muh[s] = c;
+                    }
+                } else {
+                    // outside F0 (not expected, see above): all waves recompute
+                    // the sub-block in 16 bits, codes in place of the 8-bit ones
+                    float cm[QPL];
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) cm[s] = NEG_INF;
+                    shared16(k0, th, [&](int kc, const uint32_t (&yc)[QPL][2]) {
+#pragma unroll
+                        for (int s = 0; s < QPL; ++s) {
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) {
+                                const float yv = e4m11_value((yc[s][i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
+                                if (visible(s, kc + i)) cm[s] = yv > cm[s] ? yv : cm[s];
+                            }
+                            *reinterpret_cast<uint2 *>(ycode + row[s] * YP + (kc - k0)) = make_uint2(yc[s][0], yc[s][1]);
+                        }
+                    });
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) cmf[(par * NW + w) * BQ + row[s]] = cm[s];
+                    __syncthreads();
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                        for (int ww = 0; ww < NW; ++ww) {
+                            const float c = cmf[(par * NW + ww) * BQ + row[s]];
+                            muh[s] = c > muh[s] ? c : muh[s];
+                        }
+                    par ^= 1;   // the next write goes to the other half: readers of this one may lag
+                }
+                if (pos < na) fail = fails_of(m8, muh);
+            }
+        }
+
+        // ---- D. exponentials of tile t against mu_hat
+        {
+            // the 16-bit maxima buffer of tile t+1 was last read in tile t-1
+            int *cmn = cmi_of(t + 1);
+            for (int i = tid; i < NK * BQ; i += 256) cmn[i] = INT_MIN;
+
+            double sp[QPL], spF[QPL];   // all exponentials / those of 8-bit sub-blocks
+#pragma unroll
+            for (int s = 0; s < QPL; ++s) sp[s] = spF[s] = 0.0;
+            const int th = w;   // own sub-block
+            const int ck0 = k0 + th * BK;
+            if (!(act >> th & 1u)) {
+                // inactive: zero exponentials so the P.V pass may read them
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) {
+                    u32x4 *d = reinterpret_cast<u32x4 *>(ycode + row[s] * YP + th * BK);
+                    d[0] = u32x4{0u, 0u, 0u, 0u};
+                    d[1] = u32x4{0u, 0u, 0u, 0u};
+                }
+            } else if (!((prec16 & F0) >> th & 1u)) {   // else from registers by every wave, below
+                const bool hi16 = prec16 >> th & 1u;      // one-at-a-time 16-bit codes in place
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) {
+                    u32x4 *rp = reinterpret_cast<u32x4 *>(ycode + row[s] * YP + th * BK);
+                    u32x4 *lp = reinterpret_cast<u32x4 *>(ylo + row[s] * YP + th * BK);
+                    if (ck0 > vhi[s] || ck0 + 15 < vlo[s]) {
+                        rp[0] = u32x4{0u, 0u, 0u, 0u};
+                        rp[1] = u32x4{0u, 0u, 0u, 0u};
+                        if (hi16) {
+                            lp[0] = u32x4{0u, 0u, 0u, 0u};
+                            lp[1] = u32x4{0u, 0u, 0u, 0u};
+                        }
+                        continue;
+                    }
+                    const u32x4 c0 = rp[0], c1 = rp[1];
+                    const uint32_t in[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
+                    uint32_t outw[8], outl[8];
+#pragma unroll
+                    for (int pp = 0; pp < 8; ++pp) {
+                        uint32_t res = 0, rlo = 0;
+#pragma unroll
+                        for (int t2 = 0; t2 < 2; ++t2) {
+                            const int key = ck0 + 2 * pp + t2;
+                            const uint32_t yc = (in[pp] >> (16 * t2)) & 0xFFFFu;
+                            uint32_t eh = 0, el = 0;
+                            float ev = 0.0f;
+                            if (visible(s, key)) {
+                                if (hi16) {
+                                    ev = ue5m11e_value(p.exp16[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))]);
+                                    split_bf16(ev, eh, el);
+                                } else {
+                                    eh = lut[ue5m3_code(shift_of(muh[s], e4m3_value(yc)))];
+                                    ev = bf16_value(eh);
+                                }
+                            }
+                            sp[s] += (double)ev;   // exact: multiples of 2^-41 below 2^9
+                            if (!hi16) spF[s] += (double)ev;
+                            res |= eh << (16 * t2);
+                            rlo |= el << (16 * t2);
+                        }
+                        outw[pp] = res;
+                        outl[pp] = rlo;
+                    }
+                    rp[0] = u32x4{outw[0], outw[1], outw[2], outw[3]};
+                    rp[1] = u32x4{outw[4], outw[5], outw[6], outw[7]};
+                    if (hi16) {
+                        lp[0] = u32x4{outl[0], outl[1], outl[2], outl[3]};
+                        lp[1] = u32x4{outl[4], outl[5], outl[6], outl[7]};
+                    }
+                }
+            }
+            // 16-bit exponentials of this wave's 4 keys of every stage-1
+            // sub-block of F0, from the codes held in registers
+            {
+                const uint32_t mine = prec16 & F0;
+                uint32_t m = F0;
+#pragma unroll
+                for (int g = 0; g < NK; ++g) {
+                    if (!m) break;
+                    const int tg = __builtin_ctz(m);
+                    m &= m - 1;
+                    if (!(mine >> tg & 1u)) continue;
+                    const int key0 = k0 + tg * BK + w * 4;
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) {
+                        uint32_t outw[2], outl[2];
+#pragma unroll
+                        for (int pp = 0; pp < 2; ++pp) {
+                            uint32_t res = 0, rlo = 0;
+#pragma unroll
+                            for (int t2 = 0; t2 < 2; ++t2) {
+                                const int key = key0 + 2 * pp + t2;
+                                uint32_t eh = 0, el = 0;
+                                float ev = 0.0f;
+                                if (visible(s, key)) {
+                                    const uint32_t yc = (y16r[s][2 * g + pp] >> (16 * t2)) & 0xFFFFu;
+                                    ev = ue5m11e_value(p.exp16[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))]);
+                                    split_bf16(ev, eh, el);
+                                }
+                                sp[s] += (double)ev;
+                                res |= eh << (16 * t2);
+                                rlo |= el << (16 * t2);
+                            }
+                            outw[pp] = res;
+                            outl[pp] = rlo;
+                        }
+                        *reinterpret_cast<uint2 *>(ycode + row[s] * YP + (key0 - k0)) = make_uint2(outw[0], outw[1]);
+                        *reinterpret_cast<uint2 *>(ylo + row[s] * YP + (key0 - k0)) = make_uint2(outl[0], outl[1]);
+                    }
+                }
+            }
+#pragma unroll
+            for (int s = 0; s < QPL; ++s) {
+                sps[w * BQ + row[s]] = sp[s];
+                spf[w * BQ + row[s]] = spF[s];
+            }
+        }
+        __syncthreads();   // E
+
+        // ---- lambda_hat, omega_hat, stage 2
+        double S[QPL], lam[QPL], omh[QPL];
+        bool moved = false;   // exp_doc(0) is exactly 1: skip the exponentials when no maximum moved
+#pragma unroll
+        for (int s = 0; s < QPL; ++s) moved |= muh[s] != mu[s];
+        moved = wave_any(moved);
+#pragma unroll
+        for (int s = 0; s < QPL; ++s) {
+            double tt = 0.0;
+#pragma unroll
+            for (int ww = 0; ww < NW; ++ww) tt += sps[ww * BQ + row[s]];
+            S[s] = tt;
+            if (muh[s] == NEG_INF) lam[s] = 1.0;
+            else if (mu[s] == NEG_INF) lam[s] = 0.0;
+            else lam[s] = moved ? exp_doc_k((double)mu[s] - (double)muh[s], [&](int i) { return edk[i]; }) : 1.0;
+            omh[s] = __builtin_fma(lam[s], om[s], tt);
+        }
+        uint32_t prec2 = 0;
+        if (mode == MODE_LAMP) {
+            const uint32_t F = act & ~prec16;
+            // Quick feasibility of the empty recompute set.  Every cost term
+            // E (omega_hat - E) is at most E omega_hat, so the computed xi_j
+            // stays below omega_hat_j S_F,j (1 + 2^-40) (at most a few hundred
+            // fp64 roundings), S_F,j being the exact mass of the 8-bit
+            // sub-blocks; the computed limit is at least tau omega_hat_j^2
+            // (1 - 2^-52).  S_F,j <= tau omega_hat_j (1 - 2^-38) on every row
+            // therefore implies that the exact test accepts R = {} as well.
+            bool need = false;
+            if (F) {
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) {
+                    double sf = 0.0;
+#pragma unroll
+                    for (int ww = 0; ww < NW; ++ww) sf += spf[ww * BQ + row[s]];
+                    need |= !(sf <= (p.tau * omh[s]) * (1.0 - 0x1p-38));
+                }
+                need = wave_any(need);
+            }
+            if (need) {
+                // costs c_theta,j = sum_{i in theta, ascending} E (omega_hat - E), own sub-block
+                if (F >> w & 1u) {
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) {
+                        const u32x4 *rp = reinterpret_cast<const u32x4 *>(ycode + row[s] * YP + w * BK);
+                        const u32x4 c0 = rp[0], c1 = rp[1];
+                        const uint32_t in[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
+                        double cth = 0.0;
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            const double e = (double)bf16_value((in[i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
+                            const double tt = omh[s] - e;
+                            const double pr = e * tt;
+                            cth = cth + pr;   // invisible entries hold E = 0 and add +0
+                        }
+                        cst_lds[w * BQ + row[s]] = cth;
+                    }
+                }
+                __syncthreads();
+                // feasibility of every recompute set R within F, identical in every wave
+                double cst[NK][QPL], lim[QPL];
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) {
+                    lim[s] = (p.tau * omh[s]) * omh[s];
+#pragma unroll
+                    for (int th = 0; th < NK; ++th) cst[th][s] = (F >> th & 1u) ? cst_lds[th * BQ + row[s]] : 0.0;
+                }
+                uint32_t feas = 0;
+                for (int R = 0; R < (1 << NK); ++R) {
+                    if (R & ~(int)F) continue;
+                    bool bad = false;
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) {
+                        double xi = 0.0;
+#pragma unroll
+                        for (int th = 0; th < NK; ++th)
+                            if ((F >> th & 1u) && !(R >> th & 1)) xi = xi + cst[th][s];
+                        bad |= !(xi <= lim[s]);
+                    }
+                    if (!wave_any(bad)) feas |= 1u << R;
+                }
+                // smallest recompute set first, then ascending bitmask
+                int chosen = (int)F;
+                bool found = false;
+                for (int sz = 0; sz <= NK && !found; ++sz)
+                    for (int R = 0; R < (1 << NK) && !found; ++R) {
+                        if ((R & ~(int)F) || __builtin_popcount(R) != sz) continue;
+                        if (feas >> R & 1u) {
+                            chosen = R;
+                            found = true;
+                        }
+                    }
+                prec2 = (uint32_t)chosen;
+                if (prec2) {
+                    // stage-2 recompute shared by all waves (4 keys each): 16-bit
+                    // logits and exponentials against the unchanged mu_hat
+                    double ds[QPL];
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) ds[s] = 0.0;
+                    auto s2fn = [&](int kc, const uint32_t (&yc)[QPL][2]) {
+#pragma unroll
+                        for (int s = 0; s < QPL; ++s) {
+                            const uint16_t *src = ycode + row[s] * YP + (kc - k0);
+                            uint32_t outw[2], outl[2];
+#pragma unroll
+                            for (int pp = 0; pp < 2; ++pp) {
+                                uint32_t res = 0, rlo = 0;
+#pragma unroll
+                                for (int t2 = 0; t2 < 2; ++t2) {
+                                    const int key = kc + 2 * pp + t2;
+                                    uint32_t eh = 0, el = 0;
+                                    if (visible(s, key)) {
+                                        const float old = bf16_value(src[2 * pp + t2]);
+                                        const float y = e4m11_value((yc[s][pp] >> (16 * t2)) & 0xFFFFu);
+                                        const float ev = ue5m11e_value(p.exp16[ue5m11_code(shift_of(muh[s], y))]);
+                                        split_bf16(ev, eh, el);
+                                        ds[s] = ds[s] - (double)old;
+                                        ds[s] = ds[s] + (double)ev;
+                                    }
+                                    res |= eh << (16 * t2);
+                                    rlo |= el << (16 * t2);
+                                }
+                                outw[pp] = res;
+                                outl[pp] = rlo;
+                            }
+                            *reinterpret_cast<uint2 *>(ycode + row[s] * YP + (kc - k0)) = make_uint2(outw[0], outw[1]);
+                            *reinterpret_cast<uint2 *>(ylo + row[s] * YP + (kc - k0)) = make_uint2(outl[0], outl[1]);
+                        }
+                    };
+                    for (int th = 0; th < NK; ++th) {
+                        if (!(prec2 >> th & 1u)) continue;
+                        if (F0 >> th & 1u) {
+                            // the codes of this wave's keys are already in registers
+                            const int gi = __builtin_popcount(F0 & ((1u << th) - 1u));
+                            uint32_t yc[QPL][2];
+#pragma unroll
+                            for (int s = 0; s < QPL; ++s) {
+                                yc[s][0] = y16r[s][0];
+                                yc[s][1] = y16r[s][1];
+#pragma unroll
+                                for (int g = 1; g < NK; ++g)
+                                    if (g == gi) {
+                                        yc[s][0] = y16r[s][2 * g];
+                                        yc[s][1] = y16r[s][2 * g + 1];
+                                    }
+                            }
+                            s2fn(k0 + th * BK + w * 4, yc);
+                        } else {
+                            shared16(k0, th, s2fn);
+                        }
+                    }
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) sps[w * BQ + row[s]] = ds[s];
+                    __syncthreads();
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) {
+                        double tt = S[s];
+#pragma unroll
+                        for (int ww = 0; ww < NW; ++ww) tt += sps[ww * BQ + row[s]];   // exact
+                        S[s] = tt;
+                    }
+                }
+            }
+        }
+
+        // ---- G. state update; O^T <- O^T diag(lambda_hat) + V^T E; next F0
+#pragma unroll
+        for (int s = 0; s < QPL; ++s) {
+            om[s] = __builtin_fma(lam[s], om[s], S[s]);
+            mu[s] = muh[s];
+        }
+        if (tid == 0)
+#pragma unroll
+            for (int th = 0; th < NK; ++th)
+                mrow[t * NK + th] = !(act >> th & 1u) ? PREC_INACTIVE
+                                  : (prec16 >> th & 1u) ? PREC_S1
+                                  : (prec2 >> th & 1u) ? PREC_S2 : PREC_LOW;
+        const uint32_t p16 = prec16 | prec2;
+        const int half = lane >> 5, l32 = lane & 31;
+        // V^T operands from global memory, one chunk ahead of the matrix-core
+        // work (every chunk's keys lie below N, so the loads stay in bounds)
+        auto load_v = [&](int c16, u32x4 (&a)[CT]) {
+#pragma unroll
+            for (int tt = 0; tt < CT; ++tt)
+                a[tt] = *reinterpret_cast<const u32x4 *>(vtbase + (size_t)(w * CPW + tt * 32 + l32) * p.N + k0 +
+                                                         c16 * 16 + half * 8);
+        };
+        auto pv_chunk = [&](int c16, const u32x4 (&a)[CT]) {
+            const int ck0 = k0 + c16 * 16;
+            if (!(act >> c16 & 1u) || ck0 > bv_hi || ck0 + 15 < bv_lo) return;
+            const bool hi16 = p16 >> c16 & 1u;
+#pragma unroll
+            for (int g = 0; g < QG; ++g) {
+                const int off = (g * 32 + l32) * YP + c16 * 16 + half * 8;
+                const bf16x8 bh = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(ycode + off));
+#pragma unroll
+                for (int tt = 0; tt < CT; ++tt)
+                    acc[g][tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[tt]), bh,
+                                                                         acc[g][tt], 0, 0, 0);
+                if (hi16) {   // E16 = hi + lo exactly
+                    const bf16x8 bl = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(ylo + off));
+#pragma unroll
+                    for (int tt = 0; tt < CT; ++tt)
+                        acc[g][tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[tt]), bl,
+                                                                             acc[g][tt], 0, 0, 0);
+                }
+            }
+        };
+        u32x4 va[CT], vb[CT];
+        load_v(0, va);
+        {
+            // lambda_hat of row 32g + l32 lives in lane (32g + l32) % 64, slot (32g + l32) / 64
+            float lamf[QPL];
+            bool scale = false;
+#pragma unroll
+            for (int s = 0; s < QPL; ++s) {
+                lamf[s] = (float)lam[s];
+                scale |= lamf[s] != 1.0f;
+            }
+            if (wave_any(scale)) {
+#pragma unroll
+                for (int g = 0; g < QG; ++g) {
+                    const float lg = __shfl(lamf[g / 2 < QPL ? g / 2 : 0], ((g & 1) << 5) + l32, 64);
+#pragma unroll
+                    for (int tt = 0; tt < CT; ++tt)
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) acc[g][tt][r] *= lg;
+                }
+            }
+        }
+        load_v(1, vb);
+        pv_chunk(0, va);
+        load_v(2, va);
+        pv_chunk(1, vb);
+        load_v(3, vb);
+        pv_chunk(2, va);
+        pv_chunk(3, vb);
+
+        F0 = has_next ? f0_of(t + 1, act_next) : 0u;
+        act = act_next;
+        __syncthreads();   // I: this tile's code buffer is rewritten by the pass of tile t+1
+    }
+
+    // ---- epilogue: O / omega, lse = mu + ln(omega), mask bytes of skipped tiles
+    {
+        const int half = lane >> 5, l32 = lane & 31;
+#pragma unroll
+        for (int g = 0; g < QG; ++g) {
+            const double og = __shfl(om[g / 2 < QPL ? g / 2 : 0], ((g & 1) << 5) + l32, 64);
+            const float inv = (float)(1.0 / og);
+            const int jq = q0 + g * 32 + l32;
+            float *orow = p.o + (((size_t)b * p.Hq + h) * p.N + jq) * D + w * CPW;
+#pragma unroll
+            for (int tt = 0; tt < CT; ++tt)
+#pragma unroll
+                for (int r4 = 0; r4 < 4; ++r4) {
+                    const int c = tt * 32 + r4 * 8 + half * 4;
+                    const float4 v4 = make_float4(acc[g][tt][r4 * 4 + 0] * inv, acc[g][tt][r4 * 4 + 1] * inv,
+                                                  acc[g][tt][r4 * 4 + 2] * inv, acc[g][tt][r4 * 4 + 3] * inv);
+                    *reinterpret_cast<float4 *>(orow + c) = v4;
+                }
+        }
+        if (w == 0)
+#pragma unroll
+            for (int s = 0; s < QPL; ++s)
+                p.lse[((size_t)b * p.Hq + h) * p.N + q0 + row[s]] = (float)((double)mu[s] + ::log(om[s]));
+        const int ntiles = p.N / KPT;
+        for (int tt = tid; tt < ntiles; tt += 256)
+            if (tt < t_begin || tt > t_end)
+                for (int th = 0; th < NK; ++th) mrow[tt * NK + th] = PREC_INACTIVE;
+    }
+}
+
+// ------------------------------------------------------------------ launcher
+template <int D, int BQ>
+static hipError_t launch_fwd16(const FwdParams &p, hipStream_t s)
+{
+    using C = Cfg16<D, BQ>;
+    auto kern = lamp_fwd16_kernel<D, BQ>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
+    if (e != hipSuccess) return e;
+    dim3 grid((unsigned)(p.B * p.Hq * (p.N / BQ)));
+    hipLaunchKernelGGL(kern, grid, dim3(256), C::LDS, s, p);
+    return hipGetLastError();
+}
+
+hipError_t dispatch_fwd16(int D, int BQ, const FwdParams &p, hipStream_t s, bool *found)
+{
+    *found = true;
+    if (D == 128 && BQ == 64) return launch_fwd16<128, 64>(p, s);
+    if (D == 128 && BQ == 128) return launch_fwd16<128, 128>(p, s);
+    if (D == 256 && BQ == 64) return launch_fwd16<256, 64>(p, s);
+    if (D == 256 && BQ == 128) return launch_fwd16<256, 128>(p, s);
+    *found = false;
+    return hipSuccess;
+}
+
+} // namespace lamp

@@ -31,6 +31,7 @@ struct LogitsParams {
 };
 
 bool fwd_supported(int D, int BQ, int BK, int NK);
+hipError_t dispatch_fwd16(int D, int BQ, const FwdParams &p, hipStream_t s, bool *found);
 hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found);
 hipError_t launch_transpose_v(const uint16_t *v, uint16_t *vt, int B, int Hkv, int N, int D, hipStream_t s);
 hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float *kt32,

@@ -132,6 +132,83 @@ __device__ __forceinline__ void emu8_chunk(const QP (&qrow)[QPL], const float *k
 // One channel of the 16-bit accumulation for every key and slot.
 template <int QPL, int NKEY, int... I>
 __device__ __forceinline__ void rec16_channel(float kv, const float (&q)[QPL], float (&acc)[QPL][NKEY],
+                                              std::integer_sequence<int, I...>);
+
+// Two passes over the channels fused into one loop that shares the query
+// loads: the 8-bit accumulation of the 16 keys at k32e (EMU; as emu8_pass,
+// without saturation, then checked as in emu8_chunk) and the 16-bit
+// accumulation of NKEY keys, this lane's key row being krowr (as rec16_keys).
+// The forward kernel uses it to run the 8-bit logits of the next key tile
+// together with the speculative 16-bit recompute of the current one.
+template <int D, int QPL, int NKEY, bool EMU, class QP>
+__device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k32e, const float *krowr,
+                                           uint32_t (&a8)[QPL][8], uint32_t (&c16)[QPL][NKEY > 0 ? NKEY / 2 : 1])
+{
+    static_assert(EMU || NKEY > 0, "something to compute");
+    static_assert(NKEY == 0 || NKEY == 4 || NKEY == 8 || NKEY == 12 || NKEY == 16, "0, 4, 8, 12 or 16 keys");
+    static_assert(D % 8 == 0, "channels in pairs of 4-channel groups");
+    constexpr int NA = NKEY > 0 ? NKEY : 1;
+    float acc[QPL][NA];
+#pragma unroll
+    for (int s = 0; s < QPL; ++s) {
+#pragma unroll
+        for (int p = 0; p < 8; ++p) a8[s][p] = 0u;
+#pragma unroll
+        for (int i = 0; i < NA; ++i) acc[s][i] = 0.0f;
+    }
+    const float *krowe = k32e + (size_t)(__lane_id() & 15) * D;
+    float4 kea, keb, kra, krb, qa[QPL], qb[QPL];
+    auto ld = [&](int c, float4 &ke, float4 &kr, float4 (&q4)[QPL]) {
+        if constexpr (EMU) ke = load4(krowe + c);
+        if constexpr (NKEY > 0) kr = load4(krowr + c);
+#pragma unroll
+        for (int s = 0; s < QPL; ++s) q4[s] = load4(qrow[s] + c);
+    };
+    auto run = [&](const float4 &ke, const float4 &kr, const float4 (&q4)[QPL]) {
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) {
+            float q[QPL];
+#pragma unroll
+            for (int s = 0; s < QPL; ++s) q[s] = f4_at(q4[s], cc);
+            if constexpr (EMU) emu8_channel<QPL, false>(f4_at(ke, cc), q, a8, std::make_integer_sequence<int, 8>());
+            if constexpr (NKEY > 0)
+                rec16_channel<QPL, NKEY>(f4_at(kr, cc), q, acc, std::make_integer_sequence<int, NKEY>());
+        }
+    };
+    ld(0, kea, kra, qa);
+    for (int c = 0; c < D - 8; c += 8) {
+        ld(c + 4, keb, krb, qb);
+        run(kea, kra, qa);
+        ld(c + 8, kea, kra, qa);
+        run(keb, krb, qb);
+    }
+    ld(D - 4, keb, krb, qb);
+    run(kea, kra, qa);
+    run(keb, krb, qb);
+    if constexpr (EMU) {
+        uint32_t nan = 0;
+#pragma unroll
+        for (int s = 0; s < QPL; ++s)
+#pragma unroll
+            for (int p = 0; p < 8; ++p) nan |= e4m3_nan_bits(a8[s][p]);
+        if (wave_any(nan != 0)) emu8_pass<D, QPL, true>(qrow, k32e, a8);
+    }
+    if constexpr (NKEY > 0) {
+#pragma unroll
+        for (int s = 0; s < QPL; ++s)
+#pragma unroll
+            for (int p = 0; p < NKEY / 2; ++p) {
+                uint32_t x0, x1;
+                (void)rn_e4m11((double)acc[s][2 * p], &x0);
+                (void)rn_e4m11((double)acc[s][2 * p + 1], &x1);
+                c16[s][p] = x0 | (x1 << 16);
+            }
+    }
+}
+
+// One channel of the 16-bit accumulation for every key and slot.
+template <int QPL, int NKEY, int... I>
+__device__ __forceinline__ void rec16_channel(float kv, const float (&q)[QPL], float (&acc)[QPL][NKEY],
                                               std::integer_sequence<int, I...>)
 {
 #pragma unroll
