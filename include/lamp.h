@@ -131,10 +131,15 @@ void lamp_shutdown(void);
  * lamp_get_tables: copies the device exponential tables to HOST memory:
  * lut8[256] (ue5m3 shift code -> ue5m3 exp code) and exp16[65536] (ue5m11
  * shift code -> ue5m11 exp code); either pointer may be NULL.
+ * lamp_get_exp16_parts: copies to HOST memory parts[65536], the same 16-bit
+ * exponentials as exact bf16 pairs (bits of the high part in [15:0], of the
+ * low part in [31:16]; high = the fp32 value with its low 16 bits cleared,
+ * low = value - high), the form the forward pass feeds to the matrix cores.
  */
 int lamp_selftest_e4m3(const float *in, uint8_t *out, uint8_t *raw, size_t n, void *stream);
 int lamp_selftest_exp_doc(const double *x, double *y, size_t n, void *stream);
 int lamp_get_tables(int device, uint8_t *lut8, uint16_t *exp16);
+int lamp_get_exp16_parts(int device, uint32_t *parts);
 
 const char *lamp_status_str(int status);
 const char *lamp_last_error(void);

@@ -20,8 +20,8 @@
 //      e4m11 values are multiples of 2^-17 below 2^9);
 //   B. barrier;
 //   C. stage 1 of tile t (Sec. 3.1, Eq. (7)) on the column maxima;
-//   D. exponentials of tile t (8-bit LUT in LDS, 16-bit table in global
-//      memory), 16-bit ones split into exact bf16 high and low parts;
+//   D. exponentials of tile t (8-bit LUT in LDS, 16-bit table of exact bf16
+//      high and low parts in global memory);
 //   E. barrier; lambda_hat, omega_hat, stage 2 (Eq. (8));
 //   G. state update, P.V on the bf16 matrix cores, F0(t+1);
 //   I. barrier (the code buffer of tile t is reused by tile t+2).
@@ -494,8 +494,10 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                             float ev = 0.0f;
                             if (visible(s, key)) {
                                 if (hi16) {
-                                    ev = ue5m11e_value(p.exp16[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))]);
-                                    split_bf16(ev, eh, el);
+                                    const uint32_t hl = p.exp16hl[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))];
+                                    eh = hl & 0xFFFFu;
+                                    el = hl >> 16;
+                                    ev = bf16_value(eh) + bf16_value(el);   // exact
                                 } else {
                                     eh = lut[ue5m3_code(shift_of(muh[s], e4m3_value(yc)))];
                                     ev = bf16_value(eh);
@@ -542,8 +544,10 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                                 float ev = 0.0f;
                                 if (visible(s, key)) {
                                     const uint32_t yc = (y16r[s][2 * g + pp] >> (16 * t2)) & 0xFFFFu;
-                                    ev = ue5m11e_value(p.exp16[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))]);
-                                    split_bf16(ev, eh, el);
+                                    const uint32_t hl = p.exp16hl[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))];
+                                    eh = hl & 0xFFFFu;
+                                    el = hl >> 16;
+                                    ev = bf16_value(eh) + bf16_value(el);   // exact
                                 }
                                 sp[s] += (double)ev;
                                 res |= eh << (16 * t2);
@@ -678,8 +682,10 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                                     if (visible(s, key)) {
                                         const float old = bf16_value(src[2 * pp + t2]);
                                         const float y = e4m11_value((yc[s][pp] >> (16 * t2)) & 0xFFFFu);
-                                        const float ev = ue5m11e_value(p.exp16[ue5m11_code(shift_of(muh[s], y))]);
-                                        split_bf16(ev, eh, el);
+                                        const uint32_t hl = p.exp16hl[ue5m11_code(shift_of(muh[s], y))];
+                                        eh = hl & 0xFFFFu;
+                                        el = hl >> 16;
+                                        const float ev = bf16_value(eh) + bf16_value(el);   // exact
                                         ds[s] = ds[s] - (double)old;
                                         ds[s] = ds[s] + (double)ev;
                                     }

@@ -36,6 +36,7 @@ struct DeviceState {
     uint8_t *lut8 = nullptr;
     uint16_t *lut8e = nullptr;
     uint16_t *exp16 = nullptr;
+    uint32_t *exp16hl = nullptr;
     void *ws = nullptr;
     size_t ws_bytes = 0;
 };
@@ -67,10 +68,11 @@ int init_locked(int dev)
     HIP_TRY(hipMalloc(&st->lut8, 256));
     HIP_TRY(hipMalloc(&st->lut8e, 256 * sizeof(uint16_t)));
     HIP_TRY(hipMalloc(&st->exp16, 65536 * sizeof(uint16_t)));
+    HIP_TRY(hipMalloc(&st->exp16hl, 65536 * sizeof(uint32_t)));
     unsigned *amb = nullptr;
     HIP_TRY(hipMalloc(&amb, sizeof(unsigned)));
     HIP_TRY(hipMemset(amb, 0, sizeof(unsigned)));
-    HIP_TRY(lamp::launch_build_tables(st->lut8, st->lut8e, st->exp16, amb, nullptr));
+    HIP_TRY(lamp::launch_build_tables(st->lut8, st->lut8e, st->exp16, st->exp16hl, amb, nullptr));
     unsigned h_amb = 0;
     HIP_TRY(hipMemcpy(&h_amb, amb, sizeof(unsigned), hipMemcpyDeviceToHost));
     HIP_TRY(hipFree(amb));
@@ -191,6 +193,7 @@ void lamp_shutdown(void)
         (void)hipFree(st.lut8);
         (void)hipFree(st.lut8e);
         (void)hipFree(st.exp16);
+        (void)hipFree(st.exp16hl);
         (void)hipFree(st.ws);
         st = DeviceState();
     }
@@ -225,6 +228,7 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
         if (rc) return rc;
         DeviceState *st = state_of(dev);
         p.exp16 = st->exp16;
+        p.exp16hl = st->exp16hl;
         p.lut8e = st->lut8e;
     }
     p.qt = w.qt;
@@ -388,6 +392,20 @@ int lamp_get_tables(int device, uint8_t *lut8, uint16_t *exp16)
     DeviceState *st = state_of(device);
     if (lut8) HIP_TRY(hipMemcpy(lut8, st->lut8, 256, hipMemcpyDeviceToHost));
     if (exp16) HIP_TRY(hipMemcpy(exp16, st->exp16, 65536 * sizeof(uint16_t), hipMemcpyDeviceToHost));
+    HIP_TRY(hipSetDevice(prev));
+    return LAMP_OK;
+}
+
+int lamp_get_exp16_parts(int device, uint32_t *parts)
+{
+    if (!parts) return fail(LAMP_ERR_INVALID_ARG, "null pointer");
+    int rc = lamp_init(device);
+    if (rc) return rc;
+    std::lock_guard<std::mutex> lk(g_mu);
+    int prev = 0;
+    HIP_TRY(hipGetDevice(&prev));
+    HIP_TRY(hipSetDevice(device));
+    HIP_TRY(hipMemcpy(parts, state_of(device)->exp16hl, 65536 * sizeof(uint32_t), hipMemcpyDeviceToHost));
     HIP_TRY(hipSetDevice(prev));
     return LAMP_OK;
 }

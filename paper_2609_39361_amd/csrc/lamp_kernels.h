@@ -13,6 +13,7 @@ struct FwdParams {
     const float *kt32;        // [B][Hkv][N][D] keys, fp32
     const uint16_t *vt;       // [B][Hkv][D][N] bf16, V transposed
     const uint16_t *exp16;    // ue5m11 shift code -> ue5m11 exp code
+    const uint32_t *exp16hl;  // ue5m11 shift code -> bf16 high | low << 16 of the ue5m11 exp
     const uint16_t *lut8e;    // ue5m3 shift code -> bf16 bits of the ue5m3 exp
     float *o;                 // [B][Hq][N][D]
     float *lse;               // [B][Hq][N]
@@ -38,8 +39,8 @@ hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float
                           int B, int Hq, int Hkv, int N, int D, float scale, hipStream_t s);
 hipError_t launch_logits8(const LogitsParams &p, int D, hipStream_t s);
 hipError_t launch_logits16(const LogitsParams &p, int D, hipStream_t s);
-hipError_t launch_build_tables(uint8_t *lut8, uint16_t *lut8e, uint16_t *exp16, unsigned *ambiguous,
-                               hipStream_t s);
+hipError_t launch_build_tables(uint8_t *lut8, uint16_t *lut8e, uint16_t *exp16, uint32_t *exp16hl, unsigned *ambiguous,
+                              hipStream_t s);
 hipError_t launch_selftest_e4m3(const float *in, uint8_t *out, uint8_t *raw, size_t n, hipStream_t s);
 hipError_t launch_selftest_exp_doc(const double *x, double *y, size_t n, hipStream_t s);
 

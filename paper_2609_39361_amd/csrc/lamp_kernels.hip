@@ -84,7 +84,8 @@ __device__ __forceinline__ double grid_value(uint32_t c, int mbits, int bias)
 }
 
 __global__ void build_tables_kernel(uint8_t *__restrict__ lut8, uint16_t *__restrict__ lut8e,
-                                    uint16_t *__restrict__ exp16, unsigned *__restrict__ ambiguous)
+                                    uint16_t *__restrict__ exp16, uint32_t *__restrict__ exp16hl,
+                                    unsigned *__restrict__ ambiguous)
 {
     unsigned c = blockIdx.x * blockDim.x + threadIdx.x;
     if (c >= 65536u + 256u) return;
@@ -102,6 +103,9 @@ __global__ void build_tables_kernel(uint8_t *__restrict__ lut8, uint16_t *__rest
         lut8e[code] = (uint16_t)bf16_bits((float)r);   // E8 is exact in bf16
     } else {
         exp16[code] = (uint16_t)e;
+        uint32_t eh, el;   // the same value as exact bf16 high and low parts, for P.V
+        split_bf16((float)r, eh, el);
+        exp16hl[code] = eh | (el << 16);
     }
 }
 
@@ -237,10 +241,11 @@ hipError_t launch_logits16(const LogitsParams &p, int D, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t launch_build_tables(uint8_t *lut8, uint16_t *lut8e, uint16_t *exp16, unsigned *ambiguous, hipStream_t s)
+hipError_t launch_build_tables(uint8_t *lut8, uint16_t *lut8e, uint16_t *exp16, uint32_t *exp16hl, unsigned *ambiguous,
+                              hipStream_t s)
 {
     hipLaunchKernelGGL(build_tables_kernel, dim3((65536 + 256 + 255) / 256), dim3(256), 0, s, lut8, lut8e, exp16,
-                       ambiguous);
+                       exp16hl, ambiguous);
     return hipGetLastError();
 }
 

@@ -51,6 +51,8 @@ def lib():
         L.lamp_selftest_exp_doc.restype = i32
         L.lamp_get_tables.argtypes = [i32, P, P]
         L.lamp_get_tables.restype = i32
+        L.lamp_get_exp16_parts.argtypes = [i32, P]
+        L.lamp_get_exp16_parts.restype = i32
         L.lamp_timing_enable.argtypes = [i32]
         L.lamp_timing_enable.restype = i32
         L.lamp_timing_read.argtypes = [P, P, P]
@@ -161,6 +163,15 @@ def get_tables(device=0):
     _check(lib().lamp_get_tables(int(device), lut8.ctypes.data_as(ctypes.c_void_p),
                                  exp16.ctypes.data_as(ctypes.c_void_p)))
     return lut8, exp16
+
+
+def get_exp16_parts(device=0):
+    """uint32[65536]: the 16-bit exponentials as bf16 high (bits 15:0) and low
+    (bits 31:16) parts."""
+    import numpy as np
+    parts = np.zeros(65536, dtype=np.uint32)
+    _check(lib().lamp_get_exp16_parts(int(device), parts.ctypes.data_as(ctypes.c_void_p)))
+    return parts
 
 
 def init(device=0):

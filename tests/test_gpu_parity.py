@@ -83,6 +83,19 @@ def test_tables_match_oracle(L):
     assert np.array_equal(exp16, oexp16)
 
 
+def test_exp16_parts_sum_to_table(L):
+    """The bf16 high/low pairs the forward pass reads sum exactly to the
+    oracle's 16-bit exponentials; the high part is the truncated value."""
+    _, oexp16 = O.tables()
+    parts = L.get_exp16_parts(0)
+    hi = ((parts & 0xFFFF) << 16).view(np.float32).astype(np.float64)
+    lo = ((parts >> 16) << 16).view(np.float32).astype(np.float64)
+    ref = O.decode_fmt(O.UE5M11_EXP, oexp16.astype(np.uint32))
+    assert np.array_equal(hi + lo, ref)
+    ref32 = ref.astype(np.float32).view(np.uint32)
+    assert np.array_equal((parts & 0xFFFF), ref32 >> 16)
+
+
 def test_exp_doc_bitexact(L):
     rng = np.random.default_rng(5)
     x = np.concatenate([-rng.uniform(0, 720, 500_000), -rng.uniform(0, 2, 200_000),
