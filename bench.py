@@ -32,8 +32,9 @@ OPS_PER_MAC8 = 2.0
 OPS_PER_MAC16 = 1.0
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lamp_fwd_kernel.qwen3-8b-prefill-8k.hbm_traffic.md")
-KERNEL_SOURCES = ["lamp_fwd.hip", "lamp_loops.h", "lamp_device.h", "lamp_kernels.h"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lamp_fwd16_kernel.qwen3-8b-prefill-8k.hbm_traffic.md")
+VALU_FILE = os.path.join(ROOT, "profiles", "lamp_fwd16_kernel.qwen3-8b-prefill-8k.valu_issue.md")
+KERNEL_SOURCES = ["lamp_fwd.hip", "lamp_fwd16.hip", "lamp_loops.h", "lamp_device.h", "lamp_kernels.h"]
 
 
 def kernel_source_hash():
@@ -45,21 +46,34 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
-def measured_traffic(workload, tau):
-    """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE runs,
-    or None when they were taken on other kernel sources or another workload."""
+def _profile_record(path, tag, workload, tau):
+    """The `tag: {json}` line of a committed profile summary, when it was taken
+    on the current kernel sources and on this workload; else None."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             text = f.read()
     except OSError:
         return None
     for line in text.splitlines():
-        if line.startswith("traffic-json: "):
-            rec = json.loads(line[len("traffic-json: "):])
+        if line.startswith(tag + ": "):
+            rec = json.loads(line[len(tag) + 2:])
             if rec.get("source_sha256") == kernel_source_hash() and rec.get("workload") == workload \
                     and rec.get("tau") == tau:
-                return rec["bytes_per_launch"]
+                return rec
     return None
+
+
+def measured_traffic(workload, tau):
+    """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE runs."""
+    rec = _profile_record(TRAFFIC_FILE, "traffic-json", workload, tau)
+    return None if rec is None else rec["bytes_per_launch"]
+
+
+def measured_valu_issue(workload, tau):
+    """SQ_INSTS_VALU over the launch's VALU issue capacity, from the committed
+    counter run."""
+    rec = _profile_record(VALU_FILE, "valu-json", workload, tau)
+    return None if rec is None else rec["valu_issue_fraction"]
 
 
 def visible_in_mask(w, mask):
@@ -218,12 +232,14 @@ def main():
             "unit": "T VALU lane-ops/s",
             "frac": achieved / peak,
             "traffic": measured_traffic(w.name, tau),
-            "kernel": "lamp_fwd_kernel",
+            "kernel": ("lamp_fwd16_kernel<%d,%d>" % (w.d, w.bq)) if (w.bk == 16 and w.d >= 128)
+                      else ("lamp_fwd_kernel<%d,%d,%d,%d>" % (w.d, w.bq, w.bk, w.nk)),
             "kernel_ms": kernel_ms,
             "prepass_ms": pre_ms_sum / launches,
             "ops_per_launch": alg_ops,
             "ops_per_unit": "2 per emulated 8-bit MAC, 1 per 16-bit recompute MAC",
             "algorithmic_frac_one_op_per_mac": (mac8 + mac16) / (kernel_ms * 1e-3) / VALU_LANE_OPS,
+            "valu_issue_frac_counters": measured_valu_issue(w.name, tau),
         },
         "wall_s_timed_region": wall,
     }

@@ -1,4 +1,6 @@
-// lamp_fwd.hip -- the LampAttention forward kernel for gfx950 (paper Alg. 1).
+// lamp_fwd.hip -- the LampAttention forward kernel for gfx950 (paper Alg. 1),
+// general form: d = 64, or 64-key sub-blocks.  (16-key sub-blocks with d >=
+// 128 take the tile-pipelined kernel of lamp_fwd16.hip.)
 //
 // One workgroup handles one (batch, query head, query block of BQ rows) and
 // walks its key tiles (KPT = BK*NK keys) in order.  Work split:
@@ -7,21 +9,22 @@
 //     state is small and every wave derives it from the same shared data, so
 //     it stays identical across waves without extra traffic;
 //   * wave w owns SPW = NK/NW consecutive key sub-blocks of each tile: it
-//     computes their 8-bit logits, their 16-bit recomputes and their
-//     exponentials, and publishes per-row partial results in LDS;
+//     computes their 8-bit logits and exponentials and publishes per-row
+//     partial results in LDS;
 //   * wave w owns the channel slice [w*CPW, (w+1)*CPW) of the output and
 //     accumulates O^T = V^T E for that slice on the bf16 matrix cores.
 // Per tile (Alg. 1 inner loop):
 //   1. 8-bit logits of the own sub-blocks, column maxima m8 -> LDS;
 //   2. stage 1 (Sec. 3.1, Eq. (7)): threats, sort, sequential margin tests on
-//      the shared m8; a failing sub-block is recomputed in 16 bits by its
-//      owner and raises mu_hat;
+//      the shared m8; a failing sub-block is recomputed in 16 bits by all
+//      waves (KPW keys each) and raises mu_hat;
 //   3. exponentials of the own sub-blocks against mu_hat (8-bit LUT in LDS,
-//      16-bit table in global memory), written in place of the logit codes;
-//      partial row sums -> LDS; lambda_hat, omega_hat;
+//      16-bit table in global memory), written in place of the logit codes,
+//      16-bit ones as exact bf16 high and low parts; partial row sums -> LDS;
+//      lambda_hat, omega_hat;
 //   4. stage 2 (Eq. (8)): per-sub-block costs -> LDS, feasibility of every
 //      candidate recompute set evaluated identically by every wave, 16-bit
-//      recompute of the chosen sub-blocks by their owners;
+//      recompute of the chosen sub-blocks shared by all waves;
 //   5. omega, mu update; O^T <- O^T diag(lambda_hat) + V^T E.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -58,8 +61,8 @@ struct Cfg {
     static constexpr size_t OFF_YL = OFF_Y + (size_t)BQ * YP * 2;        // low bf16 parts of E16
     static constexpr size_t OFF_LUT = OFF_YL + (size_t)BQ * YP * 2;
     static constexpr size_t OFF_M8 = OFF_LUT + 512;                       // f32 [NK][BQ]
-    static constexpr size_t OFF_CM = OFF_M8 + (size_t)NK * BQ * 4;       // f32 [NK + 2][NW][BQ]
-    static constexpr size_t OFF_SP = OFF_CM + (size_t)(NK + 2) * NW * BQ * 4;   // f64 [2][NW][BQ]
+    static constexpr size_t OFF_CM = OFF_M8 + (size_t)NK * BQ * 4;       // f32 [NK][BQ] + [2][NW][BQ]
+    static constexpr size_t OFF_SP = OFF_CM + (size_t)(NK + 2 * NW) * BQ * 4;   // f64 [2][NW][BQ]
     static constexpr size_t OFF_CO = OFF_SP + (size_t)2 * NW * BQ * 8;   // f64 [NK][BQ]
     static constexpr size_t OFF_ED = OFF_CO + (size_t)NK * BQ * 8;       // f64 [EXPDOC_NK]
     static constexpr size_t LDS = OFF_ED + (size_t)EXPDOC_NK * 8;
@@ -76,9 +79,6 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
     constexpr int QPL = C::QPL, KPT = C::KPT, NCH = C::NCH, NW = C::NW, SPW = C::SPW, CPW = C::CPW;
     constexpr int CT = C::CT, QG = C::QG, YP = C::YP, KPW = C::KPW;
     constexpr int CPS = BK / 16;   // chunks per sub-block
-    // Stage-1 recomputes in one batch (4 keys of every sub-block per wave),
-    // codes kept in registers; otherwise one shared recompute per failure.
-    constexpr bool BATCH = KPW == 4;
 
     extern __shared__ __align__(16) unsigned char smem[];
     uint16_t *ycode = reinterpret_cast<uint16_t *>(smem + C::OFF_Y);   // [BQ][YP] logit codes, then E (bf16 bits;
@@ -86,8 +86,8 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
     uint16_t *ylo = reinterpret_cast<uint16_t *>(smem + C::OFF_YL);    // [BQ][YP] low bf16 part of E16
     uint16_t *lut = reinterpret_cast<uint16_t *>(smem + C::OFF_LUT);   // [256] 8-bit exp (bf16 bits)
     float *m8s = reinterpret_cast<float *>(smem + C::OFF_M8);          // [NK][BQ] 8-bit column maxima
-    float *cms = reinterpret_cast<float *>(smem + C::OFF_CM);          // [NK][NW][BQ] 16-bit column maxima
-    float *cmf = cms + NK * NW * BQ;   // [2][NW][BQ] the same for the one-at-a-time path, by iteration parity
+    float *cms = reinterpret_cast<float *>(smem + C::OFF_CM);          // [NK][BQ] 16-bit column maxima (threshold 0)
+    float *cmf = cms + NK * BQ;   // [2][NW][BQ] per-wave maxima of a shared recompute, by iteration parity
     double *sps = reinterpret_cast<double *>(smem + C::OFF_SP);        // [NW][BQ] partial row sums of E
     double *spf = sps + NW * BQ;                                       // [NW][BQ] the same over 8-bit sub-blocks
     double *cst_lds = reinterpret_cast<double *>(smem + C::OFF_CO);    // [NK][BQ] stage-2 costs
@@ -243,8 +243,6 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
             for (int th = 0; th < NK; ++th) m8[th][s] = (p.mode != MODE_ALL16) ? m8s[th * BQ + row[s]] : NEG_INF;
         }
         uint32_t prec16 = 0;   // stage-1 (or threshold-0) sub-blocks
-        uint32_t F0 = 0;       // sub-blocks whose 16-bit codes this wave holds in y16r (batched stage 1)
-        uint32_t y16r[QPL][8]; // e4m11 codes of keys th*BK + w*4 + {0..3} of the members of F0, 2 per word
         if (p.mode == MODE_PURE8) {
 #pragma unroll
             for (int s = 0; s < QPL; ++s)
@@ -343,87 +341,6 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                 return f;
             };
             uint32_t fail = fails();
-            float cm16[NK][QPL];   // batched: 16-bit column maxima of the members of F0
-            if constexpr (BATCH) if (fail) {   // fail is identical in every wave: the barrier below is uniform
-                // Speculation: the margin test is monotone in mu_hat and mu_hat
-                // only grows, so every sub-block that stage 1 will recompute
-                // fails against mu already.  Recompute all of those at once,
-                // 4 keys of each per wave; the sequential test below then needs
-                // only their column maxima.  A sub-block outside this set that
-                // still fails takes the one-at-a-time path.
-                F0 = fail;
-                const int nf = __builtin_popcount(F0);
-                // lane key slot kk = lane%16 mod 4nf: member g = kk/4, key w*4 + kk%4 of it
-                const int kk = (lane & 15) % (4 * nf);
-                int thg = 0;
-                {
-                    uint32_t m = F0;
-                    for (int g = 0; g < kk / 4; ++g) m &= m - 1;
-                    thg = __builtin_ctz(m);
-                }
-                const float *krow = kt32 + (size_t)(k0 + thg * BK + w * 4 + (kk & 3)) * D;
-                if (nf == 1) {
-                    uint32_t c[QPL][2];
-                    rec16_keys<D, QPL, 4>(qrow, krow, c);
-#pragma unroll
-                    for (int s = 0; s < QPL; ++s)
-#pragma unroll
-                        for (int pp = 0; pp < 2; ++pp) y16r[s][pp] = c[s][pp];
-                } else if (nf == 2) {
-                    uint32_t c[QPL][4];
-                    rec16_keys<D, QPL, 8>(qrow, krow, c);
-#pragma unroll
-                    for (int s = 0; s < QPL; ++s)
-#pragma unroll
-                        for (int pp = 0; pp < 4; ++pp) y16r[s][pp] = c[s][pp];
-                } else if (nf == 3) {
-                    uint32_t c[QPL][6];
-                    rec16_keys<D, QPL, 12>(qrow, krow, c);
-#pragma unroll
-                    for (int s = 0; s < QPL; ++s)
-#pragma unroll
-                        for (int pp = 0; pp < 6; ++pp) y16r[s][pp] = c[s][pp];
-                } else if (nf == 4) {
-                    rec16_keys<D, QPL, 16>(qrow, krow, y16r);
-                }
-                // partial column maxima over this wave's 4 keys of every member
-                {
-                    uint32_t m = F0;
-#pragma unroll
-                    for (int g = 0; g < NK; ++g) {
-                        if (!m) break;
-                        const int th = __builtin_ctz(m);
-                        m &= m - 1;
-                        const int key0 = k0 + th * BK + w * 4;
-#pragma unroll
-                        for (int s = 0; s < QPL; ++s) {
-                            float cm = NEG_INF;
-#pragma unroll
-                            for (int i = 0; i < 4; ++i) {
-                                const uint32_t word = g == 0 ? y16r[s][i >> 1] : g == 1 ? y16r[s][2 + (i >> 1)]
-                                                    : g == 2 ? y16r[s][4 + (i >> 1)] : y16r[s][6 + (i >> 1)];
-                                const float yv = e4m11_value((word >> (16 * (i & 1))) & 0xFFFFu);
-                                if (visible(s, key0 + i)) cm = yv > cm ? yv : cm;
-                            }
-                            cms[(th * NW + w) * BQ + row[s]] = cm;
-                        }
-                    }
-                }
-                __syncthreads();
-#pragma unroll
-                for (int th = 0; th < NK; ++th)
-#pragma unroll
-                    for (int s = 0; s < QPL; ++s) {
-                        float c = NEG_INF;
-                        if (F0 >> th & 1u)
-#pragma unroll
-                            for (int ww = 0; ww < NW; ++ww) {
-                                const float x = cms[(th * NW + ww) * BQ + row[s]];
-                                c = x > c ? x : c;
-                            }
-                        cm16[th][s] = c;
-                    }
-            }
             int pos = 0, par = 0;
             while (true) {
                 while (pos < na && !(fail >> ((order >> (4 * pos)) & 15u) & 1u)) ++pos;
@@ -431,18 +348,6 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                 const int th = (int)((order >> (4 * pos)) & 15u);
                 ++pos;
                 prec16 |= 1u << th;
-                if (BATCH && (F0 >> th & 1u)) {
-#pragma unroll
-                    for (int s = 0; s < QPL; ++s) {
-                        float c = muh[s];
-#pragma unroll
-                        for (int t2 = 0; t2 < NK; ++t2)
-                            if (t2 == th) c = cm16[t2][s] > c ? cm16[t2][s] : c;
-                        muh[s] = c;
-                    }
-                    if (pos < na) fail = fails();
-                    continue;
-                }
                 {   // all waves recompute the sub-block in 16 bits, KPW keys each
                     float cm[QPL];
 #pragma unroll
@@ -495,7 +400,6 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                         }
                     continue;
                 }
-                if (BATCH && ((prec16 & F0) >> th & 1u)) continue;   // from registers by every wave, below
                 const bool hi16 = prec16 >> th & 1u;
                 for (int ch = 0; ch < CPS; ++ch) {
                     const int c16 = th * CPS + ch;
@@ -548,46 +452,6 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                             lp[0] = u32x4{outl[0], outl[1], outl[2], outl[3]};
                             lp[1] = u32x4{outl[4], outl[5], outl[6], outl[7]};
                         }
-                    }
-                }
-            }
-            if constexpr (BATCH) {
-                // 16-bit exponentials of this wave's 4 keys of every batched
-                // stage-1 sub-block, from the codes held in registers
-                const uint32_t mine = prec16 & F0;
-                uint32_t m = F0;
-#pragma unroll
-                for (int g = 0; g < NK; ++g) {
-                    if (!m) break;
-                    const int th = __builtin_ctz(m);
-                    m &= m - 1;
-                    if (!(mine >> th & 1u)) continue;
-                    const int key0 = k0 + th * BK + w * 4;
-#pragma unroll
-                    for (int s = 0; s < QPL; ++s) {
-                        uint32_t outw[2], outl[2];
-#pragma unroll
-                        for (int pp = 0; pp < 2; ++pp) {
-                            uint32_t res = 0, rlo = 0;
-#pragma unroll
-                            for (int t = 0; t < 2; ++t) {
-                                const int key = key0 + 2 * pp + t;
-                                uint32_t eh = 0, el = 0;
-                                float ev = 0.0f;
-                                if (visible(s, key)) {
-                                    const uint32_t yc = (y16r[s][2 * g + pp] >> (16 * t)) & 0xFFFFu;
-                                    ev = ue5m11e_value(p.exp16[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))]);
-                                    split_bf16(ev, eh, el);
-                                }
-                                sp[s] += (double)ev;
-                                res |= eh << (16 * t);
-                                rlo |= el << (16 * t);
-                            }
-                            outw[pp] = res;
-                            outl[pp] = rlo;
-                        }
-                        *reinterpret_cast<uint2 *>(ycode + row[s] * YP + (key0 - k0)) = make_uint2(outw[0], outw[1]);
-                        *reinterpret_cast<uint2 *>(ylo + row[s] * YP + (key0 - k0)) = make_uint2(outl[0], outl[1]);
                     }
                 }
             }
@@ -736,26 +600,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                     };
                     for (int th = 0; th < NK; ++th) {
                         if (!(prec2 >> th & 1u)) continue;
-                        if (BATCH && (F0 >> th & 1u)) {
-                            // the codes of this wave's keys are already in registers
-                            const uint32_t below = F0 & ((1u << th) - 1u);
-                            const int gi = __builtin_popcount(below);
-                            uint32_t yc[QPL][2];
-#pragma unroll
-                            for (int s = 0; s < QPL; ++s) {
-                                yc[s][0] = y16r[s][0];
-                                yc[s][1] = y16r[s][1];
-#pragma unroll
-                                for (int g = 1; g < NK; ++g)
-                                    if (g == gi) {
-                                        yc[s][0] = y16r[s][2 * g];
-                                        yc[s][1] = y16r[s][2 * g + 1];
-                                    }
-                            }
-                            s2fn(k0 + th * BK + w * 4, yc);
-                        } else {
-                            shared16(k0, th, s2fn);
-                        }
+                        shared16(k0, th, s2fn);
                     }
 #pragma unroll
                     for (int s = 0; s < QPL; ++s) sps[w * BQ + row[s]] = ds[s];
