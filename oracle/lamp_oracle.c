@@ -396,6 +396,34 @@ int oracle_logits16(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv
 
 enum { MASK_LOW = 0, MASK_STAGE1 = 1, MASK_STAGE2 = 2, MASK_INACTIVE = 3 };
 
+/* Variants of Algorithm 1 (flags of lamp_oracle_fwd):
+ *  ORACLE_STAGE1_OFF: the first stage is disabled (the paper's appendix on
+ *    first-stage recomputation): mu_hat is the running maximum of the 8-bit
+ *    logits and only the second stage chooses recomputations;
+ *  ORACLE_MU_TRUNC: the 8-bit shifts use mu_hat truncated to e4m3 (Sec. 3.3:
+ *    the running maxima may be rounded to e4m3 for the low-precision shifts by
+ *    dropping the low mantissa bits).
+ * Both apply for 0 < tau < inf; the two end modes ignore them. */
+enum { ORACLE_STAGE1_OFF = 1, ORACLE_MU_TRUNC = 2 };
+
+/* x truncated (rounded toward zero) to e4m3; reading: values beyond the
+ * largest e4m3 number saturate to +-448; infinities are kept. */
+static double trunc_e4m3(double x)
+{
+    if (isinf(x) || x == 0.0) return x;
+    double ax = fabs(x);
+    if (ax >= F_E4M3.maxval) return copysign(F_E4M3.maxval, x);
+    int E;
+    (void)frexp(ax, &E);
+    int e = E - 1;
+    int emin = 1 - F_E4M3.bias;
+    if (e < emin) e = emin;
+    double quantum = ldexp(1.0, e - F_E4M3.mbits);
+    return copysign(floor(ax / quantum) * quantum, x);
+}
+
+double oracle_trunc_e4m3(double x) { return trunc_e4m3(x); }
+
 /* Shifted exponential of one logit y against the running maximum mu_hat
  * (Alg. 1, exponential steps; Sec. 3.3): s = RN_shift(max(0, mu_hat - y)),
  * E = table[s].  The difference is exact in fp64 (both operands are
@@ -419,6 +447,7 @@ typedef struct {
     const uint16_t *q, *k, *v;
     int B, Hq, Hkv, N, d, causal, window, bq, bk, nk;
     double delta, tau;
+    unsigned flags;
     double *o, *lse;
     uint8_t *mask;
 } fwd_args_t;
@@ -437,6 +466,8 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
     const uint16_t *vbase = A->v + ((int64_t)b * A->Hkv + h / G) * (int64_t)N * d;
     const int pure8 = isinf(A->tau) && A->tau > 0;
     const int all16 = (A->tau == 0.0);
+    const int stage1_off = !pure8 && !all16 && (A->flags & ORACLE_STAGE1_OFF);
+    const int mu_trunc = !pure8 && !all16 && (A->flags & ORACLE_MU_TRUNC);
 
     float *qt = (float *)malloc(sizeof(float) * (size_t)bq * d);
     double *mu = (double *)malloc(sizeof(double) * bq);
@@ -497,9 +528,10 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
             }
         for (int j = 0; j < bq; ++j) muh[j] = mu[j];
 
-        if (pure8) {
-            /* The paper's 8-bit baseline (Sec. 4.1): no recomputation, the
-             * running maximum is taken over the 8-bit logits. */
+        if (pure8 || stage1_off) {
+            /* The paper's 8-bit baseline (Sec. 4.1), and the first stage
+             * disabled: no stage-1 recomputation, the running maximum is
+             * taken over the 8-bit logits. */
             for (int th = 0; th < nk; ++th)
                 if (prec[th] != MASK_INACTIVE)
                     for (int j = 0; j < bq; ++j)
@@ -567,13 +599,15 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
         }
 
         /* Exponentials against the final mu_hat: 16-bit for stage-1
-         * sub-blocks, 8-bit LUT for the rest (Alg. 1). */
+         * sub-blocks, 8-bit LUT for the rest (Alg. 1); the 8-bit ones
+         * against mu_hat truncated to e4m3 with ORACLE_MU_TRUNC. */
         for (int th = 0; th < nk; ++th)
             for (int ii = th * bk; ii < (th + 1) * bk; ++ii)
                 for (int j = 0; j < bq; ++j) {
                     size_t ix = (size_t)ii * bq + j;
-                    E[ix] = (prec[th] == MASK_INACTIVE || !vis[ix]) ? 0.0
-                            : shifted_exp(muh[j], Y[ix], prec[th] == MASK_STAGE1);
+                    const int high = prec[th] == MASK_STAGE1;
+                    const double ref = (!high && mu_trunc) ? trunc_e4m3(muh[j]) : muh[j];
+                    E[ix] = (prec[th] == MASK_INACTIVE || !vis[ix]) ? 0.0 : shifted_exp(ref, Y[ix], high);
                 }
         /* lambda_hat = exp(mu - mu_hat) in high precision (Sec. 2.2):
          * 1 when mu_hat = -inf (no mass yet), 0 when mu = -inf < mu_hat. */
@@ -680,7 +714,7 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
  * Returns 0, or -1 on invalid arguments / -2 on a table failure. */
 int lamp_oracle_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                     int B, int Hq, int Hkv, int N, int d, int causal, int window,
-                    int bq, int bk, int nk, double delta, double tau,
+                    int bq, int bk, int nk, double delta, double tau, unsigned flags,
                     double *o, double *lse, uint8_t *mask,
                     const int64_t *qblocks, int64_t nqblocks, int nthreads)
 {
@@ -690,7 +724,8 @@ int lamp_oracle_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
     if (window < 0 || (window > 0 && !causal)) return -1;
     if (!(tau >= 0.0) || !(delta >= 0.0)) return -1;
     if (build_tables()) return -2;
-    fwd_args_t A = {q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, o, lse, mask};
+    if (flags & ~(unsigned)(ORACLE_STAGE1_OFF | ORACLE_MU_TRUNC)) return -1;
+    fwd_args_t A = {q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, flags, o, lse, mask};
     int64_t nqb = (int64_t)B * Hq * (N / bq);
     int64_t count = qblocks ? nqblocks : nqb;
 #ifdef _OPENMP

@@ -36,7 +36,9 @@ def lib():
         P = ctypes.c_void_p
         i32, i64, f64 = ctypes.c_int, ctypes.c_int64, ctypes.c_double
         _lib.lamp_oracle_fwd.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32,
-                                         f64, f64, P, P, P, P, i64, i32]
+                                         f64, f64, ctypes.c_uint, P, P, P, P, i64, i32]
+        _lib.oracle_trunc_e4m3.argtypes = [f64]
+        _lib.oracle_trunc_e4m3.restype = f64
         _lib.lamp_oracle_fwd.restype = i32
         for name in ("oracle_logits8", "oracle_logits16"):
             fn = getattr(_lib, name)
@@ -154,7 +156,15 @@ def logits16(q, k, causal, window, row0, nrows, nthreads=0):
 
 
 # ---------------------------------------------------------------- forward
-def fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, qblocks=None, nthreads=0):
+STAGE1_OFF = 1   # the first stage disabled: mu_hat from the 8-bit maxima, stage 2 alone recomputes
+MU_TRUNC = 2     # 8-bit shifts against mu_hat truncated to e4m3
+
+
+def trunc_e4m3(x):
+    return lib().oracle_trunc_e4m3(float(x))
+
+
+def fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, qblocks=None, nthreads=0, flags=0):
     """The LampAttention forward pass on the CPU.
 
     Returns (o [B,Hq,N,d] fp64, lse [B,Hq,N] fp64, mask [B,Hq,N/bq,N/bk] u8).
@@ -175,7 +185,7 @@ def fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, qblocks=None, nthreads=
     else:
         qp, nq = None, 0
     rc = lib().lamp_oracle_fwd(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(causal), int(window),
-                               bq, bk, nk, float(delta), float(tau), _ptr(o), _ptr(lse), _ptr(mask),
+                               bq, bk, nk, float(delta), float(tau), int(flags), _ptr(o), _ptr(lse), _ptr(mask),
                                qp, nq, nthreads)
     if rc != 0:
         raise ValueError("lamp_oracle_fwd failed with %d" % rc)

@@ -70,8 +70,24 @@ def _shift_exp(muh, y, high, tabs):
     return M.np_decode(tabs[0][code], "ue5m3_exp")
 
 
-def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale):
-    """q [B,Hq,N,d], k/v [B,Hkv,N,d] bf16 bit patterns.  Returns o, lse, mask."""
+def _trunc_e4m3(x):
+    """Round toward zero onto the e4m3 grid (3 stored mantissa bits, smallest
+    normal 2^-6), saturating at 448; infinities kept."""
+    x = np.asarray(x, dtype=np.float64)
+    ax = np.abs(x)
+    fin = np.isfinite(ax) & (ax > 0)
+    _, ex = np.frexp(np.where(fin, ax, 1.0))
+    e = np.maximum(ex - 1, -6)
+    quantum = np.ldexp(1.0, e - 3)
+    t = np.floor(ax / quantum) * quantum
+    t = np.where(ax >= 448.0, 448.0, t)
+    return np.where(fin, np.copysign(t, x), x)
+
+
+def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=0):
+    """q [B,Hq,N,d], k/v [B,Hkv,N,d] bf16 bit patterns.  Returns o, lse, mask.
+    flags: 1 = first stage disabled, 2 = 8-bit shifts against mu_hat
+    truncated to e4m3 (both only for 0 < tau < inf)."""
     B, Hq, N, d = q.shape
     Hkv = k.shape[1]
     G = Hq // Hkv
@@ -81,6 +97,8 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale):
     mask = np.full((B, Hq, N // bq, N // bk), 3, dtype=np.uint8)
     pure8 = math.isinf(tau)
     all16 = tau == 0.0
+    stage1_off = (not pure8) and (not all16) and bool(flags & 1)
+    mu_trunc = (not pure8) and (not all16) and bool(flags & 2)
     for b in range(B):
         for h in range(Hq):
             kf_all = M.bf16_to_float(k[b, h // G])
@@ -119,7 +137,7 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale):
                             Y16 = y16_tile(qt, kf)
                         return Y16
 
-                    if pure8:
+                    if pure8 or stage1_off:
                         for th in range(nk):
                             if act[th]:
                                 muh = np.maximum(muh, m8[th])
@@ -159,7 +177,9 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale):
                         if prec[th] == 3:
                             continue
                         sl = slice(th * bk, (th + 1) * bk)
-                        e = _shift_exp(muh, np.where(vis[sl], Y[sl], 0.0), prec[th] == 1, tabs)
+                        high = prec[th] == 1
+                        ref = _trunc_e4m3(muh) if (mu_trunc and not high) else muh
+                        e = _shift_exp(ref, np.where(vis[sl], Y[sl], 0.0), high, tabs)
                         E[sl] = np.where(vis[sl], e, 0.0)
                     lam = np.where(muh == -np.inf, 1.0,
                                    np.where(mu == -np.inf, 0.0,
