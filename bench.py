@@ -46,7 +46,7 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
-def _profile_record(path, tag, workload, tau):
+def _profile_record(path, tag, workload, tau, flags=0):
     """The `tag: {json}` line of a committed profile summary, when it was taken
     on the current kernel sources and on this workload; else None."""
     try:
@@ -58,21 +58,21 @@ def _profile_record(path, tag, workload, tau):
         if line.startswith(tag + ": "):
             rec = json.loads(line[len(tag) + 2:])
             if rec.get("source_sha256") == kernel_source_hash() and rec.get("workload") == workload \
-                    and rec.get("tau") == tau:
+                    and rec.get("tau") == tau and rec.get("flags", 0) == flags:
                 return rec
     return None
 
 
-def measured_traffic(workload, tau):
+def measured_traffic(workload, tau, flags=0):
     """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE runs."""
-    rec = _profile_record(TRAFFIC_FILE, "traffic-json", workload, tau)
+    rec = _profile_record(TRAFFIC_FILE, "traffic-json", workload, tau, flags)
     return None if rec is None else rec["bytes_per_launch"]
 
 
-def measured_valu_issue(workload, tau):
+def measured_valu_issue(workload, tau, flags=0):
     """SQ_INSTS_VALU over the launch's VALU issue capacity, from the committed
     counter run."""
-    rec = _profile_record(VALU_FILE, "valu-json", workload, tau)
+    rec = _profile_record(VALU_FILE, "valu-json", workload, tau, flags)
     return None if rec is None else rec["valu_issue_fraction"]
 
 
@@ -94,7 +94,7 @@ def visible_in_mask(w, mask):
     return int((rec * cnt[None]).sum())
 
 
-def cpu_baseline(w, tau, q, k, v, budget_s=15.0, seed=0):
+def cpu_baseline(w, tau, q, k, v, budget_s=15.0, seed=0, flags=0):
     """The CPU oracle on a bounded, stated sample of query blocks."""
     from oracle import oracle as O
     rng = np.random.default_rng(seed)
@@ -110,7 +110,7 @@ def cpu_baseline(w, tau, q, k, v, budget_s=15.0, seed=0):
         batch = [int(x) for x in order[len(picked):len(picked) + n]]
         t0 = time.perf_counter()
         O.fwd(qbits, kbits, vbits, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau, qblocks=batch,
-              nthreads=threads)
+              nthreads=threads, flags=flags)
         spent += time.perf_counter() - t0
         for f in batch:
             qb = f % nqb
@@ -143,6 +143,7 @@ def main():
     ap.add_argument("--tau", type=float, default=None)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--flags", type=int, default=0, help="variants: 1 first stage off, 2 mu_hat truncation")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="before the timed steps, run one plain negating copy of this many MiB "
                          "(fp32 in, fp32 out) to calibrate the HBM byte counters")
@@ -166,7 +167,7 @@ def main():
     out = (o, lse, mask)
 
     def step():
-        lamp.attn_fwd(qd, kd, vd, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau, out=out)
+        lamp.attn_fwd(qd, kd, vd, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau, out=out, flags=args.flags)
 
     if args.copy_calib_mib > 0:
         n = args.copy_calib_mib * (1 << 20) // 4
@@ -222,7 +223,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "N": w.N, "d": w.d,
                    "causal": w.causal, "window": w.window, "bq": w.bq, "bk": w.bk, "nk": w.nk,
-                   "delta": w.delta, "tau": tau},
+                   "delta": w.delta, "tau": tau, "flags": args.flags},
         "recompute_fraction": st["recompute_fraction"],
         "tile_hist": st["tile_hist"],
         "roofline": {
@@ -231,7 +232,7 @@ def main():
             "peak": peak,
             "unit": "T VALU lane-ops/s",
             "frac": achieved / peak,
-            "traffic": measured_traffic(w.name, tau),
+            "traffic": measured_traffic(w.name, tau, args.flags),
             "kernel": ("lamp_fwd16_kernel<%d,%d>" % (w.d, w.bq)) if (w.bk == 16 and w.d >= 128)
                       else ("lamp_fwd_kernel<%d,%d,%d,%d>" % (w.d, w.bq, w.bk, w.nk)),
             "kernel_ms": kernel_ms,
@@ -239,12 +240,12 @@ def main():
             "ops_per_launch": alg_ops,
             "ops_per_unit": "2 per emulated 8-bit MAC, 1 per 16-bit recompute MAC",
             "algorithmic_frac_one_op_per_mac": (mac8 + mac16) / (kernel_ms * 1e-3) / VALU_LANE_OPS,
-            "valu_issue_frac_counters": measured_valu_issue(w.name, tau),
+            "valu_issue_frac_counters": measured_valu_issue(w.name, tau, args.flags),
         },
         "wall_s_timed_region": wall,
     }
     if not args.no_cpu:
-        result["cpu_baseline"] = cpu_baseline(w, tau, q, k, v, budget_s=args.cpu_budget)
+        result["cpu_baseline"] = cpu_baseline(w, tau, q, k, v, budget_s=args.cpu_budget, flags=args.flags)
     print(json.dumps(result), flush=True)
 
 

@@ -60,6 +60,9 @@ enum {
  * tau >= 0: threshold of Eq. (8); tau = +INFINITY is the pure 8-bit path (no
  * recomputation, the paper's 8-bit baseline) and tau = 0 recomputes every
  * active sub-block (16-bit FlashAttention in the paper's formats).
+ * flags: 0, or LAMP_STAGE1_OFF and/or LAMP_MU_TRUNC (below); they apply for
+ * 0 < tau < +INFINITY, the two end modes ignore them; other bits are
+ * LAMP_ERR_INVALID_ARG.
  *
  * Outputs: o (normalised attention output), lse (mu + ln omega per query row,
  * natural log), mask (codes above).  Every mask byte of the rows is written.
@@ -70,14 +73,27 @@ enum {
  *
  * The first call on a device builds the library's exponential tables; the
  * library also keeps a grow-only per-device workspace (fp32 copies of the
- * pre-scaled Q and of K), allocated with hipMalloc when a call needs more
- * than it holds.  Calls that overlap on one device race on that workspace.
+ * pre-scaled Q, of K and of V transposed), allocated with hipMalloc when a
+ * call needs more than it holds.  Calls that overlap on one device race on
+ * that workspace.
  */
 int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                   int B, int Hq, int Hkv, int N, int d,
                   int causal, int window, int bq, int bk, int nk,
-                  double delta, double tau,
+                  double delta, double tau, unsigned flags,
                   float *o, float *lse, uint8_t *mask, void *stream);
+
+/* Variants of Algorithm 1 (flags of lamp_attn_fwd). */
+enum {
+    /* The first stage disabled (the paper's appendix on first-stage
+     * recomputation): mu_hat is the running maximum of the 8-bit logits and
+     * the second stage alone chooses the 16-bit sub-blocks. */
+    LAMP_STAGE1_OFF = 1,
+    /* The 8-bit shifts use mu_hat truncated (toward zero) to e4m3, saturating
+     * at 448 (Sec. 3.3: the running maxima may be rounded to e4m3 for the
+     * low-precision shifts by dropping the low mantissa bits). */
+    LAMP_MU_TRUNC = 2
+};
 
 /*
  * lamp_attn_logits8 -- the 8-bit logits alone (Alg. 1, first accumulation;

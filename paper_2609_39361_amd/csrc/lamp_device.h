@@ -93,6 +93,19 @@ __device__ __forceinline__ float e4m11_value(uint32_t code)
     return (code & 0x8000u) ? -v : v;
 }
 
+// An e4m11 (or e4m3) value truncated toward zero to e4m3, saturating at 448;
+// infinities are kept.  Normal e4m3 magnitudes keep the top 3 fp32 mantissa
+// bits; below 2^-6 the e4m3 quantum is 2^-9.
+__device__ __forceinline__ float trunc_e4m3(float x)
+{
+    const float ax = __builtin_fabsf(x);
+    if (!(ax < 0x1p-6f)) {
+        if (ax >= 448.0f) return ax == __builtin_inff() ? x : __builtin_copysignf(448.0f, x);
+        return __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, x) & 0xFFF00000u);
+    }
+    return __builtin_copysignf(__builtin_truncf(ax * 512.0f) * (1.0f / 512.0f), x);
+}
+
 // --- shifts ----------------------------------------------------------------
 // Shift s = max(mu_hat - y, 2^-14) in fp32.  mu_hat (e4m11 or e4m3) and y are
 // multiples of 2^-17 of magnitude <= 511.875, so the fp32 difference is exact

@@ -243,7 +243,8 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
             for (int th = 0; th < NK; ++th) m8[th][s] = (p.mode != MODE_ALL16) ? m8s[th * BQ + row[s]] : NEG_INF;
         }
         uint32_t prec16 = 0;   // stage-1 (or threshold-0) sub-blocks
-        if (p.mode == MODE_PURE8) {
+        const bool stage1_off = (p.flags & LAMP_STAGE1_OFF) != 0u;   // flags are 0 outside the threshold mode
+        if (p.mode == MODE_PURE8 || stage1_off) {   // running maximum over the 8-bit logits
 #pragma unroll
             for (int s = 0; s < QPL; ++s)
 #pragma unroll
@@ -384,8 +385,12 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
         // ---- 3. exponentials of the own sub-blocks against mu_hat
         {
             double sp[QPL], spF[QPL];   // all exponentials / those of 8-bit sub-blocks
+            float mu8[QPL];             // the running maximum the 8-bit shifts use
 #pragma unroll
-            for (int s = 0; s < QPL; ++s) sp[s] = spF[s] = 0.0;
+            for (int s = 0; s < QPL; ++s) {
+                sp[s] = spF[s] = 0.0;
+                mu8[s] = (p.flags & LAMP_MU_TRUNC) ? trunc_e4m3(muh[s]) : muh[s];
+            }
 #pragma unroll
             for (int u = 0; u < SPW; ++u) {
                 const int th = w * SPW + u;
@@ -434,7 +439,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                                         ev = ue5m11e_value(p.exp16[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))]);
                                         split_bf16(ev, eh, el);
                                     } else {
-                                        eh = lut[ue5m3_code(shift_of(muh[s], e4m3_value(yc)))];
+                                        eh = lut[ue5m3_code(shift_of(mu8[s], e4m3_value(yc)))];
                                         ev = bf16_value(eh);
                                     }
                                 }

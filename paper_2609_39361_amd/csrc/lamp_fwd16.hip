@@ -108,6 +108,8 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     const int q0 = qb * BQ;
     const float NEG_INF = -__builtin_inff();
     const int mode = p.mode;
+    const bool stage1_off = (p.flags & LAMP_STAGE1_OFF) != 0u;   // flags are 0 outside the threshold mode
+    const bool mu_trunc = (p.flags & LAMP_MU_TRUNC) != 0u;
 
     int row[QPL], vlo[QPL], vhi[QPL];
     const float *qrow[QPL];
@@ -225,7 +227,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     // the set of sub-blocks whose 16-bit logits the next fused pass computes
     auto f0_of = [&](int tile, uint32_t act) -> uint32_t {
         if (mode == MODE_ALL16) return act;
-        if (mode == MODE_PURE8) return 0u;
+        if (mode == MODE_PURE8 || stage1_off) return 0u;
         float m8[NK][QPL];
         load_m8(tile, m8);
         return fails_of(m8, mu);
@@ -346,7 +348,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                     cm16[th][s] = f == INT_MIN ? NEG_INF : fx_value(f);
                 }
         }
-        if (mode == MODE_PURE8) {
+        if (mode == MODE_PURE8 || stage1_off) {   // running maximum over the 8-bit logits
             float m8[NK][QPL];
             load_m8(t, m8);
 #pragma unroll
@@ -453,8 +455,12 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
             for (int i = tid; i < NK * BQ; i += 256) cmn[i] = INT_MIN;
 
             double sp[QPL], spF[QPL];   // all exponentials / those of 8-bit sub-blocks
+            float mu8[QPL];             // the running maximum the 8-bit shifts use
 #pragma unroll
-            for (int s = 0; s < QPL; ++s) sp[s] = spF[s] = 0.0;
+            for (int s = 0; s < QPL; ++s) {
+                sp[s] = spF[s] = 0.0;
+                mu8[s] = mu_trunc ? trunc_e4m3(muh[s]) : muh[s];
+            }
             const int th = w;   // own sub-block
             const int ck0 = k0 + th * BK;
             if (!(act >> th & 1u)) {
@@ -499,7 +505,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                                     el = hl >> 16;
                                     ev = bf16_value(eh) + bf16_value(el);   // exact
                                 } else {
-                                    eh = lut[ue5m3_code(shift_of(muh[s], e4m3_value(yc)))];
+                                    eh = lut[ue5m3_code(shift_of(mu8[s], e4m3_value(yc)))];
                                     ev = bf16_value(eh);
                                 }
                             }

@@ -201,14 +201,15 @@ void lamp_shutdown(void)
 }
 
 int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B, int Hq, int Hkv, int N, int d,
-                  int causal, int window, int bq, int bk, int nk, double delta, double tau, float *o, float *lse,
-                  uint8_t *mask, void *stream)
+                  int causal, int window, int bq, int bk, int nk, double delta, double tau, unsigned flags, float *o,
+                  float *lse, uint8_t *mask, void *stream)
 {
     int rc = check_common(q, k, B, Hq, Hkv, N, d, causal, window);
     if (rc) return rc;
     if (!v || !o || !lse || !mask) return fail(LAMP_ERR_INVALID_ARG, "null pointer among v, o, lse, mask");
     if (!(delta >= 0.0) || std::isinf(delta)) return fail(LAMP_ERR_INVALID_ARG, "delta must be finite and >= 0");
     if (!(tau >= 0.0)) return fail(LAMP_ERR_INVALID_ARG, "tau must be >= 0 (or +inf)");
+    if (flags & ~(unsigned)(LAMP_STAGE1_OFF | LAMP_MU_TRUNC)) return fail(LAMP_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
     if (bq <= 0 || bk <= 0 || nk <= 0) return fail(LAMP_ERR_INVALID_ARG, "block sizes must be positive");
     if (N % bq || N % (bk * nk))
         return fail(LAMP_ERR_INVALID_ARG, "N=%d must be a multiple of bq=%d and of bk*nk=%d", N, bq, bk * nk);
@@ -246,6 +247,7 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
     p.delta = delta;
     p.tau = tau;
     p.mode = std::isinf(tau) ? lamp::MODE_PURE8 : (tau == 0.0 ? lamp::MODE_ALL16 : lamp::MODE_LAMP);
+    p.flags = p.mode == lamp::MODE_LAMP ? flags : 0u;
     bool timed = false;
     TimedCall tc{};
     {

@@ -4,6 +4,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "lamp.h"
+
 namespace lamp {
 
 enum { MODE_LAMP = 0, MODE_PURE8 = 1, MODE_ALL16 = 2 };
@@ -20,6 +22,7 @@ struct FwdParams {
     uint8_t *mask;            // [B][Hq][N/BQ][N/BK]
     int B, Hq, Hkv, N;
     int causal, window, mode;
+    unsigned flags;           // LAMP_STAGE1_OFF | LAMP_MU_TRUNC, 0 outside the threshold mode
     double delta, tau;
 };
 

@@ -35,7 +35,7 @@ def lib():
             raise RuntimeError("liblamp.so is not built; run `python -m paper_2609_39361_amd.build`")
         L = ctypes.CDLL(LIB_PATH)
         P, i32, f64, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_double, ctypes.c_size_t
-        L.lamp_attn_fwd.argtypes = [P, P, P] + [i32] * 5 + [i32] * 5 + [f64, f64, P, P, P, P]
+        L.lamp_attn_fwd.argtypes = [P, P, P] + [i32] * 5 + [i32] * 5 + [f64, f64, ctypes.c_uint, P, P, P, P]
         L.lamp_attn_fwd.restype = i32
         L.lamp_attn_logits8.argtypes = [P, P] + [i32] * 9 + [P, P]
         L.lamp_attn_logits8.restype = i32
@@ -93,10 +93,14 @@ def _check_inputs(q, k, v=None):
     return B, Hq, k.shape[1], N, d
 
 
-def attn_fwd(q, k, v, causal=True, window=0, bq=128, bk=16, nk=4, delta=2.0 ** -8, tau=0.5, out=None):
+STAGE1_OFF = 1   # the first stage disabled: mu_hat from the 8-bit maxima, stage 2 alone recomputes
+MU_TRUNC = 2     # 8-bit shifts against mu_hat truncated to e4m3
+
+
+def attn_fwd(q, k, v, causal=True, window=0, bq=128, bk=16, nk=4, delta=2.0 ** -8, tau=0.5, out=None, flags=0):
     """LampAttention forward pass.  Returns (o fp32 [B,Hq,N,d], lse fp32
     [B,Hq,N], mask uint8 [B,Hq,N/bq,N/bk]).  `out` may supply those three
-    tensors to write into."""
+    tensors to write into; `flags` selects the variants STAGE1_OFF, MU_TRUNC."""
     B, Hq, Hkv, N, d = _check_inputs(q, k, v)
     dev = q.device
     if out is None:
@@ -107,7 +111,7 @@ def attn_fwd(q, k, v, causal=True, window=0, bq=128, bk=16, nk=4, delta=2.0 ** -
         o, lse, mask = out
     with torch.cuda.device(dev):
         rc = lib().lamp_attn_fwd(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(causal), int(window),
-                                 bq, bk, nk, float(delta), float(tau), _ptr(o), _ptr(lse), _ptr(mask),
+                                 bq, bk, nk, float(delta), float(tau), int(flags), _ptr(o), _ptr(lse), _ptr(mask),
                                  _stream(dev))
     _check(rc)
     return o, lse, mask

@@ -49,30 +49,34 @@ def test_binding_rejects_bad_arguments_without_gpu():
     lib = ctypes.CDLL(LIB)
     lib.lamp_attn_fwd.restype = ctypes.c_int
     P = ctypes.c_void_p
-    lib.lamp_attn_fwd.argtypes = [P, P, P] + [ctypes.c_int] * 10 + [ctypes.c_double] * 2 + [P, P, P, P]
+    lib.lamp_attn_fwd.argtypes = [P, P, P] + [ctypes.c_int] * 10 + [ctypes.c_double] * 2 + [ctypes.c_uint] + [P, P, P, P]
     lib.lamp_last_error.restype = ctypes.c_char_p
     dummy = P(16)
     # Hq not a multiple of Hkv
-    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 3, 2, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5,
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 3, 2, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 0,
                            dummy, dummy, dummy, None)
     assert rc == 1 and b"multiple" in lib.lamp_last_error()
     # unsupported head dimension
-    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 96, 1, 0, 128, 16, 4, 2 ** -8, 0.5,
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 96, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 0,
                            dummy, dummy, dummy, None)
     assert rc == 2
     # window without causal
-    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 0, 16, 128, 16, 4, 2 ** -8, 0.5,
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 0, 16, 128, 16, 4, 2 ** -8, 0.5, 0,
                            dummy, dummy, dummy, None)
     assert rc == 1
     # negative threshold
-    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, -1.0,
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, -1.0, 0,
                            dummy, dummy, dummy, None)
     assert rc == 1
+    # unknown flag bits
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 4,
+                           dummy, dummy, dummy, None)
+    assert rc == 1 and b"flags" in lib.lamp_last_error()
     # block sizes that are not built
-    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 32, 16, 4, 2 ** -8, 0.5,
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 32, 16, 4, 2 ** -8, 0.5, 0,
                            dummy, dummy, dummy, None)
     assert rc == 2 and b"not built" in lib.lamp_last_error()
-    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 128, 32, 4, 2 ** -8, 0.5,
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 128, 32, 4, 2 ** -8, 0.5, 0,
                            dummy, dummy, dummy, None)
     assert rc == 2
 

@@ -159,12 +159,13 @@ def _inputs(w, keep=False):
     return r
 
 
-def _compare_fwd(L, w, tau, delta=None, qblocks=None, keep=False):
+def _compare_fwd(L, w, tau, delta=None, qblocks=None, keep=False, flags=0):
     delta = w.delta if delta is None else delta
     qd, kd, vd, qb, kb, vb = _inputs(w, keep)
-    o, lse, mask = L.attn_fwd(qd, kd, vd, w.causal, w.window, w.bq, w.bk, w.nk, delta, tau)
+    o, lse, mask = L.attn_fwd(qd, kd, vd, w.causal, w.window, w.bq, w.bk, w.nk, delta, tau, flags=flags)
     torch.cuda.synchronize()
-    ro, rlse, rmask = O.fwd(qb, kb, vb, w.causal, w.window, w.bq, w.bk, w.nk, delta, tau, qblocks=qblocks)
+    ro, rlse, rmask = O.fwd(qb, kb, vb, w.causal, w.window, w.bq, w.bk, w.nk, delta, tau, qblocks=qblocks,
+                            flags=flags)
     o, lse, mask = o.cpu().numpy(), lse.cpu().numpy(), mask.cpu().numpy()
     if qblocks is not None:
         nqb = w.N // w.bq
@@ -198,6 +199,26 @@ FWD_CASES = [
 @pytest.mark.parametrize("w", FWD_CASES, ids=[w.name for w in FWD_CASES])
 def test_fwd_parity_small(L, w, tau):
     _compare_fwd(L, w, tau)
+
+
+VARIANT_CASES = [FWD_CASES[0], FWD_CASES[1], FWD_CASES[2], FWD_CASES[3], FWD_CASES[5]]
+
+
+@pytest.mark.parametrize("flags", [1, 2, 3])
+@pytest.mark.parametrize("tau", [1.0, 0.5, 2.0 ** -5])
+@pytest.mark.parametrize("w", VARIANT_CASES, ids=[w.name for w in VARIANT_CASES])
+def test_fwd_variants_small(L, w, tau, flags):
+    """First stage off (1), mu_hat truncated for the 8-bit shifts (2), both."""
+    _compare_fwd(L, w, tau, flags=flags)
+
+
+@pytest.mark.parametrize("flags", [1, 2])
+def test_fwd_variants_config3_sampled(L, flags):
+    w = W.CONFIGS[3]
+    nqb = w.N // w.bq
+    qbl = [nqb - 1, 17, 31 * nqb + 40]
+    err, mask = _compare_fwd(L, w, 2.0 ** -5, qblocks=qbl, flags=flags)
+    _say("config 3 flags %d tau 2^-5 sampled: O err %.2e, mask %s" % (flags, err, np.bincount(mask.ravel(), minlength=4)))
 
 
 def test_fwd_delta_variant(L):
