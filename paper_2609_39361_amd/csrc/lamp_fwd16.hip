@@ -705,27 +705,51 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                             *reinterpret_cast<uint2 *>(ylo + row[s] * YP + (kc - k0)) = make_uint2(outl[0], outl[1]);
                         }
                     };
+                    // sub-blocks of R without codes from the fused pass: one batched
+                    // recompute, 4 keys of each per wave (as for F0)
+                    const uint32_t Rn = prec2 & ~F0;
+                    uint32_t y16b[QPL][8];
+                    if (Rn) {
+                        const int nr = __builtin_popcount(Rn);
+                        const int kb = (lane & 15) % (4 * nr);
+                        uint32_t m = Rn;
+                        for (int g = 0; g < kb / 4; ++g) m &= m - 1;
+                        const float *krow = kt32 + (size_t)(k0 + __builtin_ctz(m) * BK + w * 4 + (kb & 3)) * D;
+                        auto rec = [&](auto nkey_c) {
+                            constexpr int NKEY = decltype(nkey_c)::value;
+                            uint32_t c[QPL][NKEY / 2];
+                            rec16_keys<D, QPL, NKEY>(qrow, krow, c);
+#pragma unroll
+                            for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                                for (int pp = 0; pp < NKEY / 2; ++pp) y16b[s][pp] = c[s][pp];
+                        };
+                        switch (nr) {
+                        case 1: rec(std::integral_constant<int, 4>()); break;
+                        case 2: rec(std::integral_constant<int, 8>()); break;
+                        case 3: rec(std::integral_constant<int, 12>()); break;
+                        default: rec(std::integral_constant<int, 16>()); break;
+                        }
+                    }
                     for (int th = 0; th < NK; ++th) {
                         if (!(prec2 >> th & 1u)) continue;
-                        if (F0 >> th & 1u) {
-                            // the codes of this wave's keys are already in registers
-                            const int gi = __builtin_popcount(F0 & ((1u << th) - 1u));
-                            uint32_t yc[QPL][2];
+                        // this wave's 4 keys of sub-block th: codes from the fused pass
+                        // (member of F0) or from the batch above
+                        const bool inF0 = F0 >> th & 1u;
+                        const int gi = __builtin_popcount((inF0 ? F0 : Rn) & ((1u << th) - 1u));
+                        uint32_t yc[QPL][2];
 #pragma unroll
-                            for (int s = 0; s < QPL; ++s) {
-                                yc[s][0] = y16r[s][0];
-                                yc[s][1] = y16r[s][1];
+                        for (int s = 0; s < QPL; ++s) {
+                            yc[s][0] = inF0 ? y16r[s][0] : y16b[s][0];
+                            yc[s][1] = inF0 ? y16r[s][1] : y16b[s][1];
 #pragma unroll
-                                for (int g = 1; g < NK; ++g)
-                                    if (g == gi) {
-                                        yc[s][0] = y16r[s][2 * g];
-                                        yc[s][1] = y16r[s][2 * g + 1];
-                                    }
-                            }
-                            s2fn(k0 + th * BK + w * 4, yc);
-                        } else {
-                            shared16(k0, th, s2fn);
+                            for (int g = 1; g < NK; ++g)
+                                if (g == gi) {
+                                    yc[s][0] = inF0 ? y16r[s][2 * g] : y16b[s][2 * g];
+                                    yc[s][1] = inF0 ? y16r[s][2 * g + 1] : y16b[s][2 * g + 1];
+                                }
                         }
+                        s2fn(k0 + th * BK + w * 4, yc);
                     }
 #pragma unroll
                     for (int s = 0; s < QPL; ++s) sps[w * BQ + row[s]] = ds[s];
