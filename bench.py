@@ -224,6 +224,7 @@ def main():
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "N": w.N, "d": w.d,
                    "causal": w.causal, "window": w.window, "bq": w.bq, "bk": w.bk, "nk": w.nk,
                    "delta": w.delta, "tau": tau, "flags": args.flags},
+        "visible_pair_tflops": 4.0 * w.macs / (ms * 1e-3) / 1e12,   # 4*d per visible (query, key) pair
         "recompute_fraction": st["recompute_fraction"],
         "tile_hist": st["tile_hist"],
         "roofline": {
