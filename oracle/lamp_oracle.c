@@ -458,8 +458,13 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
     const int d = A->d, N = A->N, bq = A->bq, bk = A->bk, nk = A->nk;
     const int T = bk * nk;                       /* keys per tile */
     const int G = A->Hq / A->Hkv;
-    const int nkb = N / bk;                      /* key sub-blocks per row */
-    const int ntiles = N / T;
+    /* Reading for lengths that are not multiples of the block sizes: keys at
+     * or beyond N are invisible, and the last query block's rows beyond N do
+     * not exist (no visible key: they take part in no test and are not
+     * written); the mask holds every sub-block of the ceil(N/T) tiles. */
+    const int ntiles = (N + T - 1) / T;
+    const int nkb = ntiles * nk;                 /* key sub-blocks per row */
+    const int nqbh = (N + bq - 1) / bq;          /* query blocks per head */
     const int64_t q0 = (int64_t)qb * bq;
     const float s = scale_of(d);
     const uint16_t *kbase = A->k + ((int64_t)b * A->Hkv + h / G) * (int64_t)N * d;
@@ -486,11 +491,12 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
     double *thr = (double *)malloc(sizeof(double) * nk);
 
     for (int j = 0; j < bq; ++j) {
-        prescale(A->q + (((int64_t)b * A->Hq + h) * N + q0 + j) * d, d, s, qt + (size_t)j * d);
+        if (q0 + j < N) prescale(A->q + (((int64_t)b * A->Hq + h) * N + q0 + j) * d, d, s, qt + (size_t)j * d);
+        else memset(qt + (size_t)j * d, 0, sizeof(float) * (size_t)d);
         mu[j] = -INFINITY;
         om[j] = 0.0;
     }
-    uint8_t *mrow = A->mask + (((int64_t)b * A->Hq + h) * (N / bq) + qb) * nkb;
+    uint8_t *mrow = A->mask + (((int64_t)b * A->Hq + h) * nqbh + qb) * nkb;
     for (int t = 0; t < nkb; ++t) mrow[t] = MASK_INACTIVE;
 
     for (int tile = 0; tile < ntiles; ++tile) {
@@ -500,14 +506,15 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
             int act = 0;
             for (int ii = th * bk; ii < (th + 1) * bk && !act; ++ii)
                 for (int j = 0; j < bq; ++j)
-                    if (visible(k0 + ii, q0 + j, A->causal, A->window)) { act = 1; break; }
+                    if (k0 + ii < N && q0 + j < N && visible(k0 + ii, q0 + j, A->causal, A->window)) { act = 1; break; }
             prec[th] = act ? MASK_LOW : MASK_INACTIVE;
             any_active |= act;
         }
         if (!any_active) continue;               /* no state change */
         for (int ii = 0; ii < T; ++ii)
             for (int j = 0; j < bq; ++j)
-                vis[(size_t)ii * bq + j] = (unsigned char)visible(k0 + ii, q0 + j, A->causal, A->window);
+                vis[(size_t)ii * bq + j] = (unsigned char)(k0 + ii < N && q0 + j < N &&
+                                                           visible(k0 + ii, q0 + j, A->causal, A->window));
 
         /* Low-precision logits of the tile (Alg. 1: accumulate Y in low
          * precision).  In the all-16-bit mode they are never used. */
@@ -698,7 +705,7 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
     }
 
     /* Epilogue (Alg. 1): O / omega; lse = mu + ln(omega). */
-    for (int j = 0; j < bq; ++j) {
+    for (int j = 0; j < bq && q0 + j < N; ++j) {
         double *dst = A->o + (((int64_t)b * A->Hq + h) * N + q0 + j) * d;
         for (int c = 0; c < d; ++c) dst[c] = O[(size_t)j * d + c] / om[j];
         A->lse[((int64_t)b * A->Hq + h) * N + q0 + j] = mu[j] + log(om[j]);
@@ -708,9 +715,10 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
 }
 
 /* lamp_oracle_fwd: Q,K,V bf16 bit patterns [B,H,N,d] (host memory),
- * outputs o [B,Hq,N,d] fp64, lse [B,Hq,N] fp64, mask [B,Hq,N/bq,N/bk] u8.
+ * outputs o [B,Hq,N,d] fp64, lse [B,Hq,N] fp64, mask [B,Hq,ceil(N/bq),
+ * ceil(N/(bk*nk))*nk] u8 (any N >= 0; B = 0 or N = 0 computes nothing).
  * If qblocks != NULL only the listed query blocks (flat index
- * (b*Hq + h)*(N/bq) + qb) are computed; other outputs are left untouched.
+ * (b*Hq + h)*ceil(N/bq) + qb) are computed; other outputs are left untouched.
  * Returns 0, or -1 on invalid arguments / -2 on a table failure. */
 int lamp_oracle_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                     int B, int Hq, int Hkv, int N, int d, int causal, int window,
@@ -718,15 +726,16 @@ int lamp_oracle_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                     double *o, double *lse, uint8_t *mask,
                     const int64_t *qblocks, int64_t nqblocks, int nthreads)
 {
-    if (B <= 0 || Hq <= 0 || Hkv <= 0 || N <= 0 || d <= 0 || d > 1024) return -1;
+    if (B < 0 || Hq <= 0 || Hkv <= 0 || N < 0 || d <= 0 || d > 1024) return -1;
     if (Hq % Hkv || bq <= 0 || bk <= 0 || nk <= 0 || nk > 16) return -1;
-    if (N % bq || N % (bk * nk)) return -1;
     if (window < 0 || (window > 0 && !causal)) return -1;
     if (!(tau >= 0.0) || !(delta >= 0.0)) return -1;
     if (build_tables()) return -2;
     if (flags & ~(unsigned)(ORACLE_STAGE1_OFF | ORACLE_MU_TRUNC)) return -1;
+    if (B == 0 || N == 0) return 0;                /* nothing to compute */
     fwd_args_t A = {q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, flags, o, lse, mask};
-    int64_t nqb = (int64_t)B * Hq * (N / bq);
+    const int nqbh = (N + bq - 1) / bq;
+    int64_t nqb = (int64_t)B * Hq * nqbh;
     int64_t count = qblocks ? nqblocks : nqb;
 #ifdef _OPENMP
     if (nthreads > 0) omp_set_num_threads(nthreads);
@@ -734,9 +743,9 @@ int lamp_oracle_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
 #endif
     for (int64_t t = 0; t < count; ++t) {
         int64_t f = qblocks ? qblocks[t] : t;
-        int qb = (int)(f % (N / bq));
-        int h = (int)((f / (N / bq)) % Hq);
-        int b = (int)(f / ((int64_t)(N / bq) * Hq));
+        int qb = (int)(f % nqbh);
+        int h = (int)((f / nqbh) % Hq);
+        int b = (int)(f / ((int64_t)nqbh * Hq));
         fwd_qblock(&A, b, h, qb);
     }
     return 0;

@@ -167,7 +167,8 @@ def trunc_e4m3(x):
 def fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, qblocks=None, nthreads=0, flags=0):
     """The LampAttention forward pass on the CPU.
 
-    Returns (o [B,Hq,N,d] fp64, lse [B,Hq,N] fp64, mask [B,Hq,N/bq,N/bk] u8).
+    Returns (o [B,Hq,N,d] fp64, lse [B,Hq,N] fp64, mask [B,Hq,ceil(N/bq),
+    ceil(N/(bk*nk))*nk] u8); N need not be a multiple of the block sizes.
     With `qblocks` (flat indices (b*Hq+h)*(N/bq)+qb) only those query blocks
     are computed; the other rows of o/lse hold NaN and their mask bytes 0xFE.
     """
@@ -178,7 +179,8 @@ def fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, qblocks=None, nthreads=
     Hkv = k.shape[1]
     o = np.full((B, Hq, N, d), np.nan, dtype=np.float64)
     lse = np.full((B, Hq, N), np.nan, dtype=np.float64)
-    mask = np.full((B, Hq, N // bq, N // bk), 0xFE, dtype=np.uint8)
+    T = bk * nk
+    mask = np.full((B, Hq, -(-N // bq), -(-N // T) * nk), 0xFE, dtype=np.uint8)
     if qblocks is not None:
         qbl = np.ascontiguousarray(qblocks, dtype=np.int64)
         qp, nq = _ptr(qbl), qbl.size

@@ -94,7 +94,8 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=
     T = bk * nk
     o = np.zeros((B, Hq, N, d))
     lse = np.zeros((B, Hq, N))
-    mask = np.full((B, Hq, N // bq, N // bk), 3, dtype=np.uint8)
+    nqb, ntiles = -(-N // bq), -(-N // T)          # ragged lengths: keys and rows beyond N do not exist
+    mask = np.full((B, Hq, nqb, ntiles * nk), 3, dtype=np.uint8)
     pure8 = math.isinf(tau)
     all16 = tau == 0.0
     stage1_off = (not pure8) and (not all16) and bool(flags & 1)
@@ -103,17 +104,19 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=
         for h in range(Hq):
             kf_all = M.bf16_to_float(k[b, h // G])
             vf_all = M.bf16_to_float(v[b, h // G])
-            for qb in range(N // bq):
+            for qb in range(nqb):
                 q0 = qb * bq
-                qf = M.bf16_to_float(q[b, h, q0:q0 + bq])
+                nr = min(bq, N - q0)
+                qf = np.zeros((bq, d))
+                qf[:nr] = M.bf16_to_float(q[b, h, q0:q0 + nr])
                 qt = (qf * np.float64(scale)).astype(np.float32).astype(np.float64)
                 mu = np.full(bq, -np.inf)
                 om = np.zeros(bq)
                 O = np.zeros((bq, d))
                 jj = q0 + np.arange(bq)
-                for t in range(N // T):
+                for t in range(ntiles):
                     ii = t * T + np.arange(T)
-                    vis = np.ones((T, bq), dtype=bool)
+                    vis = (ii[:, None] < N) & (jj[None, :] < N)
                     if causal:
                         vis &= ii[:, None] <= jj[None, :]
                     if window > 0:
@@ -121,7 +124,7 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=
                     act = np.array([vis[th * bk:(th + 1) * bk].any() for th in range(nk)])
                     if not act.any():
                         continue
-                    kf = kf_all[ii]
+                    kf = kf_all[np.minimum(ii, N - 1)]
                     prec = np.where(act, 0, 3)
                     Y = np.full((T, bq), np.nan)
                     if not all16:
@@ -215,9 +218,10 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=
                                 e = _shift_exp(muh, np.where(vis[sl], Y[sl], 0.0), True, tabs)
                                 E[sl] = np.where(vis[sl], e, 0.0)
                     om = lam * om + E.sum(axis=0)
-                    O = O * lam[:, None] + E.T @ vf_all[ii]
+                    O = O * lam[:, None] + E.T @ vf_all[np.minimum(ii, N - 1)]
                     mu = muh
                     mask[b, h, qb, t * nk:(t + 1) * nk] = prec
-                o[b, h, q0:q0 + bq] = O / om[:, None]
-                lse[b, h, q0:q0 + bq] = mu + np.log(om)
+                with np.errstate(invalid="ignore", divide="ignore"):
+                    o[b, h, q0:q0 + nr] = (O / om[:, None])[:nr]
+                    lse[b, h, q0:q0 + nr] = (mu + np.log(om))[:nr]
     return o, lse, mask

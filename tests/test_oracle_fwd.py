@@ -220,8 +220,61 @@ def test_invalid_arguments_rejected():
     w = W.small("bad", N=64, d=16, Hq=3, Hkv=2, bq=16, bk=8, nk=2)
     q, k, v = _bits(W.small("ok", N=64, d=16, Hq=2, Hkv=1, bq=16, bk=8, nk=2))
     with pytest.raises(ValueError):
-        O.fwd(q, k, v, 1, 0, 24, 8, 2, 2 ** -8, 0.5)          # N % bq != 0
-    with pytest.raises(ValueError):
         O.fwd(q, k, v, 0, 8, 16, 8, 2, 2 ** -8, 0.5)          # window without causal
     with pytest.raises(ValueError):
         O.fwd(q, k, v, 1, 0, 16, 8, 2, 2 ** -8, -1.0)         # negative threshold
+
+
+RAGGED = [
+    (W.small("rag_causal", N=83, d=16, Hq=2, Hkv=1, bq=32, bk=8, nk=4, causal=1, seed=41), 0.5),
+    (W.small("rag_nc", N=45, d=8, Hq=1, Hkv=1, bq=16, bk=4, nk=4, causal=0, seed=42), 2 ** -5),
+    (W.small("rag_window", N=70, d=8, Hq=1, Hkv=1, bq=16, bk=8, nk=2, causal=1, window=9, seed=43), 0.5),
+    (W.small("rag_short", N=5, d=16, Hq=1, Hkv=1, bq=32, bk=8, nk=4, causal=1, seed=44), 0.5),
+    (W.small("rag_pure8", N=77, d=16, Hq=1, Hkv=1, bq=32, bk=8, nk=4, causal=1, seed=45), math.inf),
+    (W.small("rag_all16", N=77, d=16, Hq=1, Hkv=1, bq=32, bk=8, nk=4, causal=1, seed=46), 0.0),
+]
+
+
+@pytest.mark.parametrize("w,tau", RAGGED, ids=[c[0].name for c in RAGGED])
+def test_ragged_lengths_match_independent_implementation(w, tau, mp_tables):
+    """N not a multiple of the block sizes: keys and query rows beyond N do
+    not exist; the last key tile and query block are partial."""
+    q, k, v = _bits(w)
+    o, lse, mask = O.fwd(q, k, v, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau)
+    ro, rlse, rmask = R.ref_fwd(q, k, v, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau,
+                                mp_tables, O.scale(w.d))
+    assert mask.shape == (w.B, w.Hq, -(-w.N // w.bq), -(-w.N // (w.bk * w.nk)) * w.nk)
+    assert np.array_equal(mask, rmask)
+    np.testing.assert_allclose(o, ro, rtol=1e-9, atol=1e-12)
+    np.testing.assert_allclose(lse, rlse, rtol=1e-12, atol=1e-12)
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(lse))
+    # sub-blocks that lie entirely beyond N are inactive
+    T = w.bk * w.nk
+    first_void = -(-w.N // w.bk)
+    assert np.all(mask[..., first_void:] == 3)
+
+
+def test_ragged_equals_the_padded_problem_on_full_blocks():
+    """Causal: a query block whose rows all lie below N sees no key beyond N,
+    so a ragged problem and any longer one agree on those blocks (the
+    decisions of the partial block also involve its rows beyond N in the
+    longer problem, so it may differ)."""
+    w = W.small("rag_pad", N=96, d=16, Hq=1, Hkv=1, bq=32, bk=8, nk=4, causal=1, seed=47)
+    q, k, v = _bits(w)
+    n = 83
+    o, lse, mask = O.fwd(q[:, :, :n].copy(), k[:, :, :n].copy(), v[:, :, :n].copy(), 1, 0, 32, 8, 4, w.delta, 0.5)
+    o2, lse2, mask2 = O.fwd(q, k, v, 1, 0, 32, 8, 4, w.delta, 0.5)
+    full = (n // 32) * 32
+    assert np.array_equal(o[:, :, :full], o2[:, :, :full]) and np.array_equal(lse[:, :, :full], lse2[:, :, :full])
+    assert np.array_equal(mask[:, :, :n // 32], mask2[:, :, :n // 32, :mask.shape[3]])
+
+
+def test_empty_inputs():
+    q = np.zeros((1, 2, 0, 16), dtype=np.uint16)
+    k = np.zeros((1, 1, 0, 16), dtype=np.uint16)
+    o, lse, mask = O.fwd(q, k, k, 1, 0, 32, 8, 4, 2 ** -8, 0.5)
+    assert o.shape == (1, 2, 0, 16) and lse.shape == (1, 2, 0) and mask.size == 0
+    q = np.zeros((0, 2, 64, 16), dtype=np.uint16)
+    k = np.zeros((0, 1, 64, 16), dtype=np.uint16)
+    o, lse, mask = O.fwd(q, k, k, 1, 0, 32, 8, 4, 2 ** -8, 0.5)
+    assert o.size == 0 and mask.shape == (0, 2, 2, 8)
