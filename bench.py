@@ -163,7 +163,7 @@ def main():
     qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
     o = torch.empty((w.B, w.Hq, w.N, w.d), dtype=torch.float32, device=dev)
     lse = torch.empty((w.B, w.Hq, w.N), dtype=torch.float32, device=dev)
-    mask = torch.empty((w.B, w.Hq, w.N // w.bq, w.N // w.bk), dtype=torch.uint8, device=dev)
+    mask = torch.empty((w.B, w.Hq, -(-w.N // w.bq), -(-w.N // (w.bk * w.nk)) * w.nk), dtype=torch.uint8, device=dev)
     out = (o, lse, mask)
 
     def step():

@@ -14,7 +14,7 @@
  *     memory the caller owns; the library never frees or retains them.
  *   - Tensors are dense row-major: q [B][Hq][N][d], k and v [B][Hkv][N][d]
  *     (bf16 bit patterns, uint16_t), o [B][Hq][N][d] fp32, lse [B][Hq][N]
- *     fp32, mask [B][Hq][N/bq][N/bk] uint8.  Query head h reads kv head
+ *     fp32, mask [B][Hq][ceil(N/bq)][ceil(N/(bk*nk))*nk] uint8.  Query head h reads kv head
  *     h / (Hq/Hkv) (grouped-query attention).
  *   - Visibility: key i is visible to query j unless causal and i > j, or
  *     window > 0 and i <= j - window (window requires causal).
@@ -68,8 +68,12 @@ enum {
  * natural log), mask (codes above).  Every mask byte of the rows is written.
  *
  * Built configurations (LAMP_ERR_UNSUPPORTED otherwise): d in {64, 128, 256};
- * bq in {64, 128}; (bk, nk) in {(16, 4), (64, 4)}; N a multiple of bq and of
- * bk * nk; N <= 2^20.
+ * bq in {64, 128}; (bk, nk) in {(16, 4), (64, 4)}; N <= 2^20.  N need not be a
+ * multiple of the block sizes: keys at or beyond N are invisible and the last
+ * query block is partial (its missing rows take part in no test).  The mask
+ * then holds ceil(N/bq) query blocks of ceil(N/(bk*nk))*nk sub-blocks, codes
+ * of sub-blocks beyond N being 3.  B = 0 or N = 0 returns LAMP_OK and writes
+ * nothing.
  *
  * The first call on a device builds the library's exponential tables; the
  * library also keeps a grow-only per-device workspace (fp32 copies of the

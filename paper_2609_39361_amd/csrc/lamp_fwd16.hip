@@ -99,7 +99,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
 
     const int tid = threadIdx.x;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;   // w is wave-uniform
-    const int nqb = p.N / BQ;
+    const int nqb = p.Nq / BQ;   // query blocks per head (the last may be partial)
     const int BH = p.B * p.Hq;
     const int qb = nqb - 1 - (int)(blockIdx.x / BH);   // longest blocks first under causality
     const int bh = blockIdx.x % BH;
@@ -119,15 +119,19 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
         const int j = q0 + row[s];
         vlo[s] = p.window > 0 ? (j - p.window + 1 > 0 ? j - p.window + 1 : 0) : 0;
         vhi[s] = p.causal ? j : p.N - 1;
-        qrow[s] = p.qt + (((size_t)b * p.Hq + h) * p.N + j) * D;
+        if (j >= p.N) {   // a row beyond N (partial last block): no visible key
+            vlo[s] = p.N;
+            vhi[s] = -1;
+        }
+        qrow[s] = p.qt + (((size_t)b * p.Hq + h) * p.Nq + j) * D;   // zero-padded rows, in bounds
     }
     const int bv_lo = p.window > 0 ? (q0 - p.window + 1 > 0 ? q0 - p.window + 1 : 0) : 0;
-    const int bv_hi = p.causal ? q0 + BQ - 1 : p.N - 1;
+    const int bv_hi = p.causal ? (q0 + BQ - 1 < p.N - 1 ? q0 + BQ - 1 : p.N - 1) : p.N - 1;
     const int t_begin = bv_lo / KPT, t_end = bv_hi / KPT;   // every tile in between has a visible pair
 
-    const float *kt32 = p.kt32 + ((size_t)b * p.Hkv + hk) * (size_t)p.N * D;       // fp32 keys [N][D]
-    const uint16_t *vtbase = p.vt + ((size_t)b * p.Hkv + hk) * (size_t)D * p.N;    // V^T [D][N]
-    uint8_t *mrow = p.mask + (((size_t)b * p.Hq + h) * nqb + qb) * (size_t)(p.N / BK);
+    const float *kt32 = p.kt32 + ((size_t)b * p.Hkv + hk) * (size_t)p.Nk * D;       // fp32 keys [Nk][D]
+    const uint16_t *vtbase = p.vt + ((size_t)b * p.Hkv + hk) * (size_t)D * p.Nk;    // V^T [D][Nk]
+    uint8_t *mrow = p.mask + (((size_t)b * p.Hq + h) * nqb + qb) * (size_t)(p.Nk / BK);
 
     for (int i = tid; i < 256; i += 256) lut[i] = p.lut8e[i];
     if (tid < EXPDOC_NK) edk[tid] = EXPDOC_K[tid];
@@ -784,7 +788,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
         auto load_v = [&](int c16, u32x4 (&a)[CT]) {
 #pragma unroll
             for (int tt = 0; tt < CT; ++tt)
-                a[tt] = *reinterpret_cast<const u32x4 *>(vtbase + (size_t)(w * CPW + tt * 32 + l32) * p.N + k0 +
+                a[tt] = *reinterpret_cast<const u32x4 *>(vtbase + (size_t)(w * CPW + tt * 32 + l32) * p.Nk + k0 +
                                                          c16 * 16 + half * 8);
         };
         auto pv_chunk = [&](int c16, const u32x4 (&a)[CT]) {
@@ -851,6 +855,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
             const double og = __shfl(om[g / 2 < QPL ? g / 2 : 0], ((g & 1) << 5) + l32, 64);
             const float inv = (float)(1.0 / og);
             const int jq = q0 + g * 32 + l32;
+            if (jq >= p.N) continue;   // beyond N in a partial last block
             float *orow = p.o + (((size_t)b * p.Hq + h) * p.N + jq) * D + w * CPW;
 #pragma unroll
             for (int tt = 0; tt < CT; ++tt)
@@ -865,8 +870,9 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
         if (w == 0)
 #pragma unroll
             for (int s = 0; s < QPL; ++s)
-                p.lse[((size_t)b * p.Hq + h) * p.N + q0 + row[s]] = (float)((double)mu[s] + ::log(om[s]));
-        const int ntiles = p.N / KPT;
+                if (q0 + row[s] < p.N)
+                    p.lse[((size_t)b * p.Hq + h) * p.N + q0 + row[s]] = (float)((double)mu[s] + ::log(om[s]));
+        const int ntiles = p.Nk / KPT;
         for (int tt = tid; tt < ntiles; tt += 256)
             if (tt < t_begin || tt > t_end)
                 for (int th = 0; th < NK; ++th) mrow[tt * NK + th] = PREC_INACTIVE;
@@ -882,7 +888,7 @@ static hipError_t launch_fwd16(const FwdParams &p, hipStream_t s)
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
     if (e != hipSuccess) return e;
-    dim3 grid((unsigned)(p.B * p.Hq * (p.N / BQ)));
+    dim3 grid((unsigned)(p.B * p.Hq * (p.Nq / BQ)));
     hipLaunchKernelGGL(kern, grid, dim3(256), C::LDS, s, p);
     return hipGetLastError();
 }

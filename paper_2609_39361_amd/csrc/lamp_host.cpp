@@ -111,12 +111,12 @@ struct Workspace {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Grow-only workspace for the pre-scaled Q, the fp32 K and (with_vt) the
-// transposed V (lock held).
-int workspace_locked(int dev, int B, int Hq, int Hkv, int N, int d, Workspace *w, bool with_vt = false)
+// Grow-only workspace for the pre-scaled Q (Nq rows per head), the fp32 K
+// and (with_vt) the transposed V (Nk keys per head) (lock held).
+int workspace_locked(int dev, int B, int Hq, int Hkv, int Nq, int Nk, int d, Workspace *w, bool with_vt = false)
 {
     DeviceState *st = state_of(dev);
-    size_t nq = (size_t)B * Hq * N * d, nk = (size_t)B * Hkv * N * d;
+    size_t nq = (size_t)B * Hq * Nq * d, nk = (size_t)B * Hkv * Nk * d;
     size_t bq = align256(nq * 4), bk32 = align256(nk * 4), bvt = with_vt ? align256(nk * 2) : 0;
     size_t need = bq + bk32 + bvt;
     if (need > st->ws_bytes) {
@@ -138,9 +138,9 @@ int workspace_locked(int dev, int B, int Hq, int Hkv, int N, int d, Workspace *w
 
 int check_common(const void *q, const void *k, int B, int Hq, int Hkv, int N, int d, int causal, int window)
 {
-    if (!q || !k) return fail(LAMP_ERR_INVALID_ARG, "null input pointer");
-    if (B <= 0 || Hq <= 0 || Hkv <= 0 || N <= 0 || d <= 0)
-        return fail(LAMP_ERR_INVALID_ARG, "sizes must be positive (B=%d Hq=%d Hkv=%d N=%d d=%d)", B, Hq, Hkv, N, d);
+    if ((B > 0 && N > 0) && (!q || !k)) return fail(LAMP_ERR_INVALID_ARG, "null input pointer");
+    if (B < 0 || Hq <= 0 || Hkv <= 0 || N < 0 || d <= 0)
+        return fail(LAMP_ERR_INVALID_ARG, "invalid sizes (B=%d Hq=%d Hkv=%d N=%d d=%d)", B, Hq, Hkv, N, d);
     if (Hq % Hkv) return fail(LAMP_ERR_INVALID_ARG, "Hq=%d is not a multiple of Hkv=%d", Hq, Hkv);
     if (causal != 0 && causal != 1) return fail(LAMP_ERR_INVALID_ARG, "causal must be 0 or 1");
     if (window < 0) return fail(LAMP_ERR_INVALID_ARG, "window must be >= 0");
@@ -206,15 +206,17 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
 {
     int rc = check_common(q, k, B, Hq, Hkv, N, d, causal, window);
     if (rc) return rc;
-    if (!v || !o || !lse || !mask) return fail(LAMP_ERR_INVALID_ARG, "null pointer among v, o, lse, mask");
+    if ((B > 0 && N > 0) && (!v || !o || !lse || !mask))
+        return fail(LAMP_ERR_INVALID_ARG, "null pointer among v, o, lse, mask");
     if (!(delta >= 0.0) || std::isinf(delta)) return fail(LAMP_ERR_INVALID_ARG, "delta must be finite and >= 0");
     if (!(tau >= 0.0)) return fail(LAMP_ERR_INVALID_ARG, "tau must be >= 0 (or +inf)");
     if (flags & ~(unsigned)(LAMP_STAGE1_OFF | LAMP_MU_TRUNC)) return fail(LAMP_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
     if (bq <= 0 || bk <= 0 || nk <= 0) return fail(LAMP_ERR_INVALID_ARG, "block sizes must be positive");
-    if (N % bq || N % (bk * nk))
-        return fail(LAMP_ERR_INVALID_ARG, "N=%d must be a multiple of bq=%d and of bk*nk=%d", N, bq, bk * nk);
     if (!lamp::fwd_supported(d, bq, bk, nk))
         return fail(LAMP_ERR_UNSUPPORTED, "block sizes (bq=%d, bk=%d, nk=%d) not built for d=%d", bq, bk, nk, d);
+    if (B == 0 || N == 0) return LAMP_OK;   // nothing to compute
+    // the workspace holds whole query blocks and whole key tiles (zero padded)
+    const int Nq = (N + bq - 1) / bq * bq, Nk = (N + bk * nk - 1) / (bk * nk) * (bk * nk);
     int dev = 0;
     rc = current_device(&dev);
     if (rc) return rc;
@@ -225,7 +227,7 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
         std::lock_guard<std::mutex> lk(g_mu);
         rc = init_locked(dev);
         if (rc) return rc;
-        rc = workspace_locked(dev, B, Hq, Hkv, N, d, &w, true);
+        rc = workspace_locked(dev, B, Hq, Hkv, Nq, Nk, d, &w, true);
         if (rc) return rc;
         DeviceState *st = state_of(dev);
         p.exp16 = st->exp16;
@@ -242,6 +244,8 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
     p.Hq = Hq;
     p.Hkv = Hkv;
     p.N = N;
+    p.Nq = Nq;
+    p.Nk = Nk;
     p.causal = causal;
     p.window = window;
     p.delta = delta;
@@ -258,8 +262,8 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
         for (int i = 0; i < 3; ++i) HIP_TRY(hipEventCreate(&tc.e[i]));
         HIP_TRY(hipEventRecord(tc.e[0], s));
     }
-    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, d, scale_of(d), s));
-    HIP_TRY(lamp::launch_transpose_v(v, w.vt, B, Hkv, N, d, s));
+    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, Nq, Nk, d, scale_of(d), s));
+    HIP_TRY(lamp::launch_transpose_v(v, w.vt, B, Hkv, N, Nk, d, s));
     if (timed) HIP_TRY(hipEventRecord(tc.e[1], s));
     bool found = false;
     HIP_TRY(lamp::dispatch_fwd(d, bq, bk, nk, p, s, &found));
@@ -313,7 +317,7 @@ static int logits_common(const uint16_t *q, const uint16_t *k, int B, int Hq, in
     int rc = check_common(q, k, B, Hq, Hkv, N, d, causal, window);
     if (rc) return rc;
     if (!out) return fail(LAMP_ERR_INVALID_ARG, "null output pointer");
-    if (N % 16) return fail(LAMP_ERR_UNSUPPORTED, "N=%d is not a multiple of 16", N);
+    if (B == 0 || N == 0 || N % 16) return fail(LAMP_ERR_UNSUPPORTED, "N=%d is not a positive multiple of 16 (B=%d)", N, B);
     if (row0 < 0 || nrows <= 0 || row0 + nrows > N) return fail(LAMP_ERR_INVALID_ARG, "row range outside [0, N)");
     int dev = 0;
     rc = current_device(&dev);
@@ -322,7 +326,7 @@ static int logits_common(const uint16_t *q, const uint16_t *k, int B, int Hq, in
         std::lock_guard<std::mutex> lk(g_mu);
         rc = init_locked(dev);
         if (rc) return rc;
-        rc = workspace_locked(dev, B, Hq, Hkv, N, d, w);
+        rc = workspace_locked(dev, B, Hq, Hkv, N, N, d, w);
         if (rc) return rc;
     }
     *p = lamp::LogitsParams{};
@@ -348,7 +352,7 @@ int lamp_attn_logits8(const uint16_t *q, const uint16_t *k, int B, int Hq, int H
     if (rc) return rc;
     p.y8 = y8;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, d, scale_of(d), s));
+    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, N, N, d, scale_of(d), s));
     HIP_TRY(lamp::launch_logits8(p, d, s));
     return LAMP_OK;
 }
@@ -362,7 +366,7 @@ int lamp_attn_logits16(const uint16_t *q, const uint16_t *k, int B, int Hq, int 
     if (rc) return rc;
     p.y16 = y16;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, d, scale_of(d), s));
+    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, N, N, d, scale_of(d), s));
     HIP_TRY(lamp::launch_logits16(p, d, s));
     return LAMP_OK;
 }

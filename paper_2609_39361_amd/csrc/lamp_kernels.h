@@ -13,14 +13,15 @@ enum { MODE_LAMP = 0, MODE_PURE8 = 1, MODE_ALL16 = 2 };
 struct FwdParams {
     const float *qt;          // [B][Hq][N][D] pre-scaled queries, fp32
     const float *kt32;        // [B][Hkv][N][D] keys, fp32
-    const uint16_t *vt;       // [B][Hkv][D][N] bf16, V transposed
+    const uint16_t *vt;       // [B][Hkv][D][Nk] bf16, V transposed
     const uint16_t *exp16;    // ue5m11 shift code -> ue5m11 exp code
     const uint32_t *exp16hl;  // ue5m11 shift code -> bf16 high | low << 16 of the ue5m11 exp
     const uint16_t *lut8e;    // ue5m3 shift code -> bf16 bits of the ue5m3 exp
     float *o;                 // [B][Hq][N][D]
     float *lse;               // [B][Hq][N]
     uint8_t *mask;            // [B][Hq][N/BQ][N/BK]
-    int B, Hq, Hkv, N;
+    int B, Hq, Hkv, N;        // N: sequence length (visibility, O / lse rows)
+    int Nq, Nk;               // padded lengths: rows of qt, keys of kt32 / vt (whole blocks / tiles)
     int causal, window, mode;
     unsigned flags;           // LAMP_STAGE1_OFF | LAMP_MU_TRUNC, 0 outside the threshold mode
     double delta, tau;
@@ -37,9 +38,9 @@ struct LogitsParams {
 bool fwd_supported(int D, int BQ, int BK, int NK);
 hipError_t dispatch_fwd16(int D, int BQ, const FwdParams &p, hipStream_t s, bool *found);
 hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found);
-hipError_t launch_transpose_v(const uint16_t *v, uint16_t *vt, int B, int Hkv, int N, int D, hipStream_t s);
-hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float *kt32,
-                          int B, int Hq, int Hkv, int N, int D, float scale, hipStream_t s);
+hipError_t launch_transpose_v(const uint16_t *v, uint16_t *vt, int B, int Hkv, int N, int Nk, int D, hipStream_t s);
+hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float *kt32, int B, int Hq, int Hkv,
+                          int N, int Nq, int Nk, int D, float scale, hipStream_t s);
 hipError_t launch_logits8(const LogitsParams &p, int D, hipStream_t s);
 hipError_t launch_logits16(const LogitsParams &p, int D, hipStream_t s);
 hipError_t launch_build_tables(uint8_t *lut8, uint16_t *lut8e, uint16_t *exp16, uint32_t *exp16hl, unsigned *ambiguous,

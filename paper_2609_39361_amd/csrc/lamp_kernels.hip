@@ -17,39 +17,53 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // ------------------------------------------------------------------ prepass
 // q_tilde = RN32(q * s), fp32 [B][Hq][N][D].
-__global__ void prescale_q_kernel(const uint16_t *__restrict__ q, float *__restrict__ qt, float s, size_t n)
+// Pre-scaled queries q~ = RN32(q * s), rows padded with zeros from N to Nq:
+// qt [B*Hq][Nq][D] from q [B*Hq][N][D].
+__global__ void prescale_q_kernel(const uint16_t *__restrict__ q, float *__restrict__ qt, float s, int N, int Nq,
+                                  int D, size_t n)
 {
     size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     size_t stride = (size_t)gridDim.x * blockDim.x;
-    for (; i < n; i += stride) qt[i] = bf16_value(q[i]) * s;
+    for (; i < n; i += stride) {
+        const size_t c = i % (size_t)D, r = i / (size_t)D;
+        const size_t j = r % (size_t)Nq, bh = r / (size_t)Nq;
+        qt[i] = j < (size_t)N ? bf16_value(q[(bh * N + j) * D + c]) * s : 0.0f;
+    }
 }
 
-// K in fp32, same layout [B][Hkv][N][D] (bf16 -> fp32 is exact).
-__global__ void convert_k_kernel(const uint16_t *__restrict__ k, float *__restrict__ k32, size_t n)
+// K in fp32 (bf16 -> fp32 is exact), rows padded with zeros from N to Nk:
+// k32 [B*Hkv][Nk][D] from k [B*Hkv][N][D].
+__global__ void convert_k_kernel(const uint16_t *__restrict__ k, float *__restrict__ k32, int N, int Nk, int D,
+                                 size_t n)
 {
     size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     size_t stride = (size_t)gridDim.x * blockDim.x;
-    for (; i < n; i += stride) k32[i] = bf16_value(k[i]);
+    for (; i < n; i += stride) {
+        const size_t c = i % (size_t)D, r = i / (size_t)D;
+        const size_t j = r % (size_t)Nk, bh = r / (size_t)Nk;
+        k32[i] = j < (size_t)N ? bf16_value(k[(bh * N + j) * D + c]) : 0.0f;
+    }
 }
 
-// V^T [B*Hkv][D][N] from V [B*Hkv][N][D] (bf16): 64x64 tiles through LDS.
-// grid (N/64, D/64, B*Hkv); N and D are multiples of 64.
+// V^T [B*Hkv][D][Nk] from V [B*Hkv][N][D] (bf16), keys padded with zeros
+// from N to Nk: 64x64 tiles through LDS.  grid (Nk/64, D/64, B*Hkv); Nk and
+// D are multiples of 64.
 __global__ __launch_bounds__(256) void transpose_v_kernel(const uint16_t *__restrict__ v, uint16_t *__restrict__ vt,
-                                                          int N, int D)
+                                                          int N, int Nk, int D)
 {
     __shared__ uint16_t tile[64][66];
     const size_t bh = blockIdx.z;
     const int n0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
     const uint16_t *src = v + bh * (size_t)N * D;
-    uint16_t *dst = vt + bh * (size_t)D * N;
+    uint16_t *dst = vt + bh * (size_t)D * Nk;
     for (int e = threadIdx.x; e < 64 * 64; e += 256) {
         const int r = e / 64, c = e % 64;
-        tile[r][c] = src[(size_t)(n0 + r) * D + c0 + c];
+        tile[r][c] = n0 + r < N ? src[(size_t)(n0 + r) * D + c0 + c] : (uint16_t)0;
     }
     __syncthreads();
     for (int e = threadIdx.x; e < 64 * 64; e += 256) {
         const int c = e / 64, r = e % 64;
-        dst[(size_t)(c0 + c) * N + n0 + r] = tile[r][c];
+        dst[(size_t)(c0 + c) * Nk + n0 + r] = tile[r][c];
     }
 }
 
@@ -197,21 +211,21 @@ __global__ void selftest_exp_doc_kernel(const double *__restrict__ x, double *__
 }
 
 // ------------------------------------------------------------------ launchers
-hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float *kt32,
-                          int B, int Hq, int Hkv, int N, int D, float scale, hipStream_t s)
+hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float *kt32, int B, int Hq, int Hkv,
+                          int N, int Nq, int Nk, int D, float scale, hipStream_t s)
 {
-    size_t nq = (size_t)B * Hq * N * D, nk = (size_t)B * Hkv * N * D;
+    size_t nq = (size_t)B * Hq * Nq * D, nk = (size_t)B * Hkv * Nk * D;
     unsigned gq = (unsigned)((nq + 255) / 256 < 65536 ? (nq + 255) / 256 : 65536);
     unsigned gk = (unsigned)((nk + 255) / 256 < 65536 ? (nk + 255) / 256 : 65536);
-    hipLaunchKernelGGL(prescale_q_kernel, dim3(gq), dim3(256), 0, s, q, qt, scale, nq);
-    hipLaunchKernelGGL(convert_k_kernel, dim3(gk), dim3(256), 0, s, k, kt32, nk);
+    hipLaunchKernelGGL(prescale_q_kernel, dim3(gq), dim3(256), 0, s, q, qt, scale, N, Nq, D, nq);
+    hipLaunchKernelGGL(convert_k_kernel, dim3(gk), dim3(256), 0, s, k, kt32, N, Nk, D, nk);
     return hipGetLastError();
 }
 
-hipError_t launch_transpose_v(const uint16_t *v, uint16_t *vt, int B, int Hkv, int N, int D, hipStream_t s)
+hipError_t launch_transpose_v(const uint16_t *v, uint16_t *vt, int B, int Hkv, int N, int Nk, int D, hipStream_t s)
 {
-    hipLaunchKernelGGL(transpose_v_kernel, dim3((unsigned)(N / 64), (unsigned)(D / 64), (unsigned)(B * Hkv)), dim3(256),
-                       0, s, v, vt, N, D);
+    hipLaunchKernelGGL(transpose_v_kernel, dim3((unsigned)(Nk / 64), (unsigned)(D / 64), (unsigned)(B * Hkv)),
+                       dim3(256), 0, s, v, vt, N, Nk, D);
     return hipGetLastError();
 }
 

@@ -99,14 +99,15 @@ MU_TRUNC = 2     # 8-bit shifts against mu_hat truncated to e4m3
 
 def attn_fwd(q, k, v, causal=True, window=0, bq=128, bk=16, nk=4, delta=2.0 ** -8, tau=0.5, out=None, flags=0):
     """LampAttention forward pass.  Returns (o fp32 [B,Hq,N,d], lse fp32
-    [B,Hq,N], mask uint8 [B,Hq,N/bq,N/bk]).  `out` may supply those three
-    tensors to write into; `flags` selects the variants STAGE1_OFF, MU_TRUNC."""
+    [B,Hq,N], mask uint8 [B,Hq,ceil(N/bq),ceil(N/(bk*nk))*nk]); N need not be
+    a multiple of the block sizes.  `out` may supply those three tensors to
+    write into; `flags` selects the variants STAGE1_OFF, MU_TRUNC."""
     B, Hq, Hkv, N, d = _check_inputs(q, k, v)
     dev = q.device
     if out is None:
         o = torch.empty((B, Hq, N, d), dtype=torch.float32, device=dev)
         lse = torch.empty((B, Hq, N), dtype=torch.float32, device=dev)
-        mask = torch.empty((B, Hq, N // bq, N // bk), dtype=torch.uint8, device=dev)
+        mask = torch.empty((B, Hq, -(-N // bq), -(-N // (bk * nk)) * nk), dtype=torch.uint8, device=dev)
     else:
         o, lse, mask = out
     with torch.cuda.device(dev):
@@ -201,7 +202,7 @@ def timing_read():
 
 
 def mask_stats(mask, nk):
-    """Recompute statistics from a mask [B,Hq,N/bq,N/bk]: per key tile (nk
+    """Recompute statistics from a mask [B,Hq,nqb,ntiles*nk]: per key tile (nk
     sub-blocks, at least one active) the number of 16-bit sub-blocks, as a
     histogram 0..nk, plus counts per code.  Reporting only."""
     m = mask.reshape(-1, nk)

@@ -169,6 +169,13 @@ def make_inputs(w: Workload, device="cpu"):
     if gain != 1.0:
         q *= gain
         k *= gain
+    # degenerate inputs for tests: all queries zero; every query and key row of
+    # a head equal to its first row (all logits of a row equal)
+    if w.extra.get("zero_q"):
+        q.zero_()
+    if w.extra.get("const"):
+        q[:] = q[:, :, :1, :].clone()
+        k[:] = k[:, :, :1, :].clone()
     out = tuple(t.to(torch.bfloat16).contiguous() for t in (q, k, v))
     if device != "cpu":
         out = tuple(t.to(device) for t in out)

@@ -284,3 +284,53 @@ def test_fwd_config5_sampled(L, tau):
     err, mask = _compare_fwd(L, w, tau, qblocks=qbl, keep=True)
     _say("config 5 tau %s sampled: O err %.2e, mask %s (%.1f s)" % (tau, err, np.bincount(mask.ravel(), minlength=4),
                                                                    time.time() - t0))
+
+
+# ------------------------------------------------------------------ edge cases
+RAGGED_CASES = [
+    W.small("r_d128_n300", N=300, d=128, Hq=2, Hkv=1, bq=128, bk=16, nk=4, causal=1, seed=301),
+    W.small("r_d128_n77", N=77, d=128, Hq=1, Hkv=1, bq=128, bk=16, nk=4, causal=1, seed=302),
+    W.small("r_d128_nc_n200", N=200, d=128, Hq=1, Hkv=1, bq=64, bk=16, nk=4, causal=0, seed=303),
+    W.small("r_d128_win_n333", N=333, d=128, Hq=1, Hkv=1, bq=128, bk=16, nk=4, causal=1, window=70, seed=304),
+    W.small("r_d64_n200", N=200, d=64, Hq=2, Hkv=2, bq=64, bk=16, nk=4, causal=1, seed=305),
+    W.small("r_d128_bk64_n300", N=300, d=128, Hq=2, Hkv=1, bq=128, bk=64, nk=4, causal=1, seed=306),
+    W.small("r_d256_n150", N=150, d=256, Hq=1, Hkv=1, bq=128, bk=16, nk=4, causal=1, seed=307),
+]
+
+
+@pytest.mark.parametrize("tau", [math.inf, 0.5, 2.0 ** -5, 0.0])
+@pytest.mark.parametrize("w", RAGGED_CASES, ids=[w.name for w in RAGGED_CASES])
+def test_fwd_ragged_lengths(L, w, tau):
+    """N not a multiple of b_q or of the key tile: partial last query block
+    and key tile, through both kernels."""
+    _compare_fwd(L, w, tau)
+
+
+def test_fwd_empty_inputs(L):
+    for shape_q, shape_k in (((1, 2, 0, 128), (1, 1, 0, 128)), ((0, 2, 256, 128), (0, 1, 256, 128))):
+        q = torch.zeros(shape_q, dtype=torch.bfloat16, device="cuda")
+        k = torch.zeros(shape_k, dtype=torch.bfloat16, device="cuda")
+        o, lse, mask = L.attn_fwd(q, k, k, True, 0, 128, 16, 4, 2.0 ** -8, 0.5)
+        torch.cuda.synchronize()
+        assert o.numel() == 0 and lse.numel() == 0 and mask.numel() == 0
+
+
+DEGENERATE = [
+    # all queries zero: every logit is 0, |mu_hat| delta = 0, so the margin
+    # test fails on every tile and everything is recomputed in stage 1
+    W.small("g_zero_q", N=256, d=128, Hq=1, Hkv=1, bq=128, bk=16, nk=4, causal=1, seed=311, extra={"zero_q": 1}),
+    # constant rows: all logits of a row equal, every threat ties
+    W.small("g_const", N=256, d=128, Hq=1, Hkv=1, bq=128, bk=16, nk=4, causal=1, seed=312, extra={"const": 1}),
+    # large magnitudes: e4m3 and e4m11 saturate on most logits
+    W.small("g_saturate", N=256, d=128, Hq=1, Hkv=1, bq=128, bk=16, nk=4, causal=1, seed=313, extra={"gain": 8.0}),
+    W.small("g_saturate_d64_bk64", N=256, d=64, Hq=1, Hkv=1, bq=64, bk=64, nk=4, causal=0, seed=314,
+            extra={"gain": 8.0}),
+]
+
+
+@pytest.mark.parametrize("tau", [math.inf, 0.5, 0.0])
+@pytest.mark.parametrize("w", DEGENERATE, ids=[w.name for w in DEGENERATE])
+def test_fwd_degenerate_inputs(L, w, tau):
+    err, mask = _compare_fwd(L, w, tau)
+    if "zero_q" in w.extra and tau == 0.5:
+        assert np.all((mask == 1) | (mask == 3))
