@@ -221,8 +221,12 @@ def test_fwd_variants_config3_sampled(L, flags):
     _say("config 3 flags %d tau 2^-5 sampled: O err %.2e, mask %s" % (flags, err, np.bincount(mask.ravel(), minlength=4)))
 
 
-def test_fwd_delta_variant(L):
-    _compare_fwd(L, FWD_CASES[0], 0.5, delta=2.0 ** -4)
+@pytest.mark.parametrize("delta", [2.0 ** -4, 0.003, 0.0])
+@pytest.mark.parametrize("w", [FWD_CASES[0], FWD_CASES[1]], ids=[FWD_CASES[0].name, FWD_CASES[1].name])
+def test_fwd_delta_variant(L, w, delta):
+    """Safety margins that are powers of two or zero (the kernels test them
+    in fixed point) and one that is not (fp64 test)."""
+    _compare_fwd(L, w, 0.5, delta=delta)
 
 
 def test_fwd_config1_full(L):
