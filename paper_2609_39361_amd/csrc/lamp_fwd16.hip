@@ -78,7 +78,7 @@ __device__ __forceinline__ float fx_value(int f) { return (float)f * (1.0f / 131
 
 } // namespace
 
-template <int D, int BQ>
+template <int D, int BQ, int MODE>
 __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdParams p)
 {
     using C = Cfg16<D, BQ>;
@@ -107,7 +107,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     const int hk = h / (p.Hq / p.Hkv);
     const int q0 = qb * BQ;
     const float NEG_INF = -__builtin_inff();
-    const int mode = p.mode;
+    constexpr int mode = MODE;   // one instantiation per mode: only its path is compiled
     const bool stage1_off = (p.flags & LAMP_STAGE1_OFF) != 0u;   // flags are 0 outside the threshold mode
     const bool mu_trunc = (p.flags & LAMP_MU_TRUNC) != 0u;
 
@@ -880,17 +880,25 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
 }
 
 // ------------------------------------------------------------------ launcher
-template <int D, int BQ>
-static hipError_t launch_fwd16(const FwdParams &p, hipStream_t s)
+template <int D, int BQ, int MODE>
+static hipError_t launch_fwd16_mode(const FwdParams &p, hipStream_t s)
 {
     using C = Cfg16<D, BQ>;
-    auto kern = lamp_fwd16_kernel<D, BQ>;
+    auto kern = lamp_fwd16_kernel<D, BQ, MODE>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
     if (e != hipSuccess) return e;
     dim3 grid((unsigned)(p.B * p.Hq * (p.Nq / BQ)));
     hipLaunchKernelGGL(kern, grid, dim3(256), C::LDS, s, p);
     return hipGetLastError();
+}
+
+template <int D, int BQ>
+static hipError_t launch_fwd16(const FwdParams &p, hipStream_t s)
+{
+    if (p.mode == MODE_PURE8) return launch_fwd16_mode<D, BQ, MODE_PURE8>(p, s);
+    if (p.mode == MODE_ALL16) return launch_fwd16_mode<D, BQ, MODE_ALL16>(p, s);
+    return launch_fwd16_mode<D, BQ, MODE_LAMP>(p, s);
 }
 
 hipError_t dispatch_fwd16(int D, int BQ, const FwdParams &p, hipStream_t s, bool *found)
