@@ -100,11 +100,31 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     const int tid = threadIdx.x;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;   // w is wave-uniform
     const int nqb = p.Nq / BQ;   // query blocks per head (the last may be partial)
-    const int BH = p.B * p.Hq;
-    const int qb = nqb - 1 - (int)(blockIdx.x / BH);   // longest blocks first under causality
-    const int bh = blockIdx.x % BH;
-    const int b = bh / p.Hq, h = bh % p.Hq;
-    const int hk = h / (p.Hq / p.Hkv);
+    // Block order.  Workgroups are handed to the 8 XCDs round-robin (block i to
+    // XCD i mod 8), each XCD with its own L2.  When the B*Hkv key/value heads
+    // split evenly over the XCDs, XCD x takes the heads x, x+8, ... and runs the
+    // query heads of one group next to each other, so the keys and values
+    // they share stay in that XCD's L2; every XCD walks the query blocks
+    // longest first (causality).  Otherwise: longest first over all heads.
+    const int G = p.Hq / p.Hkv, KH = p.B * p.Hkv;
+    int qb, b, h, hk;
+    if (KH % 8 == 0) {
+        const int x = (int)(blockIdx.x % 8u), r = (int)(blockIdx.x / 8u);
+        const int per = (KH / 8) * G;             // blocks of one query-block rank on an XCD
+        const int qrank = r / per, rest = r % per;
+        const int j = x + 8 * (rest / G);         // key/value head, over the batch
+        qb = nqb - 1 - qrank;
+        b = j / p.Hkv;
+        hk = j % p.Hkv;
+        h = hk * G + rest % G;
+    } else {
+        const int BH = p.B * p.Hq;
+        qb = nqb - 1 - (int)(blockIdx.x / BH);   // longest blocks first under causality
+        const int bh = blockIdx.x % BH;
+        b = bh / p.Hq;
+        h = bh % p.Hq;
+        hk = h / G;
+    }
     const int q0 = qb * BQ;
     const float NEG_INF = -__builtin_inff();
     constexpr int mode = MODE;   // one instantiation per mode: only its path is compiled
