@@ -46,6 +46,11 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
+def _mode_of(tau):
+    """Template mode of the pipelined kernel: 0 threshold, 1 pure 8-bit, 2 all 16-bit."""
+    return 1 if math.isinf(tau) else (2 if tau == 0 else 0)
+
+
 def _profile_record(path, tag, workload, tau, flags=0):
     """The `tag: {json}` line of a committed profile summary, when it was taken
     on the current kernel sources and on this workload; else None."""
@@ -234,7 +239,8 @@ def main():
             "unit": "T VALU lane-ops/s",
             "frac": achieved / peak,
             "traffic": measured_traffic(w.name, tau, args.flags),
-            "kernel": ("lamp_fwd16_kernel<%d,%d>" % (w.d, w.bq)) if (w.bk == 16 and w.d >= 128)
+            "kernel": ("lamp_fwd16_kernel<%d,%d,%d>" % (w.d, w.bq, _mode_of(tau)))
+                      if (w.bk == 16 and w.d >= 128)
                       else ("lamp_fwd_kernel<%d,%d,%d,%d>" % (w.d, w.bq, w.bk, w.nk)),
             "kernel_ms": kernel_ms,
             "prepass_ms": pre_ms_sum / launches,
