@@ -277,6 +277,133 @@ int oracle_tables(uint8_t *lut8, uint16_t *exp16)
 }
 
 /* ------------------------------------------------------------------------ */
+/* The "SIM" precision profile (Sec. 4.1): the numerics of the paper's own   */
+/* simulation, which stores the 8-bit and 16-bit numbers in FP32 with the    */
+/* mantissa cut to 3 and 11 bits, accumulates by recursive FP32 FMA with a    */
+/* rounding after every step, and models the exponentials as correctly        */
+/* rounded.  Readings: "cut" is round-to-nearest-even (as for the hardware    */
+/* formats); the exponent range is FP32's, with FP32's gradual underflow (the */
+/* quantum below 2^-126 is 2^(-126-p)); there is no saturation, overflow      */
+/* gives an infinity as in FP32.                                              */
+/* ------------------------------------------------------------------------ */
+
+/* Round an exact double to p stored mantissa bits in FP32's exponent range. */
+static double round_sim(double x, int p)
+{
+    if (x == 0.0 || !isfinite(x)) return x;
+    double ax = fabs(x);
+    int E;
+    (void)frexp(ax, &E);
+    int e = E - 1;                                /* ax in [2^e, 2^(e+1)) */
+    if (e < -126) e = -126;
+    double quantum = ldexp(1.0, e - p);
+    double r = nearbyint(ax / quantum) * quantum; /* ties to even */
+    if (r >= 0x1p128) r = INFINITY;
+    return copysign(r, x);
+}
+
+/* Round the exact real hi + lo, given as hi = RN64(hi + lo) and its error lo
+ * (|lo| <= ulp(hi)/2), to p mantissa bits.  Only when hi is exactly halfway
+ * between two grid values can lo change the result: then its sign decides. */
+static double round_sim_sum(double hi, double lo, int p)
+{
+    double r = round_sim(hi, p);
+    if (lo == 0.0 || hi == 0.0 || !isfinite(hi)) return r;
+    double ah = fabs(hi);
+    int E;
+    (void)frexp(ah, &E);
+    int e = E - 1;
+    if (e < -126) e = -126;
+    double quantum = ldexp(1.0, e - p);
+    double t = ah / quantum;
+    if (t - floor(t) != 0.5) return r;
+    double mag = ((lo > 0.0) == (hi > 0.0)) ? (floor(t) + 1.0) * quantum : floor(t) * quantum;
+    if (mag >= 0x1p128) mag = INFINITY;
+    return copysign(mag, hi);
+}
+
+/* x rounded toward zero to p mantissa bits in FP32's exponent range. */
+static double trunc_sim(double x, int p)
+{
+    if (x == 0.0 || !isfinite(x)) return x;
+    double ax = fabs(x);
+    int E;
+    (void)frexp(ax, &E);
+    int e = E - 1;
+    if (e < -126) e = -126;
+    double quantum = ldexp(1.0, e - p);
+    return copysign(floor(ax / quantum) * quantum, x);
+}
+
+static long double round_sim_ld(long double x, int p)
+{
+    if (x == 0.0L) return x;
+    int E;
+    (void)frexpl(x, &E);
+    int e = E - 1;
+    if (e < -126) e = -126;
+    long double quantum = ldexpl(1.0L, e - p);
+    return nearbyintl(x / quantum) * quantum;
+}
+
+static int g_sim_fail = 0;   /* set if an exponential lies too close to a midpoint */
+
+/* E = RN_p(exp(-s)) for a shift s >= 0, correctly rounded: exp is evaluated
+ * in long double, and the enclosure exp(-s) (1 -+ 2^-60) must round to one
+ * value (otherwise g_sim_fail is raised; the test suite re-derives every
+ * value that occurs in 60-digit arithmetic). */
+static double sim_exp(double s, int p)
+{
+    long double e = expl(-(long double)s);
+    long double a = round_sim_ld(e * (1.0L - 0x1p-60L), p), b = round_sim_ld(e * (1.0L + 0x1p-60L), p);
+    if (a != b) __atomic_store_n(&g_sim_fail, 1, __ATOMIC_RELAXED);
+    return (double)round_sim_ld(e, p);
+}
+
+/* Shifted exponential in the SIM profile: s = RN_p(max(0, mu_hat - y)) of the
+ * exact difference (a TwoSum gives it as hi + lo), E = RN_p(exp(-s)); p = 11
+ * for the 16-bit path, 3 for the 8-bit one. */
+static double shifted_exp_sim(double mu_hat, double y, int high)
+{
+    const int p = high ? 11 : 3;
+    double a = mu_hat, b = -y;
+    double hi = a + b, bb = hi - a;
+    double lo = (a - (hi - bb)) + (b - bb);
+    double x = (hi > 0.0) ? round_sim_sum(hi, lo, p) : 0.0;
+    return sim_exp(x, p);
+}
+
+int oracle_round_sim(int p, const double *x, double *y, int64_t n)
+{
+    if (p != 3 && p != 11) return -1;
+    for (int64_t i = 0; i < n; ++i) y[i] = round_sim(x[i], p);
+    return 0;
+}
+
+/* s[i] = RN_p(max(0, mu[i] - y[i])) from the exact difference. */
+int oracle_shift_sim(int p, const double *mu, const double *y, double *s, int64_t n)
+{
+    if (p != 3 && p != 11) return -1;
+    for (int64_t i = 0; i < n; ++i) {
+        double a = mu[i], b = -y[i];
+        double hi = a + b, bb = hi - a;
+        double lo = (a - (hi - bb)) + (b - bb);
+        s[i] = (hi > 0.0) ? round_sim_sum(hi, lo, p) : 0.0;
+    }
+    return 0;
+}
+
+int oracle_sim_exp(int p, const double *s, double *e, int64_t n)
+{
+    if (p != 3 && p != 11) return -1;
+    g_sim_fail = 0;
+    for (int64_t i = 0; i < n; ++i) e[i] = sim_exp(s[i], p);
+    return g_sim_fail ? -2 : 0;
+}
+
+double oracle_trunc_sim3(double x) { return trunc_sim(x, 3); }
+
+/* ------------------------------------------------------------------------ */
 /* Logits.                                                                   */
 /* ------------------------------------------------------------------------ */
 
@@ -326,6 +453,26 @@ static double logit16(const float *qt, const uint16_t *k, int d)
     float acc = 0.0f;
     for (int c = 0; c < d; ++c) acc = fmaf(qt[c], bf16_to_f32(k[c]), acc);
     return round_to_fmt((double)acc, &F_E4M11);
+}
+
+/* SIM profile logits: the same recursions with the roundings of the profile
+ * (3 mantissa bits after every step; one rounding to 11 bits at the end of
+ * the FP32 chain, as for the e4m11 logit). */
+static double logit8_sim(const float *qt, const uint16_t *k, int d)
+{
+    float acc = 0.0f;
+    for (int c = 0; c < d; ++c) {
+        float t = fmaf(qt[c], bf16_to_f32(k[c]), acc);
+        acc = (float)round_sim((double)t, 3);
+    }
+    return (double)acc;
+}
+
+static double logit16_sim(const float *qt, const uint16_t *k, int d)
+{
+    float acc = 0.0f;
+    for (int c = 0; c < d; ++c) acc = fmaf(qt[c], bf16_to_f32(k[c]), acc);
+    return round_sim((double)acc, 11);
 }
 
 static int visible(int64_t i, int64_t j, int causal, int window)
@@ -390,6 +537,34 @@ int oracle_logits16(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv
     return 0;
 }
 
+/* SIM profile logit values (high = 0: 8-bit recursion, 1: 16-bit), same
+ * layout as above; invisible entries NaN. */
+int oracle_logits_sim(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv, int N, int d,
+                      int causal, int window, int row0, int nrows, int high, double *out, int nthreads)
+{
+    if (Hq % Hkv) return -1;
+    int G = Hq / Hkv;
+    float s = scale_of(d);
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for collapse(3) schedule(dynamic)
+#endif
+    for (int b = 0; b < B; ++b)
+        for (int h = 0; h < Hq; ++h)
+            for (int r = 0; r < nrows; ++r) {
+                int64_t j = row0 + r;
+                float qt[1024];
+                prescale(q + (((int64_t)b * Hq + h) * N + j) * d, d, s, qt);
+                const uint16_t *kb = k + ((int64_t)b * Hkv + h / G) * N * d;
+                double *o = out + (((int64_t)b * Hq + h) * nrows + r) * N;
+                for (int64_t i = 0; i < N; ++i) {
+                    if (!visible(i, j, causal, window)) { o[i] = NAN; continue; }
+                    o[i] = high ? logit16_sim(qt, kb + i * d, d) : logit8_sim(qt, kb + i * d, d);
+                }
+            }
+    return 0;
+}
+
 /* ------------------------------------------------------------------------ */
 /* The forward pass (Algorithm 1).                                           */
 /* ------------------------------------------------------------------------ */
@@ -403,8 +578,10 @@ enum { MASK_LOW = 0, MASK_STAGE1 = 1, MASK_STAGE2 = 2, MASK_INACTIVE = 3 };
  *  ORACLE_MU_TRUNC: the 8-bit shifts use mu_hat truncated to e4m3 (Sec. 3.3:
  *    the running maxima may be rounded to e4m3 for the low-precision shifts by
  *    dropping the low mantissa bits).
- * Both apply for 0 < tau < inf; the two end modes ignore them. */
-enum { ORACLE_STAGE1_OFF = 1, ORACLE_MU_TRUNC = 2 };
+ * Both apply for 0 < tau < inf; the two end modes ignore them.
+ *  ORACLE_SIM: the "SIM" precision profile above (Sec. 4.1) in place of the
+ *    hardware formats of Sec. 3.3, in every mode. */
+enum { ORACLE_STAGE1_OFF = 1, ORACLE_MU_TRUNC = 2, ORACLE_SIM = 4 };
 
 /* x truncated (rounded toward zero) to e4m3; reading: values beyond the
  * largest e4m3 number saturate to +-448; infinities are kept. */
@@ -473,6 +650,10 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
     const int all16 = (A->tau == 0.0);
     const int stage1_off = !pure8 && !all16 && (A->flags & ORACLE_STAGE1_OFF);
     const int mu_trunc = !pure8 && !all16 && (A->flags & ORACLE_MU_TRUNC);
+    const int sim = (A->flags & ORACLE_SIM) != 0;
+    double (*const y8f)(const float *, const uint16_t *, int) = sim ? logit8_sim : logit8;
+    double (*const y16f)(const float *, const uint16_t *, int) = sim ? logit16_sim : logit16;
+    double (*const expf_)(double, double, int) = sim ? shifted_exp_sim : shifted_exp;
 
     float *qt = (float *)malloc(sizeof(float) * (size_t)bq * d);
     double *mu = (double *)malloc(sizeof(double) * bq);
@@ -522,7 +703,7 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
             for (int ii = 0; ii < T; ++ii)
                 for (int j = 0; j < bq; ++j)
                     Y[(size_t)ii * bq + j] = vis[(size_t)ii * bq + j]
-                        ? logit8(qt + (size_t)j * d, kbase + (k0 + ii) * d, d) : NAN;
+                        ? y8f(qt + (size_t)j * d, kbase + (k0 + ii) * d, d) : NAN;
         }
         /* Column maxima per sub-block: m8[theta][j] (Sec. 3.1, C and T). */
         for (int th = 0; th < nk; ++th)
@@ -553,7 +734,7 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
                     for (int j = 0; j < bq; ++j) {
                         size_t ix = (size_t)ii * bq + j;
                         if (!vis[ix]) continue;
-                        Y[ix] = logit16(qt + (size_t)j * d, kbase + (k0 + ii) * d, d);
+                        Y[ix] = y16f(qt + (size_t)j * d, kbase + (k0 + ii) * d, d);
                         if (Y[ix] > muh[j]) muh[j] = Y[ix];
                     }
             }
@@ -599,7 +780,7 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
                     for (int j = 0; j < bq; ++j) {
                         size_t ix = (size_t)ii * bq + j;
                         if (!vis[ix]) continue;
-                        Y[ix] = logit16(qt + (size_t)j * d, kbase + (k0 + ii) * d, d);
+                        Y[ix] = y16f(qt + (size_t)j * d, kbase + (k0 + ii) * d, d);
                         if (Y[ix] > muh[j]) muh[j] = Y[ix];
                     }
             }
@@ -613,8 +794,9 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
                 for (int j = 0; j < bq; ++j) {
                     size_t ix = (size_t)ii * bq + j;
                     const int high = prec[th] == MASK_STAGE1;
-                    const double ref = (!high && mu_trunc) ? trunc_e4m3(muh[j]) : muh[j];
-                    E[ix] = (prec[th] == MASK_INACTIVE || !vis[ix]) ? 0.0 : shifted_exp(ref, Y[ix], high);
+                    const double ref = (!high && mu_trunc) ? (sim ? trunc_sim(muh[j], 3) : trunc_e4m3(muh[j]))
+                                                           : muh[j];
+                    E[ix] = (prec[th] == MASK_INACTIVE || !vis[ix]) ? 0.0 : expf_(ref, Y[ix], high);
                 }
         /* lambda_hat = exp(mu - mu_hat) in high precision (Sec. 2.2):
          * 1 when mu_hat = -inf (no mass yet), 0 when mu = -inf < mu_hat. */
@@ -622,8 +804,10 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
             if (muh[j] == -INFINITY) lam[j] = 1.0;
             else if (mu[j] == -INFINITY) lam[j] = 0.0;
             else lam[j] = exp_doc(mu[j] - muh[j]);
-            /* S_j = sum_i E_ij is exact in fp64 (every E is a multiple of
-             * 2^-41 in [0,1] and a tile holds at most 2^9 of them). */
+            /* S_j = sum_i E_ij, keys ascending.  With the hardware formats
+             * the sum is exact in fp64 (every E is a multiple of 2^-41 in
+             * [0,1] and a tile holds at most 2^9 of them); in the SIM profile
+             * (E down to 2^-137) it is the fp64 sum in this order. */
             double S = 0.0;
             for (int ii = 0; ii < T; ++ii) S += E[(size_t)ii * bq + j];
             omh[j] = fma(lam[j], om[j], S);
@@ -680,8 +864,8 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
                     for (int j = 0; j < bq; ++j) {
                         size_t ix = (size_t)ii * bq + j;
                         if (!vis[ix]) continue;
-                        Y[ix] = logit16(qt + (size_t)j * d, kbase + (k0 + ii) * d, d);
-                        E[ix] = shifted_exp(muh[j], Y[ix], 1);
+                        Y[ix] = y16f(qt + (size_t)j * d, kbase + (k0 + ii) * d, d);
+                        E[ix] = expf_(muh[j], Y[ix], 1);
                     }
             }
         }
@@ -719,7 +903,8 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
  * ceil(N/(bk*nk))*nk] u8 (any N >= 0; B = 0 or N = 0 computes nothing).
  * If qblocks != NULL only the listed query blocks (flat index
  * (b*Hq + h)*ceil(N/bq) + qb) are computed; other outputs are left untouched.
- * Returns 0, or -1 on invalid arguments / -2 on a table failure. */
+ * Returns 0, or -1 on invalid arguments / -2 on a table failure or, in the SIM
+ * profile, an exponential too close to a rounding midpoint to be certified. */
 int lamp_oracle_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                     int B, int Hq, int Hkv, int N, int d, int causal, int window,
                     int bq, int bk, int nk, double delta, double tau, unsigned flags,
@@ -731,8 +916,9 @@ int lamp_oracle_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
     if (window < 0 || (window > 0 && !causal)) return -1;
     if (!(tau >= 0.0) || !(delta >= 0.0)) return -1;
     if (build_tables()) return -2;
-    if (flags & ~(unsigned)(ORACLE_STAGE1_OFF | ORACLE_MU_TRUNC)) return -1;
+    if (flags & ~(unsigned)(ORACLE_STAGE1_OFF | ORACLE_MU_TRUNC | ORACLE_SIM)) return -1;
     if (B == 0 || N == 0) return 0;                /* nothing to compute */
+    g_sim_fail = 0;
     fwd_args_t A = {q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, flags, o, lse, mask};
     const int nqbh = (N + bq - 1) / bq;
     int64_t nqb = (int64_t)B * Hq * nqbh;
@@ -748,7 +934,7 @@ int lamp_oracle_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
         int b = (int)(f / ((int64_t)nqbh * Hq));
         fwd_qblock(&A, b, h, qb);
     }
-    return 0;
+    return g_sim_fail ? -2 : 0;
 }
 
 int oracle_max_threads(void)

@@ -58,6 +58,16 @@ def lib():
         _lib.oracle_tables.restype = i32
         _lib.oracle_scale.argtypes = [i32]
         _lib.oracle_scale.restype = ctypes.c_float
+        for name in ("oracle_round_sim", "oracle_sim_exp"):
+            fn = getattr(_lib, name)
+            fn.argtypes = [i32, P, P, i64]
+            fn.restype = i32
+        _lib.oracle_shift_sim.argtypes = [i32, P, P, P, i64]
+        _lib.oracle_shift_sim.restype = i32
+        _lib.oracle_trunc_sim3.argtypes = [f64]
+        _lib.oracle_trunc_sim3.restype = f64
+        _lib.oracle_logits_sim.argtypes = [P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, i32]
+        _lib.oracle_logits_sim.restype = i32
         _lib.oracle_max_threads.argtypes = []
         _lib.oracle_max_threads.restype = i32
     return _lib
@@ -155,9 +165,55 @@ def logits16(q, k, causal, window, row0, nrows, nthreads=0):
     return out
 
 
+# ---------------------------------------------------------------- SIM profile
+def round_sim(p, x):
+    """Round doubles to p = 3 or 11 mantissa bits in FP32's exponent range (RNE, overflow to inf)."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    y = np.empty_like(x)
+    assert lib().oracle_round_sim(p, _ptr(x), _ptr(y), x.size) == 0
+    return y
+
+
+def shift_sim(p, mu, y):
+    """RN_p(max(0, mu - y)) of the exact difference."""
+    mu = np.ascontiguousarray(mu, dtype=np.float64)
+    y = np.ascontiguousarray(np.broadcast_to(y, mu.shape), dtype=np.float64)
+    s = np.empty_like(mu)
+    assert lib().oracle_shift_sim(p, _ptr(mu), _ptr(y), _ptr(s), mu.size) == 0
+    return s
+
+
+def sim_exp(p, s):
+    """RN_p(exp(-s)), correctly rounded; raises if an enclosure cannot be certified."""
+    s = np.ascontiguousarray(s, dtype=np.float64)
+    e = np.empty_like(s)
+    rc = lib().oracle_sim_exp(p, _ptr(s), _ptr(e), s.size)
+    if rc != 0:
+        raise RuntimeError("oracle_sim_exp: %d" % rc)
+    return e
+
+
+def trunc_sim3(x):
+    return lib().oracle_trunc_sim3(float(x))
+
+
+def logits_sim(q, k, causal, window, row0, nrows, high, nthreads=0):
+    """SIM-profile logit values (high=0: 8-bit recursion, 1: 16-bit): [B,Hq,nrows,N], NaN = invisible."""
+    q = np.ascontiguousarray(q, dtype=np.uint16)
+    k = np.ascontiguousarray(k, dtype=np.uint16)
+    B, Hq, N, d = q.shape
+    Hkv = k.shape[1]
+    out = np.empty((B, Hq, nrows, N), dtype=np.float64)
+    rc = lib().oracle_logits_sim(_ptr(q), _ptr(k), B, Hq, Hkv, N, d, int(causal), int(window),
+                                 row0, nrows, int(high), _ptr(out), nthreads)
+    assert rc == 0
+    return out
+
+
 # ---------------------------------------------------------------- forward
 STAGE1_OFF = 1   # the first stage disabled: mu_hat from the 8-bit maxima, stage 2 alone recomputes
-MU_TRUNC = 2     # 8-bit shifts against mu_hat truncated to e4m3
+MU_TRUNC = 2     # 8-bit shifts against mu_hat truncated to e4m3 (SIM: to 3 mantissa bits)
+SIM = 4          # the "SIM" precision profile (FP32 range, 3/11-bit mantissas, no saturation)
 
 
 def trunc_e4m3(x):

@@ -19,6 +19,10 @@ FMT = {
     "ue5m11_shift": (11, -14, 131040.0, 15, 5, False),
     "ue5m3_exp": (3, -30, 1.875, 31, 5, False),
     "ue5m11_exp": (11, -30, 2.0 - 2.0 ** -11, 31, 5, False),
+    # the "SIM" profile (Sec. 4.1): FP32's exponent range and gradual
+    # underflow, 3 or 11 mantissa bits, no saturation (overflow gives inf)
+    "sim3": (3, -126, np.inf, 127, 8, True),
+    "sim11": (11, -126, np.inf, 127, 8, True),
 }
 
 
@@ -43,8 +47,17 @@ def np_round(x, fmt):
     r = n.astype(np.float64) * np.exp2(te.astype(np.float64))
     r = np.where(ax == 0, 0.0, r)
     r = np.minimum(r, maxval)
+    if np.isinf(maxval):
+        r = np.where(r >= 2.0 ** 128, np.inf, r)         # FP32 overflow
     r = np.where(np.isinf(ax), maxval, r)
     return np.copysign(r, x)
+
+
+def np_quantum(x, fmt):
+    """Grid spacing of a format in the binade of each |x| (x != 0)."""
+    mbits, emin = FMT[fmt][:2]
+    _, e = np.frexp(np.abs(np.asarray(x, dtype=np.float64)))
+    return np.exp2((np.maximum(e.astype(np.int64) - 1, emin) - mbits).astype(np.float64))
 
 
 def np_encode(v, fmt):
@@ -106,6 +119,48 @@ def rn64(x: Fraction):
 
 def bf16_to_float(bits):
     return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+SIM_EMIN, SIM_EMAX = -20, 8   # shifts below 2^-20 give 1, from 2^9 on 0, in both SIM widths
+
+
+@functools.lru_cache(maxsize=None)
+def mp_sim_exp(p):
+    """RN_p(exp(-s)) in the SIM profile for every shift s = (2^p + m) 2^(e-p),
+    e in [SIM_EMIN, SIM_EMAX], m in [0, 2^p), from mpmath; flat index
+    (e - SIM_EMIN) 2^p + m.  Every value is certified far from a midpoint."""
+    import mpmath as mp
+    mp.mp.prec = 160
+    n = (SIM_EMAX - SIM_EMIN + 1) << p
+    tab = np.empty(n)
+    for idx in range(n):
+        e, m = SIM_EMIN + (idx >> p), idx & ((1 << p) - 1)
+        s = Fraction((1 << p) | m) * Fraction(2) ** (e - p)
+        y = mp.exp(-mp.mpf(s.numerator) / s.denominator)
+        man, ex = mp.mpf(y).man_exp
+        yf = Fraction(int(man)) * Fraction(2) ** int(ex)
+        r = frac_round(yf, p, -126)
+        ey = yf.numerator.bit_length() - yf.denominator.bit_length()
+        if Fraction(2) ** ey > yf:
+            ey -= 1
+        qy = Fraction(2) ** (max(ey, -126) - p)
+        t = yf / qy - (yf // qy)
+        assert abs(t - Fraction(1, 2)) * qy > yf * Fraction(1, 2 ** 120)
+        tab[idx] = float(r)
+    return tab
+
+
+def sim_exp_lookup(s, p):
+    """RN_p(exp(-s)) for shifts s >= 0 on the SIM p-bit grid, from mp_sim_exp."""
+    tab = mp_sim_exp(p)
+    s = np.asarray(s, dtype=np.float64)
+    fr, e = np.frexp(np.where(s > 0, s, 1.0))
+    e = e.astype(np.int64) - 1
+    m = np.round((fr * 2.0) * (1 << p)).astype(np.int64) - (1 << p)
+    idx = (np.clip(e, SIM_EMIN, SIM_EMAX) - SIM_EMIN) * (1 << p) + m
+    v = tab[np.clip(idx, 0, tab.size - 1)]
+    v = np.where(e < SIM_EMIN, 1.0, np.where(e > SIM_EMAX, 0.0, v))
+    return np.where(s > 0, v, 1.0)
 
 
 @functools.lru_cache(maxsize=None)

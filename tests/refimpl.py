@@ -7,6 +7,7 @@ Written separately from the oracle with different methods:
     from fp64 products and a TwoSum correction instead of calling fmaf;
   * rounding to the formats with the integer model of fpmodel.py;
   * exponential tables from mpmath, lambda_hat from math.exp;
+  * the SIM profile's exact shift rounding from a TwoSum and a midpoint test;
   * the stage-2 knapsack by brute force over every g in {0,1}^N_k.
 It asserts the stage-1 invariant (every 8-bit sub-block passes the margin test
 against the final running maximum) on every tile.
@@ -42,25 +43,47 @@ def rn32_sum(p, c):
     return np.where(go_r2, r2, r)
 
 
-def y8_tile(qt, kf):
-    """qt [bq, d] fp32 values (as fp64), kf [T, d] -> Y8 values [T, bq]."""
+def y8_tile(qt, kf, fmt="e4m3"):
+    """qt [bq, d] fp32 values (as fp64), kf [T, d] -> Y8 values [T, bq]
+    (fmt "sim3" for the SIM profile)."""
     acc = np.zeros((kf.shape[0], qt.shape[0]))
     for c in range(qt.shape[1]):
         p = kf[:, c][:, None] * qt[:, c][None, :]          # exact in fp64
         t = rn32_sum(p, acc)
-        acc = M.np_round(t, "e4m3")
+        acc = M.np_round(t, fmt)
     return acc
 
 
-def y16_tile(qt, kf):
+def y16_tile(qt, kf, fmt="e4m11"):
     acc = np.zeros((kf.shape[0], qt.shape[0]))
     for c in range(qt.shape[1]):
         p = kf[:, c][:, None] * qt[:, c][None, :]           # exact in fp64
         acc = rn32_sum(p, acc)                               # FP32 FMA step
-    return M.np_round(acc, "e4m11")
+    return M.np_round(acc, fmt)
 
 
-def _shift_exp(muh, y, high, tabs):
+def sim_shift(muh, y, p):
+    """RN_p(max(0, muh - y)) of the exact difference in the SIM profile: the
+    fp64 difference and its TwoSum error; only an fp64 result exactly halfway
+    between two grid values can round differently, then the error's sign
+    decides."""
+    fmt = "sim3" if p == 3 else "sim11"
+    hi, lo = _two_sum(np.asarray(muh, dtype=np.float64), -np.asarray(y, dtype=np.float64))
+    r = M.np_round(hi, fmt)
+    with np.errstate(invalid="ignore"):
+        q = M.np_quantum(np.where(hi != 0, hi, 1.0), fmt)
+        t = np.abs(hi) / q
+        mid = (t - np.floor(t) == 0.5) & (lo != 0) & (hi != 0)
+        away = (lo > 0) == (hi > 0)
+        adj = np.copysign(np.where(away, np.floor(t) + 1, np.floor(t)) * q, hi)
+    r = np.where(mid, adj, r)
+    return np.where(hi > 0, r, 0.0)
+
+
+def _shift_exp(muh, y, high, tabs, sim=False):
+    if sim:
+        p = 11 if high else 3
+        return M.sim_exp_lookup(sim_shift(muh[None, :], y, p), p)
     x = np.maximum(muh[None, :] - y, 0.0)
     if high:
         code = M.np_encode(M.np_round(x, "ue5m11_shift"), "ue5m11_shift")
@@ -84,10 +107,27 @@ def _trunc_e4m3(x):
     return np.where(fin, np.copysign(t, x), x)
 
 
+def _trunc_sim3(x):
+    """Round toward zero to 3 mantissa bits in FP32's exponent range."""
+    x = np.asarray(x, dtype=np.float64)
+    fin = np.isfinite(x) & (x != 0)
+    q = M.np_quantum(np.where(fin, x, 1.0), "sim3")
+    return np.where(fin, np.copysign(np.floor(np.abs(x) / q) * q, x), x)
+
+
+def _colsum(E):
+    """Sum over keys in ascending order, one fp64 addition at a time."""
+    S = np.zeros(E.shape[1])
+    for r in range(E.shape[0]):
+        S = S + E[r]
+    return S
+
+
 def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=0):
     """q [B,Hq,N,d], k/v [B,Hkv,N,d] bf16 bit patterns.  Returns o, lse, mask.
     flags: 1 = first stage disabled, 2 = 8-bit shifts against mu_hat
-    truncated to e4m3 (both only for 0 < tau < inf)."""
+    truncated to e4m3 (both only for 0 < tau < inf), 4 = the SIM precision
+    profile (Sec. 4.1) in every mode."""
     B, Hq, N, d = q.shape
     Hkv = k.shape[1]
     G = Hq // Hkv
@@ -100,6 +140,9 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=
     all16 = tau == 0.0
     stage1_off = (not pure8) and (not all16) and bool(flags & 1)
     mu_trunc = (not pure8) and (not all16) and bool(flags & 2)
+    sim = bool(flags & 4)
+    f8, f16 = ("sim3", "sim11") if sim else ("e4m3", "e4m11")
+    trunc8 = _trunc_sim3 if sim else _trunc_e4m3
     for b in range(B):
         for h in range(Hq):
             kf_all = M.bf16_to_float(k[b, h // G])
@@ -128,7 +171,7 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=
                     prec = np.where(act, 0, 3)
                     Y = np.full((T, bq), np.nan)
                     if not all16:
-                        Y = y8_tile(qt, kf)
+                        Y = y8_tile(qt, kf, f8)
                     Yv = np.where(vis, Y, -np.inf)
                     m8 = np.array([Yv[th * bk:(th + 1) * bk].max(axis=0) for th in range(nk)])
                     muh = mu.copy()
@@ -137,7 +180,7 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=
                     def y16():
                         nonlocal Y16
                         if Y16 is None:
-                            Y16 = y16_tile(qt, kf)
+                            Y16 = y16_tile(qt, kf, f16)
                         return Y16
 
                     if pure8 or stage1_off:
@@ -181,13 +224,13 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=
                             continue
                         sl = slice(th * bk, (th + 1) * bk)
                         high = prec[th] == 1
-                        ref = _trunc_e4m3(muh) if (mu_trunc and not high) else muh
-                        e = _shift_exp(ref, np.where(vis[sl], Y[sl], 0.0), high, tabs)
+                        ref = trunc8(muh) if (mu_trunc and not high) else muh
+                        e = _shift_exp(ref, np.where(vis[sl], Y[sl], 0.0), high, tabs, sim)
                         E[sl] = np.where(vis[sl], e, 0.0)
                     lam = np.where(muh == -np.inf, 1.0,
                                    np.where(mu == -np.inf, 0.0,
                                             np.exp(np.where(np.isfinite(mu) & np.isfinite(muh), mu - muh, 0.0))))
-                    omh = lam * om + E.sum(axis=0)
+                    omh = lam * om + _colsum(E)
                     if not pure8 and not all16:
                         F = [th for th in range(nk) if prec[th] == 0]
                         cost = {}
@@ -215,9 +258,9 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=
                                 prec[th] = 2
                                 sl = slice(th * bk, (th + 1) * bk)
                                 Y[sl] = y16()[sl]
-                                e = _shift_exp(muh, np.where(vis[sl], Y[sl], 0.0), True, tabs)
+                                e = _shift_exp(muh, np.where(vis[sl], Y[sl], 0.0), True, tabs, sim)
                                 E[sl] = np.where(vis[sl], e, 0.0)
-                    om = lam * om + E.sum(axis=0)
+                    om = lam * om + _colsum(E)
                     O = O * lam[:, None] + E.T @ vf_all[np.minimum(ii, N - 1)]
                     mu = muh
                     mask[b, h, qb, t * nk:(t + 1) * nk] = prec
