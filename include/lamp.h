@@ -60,15 +60,18 @@ enum {
  * tau >= 0: threshold of Eq. (8); tau = +INFINITY is the pure 8-bit path (no
  * recomputation, the paper's 8-bit baseline) and tau = 0 recomputes every
  * active sub-block (16-bit FlashAttention in the paper's formats).
- * flags: 0, or LAMP_STAGE1_OFF and/or LAMP_MU_TRUNC (below); they apply for
- * 0 < tau < +INFINITY, the two end modes ignore them; other bits are
+ * flags: 0, or LAMP_STAGE1_OFF and/or LAMP_MU_TRUNC (below), which apply for
+ * 0 < tau < +INFINITY (the two end modes ignore them), and/or
+ * LAMP_SIM_PROFILE, which applies in every mode; other bits are
  * LAMP_ERR_INVALID_ARG.
  *
  * Outputs: o (normalised attention output), lse (mu + ln omega per query row,
  * natural log), mask (codes above).  Every mask byte of the rows is written.
  *
  * Built configurations (LAMP_ERR_UNSUPPORTED otherwise): d in {64, 128, 256};
- * bq in {64, 128}; (bk, nk) in {(16, 4), (64, 4)}; N <= 2^20.  N need not be a
+ * bq in {64, 128}; (bk, nk) in {(16, 4), (64, 4)}; N <= 2^20; with
+ * LAMP_SIM_PROFILE only (bk, nk) = (16, 4) and d in {128, 256}, the tiling of
+ * the paper's simulation (Sec. 4.1: 128 queries x 64 keys in 4 sub-blocks).  N need not be a
  * multiple of the block sizes: keys at or beyond N are invisible and the last
  * query block is partial (its missing rows take part in no test).  The mask
  * then holds ceil(N/bq) query blocks of ceil(N/(bk*nk))*nk sub-blocks, codes
@@ -95,8 +98,21 @@ enum {
     LAMP_STAGE1_OFF = 1,
     /* The 8-bit shifts use mu_hat truncated (toward zero) to e4m3, saturating
      * at 448 (Sec. 3.3: the running maxima may be rounded to e4m3 for the
-     * low-precision shifts by dropping the low mantissa bits). */
-    LAMP_MU_TRUNC = 2
+     * low-precision shifts by dropping the low mantissa bits); with
+     * LAMP_SIM_PROFILE, truncated to 3 mantissa bits, without saturation. */
+    LAMP_MU_TRUNC = 2,
+    /* The "SIM" precision profile (Sec. 4.1, the numerics of the paper's own
+     * simulation) in place of the formats of Sec. 3.3: the 8-bit and 16-bit
+     * numbers are FP32 values with 3 and 11 stored mantissa bits, FP32's
+     * exponent range and gradual underflow, round-to-nearest-even, no
+     * saturation (an overflow gives an infinity, as in FP32).  The 8-bit
+     * logits round to 3 bits after every FP32 FMA; the 16-bit logits are the
+     * FP32 FMA chain rounded once to 11 bits; each shift is the exact
+     * difference max(0, mu_hat - y) rounded once to 3 or 11 bits; each
+     * exponential is exp(-shift) correctly rounded to 3 or 11 bits; the row
+     * sum of a tile's exponentials is the fp64 sum over keys in ascending
+     * order.  Logits are assumed finite. */
+    LAMP_SIM_PROFILE = 4
 };
 
 /*
@@ -119,6 +135,17 @@ int lamp_attn_logits8(const uint16_t *q, const uint16_t *k,
 int lamp_attn_logits16(const uint16_t *q, const uint16_t *k,
                        int B, int Hq, int Hkv, int N, int d, int causal, int window,
                        int row0, int nrows, uint16_t *y16, void *stream);
+
+/*
+ * lamp_attn_logits_sim -- the logits of the SIM profile (LAMP_SIM_PROFILE):
+ * high = 0 the 8-bit recursion (FP32 FMA, then 3 mantissa bits, every step),
+ * high = 1 the 16-bit one (FP32 FMA chain, then 11 mantissa bits once).
+ * Values y [B][Hq][nrows][N] fp32 (device); invisible entries hold a NaN.
+ * d in {64, 128, 256}, N a multiple of 16, 0 <= row0, row0 + nrows <= N.
+ */
+int lamp_attn_logits_sim(const uint16_t *q, const uint16_t *k,
+                         int B, int Hq, int Hkv, int N, int d, int causal, int window,
+                         int row0, int nrows, int high, float *y, void *stream);
 
 /*
  * Kernel timing, for measurement.  While enabled (lamp_timing_enable(1)),
@@ -155,11 +182,17 @@ void lamp_shutdown(void);
  * exponentials as exact bf16 pairs (bits of the high part in [15:0], of the
  * low part in [31:16]; high = the fp32 value with its low 16 bits cleared,
  * low = value - high), the form the forward pass feeds to the matrix cores.
+ * lamp_get_sim_tables: copies to HOST memory the exponential tables of the
+ * SIM profile: sim8[112] (bf16 bits) and sim16[45056] (FP32 patterns), entry
+ * ((e - emin) << p) | m holding RN_p(exp(-s)) for the shift
+ * s = (2^p + m) 2^(e - p), p = 3 with e in [-6, 7], p = 11 with e in
+ * [-14, 7]; either pointer may be NULL.
  */
 int lamp_selftest_e4m3(const float *in, uint8_t *out, uint8_t *raw, size_t n, void *stream);
 int lamp_selftest_exp_doc(const double *x, double *y, size_t n, void *stream);
 int lamp_get_tables(int device, uint8_t *lut8, uint16_t *exp16);
 int lamp_get_exp16_parts(int device, uint32_t *parts);
+int lamp_get_sim_tables(int device, uint16_t *sim8, uint32_t *sim16);
 
 const char *lamp_status_str(int status);
 const char *lamp_last_error(void);

@@ -166,6 +166,70 @@ __device__ __forceinline__ void split_bf16(float ev, uint32_t &hi, uint32_t &lo)
     lo = __builtin_bit_cast(uint32_t, ev - __builtin_bit_cast(float, bits & 0xFFFF0000u)) >> 16;
 }
 
+// --- the SIM profile (Sec. 4.1) -----------------------------------------------
+// The numerics of the paper's simulation: numbers kept in FP32 with P = 3 or
+// 11 stored mantissa bits, FP32's exponent range and gradual underflow, no
+// saturation.  The rounding acts on the FP32 encoding: the fraction field is
+// rounded at bit 23-P to nearest, ties to even, a carry moving into the
+// exponent (overflow gives an infinity).
+template <int P>
+__device__ __forceinline__ float rn_sim(float x)
+{
+    constexpr uint32_t DROP = 23 - P;
+    const uint32_t b = __builtin_bit_cast(uint32_t, x);
+    return __builtin_bit_cast(float, (b + ((1u << (DROP - 1)) - 1u) + ((b >> DROP) & 1u)) & ~((1u << DROP) - 1u));
+}
+
+// mu_hat rounded toward zero to 3 mantissa bits (the optional truncation of
+// Sec. 3.3 in the SIM profile); infinities are kept.
+__device__ __forceinline__ float trunc_sim3(float x)
+{
+    return __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, x) & 0xFFF00000u);
+}
+
+// Exponential tables of the SIM profile: entry ((e - EMIN) << P) | m holds
+// RN_P(exp(-s)) for the shift s = (2^P + m) 2^(e-P).  Shifts below 2^EMIN give
+// 1 and shifts from 2^EMAX on give 0, so the first and last rows are constant
+// and shifts outside the range are clamped to them.
+constexpr int SIM8_EMIN = -6, SIM8_EMAX = 7, SIM16_EMIN = -14, SIM16_EMAX = 7;
+constexpr int SIM8_N = (SIM8_EMAX - SIM8_EMIN + 1) << 3;
+constexpr int SIM16_N = (SIM16_EMAX - SIM16_EMIN + 1) << 11;
+
+// Table index of s = RN_P(max(0, mu - y)), the exact difference rounded once.
+// The fp32 difference and its TwoSum error give the exact value; only a
+// difference lying exactly halfway between two grid values can round
+// differently from its fp32 rounding, and then the sign of the error decides.
+// mu and y are finite.
+template <int P, int EMIN, int EMAX>
+__device__ __forceinline__ uint32_t sim_shift_index(float mu, float y)
+{
+    const float s = mu - y;
+    if (!(s > 0.0f)) return 0u;   // shift 0 (a difference of 0 is exact)
+    const float bb = s - mu;
+    const float err = (mu - (s - bb)) + (-y - bb);
+    constexpr uint32_t DROP = 23 - P, HALF = 1u << (DROP - 1), LOW = (1u << DROP) - 1u;
+    const uint32_t b = __builtin_bit_cast(uint32_t, s);
+    uint32_t r = (b + (HALF - 1u) + ((b >> DROP) & 1u)) & ~LOW;
+    if ((b & LOW) == HALF && err != 0.0f) r = err > 0.0f ? b + HALF : b & ~LOW;
+    int e = (int)(r >> 23) - 127;
+    e = e < EMIN ? EMIN : (e > EMAX ? EMAX : e);
+    return ((uint32_t)(e - EMIN) << P) | ((r >> DROP) & ((1u << P) - 1u));
+}
+
+// Column maxima of SIM logits merge through an integer atomic max: the FP32
+// pattern mapped to an int that orders like the value (negative patterns
+// have their magnitude bits flipped); the map is its own inverse.
+__device__ __forceinline__ int ord_of(float y)
+{
+    const int b = __builtin_bit_cast(int, y);
+    return b ^ ((b >> 31) & 0x7FFFFFFF);
+}
+
+__device__ __forceinline__ float ord_value(int k)
+{
+    return __builtin_bit_cast(float, k ^ ((k >> 31) & 0x7FFFFFFF));
+}
+
 // --- exp_doc ----------------------------------------------------------------
 // The fp64 exponential of the rescale factor lambda_hat = exp(mu - mu_hat)
 // (Sec. 2.2: alpha_hat in high precision), fixed operation by operation so

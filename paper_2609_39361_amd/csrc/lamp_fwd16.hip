@@ -76,19 +76,59 @@ struct Cfg16 {
 __device__ __forceinline__ int fx_of(float y) { return (int)(y * 131072.0f); }
 __device__ __forceinline__ float fx_value(int f) { return (float)f * (1.0f / 131072.0f); }
 
+// Keys of the 16-bit column maxima merged by integer atomic max: exact fixed
+// point for e4m11, the order-preserving map of the FP32 pattern in the SIM
+// profile (whose values span FP32's range).
+template <bool SIMP>
+__device__ __forceinline__ int cm_key(float y)
+{
+    if constexpr (SIMP) return ord_of(y);
+    else return fx_of(y);
+}
+
+template <bool SIMP>
+__device__ __forceinline__ float cm_value(int f)
+{
+    if constexpr (SIMP) return ord_value(f);
+    else return fx_value(f);
+}
+
+// SIM 16-bit logits in LDS: the high and low 16 bits of the FP32 patterns of
+// two keys, in the code row and the low row.
+__device__ __forceinline__ uint32_t pack_hi16(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xFFFF0000u); }
+__device__ __forceinline__ uint32_t pack_lo16(uint32_t a, uint32_t b) { return (a & 0xFFFFu) | (b << 16); }
+
+// The low bf16 parts E - hi of 8 SIM 16-bit exponentials kept as the high and
+// low halves of their FP32 patterns (E has 12 significant bits, so E - hi is
+// exact in fp32 and has at most 4; its bf16 truncation is exact down to 2^-133).
+__device__ __forceinline__ u32x4 lo_bf16x8(const u32x4 &h, const u32x4 &l)
+{
+    u32x4 r;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const uint32_t hk = h[k], lk = l[k];
+        const float g0 = __builtin_bit_cast(float, hk << 16), g1 = __builtin_bit_cast(float, hk & 0xFFFF0000u);
+        const float e0 = __builtin_bit_cast(float, (hk << 16) | (lk & 0xFFFFu));
+        const float e1 = __builtin_bit_cast(float, (hk & 0xFFFF0000u) | (lk >> 16));
+        r[k] = (__builtin_bit_cast(uint32_t, e0 - g0) >> 16) | (__builtin_bit_cast(uint32_t, e1 - g1) & 0xFFFF0000u);
+    }
+    return r;
+}
+
 } // namespace
 
-template <int D, int BQ, int MODE>
+template <int D, int BQ, int MODE, bool SIMP>
 __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdParams p)
 {
     using C = Cfg16<D, BQ>;
     constexpr int NK = C::NK, BK = C::BK, KPT = C::KPT, NW = C::NW, QPL = C::QPL, CPW = C::CPW;
     constexpr int CT = C::CT, QG = C::QG, YP = C::YP;
+    constexpr int WPM = SIMP ? 4 : 2;   // words of 16-bit logits per 4 keys (SIM: FP32 patterns)
 
     extern __shared__ __align__(16) unsigned char smem[];
     uint16_t *ycode2 = reinterpret_cast<uint16_t *>(smem + C::OFF_Y);   // [2][BQ][YP] logit codes, then E
     uint16_t *ylo = reinterpret_cast<uint16_t *>(smem + C::OFF_YL);     // [BQ][YP] low bf16 part of E16
-    uint16_t *lut = reinterpret_cast<uint16_t *>(smem + C::OFF_LUT);    // [256] 8-bit exp (bf16 bits)
+    uint16_t *lut = reinterpret_cast<uint16_t *>(smem + C::OFF_LUT);    // [256] 8-bit exp (bf16 bits; SIM table)
     float *m8s2 = reinterpret_cast<float *>(smem + C::OFF_M8);          // [2][NK][BQ] 8-bit column maxima
     int *cmi2 = reinterpret_cast<int *>(smem + C::OFF_CMI);             // [2][NK][BQ] 16-bit column maxima
     float *cmf = reinterpret_cast<float *>(smem + C::OFF_CMF);          // [2][NW][BQ] one-at-a-time maxima
@@ -153,7 +193,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     const uint16_t *vtbase = p.vt + ((size_t)b * p.Hkv + hk) * (size_t)D * p.Nk;    // V^T [D][Nk]
     uint8_t *mrow = p.mask + (((size_t)b * p.Hq + h) * nqb + qb) * (size_t)(p.Nk / BK);
 
-    for (int i = tid; i < 256; i += 256) lut[i] = p.lut8e[i];
+    for (int i = tid; i < 256; i += 256) lut[i] = SIMP ? p.sim8[i] : p.lut8e[i];
     if (tid < EXPDOC_NK) edk[tid] = EXPDOC_K[tid];
     for (int i = tid; i < 2 * NK * BQ; i += 256) cmi2[i] = INT_MIN;
 
@@ -210,11 +250,12 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                 uint32_t packed[8];
 #pragma unroll
                 for (int pp = 0; pp < 8; ++pp) {
-                    const float2 yv = unpk_e4m3(a8[s][pp]);
+                    const float2 yv = SIMP ? make_float2(bf16_value(a8[s][pp] & 0xFFFFu), bf16_value(a8[s][pp] >> 16))
+                                           : unpk_e4m3(a8[s][pp]);
                     const int i0 = ck0 + 2 * pp;
                     if (full || visible(s, i0)) mx = yv.x > mx ? yv.x : mx;
                     if (full || visible(s, i0 + 1)) mx = yv.y > mx ? yv.y : mx;
-                    packed[pp] = (a8[s][pp] & 0xFFu) | ((a8[s][pp] & 0xFF00u) << 8);
+                    packed[pp] = SIMP ? a8[s][pp] : (a8[s][pp] & 0xFFu) | ((a8[s][pp] & 0xFF00u) << 8);
                 }
                 u32x4 *dst = reinterpret_cast<u32x4 *>(yc + row[s] * YP + w * BK);
                 dst[0] = u32x4{packed[0], packed[1], packed[2], packed[3]};
@@ -261,9 +302,55 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     auto shared16 = [&](int k0, int th, auto fn) {
         const int key0 = k0 + th * BK + w * 4;
         if (key0 > bv_hi || key0 + 3 < bv_lo) return;   // nothing visible in the block
-        uint32_t yc[QPL][2];
-        rec16_keys<D, QPL, 4>(qrow, kt32 + (size_t)(key0 + (lane & 3)) * D, yc);
+        uint32_t yc[QPL][WPM];
+        rec16_keys<D, QPL, 4, SIMP>(qrow, kt32 + (size_t)(key0 + (lane & 3)) * D, yc);
         fn(key0, yc);
+    };
+    // exponentials: 8-bit from the LDS table, 16-bit from the table in global
+    // memory as bf16 high / low parts (SIM: high / low halves of the FP32
+    // pattern) and the value
+    auto e8_of = [&](float m8ref, uint32_t yc) -> uint32_t {
+        if constexpr (SIMP) return lut[sim_shift_index<3, SIM8_EMIN, SIM8_EMAX>(m8ref, bf16_value(yc))];
+        else return lut[ue5m3_code(shift_of(m8ref, e4m3_value(yc)))];
+    };
+    auto e16_of = [&](float mref, float y, uint32_t &eh, uint32_t &el) -> float {
+        if constexpr (SIMP) {
+            const uint32_t eb = p.sim16[sim_shift_index<11, SIM16_EMIN, SIM16_EMAX>(mref, y)];
+            eh = eb >> 16;
+            el = eb & 0xFFFFu;
+            return __builtin_bit_cast(float, eb);
+        } else {
+            const uint32_t hl = p.exp16hl[ue5m11_code(shift_of(mref, y))];
+            eh = hl & 0xFFFFu;
+            el = hl >> 16;
+            return bf16_value(eh) + bf16_value(el);   // exact
+        }
+    };
+    // SIM profile: the row sum of the tile's exponentials, keys ascending,
+    // one fp64 addition at a time, from the values in LDS (hmask: the
+    // sub-blocks holding 16-bit exponentials)
+    auto seq_sum = [&](const uint16_t *yc, int s, uint32_t hmask) -> double {
+        double tt = 0.0;
+#pragma unroll
+        for (int c = 0; c < NK; ++c) {
+            const u32x4 *hp = reinterpret_cast<const u32x4 *>(yc + row[s] * YP + c * BK);
+            const u32x4 h0 = hp[0], h1 = hp[1];
+            u32x4 l0 = u32x4{0u, 0u, 0u, 0u}, l1 = l0;
+            if (hmask >> c & 1u) {
+                const u32x4 *lp = reinterpret_cast<const u32x4 *>(ylo + row[s] * YP + c * BK);
+                l0 = lp[0];
+                l1 = lp[1];
+            }
+            const uint32_t hw[8] = {h0[0], h0[1], h0[2], h0[3], h1[0], h1[1], h1[2], h1[3]};
+            const uint32_t lw[8] = {l0[0], l0[1], l0[2], l0[3], l1[0], l1[1], l1[2], l1[3]};
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const uint32_t hb = (hw[i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+                const uint32_t lb = (lw[i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+                tt += (double)__builtin_bit_cast(float, (hb << 16) | lb);
+            }
+        }
+        return tt;
     };
 
     // ---- prologue: 8-bit logits of the first tile, its F0
@@ -272,7 +359,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     if (mode != MODE_ALL16) {
         const bool done = own_emulated(t, act);
         uint32_t a8[QPL][8];
-        if (done) emu8_chunk<D, QPL>(qrow, kt32 + (size_t)(t * KPT + w * BK) * D, a8);
+        if (done) emu8_any<D, QPL, SIMP>(qrow, kt32 + (size_t)(t * KPT + w * BK) * D, a8);
         emit8(t, a8, done);
     }
     __syncthreads();
@@ -286,7 +373,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
 
         // ---- A. fused pass: 16-bit logits of F0 (4 keys of each member per
         // wave), 8-bit logits of this wave's sub-block of the next tile
-        uint32_t y16r[QPL][8];   // codes of keys th*16 + w*4 + {0..3} of the g-th member of F0, 2 per word
+        uint32_t y16r[QPL][4 * WPM];   // 16-bit logits of keys th*16 + w*4 + {0..3} of the g-th member of F0
         {
             const int nf = __builtin_popcount(F0);
             const int kk = nf ? (lane & 15) % (4 * nf) : 0;
@@ -303,13 +390,13 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
             auto run = [&](auto nkey_c, auto emu_c) {
                 constexpr int NKEY = decltype(nkey_c)::value;
                 constexpr bool EMU = decltype(emu_c)::value;
-                uint32_t c[QPL][NKEY > 0 ? NKEY / 2 : 1];
-                fused_pass<D, QPL, NKEY, EMU>(qrow, k32e, krowr, a8, c);
+                uint32_t c[QPL][y16_words<SIMP>(NKEY)];
+                fused_pass<D, QPL, NKEY, EMU, SIMP>(qrow, k32e, krowr, a8, c);
                 if constexpr (NKEY > 0)
 #pragma unroll
                     for (int s = 0; s < QPL; ++s)
 #pragma unroll
-                        for (int pp = 0; pp < NKEY / 2; ++pp) y16r[s][pp] = c[s][pp];
+                        for (int pp = 0; pp < y16_words<SIMP>(NKEY); ++pp) y16r[s][pp] = c[s][pp];
             };
             using T_ = std::true_type;
             using F_ = std::false_type;
@@ -346,8 +433,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                     int cm = INT_MIN;
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        const uint32_t word = y16r[s][2 * g + (i >> 1)];
-                        const int f = fx_of(e4m11_value((word >> (16 * (i & 1))) & 0xFFFFu));
+                        const int f = cm_key<SIMP>(y16_value<SIMP>(&y16r[s][g * WPM], i));
                         if (visible(s, key0 + i)) cm = f > cm ? f : cm;
                     }
                     if (cm != INT_MIN) atomicMax(&cmi[th * BQ + row[s]], cm);
@@ -369,7 +455,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
 #pragma unroll
                 for (int s = 0; s < QPL; ++s) {
                     const int f = (F0 >> th & 1u) ? cmi[th * BQ + row[s]] : INT_MIN;
-                    cm16[th][s] = f == INT_MIN ? NEG_INF : fx_value(f);
+                    cm16[th][s] = f == INT_MIN ? NEG_INF : cm_value<SIMP>(f);
                 }
         }
         if (mode == MODE_PURE8 || stage1_off) {   // running maximum over the 8-bit logits
@@ -445,15 +531,22 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                     float cm[QPL];
 #pragma unroll
                     for (int s = 0; s < QPL; ++s) cm[s] = NEG_INF;
-                    shared16(k0, th, [&](int kc, const uint32_t (&yc)[QPL][2]) {
+                    shared16(k0, th, [&](int kc, const uint32_t (&yc)[QPL][WPM]) {
 #pragma unroll
                         for (int s = 0; s < QPL; ++s) {
 #pragma unroll
                             for (int i = 0; i < 4; ++i) {
-                                const float yv = e4m11_value((yc[s][i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
+                                const float yv = y16_value<SIMP>(yc[s], i);
                                 if (visible(s, kc + i)) cm[s] = yv > cm[s] ? yv : cm[s];
                             }
-                            *reinterpret_cast<uint2 *>(ycode + row[s] * YP + (kc - k0)) = make_uint2(yc[s][0], yc[s][1]);
+                            uint2 *dst = reinterpret_cast<uint2 *>(ycode + row[s] * YP + (kc - k0));
+                            if constexpr (SIMP) {
+                                *dst = make_uint2(pack_hi16(yc[s][0], yc[s][1]), pack_hi16(yc[s][2], yc[s][3]));
+                                *reinterpret_cast<uint2 *>(ylo + row[s] * YP + (kc - k0)) =
+                                    make_uint2(pack_lo16(yc[s][0], yc[s][1]), pack_lo16(yc[s][2], yc[s][3]));
+                            } else {
+                                *dst = make_uint2(yc[s][0], yc[s][1]);
+                            }
                         }
                     });
 #pragma unroll
@@ -483,7 +576,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
 #pragma unroll
             for (int s = 0; s < QPL; ++s) {
                 sp[s] = spF[s] = 0.0;
-                mu8[s] = mu_trunc ? trunc_e4m3(muh[s]) : muh[s];
+                mu8[s] = mu_trunc ? (SIMP ? trunc_sim3(muh[s]) : trunc_e4m3(muh[s])) : muh[s];
             }
             const int th = w;   // own sub-block
             const int ck0 = k0 + th * BK;
@@ -512,6 +605,12 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                     }
                     const u32x4 c0 = rp[0], c1 = rp[1];
                     const uint32_t in[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
+                    uint32_t inl[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};   // SIM: low halves of 16-bit logits
+                    if (SIMP && hi16) {
+                        const u32x4 l0 = lp[0], l1 = lp[1];
+                        inl[0] = l0[0]; inl[1] = l0[1]; inl[2] = l0[2]; inl[3] = l0[3];
+                        inl[4] = l1[0]; inl[5] = l1[1]; inl[6] = l1[2]; inl[7] = l1[3];
+                    }
                     uint32_t outw[8], outl[8];
 #pragma unroll
                     for (int pp = 0; pp < 8; ++pp) {
@@ -524,16 +623,15 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                             float ev = 0.0f;
                             if (visible(s, key)) {
                                 if (hi16) {
-                                    const uint32_t hl = p.exp16hl[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))];
-                                    eh = hl & 0xFFFFu;
-                                    el = hl >> 16;
-                                    ev = bf16_value(eh) + bf16_value(el);   // exact
+                                    const float y = SIMP ? __builtin_bit_cast(float, (yc << 16) | ((inl[pp] >> (16 * t2)) & 0xFFFFu))
+                                                         : e4m11_value(yc);
+                                    ev = e16_of(muh[s], y, eh, el);
                                 } else {
-                                    eh = lut[ue5m3_code(shift_of(mu8[s], e4m3_value(yc)))];
+                                    eh = e8_of(mu8[s], yc);
                                     ev = bf16_value(eh);
                                 }
                             }
-                            sp[s] += (double)ev;   // exact: multiples of 2^-41 below 2^9
+                            sp[s] += (double)ev;   // exact: multiples of 2^-41 below 2^9 (SIM: not used)
                             if (!hi16) spF[s] += (double)ev;
                             res |= eh << (16 * t2);
                             rlo |= el << (16 * t2);
@@ -572,13 +670,8 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                                 const int key = key0 + 2 * pp + t2;
                                 uint32_t eh = 0, el = 0;
                                 float ev = 0.0f;
-                                if (visible(s, key)) {
-                                    const uint32_t yc = (y16r[s][2 * g + pp] >> (16 * t2)) & 0xFFFFu;
-                                    const uint32_t hl = p.exp16hl[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))];
-                                    eh = hl & 0xFFFFu;
-                                    el = hl >> 16;
-                                    ev = bf16_value(eh) + bf16_value(el);   // exact
-                                }
+                                if (visible(s, key))
+                                    ev = e16_of(muh[s], y16_value<SIMP>(&y16r[s][g * WPM], 2 * pp + t2), eh, el);
                                 sp[s] += (double)ev;
                                 res |= eh << (16 * t2);
                                 rlo |= el << (16 * t2);
@@ -608,8 +701,12 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
 #pragma unroll
         for (int s = 0; s < QPL; ++s) {
             double tt = 0.0;
+            if constexpr (SIMP) {
+                tt = seq_sum(ycode, s, prec16);
+            } else {
 #pragma unroll
-            for (int ww = 0; ww < NW; ++ww) tt += sps[ww * BQ + row[s]];
+                for (int ww = 0; ww < NW; ++ww) tt += sps[ww * BQ + row[s]];
+            }
             S[s] = tt;
             if (muh[s] == NEG_INF) lam[s] = 1.0;
             else if (mu[s] == NEG_INF) lam[s] = 0.0;
@@ -697,7 +794,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                     double ds[QPL];
 #pragma unroll
                     for (int s = 0; s < QPL; ++s) ds[s] = 0.0;
-                    auto s2fn = [&](int kc, const uint32_t (&yc)[QPL][2]) {
+                    auto s2fn = [&](int kc, const uint32_t (&yc)[QPL][WPM]) {
 #pragma unroll
                         for (int s = 0; s < QPL; ++s) {
                             const uint16_t *src = ycode + row[s] * YP + (kc - k0);
@@ -711,13 +808,11 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                                     uint32_t eh = 0, el = 0;
                                     if (visible(s, key)) {
                                         const float old = bf16_value(src[2 * pp + t2]);
-                                        const float y = e4m11_value((yc[s][pp] >> (16 * t2)) & 0xFFFFu);
-                                        const uint32_t hl = p.exp16hl[ue5m11_code(shift_of(muh[s], y))];
-                                        eh = hl & 0xFFFFu;
-                                        el = hl >> 16;
-                                        const float ev = bf16_value(eh) + bf16_value(el);   // exact
-                                        ds[s] = ds[s] - (double)old;
-                                        ds[s] = ds[s] + (double)ev;
+                                        const float ev = e16_of(muh[s], y16_value<SIMP>(yc[s], 2 * pp + t2), eh, el);
+                                        if constexpr (!SIMP) {
+                                            ds[s] = ds[s] - (double)old;
+                                            ds[s] = ds[s] + (double)ev;
+                                        }
                                     }
                                     res |= eh << (16 * t2);
                                     rlo |= el << (16 * t2);
@@ -732,7 +827,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                     // sub-blocks of R without codes from the fused pass: one batched
                     // recompute, 4 keys of each per wave (as for F0)
                     const uint32_t Rn = prec2 & ~F0;
-                    uint32_t y16b[QPL][8];
+                    uint32_t y16b[QPL][4 * WPM];
                     if (Rn) {
                         const int nr = __builtin_popcount(Rn);
                         const int kb = (lane & 15) % (4 * nr);
@@ -741,12 +836,12 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                         const float *krow = kt32 + (size_t)(k0 + __builtin_ctz(m) * BK + w * 4 + (kb & 3)) * D;
                         auto rec = [&](auto nkey_c) {
                             constexpr int NKEY = decltype(nkey_c)::value;
-                            uint32_t c[QPL][NKEY / 2];
-                            rec16_keys<D, QPL, NKEY>(qrow, krow, c);
+                            uint32_t c[QPL][y16_words<SIMP>(NKEY)];
+                            rec16_keys<D, QPL, NKEY, SIMP>(qrow, krow, c);
 #pragma unroll
                             for (int s = 0; s < QPL; ++s)
 #pragma unroll
-                                for (int pp = 0; pp < NKEY / 2; ++pp) y16b[s][pp] = c[s][pp];
+                                for (int pp = 0; pp < y16_words<SIMP>(NKEY); ++pp) y16b[s][pp] = c[s][pp];
                         };
                         switch (nr) {
                         case 1: rec(std::integral_constant<int, 4>()); break;
@@ -761,29 +856,35 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                         // (member of F0) or from the batch above
                         const bool inF0 = F0 >> th & 1u;
                         const int gi = __builtin_popcount((inF0 ? F0 : Rn) & ((1u << th) - 1u));
-                        uint32_t yc[QPL][2];
+                        uint32_t yc[QPL][WPM];
 #pragma unroll
                         for (int s = 0; s < QPL; ++s) {
-                            yc[s][0] = inF0 ? y16r[s][0] : y16b[s][0];
-                            yc[s][1] = inF0 ? y16r[s][1] : y16b[s][1];
+#pragma unroll
+                            for (int x = 0; x < WPM; ++x) yc[s][x] = inF0 ? y16r[s][x] : y16b[s][x];
 #pragma unroll
                             for (int g = 1; g < NK; ++g)
-                                if (g == gi) {
-                                    yc[s][0] = inF0 ? y16r[s][2 * g] : y16b[s][2 * g];
-                                    yc[s][1] = inF0 ? y16r[s][2 * g + 1] : y16b[s][2 * g + 1];
-                                }
+                                if (g == gi)
+#pragma unroll
+                                    for (int x = 0; x < WPM; ++x)
+                                        yc[s][x] = inF0 ? y16r[s][g * WPM + x] : y16b[s][g * WPM + x];
                         }
                         s2fn(k0 + th * BK + w * 4, yc);
                     }
+                    if constexpr (!SIMP) {
 #pragma unroll
-                    for (int s = 0; s < QPL; ++s) sps[w * BQ + row[s]] = ds[s];
+                        for (int s = 0; s < QPL; ++s) sps[w * BQ + row[s]] = ds[s];
+                    }
                     __syncthreads();
 #pragma unroll
                     for (int s = 0; s < QPL; ++s) {
-                        double tt = S[s];
+                        if constexpr (SIMP) {
+                            S[s] = seq_sum(ycode, s, prec16 | prec2);
+                        } else {
+                            double tt = S[s];
 #pragma unroll
-                        for (int ww = 0; ww < NW; ++ww) tt += sps[ww * BQ + row[s]];   // exact
-                        S[s] = tt;
+                            for (int ww = 0; ww < NW; ++ww) tt += sps[ww * BQ + row[s]];   // exact
+                            S[s] = tt;
+                        }
                     }
                 }
             }
@@ -824,7 +925,9 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                     acc[g][tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[tt]), bh,
                                                                          acc[g][tt], 0, 0, 0);
                 if (hi16) {   // E16 = hi + lo exactly
-                    const bf16x8 bl = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(ylo + off));
+                    u32x4 lw = *reinterpret_cast<const u32x4 *>(ylo + off);
+                    if constexpr (SIMP) lw = lo_bf16x8(*reinterpret_cast<const u32x4 *>(ycode + off), lw);
+                    const bf16x8 bl = __builtin_bit_cast(bf16x8, lw);
 #pragma unroll
                     for (int tt = 0; tt < CT; ++tt)
                         acc[g][tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[tt]), bl,
@@ -900,11 +1003,11 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
 }
 
 // ------------------------------------------------------------------ launcher
-template <int D, int BQ, int MODE>
+template <int D, int BQ, int MODE, bool SIMP>
 static hipError_t launch_fwd16_mode(const FwdParams &p, hipStream_t s)
 {
     using C = Cfg16<D, BQ>;
-    auto kern = lamp_fwd16_kernel<D, BQ, MODE>;
+    auto kern = lamp_fwd16_kernel<D, BQ, MODE, SIMP>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
     if (e != hipSuccess) return e;
@@ -913,12 +1016,19 @@ static hipError_t launch_fwd16_mode(const FwdParams &p, hipStream_t s)
     return hipGetLastError();
 }
 
+template <int D, int BQ, bool SIMP>
+static hipError_t launch_fwd16_prof(const FwdParams &p, hipStream_t s)
+{
+    if (p.mode == MODE_PURE8) return launch_fwd16_mode<D, BQ, MODE_PURE8, SIMP>(p, s);
+    if (p.mode == MODE_ALL16) return launch_fwd16_mode<D, BQ, MODE_ALL16, SIMP>(p, s);
+    return launch_fwd16_mode<D, BQ, MODE_LAMP, SIMP>(p, s);
+}
+
 template <int D, int BQ>
 static hipError_t launch_fwd16(const FwdParams &p, hipStream_t s)
 {
-    if (p.mode == MODE_PURE8) return launch_fwd16_mode<D, BQ, MODE_PURE8>(p, s);
-    if (p.mode == MODE_ALL16) return launch_fwd16_mode<D, BQ, MODE_ALL16>(p, s);
-    return launch_fwd16_mode<D, BQ, MODE_LAMP>(p, s);
+    if (p.flags & LAMP_SIM_PROFILE) return launch_fwd16_prof<D, BQ, true>(p, s);
+    return launch_fwd16_prof<D, BQ, false>(p, s);
 }
 
 hipError_t dispatch_fwd16(int D, int BQ, const FwdParams &p, hipStream_t s, bool *found)

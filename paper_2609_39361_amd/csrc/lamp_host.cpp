@@ -37,6 +37,8 @@ struct DeviceState {
     uint16_t *lut8e = nullptr;
     uint16_t *exp16 = nullptr;
     uint32_t *exp16hl = nullptr;
+    uint16_t *sim8 = nullptr;    // SIM profile tables
+    uint32_t *sim16 = nullptr;
     void *ws = nullptr;
     size_t ws_bytes = 0;
 };
@@ -72,7 +74,10 @@ int init_locked(int dev)
     unsigned *amb = nullptr;
     HIP_TRY(hipMalloc(&amb, sizeof(unsigned)));
     HIP_TRY(hipMemset(amb, 0, sizeof(unsigned)));
+    HIP_TRY(hipMalloc(&st->sim8, lamp::SIM8_TABLE * sizeof(uint16_t)));
+    HIP_TRY(hipMalloc(&st->sim16, lamp::SIM16_TABLE * sizeof(uint32_t)));
     HIP_TRY(lamp::launch_build_tables(st->lut8, st->lut8e, st->exp16, st->exp16hl, amb, nullptr));
+    HIP_TRY(lamp::launch_build_sim_tables(st->sim8, st->sim16, amb, nullptr));
     unsigned h_amb = 0;
     HIP_TRY(hipMemcpy(&h_amb, amb, sizeof(unsigned), hipMemcpyDeviceToHost));
     HIP_TRY(hipFree(amb));
@@ -194,6 +199,8 @@ void lamp_shutdown(void)
         (void)hipFree(st.lut8e);
         (void)hipFree(st.exp16);
         (void)hipFree(st.exp16hl);
+        (void)hipFree(st.sim8);
+        (void)hipFree(st.sim16);
         (void)hipFree(st.ws);
         st = DeviceState();
     }
@@ -210,10 +217,14 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
         return fail(LAMP_ERR_INVALID_ARG, "null pointer among v, o, lse, mask");
     if (!(delta >= 0.0) || std::isinf(delta)) return fail(LAMP_ERR_INVALID_ARG, "delta must be finite and >= 0");
     if (!(tau >= 0.0)) return fail(LAMP_ERR_INVALID_ARG, "tau must be >= 0 (or +inf)");
-    if (flags & ~(unsigned)(LAMP_STAGE1_OFF | LAMP_MU_TRUNC)) return fail(LAMP_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
+    if (flags & ~(unsigned)(LAMP_STAGE1_OFF | LAMP_MU_TRUNC | LAMP_SIM_PROFILE))
+        return fail(LAMP_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
     if (bq <= 0 || bk <= 0 || nk <= 0) return fail(LAMP_ERR_INVALID_ARG, "block sizes must be positive");
     if (!lamp::fwd_supported(d, bq, bk, nk))
         return fail(LAMP_ERR_UNSUPPORTED, "block sizes (bq=%d, bk=%d, nk=%d) not built for d=%d", bq, bk, nk, d);
+    if ((flags & LAMP_SIM_PROFILE) && !(bk == 16 && nk == 4 && (d == 128 || d == 256)))
+        return fail(LAMP_ERR_UNSUPPORTED, "the SIM profile is built for bk=16, nk=4, d in {128, 256} (bk=%d, nk=%d, d=%d)",
+                    bk, nk, d);
     if (B == 0 || N == 0) return LAMP_OK;   // nothing to compute
     // the workspace holds whole query blocks and whole key tiles (zero padded)
     const int Nq = (N + bq - 1) / bq * bq, Nk = (N + bk * nk - 1) / (bk * nk) * (bk * nk);
@@ -233,6 +244,8 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
         p.exp16 = st->exp16;
         p.exp16hl = st->exp16hl;
         p.lut8e = st->lut8e;
+        p.sim8 = st->sim8;
+        p.sim16 = st->sim16;
     }
     p.qt = w.qt;
     p.kt32 = w.kt32;
@@ -251,7 +264,7 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
     p.delta = delta;
     p.tau = tau;
     p.mode = std::isinf(tau) ? lamp::MODE_PURE8 : (tau == 0.0 ? lamp::MODE_ALL16 : lamp::MODE_LAMP);
-    p.flags = p.mode == lamp::MODE_LAMP ? flags : 0u;
+    p.flags = p.mode == lamp::MODE_LAMP ? flags : (flags & (unsigned)LAMP_SIM_PROFILE);
     bool timed = false;
     TimedCall tc{};
     {
@@ -371,6 +384,20 @@ int lamp_attn_logits16(const uint16_t *q, const uint16_t *k, int B, int Hq, int 
     return LAMP_OK;
 }
 
+int lamp_attn_logits_sim(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv, int N, int d, int causal,
+                         int window, int row0, int nrows, int high, float *y, void *stream)
+{
+    lamp::LogitsParams p;
+    Workspace w;
+    int rc = logits_common(q, k, B, Hq, Hkv, N, d, causal, window, row0, nrows, y, &p, &w);
+    if (rc) return rc;
+    p.ysim = y;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, N, N, d, scale_of(d), s));
+    HIP_TRY(lamp::launch_logits_sim(p, d, high != 0, s));
+    return LAMP_OK;
+}
+
 int lamp_selftest_e4m3(const float *in, uint8_t *out, uint8_t *raw, size_t n, void *stream)
 {
     if (!in || !out) return fail(LAMP_ERR_INVALID_ARG, "null pointer");
@@ -413,6 +440,23 @@ int lamp_get_exp16_parts(int device, uint32_t *parts)
     HIP_TRY(hipSetDevice(device));
     HIP_TRY(hipMemcpy(parts, state_of(device)->exp16hl, 65536 * sizeof(uint32_t), hipMemcpyDeviceToHost));
     HIP_TRY(hipSetDevice(prev));
+    return LAMP_OK;
+}
+
+int lamp_get_sim_tables(int device, uint16_t *sim8, uint32_t *sim16)
+{
+    int rc = lamp_init(device);
+    if (rc) return rc;
+    std::lock_guard<std::mutex> lk(g_mu);
+    int prev = 0;
+    HIP_TRY(hipGetDevice(&prev));
+    HIP_TRY(hipSetDevice(device));
+    DeviceState *st = state_of(device);
+    hipError_t e = hipSuccess;
+    if (sim8) e = hipMemcpy(sim8, st->sim8, lamp::SIM8_ENTRIES * sizeof(uint16_t), hipMemcpyDeviceToHost);
+    if (e == hipSuccess && sim16) e = hipMemcpy(sim16, st->sim16, lamp::SIM16_TABLE * sizeof(uint32_t), hipMemcpyDeviceToHost);
+    (void)hipSetDevice(prev);
+    if (e != hipSuccess) return fail(LAMP_ERR_HIP, "lamp_get_sim_tables: %s", hipGetErrorString(e));
     return LAMP_OK;
 }
 

@@ -10,6 +10,10 @@ namespace lamp {
 
 enum { MODE_LAMP = 0, MODE_PURE8 = 1, MODE_ALL16 = 2 };
 
+// Sizes of the SIM profile's exponential tables (layout in lamp_device.h):
+// the 8-bit one padded to 256 entries for the forward kernel's LDS copy.
+constexpr int SIM8_ENTRIES = 112, SIM8_TABLE = 256, SIM16_TABLE = 45056;
+
 struct FwdParams {
     const float *qt;          // [B][Hq][N][D] pre-scaled queries, fp32
     const float *kt32;        // [B][Hkv][N][D] keys, fp32
@@ -17,13 +21,15 @@ struct FwdParams {
     const uint16_t *exp16;    // ue5m11 shift code -> ue5m11 exp code
     const uint32_t *exp16hl;  // ue5m11 shift code -> bf16 high | low << 16 of the ue5m11 exp
     const uint16_t *lut8e;    // ue5m3 shift code -> bf16 bits of the ue5m3 exp
+    const uint16_t *sim8;     // SIM profile: 8-bit exp table (bf16 bits), lamp_device.h layout
+    const uint32_t *sim16;    // SIM profile: 16-bit exp table (FP32 patterns)
     float *o;                 // [B][Hq][N][D]
     float *lse;               // [B][Hq][N]
     uint8_t *mask;            // [B][Hq][N/BQ][N/BK]
     int B, Hq, Hkv, N;        // N: sequence length (visibility, O / lse rows)
     int Nq, Nk;               // padded lengths: rows of qt, keys of kt32 / vt (whole blocks / tiles)
     int causal, window, mode;
-    unsigned flags;           // LAMP_STAGE1_OFF | LAMP_MU_TRUNC, 0 outside the threshold mode
+    unsigned flags;           // LAMP_SIM_PROFILE; LAMP_STAGE1_OFF | LAMP_MU_TRUNC in the threshold mode
     double delta, tau;
 };
 
@@ -32,6 +38,7 @@ struct LogitsParams {
     const float *kt32;
     uint8_t *y8;
     uint16_t *y16;
+    float *ysim;              // SIM profile logit values
     int B, Hq, Hkv, N, causal, window, row0, nrows;
 };
 
@@ -43,6 +50,8 @@ hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float
                           int N, int Nq, int Nk, int D, float scale, hipStream_t s);
 hipError_t launch_logits8(const LogitsParams &p, int D, hipStream_t s);
 hipError_t launch_logits16(const LogitsParams &p, int D, hipStream_t s);
+hipError_t launch_logits_sim(const LogitsParams &p, int D, int high, hipStream_t s);
+hipError_t launch_build_sim_tables(uint16_t *sim8, uint32_t *sim16, unsigned *ambiguous, hipStream_t s);
 hipError_t launch_build_tables(uint8_t *lut8, uint16_t *lut8e, uint16_t *exp16, uint32_t *exp16hl, unsigned *ambiguous,
                               hipStream_t s);
 hipError_t launch_selftest_e4m3(const float *in, uint8_t *out, uint8_t *raw, size_t n, hipStream_t s);

@@ -11,6 +11,8 @@
 
 namespace lamp {
 
+static_assert(SIM8_ENTRIES == SIM8_N && SIM16_TABLE == SIM16_N && SIM8_N <= SIM8_TABLE, "SIM table sizes");
+
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -123,6 +125,33 @@ __global__ void build_tables_kernel(uint8_t *__restrict__ lut8, uint16_t *__rest
     }
 }
 
+// Exponential tables of the SIM profile (layout in lamp_device.h): entry
+// ((e - EMIN) << P) | m is RN_P(exp(-s)), s = (2^P + m) 2^(e-P), rounded to P
+// mantissa bits in FP32's exponent range (quantum 2^(-126-P) below 2^-126);
+// the same enclosure check as above.  sim8 holds 256 entries, those past
+// SIM8_N being 0.
+__global__ void build_sim_tables_kernel(uint16_t *__restrict__ sim8, uint32_t *__restrict__ sim16,
+                                        unsigned *__restrict__ ambiguous)
+{
+    unsigned c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= (unsigned)SIM16_N + (unsigned)SIM8_TABLE) return;
+    const bool small = c >= (unsigned)SIM16_N;
+    const unsigned idx = small ? c - (unsigned)SIM16_N : c;
+    if (small && idx >= (unsigned)SIM8_N) {   // padding of the 256-entry copy
+        sim8[idx] = 0;
+        return;
+    }
+    const int P = small ? 3 : 11;
+    const int e = (small ? SIM8_EMIN : SIM16_EMIN) + (int)(idx >> P);
+    const double s = __builtin_amdgcn_ldexp((double)((1u << P) | (idx & ((1u << P) - 1u))), e - P);
+    const double y = exp_doc(-s);
+    const double lo = y * (1.0 - 0x1p-48), hi = y * (1.0 + 0x1p-48);
+    const double r = rn_grid(y, P, -126);
+    if (rn_grid(lo, P, -126) != r || rn_grid(hi, P, -126) != r) atomicAdd(ambiguous, 1u);
+    if (small) sim8[idx] = (uint16_t)bf16_bits((float)r);   // 4 significant bits: exact in bf16
+    else sim16[idx] = __builtin_bit_cast(uint32_t, (float)r);
+}
+
 // ------------------------------------------------------------------ logits entry kernels
 // One wave: 64 rows x (16*NC) keys.  grid.x = B*Hq*ceil(nrows/64), grid.y = N/(16*NC).
 template <int D, int NC>
@@ -181,6 +210,44 @@ __global__ __launch_bounds__(64) void logits16_kernel(LogitsParams p)
         const int key = key0 + i;
         const bool vis = !(p.causal && key > j) && !(p.window > 0 && key <= j - p.window);
         out[i] = vis ? (uint16_t)(codes[0][i >> 1] >> (16 * (i & 1))) : (uint16_t)0xFFFF;
+    }
+}
+
+// SIM profile logit values: one wave, 64 rows x 16 keys.
+template <int D, bool HIGH>
+__global__ __launch_bounds__(64) void logits_sim_kernel(LogitsParams p)
+{
+    const int lane = threadIdx.x;
+    const int nrg = (p.nrows + 63) / 64;
+    const int bh = blockIdx.x / nrg;
+    const int rg = blockIdx.x % nrg;
+    const int b = bh / p.Hq, h = bh % p.Hq;
+    const int hk = h / (p.Hq / p.Hkv);
+    const int r = rg * 64 + lane;
+    const int rr = r < p.nrows ? r : p.nrows - 1;
+    const int j = p.row0 + rr;
+    const int key0 = blockIdx.y * 16;
+    const float *qrow[1] = {p.qt + (((size_t)b * p.Hq + h) * p.N + j) * D};
+    const float *kt = p.kt32 + (((size_t)b * p.Hkv + hk) * p.N + key0) * (size_t)D;
+    float val[16];
+    if constexpr (HIGH) {
+        uint32_t w[1][16];
+        rec16_chunk<D, 1, true>(qrow, kt, w);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) val[i] = __builtin_bit_cast(float, w[0][i]);
+    } else {
+        uint32_t w[1][8];
+        emu8s_pass<D, 1>(qrow, kt, w);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) val[i] = bf16_value((w[0][i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
+    }
+    if (r >= p.nrows) return;
+    float *out = p.ysim + (((size_t)b * p.Hq + h) * p.nrows + r) * p.N + key0;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        const int key = key0 + i;
+        const bool vis = !(p.causal && key > j) && !(p.window > 0 && key <= j - p.window);
+        out[i] = vis ? val[i] : __builtin_nanf("");
     }
 }
 
@@ -252,6 +319,28 @@ hipError_t launch_logits16(const LogitsParams &p, int D, hipStream_t s)
     if (D == 64) hipLaunchKernelGGL(logits16_kernel<64>, grid, dim3(64), 0, s, p);
     else if (D == 128) hipLaunchKernelGGL(logits16_kernel<128>, grid, dim3(64), 0, s, p);
     else hipLaunchKernelGGL(logits16_kernel<256>, grid, dim3(64), 0, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_logits_sim(const LogitsParams &p, int D, int high, hipStream_t s)
+{
+    dim3 grid((unsigned)(p.B * p.Hq * ((p.nrows + 63) / 64)), (unsigned)(p.N / 16));
+    if (high) {
+        if (D == 64) hipLaunchKernelGGL((logits_sim_kernel<64, true>), grid, dim3(64), 0, s, p);
+        else if (D == 128) hipLaunchKernelGGL((logits_sim_kernel<128, true>), grid, dim3(64), 0, s, p);
+        else hipLaunchKernelGGL((logits_sim_kernel<256, true>), grid, dim3(64), 0, s, p);
+    } else {
+        if (D == 64) hipLaunchKernelGGL((logits_sim_kernel<64, false>), grid, dim3(64), 0, s, p);
+        else if (D == 128) hipLaunchKernelGGL((logits_sim_kernel<128, false>), grid, dim3(64), 0, s, p);
+        else hipLaunchKernelGGL((logits_sim_kernel<256, false>), grid, dim3(64), 0, s, p);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_build_sim_tables(uint16_t *sim8, uint32_t *sim16, unsigned *ambiguous, hipStream_t s)
+{
+    hipLaunchKernelGGL(build_sim_tables_kernel, dim3((SIM16_N + SIM8_TABLE + 255) / 256), dim3(256), 0, s, sim8, sim16,
+                       ambiguous);
     return hipGetLastError();
 }
 

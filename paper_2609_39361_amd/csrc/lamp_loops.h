@@ -134,27 +134,132 @@ template <int QPL, int NKEY, int... I>
 __device__ __forceinline__ void rec16_channel(float kv, const float (&q)[QPL], float (&acc)[QPL][NKEY],
                                               std::integer_sequence<int, I...>);
 
+// ---- the SIM profile (Sec. 4.1): FP32 range, 3 / 11 mantissa bits, no saturation
+// Words of 16-bit logits for NKEY keys: e4m11 codes two per word, or, in the
+// SIM profile, FP32 patterns one per word.
+template <bool SIMP>
+constexpr int y16_words(int nkey)
+{
+    return nkey == 0 ? 1 : (SIMP ? nkey : nkey / 2);
+}
+
+// Value of the i-th 16-bit logit of a word array.
+template <bool SIMP>
+__device__ __forceinline__ float y16_value(const uint32_t *w, int i)
+{
+    if constexpr (SIMP) return __builtin_bit_cast(float, w[i]);
+    else return e4m11_value((w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
+}
+
+// Two SIM 8-bit logits as their bf16 patterns (exact: 3 mantissa bits).
+__device__ __forceinline__ uint32_t pack_sim8(float a, float b)
+{
+    return (__builtin_bit_cast(uint32_t, a) >> 16) | (__builtin_bit_cast(uint32_t, b) & 0xFFFF0000u);
+}
+
+// One channel of the SIM 8-bit accumulation for every key and slot:
+// acc <- RN_3(RN32(q * k + acc)).
+template <int QPL, int... I>
+__device__ __forceinline__ void emu8s_channel(float kv, const float (&q)[QPL], float (&acc)[QPL][16],
+                                              std::integer_sequence<int, I...>)
+{
+#pragma unroll
+    for (int s = 0; s < QPL; ++s) ((acc[s][I] = rn_sim<3>(fmac_bc<I>(acc[s][I], kv, q[s]))), ...);
+}
+
+// Y8 of one 16-key chunk in the SIM profile (as emu8_pass); codes[s][p]
+// receives the bf16 patterns of keys 2p (bits [15:0]) and 2p+1.
+template <int D, int QPL, class QP>
+__device__ __forceinline__ void emu8s_pass(const QP (&qrow)[QPL], const float *k32, uint32_t (&codes)[QPL][8])
+{
+    static_assert(D % 8 == 0, "channels in pairs of 4-channel groups");
+    float acc[QPL][16];
+#pragma unroll
+    for (int s = 0; s < QPL; ++s)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[s][i] = 0.0f;
+    const float *krow = k32 + (size_t)(__lane_id() & 15) * D;
+    float4 ka, kb, qa[QPL], qb[QPL];
+    auto run = [&](const float4 &k4, const float4 (&q4)[QPL]) {
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) {
+            float q[QPL];
+#pragma unroll
+            for (int s = 0; s < QPL; ++s) q[s] = f4_at(q4[s], cc);
+            emu8s_channel<QPL>(f4_at(k4, cc), q, acc, std::make_integer_sequence<int, 16>());
+        }
+    };
+    load_group<QPL>(krow, qrow, 0, ka, qa);
+    for (int c = 0; c < D - 8; c += 8) {
+        load_group<QPL>(krow, qrow, c + 4, kb, qb);
+        run(ka, qa);
+        load_group<QPL>(krow, qrow, c + 8, ka, qa);
+        run(kb, qb);
+    }
+    load_group<QPL>(krow, qrow, D - 4, kb, qb);
+    run(ka, qa);
+    run(kb, qb);
+#pragma unroll
+    for (int s = 0; s < QPL; ++s)
+#pragma unroll
+        for (int p = 0; p < 8; ++p) codes[s][p] = pack_sim8(acc[s][2 * p], acc[s][2 * p + 1]);
+}
+
+// Y8 of a 16-key chunk in either profile.
+template <int D, int QPL, bool SIMP, class QP>
+__device__ __forceinline__ void emu8_any(const QP (&qrow)[QPL], const float *k32, uint32_t (&codes)[QPL][8])
+{
+    if constexpr (SIMP) emu8s_pass<D, QPL>(qrow, k32, codes);
+    else emu8_chunk<D, QPL>(qrow, k32, codes);
+}
+
+// The 16-bit logits of the FP32 chains in acc, encoded: rounded once to e4m11
+// (codes, two per word) or, in the SIM profile, to 11 mantissa bits (FP32
+// patterns, one per word).
+template <bool SIMP, int QPL, int NKEY>
+__device__ __forceinline__ void encode16(const float (&acc)[QPL][NKEY], uint32_t (&c)[QPL][y16_words<SIMP>(NKEY)])
+{
+#pragma unroll
+    for (int s = 0; s < QPL; ++s) {
+        if constexpr (SIMP) {
+#pragma unroll
+            for (int i = 0; i < NKEY; ++i) c[s][i] = __builtin_bit_cast(uint32_t, rn_sim<11>(acc[s][i]));
+        } else {
+#pragma unroll
+            for (int p = 0; p < NKEY / 2; ++p) {
+                uint32_t x0, x1;
+                (void)rn_e4m11((double)acc[s][2 * p], &x0);
+                (void)rn_e4m11((double)acc[s][2 * p + 1], &x1);
+                c[s][p] = x0 | (x1 << 16);
+            }
+        }
+    }
+}
+
 // Two passes over the channels fused into one loop that shares the query
 // loads: the 8-bit accumulation of the 16 keys at k32e (EMU; as emu8_pass,
 // without saturation, then checked as in emu8_chunk) and the 16-bit
 // accumulation of NKEY keys, this lane's key row being krowr (as rec16_keys).
 // The forward kernel uses it to run the 8-bit logits of the next key tile
 // together with the speculative 16-bit recompute of the current one.
-template <int D, int QPL, int NKEY, bool EMU, class QP>
+template <int D, int QPL, int NKEY, bool EMU, bool SIMP, class QP>
 __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k32e, const float *krowr,
-                                           uint32_t (&a8)[QPL][8], uint32_t (&c16)[QPL][NKEY > 0 ? NKEY / 2 : 1])
+                                           uint32_t (&a8)[QPL][8], uint32_t (&c16)[QPL][y16_words<SIMP>(NKEY)])
 {
     static_assert(EMU || NKEY > 0, "something to compute");
     static_assert(NKEY == 0 || NKEY == 4 || NKEY == 8 || NKEY == 12 || NKEY == 16, "0, 4, 8, 12 or 16 keys");
     static_assert(D % 8 == 0, "channels in pairs of 4-channel groups");
     constexpr int NA = NKEY > 0 ? NKEY : 1;
-    float acc[QPL][NA];
+    constexpr int NE = (SIMP && EMU) ? 16 : 1;   // SIM 8-bit accumulators (values, not codes)
+    float acc[QPL][NA], e8[QPL][NE];
 #pragma unroll
     for (int s = 0; s < QPL; ++s) {
 #pragma unroll
         for (int p = 0; p < 8; ++p) a8[s][p] = 0u;
 #pragma unroll
         for (int i = 0; i < NA; ++i) acc[s][i] = 0.0f;
+#pragma unroll
+        for (int i = 0; i < NE; ++i) e8[s][i] = 0.0f;
     }
     const float *krowe = k32e + (size_t)(__lane_id() & 15) * D;
     float4 kea, keb, kra, krb, qa[QPL], qb[QPL];
@@ -170,7 +275,10 @@ __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k
             float q[QPL];
 #pragma unroll
             for (int s = 0; s < QPL; ++s) q[s] = f4_at(q4[s], cc);
-            if constexpr (EMU) emu8_channel<QPL, false>(f4_at(ke, cc), q, a8, std::make_integer_sequence<int, 8>());
+            if constexpr (EMU && SIMP)
+                emu8s_channel<QPL>(f4_at(ke, cc), q, e8, std::make_integer_sequence<int, 16>());
+            else if constexpr (EMU)
+                emu8_channel<QPL, false>(f4_at(ke, cc), q, a8, std::make_integer_sequence<int, 8>());
             if constexpr (NKEY > 0)
                 rec16_channel<QPL, NKEY>(f4_at(kr, cc), q, acc, std::make_integer_sequence<int, NKEY>());
         }
@@ -185,7 +293,12 @@ __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k
     ld(D - 4, keb, krb, qb);
     run(kea, kra, qa);
     run(keb, krb, qb);
-    if constexpr (EMU) {
+    if constexpr (EMU && SIMP) {
+#pragma unroll
+        for (int s = 0; s < QPL; ++s)
+#pragma unroll
+            for (int p = 0; p < 8; ++p) a8[s][p] = pack_sim8(e8[s][2 * p], e8[s][2 * p + 1]);
+    } else if constexpr (EMU) {
         uint32_t nan = 0;
 #pragma unroll
         for (int s = 0; s < QPL; ++s)
@@ -193,17 +306,7 @@ __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k
             for (int p = 0; p < 8; ++p) nan |= e4m3_nan_bits(a8[s][p]);
         if (wave_any(nan != 0)) emu8_pass<D, QPL, true>(qrow, k32e, a8);
     }
-    if constexpr (NKEY > 0) {
-#pragma unroll
-        for (int s = 0; s < QPL; ++s)
-#pragma unroll
-            for (int p = 0; p < NKEY / 2; ++p) {
-                uint32_t x0, x1;
-                (void)rn_e4m11((double)acc[s][2 * p], &x0);
-                (void)rn_e4m11((double)acc[s][2 * p + 1], &x1);
-                c16[s][p] = x0 | (x1 << 16);
-            }
-    }
+    if constexpr (NKEY > 0) encode16<SIMP>(acc, c16);
 }
 
 // One channel of the 16-bit accumulation for every key and slot.
@@ -220,12 +323,13 @@ __device__ __forceinline__ void rec16_channel(float kv, const float (&q)[QPL], f
 // (saturating).  krow is this lane's key row ([D] fp32): lane l of every
 // 16-lane row supplies key (l mod 16) and must hold key (l mod NKEY) (lanes
 // past NKEY duplicate the first keys and are not read).  codes[s][p] receives
-// the e4m11 codes of keys 2p (bits [15:0]) and 2p+1.  With few keys per
+// the e4m11 codes of keys 2p (bits [15:0]) and 2p+1 (SIM profile: rounded to
+// 11 mantissa bits, codes[s][i] the FP32 pattern of key i).  With few keys per
 // channel the loop is latency-bound, so the loads run PD 4-channel groups
 // ahead in a ring of buffers written only by loads.
-template <int D, int QPL, int NKEY, class QP>
+template <int D, int QPL, int NKEY, bool SIMP = false, class QP>
 __device__ __forceinline__ void rec16_keys(const QP (&qrow)[QPL], const float *krow,
-                                           uint32_t (&codes)[QPL][NKEY / 2])
+                                           uint32_t (&codes)[QPL][y16_words<SIMP>(NKEY)])
 {
     static_assert(NKEY == 4 || NKEY == 8 || NKEY == 12 || NKEY == 16, "4, 8, 12 or 16 keys");
     constexpr int PD0 = NKEY <= 8 ? 4 : 2;
@@ -257,22 +361,15 @@ __device__ __forceinline__ void rec16_keys(const QP (&qrow)[QPL], const float *k
     }
 #pragma unroll
     for (int r = 0; r < PD; ++r) run(r);   // the last ring, no further loads
-#pragma unroll
-    for (int s = 0; s < QPL; ++s)
-#pragma unroll
-        for (int p = 0; p < NKEY / 2; ++p) {
-            uint32_t c0, c1;
-            (void)rn_e4m11((double)acc[s][2 * p], &c0);
-            (void)rn_e4m11((double)acc[s][2 * p + 1], &c1);
-            codes[s][p] = c0 | (c1 << 16);
-        }
+    encode16<SIMP>(acc, codes);
 }
 
 // Y16 of the 16 keys starting at k32 ([key][D] fp32).
-template <int D, int QPL, class QP>
-__device__ __forceinline__ void rec16_chunk(const QP (&qrow)[QPL], const float *k32, uint32_t (&codes)[QPL][8])
+template <int D, int QPL, bool SIMP = false, class QP>
+__device__ __forceinline__ void rec16_chunk(const QP (&qrow)[QPL], const float *k32,
+                                            uint32_t (&codes)[QPL][y16_words<SIMP>(16)])
 {
-    rec16_keys<D, QPL, 16>(qrow, k32 + (size_t)(__lane_id() & 15) * D, codes);
+    rec16_keys<D, QPL, 16, SIMP>(qrow, k32 + (size_t)(__lane_id() & 15) * D, codes);
 }
 
 } // namespace lamp

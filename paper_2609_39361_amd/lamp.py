@@ -41,6 +41,10 @@ def lib():
         L.lamp_attn_logits8.restype = i32
         L.lamp_attn_logits16.argtypes = [P, P] + [i32] * 9 + [P, P]
         L.lamp_attn_logits16.restype = i32
+        L.lamp_attn_logits_sim.argtypes = [P, P] + [i32] * 10 + [P, P]
+        L.lamp_attn_logits_sim.restype = i32
+        L.lamp_get_sim_tables.argtypes = [i32, P, P]
+        L.lamp_get_sim_tables.restype = i32
         L.lamp_init.argtypes = [i32]
         L.lamp_init.restype = i32
         L.lamp_shutdown.argtypes = []
@@ -94,14 +98,16 @@ def _check_inputs(q, k, v=None):
 
 
 STAGE1_OFF = 1   # the first stage disabled: mu_hat from the 8-bit maxima, stage 2 alone recomputes
-MU_TRUNC = 2     # 8-bit shifts against mu_hat truncated to e4m3
+MU_TRUNC = 2     # 8-bit shifts against mu_hat truncated to e4m3 (SIM profile: to 3 mantissa bits)
+SIM_PROFILE = 4  # the SIM precision profile (FP32 range, 3 / 11 mantissa bits, no saturation)
 
 
 def attn_fwd(q, k, v, causal=True, window=0, bq=128, bk=16, nk=4, delta=2.0 ** -8, tau=0.5, out=None, flags=0):
     """LampAttention forward pass.  Returns (o fp32 [B,Hq,N,d], lse fp32
     [B,Hq,N], mask uint8 [B,Hq,ceil(N/bq),ceil(N/(bk*nk))*nk]); N need not be
     a multiple of the block sizes.  `out` may supply those three tensors to
-    write into; `flags` selects the variants STAGE1_OFF, MU_TRUNC."""
+    write into; `flags` selects the variants STAGE1_OFF, MU_TRUNC and the
+    SIM_PROFILE numerics."""
     B, Hq, Hkv, N, d = _check_inputs(q, k, v)
     dev = q.device
     if out is None:
@@ -142,6 +148,19 @@ def logits16(q, k, causal=True, window=0, row0=0, nrows=None):
     return y
 
 
+def logits_sim(q, k, high, causal=True, window=0, row0=0, nrows=None):
+    """SIM-profile logit values (high=False: 8-bit recursion, True: 16-bit):
+    fp32 [B,Hq,nrows,N], NaN invisible."""
+    B, Hq, Hkv, N, d = _check_inputs(q, k)
+    nrows = N - row0 if nrows is None else nrows
+    y = torch.empty((B, Hq, nrows, N), dtype=torch.float32, device=q.device)
+    with torch.cuda.device(q.device):
+        rc = lib().lamp_attn_logits_sim(_ptr(q), _ptr(k), B, Hq, Hkv, N, d, int(causal), int(window), row0, nrows,
+                                        int(bool(high)), _ptr(y), _stream(q.device))
+    _check(rc)
+    return y
+
+
 def selftest_e4m3(x):
     """(codes, raw codes) of fp32 CUDA tensor x by the device rounding sequence."""
     assert x.dtype == torch.float32 and x.is_cuda and x.is_contiguous()
@@ -177,6 +196,18 @@ def get_exp16_parts(device=0):
     parts = np.zeros(65536, dtype=np.uint32)
     _check(lib().lamp_get_exp16_parts(int(device), parts.ctypes.data_as(ctypes.c_void_p)))
     return parts
+
+
+def get_sim_tables(device=0):
+    """(sim8 uint16[112] bf16 bits, sim16 uint32[45056] FP32 patterns): the
+    SIM profile's exponential tables, entry ((e - emin) << p) | m for the shift
+    (2^p + m) 2^(e - p); p = 3, e in [-6, 7] and p = 11, e in [-14, 7]."""
+    import numpy as np
+    sim8 = np.zeros(112, dtype=np.uint16)
+    sim16 = np.zeros(45056, dtype=np.uint32)
+    _check(lib().lamp_get_sim_tables(int(device), sim8.ctypes.data_as(ctypes.c_void_p),
+                                     sim16.ctypes.data_as(ctypes.c_void_p)))
+    return sim8, sim16
 
 
 def init(device=0):

@@ -69,9 +69,16 @@ def test_binding_rejects_bad_arguments_without_gpu():
                            dummy, dummy, dummy, None)
     assert rc == 1
     # unknown flag bits
-    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 4,
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 8,
                            dummy, dummy, dummy, None)
     assert rc == 1 and b"flags" in lib.lamp_last_error()
+    # the SIM profile is built for 16-key sub-blocks and d >= 128 only
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 128, 64, 4, 2 ** -8, 0.5, 4,
+                           dummy, dummy, dummy, None)
+    assert rc == 2 and b"SIM" in lib.lamp_last_error()
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 64, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 4,
+                           dummy, dummy, dummy, None)
+    assert rc == 2 and b"SIM" in lib.lamp_last_error()
     # block sizes that are not built
     rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 32, 16, 4, 2 ** -8, 0.5, 0,
                            dummy, dummy, dummy, None)

@@ -338,3 +338,95 @@ def test_fwd_degenerate_inputs(L, w, tau):
     err, mask = _compare_fwd(L, w, tau)
     if "zero_q" in w.extra and tau == 0.5:
         assert np.all((mask == 1) | (mask == 3))
+
+
+# ------------------------------------------------------------------ SIM profile
+def _sim_grid(p, emin, emax):
+    idx = np.arange((emax - emin + 1) << p)
+    e = emin + (idx >> p)
+    m = idx & ((1 << p) - 1)
+    return ((1 << p) + m) * np.exp2((e - p).astype(np.float64))
+
+
+def test_sim_tables_match_oracle(L):
+    """The SIM profile's exponential tables, entry by entry, against the
+    oracle's correctly rounded exponentials; shifts below the first row give
+    1 and beyond the last 0 in the oracle, as the kernel's clamping assumes."""
+    sim8, sim16 = L.get_sim_tables(0)
+    for p, emin, emax, got in ((3, -6, 7, (sim8.astype(np.uint32) << 16).view(np.float32)),
+                               (11, -14, 7, sim16.view(np.float32))):
+        s = _sim_grid(p, emin, emax)
+        ref = O.sim_exp(p, s)
+        assert np.array_equal(got.astype(np.float64), ref)
+        assert np.all(ref[: 1 << p] == 1.0) and np.all(ref[-(1 << p):] == 0.0)
+        below = _sim_grid(p, -40, emin - 1)
+        above = _sim_grid(p, emax + 1, emax + 3)
+        assert np.all(O.sim_exp(p, below) == 1.0) and np.all(O.sim_exp(p, above) == 0.0)
+
+
+SIM_LOGIT_CASES = [LOGIT_CASES[0], LOGIT_CASES[1], LOGIT_CASES[2], LOGIT_CASES[3], LOGIT_CASES[4], LOGIT_CASES[5]]
+
+
+@pytest.mark.parametrize("high", [0, 1])
+@pytest.mark.parametrize("w", SIM_LOGIT_CASES, ids=[w.name for w in SIM_LOGIT_CASES])
+def test_logits_sim_bitexact(L, w, high):
+    q, k, v = W.make_inputs(w)
+    ref = O.logits_sim(O.bf16_bits(q), O.bf16_bits(k), w.causal, w.window, 0, w.N, high)
+    got = L.logits_sim(q.cuda(), k.cuda(), high, w.causal, w.window, 0, w.N).cpu().numpy().astype(np.float64)
+    assert np.array_equal(np.isnan(got), np.isnan(ref))
+    vis = ~np.isnan(ref)
+    assert np.array_equal(got[vis], ref[vis]), "%d values differ" % (got[vis] != ref[vis]).sum()
+
+
+SIM_FWD_CASES = [FWD_CASES[0], FWD_CASES[3], FWD_CASES[5],
+                 W.small("s_gqa_d128_bq64", N=384, d=128, Hq=4, Hkv=2, bq=64, bk=16, nk=4, causal=1, seed=211),
+                 W.small("s_outlier_d128", N=256, d=128, Hq=1, Hkv=1, bq=128, bk=16, nk=4, causal=0, seed=212,
+                         kind="outlier", n_outlier=2, outlier_gain=40.0)]
+
+
+@pytest.mark.parametrize("tau", [math.inf, 1.0, 0.5, 2.0 ** -5, 0.0])
+@pytest.mark.parametrize("w", SIM_FWD_CASES, ids=[w.name for w in SIM_FWD_CASES])
+def test_fwd_sim_small(L, w, tau):
+    _compare_fwd(L, w, tau, flags=O.SIM)
+
+
+@pytest.mark.parametrize("flags", [O.SIM | O.STAGE1_OFF, O.SIM | O.MU_TRUNC])
+@pytest.mark.parametrize("w", [FWD_CASES[0], FWD_CASES[5]], ids=[FWD_CASES[0].name, FWD_CASES[5].name])
+def test_fwd_sim_variants(L, w, flags):
+    _compare_fwd(L, w, 2.0 ** -5, flags=flags)
+
+
+@pytest.mark.parametrize("tau", [math.inf, 0.5, 0.0])
+@pytest.mark.parametrize("w", [RAGGED_CASES[0], RAGGED_CASES[2], RAGGED_CASES[3], RAGGED_CASES[6]] + DEGENERATE[:3],
+                         ids=[w.name for w in [RAGGED_CASES[0], RAGGED_CASES[2], RAGGED_CASES[3], RAGGED_CASES[6]]
+                              + DEGENERATE[:3]])
+def test_fwd_sim_ragged_and_degenerate(L, w, tau):
+    _compare_fwd(L, w, tau, flags=O.SIM)
+
+
+@pytest.mark.parametrize("tau", [0.5, 2.0 ** -5])
+def test_fwd_sim_config3_sampled(L, tau):
+    w = W.CONFIGS[3]
+    nqb = w.N // w.bq
+    qbl = [nqb - 1, 21, 31 * nqb + nqb - 1]
+    err, mask = _compare_fwd(L, w, tau, qblocks=qbl, flags=O.SIM)
+    _say("config 3 SIM tau %s sampled: O err %.2e, mask %s" % (tau, err, np.bincount(mask.ravel(), minlength=4)))
+
+
+def test_fwd_sim_config4_global_sampled(L):
+    w = W.CONFIGS[40]
+    nqb = w.N // w.bq
+    qbl = [nqb - 1, (w.Hq - 1) * nqb + nqb // 2]
+    err, mask = _compare_fwd(L, w, w.tau, qblocks=qbl, flags=O.SIM)
+    _say("config 40 SIM sampled: O err %.2e, mask %s" % (err, np.bincount(mask.ravel(), minlength=4)))
+
+
+@pytest.mark.parametrize("tau", W.TAU_SWEEP)
+def test_fwd_sim_config5_sampled(L, tau):
+    w = W.CONFIGS[5]
+    nqb = w.N // w.bq
+    qbl = [nqb - 1, (3 * w.Hq + 31) * nqb + nqb - 1, (2 * w.Hq + 20) * nqb + nqb // 4]
+    t0 = time.time()
+    err, mask = _compare_fwd(L, w, tau, qblocks=qbl, keep=True, flags=O.SIM)
+    _say("config 5 SIM tau %s sampled: O err %.2e, mask %s (%.1f s)" % (
+        tau, err, np.bincount(mask.ravel(), minlength=4), time.time() - t0))
