@@ -30,6 +30,11 @@ VALU_LANE_OPS = 256 * 4 * 16 * 2.4e9          # 39.3e12 lane-instructions / s
 OPS_PER_MAC8 = 2.0
 # 16-bit recompute: one fp32 FMA per multiply-add.
 OPS_PER_MAC16 = 1.0
+# SIM precision profile (flag 4): the 8-bit step is one fp32 FMA and a
+# round-to-nearest-even of the FP32 encoding to 3 mantissa bits (bit-field
+# extract of the last kept bit, one 3-input add, one mask): 4 per MAC.
+OPS_PER_MAC8_SIM = 4.0
+SIM_FLAG = 4
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lamp_fwd16_kernel.qwen3-8b-prefill-8k.hbm_traffic.md")
@@ -148,7 +153,8 @@ def main():
     ap.add_argument("--tau", type=float, default=None)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
-    ap.add_argument("--flags", type=int, default=0, help="variants: 1 first stage off, 2 mu_hat truncation")
+    ap.add_argument("--flags", type=int, default=0,
+                    help="variants: 1 first stage off, 2 mu_hat truncation, 4 SIM precision profile")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="before the timed steps, run one plain negating copy of this many MiB "
                          "(fp32 in, fp32 out) to calibrate the HBM byte counters")
@@ -210,7 +216,8 @@ def main():
     mask_np = mask.cpu().numpy()
     mac8 = 0 if tau == 0 else w.macs
     mac16 = visible_in_mask(w, mask_np) * w.d
-    alg_ops = OPS_PER_MAC8 * mac8 + OPS_PER_MAC16 * mac16
+    sim = bool(args.flags & SIM_FLAG)
+    alg_ops = (OPS_PER_MAC8_SIM if sim else OPS_PER_MAC8) * mac8 + OPS_PER_MAC16 * mac16
     achieved = alg_ops / (kernel_ms * 1e-3) / 1e12
     peak = VALU_LANE_OPS / 1e12
     result = {
@@ -224,7 +231,8 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "e4m3/e4m11 emulated (fp32 FMA + fp8 conversions), bf16 inputs, fp32 output",
+        "dtype": ("SIM profile: fp32 with 3/11-bit mantissas (fp32 FMA + integer rounding), bf16 inputs, fp32 output"
+                  if sim else "e4m3/e4m11 emulated (fp32 FMA + fp8 conversions), bf16 inputs, fp32 output"),
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "N": w.N, "d": w.d,
                    "causal": w.causal, "window": w.window, "bq": w.bq, "bk": w.bk, "nk": w.nk,
@@ -239,13 +247,14 @@ def main():
             "unit": "T VALU lane-ops/s",
             "frac": achieved / peak,
             "traffic": measured_traffic(w.name, tau, args.flags),
-            "kernel": ("lamp_fwd16_kernel<%d,%d,%d>" % (w.d, w.bq, _mode_of(tau)))
+            "kernel": ("lamp_fwd16_kernel<%d,%d,%d,%s>" % (w.d, w.bq, _mode_of(tau), "true" if sim else "false"))
                       if (w.bk == 16 and w.d >= 128)
                       else ("lamp_fwd_kernel<%d,%d,%d,%d>" % (w.d, w.bq, w.bk, w.nk)),
             "kernel_ms": kernel_ms,
             "prepass_ms": pre_ms_sum / launches,
             "ops_per_launch": alg_ops,
-            "ops_per_unit": "2 per emulated 8-bit MAC, 1 per 16-bit recompute MAC",
+            "ops_per_unit": ("%d per emulated 8-bit MAC, 1 per 16-bit recompute MAC"
+                             % (OPS_PER_MAC8_SIM if sim else OPS_PER_MAC8)),
             "algorithmic_frac_one_op_per_mac": (mac8 + mac16) / (kernel_ms * 1e-3) / VALU_LANE_OPS,
             "valu_issue_frac_counters": measured_valu_issue(w.name, tau, args.flags),
         },
