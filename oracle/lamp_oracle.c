@@ -937,6 +937,191 @@ int lamp_oracle_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
     return g_sim_fail ? -2 : 0;
 }
 
+/* ------------------------------------------------------------------------ */
+/* The vector form for single query rows (Sec. 2, "Look-ahead distribution   */
+/* of precisions", Eq. (6)): decode against a key/value cache.               */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    const uint16_t *q, *k, *v;
+    int B, Hq, Hkv, M, N, d, causal, window, tk;
+    double delta, tau;
+    double *o, *lse;
+    uint8_t *mask;
+} dec_args_t;
+
+typedef struct {
+    double key;
+    int idx;
+} kidx_t;
+
+/* ascending cost; reading: ties by ascending key index */
+static int cmp_kidx(const void *pa, const void *pb)
+{
+    const kidx_t *a = (const kidx_t *)pa, *b = (const kidx_t *)pb;
+    if (a->key < b->key) return -1;
+    if (a->key > b->key) return 1;
+    return (a->idx > b->idx) - (a->idx < b->idx);
+}
+
+/* One query row: the online-softmax update of Sec. 2 over key tiles of tk
+ * logits, each tile with the two-step look-ahead of Sec. 2:
+ *   1. the maximizer c of the tile's 8-bit logits (reading: the first index
+ *      attaining the maximum) passes if mu > fl(y_c) + |mu| delta, tested as
+ *      mu > fma(|mu|, delta, fl(y_c)) (mu = -inf fails); then mu_hat = mu;
+ *      otherwise y_c is recomputed in 16 bits, g_c = 0, and
+ *      mu_hat = max(mu, y16_c);
+ *   2. Eq. (6), a knapsack with uniform values solved greedily: the costs
+ *      p_i (1 - p_i) of the remaining 8-bit logits, taken in the scaled form
+ *      E_i (omega_hat - E_i) against tau omega_hat^2 (as in Eq. (8)), are
+ *      sorted ascending (ties by index) and accumulated in fp64 while the sum
+ *      stays within the limit; the first cost that would pass it and every
+ *      later one are recomputed in 16 bits against the same mu_hat.
+ * tau = +inf keeps every logit in 8 bits (mu_hat = max(mu, max fl(y)));
+ * tau = 0 recomputes every visible logit. */
+static void dec_row(const dec_args_t *A, int b, int h, int r)
+{
+    const int d = A->d, N = A->N, tk = A->tk;
+    const int64_t P = (int64_t)N - A->M + r;           /* the query's position */
+    const int G = A->Hq / A->Hkv;
+    const int ntiles = (N + tk - 1) / tk;
+    const float s = scale_of(d);
+    const uint16_t *kbase = A->k + ((int64_t)b * A->Hkv + h / G) * (int64_t)N * d;
+    const uint16_t *vbase = A->v + ((int64_t)b * A->Hkv + h / G) * (int64_t)N * d;
+    const int pure8 = isinf(A->tau) && A->tau > 0;
+    const int all16 = (A->tau == 0.0);
+    const int64_t row = ((int64_t)b * A->Hq + h) * A->M + r;
+
+    float *qt = (float *)malloc(sizeof(float) * (size_t)d);
+    double *O = (double *)calloc((size_t)d, sizeof(double));
+    double *Y = (double *)malloc(sizeof(double) * (size_t)tk);
+    double *E = (double *)malloc(sizeof(double) * (size_t)tk);
+    unsigned char *vis = (unsigned char *)malloc((size_t)tk);
+    unsigned char *prec = (unsigned char *)malloc((size_t)tk);
+    kidx_t *F = (kidx_t *)malloc(sizeof(kidx_t) * (size_t)tk);
+    prescale(A->q + row * d, d, s, qt);
+    double mu = -INFINITY, om = 0.0;
+    uint8_t *mrow = A->mask + row * (int64_t)ntiles * tk;
+    for (int64_t i = 0; i < (int64_t)ntiles * tk; ++i) mrow[i] = MASK_INACTIVE;
+
+    for (int t = 0; t < ntiles; ++t) {
+        const int64_t k0 = (int64_t)t * tk;
+        int nvis = 0;
+        for (int i = 0; i < tk; ++i) {
+            vis[i] = (unsigned char)(k0 + i < N && visible(k0 + i, P, A->causal, A->window));
+            nvis += vis[i];
+            prec[i] = vis[i] ? MASK_LOW : MASK_INACTIVE;
+        }
+        if (!nvis) continue;                     /* no state change */
+        double muh;
+        if (all16) {
+            muh = mu;
+            for (int i = 0; i < tk; ++i) {
+                if (!vis[i]) continue;
+                Y[i] = logit16(qt, kbase + (k0 + i) * d, d);
+                prec[i] = MASK_STAGE1;
+                if (Y[i] > muh) muh = Y[i];
+            }
+        } else {
+            int c = -1;
+            for (int i = 0; i < tk; ++i) {
+                if (!vis[i]) continue;
+                Y[i] = logit8(qt, kbase + (k0 + i) * d, d);
+                if (c < 0 || Y[i] > Y[c]) c = i;
+            }
+            if (pure8) {
+                muh = Y[c] > mu ? Y[c] : mu;
+            } else if (mu > fma(fabs(mu), A->delta, Y[c])) {
+                muh = mu;
+            } else {
+                Y[c] = logit16(qt, kbase + (k0 + c) * d, d);
+                prec[c] = MASK_STAGE1;
+                muh = Y[c] > mu ? Y[c] : mu;
+            }
+        }
+        for (int i = 0; i < tk; ++i)
+            E[i] = vis[i] ? shifted_exp(muh, Y[i], prec[i] == MASK_STAGE1) : 0.0;
+        const double lam = (mu == -INFINITY) ? 0.0 : exp_doc(mu - muh);
+        double S = 0.0;
+        for (int i = 0; i < tk; ++i) S += E[i];  /* exact (multiples of 2^-41) */
+        const double omh = fma(lam, om, S);
+        if (!pure8 && !all16) {
+            int nf = 0;
+            for (int i = 0; i < tk; ++i) {
+                if (prec[i] != MASK_LOW) continue;
+                double tt = omh - E[i];
+                F[nf].key = E[i] * tt;
+                F[nf].idx = i;
+                ++nf;
+            }
+            qsort(F, (size_t)nf, sizeof(kidx_t), cmp_kidx);
+            const double lim = (A->tau * omh) * omh;
+            double xi = 0.0;
+            int a = 0;
+            for (; a < nf; ++a) {
+                double nx = xi + F[a].key;
+                if (!(nx <= lim)) break;
+                xi = nx;
+            }
+            for (; a < nf; ++a) {                 /* recomputed in 16 bits */
+                int i = F[a].idx;
+                Y[i] = logit16(qt, kbase + (k0 + i) * d, d);
+                E[i] = shifted_exp(muh, Y[i], 1);
+                prec[i] = MASK_STAGE2;
+            }
+        }
+        double S2 = 0.0;
+        for (int i = 0; i < tk; ++i) S2 += E[i];
+        om = fma(lam, om, S2);
+        for (int c = 0; c < d; ++c) O[c] *= lam;
+        for (int i = 0; i < tk; ++i) {
+            if (E[i] == 0.0) continue;
+            const uint16_t *vr = vbase + (k0 + i) * d;
+            for (int c = 0; c < d; ++c) O[c] += E[i] * (double)bf16_to_f32(vr[c]);
+        }
+        mu = muh;
+        for (int i = 0; i < tk; ++i) mrow[k0 + i] = prec[i];
+    }
+    double *dst = A->o + row * d;
+    for (int c = 0; c < d; ++c) dst[c] = O[c] / om;
+    A->lse[row] = mu + log(om);
+    free(qt); free(O); free(Y); free(E); free(vis); free(prec); free(F);
+}
+
+/* lamp_oracle_decode: q [B,Hq,M,d] (M query rows at positions N-M .. N-1),
+ * k, v [B,Hkv,N,d] bf16 bit patterns (host); o [B,Hq,M,d] fp64, lse [B,Hq,M]
+ * fp64, mask [B,Hq,M,ceil(N/tk)*tk] u8 per key (0 8-bit, 1 the maximizer
+ * recomputed by the look-ahead test (every logit at tau = 0), 2 recomputed by
+ * the knapsack, 3 invisible).  rows != NULL computes only the listed rows
+ * (flat (b*Hq + h)*M + r).  flags must be 0.  Returns 0, -1 on invalid
+ * arguments, -2 on a table failure. */
+int lamp_oracle_decode(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                       int B, int Hq, int Hkv, int M, int N, int d, int causal, int window, int tk,
+                       double delta, double tau, unsigned flags, double *o, double *lse, uint8_t *mask,
+                       const int64_t *rows, int64_t nrows, int nthreads)
+{
+    if (B < 0 || Hq <= 0 || Hkv <= 0 || M < 0 || N < 0 || M > N || d <= 0 || d > 1024) return -1;
+    if (Hq % Hkv || tk <= 0 || window < 0 || (window > 0 && !causal)) return -1;
+    if (!(tau >= 0.0) || !(delta >= 0.0) || flags) return -1;
+    if (build_tables()) return -2;
+    if (B == 0 || M == 0) return 0;
+    dec_args_t A = {q, k, v, B, Hq, Hkv, M, N, d, causal, window, tk, delta, tau, o, lse, mask};
+    const int64_t total = (int64_t)B * Hq * M;
+    const int64_t count = rows ? nrows : total;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+#endif
+    for (int64_t t = 0; t < count; ++t) {
+        int64_t f = rows ? rows[t] : t;
+        int r = (int)(f % M);
+        int h = (int)((f / M) % Hq);
+        int b = (int)(f / ((int64_t)M * Hq));
+        dec_row(&A, b, h, r);
+    }
+    return 0;
+}
+
 int oracle_max_threads(void)
 {
 #ifdef _OPENMP

@@ -68,6 +68,8 @@ def lib():
         _lib.oracle_trunc_sim3.restype = f64
         _lib.oracle_logits_sim.argtypes = [P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, i32]
         _lib.oracle_logits_sim.restype = i32
+        _lib.lamp_oracle_decode.argtypes = [P, P, P] + [i32] * 9 + [f64, f64, ctypes.c_uint, P, P, P, P, i64, i32]
+        _lib.lamp_oracle_decode.restype = i32
         _lib.oracle_max_threads.argtypes = []
         _lib.oracle_max_threads.restype = i32
     return _lib
@@ -252,3 +254,30 @@ def fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, qblocks=None, nthreads=
 
 def max_threads():
     return lib().oracle_max_threads()
+
+
+def decode(q, k, v, causal, window, tk, delta, tau, rows=None, nthreads=0):
+    """The vector-LAMP decode pass (Sec. 2, Eq. (6)) on the CPU.
+
+    q [B,Hq,M,d]: M query rows at positions N-M .. N-1; k, v [B,Hkv,N,d].
+    Returns (o [B,Hq,M,d] fp64, lse [B,Hq,M] fp64, mask [B,Hq,M,ceil(N/tk)*tk]
+    u8 per key).  With `rows` (flat (b*Hq+h)*M+r) only those rows are computed
+    (the others hold NaN and mask 0xFE)."""
+    q = np.ascontiguousarray(q, dtype=np.uint16)
+    k = np.ascontiguousarray(k, dtype=np.uint16)
+    v = np.ascontiguousarray(v, dtype=np.uint16)
+    B, Hq, M, d = q.shape
+    Hkv, N = k.shape[1], k.shape[2]
+    o = np.full((B, Hq, M, d), np.nan, dtype=np.float64)
+    lse = np.full((B, Hq, M), np.nan, dtype=np.float64)
+    mask = np.full((B, Hq, M, -(-N // tk) * tk), 0xFE, dtype=np.uint8)
+    if rows is not None:
+        rl = np.ascontiguousarray(rows, dtype=np.int64)
+        rp, nr = _ptr(rl), rl.size
+    else:
+        rp, nr = None, 0
+    rc = lib().lamp_oracle_decode(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, M, N, d, int(causal), int(window), tk,
+                                  float(delta), float(tau), 0, _ptr(o), _ptr(lse), _ptr(mask), rp, nr, nthreads)
+    if rc != 0:
+        raise ValueError("lamp_oracle_decode failed with %d" % rc)
+    return o, lse, mask

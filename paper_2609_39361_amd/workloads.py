@@ -49,6 +49,7 @@ class Workload:
     outlier_gain: float = 1.0
     sink_rows: int = 0            # key rows scaled by sink_gain per (b, h)
     sink_gain: float = 1.0
+    M: int = 0                    # decode form: query rows per (b, h) at positions N-M .. N-1 (0: prefill)
     extra: dict = field(default_factory=dict)
 
     def replace(self, **kw):
@@ -60,6 +61,10 @@ class Workload:
     def visible_logits(self):
         """Number of (query, key) pairs the mask leaves visible, all heads."""
         N, W = self.N, self.window
+        if self.M > 0:   # query rows at positions N-M .. N-1 against N keys
+            pos = np.arange(N - self.M, N)
+            vis = np.full(self.M, N) if not self.causal else (pos + 1 if W <= 0 else np.minimum(pos + 1, W))
+            return self.B * self.Hq * int(vis.sum())
         if not self.causal:
             per = N * N
         elif W <= 0 or W >= N:
@@ -75,7 +80,10 @@ class Workload:
 
     @property
     def eff_flops(self):
-        """Effective attention FLOP: 4*B*H*N^2*d, halved for causal."""
+        """Effective attention FLOP: 4*B*H*N^2*d, halved for causal (decode
+        form: 4*d per visible (query, key) pair)."""
+        if self.M > 0:
+            return 4.0 * self.d * self.visible_logits
         f = 4.0 * self.B * self.Hq * self.N * self.N * self.d
         return f / 2 if self.causal else f
 
@@ -96,6 +104,11 @@ CONFIGS = {
                  kind="rope_lognormal", rope_base=1e6, scale_sigma=1.0),
     5: Workload("c5_long_context_b4_n32768", 4, 32, 8, 32768, 128, 1, 0, 128, 16, 4, seed=4,
                 kind="rope_student_t", rope_base=1e6),
+    # Decode form (vector LAMP, Sec. 2, Eq. (6)): one new query row per
+    # sequence against an 8K key/value cache, Qwen3-8B attention shape and
+    # config-3 statistics; key tiles of 64 logits (bk), one row per update.
+    6: Workload("c6_qwen3_8b_decode_b32_kv8192", 32, 32, 8, 8192, 128, 1, 0, 1, 64, 1, seed=5,
+                kind="rope_lognormal", rope_base=1e6, scale_sigma=0.75, M=1),
 }
 
 TAU_SWEEP = [math.inf, 1.0, 0.5, 2.0 ** -5, 0.0]
@@ -121,7 +134,8 @@ def make_inputs(w: Workload, device="cpu"):
     g = torch.Generator("cpu")
     g.manual_seed(int(w.seed))
     B, Hq, Hkv, N, d = w.B, w.Hq, w.Hkv, w.N, w.d
-    q = torch.randn((B, Hq, N, d), generator=g, dtype=torch.float32)
+    nq = w.M if w.M > 0 else N          # decode form: the last M positions only
+    q = torch.randn((B, Hq, nq, d), generator=g, dtype=torch.float32)
     k = torch.randn((B, Hkv, N, d), generator=g, dtype=torch.float32)
     v = torch.randn((B, Hkv, N, d), generator=g, dtype=torch.float32)
     if w.kind == "outlier":
@@ -152,7 +166,7 @@ def make_inputs(w: Workload, device="cpu"):
         q *= sq
         k *= sk
         if w.rope_base > 0:
-            _rope_(q, w.rope_base)
+            _rope_(q, w.rope_base, N - nq)
             _rope_(k, w.rope_base)
     elif w.kind == "gauss":
         pass
@@ -160,7 +174,7 @@ def make_inputs(w: Workload, device="cpu"):
         # Small integers: every partial sum is exactly representable in the
         # accumulator formats (used by tests).
         lim = int(w.extra.get("lim", 2))
-        q = torch.randint(-lim, lim + 1, (B, Hq, N, d), generator=g).float()
+        q = torch.randint(-lim, lim + 1, (B, Hq, nq, d), generator=g).float()
         k = torch.randint(-lim, lim + 1, (B, Hkv, N, d), generator=g).float()
         v = torch.randint(-lim, lim + 1, (B, Hkv, N, d), generator=g).float()
     else:
@@ -176,6 +190,8 @@ def make_inputs(w: Workload, device="cpu"):
     if w.extra.get("const"):
         q[:] = q[:, :, :1, :].clone()
         k[:] = k[:, :, :1, :].clone()
+    if w.kind == "outlier" and w.M > 0:
+        raise ValueError("outlier recipe is for the prefill form")
     out = tuple(t.to(torch.bfloat16).contiguous() for t in (q, k, v))
     if device != "cpu":
         out = tuple(t.to(device) for t in out)

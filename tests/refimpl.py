@@ -268,3 +268,92 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=
                     o[b, h, q0:q0 + nr] = (O / om[:, None])[:nr]
                     lse[b, h, q0:q0 + nr] = (mu + np.log(om))[:nr]
     return o, lse, mask
+
+
+def ref_decode(q, k, v, causal, window, tk, delta, tau, tabs, scale):
+    """The vector-LAMP decode pass (Sec. 2, Eq. (6)), independently: q
+    [B,Hq,M,d] rows at positions N-M .. N-1, k/v [B,Hkv,N,d] bf16 patterns.
+    The greedy knapsack is checked on every tile against the exact optimum
+    (largest number of 8-bit logits whose exact cost sum fits the limit)."""
+    from fractions import Fraction
+    B, Hq, Mr, d = q.shape
+    Hkv, N = k.shape[1], k.shape[2]
+    G = Hq // Hkv
+    ntiles = -(-N // tk)
+    o = np.zeros((B, Hq, Mr, d))
+    lse = np.zeros((B, Hq, Mr))
+    mask = np.full((B, Hq, Mr, ntiles * tk), 3, dtype=np.uint8)
+    pure8, all16 = math.isinf(tau), tau == 0.0
+    for b in range(B):
+        for h in range(Hq):
+            kf_all = M.bf16_to_float(k[b, h // G])
+            vf_all = M.bf16_to_float(v[b, h // G])
+            for r in range(Mr):
+                P = N - Mr + r
+                qt = (M.bf16_to_float(q[b, h, r]) * np.float64(scale)).astype(np.float32).astype(np.float64)
+                mu, om = -np.inf, 0.0
+                O = np.zeros(d)
+                for t in range(ntiles):
+                    ii = t * tk + np.arange(tk)
+                    vis = ii < N
+                    if causal:
+                        vis &= ii <= P
+                    if window > 0:
+                        vis &= ii > P - window
+                    if not vis.any():
+                        continue
+                    kf = kf_all[np.minimum(ii, N - 1)]
+                    prec = np.where(vis, 0, 3)
+                    Y16 = y16_tile(qt[None, :], kf)[:, 0]
+                    if all16:
+                        Y = Y16.copy()
+                        prec[vis] = 1
+                        muh = max(mu, Y[vis].max())
+                    else:
+                        Y = y8_tile(qt[None, :], kf)[:, 0]
+                        yv = np.where(vis, Y, -np.inf)
+                        c = int(np.argmax(yv))            # first index of the maximum
+                        if pure8:
+                            muh = max(mu, Y[c])
+                        elif mu > Y[c] + abs(mu) * delta:
+                            muh = mu
+                        else:
+                            Y[c] = Y16[c]
+                            prec[c] = 1
+                            muh = max(mu, Y[c])
+                    E = np.zeros(tk)
+                    for i in np.nonzero(vis)[0]:
+                        E[i] = _shift_exp(np.array([muh]), np.array([[Y[i]]]), prec[i] == 1, tabs)[0, 0]
+                    lam = 0.0 if mu == -np.inf else math.exp(mu - muh)
+                    omh = lam * om + _colsum(E[:, None])[0]
+                    if not pure8 and not all16:
+                        F = [i for i in range(tk) if prec[i] == 0]
+                        kap = {i: E[i] * (omh - E[i]) for i in F}
+                        order = sorted(F, key=lambda i: (kap[i], i))
+                        lim = (tau * omh) * omh
+                        xi, nkeep = 0.0, 0
+                        for i in order:
+                            if not (xi + kap[i] <= lim):
+                                break
+                            xi += kap[i]
+                            nkeep += 1
+                        # exact optimum of the uniform-value knapsack
+                        exact = sorted(Fraction(kap[i]) for i in F)
+                        acc, best = Fraction(0), 0
+                        for x in exact:
+                            if acc + x > Fraction(lim):
+                                break
+                            acc += x
+                            best += 1
+                        assert nkeep == best, (b, h, r, t, nkeep, best)
+                        for i in order[nkeep:]:
+                            prec[i] = 2
+                            Y[i] = Y16[i]
+                            E[i] = _shift_exp(np.array([muh]), np.array([[Y[i]]]), True, tabs)[0, 0]
+                    om = lam * om + _colsum(E[:, None])[0]
+                    O = O * lam + E @ vf_all[np.minimum(ii, N - 1)]
+                    mu = muh
+                    mask[b, h, r, t * tk:(t + 1) * tk] = prec
+                o[b, h, r] = O / om
+                lse[b, h, r] = mu + math.log(om)
+    return o, lse, mask
