@@ -144,12 +144,112 @@ def cpu_baseline(w, tau, q, k, v, budget_s=15.0, seed=0, flags=0):
     }
 
 
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, public figure
+
+
+def cpu_baseline_decode(w, tau, q, k, v, budget_s=15.0, seed=0):
+    """The CPU oracle of the decode form on a bounded, stated sample of query rows."""
+    from oracle import oracle as O
+    rng = np.random.default_rng(seed)
+    nrows = w.B * w.Hq * w.M
+    qbits, kbits, vbits = O.bf16_bits(q), O.bf16_bits(k), O.bf16_bits(v)
+    threads = O.max_threads()
+    order = rng.permutation(nrows)
+    picked, spent = [], 0.0
+    first = True
+    while spent < budget_s and len(picked) < nrows:
+        n = 1 if first else max(1, min(4 * threads, int((budget_s - spent) / max(spent / len(picked), 1e-3))))
+        batch = [int(x) for x in order[len(picked):len(picked) + n]]
+        t0 = time.perf_counter()
+        O.decode(qbits, kbits, vbits, w.causal, w.window, w.bk, w.delta, tau, rows=batch, nthreads=threads)
+        spent += time.perf_counter() - t0
+        picked += batch
+        first = False
+    flops = w.eff_flops * len(picked) / nrows
+    return {"value": flops / spent / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": "%d of %d query rows (seeded random), %.1f s, effective FLOP of the sampled rows" % (
+                len(picked), nrows, spent)}
+
+
+def main_decode(args, w, tau):
+    """Bench line of the decode form (vector LAMP, Sec. 2, Eq. (6))."""
+    import torch
+    from paper_2609_39361_amd import lamp, workloads as W
+    if args.flags:
+        raise SystemExit("the decode form takes no flags")
+    dev = torch.device("cuda:0")
+    q, k, v = W.make_inputs(w)
+    qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
+    tk = w.bk
+    o = torch.empty((w.B, w.Hq, w.M, w.d), dtype=torch.float32, device=dev)
+    lse = torch.empty((w.B, w.Hq, w.M), dtype=torch.float32, device=dev)
+    mask = torch.empty((w.B, w.Hq, w.M, -(-w.N // tk) * tk), dtype=torch.uint8, device=dev)
+
+    def step():
+        lamp.attn_decode(qd, kd, vd, w.causal, w.window, tk, w.delta, tau, out=(o, lse, mask))
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    lamp.timing_read()
+    lamp.timing_enable(True)
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        starts[i].record()
+        step()
+        ends[i].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    lamp.timing_enable(False)
+    launches, kern_ms_sum, pre_ms_sum = lamp.timing_read()
+    kernel_ms = kern_ms_sum / launches
+    ms = float(np.mean([s_.elapsed_time(e_) for s_, e_ in zip(starts, ends)]))
+    m = mask.cpu().numpy()
+    vis = int((m != 3).sum())
+    s1, s2 = int((m == 1).sum()), int((m == 2).sum())
+    # algorithmic HBM bytes: the cache (K and V of every key/value head), the
+    # queries, and the outputs (O, lse, one mask byte per key and row)
+    nbytes = (2 * w.B * w.Hkv * w.N * w.d * 2 + w.B * w.Hq * w.M * w.d * 2
+              + w.B * w.Hq * w.M * (w.d * 4 + 4) + m.size)
+    achieved = nbytes / (kernel_ms * 1e-3) / 1e9
+    mac8 = 0 if tau == 0 else w.macs
+    mac16 = (s1 + s2) * w.d
+    result = {
+        "metric": "effective attention TFLOP/s (4*d per visible (query, key) pair), decode form, 1 GPU",
+        "value": w.eff_flops / (ms * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "e4m3/e4m11 emulated (fp32 FMA + fp8 conversions), bf16 cache, fp32 output",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "M": w.M, "N": w.N, "d": w.d,
+                   "causal": w.causal, "window": w.window, "tk": tk, "delta": w.delta, "tau": tau},
+        "tokens_per_s": w.B * w.M / (ms * 1e-3),
+        "recompute_fraction": (s1 + s2) / vis,
+        "lookahead_recomputes": s1, "knapsack_recomputes": s2,
+        "roofline": {
+            "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+            "kernel": "dec_logits8_kernel<%d> + dec_lamp_kernel<%d,%d>" % (w.d, w.d, _mode_of(tau)),
+            "kernel_ms": kernel_ms, "prepass_ms": pre_ms_sum / launches,
+            "bytes_per_launch": nbytes,
+            "valu_frac_algorithmic": (OPS_PER_MAC8 * mac8 + OPS_PER_MAC16 * mac16) / (kernel_ms * 1e-3) / VALU_LANE_OPS,
+        },
+        "wall_s_timed_region": wall,
+    }
+    if not args.no_cpu:
+        result["cpu_baseline"] = cpu_baseline_decode(w, tau, q, k, v, budget_s=args.cpu_budget)
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", type=int, default=3, help="config id (1, 2, 3, 4, 40, 5)")
+    ap.add_argument("--workload", type=int, default=3, help="config id (1, 2, 3, 4, 40, 5; 6 decode form)")
     ap.add_argument("--tau", type=float, default=None)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
@@ -169,6 +269,8 @@ def main():
 
     w = W.CONFIGS[args.workload]
     tau = w.tau if args.tau is None else args.tau
+    if w.M > 0:
+        return main_decode(args, w, tau)
     dev = torch.device("cuda:0")
     q, k, v = W.make_inputs(w)
     qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)

@@ -116,6 +116,36 @@ enum {
 };
 
 /*
+ * lamp_attn_decode -- LampAttention for query rows against a key/value cache
+ * in the vector form of the look-ahead (Sec. 2: the two-step procedure and the
+ * greedy knapsack of Eq. (6)), e.g. one new token per sequence (decode).
+ *
+ * q [B][Hq][M][d]: M query rows per (b, h) at positions N-M .. N-1; k, v
+ * [B][Hkv][N][d]: the cache (bf16, 16-byte aligned).  Each row visits its key
+ * tiles of tk keys in order; in each tile the maximizer c of the 8-bit logits
+ * passes if mu > fma(|mu|, delta, fl(y_c)) (mu_hat = mu), otherwise y_c is
+ * recomputed in 16 bits and mu_hat = max(mu, y16_c); the other 8-bit logits
+ * are sorted by E (omega_hat - E) ascending (ties by key) and kept while the
+ * fp64 running sum stays within (tau omega_hat) omega_hat, the rest being
+ * recomputed in 16 bits against the same mu_hat.  tau = +INFINITY keeps every
+ * logit in 8 bits, tau = 0 recomputes them all.
+ *
+ * Outputs: o [B][Hq][M][d] fp32, lse [B][Hq][M] fp32, mask
+ * [B][Hq][M][ceil(N/tk)*tk] uint8, one code per key (0 8-bit, 1 the maximizer
+ * recomputed by the look-ahead test -- every key at tau = 0 --, 2 recomputed
+ * by the knapsack, 3 invisible).  Built: tk = 64, d in {64, 128, 256};
+ * flags must be 0.  B = 0 or M = 0 returns LAMP_OK and writes nothing.  The
+ * library keeps a grow-only per-device workspace (the pre-scaled queries, the
+ * 8-bit logit codes, the exponentials, per-tile rescale factors and partial
+ * outputs: about B*Hq*M*(5*ceil(N/64)*64 + 4d*(1 + ceil(N/512))) bytes);
+ * calls that overlap on one device race on it.
+ */
+int lamp_attn_decode(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                     int B, int Hq, int Hkv, int M, int N, int d,
+                     int causal, int window, int tk, double delta, double tau, unsigned flags,
+                     float *o, float *lse, uint8_t *mask, void *stream);
+
+/*
  * lamp_attn_logits8 -- the 8-bit logits alone (Alg. 1, first accumulation;
  * Sec. 4.1 recursive FMA summation rounded to e4m3 after every step).
  * Writes the e4m3 codes of rows [row0, row0 + nrows) of every (b, h):

@@ -28,7 +28,7 @@ LIB = os.path.join(HERE, "liblamp.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["lamp_kernels.hip", "lamp_fwd.hip", "lamp_fwd16.hip", "lamp_host.cpp"]
+SOURCES = ["lamp_kernels.hip", "lamp_fwd.hip", "lamp_fwd16.hip", "lamp_decode.hip", "lamp_host.cpp"]
 
 DPP_VGPR_WAITS = 2
 DPP_EXEC_WAITS = 5
@@ -162,7 +162,7 @@ def build(verbose=False, extra=()):
             print(out)
         asm_files = sorted(glob.glob(os.path.join(work, "*-hip-amdgcn-amd-amdhsa-" + ARCH + ".s")))
         names = {os.path.basename(f).split("-hip-")[0] for f in asm_files}
-        if not {"lamp_fwd", "lamp_fwd16", "lamp_kernels"} <= names:
+        if not {"lamp_fwd", "lamp_fwd16", "lamp_decode", "lamp_kernels"} <= names:
             os.remove(tmp)
             raise RuntimeError("device assembly of the kernel sources missing: %r" % asm_files)
         bad = []

@@ -41,6 +41,8 @@ struct DeviceState {
     uint32_t *sim16 = nullptr;
     void *ws = nullptr;
     size_t ws_bytes = 0;
+    void *dws = nullptr;         // decode workspace: pre-scaled queries, 8-bit logit codes
+    size_t dws_bytes = 0;
 };
 
 std::mutex g_mu;
@@ -141,9 +143,13 @@ int workspace_locked(int dev, int B, int Hq, int Hkv, int Nq, int Nk, int d, Wor
     return LAMP_OK;
 }
 
-int check_common(const void *q, const void *k, int B, int Hq, int Hkv, int N, int d, int causal, int window)
+// rows: query rows per (b, h) to compute (N for the prefill form; M for the
+// decode form, whose query pointer may be null when M = 0).
+int check_common(const void *q, const void *k, int B, int Hq, int Hkv, int N, int d, int causal, int window,
+                 int rows = -1)
 {
-    if ((B > 0 && N > 0) && (!q || !k)) return fail(LAMP_ERR_INVALID_ARG, "null input pointer");
+    if (rows < 0) rows = N;
+    if ((B > 0 && N > 0 && rows > 0) && (!q || !k)) return fail(LAMP_ERR_INVALID_ARG, "null input pointer");
     if (B < 0 || Hq <= 0 || Hkv <= 0 || N < 0 || d <= 0)
         return fail(LAMP_ERR_INVALID_ARG, "invalid sizes (B=%d Hq=%d Hkv=%d N=%d d=%d)", B, Hq, Hkv, N, d);
     if (Hq % Hkv) return fail(LAMP_ERR_INVALID_ARG, "Hq=%d is not a multiple of Hkv=%d", Hq, Hkv);
@@ -192,7 +198,7 @@ void lamp_shutdown(void)
     if (hipGetDevice(&prev) != hipSuccess) return;
     for (size_t i = 0; i < g_dev.size(); ++i) {
         DeviceState &st = g_dev[i];
-        if (!st.ready && !st.ws) continue;
+        if (!st.ready && !st.ws && !st.dws) continue;
         if (hipSetDevice((int)i) != hipSuccess) continue;
         (void)hipDeviceSynchronize();
         (void)hipFree(st.lut8);
@@ -202,6 +208,7 @@ void lamp_shutdown(void)
         (void)hipFree(st.sim8);
         (void)hipFree(st.sim16);
         (void)hipFree(st.ws);
+        (void)hipFree(st.dws);
         st = DeviceState();
     }
     (void)hipSetDevice(prev);
@@ -282,6 +289,93 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
     HIP_TRY(lamp::dispatch_fwd(d, bq, bk, nk, p, s, &found));
     if (!found)
         return fail(LAMP_ERR_UNSUPPORTED, "block sizes (bq=%d, bk=%d, nk=%d) not built for d=%d", bq, bk, nk, d);
+    if (timed) {
+        HIP_TRY(hipEventRecord(tc.e[2], s));
+        std::lock_guard<std::mutex> lk(g_tmu);
+        g_timed.push_back(tc);
+    }
+    return LAMP_OK;
+}
+
+int lamp_attn_decode(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B, int Hq, int Hkv, int M, int N,
+                     int d, int causal, int window, int tk, double delta, double tau, unsigned flags, float *o,
+                     float *lse, uint8_t *mask, void *stream)
+{
+    if (M < 0 || M > N) return fail(LAMP_ERR_INVALID_ARG, "M=%d query rows must lie in [0, N=%d]", M, N);
+    int rc = check_common(q, k, B, Hq, Hkv, N, d, causal, window, M);
+    if (rc) return rc;
+    if ((B > 0 && M > 0) && (!q || !k || !v || !o || !lse || !mask))
+        return fail(LAMP_ERR_INVALID_ARG, "null pointer among q, k, v, o, lse, mask");
+    if (!(delta >= 0.0) || std::isinf(delta)) return fail(LAMP_ERR_INVALID_ARG, "delta must be finite and >= 0");
+    if (!(tau >= 0.0)) return fail(LAMP_ERR_INVALID_ARG, "tau must be >= 0 (or +inf)");
+    if (flags) return fail(LAMP_ERR_INVALID_ARG, "unknown flags 0x%x (the decode form takes none)", flags);
+    if (tk != 64) return fail(LAMP_ERR_UNSUPPORTED, "keys per update tk=%d not built (64)", tk);
+    if (B == 0 || M == 0) return LAMP_OK;   // nothing to compute
+    const int Np = (N + 63) / 64 * 64, nch = (N + 511) / 512;   // key chunks of the P.V pass
+    const size_t nrows = (size_t)B * Hq * M;
+    const size_t bq = align256(nrows * d * 4), by8 = align256(nrows * Np);
+    const size_t be = align256(nrows * Np * 4), bf = align256(nrows * (Np / 64) * 8);
+    const size_t bpart = align256(nrows * nch * d * 4), need = bq + by8 + be + bf + bpart;
+    int dev = 0;
+    rc = current_device(&dev);
+    if (rc) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    lamp::DecParams p{};
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        rc = init_locked(dev);
+        if (rc) return rc;
+        DeviceState *st = state_of(dev);
+        if (need > st->dws_bytes) {
+            if (st->dws) {
+                HIP_TRY(hipDeviceSynchronize());
+                HIP_TRY(hipFree(st->dws));
+                st->dws = nullptr;
+                st->dws_bytes = 0;
+            }
+            HIP_TRY(hipMalloc(&st->dws, need));
+            st->dws_bytes = need;
+        }
+        char *base = static_cast<char *>(st->dws);
+        p.qt = reinterpret_cast<float *>(base);
+        p.y8 = reinterpret_cast<uint8_t *>(base + bq);
+        p.e = reinterpret_cast<float *>(base + bq + by8);
+        p.f = reinterpret_cast<double *>(base + bq + by8 + be);
+        p.part = reinterpret_cast<float *>(base + bq + by8 + be + bf);
+        p.lut8e = st->lut8e;
+        p.exp16hl = st->exp16hl;
+    }
+    p.k = k;
+    p.v = v;
+    p.o = o;
+    p.lse = lse;
+    p.mask = mask;
+    p.B = B;
+    p.Hq = Hq;
+    p.Hkv = Hkv;
+    p.M = M;
+    p.N = N;
+    p.Np = Np;
+    const int first = window > 0 ? N - M - window + 1 : 0;
+    p.kb0 = first > 0 ? first / 64 * 64 : 0;
+    p.causal = causal;
+    p.window = window;
+    p.delta = delta;
+    p.tau = tau;
+    p.mode = std::isinf(tau) ? lamp::MODE_PURE8 : (tau == 0.0 ? lamp::MODE_ALL16 : lamp::MODE_LAMP);
+    bool timed = false;
+    TimedCall tc{};
+    {
+        std::lock_guard<std::mutex> lk(g_tmu);
+        timed = g_timing;
+    }
+    if (timed) {
+        for (int i = 0; i < 3; ++i) HIP_TRY(hipEventCreate(&tc.e[i]));
+        HIP_TRY(hipEventRecord(tc.e[0], s));
+    }
+    HIP_TRY(lamp::launch_prescale_q(q, const_cast<float *>(p.qt), B * Hq, M, d, scale_of(d), s));
+    if (timed) HIP_TRY(hipEventRecord(tc.e[1], s));
+    HIP_TRY(lamp::launch_decode(d, p, s));
     if (timed) {
         HIP_TRY(hipEventRecord(tc.e[2], s));
         std::lock_guard<std::mutex> lk(g_tmu);

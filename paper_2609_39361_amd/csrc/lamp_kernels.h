@@ -42,6 +42,28 @@ struct LogitsParams {
     int B, Hq, Hkv, N, causal, window, row0, nrows;
 };
 
+// Decode form (vector LAMP, Sec. 2): M query rows per (b, h) at positions
+// N-M .. N-1 against a bf16 key/value cache of N keys.
+struct DecParams {
+    const float *qt;          // [B][Hq][M][D] pre-scaled queries
+    const uint16_t *k, *v;    // [B][Hkv][N][D] bf16 cache
+    uint8_t *y8;              // [B][Hq][M][Np] 8-bit logit codes (workspace)
+    float *e;                 // [B][Hkv][Np][G*M] exponentials of the visited tiles (workspace)
+    double *f;                // [B][Hkv][Np/64][G*M] lambda_hat per tile, then the P.V factor (workspace)
+    float *part;              // [B][Hq][M][ceil(N/512)][D] partial outputs of the key chunks (workspace)
+    const uint16_t *lut8e;    // ue5m3 shift code -> bf16 bits of the ue5m3 exp
+    const uint32_t *exp16hl;  // ue5m11 shift code -> bf16 high | low << 16 of the ue5m11 exp
+    float *o, *lse;           // [B][Hq][M][D], [B][Hq][M]
+    uint8_t *mask;            // [B][Hq][M][Np] one code per key
+    int B, Hq, Hkv, M, N;
+    int Np;                   // keys rounded up to whole tiles of 64
+    int kb0;                  // first key any row can see (a multiple of 64)
+    int causal, window, mode;
+    double delta, tau;
+};
+
+hipError_t launch_decode(int D, const DecParams &p, hipStream_t s);
+hipError_t launch_prescale_q(const uint16_t *q, float *qt, int BH, int rows, int D, float scale, hipStream_t s);
 bool fwd_supported(int D, int BQ, int BK, int NK);
 hipError_t dispatch_fwd16(int D, int BQ, const FwdParams &p, hipStream_t s, bool *found);
 hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found);

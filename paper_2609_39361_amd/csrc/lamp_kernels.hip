@@ -289,6 +289,14 @@ hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float
     return hipGetLastError();
 }
 
+hipError_t launch_prescale_q(const uint16_t *q, float *qt, int BH, int rows, int D, float scale, hipStream_t s)
+{
+    size_t n = (size_t)BH * rows * D;
+    unsigned g = (unsigned)((n + 255) / 256 < 65536 ? (n + 255) / 256 : 65536);
+    hipLaunchKernelGGL(prescale_q_kernel, dim3(g), dim3(256), 0, s, q, qt, scale, rows, rows, D, n);
+    return hipGetLastError();
+}
+
 hipError_t launch_transpose_v(const uint16_t *v, uint16_t *vt, int B, int Hkv, int N, int Nk, int D, hipStream_t s)
 {
     hipLaunchKernelGGL(transpose_v_kernel, dim3((unsigned)(Nk / 64), (unsigned)(D / 64), (unsigned)(B * Hkv)),

@@ -41,6 +41,8 @@ def lib():
         L.lamp_attn_logits8.restype = i32
         L.lamp_attn_logits16.argtypes = [P, P] + [i32] * 9 + [P, P]
         L.lamp_attn_logits16.restype = i32
+        L.lamp_attn_decode.argtypes = [P, P, P] + [i32] * 9 + [f64, f64, ctypes.c_uint, P, P, P, P]
+        L.lamp_attn_decode.restype = i32
         L.lamp_attn_logits_sim.argtypes = [P, P] + [i32] * 10 + [P, P]
         L.lamp_attn_logits_sim.restype = i32
         L.lamp_get_sim_tables.argtypes = [i32, P, P]
@@ -120,6 +122,33 @@ def attn_fwd(q, k, v, causal=True, window=0, bq=128, bk=16, nk=4, delta=2.0 ** -
         rc = lib().lamp_attn_fwd(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(causal), int(window),
                                  bq, bk, nk, float(delta), float(tau), int(flags), _ptr(o), _ptr(lse), _ptr(mask),
                                  _stream(dev))
+    _check(rc)
+    return o, lse, mask
+
+
+def attn_decode(q, k, v, causal=True, window=0, tk=64, delta=2.0 ** -8, tau=0.5, out=None, flags=0):
+    """LampAttention in the vector form (Sec. 2, Eq. (6)) for M query rows per
+    (b, h) at positions N-M .. N-1: q [B,Hq,M,d], k / v [B,Hkv,N,d] bf16.
+    Returns (o fp32 [B,Hq,M,d], lse fp32 [B,Hq,M], mask uint8
+    [B,Hq,M,ceil(N/tk)*tk] one code per key)."""
+    if q.dim() != 4 or k.dim() != 4 or v.shape != k.shape:
+        raise ValueError("q [B,Hq,M,d], k and v [B,Hkv,N,d] expected")
+    B, Hq, M, d = q.shape
+    Hkv, N = k.shape[1], k.shape[2]
+    for t in (q, k, v):
+        if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError("q, k, v must be contiguous bf16 CUDA tensors")
+    dev = q.device
+    if out is None:
+        o = torch.empty((B, Hq, M, d), dtype=torch.float32, device=dev)
+        lse = torch.empty((B, Hq, M), dtype=torch.float32, device=dev)
+        mask = torch.empty((B, Hq, M, -(-N // tk) * tk), dtype=torch.uint8, device=dev)
+    else:
+        o, lse, mask = out
+    with torch.cuda.device(dev):
+        rc = lib().lamp_attn_decode(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, M, N, d, int(causal), int(window), tk,
+                                    float(delta), float(tau), int(flags), _ptr(o), _ptr(lse), _ptr(mask),
+                                    _stream(dev))
     _check(rc)
     return o, lse, mask
 

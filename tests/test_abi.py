@@ -88,6 +88,24 @@ def test_binding_rejects_bad_arguments_without_gpu():
     assert rc == 2
 
 
+def test_decode_rejects_bad_arguments_without_gpu():
+    if not os.path.exists(LIB):
+        pytest.skip("liblamp.so not built")
+    lib = ctypes.CDLL(LIB)
+    P = ctypes.c_void_p
+    lib.lamp_attn_decode.restype = ctypes.c_int
+    lib.lamp_attn_decode.argtypes = [P, P, P] + [ctypes.c_int] * 9 + [ctypes.c_double] * 2 + [ctypes.c_uint] + [P] * 4
+    lib.lamp_last_error.restype = ctypes.c_char_p
+    d = P(16)
+    # (B, Hq, Hkv, M, N, d, causal, window, tk)
+    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 128, 1, 0, 32, 2 ** -8, 0.5, 0, d, d, d, None) == 2
+    assert b"tk" in lib.lamp_last_error()
+    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 128, 1, 0, 64, 2 ** -8, 0.5, 4, d, d, d, None) == 1
+    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 300, 256, 128, 1, 0, 64, 2 ** -8, 0.5, 0, d, d, d, None) == 1
+    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 96, 1, 0, 64, 2 ** -8, 0.5, 0, d, d, d, None) == 2
+    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 128, 1, 0, 64, 2 ** -8, -1.0, 0, d, d, d, None) == 1
+
+
 def test_timing_read_without_calls():
     """Timing bookkeeping is host-only: nothing recorded reads as zero."""
     if not os.path.exists(LIB):
