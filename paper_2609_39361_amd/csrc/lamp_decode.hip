@@ -18,7 +18,7 @@
 //   dec_logits8_kernel  the 8-bit logits of every (query row, key), which
 //                       depend on no decision: one thread per key, the 4 query
 //                       rows of a group accumulated together, queries read
-//                       through scalar loads, keys staged through LDS from
+//                       from LDS (broadcast), keys staged through LDS from
 //                       coalesced loads of the bf16 cache (no fp32 copy);
 //   dec_lamp_kernel     the decisions, one wave per query row: lane i holds
 //                       key i of the tile; DPP reductions, a bitonic sort of
@@ -153,8 +153,8 @@ __device__ __forceinline__ uint64_t wave_or_u64(uint64_t v)
 constexpr int P1_CH = 64, P1_PITCH = P1_CH + 8;
 
 template <int D, bool SAT>
-__device__ __forceinline__ void dec8_staged(const uint16_t *kblk, int nvalid, uint16_t *tile, kptr32_t q0, kptr32_t q1,
-                                            kptr32_t q2, kptr32_t q3, uint32_t (&acc)[2])
+__device__ __forceinline__ void dec8_staged(const uint16_t *kblk, int nvalid, uint16_t *tile, const float *qs,
+                                            uint32_t (&acc)[2])
 {
     const int tid = threadIdx.x;
     acc[0] = acc[1] = 0u;
@@ -171,16 +171,24 @@ __device__ __forceinline__ void dec8_staged(const uint16_t *kblk, int nvalid, ui
         for (int c = 0; c < P1_CH; c += 8) {
             float kf[8];
             unpack8(*reinterpret_cast<const uint4 *>(tile + tid * P1_PITCH + c), kf);
+            // the 4 rows' queries for these 8 channels: broadcast LDS reads
+            float qv[4][8];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float4 a = *reinterpret_cast<const float4 *>(qs + i * D + c0 + c);
+                const float4 b = *reinterpret_cast<const float4 *>(qs + i * D + c0 + c + 4);
+                qv[i][0] = a.x; qv[i][1] = a.y; qv[i][2] = a.z; qv[i][3] = a.w;
+                qv[i][4] = b.x; qv[i][5] = b.y; qv[i][6] = b.z; qv[i][7] = b.w;
+            }
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
-                const int ch = c0 + c + j;
                 const float2 a = unpk_e4m3(acc[0]);
-                const float x = __builtin_fmaf(q0[ch], kf[j], a.x);
-                const float y = __builtin_fmaf(q1[ch], kf[j], a.y);
+                const float x = __builtin_fmaf(qv[0][j], kf[j], a.x);
+                const float y = __builtin_fmaf(qv[1][j], kf[j], a.y);
                 acc[0] = SAT ? pk_e4m3_sat(x, y, acc[0]) : pk_e4m3(x, y, acc[0]);
                 const float2 bb = unpk_e4m3(acc[1]);
-                const float z = __builtin_fmaf(q2[ch], kf[j], bb.x);
-                const float u = __builtin_fmaf(q3[ch], kf[j], bb.y);
+                const float z = __builtin_fmaf(qv[2][j], kf[j], bb.x);
+                const float u = __builtin_fmaf(qv[3][j], kf[j], bb.y);
                 acc[1] = SAT ? pk_e4m3_sat(z, u, acc[1]) : pk_e4m3(z, u, acc[1]);
             }
         }
@@ -192,6 +200,7 @@ template <int D>
 __global__ __launch_bounds__(256) void dec_logits8_kernel(DecParams p)
 {
     __shared__ __align__(16) uint16_t tile[256 * P1_PITCH];
+    __shared__ __align__(16) float qs[4 * D];   // the group's 4 pre-scaled query rows
     const int G = p.Hq / p.Hkv;
     const int rows = G * p.M, ngroups = (rows + 3) / 4;
     const int grp = (int)(blockIdx.y % (unsigned)ngroups);
@@ -209,14 +218,14 @@ __global__ __launch_bounds__(256) void dec_logits8_kernel(DecParams p)
         const int h = hk * G + rho / p.M, r = rho % p.M;
         qrow[i] = ((size_t)b * p.Hq + h) * p.M + r;
     }
-    const kptr32_t q0 = (kptr32_t)(p.qt + qrow[0] * D), q1 = (kptr32_t)(p.qt + qrow[1] * D);
-    const kptr32_t q2 = (kptr32_t)(p.qt + qrow[2] * D), q3 = (kptr32_t)(p.qt + qrow[3] * D);
+    for (int x = (int)threadIdx.x; x < 4 * D; x += 256) qs[x] = p.qt[qrow[x / D] * D + x % D];
+    __syncthreads();
     uint32_t acc[2];
-    dec8_staged<D, false>(kblk, nvalid, tile, q0, q1, q2, q3, acc);
+    dec8_staged<D, false>(kblk, nvalid, tile, qs, acc);
     // an overflow somewhere gives a NaN code at the end of its chain: the
     // workgroup re-runs its chains with the saturating conversion
     if (__syncthreads_or((e4m3_nan_bits(acc[0]) | e4m3_nan_bits(acc[1])) != 0u))
-        dec8_staged<D, true>(kblk, nvalid, tile, q0, q1, q2, q3, acc);
+        dec8_staged<D, true>(kblk, nvalid, tile, qs, acc);
     if (key >= p.N) return;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -236,6 +245,7 @@ __global__ __launch_bounds__(256) void dec_lamp_kernel(DecParams p)
 {
     __shared__ uint16_t lut[256];
     __shared__ double edk[EXPDOC_NK];
+    __shared__ __align__(16) uint8_t cbuf[4][16 * TK];   // per wave: the codes of 16 tiles
     const int tid = threadIdx.x, lane = tid & 63;
     for (int i = tid; i < 256; i += 256) lut[i] = p.lut8e[i];
     if (tid < EXPDOC_NK) edk[tid] = EXPDOC_K[tid];
@@ -269,22 +279,27 @@ __global__ __launch_bounds__(256) void dec_lamp_kernel(DecParams p)
         if (t < t_begin || t > t_end)
             for (int i = 0; i < TK; ++i) mrow[t * TK + i] = 3;
 
-    // the 8-bit logit codes are loaded PF tiles ahead (a ring of registers)
-    constexpr int PF = 4;
-    uint8_t ring[PF];
-    auto code_at = [&](int tt) -> uint8_t {
-        const int kk = tt * TK + lane;
-        return (MODE != MODE_ALL16 && tt <= t_end && kk >= vlo && kk <= vhi) ? y8row[kk] : (uint8_t)0;
+    // The 8-bit logit codes arrive 16 tiles at a time: one 16-byte load per
+    // lane (keys 16 lane .. 16 lane + 15 of the block), held in registers one
+    // block ahead and passed through this wave's LDS buffer, so no global load
+    // is waited for inside the tile loop (on gfx950 a wait for a load also
+    // waits for every earlier store of the wave).
+    uint8_t *cb = cbuf[tid >> 6];
+    auto load_block = [&](int tb) -> uint4 {
+        const int k = tb * TK + 16 * lane;
+        return (MODE != MODE_ALL16 && tb <= t_end && k + 16 <= p.Np) ? *reinterpret_cast<const uint4 *>(y8row + k)
+                                                                      : make_uint4(0u, 0u, 0u, 0u);
     };
-#pragma unroll
-    for (int i = 0; i < PF; ++i) ring[i] = code_at(t_begin + i);
+    uint4 nxt = load_block(t_begin);
     for (int t = t_begin; t <= t_end; ++t) {
         const int key = t * TK + lane;
         const bool vis = key >= vlo && key <= vhi;   // vhi < N
-        const uint8_t code = ring[0];
-#pragma unroll
-        for (int i = 0; i + 1 < PF; ++i) ring[i] = ring[i + 1];
-        ring[PF - 1] = code_at(t + PF);
+        const int tb = (t - t_begin) & 15;
+        if (MODE != MODE_ALL16 && tb == 0) {
+            *reinterpret_cast<uint4 *>(cb + 16 * lane) = nxt;   // LDS operations of a wave stay in order
+            nxt = load_block(t + 16);
+        }
+        const uint8_t code = MODE != MODE_ALL16 ? cb[tb * TK + lane] : (uint8_t)0;
         const int keyc = key < p.N ? key : p.N - 1;
         const uint16_t *krow = kbase + (size_t)keyc * D;
         float y = NEG_INF;   // this key's logit in the precision chosen for it
