@@ -85,11 +85,12 @@ __device__ __forceinline__ float rn_e4m11(double y, uint32_t *code)
     return sign ? -v : v;
 }
 
+// Value of an e4m11 code, exact in fp32, without branches: the significand
+// (with its implicit bit for a normal code) scaled by 2^(max(ex, 1) - 18).
 __device__ __forceinline__ float e4m11_value(uint32_t code)
 {
-    uint32_t ex = (code >> 11) & 0xFu, m = code & 0x7FFu;
-    float v = ex ? __builtin_bit_cast(float, ((ex + 120u) << 23) | (m << 12))
-                 : (float)m * 0x1p-17f;
+    const uint32_t ex = (code >> 11) & 0xFu, m = code & 0x7FFu;
+    const float v = __builtin_amdgcn_ldexpf((float)(ex ? m | 0x800u : m), (int)(ex ? ex : 1u) - 18);
     return (code & 0x8000u) ? -v : v;
 }
 

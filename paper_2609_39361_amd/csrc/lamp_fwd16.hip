@@ -253,8 +253,11 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                     const float2 yv = SIMP ? make_float2(bf16_value(a8[s][pp] & 0xFFFFu), bf16_value(a8[s][pp] >> 16))
                                            : unpk_e4m3(a8[s][pp]);
                     const int i0 = ck0 + 2 * pp;
-                    if (full || visible(s, i0)) mx = yv.x > mx ? yv.x : mx;
-                    if (full || visible(s, i0 + 1)) mx = yv.y > mx ? yv.y : mx;
+                    // invisible keys enter as -inf, by selection rather than branches
+                    const float x0 = (full || visible(s, i0)) ? yv.x : NEG_INF;
+                    const float x1 = (full || visible(s, i0 + 1)) ? yv.y : NEG_INF;
+                    mx = x0 > mx ? x0 : mx;
+                    mx = x1 > mx ? x1 : mx;
                     packed[pp] = SIMP ? a8[s][pp] : (a8[s][pp] & 0xFFu) | ((a8[s][pp] & 0xFF00u) << 8);
                 }
                 u32x4 *dst = reinterpret_cast<u32x4 *>(yc + row[s] * YP + w * BK);
@@ -565,6 +568,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
             }
         }
 
+
         // ---- D. exponentials of tile t against mu_hat
         {
             // the 16-bit maxima buffer of tile t+1 was last read in tile t-1
@@ -588,8 +592,56 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                     d[0] = u32x4{0u, 0u, 0u, 0u};
                     d[1] = u32x4{0u, 0u, 0u, 0u};
                 }
-            } else if (!((prec16 & F0) >> th & 1u)) {   // else from registers by every wave, below
-                const bool hi16 = prec16 >> th & 1u;      // one-at-a-time 16-bit codes in place
+            } else if (!(prec16 >> th & 1u)) {
+                // 8-bit sub-block, straight-line: all codes read, all table
+                // indices formed and all table reads issued before the first is
+                // used; invisible keys get E = 0 by selection.  The row sums are
+                // exact in fp64 in any order (multiples of 2^-41 below 2^7), so
+                // they run as four independent chains.
+                bool full = true;
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) full &= ck0 >= vlo[s] && ck0 + 15 <= vhi[s];
+                auto run8 = [&](auto full_c) {
+                    constexpr bool FULL = decltype(full_c)::value;
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) {
+                        u32x4 *rp = reinterpret_cast<u32x4 *>(ycode + row[s] * YP + th * BK);
+                        const u32x4 c0 = rp[0], c1 = rp[1];
+                        const uint32_t in[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
+                        uint32_t eb[16];
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            uint32_t x;
+                            if constexpr (SIMP) {
+                                x = sim_shift_index<3, SIM8_EMIN, SIM8_EMAX>(mu8[s], bf16_value((in[i >> 1] >> (16 * (i & 1))) & 0xFFFFu));
+                            } else {
+                                // the e4m3 code sits in the low byte of its 16-bit slot
+                                const float y = (i & 1) ? __builtin_amdgcn_cvt_f32_fp8((int)in[i >> 1], 2)
+                                                        : __builtin_amdgcn_cvt_f32_fp8((int)in[i >> 1], 0);
+                                x = ue5m3_code(shift_of(mu8[s], y));
+                            }
+                            // an invisible key reads the table's last entry, whose
+                            // exponential is 0 (the largest shift), so that every
+                            // read is issued unconditionally
+                            if constexpr (!FULL) x = visible(s, ck0 + i) ? x : (SIMP ? SIM8_N - 1 : 255u);
+                            eb[i] = lut[x];
+                        }
+                        double a4[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) a4[i & 3] += (double)bf16_value(eb[i]);
+                        const double ts = (a4[0] + a4[1]) + (a4[2] + a4[3]);
+                        sp[s] += ts;
+                        spF[s] += ts;
+                        rp[0] = u32x4{eb[0] | eb[1] << 16, eb[2] | eb[3] << 16, eb[4] | eb[5] << 16, eb[6] | eb[7] << 16};
+                        rp[1] = u32x4{eb[8] | eb[9] << 16, eb[10] | eb[11] << 16, eb[12] | eb[13] << 16,
+                                      eb[14] | eb[15] << 16};
+                    }
+                };
+                if (!wave_any(!full)) run8(std::true_type());
+                else run8(std::false_type());
+            } else if (!(F0 >> th & 1u)) {
+                // a stage-1 sub-block outside F0: its one-at-a-time 16-bit codes
+                // are in place (the members of F0 are done from registers below)
 #pragma unroll
                 for (int s = 0; s < QPL; ++s) {
                     u32x4 *rp = reinterpret_cast<u32x4 *>(ycode + row[s] * YP + th * BK);
@@ -597,16 +649,14 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                     if (ck0 > vhi[s] || ck0 + 15 < vlo[s]) {
                         rp[0] = u32x4{0u, 0u, 0u, 0u};
                         rp[1] = u32x4{0u, 0u, 0u, 0u};
-                        if (hi16) {
-                            lp[0] = u32x4{0u, 0u, 0u, 0u};
-                            lp[1] = u32x4{0u, 0u, 0u, 0u};
-                        }
+                        lp[0] = u32x4{0u, 0u, 0u, 0u};
+                        lp[1] = u32x4{0u, 0u, 0u, 0u};
                         continue;
                     }
                     const u32x4 c0 = rp[0], c1 = rp[1];
                     const uint32_t in[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
                     uint32_t inl[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};   // SIM: low halves of 16-bit logits
-                    if (SIMP && hi16) {
+                    if (SIMP) {
                         const u32x4 l0 = lp[0], l1 = lp[1];
                         inl[0] = l0[0]; inl[1] = l0[1]; inl[2] = l0[2]; inl[3] = l0[3];
                         inl[4] = l1[0]; inl[5] = l1[1]; inl[6] = l1[2]; inl[7] = l1[3];
@@ -622,17 +672,11 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                             uint32_t eh = 0, el = 0;
                             float ev = 0.0f;
                             if (visible(s, key)) {
-                                if (hi16) {
-                                    const float y = SIMP ? __builtin_bit_cast(float, (yc << 16) | ((inl[pp] >> (16 * t2)) & 0xFFFFu))
-                                                         : e4m11_value(yc);
-                                    ev = e16_of(muh[s], y, eh, el);
-                                } else {
-                                    eh = e8_of(mu8[s], yc);
-                                    ev = bf16_value(eh);
-                                }
+                                const float y = SIMP ? __builtin_bit_cast(float, (yc << 16) | ((inl[pp] >> (16 * t2)) & 0xFFFFu))
+                                                     : e4m11_value(yc);
+                                ev = e16_of(muh[s], y, eh, el);
                             }
-                            sp[s] += (double)ev;   // exact: multiples of 2^-41 below 2^9 (SIM: not used)
-                            if (!hi16) spF[s] += (double)ev;
+                            sp[s] += (double)ev;
                             res |= eh << (16 * t2);
                             rlo |= el << (16 * t2);
                         }
@@ -641,46 +685,67 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                     }
                     rp[0] = u32x4{outw[0], outw[1], outw[2], outw[3]};
                     rp[1] = u32x4{outw[4], outw[5], outw[6], outw[7]};
-                    if (hi16) {
-                        lp[0] = u32x4{outl[0], outl[1], outl[2], outl[3]};
-                        lp[1] = u32x4{outl[4], outl[5], outl[6], outl[7]};
-                    }
+                    lp[0] = u32x4{outl[0], outl[1], outl[2], outl[3]};
+                    lp[1] = u32x4{outl[4], outl[5], outl[6], outl[7]};
                 }
             }
             // 16-bit exponentials of this wave's 4 keys of every stage-1
-            // sub-block of F0, from the codes held in registers
-            {
-                const uint32_t mine = prec16 & F0;
-                uint32_t m = F0;
+            // sub-block of F0, from the codes held in registers: all table reads
+            // of all such members issued first
+            const uint32_t mine = prec16 & F0;
+            if (mine) {
+                int tg[NK];
+                bool use[NK];
+                {
+                    uint32_t m = F0;
+#pragma unroll
+                    for (int g = 0; g < NK; ++g) {
+                        tg[g] = m ? __builtin_ctz(m) : 0;
+                        use[g] = m != 0u && (mine >> tg[g] & 1u);
+                        m &= m - 1;
+                    }
+                }
 #pragma unroll
                 for (int g = 0; g < NK; ++g) {
-                    if (!m) break;
-                    const int tg = __builtin_ctz(m);
-                    m &= m - 1;
-                    if (!(mine >> tg & 1u)) continue;
-                    const int key0 = k0 + tg * BK + w * 4;
+                    if (!use[g]) continue;
+                    // the 8 table reads of this member issued before the first is used
+                    uint32_t hl[QPL][4];
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const float y = y16_value<SIMP>(&y16r[s][g * WPM], i);
+                            if constexpr (SIMP) hl[s][i] = p.sim16[sim_shift_index<11, SIM16_EMIN, SIM16_EMAX>(muh[s], y)];
+                            else hl[s][i] = p.exp16hl[ue5m11_code(shift_of(muh[s], y))];
+                        }
+                    const int key0 = k0 + tg[g] * BK + w * 4;
 #pragma unroll
                     for (int s = 0; s < QPL; ++s) {
-                        uint32_t outw[2], outl[2];
+                        uint32_t eh[4], el[4];
+                        double ev[4];
 #pragma unroll
-                        for (int pp = 0; pp < 2; ++pp) {
-                            uint32_t res = 0, rlo = 0;
-#pragma unroll
-                            for (int t2 = 0; t2 < 2; ++t2) {
-                                const int key = key0 + 2 * pp + t2;
-                                uint32_t eh = 0, el = 0;
-                                float ev = 0.0f;
-                                if (visible(s, key))
-                                    ev = e16_of(muh[s], y16_value<SIMP>(&y16r[s][g * WPM], 2 * pp + t2), eh, el);
-                                sp[s] += (double)ev;
-                                res |= eh << (16 * t2);
-                                rlo |= el << (16 * t2);
+                        for (int i = 0; i < 4; ++i) {
+                            const uint32_t x = hl[s][i];
+                            float v;
+                            if constexpr (SIMP) {
+                                eh[i] = x >> 16;
+                                el[i] = x & 0xFFFFu;
+                                v = __builtin_bit_cast(float, x);
+                            } else {
+                                eh[i] = x & 0xFFFFu;
+                                el[i] = x >> 16;
+                                v = bf16_value(eh[i]) + bf16_value(el[i]);   // exact
                             }
-                            outw[pp] = res;
-                            outl[pp] = rlo;
+                            const bool vis = visible(s, key0 + i);
+                            eh[i] = vis ? eh[i] : 0u;
+                            el[i] = vis ? el[i] : 0u;
+                            ev[i] = vis ? (double)v : 0.0;
                         }
-                        *reinterpret_cast<uint2 *>(ycode + row[s] * YP + (key0 - k0)) = make_uint2(outw[0], outw[1]);
-                        *reinterpret_cast<uint2 *>(ylo + row[s] * YP + (key0 - k0)) = make_uint2(outl[0], outl[1]);
+                        sp[s] += (ev[0] + ev[1]) + (ev[2] + ev[3]);
+                        *reinterpret_cast<uint2 *>(ycode + row[s] * YP + (key0 - k0)) =
+                            make_uint2(eh[0] | eh[1] << 16, eh[2] | eh[3] << 16);
+                        *reinterpret_cast<uint2 *>(ylo + row[s] * YP + (key0 - k0)) =
+                            make_uint2(el[0] | el[1] << 16, el[2] | el[3] << 16);
                     }
                 }
             }
