@@ -28,7 +28,7 @@ LIB = os.path.join(HERE, "liblamp.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["lamp_kernels.hip", "lamp_fwd.hip", "lamp_fwd16.hip", "lamp_decode.hip", "lamp_host.cpp"]
+SOURCES = ["lamp_kernels.hip", "lamp_fwd.hip", "lamp_fwd16.hip", "lamp_decode.hip", "lamp_rates.hip", "lamp_host.cpp"]
 
 DPP_VGPR_WAITS = 2
 DPP_EXEC_WAITS = 5
@@ -139,28 +139,45 @@ def scan_dpp_hazards(asm):
     return sorted(set(found))
 
 
-def build(verbose=False, extra=()):
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC, "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-shared",
-           "-ffp-contract=off", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           "-I", os.path.join(ROOT, "include"), "-I", CSRC,
-           "-Wno-unused-command-line-argument", "-save-temps"]
-    cmd += list(extra)
-    cmd += [os.path.join(CSRC, s) for s in SOURCES]
-    cmd += ["-o", tmp]
+def _compile(src, work, flags, verbose):
+    """One source to an object in its own directory (device assembly kept)."""
+    sub = os.path.join(work, os.path.splitext(os.path.basename(src))[0])
+    os.makedirs(sub, exist_ok=True)
+    obj = os.path.join(sub, os.path.basename(src) + ".o")
+    cmd = [HIPCC] + flags + ["-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True, cwd=sub)
+    out = "\n".join(l for l in r.stdout.splitlines() if "packed-fp32-ops' is not a recognized feature" not in l)
+    return r.returncode, obj, out
+
+
+def build(verbose=False, extra=()):
+    from concurrent.futures import ThreadPoolExecutor
+    tmp = LIB + ".tmp%d" % os.getpid()
+    flags = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",
+             "-ffp-contract=off", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+             "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+             "-Wno-unused-command-line-argument", "-save-temps"] + list(extra)
+    jobs = max(1, min(len(SOURCES), int(os.environ.get("MAX_JOBS", "0")) or (os.cpu_count() or 1)))
     with tempfile.TemporaryDirectory(prefix="lamp_build_") as work:
-        r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True, cwd=work)
-        out = "\n".join(l for l in r.stdout.splitlines()
-                        if "packed-fp32-ops' is not a recognized feature" not in l)
+        with ThreadPoolExecutor(max_workers=jobs) as ex:
+            res = list(ex.map(lambda s: _compile(os.path.join(CSRC, s), work, flags, verbose), SOURCES))
+        failed = [out for rc, _, out in res if rc != 0]
+        if failed:
+            raise RuntimeError("hipcc failed:\n" + "\n".join(failed))
+        for _, _, out in res:
+            if verbose and out.strip():
+                print(out)
+        link = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC"] + [o for _, o, _ in res] + ["-o", tmp]
+        if verbose:
+            print(" ".join(link), flush=True)
+        r = subprocess.run(link, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True, cwd=work)
         if r.returncode != 0:
             if os.path.exists(tmp):
                 os.remove(tmp)
-            raise RuntimeError("hipcc failed:\n" + out)
-        if verbose and out.strip():
-            print(out)
-        asm_files = sorted(glob.glob(os.path.join(work, "*-hip-amdgcn-amd-amdhsa-" + ARCH + ".s")))
+            raise RuntimeError("link failed:\n" + r.stdout)
+        asm_files = sorted(glob.glob(os.path.join(work, "*", "*-hip-amdgcn-amd-amdhsa-" + ARCH + ".s")))
         names = {os.path.basename(f).split("-hip-")[0] for f in asm_files}
         if not {"lamp_fwd", "lamp_fwd16", "lamp_decode", "lamp_kernels"} <= names:
             os.remove(tmp)

@@ -756,10 +756,16 @@ bool fwd_supported(int D, int BQ, int BK, int NK)
     return (D == 64 || D == 128 || D == 256) && (BQ == 64 || BQ == 128) && (BK == 16 || BK == 64) && NK == 4;
 }
 
+bool fwd_grouped(int D, int BQ, int BK, int NK)
+{
+    (void)BQ;
+    return BK == 16 && NK == 4 && D >= 128;
+}
+
 hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found)
 {
     // 16-key sub-blocks with d >= 128: the kernel pipelined across key tiles
-    if (BK == 16 && NK == 4 && D >= 128) return dispatch_fwd16(D, BQ, p, s, found);
+    if (fwd_grouped(D, BQ, BK, NK)) return dispatch_fwd16(D, BQ, p, s, found);
     *found = true;
     LAMP_FWD_CASE(64, 64, 16, 4)
     LAMP_FWD_CASE(64, 128, 16, 4)

@@ -183,13 +183,16 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
             vlo[s] = p.N;
             vhi[s] = -1;
         }
-        qrow[s] = p.qt + (((size_t)b * p.Hq + h) * p.Nq + j) * D;   // zero-padded rows, in bounds
+        // grouped layout: 64-row blocks stored [group][row][4] (zero-padded rows, in bounds)
+        qrow[s] = p.qt + ((size_t)b * p.Hq + h) * p.Nq * D + (size_t)(j / 64) * 64 * D + (j % 64) * 4;
     }
     const int bv_lo = p.window > 0 ? (q0 - p.window + 1 > 0 ? q0 - p.window + 1 : 0) : 0;
     const int bv_hi = p.causal ? (q0 + BQ - 1 < p.N - 1 ? q0 + BQ - 1 : p.N - 1) : p.N - 1;
     const int t_begin = bv_lo / KPT, t_end = bv_hi / KPT;   // every tile in between has a visible pair
 
-    const float *kt32 = p.kt32 + ((size_t)b * p.Hkv + hk) * (size_t)p.Nk * D;       // fp32 keys [Nk][D]
+    const float *kt32 = p.kt32 + ((size_t)b * p.Hkv + hk) * (size_t)p.Nk * D;   // fp32 keys, grouped layout
+    // row of key i in the grouped layout (16-key blocks stored [group][key][4])
+    auto krow_of = [&](int i) { return kt32 + (size_t)(i / 16) * 16 * D + (i % 16) * 4; };
     const uint16_t *vtbase = p.vt + ((size_t)b * p.Hkv + hk) * (size_t)D * p.Nk;    // V^T [D][Nk]
     uint8_t *mrow = p.mask + (((size_t)b * p.Hq + h) * nqb + qb) * (size_t)(p.Nk / BK);
 
@@ -306,7 +309,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
         const int key0 = k0 + th * BK + w * 4;
         if (key0 > bv_hi || key0 + 3 < bv_lo) return;   // nothing visible in the block
         uint32_t yc[QPL][WPM];
-        rec16_keys<D, QPL, 4, SIMP>(qrow, kt32 + (size_t)(key0 + (lane & 3)) * D, yc);
+        rec16_keys<D, QPL, 4, SIMP, GrpLay>(qrow, krow_of(key0 + (lane & 3)), yc);
         fn(key0, yc);
     };
     // exponentials: 8-bit from the LDS table, 16-bit from the table in global
@@ -362,7 +365,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     if (mode != MODE_ALL16) {
         const bool done = own_emulated(t, act);
         uint32_t a8[QPL][8];
-        if (done) emu8_any<D, QPL, SIMP>(qrow, kt32 + (size_t)(t * KPT + w * BK) * D, a8);
+        if (done) emu8_any<D, QPL, SIMP, GrpLay>(qrow, kt32 + (size_t)(t * KPT + w * BK) * D, a8);
         emit8(t, a8, done);
     }
     __syncthreads();
@@ -386,7 +389,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                 for (int g = 0; g < kk / 4; ++g) m &= m - 1;
                 thg = __builtin_ctz(m);
             }
-            const float *krowr = kt32 + (size_t)(k0 + thg * BK + w * 4 + (kk & 3)) * D;
+            const float *krowr = krow_of(k0 + thg * BK + w * 4 + (kk & 3));
             const bool emu = mode != MODE_ALL16 && has_next && own_emulated(t + 1, act_next);
             const float *k32e = kt32 + (size_t)(k0 + KPT + w * BK) * D;   // read only when emu (then below N)
             uint32_t a8[QPL][8];
@@ -394,7 +397,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                 constexpr int NKEY = decltype(nkey_c)::value;
                 constexpr bool EMU = decltype(emu_c)::value;
                 uint32_t c[QPL][y16_words<SIMP>(NKEY)];
-                fused_pass<D, QPL, NKEY, EMU, SIMP>(qrow, k32e, krowr, a8, c);
+                fused_pass<D, QPL, NKEY, EMU, SIMP, GrpLay>(qrow, k32e, krowr, a8, c);
                 if constexpr (NKEY > 0)
 #pragma unroll
                     for (int s = 0; s < QPL; ++s)
@@ -898,11 +901,11 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                         const int kb = (lane & 15) % (4 * nr);
                         uint32_t m = Rn;
                         for (int g = 0; g < kb / 4; ++g) m &= m - 1;
-                        const float *krow = kt32 + (size_t)(k0 + __builtin_ctz(m) * BK + w * 4 + (kb & 3)) * D;
+                        const float *krow = krow_of(k0 + __builtin_ctz(m) * BK + w * 4 + (kb & 3));
                         auto rec = [&](auto nkey_c) {
                             constexpr int NKEY = decltype(nkey_c)::value;
                             uint32_t c[QPL][y16_words<SIMP>(NKEY)];
-                            rec16_keys<D, QPL, NKEY, SIMP>(qrow, krow, c);
+                            rec16_keys<D, QPL, NKEY, SIMP, GrpLay>(qrow, krow, c);
 #pragma unroll
                             for (int s = 0; s < QPL; ++s)
 #pragma unroll

@@ -282,7 +282,8 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
         for (int i = 0; i < 3; ++i) HIP_TRY(hipEventCreate(&tc.e[i]));
         HIP_TRY(hipEventRecord(tc.e[0], s));
     }
-    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, Nq, Nk, d, scale_of(d), s));
+    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, Nq, Nk, d, scale_of(d), s,
+                                 lamp::fwd_grouped(d, bq, bk, nk)));
     HIP_TRY(lamp::launch_transpose_v(v, w.vt, B, Hkv, N, Nk, d, s));
     if (timed) HIP_TRY(hipEventRecord(tc.e[1], s));
     bool found = false;
@@ -381,6 +382,13 @@ int lamp_attn_decode(const uint16_t *q, const uint16_t *k, const uint16_t *v, in
         std::lock_guard<std::mutex> lk(g_tmu);
         g_timed.push_back(tc);
     }
+    return LAMP_OK;
+}
+
+int lamp_issue_rates(double *ns_per_simd, void *stream)
+{
+    if (!ns_per_simd) return fail(LAMP_ERR_INVALID_ARG, "null output pointer");
+    HIP_TRY(lamp::measure_issue_rates(ns_per_simd, static_cast<hipStream_t>(stream)));
     return LAMP_OK;
 }
 

@@ -15,8 +15,8 @@ enum { MODE_LAMP = 0, MODE_PURE8 = 1, MODE_ALL16 = 2 };
 constexpr int SIM8_ENTRIES = 112, SIM8_TABLE = 256, SIM16_TABLE = 45056;
 
 struct FwdParams {
-    const float *qt;          // [B][Hq][N][D] pre-scaled queries, fp32
-    const float *kt32;        // [B][Hkv][N][D] keys, fp32
+    const float *qt;          // [B][Hq][Nq][D] pre-scaled queries, fp32 (row or grouped layout, see launch_prepass)
+    const float *kt32;        // [B][Hkv][Nk][D] keys, fp32 (row or grouped layout)
     const uint16_t *vt;       // [B][Hkv][D][Nk] bf16, V transposed
     const uint16_t *exp16;    // ue5m11 shift code -> ue5m11 exp code
     const uint32_t *exp16hl;  // ue5m11 shift code -> bf16 high | low << 16 of the ue5m11 exp
@@ -68,8 +68,17 @@ bool fwd_supported(int D, int BQ, int BK, int NK);
 hipError_t dispatch_fwd16(int D, int BQ, const FwdParams &p, hipStream_t s, bool *found);
 hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found);
 hipError_t launch_transpose_v(const uint16_t *v, uint16_t *vt, int B, int Hkv, int N, int Nk, int D, hipStream_t s);
+
+// Issue rates of the logit loops' instructions (lamp_rates.hip): ns per
+// wave-instruction (per emulated step for RATE_STEP) per SIMD, into ns[RATE_N].
+enum { RATE_FMAC = 0, RATE_FMAC_DPP = 1, RATE_DECODE = 2, RATE_ENCODE = 3, RATE_STEP = 4, RATE_N = 5 };
+hipError_t measure_issue_rates(double *ns, hipStream_t s);
+// grouped: the layout of the pipelined kernel (queries in 64-row and keys in
+// 16-row blocks, each block stored [D/4][rows][4]); otherwise [rows][D].
 hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float *kt32, int B, int Hq, int Hkv,
-                          int N, int Nq, int Nk, int D, float scale, hipStream_t s);
+                          int N, int Nq, int Nk, int D, float scale, hipStream_t s, bool grouped = false);
+// whether dispatch_fwd runs the pipelined kernel (which reads the grouped layout)
+bool fwd_grouped(int D, int BQ, int BK, int NK);
 hipError_t launch_logits8(const LogitsParams &p, int D, hipStream_t s);
 hipError_t launch_logits16(const LogitsParams &p, int D, hipStream_t s);
 hipError_t launch_logits_sim(const LogitsParams &p, int D, int high, hipStream_t s);

@@ -18,31 +18,49 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // ------------------------------------------------------------------ prepass
-// q_tilde = RN32(q * s), fp32 [B][Hq][N][D].
+// Row (j) and channel (c) of element i of a [rows][D] matrix per head, in the
+// row layout (blk = 0) or in the grouped layout with blocks of blk rows, each
+// block stored [D/4][blk][4] (one 4-channel group of a block contiguous).
+__device__ __forceinline__ void rc_of(size_t i, int D, int blk, size_t &j, size_t &c)
+{
+    if (blk == 0) {
+        c = i % (size_t)D;
+        j = i / (size_t)D;
+        return;
+    }
+    const size_t per = (size_t)blk * D, r = i % per;
+    j = (i / per) * blk + (r % ((size_t)blk * 4)) / 4;
+    c = (r / ((size_t)blk * 4)) * 4 + r % 4;
+}
+
 // Pre-scaled queries q~ = RN32(q * s), rows padded with zeros from N to Nq:
-// qt [B*Hq][Nq][D] from q [B*Hq][N][D].
+// qt [B*Hq][Nq][D] from q [B*Hq][N][D] (grouped layout: blk = 64).
 __global__ void prescale_q_kernel(const uint16_t *__restrict__ q, float *__restrict__ qt, float s, int N, int Nq,
-                                  int D, size_t n)
+                                  int D, size_t n, int blk)
 {
     size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     size_t stride = (size_t)gridDim.x * blockDim.x;
+    const size_t per = (size_t)Nq * D;
     for (; i < n; i += stride) {
-        const size_t c = i % (size_t)D, r = i / (size_t)D;
-        const size_t j = r % (size_t)Nq, bh = r / (size_t)Nq;
+        size_t j, c;
+        rc_of(i % per, D, blk, j, c);
+        const size_t bh = i / per;
         qt[i] = j < (size_t)N ? bf16_value(q[(bh * N + j) * D + c]) * s : 0.0f;
     }
 }
 
 // K in fp32 (bf16 -> fp32 is exact), rows padded with zeros from N to Nk:
-// k32 [B*Hkv][Nk][D] from k [B*Hkv][N][D].
+// k32 [B*Hkv][Nk][D] from k [B*Hkv][N][D] (grouped layout: blk = 16).
 __global__ void convert_k_kernel(const uint16_t *__restrict__ k, float *__restrict__ k32, int N, int Nk, int D,
-                                 size_t n)
+                                 size_t n, int blk)
 {
     size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     size_t stride = (size_t)gridDim.x * blockDim.x;
+    const size_t per = (size_t)Nk * D;
     for (; i < n; i += stride) {
-        const size_t c = i % (size_t)D, r = i / (size_t)D;
-        const size_t j = r % (size_t)Nk, bh = r / (size_t)Nk;
+        size_t j, c;
+        rc_of(i % per, D, blk, j, c);
+        const size_t bh = i / per;
         k32[i] = j < (size_t)N ? bf16_value(k[(bh * N + j) * D + c]) : 0.0f;
     }
 }
@@ -279,13 +297,13 @@ __global__ void selftest_exp_doc_kernel(const double *__restrict__ x, double *__
 
 // ------------------------------------------------------------------ launchers
 hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float *kt32, int B, int Hq, int Hkv,
-                          int N, int Nq, int Nk, int D, float scale, hipStream_t s)
+                          int N, int Nq, int Nk, int D, float scale, hipStream_t s, bool grouped)
 {
     size_t nq = (size_t)B * Hq * Nq * D, nk = (size_t)B * Hkv * Nk * D;
     unsigned gq = (unsigned)((nq + 255) / 256 < 65536 ? (nq + 255) / 256 : 65536);
     unsigned gk = (unsigned)((nk + 255) / 256 < 65536 ? (nk + 255) / 256 : 65536);
-    hipLaunchKernelGGL(prescale_q_kernel, dim3(gq), dim3(256), 0, s, q, qt, scale, N, Nq, D, nq);
-    hipLaunchKernelGGL(convert_k_kernel, dim3(gk), dim3(256), 0, s, k, kt32, N, Nk, D, nk);
+    hipLaunchKernelGGL(prescale_q_kernel, dim3(gq), dim3(256), 0, s, q, qt, scale, N, Nq, D, nq, grouped ? 64 : 0);
+    hipLaunchKernelGGL(convert_k_kernel, dim3(gk), dim3(256), 0, s, k, kt32, N, Nk, D, nk, grouped ? 16 : 0);
     return hipGetLastError();
 }
 
@@ -293,7 +311,7 @@ hipError_t launch_prescale_q(const uint16_t *q, float *qt, int BH, int rows, int
 {
     size_t n = (size_t)BH * rows * D;
     unsigned g = (unsigned)((n + 255) / 256 < 65536 ? (n + 255) / 256 : 65536);
-    hipLaunchKernelGGL(prescale_q_kernel, dim3(g), dim3(256), 0, s, q, qt, scale, rows, rows, D, n);
+    hipLaunchKernelGGL(prescale_q_kernel, dim3(g), dim3(256), 0, s, q, qt, scale, rows, rows, D, n, 0);
     return hipGetLastError();
 }
 

@@ -26,6 +26,45 @@ __device__ __forceinline__ float fmac_bc(float acc, float kv, float q)
     return acc;
 }
 
+// Two code words of two accumulators each advanced by one channel in a single
+// statement: word a holds the codes of keys I0, I1 of query value qa, word b
+// those of keys J0, J1 of qb; each pair is decoded, the FMAs read the keys by
+// row broadcast, and the results are rounded to e4m3 into bits [15:0] of the
+// word (bits [31:16] kept; no saturation, see pk_e4m3).  The decoded values go
+// to four fixed registers that the statement declares clobbered, so the two
+// chains interleave with no wait state between the statements of one chain
+// that the compiler, not seeing into the assembly, would otherwise insert
+// after every separate asm statement.
+template <int I0, int I1, int J0, int J1>
+__device__ __forceinline__ void emu8_words(uint32_t &a, uint32_t &b, float kv, float qa, float qb)
+{
+    asm("v_cvt_pk_f32_fp8 v[248:249], %0\n\t"
+        "v_cvt_pk_f32_fp8 v[250:251], %1\n\t"
+        "v_fmac_f32_dpp v248, %2, %3 row_newbcast:%5 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp v249, %2, %3 row_newbcast:%6 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp v250, %2, %4 row_newbcast:%7 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp v251, %2, %4 row_newbcast:%8 row_mask:0xf bank_mask:0xf\n\t"
+        "v_cvt_pk_fp8_f32 %0, v248, v249\n\t"
+        "v_cvt_pk_fp8_f32 %1, v250, v251"
+        : "+v"(a), "+v"(b)
+        : "v"(kv), "v"(qa), "v"(qb), "n"(I0), "n"(I1), "n"(J0), "n"(J1)
+        : "v248", "v249", "v250", "v251");
+}
+
+// Where the loops find the fp32 queries and keys.  Row layout ([row][D]): the
+// 4-channel group g of a row is at offset 4g and consecutive keys are D apart.
+// Grouped layout (the pipelined kernel): queries in blocks of 64 rows and keys
+// in blocks of 16, each block stored [group][row][4], so that one 4-channel
+// group of a block is contiguous: group g of a query row is at 256g, of a key
+// row at 64g, and consecutive keys of a block are 4 apart.
+template <int QS_, int KS_, int KR_>
+struct Lay {
+    static constexpr int QS = QS_, KS = KS_, KR = KR_;   // query / key group stride, key row stride
+};
+template <int D>
+using RowLay = Lay<4, 4, D>;
+using GrpLay = Lay<256, 64, 4>;
+
 // Query rows come either from global memory (const float *) or from LDS
 // (lds_cfptr, so that the loads are ds_read_b128 rather than flat loads).
 typedef const __attribute__((address_space(3))) float *lds_cfptr;
@@ -39,13 +78,13 @@ __device__ __forceinline__ float4 load4(lds_cfptr p)
 }
 
 // Loads of a 4-channel group: this lane's key row and query rows.
-template <int QPL, class QP>
+template <int QPL, class LY, class QP>
 __device__ __forceinline__ void load_group(const float *krow, const QP (&qrow)[QPL], int c, float4 &k4,
                                            float4 (&q4)[QPL])
 {
-    k4 = *reinterpret_cast<const float4 *>(krow + c);
+    k4 = *reinterpret_cast<const float4 *>(krow + (c / 4) * LY::KS);
 #pragma unroll
-    for (int s = 0; s < QPL; ++s) q4[s] = load4(qrow[s] + c);
+    for (int s = 0; s < QPL; ++s) q4[s] = load4(qrow[s] + (c / 4) * LY::QS);
 }
 
 __device__ __forceinline__ float f4_at(const float4 &v, int i)
@@ -67,19 +106,34 @@ __device__ __forceinline__ void emu8_pair(float kv, const float (&q)[QPL], uint3
     }
 }
 
+// Two words of the non-saturating pass at once: the two query rows of a word
+// index (QPL = 2), or words P and P + 1 of one row (QPL = 1).
+template <int QPL, int P>
+__device__ __forceinline__ void emu8_two(float kv, const float (&q)[QPL], uint32_t (&acc)[QPL][8])
+{
+    if constexpr (QPL == 2) {
+        emu8_words<2 * P, 2 * P + 1, 2 * P, 2 * P + 1>(acc[0][P], acc[1][P], kv, q[0], q[1]);
+    } else if constexpr (P % 2 == 0) {
+#pragma unroll
+        for (int s = 0; s < QPL; ++s)
+            emu8_words<2 * P, 2 * P + 1, 2 * P + 2, 2 * P + 3>(acc[s][P], acc[s][P + 1], kv, q[s], q[s]);
+    }
+}
+
 template <int QPL, bool SAT, int... P>
 __device__ __forceinline__ void emu8_channel(float kv, const float (&q)[QPL], uint32_t (&acc)[QPL][8],
                                              std::integer_sequence<int, P...>)
 {
-    (emu8_pair<QPL, SAT, P>(kv, q, acc), ...);
+    if constexpr (SAT || (QPL != 1 && QPL != 2)) (emu8_pair<QPL, SAT, P>(kv, q, acc), ...);
+    else (emu8_two<QPL, P>(kv, q, acc), ...);
 }
 
 // Y8 of one 16-key chunk for QPL query rows of this lane (Sec. 4.1:
 // acc <- RN_e4m3(RN32(q_tilde * k + acc)), channels ascending, from +0).
-// k32 is the fp32 key matrix at the chunk's first key ([key][D]); qrow[s] the
-// fp32 pre-scaled query row of slot s.  acc[s][p] receives the codes of keys
-// 2p, 2p+1 in bits [15:0].
-template <int D, int QPL, bool SAT, class QP>
+// k32 points at the chunk's first key (layout LY); qrow[s] at the fp32
+// pre-scaled query row of slot s.  acc[s][p] receives the codes of keys 2p,
+// 2p+1 in bits [15:0].
+template <int D, int QPL, bool SAT, class LY = RowLay<D>, class QP>
 __device__ __forceinline__ void emu8_pass(const QP (&qrow)[QPL], const float *k32, uint32_t (&acc)[QPL][8])
 {
     static_assert(D % 8 == 0, "channels in pairs of 4-channel groups");
@@ -87,7 +141,7 @@ __device__ __forceinline__ void emu8_pass(const QP (&qrow)[QPL], const float *k3
     for (int s = 0; s < QPL; ++s)
 #pragma unroll
         for (int p = 0; p < 8; ++p) acc[s][p] = 0u;
-    const float *krow = k32 + (size_t)(__lane_id() & 15) * D;
+    const float *krow = k32 + (size_t)(__lane_id() & 15) * LY::KR;
     // Two alternating load buffers: the key registers feeding the DPP
     // broadcast are only ever written by vector loads, never copied.
     float4 ka, kb, qa[QPL], qb[QPL];
@@ -102,14 +156,14 @@ __device__ __forceinline__ void emu8_pass(const QP (&qrow)[QPL], const float *k3
     };
     // steady state, then the last pair of groups without further loads (the
     // offsets stay affine in c, so they fold into the loads' immediates)
-    load_group<QPL>(krow, qrow, 0, ka, qa);
+    load_group<QPL, LY>(krow, qrow, 0, ka, qa);
     for (int c = 0; c < D - 8; c += 8) {
-        load_group<QPL>(krow, qrow, c + 4, kb, qb);
+        load_group<QPL, LY>(krow, qrow, c + 4, kb, qb);
         run(ka, qa);
-        load_group<QPL>(krow, qrow, c + 8, ka, qa);
+        load_group<QPL, LY>(krow, qrow, c + 8, ka, qa);
         run(kb, qb);
     }
-    load_group<QPL>(krow, qrow, D - 4, kb, qb);
+    load_group<QPL, LY>(krow, qrow, D - 4, kb, qb);
     run(ka, qa);
     run(kb, qb);
 }
@@ -117,16 +171,16 @@ __device__ __forceinline__ void emu8_pass(const QP (&qrow)[QPL], const float *k3
 // The fast pass uses the non-saturating conversion; if any lane of the wave
 // overflowed somewhere (a NaN code at the end of a chain), the chunk is
 // recomputed with the saturating conversion.
-template <int D, int QPL, class QP>
+template <int D, int QPL, class LY = RowLay<D>, class QP>
 __device__ __forceinline__ void emu8_chunk(const QP (&qrow)[QPL], const float *k32, uint32_t (&acc)[QPL][8])
 {
-    emu8_pass<D, QPL, false>(qrow, k32, acc);
+    emu8_pass<D, QPL, false, LY>(qrow, k32, acc);
     uint32_t nan = 0;
 #pragma unroll
     for (int s = 0; s < QPL; ++s)
 #pragma unroll
         for (int p = 0; p < 8; ++p) nan |= e4m3_nan_bits(acc[s][p]);
-    if (wave_any(nan != 0)) emu8_pass<D, QPL, true>(qrow, k32, acc);
+    if (wave_any(nan != 0)) emu8_pass<D, QPL, true, LY>(qrow, k32, acc);
 }
 
 // One channel of the 16-bit accumulation for every key and slot.
@@ -169,7 +223,7 @@ __device__ __forceinline__ void emu8s_channel(float kv, const float (&q)[QPL], f
 
 // Y8 of one 16-key chunk in the SIM profile (as emu8_pass); codes[s][p]
 // receives the bf16 patterns of keys 2p (bits [15:0]) and 2p+1.
-template <int D, int QPL, class QP>
+template <int D, int QPL, class LY = RowLay<D>, class QP>
 __device__ __forceinline__ void emu8s_pass(const QP (&qrow)[QPL], const float *k32, uint32_t (&codes)[QPL][8])
 {
     static_assert(D % 8 == 0, "channels in pairs of 4-channel groups");
@@ -178,7 +232,7 @@ __device__ __forceinline__ void emu8s_pass(const QP (&qrow)[QPL], const float *k
     for (int s = 0; s < QPL; ++s)
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[s][i] = 0.0f;
-    const float *krow = k32 + (size_t)(__lane_id() & 15) * D;
+    const float *krow = k32 + (size_t)(__lane_id() & 15) * LY::KR;
     float4 ka, kb, qa[QPL], qb[QPL];
     auto run = [&](const float4 &k4, const float4 (&q4)[QPL]) {
 #pragma unroll
@@ -189,14 +243,14 @@ __device__ __forceinline__ void emu8s_pass(const QP (&qrow)[QPL], const float *k
             emu8s_channel<QPL>(f4_at(k4, cc), q, acc, std::make_integer_sequence<int, 16>());
         }
     };
-    load_group<QPL>(krow, qrow, 0, ka, qa);
+    load_group<QPL, LY>(krow, qrow, 0, ka, qa);
     for (int c = 0; c < D - 8; c += 8) {
-        load_group<QPL>(krow, qrow, c + 4, kb, qb);
+        load_group<QPL, LY>(krow, qrow, c + 4, kb, qb);
         run(ka, qa);
-        load_group<QPL>(krow, qrow, c + 8, ka, qa);
+        load_group<QPL, LY>(krow, qrow, c + 8, ka, qa);
         run(kb, qb);
     }
-    load_group<QPL>(krow, qrow, D - 4, kb, qb);
+    load_group<QPL, LY>(krow, qrow, D - 4, kb, qb);
     run(ka, qa);
     run(kb, qb);
 #pragma unroll
@@ -206,11 +260,11 @@ __device__ __forceinline__ void emu8s_pass(const QP (&qrow)[QPL], const float *k
 }
 
 // Y8 of a 16-key chunk in either profile.
-template <int D, int QPL, bool SIMP, class QP>
+template <int D, int QPL, bool SIMP, class LY = RowLay<D>, class QP>
 __device__ __forceinline__ void emu8_any(const QP (&qrow)[QPL], const float *k32, uint32_t (&codes)[QPL][8])
 {
-    if constexpr (SIMP) emu8s_pass<D, QPL>(qrow, k32, codes);
-    else emu8_chunk<D, QPL>(qrow, k32, codes);
+    if constexpr (SIMP) emu8s_pass<D, QPL, LY>(qrow, k32, codes);
+    else emu8_chunk<D, QPL, LY>(qrow, k32, codes);
 }
 
 // The 16-bit logits of the FP32 chains in acc, encoded: rounded once to e4m11
@@ -242,7 +296,7 @@ __device__ __forceinline__ void encode16(const float (&acc)[QPL][NKEY], uint32_t
 // accumulation of NKEY keys, this lane's key row being krowr (as rec16_keys).
 // The forward kernel uses it to run the 8-bit logits of the next key tile
 // together with the speculative 16-bit recompute of the current one.
-template <int D, int QPL, int NKEY, bool EMU, bool SIMP, class QP>
+template <int D, int QPL, int NKEY, bool EMU, bool SIMP, class LY = RowLay<D>, class QP>
 __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k32e, const float *krowr,
                                            uint32_t (&a8)[QPL][8], uint32_t (&c16)[QPL][y16_words<SIMP>(NKEY)])
 {
@@ -261,13 +315,13 @@ __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k
 #pragma unroll
         for (int i = 0; i < NE; ++i) e8[s][i] = 0.0f;
     }
-    const float *krowe = k32e + (size_t)(__lane_id() & 15) * D;
+    const float *krowe = k32e + (size_t)(__lane_id() & 15) * LY::KR;
     float4 kea, keb, kra, krb, qa[QPL], qb[QPL];
     auto ld = [&](int c, float4 &ke, float4 &kr, float4 (&q4)[QPL]) {
-        if constexpr (EMU) ke = load4(krowe + c);
-        if constexpr (NKEY > 0) kr = load4(krowr + c);
+        if constexpr (EMU) ke = load4(krowe + (c / 4) * LY::KS);
+        if constexpr (NKEY > 0) kr = load4(krowr + (c / 4) * LY::KS);
 #pragma unroll
-        for (int s = 0; s < QPL; ++s) q4[s] = load4(qrow[s] + c);
+        for (int s = 0; s < QPL; ++s) q4[s] = load4(qrow[s] + (c / 4) * LY::QS);
     };
     auto run = [&](const float4 &ke, const float4 &kr, const float4 (&q4)[QPL]) {
 #pragma unroll
@@ -304,7 +358,7 @@ __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k
         for (int s = 0; s < QPL; ++s)
 #pragma unroll
             for (int p = 0; p < 8; ++p) nan |= e4m3_nan_bits(a8[s][p]);
-        if (wave_any(nan != 0)) emu8_pass<D, QPL, true>(qrow, k32e, a8);
+        if (wave_any(nan != 0)) emu8_pass<D, QPL, true, LY>(qrow, k32e, a8);
     }
     if constexpr (NKEY > 0) encode16<SIMP>(acc, c16);
 }
@@ -320,14 +374,14 @@ __device__ __forceinline__ void rec16_channel(float kv, const float (&q)[QPL], f
 
 // Y16 of NKEY keys (NKEY in {4, 8, 12, 16}) for QPL query rows: the FP32 FMA
 // chain over the channels in ascending order from +0, rounded once to e4m11
-// (saturating).  krow is this lane's key row ([D] fp32): lane l of every
+// (saturating).  krow is this lane's key row (layout LY): lane l of every
 // 16-lane row supplies key (l mod 16) and must hold key (l mod NKEY) (lanes
 // past NKEY duplicate the first keys and are not read).  codes[s][p] receives
 // the e4m11 codes of keys 2p (bits [15:0]) and 2p+1 (SIM profile: rounded to
 // 11 mantissa bits, codes[s][i] the FP32 pattern of key i).  With few keys per
 // channel the loop is latency-bound, so the loads run PD 4-channel groups
 // ahead in a ring of buffers written only by loads.
-template <int D, int QPL, int NKEY, bool SIMP = false, class QP>
+template <int D, int QPL, int NKEY, bool SIMP = false, class LY = RowLay<D>, class QP>
 __device__ __forceinline__ void rec16_keys(const QP (&qrow)[QPL], const float *krow,
                                            uint32_t (&codes)[QPL][y16_words<SIMP>(NKEY)])
 {
@@ -351,12 +405,12 @@ __device__ __forceinline__ void rec16_keys(const QP (&qrow)[QPL], const float *k
         }
     };
 #pragma unroll
-    for (int r = 0; r < PD; ++r) load_group<QPL>(krow, qrow, 4 * r, kb[r], qb[r]);
+    for (int r = 0; r < PD; ++r) load_group<QPL, LY>(krow, qrow, 4 * r, kb[r], qb[r]);
     for (int c = 0; c < D - 4 * PD; c += 4 * PD) {
 #pragma unroll
         for (int r = 0; r < PD; ++r) {
             run(r);
-            load_group<QPL>(krow, qrow, c + 4 * (r + PD), kb[r], qb[r]);
+            load_group<QPL, LY>(krow, qrow, c + 4 * (r + PD), kb[r], qb[r]);
         }
     }
 #pragma unroll
@@ -365,11 +419,11 @@ __device__ __forceinline__ void rec16_keys(const QP (&qrow)[QPL], const float *k
 }
 
 // Y16 of the 16 keys starting at k32 ([key][D] fp32).
-template <int D, int QPL, bool SIMP = false, class QP>
+template <int D, int QPL, bool SIMP = false, class LY = RowLay<D>, class QP>
 __device__ __forceinline__ void rec16_chunk(const QP (&qrow)[QPL], const float *k32,
                                             uint32_t (&codes)[QPL][y16_words<SIMP>(16)])
 {
-    rec16_keys<D, QPL, 16, SIMP>(qrow, k32 + (size_t)(__lane_id() & 15) * D, codes);
+    rec16_keys<D, QPL, 16, SIMP, LY>(qrow, k32 + (size_t)(__lane_id() & 15) * LY::KR, codes);
 }
 
 } // namespace lamp

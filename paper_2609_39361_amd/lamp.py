@@ -59,6 +59,8 @@ def lib():
         L.lamp_get_tables.restype = i32
         L.lamp_get_exp16_parts.argtypes = [i32, P]
         L.lamp_get_exp16_parts.restype = i32
+        L.lamp_issue_rates.argtypes = [P, P]
+        L.lamp_issue_rates.restype = i32
         L.lamp_timing_enable.argtypes = [i32]
         L.lamp_timing_enable.restype = i32
         L.lamp_timing_read.argtypes = [P, P, P]
@@ -259,6 +261,18 @@ def timing_read():
     n, tf, tp = ctypes.c_int(0), ctypes.c_double(0.0), ctypes.c_double(0.0)
     _check(lib().lamp_timing_read(ctypes.byref(n), ctypes.byref(tf), ctypes.byref(tp)))
     return n.value, tf.value, tp.value
+
+
+ISSUE_RATE_KINDS = ("fmac_f32", "fmac_f32_dpp", "cvt_pk_f32_fp8", "cvt_pk_fp8_f32", "emulated_step")
+
+
+def issue_rates():
+    """Nanoseconds per wave-instruction per SIMD of the logit loops'
+    instructions on the current device (dict keyed by ISSUE_RATE_KINDS; the
+    last is one emulated 8-bit step, two multiply-adds per lane)."""
+    ns = (ctypes.c_double * len(ISSUE_RATE_KINDS))()
+    _check(lib().lamp_issue_rates(ns, _stream(torch.device("cuda", torch.cuda.current_device()))))
+    return dict(zip(ISSUE_RATE_KINDS, list(ns)))
 
 
 def mask_stats(mask, nk):
