@@ -67,7 +67,8 @@ struct Cfg16 {
     static constexpr size_t OFF_CMF = OFF_CMI + (size_t)2 * NK * BQ * 4;  // f32 [2][NW][BQ] | f64 [NK][BQ]
     static constexpr size_t OFF_SP = OFF_CMF + CMF;                     // f64 [2][NW][BQ]
     static constexpr size_t OFF_ED = OFF_SP + (size_t)2 * NW * BQ * 8;  // f64 [EXPDOC_NK]
-    static constexpr size_t LDS = OFF_ED + (size_t)EXPDOC_NK * 8;
+    static constexpr size_t OFF_TS = OFF_ED + (size_t)EXPDOC_NK * 8;    // i32 [2][NK] sub-block threats
+    static constexpr size_t LDS = OFF_TS + (size_t)2 * NK * 4;
     static_assert(BQ == 64 || BQ == 128, "64 or 128 query rows per block");
     static_assert(CPW % 32 == 0, "whole 32-channel tiles per wave");
 };
@@ -84,6 +85,15 @@ __device__ __forceinline__ int cm_key(float y)
 {
     if constexpr (SIMP) return ord_of(y);
     else return fx_of(y);
+}
+
+// fx_of of an e4m11 code, from the code: the significand (with its implicit
+// bit when normal) shifted by max(ex, 1) - 1.
+__device__ __forceinline__ int e4m11_fx(uint32_t code)
+{
+    const uint32_t ex = (code >> 11) & 0xFu, m = code & 0x7FFu;
+    const int mag = ex ? (int)((m | 0x800u) << (ex - 1u)) : (int)m;
+    return (code & 0x8000u) ? -mag : mag;
 }
 
 template <bool SIMP>
@@ -115,6 +125,25 @@ __device__ __forceinline__ u32x4 lo_bf16x8(const u32x4 &h, const u32x4 &l)
     return r;
 }
 
+// Maximum of an int over the wave, returned to every lane: DPP exchanges inside
+// each 16-lane row (quad swaps, then rotations by 4 and 8), then the four row
+// maxima through scalar registers.
+__device__ __forceinline__ int wave_max_i32(int v)
+{
+    int o = __builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false);    // quad_perm [1,0,3,2]
+    v = o > v ? o : v;
+    o = __builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false);        // quad_perm [2,3,0,1]
+    v = o > v ? o : v;
+    o = __builtin_amdgcn_update_dpp(v, v, 0x124, 0xF, 0xF, false);       // row_ror:4
+    v = o > v ? o : v;
+    o = __builtin_amdgcn_update_dpp(v, v, 0x128, 0xF, 0xF, false);       // row_ror:8
+    v = o > v ? o : v;
+    const int a = __builtin_amdgcn_readlane(v, 0), b = __builtin_amdgcn_readlane(v, 16);
+    const int c = __builtin_amdgcn_readlane(v, 32), d = __builtin_amdgcn_readlane(v, 48);
+    const int ab = a > b ? a : b, cd = c > d ? c : d;
+    return ab > cd ? ab : cd;
+}
+
 } // namespace
 
 template <int D, int BQ, int MODE, bool SIMP>
@@ -136,6 +165,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     double *sps = reinterpret_cast<double *>(smem + C::OFF_SP);         // [NW][BQ] partial row sums of E
     double *spf = sps + NW * BQ;                                        // [NW][BQ] over 8-bit sub-blocks
     double *edk = reinterpret_cast<double *>(smem + C::OFF_ED);         // exp_doc constants
+    int *tsl = reinterpret_cast<int *>(smem + C::OFF_TS);               // [2][NK] threats of a tile
 
     const int tid = threadIdx.x;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;   // w is wave-uniform
@@ -295,6 +325,28 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
 #pragma unroll
             for (int s = 0; s < QPL; ++s) m8[th][s] = m8s[th * BQ + row[s]];
     };
+    // Threat of this wave's sub-block of `tile` against the running maximum mu
+    // (the stage-1 ordering of Eq. (7)): T = max over rows with a visible 8-bit
+    // logit of (m8 - mu), +inf where mu = -inf.  With the formats of Sec. 3.3
+    // both are multiples of 2^-17 below 2^9, so T is exact as an int in those
+    // units (INT_MAX for +inf, INT_MIN when no row has a visible logit).  Each
+    // wave computes the threat of its own sub-block after the tile before
+    // `tile` is complete, and the stage-1 test of `tile` reads all four.
+    auto own_threat = [&](int tile) {
+        if constexpr (!SIMP) {
+            const float *m8s = m8s_of(tile);
+            int tv = INT_MIN;
+#pragma unroll
+            for (int s = 0; s < QPL; ++s) {
+                const float m8v = m8s[w * BQ + row[s]];
+                const bool vis = m8v > NEG_INF, muinf = mu[s] == NEG_INF;   // infinities never converted
+                const int d = muinf ? INT_MAX : fx_of(vis ? m8v : 0.0f) - fx_of(muinf ? 0.0f : mu[s]);
+                tv = (vis && d > tv) ? d : tv;
+            }
+            const int T = wave_max_i32(tv);
+            if (lane == 0) tsl[(tile & 1) * NK + w] = T;
+        }
+    };
     // the set of sub-blocks whose 16-bit logits the next fused pass computes
     auto f0_of = [&](int tile, uint32_t act) -> uint32_t {
         if (mode == MODE_ALL16) return act;
@@ -370,6 +422,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     }
     __syncthreads();
     uint32_t F0 = f0_of(t, act);
+    if (mode == MODE_LAMP && !stage1_off) own_threat(t);
 
     for (; t <= t_end; ++t) {
         const int k0 = t * KPT;
@@ -439,8 +492,10 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                     int cm = INT_MIN;
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        const int f = cm_key<SIMP>(y16_value<SIMP>(&y16r[s][g * WPM], i));
-                        if (visible(s, key0 + i)) cm = f > cm ? f : cm;
+                        int f;
+                        if constexpr (SIMP) f = cm_key<SIMP>(y16_value<SIMP>(&y16r[s][g * WPM], i));
+                        else f = e4m11_fx((y16r[s][g * WPM + (i >> 1)] >> (16 * (i & 1))) & 0xFFFFu);
+                        cm = (visible(s, key0 + i) && f > cm) ? f : cm;
                     }
                     if (cm != INT_MIN) atomicMax(&cmi[th * BQ + row[s]], cm);
                 }
@@ -480,18 +535,26 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
         } else {
             float m8[NK][QPL];
             load_m8(t, m8);
-            // threats T_theta = max_j (m8 - mu_j), exact in fp64 (+inf when mu_j = -inf)
-            double T[NK];
+            // threats T_theta = max_j (m8 - mu_j) (+inf when mu_j = -inf): exact
+            // ints from the four waves (own_threat), or, in the SIM profile,
+            // exact in fp64
+            using TT = std::conditional_t<SIMP, double, int>;
+            TT T[NK];
+            if constexpr (SIMP) {
 #pragma unroll
-            for (int th = 0; th < NK; ++th) {
-                double tv = -__builtin_inf();
+                for (int th = 0; th < NK; ++th) {
+                    double tv = -__builtin_inf();
 #pragma unroll
-                for (int s = 0; s < QPL; ++s)
-                    if (m8[th][s] > NEG_INF) {
-                        const double d = (double)m8[th][s] - (double)mu[s];
-                        tv = d > tv ? d : tv;
-                    }
-                T[th] = wave_max_f64(tv);
+                    for (int s = 0; s < QPL; ++s)
+                        if (m8[th][s] > NEG_INF) {
+                            const double d = (double)m8[th][s] - (double)mu[s];
+                            tv = d > tv ? d : tv;
+                        }
+                    T[th] = wave_max_f64(tv);
+                }
+            } else {
+#pragma unroll
+                for (int th = 0; th < NK; ++th) T[th] = tsl[(t & 1) * NK + th];
             }
             // descending threat, ties by index; order packed 4 bits per rank
             uint32_t order = 0, taken = 0;
@@ -499,7 +562,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
 #pragma unroll
             for (int r = 0; r < NK; ++r) {
                 int best = -1;
-                double bt = 0.0;
+                TT bt = 0;
 #pragma unroll
                 for (int th = 0; th < NK; ++th) {
                     const bool cand = (act >> th & 1u) && !(taken >> th & 1u);
@@ -1034,6 +1097,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
         pv_chunk(3, vb);
 
         F0 = has_next ? f0_of(t + 1, act_next) : 0u;
+        if (mode == MODE_LAMP && !stage1_off && has_next) own_threat(t + 1);
         act = act_next;
         __syncthreads();   // I: this tile's code buffer is rewritten by the pass of tile t+1
     }
