@@ -114,3 +114,15 @@ def test_timing_read_without_calls():
     lamp.timing_enable(True)
     lamp.timing_enable(False)
     assert lamp.timing_read() == (0, 0.0, 0.0)
+
+
+def test_issue_rates_rejects_null_without_gpu():
+    """lamp_issue_rates validates its output pointer before any device call."""
+    if not os.path.exists(LIB):
+        pytest.skip("liblamp.so not built")
+    lib = ctypes.CDLL(LIB)
+    lib.lamp_issue_rates.restype = ctypes.c_int
+    lib.lamp_issue_rates.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    lib.lamp_last_error.restype = ctypes.c_char_p
+    assert lib.lamp_issue_rates(None, None) == 1
+    assert b"null" in lib.lamp_last_error()
