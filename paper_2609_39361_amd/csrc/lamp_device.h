@@ -87,6 +87,22 @@ __device__ __forceinline__ float rn_e4m11(double y, uint32_t *code)
 
 // Value of an e4m11 code, exact in fp32, without branches: the significand
 // (with its implicit bit for a normal code) scaled by 2^(max(ex, 1) - 18).
+// The same rounding of a finite fp32 value, on its bit pattern (identical to
+// rn_e4m11((double)x)): from 2^-6 on, round to nearest even at bit 12 of the
+// fp32 pattern (a carry moves into the exponent); below, add and subtract
+// 1.5 * 2^6, whose ulp is the subnormal quantum 2^-17; then saturate.
+__device__ __forceinline__ float rn_e4m11_f32(float x, uint32_t *code)
+{
+    const uint32_t b = __builtin_bit_cast(uint32_t, x), sign = b & 0x80000000u, ab = b & 0x7FFFFFFFu;
+    const float ax = __builtin_bit_cast(float, ab);
+    const uint32_t rn = (ab + 0x7FFu + ((ab >> 12) & 1u)) & 0xFFFFF000u;
+    const float as = (ax + 96.0f) - 96.0f;
+    uint32_t r = ab < 0x3C800000u ? __builtin_bit_cast(uint32_t, as) : rn;   // 0x3C800000 = 2^-6
+    r = r < 0x43FFF000u ? r : 0x43FFF000u;                                     // 0x43FFF000 = 511.875
+    *code = (sign >> 16) | (r >= 0x3C800000u ? (r >> 12) - 0x3C000u : (uint32_t)(as * 131072.0f));
+    return __builtin_bit_cast(float, r | sign);
+}
+
 __device__ __forceinline__ float e4m11_value(uint32_t code)
 {
     const uint32_t ex = (code >> 11) & 0xFu, m = code & 0x7FFu;

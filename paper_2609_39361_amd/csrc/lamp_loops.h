@@ -282,8 +282,8 @@ __device__ __forceinline__ void encode16(const float (&acc)[QPL][NKEY], uint32_t
 #pragma unroll
             for (int p = 0; p < NKEY / 2; ++p) {
                 uint32_t x0, x1;
-                (void)rn_e4m11((double)acc[s][2 * p], &x0);
-                (void)rn_e4m11((double)acc[s][2 * p + 1], &x1);
+                (void)rn_e4m11_f32(acc[s][2 * p], &x0);
+                (void)rn_e4m11_f32(acc[s][2 * p + 1], &x1);
                 c[s][p] = x0 | (x1 << 16);
             }
         }
