@@ -175,8 +175,6 @@ def main_decode(args, w, tau):
     """Bench line of the decode form (vector LAMP, Sec. 2, Eq. (6))."""
     import torch
     from paper_2609_39361_amd import lamp, workloads as W
-    if args.flags:
-        raise SystemExit("the decode form takes no flags")
     dev = torch.device("cuda:0")
     q, k, v = W.make_inputs(w)
     qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
@@ -251,11 +249,13 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", type=int, default=3, help="config id (1, 2, 3, 4, 40, 5; 6 decode form)")
-    ap.add_argument("--tau", type=float, default=None)
+    ap.add_argument("--tau", type=str, default=None,
+                    help="threshold, or a comma-separated sweep (one JSON line each, inputs drawn once)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
-    ap.add_argument("--flags", type=int, default=0,
-                    help="variants: 1 first stage off, 2 mu_hat truncation, 4 SIM precision profile")
+    ap.add_argument("--flags", type=str, default="0",
+                    help="variants: 1 first stage off, 2 mu_hat truncation, 4 SIM precision profile; "
+                         "a comma-separated list sweeps them (outer loop)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="before the timed steps, run one plain negating copy of this many MiB "
                          "(fp32 in, fp32 out) to calibrate the HBM byte counters")
@@ -269,9 +269,14 @@ def main():
     from paper_2609_39361_amd import lamp, workloads as W
 
     w = W.CONFIGS[args.workload]
-    tau = w.tau if args.tau is None else args.tau
+    taus = [w.tau] if args.tau is None else [float(x) for x in args.tau.split(",")]
+    flags_list = [int(x) for x in args.flags.split(",")]
     if w.M > 0:
-        return main_decode(args, w, tau)
+        if flags_list != [0]:
+            raise SystemExit("the decode form takes no flags")
+        for tau in taus:
+            main_decode(args, w, tau)
+        return
     dev = torch.device("cuda:0")
     q, k, v = W.make_inputs(w)
     qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
@@ -279,10 +284,6 @@ def main():
     lse = torch.empty((w.B, w.Hq, w.N), dtype=torch.float32, device=dev)
     mask = torch.empty((w.B, w.Hq, -(-w.N // w.bq), -(-w.N // (w.bk * w.nk)) * w.nk), dtype=torch.uint8, device=dev)
     out = (o, lse, mask)
-
-    def step():
-        lamp.attn_fwd(qd, kd, vd, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau, out=out, flags=args.flags)
-
     if args.copy_calib_mib > 0:
         n = args.copy_calib_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device=dev)
@@ -291,6 +292,22 @@ def main():
         torch.neg(src, out=dst)
         torch.cuda.synchronize()
         del src, dst
+    for flags in flags_list:
+        for tau in taus:
+            run_fwd(args, w, tau, flags, (q, k, v), (qd, kd, vd), out, dev)
+
+
+def run_fwd(args, w, tau, flags, host_inputs, dev_inputs, out, dev):
+    """One bench line of the forward pass at threshold tau and variant flags."""
+    import torch
+    from paper_2609_39361_amd import lamp
+    q, k, v = host_inputs
+    qd, kd, vd = dev_inputs
+    o, lse, mask = out
+
+    def step():
+        lamp.attn_fwd(qd, kd, vd, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau, out=out, flags=flags)
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -319,7 +336,7 @@ def main():
     mask_np = mask.cpu().numpy()
     mac8 = 0 if tau == 0 else w.macs
     mac16 = visible_in_mask(w, mask_np) * w.d
-    sim = bool(args.flags & SIM_FLAG)
+    sim = bool(flags & SIM_FLAG)
     issue_floor = None
     if not sim:
         # the multiply-adds alone at the issue rates measured on this device:
@@ -353,7 +370,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "N": w.N, "d": w.d,
                    "causal": w.causal, "window": w.window, "bq": w.bq, "bk": w.bk, "nk": w.nk,
-                   "delta": w.delta, "tau": tau, "flags": args.flags},
+                   "delta": w.delta, "tau": tau, "flags": flags},
         "visible_pair_tflops": 4.0 * w.macs / (ms * 1e-3) / 1e12,   # 4*d per visible (query, key) pair
         "recompute_fraction": st["recompute_fraction"],
         "tile_hist": st["tile_hist"],
@@ -363,7 +380,7 @@ def main():
             "peak": peak,
             "unit": "T VALU lane-ops/s",
             "frac": achieved / peak,
-            "traffic": measured_traffic(w.name, tau, args.flags),
+            "traffic": measured_traffic(w.name, tau, flags),
             "kernel": ("lamp_fwd16_kernel<%d,%d,%d,%s>" % (w.d, w.bq, _mode_of(tau), "true" if sim else "false"))
                       if (w.bk == 16 and w.d >= 128)
                       else ("lamp_fwd_kernel<%d,%d,%d,%d>" % (w.d, w.bq, w.bk, w.nk)),
@@ -373,13 +390,13 @@ def main():
             "ops_per_unit": ("%d per emulated 8-bit MAC, 1 per 16-bit recompute MAC"
                              % (OPS_PER_MAC8_SIM if sim else OPS_PER_MAC8)),
             "algorithmic_frac_one_op_per_mac": (mac8 + mac16) / (kernel_ms * 1e-3) / VALU_LANE_OPS,
-            "valu_issue_frac_counters": measured_valu_issue(w.name, tau, args.flags),
+            "valu_issue_frac_counters": measured_valu_issue(w.name, tau, flags),
             "issue_floor": issue_floor,
         },
         "wall_s_timed_region": wall,
     }
     if not args.no_cpu:
-        result["cpu_baseline"] = cpu_baseline(w, tau, q, k, v, budget_s=args.cpu_budget, flags=args.flags)
+        result["cpu_baseline"] = cpu_baseline(w, tau, q, k, v, budget_s=args.cpu_budget, flags=flags)
     print(json.dumps(result), flush=True)
 
 
