@@ -18,51 +18,62 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // ------------------------------------------------------------------ prepass
-// Row (j) and channel (c) of element i of a [rows][D] matrix per head, in the
-// row layout (blk = 0) or in the grouped layout with blocks of blk rows, each
-// block stored [D/4][blk][4] (one 4-channel group of a block contiguous).
-__device__ __forceinline__ void rc_of(size_t i, int D, int blk, size_t &j, size_t &c)
+// One thread per 4 channels of one row of one head.  u (below rows * D/4)
+// indexes the float4 groups of a head's output in storage order: the row
+// layout (blk = 0) stores [rows][D]; the grouped layout stores blocks of blk
+// rows, each [D/4][blk][4], so that one 4-channel group of a block is
+// contiguous.  Returns the row j and group g of u.
+__device__ __forceinline__ void rg_of(int u, int G, int blk, int &j, int &g)
 {
     if (blk == 0) {
-        c = i % (size_t)D;
-        j = i / (size_t)D;
+        j = u / G;
+        g = u % G;
         return;
     }
-    const size_t per = (size_t)blk * D, r = i % per;
-    j = (i / per) * blk + (r % ((size_t)blk * 4)) / 4;
-    c = (r / ((size_t)blk * 4)) * 4 + r % 4;
+    const int per = blk * G, r = u % per;
+    j = (u / per) * blk + r % blk;
+    g = r / blk;
+}
+
+// 4 bf16 values (8 bytes) as fp32, times s (s = 1: exact conversion)
+__device__ __forceinline__ float4 bf16x4_scaled(const uint16_t *p, float s)
+{
+    const uint2 w = *reinterpret_cast<const uint2 *>(p);
+    return make_float4(bf16_value(w.x & 0xFFFFu) * s, bf16_value(w.x >> 16) * s, bf16_value(w.y & 0xFFFFu) * s,
+                       bf16_value(w.y >> 16) * s);
 }
 
 // Pre-scaled queries q~ = RN32(q * s), rows padded with zeros from N to Nq:
-// qt [B*Hq][Nq][D] from q [B*Hq][N][D] (grouped layout: blk = 64).
+// qt [BH][Nq][D] from q [BH][N][D] (grouped layout: blk = 64).  Grid: x over
+// the float4 groups of a head, y over heads (both grid-stride).
 __global__ void prescale_q_kernel(const uint16_t *__restrict__ q, float *__restrict__ qt, float s, int N, int Nq,
-                                  int D, size_t n, int blk)
+                                  int D, int BH, int blk)
 {
-    size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    size_t stride = (size_t)gridDim.x * blockDim.x;
-    const size_t per = (size_t)Nq * D;
-    for (; i < n; i += stride) {
-        size_t j, c;
-        rc_of(i % per, D, blk, j, c);
-        const size_t bh = i / per;
-        qt[i] = j < (size_t)N ? bf16_value(q[(bh * N + j) * D + c]) * s : 0.0f;
-    }
+    const int G = D / 4, n4 = Nq * G;
+    for (int bh = blockIdx.y; bh < BH; bh += gridDim.y)
+        for (int u = blockIdx.x * blockDim.x + threadIdx.x; u < n4; u += gridDim.x * blockDim.x) {
+            int j, g;
+            rg_of(u, G, blk, j, g);
+            const float4 v = j < N ? bf16x4_scaled(q + ((size_t)bh * N + j) * D + 4 * g, s)
+                                   : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            reinterpret_cast<float4 *>(qt + (size_t)bh * Nq * D)[u] = v;
+        }
 }
 
 // K in fp32 (bf16 -> fp32 is exact), rows padded with zeros from N to Nk:
-// k32 [B*Hkv][Nk][D] from k [B*Hkv][N][D] (grouped layout: blk = 16).
+// k32 [BH][Nk][D] from k [BH][N][D] (grouped layout: blk = 16).
 __global__ void convert_k_kernel(const uint16_t *__restrict__ k, float *__restrict__ k32, int N, int Nk, int D,
-                                 size_t n, int blk)
+                                 int BH, int blk)
 {
-    size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    size_t stride = (size_t)gridDim.x * blockDim.x;
-    const size_t per = (size_t)Nk * D;
-    for (; i < n; i += stride) {
-        size_t j, c;
-        rc_of(i % per, D, blk, j, c);
-        const size_t bh = i / per;
-        k32[i] = j < (size_t)N ? bf16_value(k[(bh * N + j) * D + c]) : 0.0f;
-    }
+    const int G = D / 4, n4 = Nk * G;
+    for (int bh = blockIdx.y; bh < BH; bh += gridDim.y)
+        for (int u = blockIdx.x * blockDim.x + threadIdx.x; u < n4; u += gridDim.x * blockDim.x) {
+            int j, g;
+            rg_of(u, G, blk, j, g);
+            const float4 v = j < N ? bf16x4_scaled(k + ((size_t)bh * N + j) * D + 4 * g, 1.0f)
+                                   : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            reinterpret_cast<float4 *>(k32 + (size_t)bh * Nk * D)[u] = v;
+        }
 }
 
 // V^T [B*Hkv][D][Nk] from V [B*Hkv][N][D] (bf16), keys padded with zeros
@@ -296,22 +307,28 @@ __global__ void selftest_exp_doc_kernel(const double *__restrict__ x, double *__
 }
 
 // ------------------------------------------------------------------ launchers
+// Grid of the prepass kernels: 256-thread blocks over one head's float4
+// groups (x), heads (y); both capped, the kernels stride over the rest.
+static dim3 prepass_grid(int BH, int rows, int D)
+{
+    const long n4 = (long)rows * (D / 4);
+    const long gx = (n4 + 255) / 256;
+    return dim3((unsigned)(gx < 4096 ? (gx > 0 ? gx : 1) : 4096), (unsigned)(BH < 65535 ? (BH > 0 ? BH : 1) : 65535));
+}
+
 hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float *kt32, int B, int Hq, int Hkv,
                           int N, int Nq, int Nk, int D, float scale, hipStream_t s, bool grouped)
 {
-    size_t nq = (size_t)B * Hq * Nq * D, nk = (size_t)B * Hkv * Nk * D;
-    unsigned gq = (unsigned)((nq + 255) / 256 < 65536 ? (nq + 255) / 256 : 65536);
-    unsigned gk = (unsigned)((nk + 255) / 256 < 65536 ? (nk + 255) / 256 : 65536);
-    hipLaunchKernelGGL(prescale_q_kernel, dim3(gq), dim3(256), 0, s, q, qt, scale, N, Nq, D, nq, grouped ? 64 : 0);
-    hipLaunchKernelGGL(convert_k_kernel, dim3(gk), dim3(256), 0, s, k, kt32, N, Nk, D, nk, grouped ? 16 : 0);
+    hipLaunchKernelGGL(prescale_q_kernel, prepass_grid(B * Hq, Nq, D), dim3(256), 0, s, q, qt, scale, N, Nq, D, B * Hq,
+                       grouped ? 64 : 0);
+    hipLaunchKernelGGL(convert_k_kernel, prepass_grid(B * Hkv, Nk, D), dim3(256), 0, s, k, kt32, N, Nk, D, B * Hkv,
+                       grouped ? 16 : 0);
     return hipGetLastError();
 }
 
 hipError_t launch_prescale_q(const uint16_t *q, float *qt, int BH, int rows, int D, float scale, hipStream_t s)
 {
-    size_t n = (size_t)BH * rows * D;
-    unsigned g = (unsigned)((n + 255) / 256 < 65536 ? (n + 255) / 256 : 65536);
-    hipLaunchKernelGGL(prescale_q_kernel, dim3(g), dim3(256), 0, s, q, qt, scale, rows, rows, D, n, 0);
+    hipLaunchKernelGGL(prescale_q_kernel, prepass_grid(BH, rows, D), dim3(256), 0, s, q, qt, scale, rows, rows, D, BH, 0);
     return hipGetLastError();
 }
 
