@@ -57,13 +57,18 @@ __device__ __forceinline__ void emu8_words(uint32_t &a, uint32_t &b, float kv, f
 // in blocks of 16, each block stored [group][row][4], so that one 4-channel
 // group of a block is contiguous: group g of a query row is at 256g, of a key
 // row at 64g, and consecutive keys of a block are 4 apart.
-template <int QS_, int KS_, int KR_>
+// WORDS selects the two-word 8-bit statement (emu8_words) for two query rows
+// per lane: its four fixed temporaries sit at the top of the register file,
+// so it is only for kernels that use the whole file anyway (the pipelined
+// kernel at 128 rows per block, two waves per SIMD).
+template <int QS_, int KS_, int KR_, bool WORDS_>
 struct Lay {
     static constexpr int QS = QS_, KS = KS_, KR = KR_;   // query / key group stride, key row stride
+    static constexpr bool WORDS = WORDS_;
 };
 template <int D>
-using RowLay = Lay<4, 4, D>;
-using GrpLay = Lay<256, 64, 4>;
+using RowLay = Lay<4, 4, D, false>;
+using GrpLay = Lay<256, 64, 4, true>;
 
 // Query rows come either from global memory (const float *) or from LDS
 // (lds_cfptr, so that the loads are ds_read_b128 rather than flat loads).
@@ -106,26 +111,16 @@ __device__ __forceinline__ void emu8_pair(float kv, const float (&q)[QPL], uint3
     }
 }
 
-// Two words of the non-saturating pass at once: the two query rows of a word
-// index (QPL = 2), or words P and P + 1 of one row (QPL = 1).
-template <int QPL, int P>
-__device__ __forceinline__ void emu8_two(float kv, const float (&q)[QPL], uint32_t (&acc)[QPL][8])
-{
-    if constexpr (QPL == 2) {
-        emu8_words<2 * P, 2 * P + 1, 2 * P, 2 * P + 1>(acc[0][P], acc[1][P], kv, q[0], q[1]);
-    } else if constexpr (P % 2 == 0) {
-#pragma unroll
-        for (int s = 0; s < QPL; ++s)
-            emu8_words<2 * P, 2 * P + 1, 2 * P + 2, 2 * P + 3>(acc[s][P], acc[s][P + 1], kv, q[s], q[s]);
-    }
-}
-
-template <int QPL, bool SAT, int... P>
+// One channel of the non-saturating pass over every word: with WORDS and two
+// query rows per lane, the two rows of a word index in one statement
+// (emu8_words); otherwise one pair at a time (emu8_pair).
+template <int QPL, bool SAT, bool WORDS, int... P>
 __device__ __forceinline__ void emu8_channel(float kv, const float (&q)[QPL], uint32_t (&acc)[QPL][8],
                                              std::integer_sequence<int, P...>)
 {
-    if constexpr (SAT || (QPL != 1 && QPL != 2)) (emu8_pair<QPL, SAT, P>(kv, q, acc), ...);
-    else (emu8_two<QPL, P>(kv, q, acc), ...);
+    if constexpr (!SAT && WORDS && QPL == 2)
+        (emu8_words<2 * P, 2 * P + 1, 2 * P, 2 * P + 1>(acc[0][P], acc[1][P], kv, q[0], q[1]), ...);
+    else (emu8_pair<QPL, SAT, P>(kv, q, acc), ...);
 }
 
 // Y8 of one 16-key chunk for QPL query rows of this lane (Sec. 4.1:
@@ -151,7 +146,7 @@ __device__ __forceinline__ void emu8_pass(const QP (&qrow)[QPL], const float *k3
             float q[QPL];
 #pragma unroll
             for (int s = 0; s < QPL; ++s) q[s] = f4_at(q4[s], cc);
-            emu8_channel<QPL, SAT>(f4_at(k4, cc), q, acc, std::make_integer_sequence<int, 8>());
+            emu8_channel<QPL, SAT, LY::WORDS>(f4_at(k4, cc), q, acc, std::make_integer_sequence<int, 8>());
         }
     };
     // steady state, then the last pair of groups without further loads (the
@@ -332,7 +327,7 @@ __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k
             if constexpr (EMU && SIMP)
                 emu8s_channel<QPL>(f4_at(ke, cc), q, e8, std::make_integer_sequence<int, 16>());
             else if constexpr (EMU)
-                emu8_channel<QPL, false>(f4_at(ke, cc), q, a8, std::make_integer_sequence<int, 8>());
+                emu8_channel<QPL, false, LY::WORDS>(f4_at(ke, cc), q, a8, std::make_integer_sequence<int, 8>());
             if constexpr (NKEY > 0)
                 rec16_channel<QPL, NKEY>(f4_at(kr, cc), q, acc, std::make_integer_sequence<int, NKEY>());
         }
