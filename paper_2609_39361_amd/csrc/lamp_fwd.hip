@@ -28,6 +28,7 @@
 //   5. omega, mu update; O^T <- O^T diag(lambda_hat) + V^T E.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <type_traits>
 
 #include "lamp_device.h"
 #include "lamp_kernels.h"
@@ -221,8 +222,11 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                             for (int pp = 0; pp < 8; ++pp) {
                                 const float2 yv = unpk_e4m3(a8[s][pp]);
                                 const int i0 = ck0 + 2 * pp;
-                                if (full || visible(s, i0)) mx[s] = yv.x > mx[s] ? yv.x : mx[s];
-                                if (full || visible(s, i0 + 1)) mx[s] = yv.y > mx[s] ? yv.y : mx[s];
+                                // invisible keys enter as -inf, by selection rather than branches
+                                const float x0 = (full || visible(s, i0)) ? yv.x : NEG_INF;
+                                const float x1 = (full || visible(s, i0 + 1)) ? yv.y : NEG_INF;
+                                mx[s] = x0 > mx[s] ? x0 : mx[s];
+                                mx[s] = x1 > mx[s] ? x1 : mx[s];
                                 packed[pp] = (a8[s][pp] & 0xFFu) | ((a8[s][pp] & 0xFF00u) << 8);
                             }
                             u32x4 *dst = reinterpret_cast<u32x4 *>(ycode + row[s] * YP + c16 * 16);
@@ -410,59 +414,70 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                     continue;
                 }
                 const bool hi16 = prec16 >> th & 1u;
-                for (int ch = 0; ch < CPS; ++ch) {
-                    const int c16 = th * CPS + ch;
-                    const int ck0 = k0 + c16 * 16;
+                // Straight-line per 16-key chunk and row: all codes read, all
+                // table indices formed (an invisible key reads the table's last
+                // entry, whose exponential is 0), all table reads issued, then
+                // the sums, which are exact in fp64 in any order (multiples of
+                // 2^-41 below 2^9).
+                auto run = [&](auto hi_c) {
+                    constexpr bool HI = decltype(hi_c)::value;
+                    for (int ch = 0; ch < CPS; ++ch) {
+                        const int c16 = th * CPS + ch;
+                        const int ck0 = k0 + c16 * 16;
 #pragma unroll
-                    for (int s = 0; s < QPL; ++s) {
-                        u32x4 *rp = reinterpret_cast<u32x4 *>(ycode + row[s] * YP + c16 * 16);
-                        u32x4 *lp = reinterpret_cast<u32x4 *>(ylo + row[s] * YP + c16 * 16);
-                        if (ck0 > vhi[s] || ck0 + 15 < vlo[s]) {
-                            rp[0] = u32x4{0u, 0u, 0u, 0u};
-                            rp[1] = u32x4{0u, 0u, 0u, 0u};
-                            if (hi16) {
-                                lp[0] = u32x4{0u, 0u, 0u, 0u};
-                                lp[1] = u32x4{0u, 0u, 0u, 0u};
-                            }
-                            continue;
-                        }
-                        const u32x4 c0 = rp[0], c1 = rp[1];
-                        const uint32_t in[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
-                        uint32_t outw[8], outl[8];
+                        for (int s = 0; s < QPL; ++s) {
+                            u32x4 *rp = reinterpret_cast<u32x4 *>(ycode + row[s] * YP + c16 * 16);
+                            u32x4 *lp = reinterpret_cast<u32x4 *>(ylo + row[s] * YP + c16 * 16);
+                            const u32x4 c0 = rp[0], c1 = rp[1];
+                            const uint32_t in[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
+                            uint32_t eb[16];
 #pragma unroll
-                        for (int pp = 0; pp < 8; ++pp) {
-                            uint32_t res = 0, rlo = 0;
-#pragma unroll
-                            for (int t = 0; t < 2; ++t) {
-                                const int key = ck0 + 2 * pp + t;
-                                const uint32_t yc = (in[pp] >> (16 * t)) & 0xFFFFu;
-                                uint32_t eh = 0, el = 0;
-                                float ev = 0.0f;
-                                if (visible(s, key)) {
-                                    if (hi16) {
-                                        ev = ue5m11e_value(p.exp16[ue5m11_code(shift_of(muh[s], e4m11_value(yc)))]);
-                                        split_bf16(ev, eh, el);
-                                    } else {
-                                        eh = lut[ue5m3_code(shift_of(mu8[s], e4m3_value(yc)))];
-                                        ev = bf16_value(eh);
-                                    }
+                            for (int i = 0; i < 16; ++i) {
+                                const uint32_t yc = (in[i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+                                const bool vis = visible(s, ck0 + i);
+                                if constexpr (HI) {
+                                    const uint32_t x = ue5m11_code(shift_of(muh[s], e4m11_value(yc)));
+                                    eb[i] = p.exp16[vis ? x : 65535u];
+                                } else {
+                                    const float y = (i & 1) ? __builtin_amdgcn_cvt_f32_fp8((int)in[i >> 1], 2)
+                                                            : __builtin_amdgcn_cvt_f32_fp8((int)in[i >> 1], 0);
+                                    const uint32_t x = ue5m3_code(shift_of(mu8[s], y));
+                                    eb[i] = lut[vis ? x : 255u];
                                 }
-                                sp[s] += (double)ev;   // exact: multiples of 2^-41 below 2^9
-                                if (!hi16) spF[s] += (double)ev;
-                                res |= eh << (16 * t);
-                                rlo |= el << (16 * t);
                             }
-                            outw[pp] = res;
-                            outl[pp] = rlo;
-                        }
-                        rp[0] = u32x4{outw[0], outw[1], outw[2], outw[3]};
-                        rp[1] = u32x4{outw[4], outw[5], outw[6], outw[7]};
-                        if (hi16) {
-                            lp[0] = u32x4{outl[0], outl[1], outl[2], outl[3]};
-                            lp[1] = u32x4{outl[4], outl[5], outl[6], outl[7]};
+                            double a4[4] = {0.0, 0.0, 0.0, 0.0};
+                            uint32_t eh[16], el[16];
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) {
+                                float ev;
+                                if constexpr (HI) {
+                                    ev = ue5m11e_value(eb[i]);
+                                    split_bf16(ev, eh[i], el[i]);
+                                } else {
+                                    eh[i] = eb[i];
+                                    el[i] = 0u;
+                                    ev = bf16_value(eb[i]);
+                                }
+                                a4[i & 3] += (double)ev;
+                            }
+                            const double ts = (a4[0] + a4[1]) + (a4[2] + a4[3]);
+                            sp[s] += ts;
+                            if constexpr (!HI) spF[s] += ts;
+                            rp[0] = u32x4{eh[0] | eh[1] << 16, eh[2] | eh[3] << 16, eh[4] | eh[5] << 16,
+                                          eh[6] | eh[7] << 16};
+                            rp[1] = u32x4{eh[8] | eh[9] << 16, eh[10] | eh[11] << 16, eh[12] | eh[13] << 16,
+                                          eh[14] | eh[15] << 16};
+                            if constexpr (HI) {
+                                lp[0] = u32x4{el[0] | el[1] << 16, el[2] | el[3] << 16, el[4] | el[5] << 16,
+                                              el[6] | el[7] << 16};
+                                lp[1] = u32x4{el[8] | el[9] << 16, el[10] | el[11] << 16, el[12] | el[13] << 16,
+                                              el[14] | el[15] << 16};
+                            }
                         }
                     }
-                }
+                };
+                if (hi16) run(std::true_type());
+                else run(std::false_type());
             }
 #pragma unroll
             for (int s = 0; s < QPL; ++s) {
