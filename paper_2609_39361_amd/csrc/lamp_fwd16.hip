@@ -364,13 +364,9 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
         rec16_keys<D, QPL, 4, SIMP, GrpLay>(qrow, krow_of(key0 + (lane & 3)), yc);
         fn(key0, yc);
     };
-    // exponentials: 8-bit from the LDS table, 16-bit from the table in global
-    // memory as bf16 high / low parts (SIM: high / low halves of the FP32
-    // pattern) and the value
-    auto e8_of = [&](float m8ref, uint32_t yc) -> uint32_t {
-        if constexpr (SIMP) return lut[sim_shift_index<3, SIM8_EMIN, SIM8_EMAX>(m8ref, bf16_value(yc))];
-        else return lut[ue5m3_code(shift_of(m8ref, e4m3_value(yc)))];
-    };
+    // a 16-bit exponential from the table in global memory as bf16 high / low
+    // parts (SIM: high / low halves of the FP32 pattern) and the value (the
+    // 8-bit ones are formed inline in the exponential phase)
     auto e16_of = [&](float mref, float y, uint32_t &eh, uint32_t &el) -> float {
         if constexpr (SIMP) {
             const uint32_t eb = p.sim16[sim_shift_index<11, SIM16_EMIN, SIM16_EMAX>(mref, y)];
