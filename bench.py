@@ -337,20 +337,20 @@ def run_fwd(args, w, tau, flags, host_inputs, dev_inputs, out, dev):
     mac8 = 0 if tau == 0 else w.macs
     mac16 = visible_in_mask(w, mask_np) * w.d
     sim = bool(flags & SIM_FLAG)
-    issue_floor = None
-    if not sim:
-        # the multiply-adds alone at the issue rates measured on this device:
-        # one emulated 8-bit step is two multiply-adds per lane (128 per
-        # wave), one 16-bit FMA with its broadcast key one per lane
-        rates = lamp.issue_rates()
-        simds = 4 * torch.cuda.get_device_properties(dev).multi_processor_count
-        floor_ms = (mac8 / 128.0 * rates["emulated_step"] + mac16 / 64.0 * rates["fmac_f32_dpp"]) / simds * 1e-6
-        issue_floor = {
-            "ms": floor_ms, "frac": floor_ms / kernel_ms,
-            "ns_per_wave_instruction_per_simd": rates,
-            "counts": "emulated 8-bit steps of every visible logit and 16-bit FMAs of the recomputed sub-blocks "
-                      "(not the speculative ones); exponentials, stage logic and P.V not included",
-        }
+    # the multiply-adds alone at the issue rates measured on this device: one
+    # emulated 8-bit step is two multiply-adds per lane (128 per wave), one
+    # SIM step one (64 per wave), one 16-bit FMA with its broadcast key one
+    rates = lamp.issue_rates()
+    simds = 4 * torch.cuda.get_device_properties(dev).multi_processor_count
+    step8 = rates["emulated_step_sim"] / 64.0 if sim else rates["emulated_step"] / 128.0
+    floor_ms = (mac8 * step8 + mac16 / 64.0 * rates["fmac_f32_dpp"]) / simds * 1e-6
+    issue_floor = {
+        "ms": floor_ms, "frac": floor_ms / kernel_ms,
+        "ns_per_wave_instruction_per_simd": rates,
+        "counts": "emulated 8-bit steps (%s) of every visible logit and 16-bit FMAs of the recomputed sub-blocks "
+                  "(not the speculative ones); exponentials, stage logic and P.V not included"
+                  % ("SIM profile" if sim else "hardware formats"),
+    }
     alg_ops = (OPS_PER_MAC8_SIM if sim else OPS_PER_MAC8) * mac8 + OPS_PER_MAC16 * mac16
     achieved = alg_ops / (kernel_ms * 1e-3) / 1e12
     peak = VALU_LANE_OPS / 1e12

@@ -194,11 +194,13 @@ int lamp_timing_read(int *launches, double *fwd_ms, double *prepass_ms);
  * Issue rates of the VALU instructions the logit loops are made of, measured
  * on the current device, for the benchmark's instruction-mix floor of the
  * forward kernel (which is bound by VALU issue).  ns_per_simd (HOST memory,
- * 5 entries) receives the nanoseconds one SIMD spends per wave-instruction
+ * 6 entries) receives the nanoseconds one SIMD spends per wave-instruction
  * of: [0] an fp32 FMA on VGPR operands, [1] an fp32 FMA reading its first
  * operand through a DPP row broadcast, [2] a packed e4m3 -> fp32 decode,
- * [3] a packed fp32 -> e4m3 rounding, and [4] per emulated step of the 8-bit
- * loop (decode, two broadcast FMAs, rounding: two multiply-adds per lane).
+ * [3] a packed fp32 -> e4m3 rounding, [4] per emulated step of the 8-bit
+ * loop (decode, two broadcast FMAs, rounding: two multiply-adds per lane),
+ * and [5] per emulated step of the SIM profile's 8-bit loop (a broadcast FMA
+ * and the 3-instruction rounding of the FP32 pattern: one multiply-add).
  * Each kind runs 16 independent chains per lane at 8 waves per SIMD.  The
  * call allocates a small device buffer, runs on `stream` and waits for it;
  * it takes a few milliseconds.

@@ -71,7 +71,7 @@ hipError_t launch_transpose_v(const uint16_t *v, uint16_t *vt, int B, int Hkv, i
 
 // Issue rates of the logit loops' instructions (lamp_rates.hip): ns per
 // wave-instruction (per emulated step for RATE_STEP) per SIMD, into ns[RATE_N].
-enum { RATE_FMAC = 0, RATE_FMAC_DPP = 1, RATE_DECODE = 2, RATE_ENCODE = 3, RATE_STEP = 4, RATE_N = 5 };
+enum { RATE_FMAC = 0, RATE_FMAC_DPP = 1, RATE_DECODE = 2, RATE_ENCODE = 3, RATE_STEP = 4, RATE_STEP_SIM = 5, RATE_N = 6 };
 hipError_t measure_issue_rates(double *ns, hipStream_t s);
 // grouped: the layout of the pipelined kernel (queries in 64-row and keys in
 // 16-row blocks, each block stored [D/4][rows][4]); otherwise [rows][D].

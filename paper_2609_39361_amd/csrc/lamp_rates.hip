@@ -126,6 +126,34 @@ __global__ __launch_bounds__(256) void rate_step_kernel(float *out, int iters, f
     out[blockIdx.x * blockDim.x + threadIdx.x] = (float)s;
 }
 
+// the emulated step of the SIM profile's 8-bit loop: one broadcast FMA and
+// the round-to-nearest-even of the FP32 pattern to 3 mantissa bits (last kept
+// bit extracted, one 3-input add, one mask), per multiply-add
+__global__ __launch_bounds__(256) void rate_step_sim_kernel(float *out, int iters, float q)
+{
+    float a[16];
+    const float k = (float)threadIdx.x * 1e-3f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) a[i] = (float)i * 1e-3f;
+    asm volatile("s_nop 4");
+    for (int it = 0; it < iters; ++it) {
+#define LAMP_F(i)                                                                                     \
+    asm volatile("v_fmac_f32_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf\n\t"           \
+                 "v_bfe_u32 v40, %0, 20, 1\n\t"                                                      \
+                 "v_add3_u32 %0, %0, v40, %4\n\t"                                                    \
+                 "v_and_b32 %0, %5, %0"                                                              \
+                 : "+v"(a[i])                                                                        \
+                 : "v"(k), "v"(q), "n"(i), "v"(0x7FFFFu), "v"(0xFFF00000u)                           \
+                 : "v40");
+        LAMP_REP16(LAMP_F)
+#undef LAMP_F
+    }
+    float s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s += a[i];
+    out[blockIdx.x * blockDim.x + threadIdx.x] = s;
+}
+
 #undef LAMP_REP16
 
 } // namespace
@@ -143,9 +171,9 @@ hipError_t measure_issue_rates(double *ns, hipStream_t s)
     if (e != hipSuccess) return e;
     hipEvent_t e0 = nullptr, e1 = nullptr;
     void (*kern[RATE_N])(float *, int, float) = {rate_fmac_kernel, rate_fmac_dpp_kernel, rate_decode_kernel,
-                                                 rate_encode_kernel, rate_step_kernel};
+                                                 rate_encode_kernel, rate_step_kernel, rate_step_sim_kernel};
     if ((e = hipEventCreate(&e0)) == hipSuccess && (e = hipEventCreate(&e1)) == hipSuccess) {
-        // instructions (steps for the last kind) per SIMD of one launch
+        // instructions (steps for the last two kinds) per SIMD of one launch
         const double per_simd = (double)blocks * (threads / 64) * iters * 16 / ((double)cus * 4);
         for (int i = 0; i < RATE_N && e == hipSuccess; ++i) {
             hipLaunchKernelGGL(kern[i], dim3(blocks), dim3(threads), 0, s, out, 64, 1.0f);   // warm-up

@@ -263,13 +263,15 @@ def timing_read():
     return n.value, tf.value, tp.value
 
 
-ISSUE_RATE_KINDS = ("fmac_f32", "fmac_f32_dpp", "cvt_pk_f32_fp8", "cvt_pk_fp8_f32", "emulated_step")
+ISSUE_RATE_KINDS = ("fmac_f32", "fmac_f32_dpp", "cvt_pk_f32_fp8", "cvt_pk_fp8_f32", "emulated_step",
+                    "emulated_step_sim")
 
 
 def issue_rates():
     """Nanoseconds per wave-instruction per SIMD of the logit loops'
-    instructions on the current device (dict keyed by ISSUE_RATE_KINDS; the
-    last is one emulated 8-bit step, two multiply-adds per lane)."""
+    instructions on the current device (dict keyed by ISSUE_RATE_KINDS;
+    emulated_step is one step of the 8-bit loop, two multiply-adds per lane,
+    emulated_step_sim one of the SIM profile's, one multiply-add)."""
     ns = (ctypes.c_double * len(ISSUE_RATE_KINDS))()
     _check(lib().lamp_issue_rates(ns, _stream(torch.device("cuda", torch.cuda.current_device()))))
     return dict(zip(ISSUE_RATE_KINDS, list(ns)))
