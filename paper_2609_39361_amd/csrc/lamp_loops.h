@@ -70,6 +70,16 @@ template <int D>
 using RowLay = Lay<4, 4, D, false>;
 using GrpLay = Lay<256, 64, 4, true>;
 
+// Two wait states that nothing is scheduled across.  The register allocator
+// may copy a loaded key register with a VALU move where a loop is entered or
+// left (to line up the loop-carried buffers); placed at the top of every loop
+// over channel groups and after it, this keeps each DPP read of a key at least
+// two wait states behind such a copy.  The build check verifies the result.
+__device__ __forceinline__ void dpp_guard()
+{
+    asm volatile("s_nop 1");
+}
+
 // Query rows come either from global memory (const float *) or from LDS
 // (lds_cfptr, so that the loads are ds_read_b128 rather than flat loads).
 typedef const __attribute__((address_space(3))) float *lds_cfptr;
@@ -153,12 +163,14 @@ __device__ __forceinline__ void emu8_pass(const QP (&qrow)[QPL], const float *k3
     // offsets stay affine in c, so they fold into the loads' immediates)
     load_group<QPL, LY>(krow, qrow, 0, ka, qa);
     for (int c = 0; c < D - 8; c += 8) {
+        dpp_guard();
         load_group<QPL, LY>(krow, qrow, c + 4, kb, qb);
         run(ka, qa);
         load_group<QPL, LY>(krow, qrow, c + 8, ka, qa);
         run(kb, qb);
     }
     load_group<QPL, LY>(krow, qrow, D - 4, kb, qb);
+    dpp_guard();
     run(ka, qa);
     run(kb, qb);
 }
@@ -240,12 +252,14 @@ __device__ __forceinline__ void emu8s_pass(const QP (&qrow)[QPL], const float *k
     };
     load_group<QPL, LY>(krow, qrow, 0, ka, qa);
     for (int c = 0; c < D - 8; c += 8) {
+        dpp_guard();
         load_group<QPL, LY>(krow, qrow, c + 4, kb, qb);
         run(ka, qa);
         load_group<QPL, LY>(krow, qrow, c + 8, ka, qa);
         run(kb, qb);
     }
     load_group<QPL, LY>(krow, qrow, D - 4, kb, qb);
+    dpp_guard();
     run(ka, qa);
     run(kb, qb);
 #pragma unroll
@@ -334,12 +348,14 @@ __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k
     };
     ld(0, kea, kra, qa);
     for (int c = 0; c < D - 8; c += 8) {
+        dpp_guard();
         ld(c + 4, keb, krb, qb);
         run(kea, kra, qa);
         ld(c + 8, kea, kra, qa);
         run(keb, krb, qb);
     }
     ld(D - 4, keb, krb, qb);
+    dpp_guard();
     run(kea, kra, qa);
     run(keb, krb, qb);
     if constexpr (EMU && SIMP) {
@@ -402,12 +418,14 @@ __device__ __forceinline__ void rec16_keys(const QP (&qrow)[QPL], const float *k
 #pragma unroll
     for (int r = 0; r < PD; ++r) load_group<QPL, LY>(krow, qrow, 4 * r, kb[r], qb[r]);
     for (int c = 0; c < D - 4 * PD; c += 4 * PD) {
+        dpp_guard();
 #pragma unroll
         for (int r = 0; r < PD; ++r) {
             run(r);
             load_group<QPL, LY>(krow, qrow, c + 4 * (r + PD), kb[r], qb[r]);
         }
     }
+    dpp_guard();
 #pragma unroll
     for (int r = 0; r < PD; ++r) run(r);   // the last ring, no further loads
     encode16<SIMP>(acc, codes);
