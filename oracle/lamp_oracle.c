@@ -475,6 +475,113 @@ static double logit16_sim(const float *qt, const uint16_t *k, int d)
     return round_sim((double)acc, 11);
 }
 
+/* ------------------------------------------------------------------------ */
+/* Stochastic rounding of the 8-bit accumulation.                            */
+/* ------------------------------------------------------------------------ */
+/* Sec. 3.3 ("Floating-point formats") names stochastic rounding (Croci et al.
+ * 2022) as the alternative to round-to-nearest for the e4m3 accumulation, to
+ * counter swamping.  The paper fixes neither the generator nor the number of
+ * random bits; the readings taken:
+ *   - each step rounds the FP32 FMA result t (as in the round-to-nearest
+ *     recursion) to one of its two e4m3 neighbours: a = min(|t|, 448), lo the
+ *     e4m3 number next to a toward zero, u = 2^(max(e, -6) - 3) its spacing
+ *     (e the binary exponent of a); the result is lo + u when
+ *     floor(2^20 (a - lo) / u) + r >= 2^20 and lo otherwise, with the sign of
+ *     t (saturating at 448, as the round-to-nearest recursion; a zero keeps
+ *     the sign of t).  r is a uniform 20-bit integer, so the probability of
+ *     rounding away from zero is the distance to lo in units of u, cut to
+ *     20 bits (exact for a normal-range a, whose FP32 pattern has 20 bits below
+ *     e4m3's last mantissa bit);
+ *   - r comes from the counter-based generator Philox4x64-10 (Salmon, Moraes,
+ *     Dror and Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC 2011),
+ *     key (seed, 0), counter (j, i, b*Hq + h, c / 8) for query row j, key i,
+ *     query head h of batch b and channel c: the four 64-bit words of one
+ *     call cut into eight 32-bit halves (low half first), the half of
+ *     channel c being number c mod 8, r its top 20 bits.  The numbers depend
+ *     on the logit and the channel alone, not on any blocking. */
+
+/* (hi, lo) = a * b, full 128-bit product. */
+static void mulhilo64(uint64_t a, uint64_t b, uint64_t *hi, uint64_t *lo)
+{
+    unsigned __int128 p = (unsigned __int128)a * b;
+    *hi = (uint64_t)(p >> 64);
+    *lo = (uint64_t)p;
+}
+
+/* Philox4x64-10 of counter c under key k (SC 2011: the 4x64 round with
+ * multipliers M0, M1 and Weyl key increments W0, W1; ten rounds, the first
+ * with the key as given). */
+void oracle_philox4x64_10(const uint64_t c_in[4], const uint64_t k_in[2], uint64_t out[4])
+{
+    const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+    const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+    uint64_t c0 = c_in[0], c1 = c_in[1], c2 = c_in[2], c3 = c_in[3];
+    uint64_t k0 = k_in[0], k1 = k_in[1];
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) { k0 += W0; k1 += W1; }
+        uint64_t hi0, lo0, hi1, lo1;
+        mulhilo64(M0, c0, &hi0, &lo0);
+        mulhilo64(M1, c2, &hi1, &lo1);
+        uint64_t n0 = hi1 ^ c1 ^ k0, n1 = lo1, n2 = hi0 ^ c3 ^ k1, n3 = lo0;
+        c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* Stochastic rounding of t to e4m3 with the 20-bit random integer r (above). */
+static double sr_e4m3(double t, uint32_t r)
+{
+    double a = fabs(t);
+    if (a > F_E4M3.maxval) a = F_E4M3.maxval;
+    int E;
+    (void)frexp(a, &E);                 /* a = f 2^E, f in [1/2, 1); a = 0: E = 0 */
+    int e = E - 1;
+    int emin = 1 - F_E4M3.bias;
+    if (e < emin) e = emin;
+    double u = ldexp(1.0, e - F_E4M3.mbits);
+    double lo = floor(a / u) * u;
+    double frac20 = floor((a - lo) / u * 1048576.0);
+    double res = (frac20 + (double)r >= 1048576.0) ? lo + u : lo;
+    return copysign(res, t);
+}
+
+int oracle_sr_e4m3(const double *t, const uint32_t *r, double *y, int64_t n)
+{
+    for (int64_t i = 0; i < n; ++i) {
+        if (r[i] >= (1u << 20)) return -1;
+        y[i] = sr_e4m3(t[i], r[i]);
+    }
+    return 0;
+}
+
+/* 20-bit random integer of channel c of the logit (j, i) of head bh. */
+static uint32_t sr_bits(uint64_t seed, int64_t bh, int64_t j, int64_t i, int c, uint64_t w[4], int *have)
+{
+    if (c % 8 == 0 || !*have) {
+        const uint64_t ctr[4] = {(uint64_t)j, (uint64_t)i, (uint64_t)bh, (uint64_t)(c / 8)};
+        const uint64_t key[2] = {seed, 0};
+        oracle_philox4x64_10(ctr, key, w);
+        *have = 1;
+    }
+    const uint64_t word = w[(c % 8) / 2];
+    const uint32_t half = (c % 2) ? (uint32_t)(word >> 32) : (uint32_t)word;
+    return half >> 12;
+}
+
+/* Low-precision logit with stochastic rounding: the recursion of logit8 with
+ * sr_e4m3 in place of round-to-nearest. */
+static double logit8_sr(const float *qt, const uint16_t *k, int d, uint64_t seed, int64_t bh, int64_t j, int64_t i)
+{
+    float acc = 0.0f;
+    uint64_t w[4];
+    int have = 0;
+    for (int c = 0; c < d; ++c) {
+        float t = fmaf(qt[c], bf16_to_f32(k[c]), acc);
+        acc = (float)sr_e4m3((double)t, sr_bits(seed, bh, j, i, c, w, &have));
+    }
+    return (double)acc;
+}
+
 static int visible(int64_t i, int64_t j, int causal, int window)
 {
     if (causal && i > j) return 0;
@@ -505,6 +612,33 @@ int oracle_logits8(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv,
                 for (int64_t i = 0; i < N; ++i) {
                     if (!visible(i, j, causal, window)) { o[i] = 0xFF; continue; }
                     o[i] = (uint8_t)encode_fmt(logit8(qt, kb + i * d, d), &F_E4M3);
+                }
+            }
+    return 0;
+}
+
+/* Y8 codes with stochastic rounding (seed above), same layout. */
+int oracle_logits8_sr(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv, int N, int d,
+                      int causal, int window, int row0, int nrows, uint64_t seed, uint8_t *out, int nthreads)
+{
+    if (Hq % Hkv) return -1;
+    int G = Hq / Hkv;
+    float s = scale_of(d);
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for collapse(3) schedule(dynamic)
+#endif
+    for (int b = 0; b < B; ++b)
+        for (int h = 0; h < Hq; ++h)
+            for (int r = 0; r < nrows; ++r) {
+                int64_t j = row0 + r;
+                float qt[1024];
+                prescale(q + (((int64_t)b * Hq + h) * N + j) * d, d, s, qt);
+                const uint16_t *kb = k + ((int64_t)b * Hkv + h / G) * N * d;
+                uint8_t *o = out + (((int64_t)b * Hq + h) * nrows + r) * N;
+                for (int64_t i = 0; i < N; ++i) {
+                    if (!visible(i, j, causal, window)) { o[i] = 0xFF; continue; }
+                    o[i] = (uint8_t)encode_fmt(logit8_sr(qt, kb + i * d, d, seed, (int64_t)b * Hq + h, j, i), &F_E4M3);
                 }
             }
     return 0;
@@ -580,8 +714,10 @@ enum { MASK_LOW = 0, MASK_STAGE1 = 1, MASK_STAGE2 = 2, MASK_INACTIVE = 3 };
  *    dropping the low mantissa bits).
  * Both apply for 0 < tau < inf; the two end modes ignore them.
  *  ORACLE_SIM: the "SIM" precision profile above (Sec. 4.1) in place of the
- *    hardware formats of Sec. 3.3, in every mode. */
-enum { ORACLE_STAGE1_OFF = 1, ORACLE_MU_TRUNC = 2, ORACLE_SIM = 4 };
+ *    hardware formats of Sec. 3.3, in every mode;
+ *  ORACLE_SR8: the 8-bit logits rounded stochastically (logit8_sr, with the
+ *    seed argument), in the modes that compute them; not with ORACLE_SIM. */
+enum { ORACLE_STAGE1_OFF = 1, ORACLE_MU_TRUNC = 2, ORACLE_SIM = 4, ORACLE_SR8 = 8 };
 
 /* x truncated (rounded toward zero) to e4m3; reading: values beyond the
  * largest e4m3 number saturate to +-448; infinities are kept. */
@@ -625,6 +761,7 @@ typedef struct {
     int B, Hq, Hkv, N, d, causal, window, bq, bk, nk;
     double delta, tau;
     unsigned flags;
+    uint64_t seed;
     double *o, *lse;
     uint8_t *mask;
 } fwd_args_t;
@@ -651,6 +788,8 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
     const int stage1_off = !pure8 && !all16 && (A->flags & ORACLE_STAGE1_OFF);
     const int mu_trunc = !pure8 && !all16 && (A->flags & ORACLE_MU_TRUNC);
     const int sim = (A->flags & ORACLE_SIM) != 0;
+    const int sr8 = (A->flags & ORACLE_SR8) != 0;
+    const int64_t bh = (int64_t)b * A->Hq + h;
     double (*const y8f)(const float *, const uint16_t *, int) = sim ? logit8_sim : logit8;
     double (*const y16f)(const float *, const uint16_t *, int) = sim ? logit16_sim : logit16;
     double (*const expf_)(double, double, int) = sim ? shifted_exp_sim : shifted_exp;
@@ -703,7 +842,8 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
             for (int ii = 0; ii < T; ++ii)
                 for (int j = 0; j < bq; ++j)
                     Y[(size_t)ii * bq + j] = vis[(size_t)ii * bq + j]
-                        ? y8f(qt + (size_t)j * d, kbase + (k0 + ii) * d, d) : NAN;
+                        ? (sr8 ? logit8_sr(qt + (size_t)j * d, kbase + (k0 + ii) * d, d, A->seed, bh, q0 + j, k0 + ii)
+                               : y8f(qt + (size_t)j * d, kbase + (k0 + ii) * d, d)) : NAN;
         }
         /* Column maxima per sub-block: m8[theta][j] (Sec. 3.1, C and T). */
         for (int th = 0; th < nk; ++th)
@@ -905,21 +1045,22 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
  * (b*Hq + h)*ceil(N/bq) + qb) are computed; other outputs are left untouched.
  * Returns 0, or -1 on invalid arguments / -2 on a table failure or, in the SIM
  * profile, an exponential too close to a rounding midpoint to be certified. */
-int lamp_oracle_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
-                    int B, int Hq, int Hkv, int N, int d, int causal, int window,
-                    int bq, int bk, int nk, double delta, double tau, unsigned flags,
-                    double *o, double *lse, uint8_t *mask,
-                    const int64_t *qblocks, int64_t nqblocks, int nthreads)
+int lamp_oracle_fwd_seeded(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                           int B, int Hq, int Hkv, int N, int d, int causal, int window,
+                           int bq, int bk, int nk, double delta, double tau, unsigned flags, uint64_t seed,
+                           double *o, double *lse, uint8_t *mask,
+                           const int64_t *qblocks, int64_t nqblocks, int nthreads)
 {
     if (B < 0 || Hq <= 0 || Hkv <= 0 || N < 0 || d <= 0 || d > 1024) return -1;
     if (Hq % Hkv || bq <= 0 || bk <= 0 || nk <= 0 || nk > 16) return -1;
     if (window < 0 || (window > 0 && !causal)) return -1;
     if (!(tau >= 0.0) || !(delta >= 0.0)) return -1;
     if (build_tables()) return -2;
-    if (flags & ~(unsigned)(ORACLE_STAGE1_OFF | ORACLE_MU_TRUNC | ORACLE_SIM)) return -1;
+    if (flags & ~(unsigned)(ORACLE_STAGE1_OFF | ORACLE_MU_TRUNC | ORACLE_SIM | ORACLE_SR8)) return -1;
+    if ((flags & ORACLE_SR8) && (flags & ORACLE_SIM)) return -1;
     if (B == 0 || N == 0) return 0;                /* nothing to compute */
     g_sim_fail = 0;
-    fwd_args_t A = {q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, flags, o, lse, mask};
+    fwd_args_t A = {q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, flags, seed, o, lse, mask};
     const int nqbh = (N + bq - 1) / bq;
     int64_t nqb = (int64_t)B * Hq * nqbh;
     int64_t count = qblocks ? nqblocks : nqb;
@@ -935,6 +1076,17 @@ int lamp_oracle_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
         fwd_qblock(&A, b, h, qb);
     }
     return g_sim_fail ? -2 : 0;
+}
+
+/* lamp_oracle_fwd: the above with seed 0 (ORACLE_SR8 takes the seeded form). */
+int lamp_oracle_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                    int B, int Hq, int Hkv, int N, int d, int causal, int window,
+                    int bq, int bk, int nk, double delta, double tau, unsigned flags,
+                    double *o, double *lse, uint8_t *mask,
+                    const int64_t *qblocks, int64_t nqblocks, int nthreads)
+{
+    return lamp_oracle_fwd_seeded(q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, flags, 0,
+                                  o, lse, mask, qblocks, nqblocks, nthreads);
 }
 
 /* ------------------------------------------------------------------------ */

@@ -40,6 +40,15 @@ def lib():
         _lib.oracle_trunc_e4m3.argtypes = [f64]
         _lib.oracle_trunc_e4m3.restype = f64
         _lib.lamp_oracle_fwd.restype = i32
+        _lib.lamp_oracle_fwd_seeded.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32,
+                                                f64, f64, ctypes.c_uint, ctypes.c_uint64, P, P, P, P, i64, i32]
+        _lib.lamp_oracle_fwd_seeded.restype = i32
+        _lib.oracle_philox4x64_10.argtypes = [P, P, P]
+        _lib.oracle_philox4x64_10.restype = None
+        _lib.oracle_sr_e4m3.argtypes = [P, P, P, i64]
+        _lib.oracle_sr_e4m3.restype = i32
+        _lib.oracle_logits8_sr.argtypes = [P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32, ctypes.c_uint64, P, i32]
+        _lib.oracle_logits8_sr.restype = i32
         for name in ("oracle_logits8", "oracle_logits16"):
             fn = getattr(_lib, name)
             fn.argtypes = [P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, i32]
@@ -154,6 +163,40 @@ def logits8(q, k, causal, window, row0, nrows, nthreads=0):
     return out
 
 
+def philox4x64_10(counter, key):
+    """Philox4x64-10 (Salmon et al., SC 2011) of one counter (4 words) under key (2 words)."""
+    c = np.ascontiguousarray(counter, dtype=np.uint64)
+    kk = np.ascontiguousarray(key, dtype=np.uint64)
+    assert c.shape == (4,) and kk.shape == (2,)
+    out = np.empty(4, dtype=np.uint64)
+    lib().oracle_philox4x64_10(_ptr(c), _ptr(kk), _ptr(out))
+    return out
+
+
+def sr_e4m3(t, r):
+    """Stochastic rounding of values t to e4m3 with 20-bit random integers r (fp64 results)."""
+    t = np.ascontiguousarray(t, dtype=np.float64)
+    r = np.ascontiguousarray(np.broadcast_to(r, t.shape), dtype=np.uint32)
+    y = np.empty_like(t)
+    rc = lib().oracle_sr_e4m3(_ptr(t), _ptr(r), _ptr(y), t.size)
+    if rc != 0:
+        raise ValueError("random integers must lie in [0, 2^20)")
+    return y
+
+
+def logits8_sr(q, k, causal, window, row0, nrows, seed, nthreads=0):
+    """e4m3 codes of the 8-bit logits with stochastic rounding, layout of logits8."""
+    q = np.ascontiguousarray(q, dtype=np.uint16)
+    k = np.ascontiguousarray(k, dtype=np.uint16)
+    B, Hq, N, d = q.shape
+    Hkv = k.shape[1]
+    out = np.empty((B, Hq, nrows, N), dtype=np.uint8)
+    rc = lib().oracle_logits8_sr(_ptr(q), _ptr(k), B, Hq, Hkv, N, d, int(causal), int(window),
+                                 row0, nrows, int(seed), _ptr(out), nthreads)
+    assert rc == 0
+    return out
+
+
 def logits16(q, k, causal, window, row0, nrows, nthreads=0):
     """e4m11 codes of the 16-bit logits, same layout; invisible entries hold 0xFFFF."""
     q = np.ascontiguousarray(q, dtype=np.uint16)
@@ -216,19 +259,22 @@ def logits_sim(q, k, causal, window, row0, nrows, high, nthreads=0):
 STAGE1_OFF = 1   # the first stage disabled: mu_hat from the 8-bit maxima, stage 2 alone recomputes
 MU_TRUNC = 2     # 8-bit shifts against mu_hat truncated to e4m3 (SIM: to 3 mantissa bits)
 SIM = 4          # the "SIM" precision profile (FP32 range, 3/11-bit mantissas, no saturation)
+SR8 = 8          # the 8-bit accumulation rounded stochastically (seeded Philox4x64-10 bits)
 
 
 def trunc_e4m3(x):
     return lib().oracle_trunc_e4m3(float(x))
 
 
-def fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, qblocks=None, nthreads=0, flags=0):
+def fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, qblocks=None, nthreads=0, flags=0, seed=0):
     """The LampAttention forward pass on the CPU.
 
     Returns (o [B,Hq,N,d] fp64, lse [B,Hq,N] fp64, mask [B,Hq,ceil(N/bq),
     ceil(N/(bk*nk))*nk] u8); N need not be a multiple of the block sizes.
     With `qblocks` (flat indices (b*Hq+h)*(N/bq)+qb) only those query blocks
     are computed; the other rows of o/lse hold NaN and their mask bytes 0xFE.
+    `seed` keys the random numbers of flag 8 (stochastic rounding of the
+    8-bit accumulation).
     """
     q = np.ascontiguousarray(q, dtype=np.uint16)
     k = np.ascontiguousarray(k, dtype=np.uint16)
@@ -244,9 +290,9 @@ def fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, qblocks=None, nthreads=
         qp, nq = _ptr(qbl), qbl.size
     else:
         qp, nq = None, 0
-    rc = lib().lamp_oracle_fwd(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(causal), int(window),
-                               bq, bk, nk, float(delta), float(tau), int(flags), _ptr(o), _ptr(lse), _ptr(mask),
-                               qp, nq, nthreads)
+    rc = lib().lamp_oracle_fwd_seeded(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(causal), int(window),
+                                      bq, bk, nk, float(delta), float(tau), int(flags), int(seed),
+                                      _ptr(o), _ptr(lse), _ptr(mask), qp, nq, nthreads)
     if rc != 0:
         raise ValueError("lamp_oracle_fwd failed with %d" % rc)
     return o, lse, mask

@@ -54,6 +54,75 @@ def y8_tile(qt, kf, fmt="e4m3"):
     return acc
 
 
+# ---- stochastic rounding of the 8-bit accumulation (Sec. 3.3's alternative
+# to round-to-nearest).  Written apart from the oracle: the random words come
+# from numpy's own Philox4x64-10 generator (which increments its counter
+# before each block, hence the counter minus one below), the e4m3 neighbours
+# from a search of the enumerated e4m3 magnitudes.
+_E4M3_MAGS = None
+
+
+def e4m3_mags():
+    global _E4M3_MAGS
+    if _E4M3_MAGS is None:
+        # e4m3: bias 7, 3 stored bits, subnormals below 2^-6, 0x7F the NaN
+        vals = []
+        for code in range(0x7F):
+            e, m = code >> 3, code & 7
+            vals.append(m * 2.0 ** -9 if e == 0 else (1 + m / 8.0) * 2.0 ** (e - 7))
+        _E4M3_MAGS = np.array(vals)
+    return _E4M3_MAGS
+
+
+def sr_words(seed, j, i, bh, g):
+    """The 4 words of Philox4x64-10 at counter (j, i, bh, g), key (seed, 0)."""
+    # numpy's generator adds one to the (256-bit) counter before producing a
+    # block: start it one below
+    n = (int(j) | int(i) << 64 | int(bh) << 128 | int(g) << 192) - 1
+    n %= 1 << 256
+    ctr = np.array([(n >> (64 * t)) & ((1 << 64) - 1) for t in range(4)], dtype=np.uint64)
+    gen = np.random.Philox(counter=ctr, key=np.array([seed, 0], dtype=np.uint64))
+    return gen.random_raw(4)
+
+
+def sr_r20(words, c):
+    """20-bit random integer of channel c from the words of its group."""
+    w = int(words[(c % 8) // 2])
+    half = (w >> 32) if c % 2 else (w & 0xFFFFFFFF)
+    return half >> 12
+
+
+def sr_round(t, r):
+    """Stochastic rounding of fp64 values t (fp32 numbers) to e4m3, random integers r < 2^20."""
+    mags = e4m3_mags()
+    a = np.minimum(np.abs(t), 448.0)
+    idx = np.searchsorted(mags, a, side="right") - 1
+    lo = mags[idx]
+    hi = mags[np.minimum(idx + 1, mags.size - 1)]
+    u = np.where(hi > lo, hi - lo, 1.0)
+    frac20 = np.floor((a - lo) / u * 2.0 ** 20)
+    res = np.where(frac20 + r >= 2.0 ** 20, hi, lo)
+    return np.copysign(res, t)
+
+
+def y8_tile_sr(qt, kf, seed, bh, rows, keys):
+    """Y8 values [T, bq] with stochastic rounding; rows / keys: the query and
+    key indices of qt's rows and kf's rows."""
+    T, bq, d = kf.shape[0], qt.shape[0], qt.shape[1]
+    r = np.zeros((d, T, bq))
+    for a, i in enumerate(keys):
+        for bb, j in enumerate(rows):
+            for g in range(d // 8):
+                wds = sr_words(seed, int(j), int(i), bh, g)
+                for c in range(8 * g, 8 * g + 8):
+                    r[c, a, bb] = sr_r20(wds, c)
+    acc = np.zeros((T, bq))
+    for c in range(d):
+        p = kf[:, c][:, None] * qt[:, c][None, :]          # exact in fp64
+        acc = sr_round(rn32_sum(p, acc), r[c])
+    return acc
+
+
 def y16_tile(qt, kf, fmt="e4m11"):
     acc = np.zeros((kf.shape[0], qt.shape[0]))
     for c in range(qt.shape[1]):
@@ -123,11 +192,12 @@ def _colsum(E):
     return S
 
 
-def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=0):
+def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=0, seed=0):
     """q [B,Hq,N,d], k/v [B,Hkv,N,d] bf16 bit patterns.  Returns o, lse, mask.
     flags: 1 = first stage disabled, 2 = 8-bit shifts against mu_hat
     truncated to e4m3 (both only for 0 < tau < inf), 4 = the SIM precision
-    profile (Sec. 4.1) in every mode."""
+    profile (Sec. 4.1) in every mode, 8 = the 8-bit accumulation rounded
+    stochastically with random words keyed by `seed`."""
     B, Hq, N, d = q.shape
     Hkv = k.shape[1]
     G = Hq // Hkv
@@ -170,7 +240,9 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=
                     kf = kf_all[np.minimum(ii, N - 1)]
                     prec = np.where(act, 0, 3)
                     Y = np.full((T, bq), np.nan)
-                    if not all16:
+                    if not all16 and flags & 8:
+                        Y = y8_tile_sr(qt, kf, seed, b * Hq + h, jj, ii)
+                    elif not all16:
                         Y = y8_tile(qt, kf, f8)
                     Yv = np.where(vis, Y, -np.inf)
                     m8 = np.array([Yv[th * bk:(th + 1) * bk].max(axis=0) for th in range(nk)])
