@@ -116,6 +116,37 @@ enum {
 };
 
 /*
+ * lamp_attn_fwd_sr -- lamp_attn_fwd with the 8-bit accumulation rounded
+ * stochastically instead of to nearest (Sec. 3.3, "Floating-point formats":
+ * stochastic rounding as the remedy for the swamping of e4m3 accumulation).
+ *
+ * Each FP32 FMA result t of the 8-bit recursion goes to one of its two e4m3
+ * neighbours: with a = min(|t|, 448), lo the e4m3 number next to a toward
+ * zero and u its spacing, to lo + u when floor(2^20 (a - lo) / u) + r >= 2^20,
+ * else to lo, with the sign of t.  r is the top 20 bits of a 32-bit half of
+ * Philox4x64-10 (Salmon et al., SC 2011) under key (seed, 0) at counter
+ * (j, i, b*Hq + h, c / 8) -- query row j, key i, query head h of batch b,
+ * channel c -- half number c mod 8 of the four 64-bit outputs, low half
+ * first.  The numbers depend on the logit and the channel alone, so the
+ * result does not depend on the block sizes, and the 8-bit logits are those
+ * of lamp_attn_logits8_sr with the same seed.  Everything else is as in
+ * lamp_attn_fwd (the 16-bit logits keep round-to-nearest; tau = 0 computes
+ * no 8-bit logit and equals lamp_attn_fwd).
+ *
+ * Arguments, layouts, outputs and workspace as lamp_attn_fwd; flags: 0,
+ * LAMP_STAGE1_OFF and/or LAMP_MU_TRUNC; LAMP_SIM_PROFILE gives
+ * LAMP_ERR_UNSUPPORTED.  Built for the configurations lamp_attn_fwd lists for
+ * the formats of Sec. 3.3.  The generator costs some hundred VALU operations
+ * per 8 multiply-adds: expect this pass to run far slower than
+ * lamp_attn_fwd.
+ */
+int lamp_attn_fwd_sr(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                     int B, int Hq, int Hkv, int N, int d,
+                     int causal, int window, int bq, int bk, int nk,
+                     double delta, double tau, unsigned flags, uint64_t seed,
+                     float *o, float *lse, uint8_t *mask, void *stream);
+
+/*
  * lamp_attn_decode -- LampAttention for query rows against a key/value cache
  * in the vector form of the look-ahead (Sec. 2: the two-step procedure and the
  * greedy knapsack of Eq. (6)), e.g. one new token per sequence (decode).
@@ -155,6 +186,14 @@ int lamp_attn_decode(const uint16_t *q, const uint16_t *k, const uint16_t *v,
 int lamp_attn_logits8(const uint16_t *q, const uint16_t *k,
                       int B, int Hq, int Hkv, int N, int d, int causal, int window,
                       int row0, int nrows, uint8_t *y8, void *stream);
+
+/*
+ * lamp_attn_logits8_sr -- lamp_attn_logits8 with the stochastic rounding of
+ * lamp_attn_fwd_sr (same seed, same numbers).  Same arguments and layout.
+ */
+int lamp_attn_logits8_sr(const uint16_t *q, const uint16_t *k,
+                         int B, int Hq, int Hkv, int N, int d, int causal, int window,
+                         int row0, int nrows, uint64_t seed, uint8_t *y8, void *stream);
 
 /*
  * lamp_attn_logits16 -- the 16-bit logits of the recompute steps (Alg. 1):

@@ -33,6 +33,7 @@
 #include "lamp_device.h"
 #include "lamp_kernels.h"
 #include "lamp_loops.h"
+#include "lamp_sr.h"
 
 #ifndef LAMP_MIN_WAVES
 #define LAMP_MIN_WAVES 2   // minimum waves per SIMD requested from the register allocator
@@ -73,7 +74,9 @@ struct Cfg {
     static_assert(KPW == 4 || KPW == 8 || KPW % 16 == 0, "recompute split in 4, 8 or multiples of 16 keys");
 };
 
-template <int D, int BQ, int BK, int NK>
+// SR: the 8-bit logits with stochastic rounding (lamp_sr.h) in place of
+// round-to-nearest.
+template <int D, int BQ, int BK, int NK, bool SR>
 __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) void lamp_fwd_kernel(FwdParams p)
 {
     using C = Cfg<D, BQ, BK, NK>;
@@ -213,7 +216,14 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                         const int ck0 = k0 + c16 * 16;
                         if (ck0 > bv_hi || ck0 + 15 < bv_lo) continue;   // nothing visible in the block
                         uint32_t a8[QPL][8];
-                        emu8_chunk<D, QPL>(qrow, kt32 + (size_t)ck0 * D, a8);
+                        if constexpr (SR) {
+                            int jq[QPL];
+#pragma unroll
+                            for (int s = 0; s < QPL; ++s) jq[s] = q0 + row[s];
+                            sr8_chunk<D, QPL>(qrow, kt32 + (size_t)ck0 * D, p.seed, (uint64_t)bh, jq, ck0, a8);
+                        } else {
+                            emu8_chunk<D, QPL>(qrow, kt32 + (size_t)ck0 * D, a8);
+                        }
 #pragma unroll
                         for (int s = 0; s < QPL; ++s) {
                             const bool full = ck0 >= vlo[s] && ck0 + 15 <= vhi[s];
@@ -749,11 +759,11 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
 }
 
 // ------------------------------------------------------------------ launcher
-template <int D, int BQ, int BK, int NK>
+template <int D, int BQ, int BK, int NK, bool SR = false>
 static hipError_t launch_fwd(const FwdParams &p, hipStream_t s)
 {
     using C = Cfg<D, BQ, BK, NK>;
-    auto kern = lamp_fwd_kernel<D, BQ, BK, NK>;
+    auto kern = lamp_fwd_kernel<D, BQ, BK, NK, SR>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
     if (e != hipSuccess) return e;
@@ -789,6 +799,21 @@ hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipSt
     LAMP_FWD_D(128)
     LAMP_FWD_D(256)
 #undef LAMP_FWD_D
+    *found = false;
+    return hipSuccess;
+}
+
+hipError_t dispatch_fwd_sr(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found)
+{
+    *found = true;
+#define LAMP_FWD_SR(D_, BQ_, BK_)                                            \
+    if (D == D_ && BQ == BQ_ && BK == BK_ && NK == 4) return launch_fwd<D_, BQ_, BK_, 4, true>(p, s);
+#define LAMP_FWD_SR_D(D_) LAMP_FWD_SR(D_, 64, 16) LAMP_FWD_SR(D_, 128, 16) LAMP_FWD_SR(D_, 64, 64) LAMP_FWD_SR(D_, 128, 64)
+    LAMP_FWD_SR_D(64)
+    LAMP_FWD_SR_D(128)
+    LAMP_FWD_SR_D(256)
+#undef LAMP_FWD_SR_D
+#undef LAMP_FWD_SR
     *found = false;
     return hipSuccess;
 }

@@ -214,9 +214,10 @@ void lamp_shutdown(void)
     (void)hipSetDevice(prev);
 }
 
-int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B, int Hq, int Hkv, int N, int d,
-                  int causal, int window, int bq, int bk, int nk, double delta, double tau, unsigned flags, float *o,
-                  float *lse, uint8_t *mask, void *stream)
+// The forward pass; sr: the 8-bit logits rounded stochastically with `seed`.
+static int fwd_impl(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B, int Hq, int Hkv, int N, int d,
+                    int causal, int window, int bq, int bk, int nk, double delta, double tau, unsigned flags, bool sr,
+                    uint64_t seed, float *o, float *lse, uint8_t *mask, void *stream)
 {
     int rc = check_common(q, k, B, Hq, Hkv, N, d, causal, window);
     if (rc) return rc;
@@ -229,6 +230,8 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
     if (bq <= 0 || bk <= 0 || nk <= 0) return fail(LAMP_ERR_INVALID_ARG, "block sizes must be positive");
     if (!lamp::fwd_supported(d, bq, bk, nk))
         return fail(LAMP_ERR_UNSUPPORTED, "block sizes (bq=%d, bk=%d, nk=%d) not built for d=%d", bq, bk, nk, d);
+    if (sr && (flags & LAMP_SIM_PROFILE))
+        return fail(LAMP_ERR_UNSUPPORTED, "stochastic rounding is built for the formats of Sec. 3.3, not the SIM profile");
     if ((flags & LAMP_SIM_PROFILE) && !(bk == 16 && nk == 4 && (d == 128 || d == 256)))
         return fail(LAMP_ERR_UNSUPPORTED, "the SIM profile is built for bk=16, nk=4, d in {128, 256} (bk=%d, nk=%d, d=%d)",
                     bk, nk, d);
@@ -272,6 +275,9 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
     p.tau = tau;
     p.mode = std::isinf(tau) ? lamp::MODE_PURE8 : (tau == 0.0 ? lamp::MODE_ALL16 : lamp::MODE_LAMP);
     p.flags = p.mode == lamp::MODE_LAMP ? flags : (flags & (unsigned)LAMP_SIM_PROFILE);
+    p.seed = seed;
+    // the all-16-bit mode computes no 8-bit logit: the rounding mode does not matter there
+    const bool use_sr = sr && p.mode != lamp::MODE_ALL16;
     bool timed = false;
     TimedCall tc{};
     {
@@ -283,11 +289,12 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
         HIP_TRY(hipEventRecord(tc.e[0], s));
     }
     HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, Nq, Nk, d, scale_of(d), s,
-                                 lamp::fwd_grouped(d, bq, bk, nk)));
+                                 !use_sr && lamp::fwd_grouped(d, bq, bk, nk)));
     HIP_TRY(lamp::launch_transpose_v(v, w.vt, B, Hkv, N, Nk, d, s));
     if (timed) HIP_TRY(hipEventRecord(tc.e[1], s));
     bool found = false;
-    HIP_TRY(lamp::dispatch_fwd(d, bq, bk, nk, p, s, &found));
+    if (use_sr) HIP_TRY(lamp::dispatch_fwd_sr(d, bq, bk, nk, p, s, &found));
+    else HIP_TRY(lamp::dispatch_fwd(d, bq, bk, nk, p, s, &found));
     if (!found)
         return fail(LAMP_ERR_UNSUPPORTED, "block sizes (bq=%d, bk=%d, nk=%d) not built for d=%d", bq, bk, nk, d);
     if (timed) {
@@ -296,6 +303,22 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
         g_timed.push_back(tc);
     }
     return LAMP_OK;
+}
+
+int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B, int Hq, int Hkv, int N, int d,
+                  int causal, int window, int bq, int bk, int nk, double delta, double tau, unsigned flags, float *o,
+                  float *lse, uint8_t *mask, void *stream)
+{
+    return fwd_impl(q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, flags, false, 0, o, lse, mask,
+                    stream);
+}
+
+int lamp_attn_fwd_sr(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B, int Hq, int Hkv, int N, int d,
+                     int causal, int window, int bq, int bk, int nk, double delta, double tau, unsigned flags,
+                     uint64_t seed, float *o, float *lse, uint8_t *mask, void *stream)
+{
+    return fwd_impl(q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, flags, true, seed, o, lse, mask,
+                    stream);
 }
 
 int lamp_attn_decode(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B, int Hq, int Hkv, int M, int N,
@@ -469,6 +492,21 @@ int lamp_attn_logits8(const uint16_t *q, const uint16_t *k, int B, int Hq, int H
     hipStream_t s = static_cast<hipStream_t>(stream);
     HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, N, N, d, scale_of(d), s));
     HIP_TRY(lamp::launch_logits8(p, d, s));
+    return LAMP_OK;
+}
+
+int lamp_attn_logits8_sr(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv, int N, int d, int causal,
+                         int window, int row0, int nrows, uint64_t seed, uint8_t *y8, void *stream)
+{
+    lamp::LogitsParams p;
+    Workspace w;
+    int rc = logits_common(q, k, B, Hq, Hkv, N, d, causal, window, row0, nrows, y8, &p, &w);
+    if (rc) return rc;
+    p.y8 = y8;
+    p.seed = seed;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, N, N, d, scale_of(d), s));
+    HIP_TRY(lamp::launch_logits8(p, d, s, true));
     return LAMP_OK;
 }
 

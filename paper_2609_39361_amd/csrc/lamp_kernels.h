@@ -31,6 +31,7 @@ struct FwdParams {
     int causal, window, mode;
     unsigned flags;           // LAMP_SIM_PROFILE; LAMP_STAGE1_OFF | LAMP_MU_TRUNC in the threshold mode
     double delta, tau;
+    uint64_t seed;            // key of the stochastic-rounding generator (dispatch_fwd_sr)
 };
 
 struct LogitsParams {
@@ -40,6 +41,7 @@ struct LogitsParams {
     uint16_t *y16;
     float *ysim;              // SIM profile logit values
     int B, Hq, Hkv, N, causal, window, row0, nrows;
+    uint64_t seed;            // stochastic rounding of the 8-bit logits (launch_logits8, sr)
 };
 
 // Decode form (vector LAMP, Sec. 2): M query rows per (b, h) at positions
@@ -67,6 +69,8 @@ hipError_t launch_prescale_q(const uint16_t *q, float *qt, int BH, int rows, int
 bool fwd_supported(int D, int BQ, int BK, int NK);
 hipError_t dispatch_fwd16(int D, int BQ, const FwdParams &p, hipStream_t s, bool *found);
 hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found);
+// the general kernel with stochastically rounded 8-bit logits (row layout)
+hipError_t dispatch_fwd_sr(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found);
 hipError_t launch_transpose_v(const uint16_t *v, uint16_t *vt, int B, int Hkv, int N, int Nk, int D, hipStream_t s);
 
 // Issue rates of the logit loops' instructions (lamp_rates.hip): ns per
@@ -79,7 +83,7 @@ hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float
                           int N, int Nq, int Nk, int D, float scale, hipStream_t s, bool grouped = false);
 // whether dispatch_fwd runs the pipelined kernel (which reads the grouped layout)
 bool fwd_grouped(int D, int BQ, int BK, int NK);
-hipError_t launch_logits8(const LogitsParams &p, int D, hipStream_t s);
+hipError_t launch_logits8(const LogitsParams &p, int D, hipStream_t s, bool sr = false);
 hipError_t launch_logits16(const LogitsParams &p, int D, hipStream_t s);
 hipError_t launch_logits_sim(const LogitsParams &p, int D, int high, hipStream_t s);
 hipError_t launch_build_sim_tables(uint16_t *sim8, uint32_t *sim16, unsigned *ambiguous, hipStream_t s);

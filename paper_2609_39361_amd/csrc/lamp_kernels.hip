@@ -8,6 +8,8 @@
 #include "lamp_device.h"
 #include "lamp_kernels.h"
 #include "lamp_loops.h"
+#include "lamp_sr.h"
+#include "lamp_sr.h"
 
 namespace lamp {
 
@@ -183,7 +185,7 @@ __global__ void build_sim_tables_kernel(uint16_t *__restrict__ sim8, uint32_t *_
 
 // ------------------------------------------------------------------ logits entry kernels
 // One wave: 64 rows x (16*NC) keys.  grid.x = B*Hq*ceil(nrows/64), grid.y = N/(16*NC).
-template <int D, int NC>
+template <int D, int NC, bool SR>
 __global__ __launch_bounds__(64) void logits8_kernel(LogitsParams p)
 {
     const int lane = threadIdx.x;
@@ -200,7 +202,12 @@ __global__ __launch_bounds__(64) void logits8_kernel(LogitsParams p)
         const int key0 = (blockIdx.y * NC + g) * 16;
         const float *kt = p.kt32 + (((size_t)b * p.Hkv + hk) * p.N + key0) * (size_t)D;
         uint32_t acc[1][8];
-        emu8_chunk<D, 1>(qrow, kt, acc);
+        if constexpr (SR) {
+            const int jq[1] = {j};
+            sr8_chunk<D, 1>(qrow, kt, p.seed, (uint64_t)bh, jq, key0, acc);
+        } else {
+            emu8_chunk<D, 1>(qrow, kt, acc);
+        }
         if (r < p.nrows) {
             uint8_t *out = p.y8 + (((size_t)b * p.Hq + h) * p.nrows + r) * p.N + key0;
 #pragma unroll
@@ -339,20 +346,27 @@ hipError_t launch_transpose_v(const uint16_t *v, uint16_t *vt, int B, int Hkv, i
     return hipGetLastError();
 }
 
-hipError_t launch_logits8(const LogitsParams &p, int D, hipStream_t s)
+template <bool SR>
+static void launch_logits8_t(const LogitsParams &p, int D, hipStream_t s)
 {
     const unsigned gx = (unsigned)(p.B * p.Hq * ((p.nrows + 63) / 64));
     if (p.N % 64 == 0) {
         dim3 grid(gx, (unsigned)(p.N / 64));
-        if (D == 64) hipLaunchKernelGGL((logits8_kernel<64, 4>), grid, dim3(64), 0, s, p);
-        else if (D == 128) hipLaunchKernelGGL((logits8_kernel<128, 4>), grid, dim3(64), 0, s, p);
-        else hipLaunchKernelGGL((logits8_kernel<256, 4>), grid, dim3(64), 0, s, p);
+        if (D == 64) hipLaunchKernelGGL((logits8_kernel<64, 4, SR>), grid, dim3(64), 0, s, p);
+        else if (D == 128) hipLaunchKernelGGL((logits8_kernel<128, 4, SR>), grid, dim3(64), 0, s, p);
+        else hipLaunchKernelGGL((logits8_kernel<256, 4, SR>), grid, dim3(64), 0, s, p);
     } else {
         dim3 grid(gx, (unsigned)(p.N / 16));
-        if (D == 64) hipLaunchKernelGGL((logits8_kernel<64, 1>), grid, dim3(64), 0, s, p);
-        else if (D == 128) hipLaunchKernelGGL((logits8_kernel<128, 1>), grid, dim3(64), 0, s, p);
-        else hipLaunchKernelGGL((logits8_kernel<256, 1>), grid, dim3(64), 0, s, p);
+        if (D == 64) hipLaunchKernelGGL((logits8_kernel<64, 1, SR>), grid, dim3(64), 0, s, p);
+        else if (D == 128) hipLaunchKernelGGL((logits8_kernel<128, 1, SR>), grid, dim3(64), 0, s, p);
+        else hipLaunchKernelGGL((logits8_kernel<256, 1, SR>), grid, dim3(64), 0, s, p);
     }
+}
+
+hipError_t launch_logits8(const LogitsParams &p, int D, hipStream_t s, bool sr)
+{
+    if (sr) launch_logits8_t<true>(p, D, s);
+    else launch_logits8_t<false>(p, D, s);
     return hipGetLastError();
 }
 

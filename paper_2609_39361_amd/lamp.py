@@ -39,6 +39,11 @@ def lib():
         L.lamp_attn_fwd.restype = i32
         L.lamp_attn_logits8.argtypes = [P, P] + [i32] * 9 + [P, P]
         L.lamp_attn_logits8.restype = i32
+        L.lamp_attn_fwd_sr.argtypes = ([P, P, P] + [i32] * 5 + [i32] * 5 + [f64, f64, ctypes.c_uint, ctypes.c_uint64]
+                                       + [P, P, P, P])
+        L.lamp_attn_fwd_sr.restype = i32
+        L.lamp_attn_logits8_sr.argtypes = [P, P] + [i32] * 9 + [ctypes.c_uint64, P, P]
+        L.lamp_attn_logits8_sr.restype = i32
         L.lamp_attn_logits16.argtypes = [P, P] + [i32] * 9 + [P, P]
         L.lamp_attn_logits16.restype = i32
         L.lamp_attn_decode.argtypes = [P, P, P] + [i32] * 9 + [f64, f64, ctypes.c_uint, P, P, P, P]
@@ -106,12 +111,14 @@ MU_TRUNC = 2     # 8-bit shifts against mu_hat truncated to e4m3 (SIM profile: t
 SIM_PROFILE = 4  # the SIM precision profile (FP32 range, 3 / 11 mantissa bits, no saturation)
 
 
-def attn_fwd(q, k, v, causal=True, window=0, bq=128, bk=16, nk=4, delta=2.0 ** -8, tau=0.5, out=None, flags=0):
+def attn_fwd(q, k, v, causal=True, window=0, bq=128, bk=16, nk=4, delta=2.0 ** -8, tau=0.5, out=None, flags=0,
+             sr_seed=None):
     """LampAttention forward pass.  Returns (o fp32 [B,Hq,N,d], lse fp32
     [B,Hq,N], mask uint8 [B,Hq,ceil(N/bq),ceil(N/(bk*nk))*nk]); N need not be
     a multiple of the block sizes.  `out` may supply those three tensors to
     write into; `flags` selects the variants STAGE1_OFF, MU_TRUNC and the
-    SIM_PROFILE numerics."""
+    SIM_PROFILE numerics.  With `sr_seed` (an int below 2^64) the 8-bit
+    accumulation is rounded stochastically with that seed (lamp_attn_fwd_sr)."""
     B, Hq, Hkv, N, d = _check_inputs(q, k, v)
     dev = q.device
     if out is None:
@@ -121,9 +128,14 @@ def attn_fwd(q, k, v, causal=True, window=0, bq=128, bk=16, nk=4, delta=2.0 ** -
     else:
         o, lse, mask = out
     with torch.cuda.device(dev):
-        rc = lib().lamp_attn_fwd(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(causal), int(window),
-                                 bq, bk, nk, float(delta), float(tau), int(flags), _ptr(o), _ptr(lse), _ptr(mask),
-                                 _stream(dev))
+        if sr_seed is None:
+            rc = lib().lamp_attn_fwd(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(causal), int(window),
+                                     bq, bk, nk, float(delta), float(tau), int(flags), _ptr(o), _ptr(lse), _ptr(mask),
+                                     _stream(dev))
+        else:
+            rc = lib().lamp_attn_fwd_sr(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(causal), int(window),
+                                        bq, bk, nk, float(delta), float(tau), int(flags), int(sr_seed),
+                                        _ptr(o), _ptr(lse), _ptr(mask), _stream(dev))
     _check(rc)
     return o, lse, mask
 
@@ -155,14 +167,19 @@ def attn_decode(q, k, v, causal=True, window=0, tk=64, delta=2.0 ** -8, tau=0.5,
     return o, lse, mask
 
 
-def logits8(q, k, causal=True, window=0, row0=0, nrows=None):
-    """e4m3 codes of the 8-bit logits of rows [row0, row0+nrows): uint8 [B,Hq,nrows,N], 0xFF invisible."""
+def logits8(q, k, causal=True, window=0, row0=0, nrows=None, sr_seed=None):
+    """e4m3 codes of the 8-bit logits of rows [row0, row0+nrows): uint8 [B,Hq,nrows,N], 0xFF invisible;
+    with `sr_seed`, stochastically rounded (lamp_attn_logits8_sr)."""
     B, Hq, Hkv, N, d = _check_inputs(q, k)
     nrows = N - row0 if nrows is None else nrows
     y = torch.empty((B, Hq, nrows, N), dtype=torch.uint8, device=q.device)
     with torch.cuda.device(q.device):
-        rc = lib().lamp_attn_logits8(_ptr(q), _ptr(k), B, Hq, Hkv, N, d, int(causal), int(window), row0, nrows,
-                                     _ptr(y), _stream(q.device))
+        if sr_seed is None:
+            rc = lib().lamp_attn_logits8(_ptr(q), _ptr(k), B, Hq, Hkv, N, d, int(causal), int(window), row0, nrows,
+                                         _ptr(y), _stream(q.device))
+        else:
+            rc = lib().lamp_attn_logits8_sr(_ptr(q), _ptr(k), B, Hq, Hkv, N, d, int(causal), int(window), row0,
+                                            nrows, int(sr_seed), _ptr(y), _stream(q.device))
     _check(rc)
     return y
 

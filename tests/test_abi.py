@@ -126,3 +126,23 @@ def test_issue_rates_rejects_null_without_gpu():
     lib.lamp_last_error.restype = ctypes.c_char_p
     assert lib.lamp_issue_rates(None, None) == 1
     assert b"null" in lib.lamp_last_error()
+
+
+def test_fwd_sr_rejects_bad_arguments_without_gpu():
+    """lamp_attn_fwd_sr checks its arguments before any device call: unknown
+    flags, the SIM profile (not built with stochastic rounding), block sizes."""
+    if not os.path.exists(LIB):
+        pytest.skip("liblamp.so not built")
+    lib = ctypes.CDLL(LIB)
+    P = ctypes.c_void_p
+    lib.lamp_attn_fwd_sr.restype = ctypes.c_int
+    lib.lamp_attn_fwd_sr.argtypes = ([P, P, P] + [ctypes.c_int] * 10 + [ctypes.c_double] * 2 + [ctypes.c_uint]
+                                     + [ctypes.c_uint64] + [P, P, P, P])
+    lib.lamp_last_error.restype = ctypes.c_char_p
+    d = ctypes.c_void_p(16)
+    args = (d, d, d, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5)
+    assert lib.lamp_attn_fwd_sr(*args, 16, 1, d, d, d, None) == 1
+    assert lib.lamp_attn_fwd_sr(*args, 4, 1, d, d, d, None) == 2
+    assert b"SIM" in lib.lamp_last_error()
+    assert lib.lamp_attn_fwd_sr(d, d, d, 1, 2, 1, 256, 128, 1, 0, 128, 32, 4, 2 ** -8, 0.5, 0, 2 ** 64 - 1,
+                                d, d, d, None) == 2
