@@ -104,8 +104,9 @@ def visible_in_mask(w, mask):
     return int((rec * cnt[None]).sum())
 
 
-def cpu_baseline(w, tau, q, k, v, budget_s=15.0, seed=0, flags=0):
-    """The CPU oracle on a bounded, stated sample of query blocks."""
+def cpu_baseline(w, tau, q, k, v, budget_s=15.0, seed=0, flags=0, sr_seed=None):
+    """The CPU oracle on a bounded, stated sample of query blocks (with
+    sr_seed: the stochastically rounded 8-bit accumulation)."""
     from oracle import oracle as O
     rng = np.random.default_rng(seed)
     nqb = w.N // w.bq
@@ -120,7 +121,8 @@ def cpu_baseline(w, tau, q, k, v, budget_s=15.0, seed=0, flags=0):
         batch = [int(x) for x in order[len(picked):len(picked) + n]]
         t0 = time.perf_counter()
         O.fwd(qbits, kbits, vbits, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau, qblocks=batch,
-              nthreads=threads, flags=flags)
+              nthreads=threads, flags=flags | (O.SR8 if sr_seed is not None else 0),
+              seed=sr_seed if sr_seed is not None else 0)
         spent += time.perf_counter() - t0
         for f in batch:
             qb = f % nqb
@@ -256,6 +258,8 @@ def main():
     ap.add_argument("--flags", type=str, default="0",
                     help="variants: 1 first stage off, 2 mu_hat truncation, 4 SIM precision profile; "
                          "a comma-separated list sweeps them (outer loop)")
+    ap.add_argument("--sr-seed", type=int, default=None,
+                    help="round the 8-bit accumulation stochastically with this seed (lamp_attn_fwd_sr)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="before the timed steps, run one plain negating copy of this many MiB "
                          "(fp32 in, fp32 out) to calibrate the HBM byte counters")
@@ -272,8 +276,8 @@ def main():
     taus = [w.tau] if args.tau is None else [float(x) for x in args.tau.split(",")]
     flags_list = [int(x) for x in args.flags.split(",")]
     if w.M > 0:
-        if flags_list != [0]:
-            raise SystemExit("the decode form takes no flags")
+        if flags_list != [0] or args.sr_seed is not None:
+            raise SystemExit("the decode form takes no flags and no stochastic rounding")
         for tau in taus:
             main_decode(args, w, tau)
         return
@@ -305,8 +309,11 @@ def run_fwd(args, w, tau, flags, host_inputs, dev_inputs, out, dev):
     qd, kd, vd = dev_inputs
     o, lse, mask = out
 
+    sr = args.sr_seed is not None and tau != 0.0   # threshold 0 computes no 8-bit logit
+
     def step():
-        lamp.attn_fwd(qd, kd, vd, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau, out=out, flags=flags)
+        lamp.attn_fwd(qd, kd, vd, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau, out=out, flags=flags,
+                      sr_seed=args.sr_seed)
 
     for _ in range(args.warmup):
         step()
@@ -344,7 +351,7 @@ def run_fwd(args, w, tau, flags, host_inputs, dev_inputs, out, dev):
     simds = 4 * torch.cuda.get_device_properties(dev).multi_processor_count
     step8 = rates["emulated_step_sim"] / 64.0 if sim else rates["emulated_step"] / 128.0
     floor_ms = (mac8 * step8 + mac16 / 64.0 * rates["fmac_f32_dpp"]) / simds * 1e-6
-    issue_floor = {
+    issue_floor = None if sr else {
         "ms": floor_ms, "frac": floor_ms / kernel_ms,
         "ns_per_wave_instruction_per_simd": rates,
         "counts": "emulated 8-bit steps (%s) of every visible logit and 16-bit FMAs of the recomputed sub-blocks "
@@ -366,11 +373,14 @@ def run_fwd(args, w, tau, flags, host_inputs, dev_inputs, out, dev):
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": ("SIM profile: fp32 with 3/11-bit mantissas (fp32 FMA + integer rounding), bf16 inputs, fp32 output"
-                  if sim else "e4m3/e4m11 emulated (fp32 FMA + fp8 conversions), bf16 inputs, fp32 output"),
+                  if sim else
+                  "e4m3 stochastically rounded (fp32 FMA + Philox4x64-10 bits), e4m11, bf16 inputs, fp32 output"
+                  if sr else "e4m3/e4m11 emulated (fp32 FMA + fp8 conversions), bf16 inputs, fp32 output"),
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "N": w.N, "d": w.d,
                    "causal": w.causal, "window": w.window, "bq": w.bq, "bk": w.bk, "nk": w.nk,
-                   "delta": w.delta, "tau": tau, "flags": flags},
+                   "delta": w.delta, "tau": tau, "flags": flags,
+                   "rounding_8bit": ("stochastic, seed %d" % args.sr_seed) if sr else "nearest-even"},
         "visible_pair_tflops": 4.0 * w.macs / (ms * 1e-3) / 1e12,   # 4*d per visible (query, key) pair
         "recompute_fraction": st["recompute_fraction"],
         "tile_hist": st["tile_hist"],
@@ -380,8 +390,9 @@ def run_fwd(args, w, tau, flags, host_inputs, dev_inputs, out, dev):
             "peak": peak,
             "unit": "T VALU lane-ops/s",
             "frac": achieved / peak,
-            "traffic": measured_traffic(w.name, tau, flags),
-            "kernel": ("lamp_fwd16_kernel<%d,%d,%d,%s>" % (w.d, w.bq, _mode_of(tau), "true" if sim else "false"))
+            "traffic": None if sr else measured_traffic(w.name, tau, flags),
+            "kernel": ("lamp_fwd_kernel<%d,%d,%d,%d,SR>" % (w.d, w.bq, w.bk, w.nk)) if sr
+                      else ("lamp_fwd16_kernel<%d,%d,%d,%s>" % (w.d, w.bq, _mode_of(tau), "true" if sim else "false"))
                       if (w.bk == 16 and w.d >= 128)
                       else ("lamp_fwd_kernel<%d,%d,%d,%d>" % (w.d, w.bq, w.bk, w.nk)),
             "kernel_ms": kernel_ms,
@@ -390,13 +401,14 @@ def run_fwd(args, w, tau, flags, host_inputs, dev_inputs, out, dev):
             "ops_per_unit": ("%d per emulated 8-bit MAC, 1 per 16-bit recompute MAC"
                              % (OPS_PER_MAC8_SIM if sim else OPS_PER_MAC8)),
             "algorithmic_frac_one_op_per_mac": (mac8 + mac16) / (kernel_ms * 1e-3) / VALU_LANE_OPS,
-            "valu_issue_frac_counters": measured_valu_issue(w.name, tau, flags),
+            "valu_issue_frac_counters": None if sr else measured_valu_issue(w.name, tau, flags),
             "issue_floor": issue_floor,
         },
         "wall_s_timed_region": wall,
     }
     if not args.no_cpu:
-        result["cpu_baseline"] = cpu_baseline(w, tau, q, k, v, budget_s=args.cpu_budget, flags=flags)
+        result["cpu_baseline"] = cpu_baseline(w, tau, q, k, v, budget_s=args.cpu_budget, flags=flags,
+                                              sr_seed=args.sr_seed if sr else None)
     print(json.dumps(result), flush=True)
 
 
