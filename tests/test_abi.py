@@ -146,3 +146,23 @@ def test_fwd_sr_rejects_bad_arguments_without_gpu():
     assert b"SIM" in lib.lamp_last_error()
     assert lib.lamp_attn_fwd_sr(d, d, d, 1, 2, 1, 256, 128, 1, 0, 128, 32, 4, 2 ** -8, 0.5, 0, 2 ** 64 - 1,
                                 d, d, d, None) == 2
+
+
+def test_length_limits_without_gpu():
+    """N above 2^20, or B*Hq*N above 2^31, is LAMP_ERR_UNSUPPORTED before any
+    device call; N = 2^20 itself passes the argument checks (the GPU tests run
+    it)."""
+    if not os.path.exists(LIB):
+        pytest.skip("liblamp.so not built")
+    lib = ctypes.CDLL(LIB)
+    P = ctypes.c_void_p
+    lib.lamp_attn_fwd.restype = ctypes.c_int
+    lib.lamp_attn_fwd.argtypes = [P, P, P] + [ctypes.c_int] * 10 + [ctypes.c_double] * 2 + [ctypes.c_uint] + [P, P, P, P]
+    lib.lamp_last_error.restype = ctypes.c_char_p
+    d = ctypes.c_void_p(16)
+    assert lib.lamp_attn_fwd(d, d, d, 1, 1, 1, (1 << 20) + 1, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 0,
+                             d, d, d, None) == 2
+    assert b"2^20" in lib.lamp_last_error()
+    assert lib.lamp_attn_fwd(d, d, d, 4096, 1024, 1, 1 << 20, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 0,
+                             d, d, d, None) == 2
+    assert b"2^31" in lib.lamp_last_error()

@@ -91,6 +91,16 @@ def test_decode_empty(L):
     assert o.numel() == 0 and mask.numel() == 0
 
 
+def test_decode_maximum_cache(L):
+    """A cache of N = 2^20 keys, the longest the library accepts, for two
+    query rows of four heads; every row checked against the oracle."""
+    w = W.small("dg_max_n", B=1, Hq=4, Hkv=1, N=1 << 20, d=128, causal=1, seed=421, M=2, bk=64, kind="gauss")
+    t0 = time.time()
+    err, mask = _compare(L, w, 0.5)
+    _say("decode N = 2^20: O err %.2e, mask %s (%.1f s)" % (err, np.bincount(mask.ravel(), minlength=4),
+                                                            time.time() - t0))
+
+
 @pytest.mark.parametrize("tau", W.TAU_SWEEP)
 def test_decode_config6_sampled(L, tau):
     """Qwen3-8B-shaped decode (32 sequences, 32/8 heads, 8K cache) at full

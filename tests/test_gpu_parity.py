@@ -310,6 +310,21 @@ def test_fwd_ragged_lengths(L, w, tau):
     _compare_fwd(L, w, tau)
 
 
+def test_fwd_maximum_length(L):
+    """N = 2^20, the longest sequence the library accepts, through the
+    pipelined kernel (d=128, 16-key sub-blocks) with a 256-key sliding window
+    (so the pass stays short): the oracle computes the first, a middle and the
+    last query block; their rows of O, lse and their mask bytes (65536
+    sub-blocks each) must match."""
+    w = W.small("max_n_window", N=1 << 20, d=128, Hq=1, Hkv=1, bq=128, bk=16, nk=4, causal=1, window=256,
+                seed=321, kind="gauss")
+    nqb = w.N // w.bq
+    t0 = time.time()
+    err, mask = _compare_fwd(L, w, 0.5, qblocks=[0, nqb // 2, nqb - 1])
+    _say("N = 2^20 sampled: O err %.2e, mask %s (%.1f s)" % (err, np.bincount(mask.ravel(), minlength=4),
+                                                             time.time() - t0))
+
+
 def test_fwd_empty_inputs(L):
     for shape_q, shape_k in (((1, 2, 0, 128), (1, 1, 0, 128)), ((0, 2, 256, 128), (0, 1, 256, 128))):
         q = torch.zeros(shape_q, dtype=torch.bfloat16, device="cuda")
