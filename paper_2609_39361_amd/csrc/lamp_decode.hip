@@ -51,17 +51,22 @@ __device__ __forceinline__ void unpack8(const uint4 &w, float (&f)[8])
 }
 
 // 16-bit logit of this lane's key: the FP32 FMA chain over the channels in
-// ascending order from +0, rounded once to e4m11 (saturating).
+// ascending order from +0, rounded once to e4m11 (saturating).  The key row's
+// loads are all issued before the chain starts: the decision loop waits for
+// this recompute, so its cost is one memory round trip, not one per group.
 template <int D>
 __device__ __forceinline__ float dec16_chain(const uint16_t *krow, kptr32_t q)
 {
-    float acc = 0.0f;
-#pragma unroll 2
-    for (int c = 0; c < D; c += 8) {
-        float kf[8];
-        unpack8(*reinterpret_cast<const uint4 *>(krow + c), kf);
+    uint4 kw[D / 8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc = __builtin_fmaf(q[c + j], kf[j], acc);
+    for (int g = 0; g < D / 8; ++g) kw[g] = *reinterpret_cast<const uint4 *>(krow + 8 * g);
+    float acc = 0.0f;
+#pragma unroll
+    for (int g = 0; g < D / 8; ++g) {
+        float kf[8];
+        unpack8(kw[g], kf);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc = __builtin_fmaf(q[8 * g + j], kf[j], acc);
     }
     uint32_t code;
     return rn_e4m11((double)acc, &code);
@@ -131,13 +136,6 @@ __device__ __forceinline__ double wave_sum_f64(double v)
     v += dpp_f64<0x141>(v);
     v += dpp_f64<0x140>(v);
     return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
-}
-
-__device__ __forceinline__ uint64_t wave_or_u64(uint64_t v)
-{
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) v |= __shfl_xor(v, m, 64);
-    return v;
 }
 
 } // namespace
@@ -383,19 +381,25 @@ __global__ __launch_bounds__(256) void dec_lamp_kernel(DecParams p)
                         }
                     }
                 }
-                // the greedy: sorted costs summed one at a time in fp64
+                // the greedy: sorted costs summed one at a time in fp64, in
+                // straight-line code on values read out of their lanes (the
+                // index of the first cost that is infinite or would pass the
+                // limit is the count kept; the sum after it is not used)
                 const double lim = (p.tau * omh) * omh;
                 double xi = 0.0;
-                int nkeep = 0;
-                for (; nkeep < 64; ++nkeep) {
-                    const double kk = __shfl(kap, nkeep, 64);
-                    if (kk == __builtin_inf()) break;
+                int nkeep = 64;
+#pragma unroll
+                for (int i = 0; i < 64; ++i) {
+                    const double kk = readlane_f64(kap, i);
                     const double nx = xi + kk;
-                    if (!(nx <= lim)) break;
+                    const bool ok = kk != __builtin_inf() && nx <= lim;
+                    nkeep = (nkeep == 64 && !ok) ? i : nkeep;
                     xi = nx;
                 }
-                const uint64_t rbits =
-                    wave_or_u64((lane >= nkeep && kap != __builtin_inf()) ? (1ull << idx) : 0ull);
+                // sorted position -> key lane: each sorted slot sends its
+                // recompute flag to the lane of its key (idx is a permutation)
+                const int rflag = __builtin_amdgcn_ds_permute(idx << 2, (lane >= nkeep && kap != __builtin_inf()) ? 1 : 0);
+                const uint64_t rbits = __ballot(rflag != 0);
                 if (rbits) {
                     if (!have16) {
                         y16 = dec16_chain<D>(krow, qv);
