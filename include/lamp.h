@@ -123,11 +123,11 @@ enum {
  * Each FP32 FMA result t of the 8-bit recursion goes to one of its two e4m3
  * neighbours: with a = min(|t|, 448), lo the e4m3 number next to a toward
  * zero and u its spacing, to lo + u when floor(2^20 (a - lo) / u) + r >= 2^20,
- * else to lo, with the sign of t.  r is the top 20 bits of a 32-bit half of
+ * else to lo, with the sign of t.  r is a 20-bit field of the output of
  * Philox4x64-10 (Salmon et al., SC 2011) under key (seed, 0) at counter
- * (j, i, b*Hq + h, c / 8) -- query row j, key i, query head h of batch b,
- * channel c -- half number c mod 8 of the four 64-bit outputs, low half
- * first.  The numbers depend on the logit and the channel alone, so the
+ * (j, i, b*Hq + h, c / 12) -- query row j, key i, query head h of batch b,
+ * channel c: with m = c mod 12, bits [20 (m mod 3), 20 (m mod 3) + 20) of
+ * output word m / 3.  The numbers depend on the logit and the channel alone, so the
  * result does not depend on the block sizes, and the 8-bit logits are those
  * of lamp_attn_logits8_sr with the same seed.  Everything else is as in
  * lamp_attn_fwd (the 16-bit logits keep round-to-nearest; tau = 0 computes

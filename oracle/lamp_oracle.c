@@ -494,11 +494,12 @@ static double logit16_sim(const float *qt, const uint16_t *k, int d)
  *     e4m3's last mantissa bit);
  *   - r comes from the counter-based generator Philox4x64-10 (Salmon, Moraes,
  *     Dror and Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC 2011),
- *     key (seed, 0), counter (j, i, b*Hq + h, c / 8) for query row j, key i,
- *     query head h of batch b and channel c: the four 64-bit words of one
- *     call cut into eight 32-bit halves (low half first), the half of
- *     channel c being number c mod 8, r its top 20 bits.  The numbers depend
- *     on the logit and the channel alone, not on any blocking. */
+ *     key (seed, 0), counter (j, i, b*Hq + h, c / 12) for query row j, key
+ *     i, query head h of batch b and channel c: each of the four 64-bit
+ *     words of one call holds three 20-bit fields (bits 0-19, 20-39, 40-59;
+ *     bits 60-63 unused), and channel c takes field (c mod 12) mod 3 of word
+ *     (c mod 12) / 3.  The numbers depend on the logit and the channel alone,
+ *     not on any blocking. */
 
 /* (hi, lo) = a * b, full 128-bit product. */
 static void mulhilo64(uint64_t a, uint64_t b, uint64_t *hi, uint64_t *lo)
@@ -557,15 +558,14 @@ int oracle_sr_e4m3(const double *t, const uint32_t *r, double *y, int64_t n)
 /* 20-bit random integer of channel c of the logit (j, i) of head bh. */
 static uint32_t sr_bits(uint64_t seed, int64_t bh, int64_t j, int64_t i, int c, uint64_t w[4], int *have)
 {
-    if (c % 8 == 0 || !*have) {
-        const uint64_t ctr[4] = {(uint64_t)j, (uint64_t)i, (uint64_t)bh, (uint64_t)(c / 8)};
+    if (c % 12 == 0 || !*have) {
+        const uint64_t ctr[4] = {(uint64_t)j, (uint64_t)i, (uint64_t)bh, (uint64_t)(c / 12)};
         const uint64_t key[2] = {seed, 0};
         oracle_philox4x64_10(ctr, key, w);
         *have = 1;
     }
-    const uint64_t word = w[(c % 8) / 2];
-    const uint32_t half = (c % 2) ? (uint32_t)(word >> 32) : (uint32_t)word;
-    return half >> 12;
+    const int m = c % 12;
+    return (uint32_t)((w[m / 3] >> (20 * (m % 3))) & 0xFFFFFu);
 }
 
 /* Low-precision logit with stochastic rounding: the recursion of logit8 with

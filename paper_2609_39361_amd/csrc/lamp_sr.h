@@ -11,14 +11,16 @@
 //     20-bit integer;
 //   - r comes from the counter-based generator Philox4x64-10 (Salmon, Moraes,
 //     Dror and Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC 2011)
-//     under key (seed, 0) at counter (j, i, b*Hq + h, c / 8) for query row j,
-//     key i, query head h of batch b and channel c; the four 64-bit outputs
-//     are read as eight 32-bit halves, low half first, and channel c takes
-//     the top 20 bits of half c mod 8.
+//     under key (seed, 0) at counter (j, i, b*Hq + h, c / 12) for query row
+//     j, key i, query head h of batch b and channel c; each of the four
+//     64-bit outputs holds three 20-bit fields (bits 0-19, 20-39, 40-59), and
+//     channel c takes field (c mod 12) mod 3 of output (c mod 12) / 3, so
+//     one call serves twelve channels.
 // The random numbers depend on the logit and the channel only, so the 8-bit
 // logits are the same under every blocking and in the logits entry point.
 #pragma once
 #include <stdint.h>
+#include <utility>
 
 #include "lamp_device.h"
 
@@ -46,36 +48,68 @@ __device__ __forceinline__ void philox4x64_10(uint64_t (&c)[4], uint64_t k0, uin
     }
 }
 
-// The 20-bit random integer of channel u (0..7) of a group from its words.
-__device__ __forceinline__ uint32_t sr_r20(const uint64_t (&w)[4], int u)
+// The 20-bit random integer of channel u (0..11) of a group from its words.
+template <int U>
+__device__ __forceinline__ uint32_t sr_r20(const uint64_t (&w)[4])
 {
-    const uint64_t word = w[u >> 1];
-    const uint32_t half = (u & 1) ? (uint32_t)(word >> 32) : (uint32_t)word;
-    return half >> 12;
+    return (uint32_t)((w[U / 3] >> (20 * (U % 3))) & 0xFFFFFull);
 }
 
 // Stochastic rounding of a finite fp32 value to e4m3 (saturating at 448),
-// returned as the fp32 value.  In the normal e4m3 range the FP32 pattern has
-// exactly 20 bits below e4m3's last mantissa bit: adding r to them carries
-// into that bit when the rounding goes up.  Below 2^-6 the spacing is 2^-9
-// and the distance to the lower neighbour is taken in units of 2^-29 (all
-// steps exact).
+// returned as the fp32 value, without branches.  In the normal e4m3 range the
+// FP32 pattern has exactly 20 bits below e4m3's last mantissa bit: adding r
+// to them carries into that bit when the rounding goes up.  Below 2^-6 the
+// spacing is 2^-9: the magnitude in units of 2^-29, truncated to an integer
+// (the floor the rounding asks for), takes the same carry step, and the
+// result is converted back (all steps exact).
 __device__ __forceinline__ float sr_e4m3(float t, uint32_t r)
 {
     const uint32_t bits = __builtin_bit_cast(uint32_t, t);
     const uint32_t sign = bits & 0x80000000u;
     uint32_t a = bits & 0x7FFFFFFFu;
-    a = a < 0x43E00000u ? a : 0x43E00000u;                 // 448
-    uint32_t res;
-    if (a >= 0x3C800000u) {                                  // 2^-6
-        res = (a & 0xFFF00000u) + (((a & 0xFFFFFu) + r) & 0x100000u);
-    } else {
-        const float af = __builtin_bit_cast(float, a);
-        const float lo = __builtin_floorf(af * 512.0f) * (1.0f / 512.0f);
-        const uint32_t f20 = (uint32_t)((af - lo) * 536870912.0f);   // 2^29
-        res = __builtin_bit_cast(uint32_t, lo + (f20 + r >= 0x100000u ? 1.0f / 512.0f : 0.0f));
+    a = a < 0x43E00000u ? a : 0x43E00000u;                                 // 448
+    const bool sub = a < 0x3C800000u;                                       // below 2^-6
+    const uint32_t n = (uint32_t)(__builtin_bit_cast(float, a) * 536870912.0f);   // 2^29 units, floor
+    const uint32_t x = sub ? n : a;
+    const uint32_t y = (x & 0xFFF00000u) + (((x & 0xFFFFFu) + r) & 0x100000u);
+    const uint32_t ys = __builtin_bit_cast(uint32_t, (float)y * (1.0f / 536870912.0f));
+    return __builtin_bit_cast(float, (sub ? ys : y) | sign);
+}
+
+// The steps of one row over the channels U... of a group, in order.
+template <int NC, int... U>
+__device__ __forceinline__ float sr8_steps(const float (&qv)[NC], const float (&kv)[NC], const uint64_t (&w)[4],
+                                           float v, std::integer_sequence<int, U...>)
+{
+    ((v = sr_e4m3(__builtin_fmaf(qv[U], kv[U], v), sr_r20<U>(w))), ...);
+    return v;
+}
+
+// NC channels from c0 of one key and QPL rows: the group's Philox call, then
+// the NC steps of each row's recursion.
+template <int NC, int QPL>
+__device__ __forceinline__ void sr8_group(const float *const (&qrow)[QPL], const float *krow, int c0, uint64_t seed,
+                                          uint64_t bh, const int (&j)[QPL], uint32_t key, float (&y)[QPL])
+{
+    static_assert(NC % 4 == 0 && NC <= 12, "whole 4-channel loads, at most one call");
+    float kv[NC];
+#pragma unroll
+    for (int u = 0; u < NC; u += 4) {
+        const float4 a = *reinterpret_cast<const float4 *>(krow + c0 + u);
+        kv[u] = a.x; kv[u + 1] = a.y; kv[u + 2] = a.z; kv[u + 3] = a.w;
     }
-    return __builtin_bit_cast(float, res | sign);
+#pragma unroll
+    for (int s = 0; s < QPL; ++s) {
+        float qv[NC];
+#pragma unroll
+        for (int u = 0; u < NC; u += 4) {
+            const float4 a = *reinterpret_cast<const float4 *>(qrow[s] + c0 + u);
+            qv[u] = a.x; qv[u + 1] = a.y; qv[u + 2] = a.z; qv[u + 3] = a.w;
+        }
+        uint64_t w[4] = {(uint64_t)(uint32_t)j[s], (uint64_t)key, bh, (uint64_t)(c0 / 12)};
+        philox4x64_10(w, seed, 0);
+        y[s] = sr8_steps(qv, kv, w, y[s], std::make_integer_sequence<int, NC>{});
+    }
 }
 
 // 8-bit logits with stochastic rounding for 16 keys and QPL query rows per
@@ -87,33 +121,19 @@ template <int D, int QPL>
 __device__ __forceinline__ void sr8_chunk(const float *const (&qrow)[QPL], const float *k32, uint64_t seed,
                                           uint64_t bh, const int (&j)[QPL], int i0, uint32_t (&acc)[QPL][8])
 {
-    static_assert(D % 8 == 0, "channel groups of 8");
+    static_assert(D % 4 == 0, "channel groups of 4");
 #pragma unroll
     for (int s = 0; s < QPL; ++s)
 #pragma unroll
         for (int p = 0; p < 8; ++p) acc[s][p] = 0u;
     for (int kk = 0; kk < 16; ++kk) {
         const float *krow = k32 + (size_t)kk * D;
+        const uint32_t key = (uint32_t)(i0 + kk);
         float y[QPL];
 #pragma unroll
         for (int s = 0; s < QPL; ++s) y[s] = 0.0f;
-        for (int g = 0; g < D / 8; ++g) {
-            const float4 ka = *reinterpret_cast<const float4 *>(krow + 8 * g);
-            const float4 kb = *reinterpret_cast<const float4 *>(krow + 8 * g + 4);
-            const float kv[8] = {ka.x, ka.y, ka.z, ka.w, kb.x, kb.y, kb.z, kb.w};
-#pragma unroll
-            for (int s = 0; s < QPL; ++s) {
-                const float4 qa = *reinterpret_cast<const float4 *>(qrow[s] + 8 * g);
-                const float4 qb = *reinterpret_cast<const float4 *>(qrow[s] + 8 * g + 4);
-                const float qv[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
-                uint64_t w[4] = {(uint64_t)(uint32_t)j[s], (uint64_t)(uint32_t)(i0 + kk), bh, (uint64_t)g};
-                philox4x64_10(w, seed, 0);
-                float v = y[s];
-#pragma unroll
-                for (int u = 0; u < 8; ++u) v = sr_e4m3(__builtin_fmaf(qv[u], kv[u], v), sr_r20(w, u));
-                y[s] = v;
-            }
-        }
+        for (int g = 0; g < D / 12; ++g) sr8_group<12, QPL>(qrow, krow, 12 * g, seed, bh, j, key, y);
+        if constexpr (D % 12 != 0) sr8_group<D % 12, QPL>(qrow, krow, D / 12 * 12, seed, bh, j, key, y);
         // the code of key kk into its byte (exact: y is an e4m3 value)
 #pragma unroll
         for (int s = 0; s < QPL; ++s) {

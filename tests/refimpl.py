@@ -86,10 +86,10 @@ def sr_words(seed, j, i, bh, g):
 
 
 def sr_r20(words, c):
-    """20-bit random integer of channel c from the words of its group."""
-    w = int(words[(c % 8) // 2])
-    half = (w >> 32) if c % 2 else (w & 0xFFFFFFFF)
-    return half >> 12
+    """20-bit random integer of channel c from the words of its group of 12:
+    field (c mod 12) mod 3 (bits 0-19, 20-39, 40-59) of word (c mod 12) // 3."""
+    m = c % 12
+    return (int(words[m // 3]) >> (20 * (m % 3))) & 0xFFFFF
 
 
 def sr_round(t, r):
@@ -112,9 +112,9 @@ def y8_tile_sr(qt, kf, seed, bh, rows, keys):
     r = np.zeros((d, T, bq))
     for a, i in enumerate(keys):
         for bb, j in enumerate(rows):
-            for g in range(d // 8):
+            for g in range(-(-d // 12)):
                 wds = sr_words(seed, int(j), int(i), bh, g)
-                for c in range(8 * g, 8 * g + 8):
+                for c in range(12 * g, min(12 * g + 12, d)):
                     r[c, a, bb] = sr_r20(wds, c)
     acc = np.zeros((T, bq))
     for c in range(d):

@@ -5,8 +5,9 @@ Readings (the paper fixes neither generator nor bit count): each FP32 FMA
 result is rounded to one of its two e4m3 neighbours, away from zero when
 floor(2^20 * distance to the lower one / spacing) + r >= 2^20 for a 20-bit
 uniform r, saturating at 448; r comes from Philox4x64-10 keyed by (seed, 0)
-at counter (query row, key, b*Hq + h, channel / 8), half (channel mod 8) of
-the four output words, top 20 bits.
+at counter (query row, key, b*Hq + h, channel / 12): three 20-bit fields of
+each of the four output words, field (channel mod 12) mod 3 of word
+(channel mod 12) / 3.
 
 Pinned by: numpy's own Philox4x64-10 (an independent implementation of the
 published generator); the rounding against the enumerated e4m3 grid and a
