@@ -5,7 +5,6 @@ Bar as for the round-to-nearest path: 8-bit logit codes and recompute masks
 bit-exact (the random numbers come from the same counter-based generator on
 both sides, written separately); O within 2e-3 of max|O|; lse within 1e-4.
 """
-import ctypes
 import math
 import sys
 import time

@@ -9,7 +9,6 @@ from fractions import Fraction
 
 import numpy as np
 import pytest
-import torch
 
 from oracle import oracle as O
 import fpmodel as M

@@ -1,7 +1,6 @@
 """Pins of the oracle's exponential tables (paper Sec. 3.3: 8-bit LUT exp; Sec.
 4.1: exponentials correctly rounded) and of exp_doc, the documented fp64
 exponential of the rescale factor (Sec. 2.2: alpha_hat in high precision)."""
-import math
 
 import mpmath as mp
 import numpy as np

@@ -19,7 +19,6 @@ rest on; they check the analysis itself, independently of the oracle.
 import math
 
 import numpy as np
-import pytest
 import torch
 
 
