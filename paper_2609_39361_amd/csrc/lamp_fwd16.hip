@@ -275,30 +275,40 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
         const int ck0 = tile * KPT + w * BK;
         uint16_t *yc = ycode_of(tile);
         float *m8s = m8s_of(tile);
+        bool full = true;
 #pragma unroll
-        for (int s = 0; s < QPL; ++s) {
-            float mx = NEG_INF;
-            if (done) {
-                const bool full = ck0 >= vlo[s] && ck0 + 15 <= vhi[s];
-                uint32_t packed[8];
+        for (int s = 0; s < QPL; ++s) full &= ck0 >= vlo[s] && ck0 + 15 <= vhi[s];
+        // FULL: every key of the sub-block visible to every row of the wave
+        // (a uniform branch), so no per-key visibility test
+        auto run = [&](auto full_c) {
+            constexpr bool FULL = decltype(full_c)::value;
 #pragma unroll
-                for (int pp = 0; pp < 8; ++pp) {
-                    const float2 yv = SIMP ? make_float2(bf16_value(a8[s][pp] & 0xFFFFu), bf16_value(a8[s][pp] >> 16))
-                                           : unpk_e4m3(a8[s][pp]);
-                    const int i0 = ck0 + 2 * pp;
-                    // invisible keys enter as -inf, by selection rather than branches
-                    const float x0 = (full || visible(s, i0)) ? yv.x : NEG_INF;
-                    const float x1 = (full || visible(s, i0 + 1)) ? yv.y : NEG_INF;
-                    mx = x0 > mx ? x0 : mx;
-                    mx = x1 > mx ? x1 : mx;
-                    packed[pp] = SIMP ? a8[s][pp] : (a8[s][pp] & 0xFFu) | ((a8[s][pp] & 0xFF00u) << 8);
+            for (int s = 0; s < QPL; ++s) {
+                float mx = NEG_INF;
+                if (done) {
+                    uint32_t packed[8];
+#pragma unroll
+                    for (int pp = 0; pp < 8; ++pp) {
+                        const float2 yv = SIMP ? make_float2(bf16_value(a8[s][pp] & 0xFFFFu),
+                                                             bf16_value(a8[s][pp] >> 16))
+                                               : unpk_e4m3(a8[s][pp]);
+                        const int i0 = ck0 + 2 * pp;
+                        // invisible keys enter as -inf, by selection rather than branches
+                        const float x0 = (FULL || visible(s, i0)) ? yv.x : NEG_INF;
+                        const float x1 = (FULL || visible(s, i0 + 1)) ? yv.y : NEG_INF;
+                        mx = x0 > mx ? x0 : mx;
+                        mx = x1 > mx ? x1 : mx;
+                        packed[pp] = SIMP ? a8[s][pp] : (a8[s][pp] & 0xFFu) | ((a8[s][pp] & 0xFF00u) << 8);
+                    }
+                    u32x4 *dst = reinterpret_cast<u32x4 *>(yc + row[s] * YP + w * BK);
+                    dst[0] = u32x4{packed[0], packed[1], packed[2], packed[3]};
+                    dst[1] = u32x4{packed[4], packed[5], packed[6], packed[7]};
                 }
-                u32x4 *dst = reinterpret_cast<u32x4 *>(yc + row[s] * YP + w * BK);
-                dst[0] = u32x4{packed[0], packed[1], packed[2], packed[3]};
-                dst[1] = u32x4{packed[4], packed[5], packed[6], packed[7]};
+                m8s[w * BQ + row[s]] = mx;
             }
-            m8s[w * BQ + row[s]] = mx;
-        }
+        };
+        if (!wave_any(!full)) run(std::true_type());
+        else run(std::false_type());
     };
     // the margin test of every sub-block of `tile` against mu_hat (Eq. (7)):
     // mu_hat_j > fma(|mu_hat_j|, delta, m8); columns without a visible entry
