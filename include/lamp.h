@@ -23,7 +23,9 @@
  *   - Every function returns a lamp_status; nothing aborts or throws across
  *     the ABI.  lamp_last_error() describes the last failure of the calling
  *     thread.
- *   - Inputs must be finite; non-finite inputs give unspecified results.
+ *   - Inputs are assumed finite.  A non-finite q, k or v element gives
+ *     unspecified results unless the call asks for the check
+ *     (LAMP_CHECK_FINITE), which then returns LAMP_ERR_NONFINITE_INPUT.
  */
 #ifndef LAMP_H
 #define LAMP_H
@@ -40,8 +42,14 @@ typedef enum {
     LAMP_ERR_INVALID_ARG = 1,   /* null pointer, negative size, bad parameter */
     LAMP_ERR_UNSUPPORTED = 2,   /* valid but not built: shape or block sizes */
     LAMP_ERR_HIP = 3,           /* a HIP runtime call failed */
-    LAMP_ERR_INIT = 4           /* device tables could not be built */
+    LAMP_ERR_INIT = 4,          /* device tables could not be built (or, for
+                                   lamp_attn_fwd_noalloc, were not built yet) */
+    LAMP_ERR_NONFINITE_INPUT = 5,  /* LAMP_CHECK_FINITE found a NaN or an infinity in q, k or v */
+    LAMP_ERR_WORKSPACE = 6      /* the workspace is too small and may not grow now */
 } lamp_status;
+
+/* Optional arguments of the forward entry points (defined below). */
+struct lamp_fwd_extra;
 
 /* Mask codes, one byte per (query block, key sub-block). */
 enum {
@@ -78,17 +86,116 @@ enum {
  * of sub-blocks beyond N being 3.  B = 0 or N = 0 returns LAMP_OK and writes
  * nothing.
  *
- * The first call on a device builds the library's exponential tables; the
- * library also keeps a grow-only per-device workspace (fp32 copies of the
- * pre-scaled Q, of K and of V transposed), allocated with hipMalloc when a
- * call needs more than it holds.  Calls that overlap on one device race on
- * that workspace.
+ * extra: NULL, or the optional outputs and the workspace (lamp_fwd_extra
+ * below).
+ *
+ * Workspace.  A call needs lamp_attn_fwd_workspace_size(...) bytes of device
+ * memory for the prepass (the pre-scaled Q and K in fp32, V transposed) and a
+ * check flag.  With extra->workspace set, the call uses that memory and
+ * allocates nothing; calls on distinct workspaces may overlap.  Otherwise it
+ * uses the library's per-device workspace: when that is too small the call
+ * allocates a larger one (never while `stream` is being captured into a graph:
+ * then LAMP_ERR_WORKSPACE) and keeps the old one until lamp_reserve or
+ * lamp_shutdown, so launches still in flight never see memory freed;
+ * lamp_reserve sizes it ahead of time.  Calls that overlap on one device
+ * without their own workspace race on the library's.
+ *
+ * The first call on a device builds the library's exponential tables (or
+ * lamp_init, ahead of time).
  */
 int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                   int B, int Hq, int Hkv, int N, int d,
                   int causal, int window, int bq, int bk, int nk,
                   double delta, double tau, unsigned flags,
-                  float *o, float *lse, uint8_t *mask, void *stream);
+                  float *o, float *lse, uint8_t *mask,
+                  const struct lamp_fwd_extra *extra, void *stream);
+
+/*
+ * Optional arguments of the forward entry points (lamp_attn_fwd,
+ * lamp_attn_fwd_sr, lamp_attn_fwd_noalloc; lamp_attn_decode takes only the
+ * workspace).  A zero-initialised struct asks for nothing.
+ *
+ * stats: DEVICE pointer to LAMP_STATS_WORDS(nk) uint64_t counters that the
+ *   call ADDS to (the caller zeroes them); word meanings below.
+ * dbg_y8, dbg_y16, dbg_qb0, dbg_nqb: observables of the forward kernel for
+ *   the query blocks [dbg_qb0, dbg_qb0 + dbg_nqb) of every (b, h), for tests.
+ *   With Nt = ceil(N/(bk*nk))*bk*nk keys and rows r = (qb - dbg_qb0)*bq + i:
+ *   dbg_y8 (DEVICE, uint8 [B][Hq][dbg_nqb*bq][Nt]) receives the e4m3 code of
+ *   every visible pair's 8-bit logit as the forward kernel computed it (Alg. 1,
+ *   low-precision accumulation), 0xFF elsewhere and everywhere at tau = 0;
+ *   dbg_y16 (DEVICE, uint16 [B][Hq][dbg_nqb*bq][Nt]) receives the e4m11 code
+ *   of every visible pair's 16-bit logit in the sub-blocks recomputed in 16
+ *   bits (mask codes 1 and 2), 0xFFFF elsewhere.  Either pointer may be NULL.
+ *   Rows at or beyond N hold 0xFF / 0xFFFF.  Not with LAMP_SIM_PROFILE
+ *   (LAMP_ERR_UNSUPPORTED).  The arrays are filled with hipMemsetAsync on
+ *   `stream` first.
+ * workspace, workspace_bytes: DEVICE memory for the prepass (above), aligned
+ *   to 256 bytes, at least the size the workspace-size call gives; the
+ *   library writes it and does not retain it after the stream has passed the
+ *   call.
+ */
+typedef struct lamp_fwd_extra {
+    uint64_t *stats;
+    uint8_t *dbg_y8;
+    uint16_t *dbg_y16;
+    int dbg_qb0;
+    int dbg_nqb;
+    void *workspace;
+    size_t workspace_bytes;
+} lamp_fwd_extra;
+
+/*
+ * Statistics words (lamp_fwd_extra.stats), summed over every query block of
+ * the call.  Words 0-5 and the histogram follow from the definition of the
+ * method (the CPU reference counts them the same way); words 6 and 7 describe
+ * the forward kernel's speculative schedule.
+ *   LAMP_STAT_TILES     (query block, key tile) pairs with an active sub-block
+ *   LAMP_STAT_STAGE1    sub-blocks recomputed by the first stage (mask code 1;
+ *                       every active sub-block at tau = 0)
+ *   LAMP_STAT_STAGE2    sub-blocks recomputed by the second stage (code 2)
+ *   LAMP_STAT_INACTIVE  sub-blocks without a visible pair (code 3)
+ *   LAMP_STAT_SAT8      visible 8-bit logits whose accumulation was clamped to
+ *                       +-448 in some step (Sec. 3.3 assumes QK-Norm so that
+ *                       this never happens): round-to-nearest gave a value
+ *                       beyond 448, or, with stochastic rounding, |t| > 448;
+ *                       0 in the SIM profile, which does not saturate
+ *   LAMP_STAT_SAT16     16-bit logits of recomputed sub-blocks (visible pairs)
+ *                       whose rounding to e4m11 was clamped to +-511.875; 0
+ *                       in the SIM profile
+ *   LAMP_STAT_SPEC_UNUSED  sub-blocks whose 16-bit logits the kernel computed
+ *                       speculatively but did not use
+ *   LAMP_STAT_LATE16    sub-blocks recomputed in 16 bits outside the
+ *                       speculative batch (one at a time or after stage 2)
+ *   LAMP_STAT_HIST + c  key tiles (with an active sub-block) in which c of the
+ *                       nk sub-blocks were recomputed in 16 bits, c = 0..nk
+ */
+enum {
+    LAMP_STAT_TILES = 0,
+    LAMP_STAT_STAGE1 = 1,
+    LAMP_STAT_STAGE2 = 2,
+    LAMP_STAT_INACTIVE = 3,
+    LAMP_STAT_SAT8 = 4,
+    LAMP_STAT_SAT16 = 5,
+    LAMP_STAT_SPEC_UNUSED = 6,
+    LAMP_STAT_LATE16 = 7,
+    LAMP_STAT_HIST = 8
+};
+#define LAMP_STATS_WORDS(nk) (LAMP_STAT_HIST + (nk) + 1)
+
+/* Bytes of workspace lamp_attn_fwd / lamp_attn_fwd_sr need for these sizes
+ * (0 for invalid sizes; B = 0 or N = 0 needs none). */
+size_t lamp_attn_fwd_workspace_size(int B, int Hq, int Hkv, int N, int d, int bq, int bk, int nk);
+
+/* Bytes of workspace lamp_attn_decode needs (0 for invalid sizes). */
+size_t lamp_attn_decode_workspace_size(int B, int Hq, int Hkv, int M, int N, int d);
+
+/*
+ * lamp_reserve -- grow the library's own workspace of `device` to at least
+ * `bytes` now, so that later calls without a workspace of their own never
+ * allocate.  Synchronous: waits for the device, then frees the workspaces
+ * earlier growth retired.  The workspace never shrinks.
+ */
+int lamp_reserve(int device, size_t bytes);
 
 /* Variants of Algorithm 1 (flags of lamp_attn_fwd). */
 enum {
@@ -112,7 +219,13 @@ enum {
      * exponential is exp(-shift) correctly rounded to 3 or 11 bits; the row
      * sum of a tile's exponentials is the fp64 sum over keys in ascending
      * order.  Logits are assumed finite. */
-    LAMP_SIM_PROFILE = 4
+    LAMP_SIM_PROFILE = 4,
+    /* Check q, k and v for NaN and infinity in the prepass (which reads every
+     * element anyway) and return LAMP_ERR_NONFINITE_INPUT without running the
+     * forward kernel if one is found.  The call then waits for its prepass on
+     * `stream` (it is synchronous), and refuses a stream being captured into a
+     * graph (LAMP_ERR_INVALID_ARG).  Applies in every mode. */
+    LAMP_CHECK_FINITE = 8
 };
 
 /*
@@ -133,8 +246,8 @@ enum {
  * lamp_attn_fwd (the 16-bit logits keep round-to-nearest; tau = 0 computes
  * no 8-bit logit and equals lamp_attn_fwd).
  *
- * Arguments, layouts, outputs and workspace as lamp_attn_fwd; flags: 0,
- * LAMP_STAGE1_OFF and/or LAMP_MU_TRUNC; LAMP_SIM_PROFILE gives
+ * Arguments, layouts, outputs, extra and workspace as lamp_attn_fwd; flags: 0,
+ * LAMP_STAGE1_OFF, LAMP_MU_TRUNC and/or LAMP_CHECK_FINITE; LAMP_SIM_PROFILE gives
  * LAMP_ERR_UNSUPPORTED.  Built for the configurations lamp_attn_fwd lists for
  * the formats of Sec. 3.3.  The generator costs some hundred VALU operations
  * per 8 multiply-adds: expect this pass to run far slower than
@@ -144,7 +257,8 @@ int lamp_attn_fwd_sr(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                      int B, int Hq, int Hkv, int N, int d,
                      int causal, int window, int bq, int bk, int nk,
                      double delta, double tau, unsigned flags, uint64_t seed,
-                     float *o, float *lse, uint8_t *mask, void *stream);
+                     float *o, float *lse, uint8_t *mask,
+                     const struct lamp_fwd_extra *extra, void *stream);
 
 /*
  * lamp_attn_decode -- LampAttention for query rows against a key/value cache
@@ -166,15 +280,17 @@ int lamp_attn_fwd_sr(const uint16_t *q, const uint16_t *k, const uint16_t *v,
  * recomputed by the look-ahead test -- every key at tau = 0 --, 2 recomputed
  * by the knapsack, 3 invisible).  Built: tk = 64, d in {64, 128, 256};
  * flags must be 0.  B = 0 or M = 0 returns LAMP_OK and writes nothing.  The
- * library keeps a grow-only per-device workspace (the pre-scaled queries, the
- * 8-bit logit codes, the exponentials, per-tile rescale factors and partial
- * outputs: about B*Hq*M*(5*ceil(N/64)*64 + 4d*(1 + ceil(N/512))) bytes);
- * calls that overlap on one device race on it.
+ * workspace (the pre-scaled queries, the 8-bit logit codes, the
+ * exponentials, per-tile rescale factors and partial outputs:
+ * lamp_attn_decode_workspace_size bytes) comes from extra->workspace or from
+ * the library's per-device workspace, as for lamp_attn_fwd; extra->stats and
+ * the dbg pointers must be NULL (LAMP_ERR_UNSUPPORTED).
  */
 int lamp_attn_decode(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                      int B, int Hq, int Hkv, int M, int N, int d,
                      int causal, int window, int tk, double delta, double tau, unsigned flags,
-                     float *o, float *lse, uint8_t *mask, void *stream);
+                     float *o, float *lse, uint8_t *mask,
+                     const struct lamp_fwd_extra *extra, void *stream);
 
 /*
  * lamp_attn_logits8 -- the 8-bit logits alone (Alg. 1, first accumulation;
@@ -249,7 +365,8 @@ int lamp_issue_rates(double *ns_per_simd, void *stream);
 /* Build the device tables of `device` now (otherwise done by the first call). */
 int lamp_init(int device);
 
-/* Release every device table and workspace the library holds. */
+/* Release every device table and workspace the library holds (waits for
+ * every device the library used). */
 void lamp_shutdown(void);
 
 /*

@@ -61,13 +61,18 @@ static const ofmt_t F_UE5M11_SHIFT = {5, 11, 15, 0, 131040.0};
 static const ofmt_t F_UE5M3_EXP = {5, 3, 31, 0, 1.875};
 static const ofmt_t F_UE5M11_EXP = {5, 11, 31, 0, 2.0 - 0x1p-11};
 
-/* Round an exact double to the format grid (RNE, subnormals, saturation). */
-static double round_to_fmt(double x, const ofmt_t *f)
+/* Round an exact double to the format grid (RNE, subnormals, saturation);
+ * *sat (may be NULL) is set to 1 when the rounded magnitude exceeded the
+ * largest value and was clamped to it. */
+static double round_to_fmt_s(double x, const ofmt_t *f, int *sat)
 {
     if (isnan(x)) return x;
     if (x == 0.0) return x;                       /* keeps the sign of zero */
     double ax = fabs(x);
-    if (isinf(ax)) return copysign(f->maxval, x);
+    if (isinf(ax)) {
+        if (sat) *sat = 1;
+        return copysign(f->maxval, x);
+    }
     int E;
     (void)frexp(ax, &E);                          /* ax = fr * 2^E, fr in [0.5,1) */
     int e = E - 1;                                /* ax in [2^e, 2^(e+1)) */
@@ -75,9 +80,14 @@ static double round_to_fmt(double x, const ofmt_t *f)
     if (e < emin) e = emin;
     double quantum = ldexp(1.0, e - f->mbits);
     double r = nearbyint(ax / quantum) * quantum; /* default mode: ties to even */
-    if (r > f->maxval) r = f->maxval;
+    if (r > f->maxval) {
+        r = f->maxval;
+        if (sat) *sat = 1;
+    }
     return copysign(r, x);
 }
+
+static double round_to_fmt(double x, const ofmt_t *f) { return round_to_fmt_s(x, f, NULL); }
 
 /* Code of a value that already lies on the grid. */
 static uint32_t encode_fmt(double v, const ofmt_t *f)
@@ -432,34 +442,58 @@ static void prescale(const uint16_t *q, int d, float s, float *qt)
 
 /* Low-precision logit (Sec. 4.1 and Alg. 1): recursive summation with one
  * FP32 FMA per step, the running sum rounded to e4m3 after every step,
- * channels in ascending order, starting from +0. */
-static double logit8(const float *qt, const uint16_t *k, int d)
+ * channels in ascending order, starting from +0.  *sat (may be NULL) is set
+ * when some step was clamped to +-448 (Sec. 3.3 assumes QK-Norm keeps the
+ * sums in range; these inputs need not). */
+static double logit8_s(const float *qt, const uint16_t *k, int d, int *sat)
 {
     float acc = 0.0f;
     for (int c = 0; c < d; ++c) {
         float t = fmaf(qt[c], bf16_to_f32(k[c]), acc);
-        acc = (float)round_to_fmt((double)t, &F_E4M3);
+        acc = (float)round_to_fmt_s((double)t, &F_E4M3, sat);
     }
     return (double)acc;
 }
 
+static double logit8(const float *qt, const uint16_t *k, int d) { return logit8_s(qt, k, d, NULL); }
+
 /* High-precision logit (Alg. 1, recompute steps; Sec. 3.3 gives e4m11 as the
- * 16-bit accumulator format).  Reading: as in the paper's simulation (Sec.
- * 4.1: FP32 storage, recursive summation with FP32 FMA), the dot product is
- * accumulated by a sequential FP32 FMA chain in ascending channel order,
- * starting from +0, and the sum is rounded once to e4m11 (saturating). */
-static double logit16(const float *qt, const uint16_t *k, int d)
+ * 16-bit accumulator format).  Reading: the dot product is accumulated by a
+ * sequential FP32 FMA chain in ascending channel order, starting from +0,
+ * and the sum is rounded once to e4m11 (saturating; *sat set when clamped).
+ * This is 16-bit accumulation taken at FP32 accumulation precision, the
+ * reading named for the recompute (FP32 accumulation); the paper's own
+ * simulation keeps its numbers in FP32 and accumulates by FP32 FMA (Sec. 4.1).
+ * The literal alternative of Sec. 3.3, e4m11 as the accumulator itself, is
+ * logit16_step below. */
+static double logit16_s(const float *qt, const uint16_t *k, int d, int *sat)
 {
     float acc = 0.0f;
     for (int c = 0; c < d; ++c) acc = fmaf(qt[c], bf16_to_f32(k[c]), acc);
-    return round_to_fmt((double)acc, &F_E4M11);
+    return round_to_fmt_s((double)acc, &F_E4M11, sat);
+}
+
+static double logit16(const float *qt, const uint16_t *k, int d) { return logit16_s(qt, k, d, NULL); }
+
+/* The literal reading of Sec. 3.3 ("16-bit e4m11 format to accumulate"): the
+ * 8-bit recursion with e4m11 in place of e4m3, i.e. every FP32 FMA result
+ * rounded to e4m11 (saturating) before the next step. */
+static double logit16_step(const float *qt, const uint16_t *k, int d, int *sat)
+{
+    float acc = 0.0f;
+    for (int c = 0; c < d; ++c) {
+        float t = fmaf(qt[c], bf16_to_f32(k[c]), acc);
+        acc = (float)round_to_fmt_s((double)t, &F_E4M11, sat);
+    }
+    return (double)acc;
 }
 
 /* SIM profile logits: the same recursions with the roundings of the profile
  * (3 mantissa bits after every step; one rounding to 11 bits at the end of
- * the FP32 chain, as for the e4m11 logit). */
-static double logit8_sim(const float *qt, const uint16_t *k, int d)
+ * the FP32 chain, as for the e4m11 logit).  The profile does not saturate. */
+static double logit8_sim_s(const float *qt, const uint16_t *k, int d, int *sat)
 {
+    (void)sat;
     float acc = 0.0f;
     for (int c = 0; c < d; ++c) {
         float t = fmaf(qt[c], bf16_to_f32(k[c]), acc);
@@ -468,11 +502,28 @@ static double logit8_sim(const float *qt, const uint16_t *k, int d)
     return (double)acc;
 }
 
-static double logit16_sim(const float *qt, const uint16_t *k, int d)
+static double logit8_sim(const float *qt, const uint16_t *k, int d) { return logit8_sim_s(qt, k, d, NULL); }
+
+static double logit16_sim_s(const float *qt, const uint16_t *k, int d, int *sat)
 {
+    (void)sat;
     float acc = 0.0f;
     for (int c = 0; c < d; ++c) acc = fmaf(qt[c], bf16_to_f32(k[c]), acc);
     return round_sim((double)acc, 11);
+}
+
+static double logit16_sim(const float *qt, const uint16_t *k, int d) { return logit16_sim_s(qt, k, d, NULL); }
+
+/* The literal Sec. 3.3 reading in the SIM profile: 11 bits after every step. */
+static double logit16_sim_step(const float *qt, const uint16_t *k, int d, int *sat)
+{
+    (void)sat;
+    float acc = 0.0f;
+    for (int c = 0; c < d; ++c) {
+        float t = fmaf(qt[c], bf16_to_f32(k[c]), acc);
+        acc = (float)round_sim((double)t, 11);
+    }
+    return (double)acc;
 }
 
 /* ------------------------------------------------------------------------ */
@@ -569,17 +620,25 @@ static uint32_t sr_bits(uint64_t seed, int64_t bh, int64_t j, int64_t i, int c, 
 }
 
 /* Low-precision logit with stochastic rounding: the recursion of logit8 with
- * sr_e4m3 in place of round-to-nearest. */
-static double logit8_sr(const float *qt, const uint16_t *k, int d, uint64_t seed, int64_t bh, int64_t j, int64_t i)
+ * sr_e4m3 in place of round-to-nearest; *sat (may be NULL) is set when some
+ * step's |t| exceeded 448 and was clamped. */
+static double logit8_sr_s(const float *qt, const uint16_t *k, int d, uint64_t seed, int64_t bh, int64_t j,
+                          int64_t i, int *sat)
 {
     float acc = 0.0f;
     uint64_t w[4];
     int have = 0;
     for (int c = 0; c < d; ++c) {
         float t = fmaf(qt[c], bf16_to_f32(k[c]), acc);
+        if (sat && fabs((double)t) > F_E4M3.maxval) *sat = 1;
         acc = (float)sr_e4m3((double)t, sr_bits(seed, bh, j, i, c, w, &have));
     }
     return (double)acc;
+}
+
+static double logit8_sr(const float *qt, const uint16_t *k, int d, uint64_t seed, int64_t bh, int64_t j, int64_t i)
+{
+    return logit8_sr_s(qt, k, d, seed, bh, j, i, NULL);
 }
 
 static int visible(int64_t i, int64_t j, int causal, int window)
@@ -671,6 +730,35 @@ int oracle_logits16(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv
     return 0;
 }
 
+/* Y16 codes by the literal reading of Sec. 3.3 (e4m11 as the accumulator,
+ * rounded after every FP32 FMA; logit16_step), same layout as
+ * oracle_logits16. */
+int oracle_logits16_step(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv, int N, int d,
+                         int causal, int window, int row0, int nrows, uint16_t *out, int nthreads)
+{
+    if (Hq % Hkv) return -1;
+    int G = Hq / Hkv;
+    float s = scale_of(d);
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for collapse(3) schedule(dynamic)
+#endif
+    for (int b = 0; b < B; ++b)
+        for (int h = 0; h < Hq; ++h)
+            for (int r = 0; r < nrows; ++r) {
+                int64_t j = row0 + r;
+                float qt[1024];
+                prescale(q + (((int64_t)b * Hq + h) * N + j) * d, d, s, qt);
+                const uint16_t *kb = k + ((int64_t)b * Hkv + h / G) * N * d;
+                uint16_t *o = out + (((int64_t)b * Hq + h) * nrows + r) * N;
+                for (int64_t i = 0; i < N; ++i) {
+                    if (!visible(i, j, causal, window)) { o[i] = 0xFFFF; continue; }
+                    o[i] = (uint16_t)encode_fmt(logit16_step(qt, kb + i * d, d, NULL), &F_E4M11);
+                }
+            }
+    return 0;
+}
+
 /* SIM profile logit values (high = 0: 8-bit recursion, 1: 16-bit), same
  * layout as above; invisible entries NaN. */
 int oracle_logits_sim(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv, int N, int d,
@@ -716,8 +804,21 @@ enum { MASK_LOW = 0, MASK_STAGE1 = 1, MASK_STAGE2 = 2, MASK_INACTIVE = 3 };
  *  ORACLE_SIM: the "SIM" precision profile above (Sec. 4.1) in place of the
  *    hardware formats of Sec. 3.3, in every mode;
  *  ORACLE_SR8: the 8-bit logits rounded stochastically (logit8_sr, with the
- *    seed argument), in the modes that compute them; not with ORACLE_SIM. */
-enum { ORACLE_STAGE1_OFF = 1, ORACLE_MU_TRUNC = 2, ORACLE_SIM = 4, ORACLE_SR8 = 8 };
+ *    seed argument), in the modes that compute them; not with ORACLE_SIM;
+ *  ORACLE_Y16_STEP: the 16-bit logits by the literal reading of Sec. 3.3,
+ *    e4m11 (or, in the SIM profile, 11 bits) as the accumulator, rounded after
+ *    every FP32 FMA (logit16_step), instead of the FP32 chain rounded once.
+ *    An alternative reading for study; the GPU library does not build it. */
+enum { ORACLE_STAGE1_OFF = 1, ORACLE_MU_TRUNC = 2, ORACLE_SIM = 4, ORACLE_SR8 = 8, ORACLE_Y16_STEP = 16 };
+
+/* Statistics words (lamp_oracle_fwd_ex), counted from the definitions: the
+ * (query block, key tile) pairs with an active sub-block, the stage-1 and
+ * stage-2 sub-blocks (mask codes 1 and 2), the inactive ones (code 3), the
+ * visible 8-bit logits whose recursion was clamped at some step, the visible
+ * 16-bit logits of recomputed sub-blocks whose rounding was clamped, two
+ * words of the GPU kernel's schedule (left 0 here), then the histogram of
+ * 16-bit sub-blocks per active tile, 0..nk. */
+enum { OST_TILES = 0, OST_S1, OST_S2, OST_INACTIVE, OST_SAT8, OST_SAT16, OST_HIST = 8 };
 
 /* x truncated (rounded toward zero) to e4m3; reading: values beyond the
  * largest e4m3 number saturate to +-448; infinities are kept. */
@@ -764,6 +865,7 @@ typedef struct {
     uint64_t seed;
     double *o, *lse;
     uint8_t *mask;
+    uint64_t *stats;
 } fwd_args_t;
 
 /* One query block (Alg. 1, body of the outer parallel loop). */
@@ -789,9 +891,13 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
     const int mu_trunc = !pure8 && !all16 && (A->flags & ORACLE_MU_TRUNC);
     const int sim = (A->flags & ORACLE_SIM) != 0;
     const int sr8 = (A->flags & ORACLE_SR8) != 0;
+    const int y16step = (A->flags & ORACLE_Y16_STEP) != 0;
     const int64_t bh = (int64_t)b * A->Hq + h;
-    double (*const y8f)(const float *, const uint16_t *, int) = sim ? logit8_sim : logit8;
-    double (*const y16f)(const float *, const uint16_t *, int) = sim ? logit16_sim : logit16;
+    double (*const y8f)(const float *, const uint16_t *, int, int *) = sim ? logit8_sim_s : logit8_s;
+    double (*const y16f)(const float *, const uint16_t *, int, int *) =
+        sim ? (y16step ? logit16_sim_step : logit16_sim_s) : (y16step ? logit16_step : logit16_s);
+    /* statistics of this query block (added to A->stats at the end) */
+    uint64_t st_tiles = 0, st_s1 = 0, st_s2 = 0, st_sat8 = 0, st_sat16 = 0, st_hist[17] = {0};
     double (*const expf_)(double, double, int) = sim ? shifted_exp_sim : shifted_exp;
 
     float *qt = (float *)malloc(sizeof(float) * (size_t)bq * d);
@@ -840,10 +946,14 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
          * precision).  In the all-16-bit mode they are never used. */
         if (!all16) {
             for (int ii = 0; ii < T; ++ii)
-                for (int j = 0; j < bq; ++j)
+                for (int j = 0; j < bq; ++j) {
+                    int sat = 0;
                     Y[(size_t)ii * bq + j] = vis[(size_t)ii * bq + j]
-                        ? (sr8 ? logit8_sr(qt + (size_t)j * d, kbase + (k0 + ii) * d, d, A->seed, bh, q0 + j, k0 + ii)
-                               : y8f(qt + (size_t)j * d, kbase + (k0 + ii) * d, d)) : NAN;
+                        ? (sr8 ? logit8_sr_s(qt + (size_t)j * d, kbase + (k0 + ii) * d, d, A->seed, bh, q0 + j,
+                                             k0 + ii, &sat)
+                               : y8f(qt + (size_t)j * d, kbase + (k0 + ii) * d, d, &sat)) : NAN;
+                    st_sat8 += (uint64_t)sat;
+                }
         }
         /* Column maxima per sub-block: m8[theta][j] (Sec. 3.1, C and T). */
         for (int th = 0; th < nk; ++th)
@@ -874,7 +984,9 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
                     for (int j = 0; j < bq; ++j) {
                         size_t ix = (size_t)ii * bq + j;
                         if (!vis[ix]) continue;
-                        Y[ix] = y16f(qt + (size_t)j * d, kbase + (k0 + ii) * d, d);
+                        int sat = 0;
+                        Y[ix] = y16f(qt + (size_t)j * d, kbase + (k0 + ii) * d, d, &sat);
+                        st_sat16 += (uint64_t)sat;
                         if (Y[ix] > muh[j]) muh[j] = Y[ix];
                     }
             }
@@ -920,7 +1032,9 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
                     for (int j = 0; j < bq; ++j) {
                         size_t ix = (size_t)ii * bq + j;
                         if (!vis[ix]) continue;
-                        Y[ix] = y16f(qt + (size_t)j * d, kbase + (k0 + ii) * d, d);
+                        int sat = 0;
+                        Y[ix] = y16f(qt + (size_t)j * d, kbase + (k0 + ii) * d, d, &sat);
+                        st_sat16 += (uint64_t)sat;
                         if (Y[ix] > muh[j]) muh[j] = Y[ix];
                     }
             }
@@ -1004,7 +1118,9 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
                     for (int j = 0; j < bq; ++j) {
                         size_t ix = (size_t)ii * bq + j;
                         if (!vis[ix]) continue;
-                        Y[ix] = y16f(qt + (size_t)j * d, kbase + (k0 + ii) * d, d);
+                        int sat = 0;
+                        Y[ix] = y16f(qt + (size_t)j * d, kbase + (k0 + ii) * d, d, &sat);
+                        st_sat16 += (uint64_t)sat;
                         E[ix] = expf_(muh[j], Y[ix], 1);
                     }
             }
@@ -1026,6 +1142,31 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
             mu[j] = muh[j];
         }
         for (int th = 0; th < nk; ++th) mrow[tile * nk + th] = (uint8_t)prec[th];
+        int nrec = 0;
+        for (int th = 0; th < nk; ++th) {
+            st_s1 += prec[th] == MASK_STAGE1;
+            st_s2 += prec[th] == MASK_STAGE2;
+            nrec += prec[th] == MASK_STAGE1 || prec[th] == MASK_STAGE2;
+        }
+        ++st_tiles;
+        ++st_hist[nrec];
+    }
+    if (A->stats) {
+        uint64_t inactive = 0;
+        for (int t = 0; t < nkb; ++t) inactive += mrow[t] == MASK_INACTIVE;
+        uint64_t *S = A->stats;
+#ifdef _OPENMP
+#pragma omp critical(oracle_stats)
+#endif
+        {
+            S[OST_TILES] += st_tiles;
+            S[OST_S1] += st_s1;
+            S[OST_S2] += st_s2;
+            S[OST_INACTIVE] += inactive;
+            S[OST_SAT8] += st_sat8;
+            S[OST_SAT16] += st_sat16;
+            for (int c = 0; c <= nk; ++c) S[OST_HIST + c] += st_hist[c];
+        }
     }
 
     /* Epilogue (Alg. 1): O / omega; lse = mu + ln(omega). */
@@ -1043,24 +1184,27 @@ static void fwd_qblock(const fwd_args_t *A, int b, int h, int qb)
  * ceil(N/(bk*nk))*nk] u8 (any N >= 0; B = 0 or N = 0 computes nothing).
  * If qblocks != NULL only the listed query blocks (flat index
  * (b*Hq + h)*ceil(N/bq) + qb) are computed; other outputs are left untouched.
+ * stats != NULL: the statistics words (OST_*, 8 + nk + 1 of them) of the
+ * computed query blocks are added to it.
  * Returns 0, or -1 on invalid arguments / -2 on a table failure or, in the SIM
  * profile, an exponential too close to a rounding midpoint to be certified. */
-int lamp_oracle_fwd_seeded(const uint16_t *q, const uint16_t *k, const uint16_t *v,
-                           int B, int Hq, int Hkv, int N, int d, int causal, int window,
-                           int bq, int bk, int nk, double delta, double tau, unsigned flags, uint64_t seed,
-                           double *o, double *lse, uint8_t *mask,
-                           const int64_t *qblocks, int64_t nqblocks, int nthreads)
+int lamp_oracle_fwd_ex(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                       int B, int Hq, int Hkv, int N, int d, int causal, int window,
+                       int bq, int bk, int nk, double delta, double tau, unsigned flags, uint64_t seed,
+                       double *o, double *lse, uint8_t *mask,
+                       const int64_t *qblocks, int64_t nqblocks, int nthreads, uint64_t *stats)
 {
     if (B < 0 || Hq <= 0 || Hkv <= 0 || N < 0 || d <= 0 || d > 1024) return -1;
     if (Hq % Hkv || bq <= 0 || bk <= 0 || nk <= 0 || nk > 16) return -1;
     if (window < 0 || (window > 0 && !causal)) return -1;
     if (!(tau >= 0.0) || !(delta >= 0.0)) return -1;
     if (build_tables()) return -2;
-    if (flags & ~(unsigned)(ORACLE_STAGE1_OFF | ORACLE_MU_TRUNC | ORACLE_SIM | ORACLE_SR8)) return -1;
+    if (flags & ~(unsigned)(ORACLE_STAGE1_OFF | ORACLE_MU_TRUNC | ORACLE_SIM | ORACLE_SR8 | ORACLE_Y16_STEP)) return -1;
     if ((flags & ORACLE_SR8) && (flags & ORACLE_SIM)) return -1;
     if (B == 0 || N == 0) return 0;                /* nothing to compute */
     g_sim_fail = 0;
-    fwd_args_t A = {q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, flags, seed, o, lse, mask};
+    fwd_args_t A = {q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, flags, seed, o, lse, mask,
+                    stats};
     const int nqbh = (N + bq - 1) / bq;
     int64_t nqb = (int64_t)B * Hq * nqbh;
     int64_t count = qblocks ? nqblocks : nqb;
@@ -1076,6 +1220,17 @@ int lamp_oracle_fwd_seeded(const uint16_t *q, const uint16_t *k, const uint16_t 
         fwd_qblock(&A, b, h, qb);
     }
     return g_sim_fail ? -2 : 0;
+}
+
+/* The above without statistics. */
+int lamp_oracle_fwd_seeded(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                           int B, int Hq, int Hkv, int N, int d, int causal, int window,
+                           int bq, int bk, int nk, double delta, double tau, unsigned flags, uint64_t seed,
+                           double *o, double *lse, uint8_t *mask,
+                           const int64_t *qblocks, int64_t nqblocks, int nthreads)
+{
+    return lamp_oracle_fwd_ex(q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, flags, seed, o, lse,
+                              mask, qblocks, nqblocks, nthreads, NULL);
 }
 
 /* lamp_oracle_fwd: the above with seed 0 (ORACLE_SR8 takes the seeded form). */

@@ -43,13 +43,16 @@ def lib():
         _lib.lamp_oracle_fwd_seeded.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32,
                                                 f64, f64, ctypes.c_uint, ctypes.c_uint64, P, P, P, P, i64, i32]
         _lib.lamp_oracle_fwd_seeded.restype = i32
+        _lib.lamp_oracle_fwd_ex.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32,
+                                            f64, f64, ctypes.c_uint, ctypes.c_uint64, P, P, P, P, i64, i32, P]
+        _lib.lamp_oracle_fwd_ex.restype = i32
         _lib.oracle_philox4x64_10.argtypes = [P, P, P]
         _lib.oracle_philox4x64_10.restype = None
         _lib.oracle_sr_e4m3.argtypes = [P, P, P, i64]
         _lib.oracle_sr_e4m3.restype = i32
         _lib.oracle_logits8_sr.argtypes = [P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32, ctypes.c_uint64, P, i32]
         _lib.oracle_logits8_sr.restype = i32
-        for name in ("oracle_logits8", "oracle_logits16"):
+        for name in ("oracle_logits8", "oracle_logits16", "oracle_logits16_step"):
             fn = getattr(_lib, name)
             fn.argtypes = [P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, i32]
             fn.restype = i32
@@ -210,6 +213,20 @@ def logits16(q, k, causal, window, row0, nrows, nthreads=0):
     return out
 
 
+def logits16_step(q, k, causal, window, row0, nrows, nthreads=0):
+    """e4m11 codes of the 16-bit logits with e4m11 as the accumulator (rounded
+    after every FMA), layout of logits16."""
+    q = np.ascontiguousarray(q, dtype=np.uint16)
+    k = np.ascontiguousarray(k, dtype=np.uint16)
+    B, Hq, N, d = q.shape
+    Hkv = k.shape[1]
+    out = np.empty((B, Hq, nrows, N), dtype=np.uint16)
+    rc = lib().oracle_logits16_step(_ptr(q), _ptr(k), B, Hq, Hkv, N, d, int(causal), int(window),
+                                    row0, nrows, _ptr(out), nthreads)
+    assert rc == 0
+    return out
+
+
 # ---------------------------------------------------------------- SIM profile
 def round_sim(p, x):
     """Round doubles to p = 3 or 11 mantissa bits in FP32's exponent range (RNE, overflow to inf)."""
@@ -260,13 +277,18 @@ STAGE1_OFF = 1   # the first stage disabled: mu_hat from the 8-bit maxima, stage
 MU_TRUNC = 2     # 8-bit shifts against mu_hat truncated to e4m3 (SIM: to 3 mantissa bits)
 SIM = 4          # the "SIM" precision profile (FP32 range, 3/11-bit mantissas, no saturation)
 SR8 = 8          # the 8-bit accumulation rounded stochastically (seeded Philox4x64-10 bits)
+Y16_STEP = 16    # the 16-bit logits with e4m11 as the accumulator (rounded after every FMA; Sec. 3.3 literally)
+
+STAT_NAMES = ("tiles", "stage1", "stage2", "inactive", "sat8", "sat16", "spec_unused", "late16")
+STAT_HIST = len(STAT_NAMES)
 
 
 def trunc_e4m3(x):
     return lib().oracle_trunc_e4m3(float(x))
 
 
-def fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, qblocks=None, nthreads=0, flags=0, seed=0):
+def fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, qblocks=None, nthreads=0, flags=0, seed=0,
+        stats=False):
     """The LampAttention forward pass on the CPU.
 
     Returns (o [B,Hq,N,d] fp64, lse [B,Hq,N] fp64, mask [B,Hq,ceil(N/bq),
@@ -274,7 +296,9 @@ def fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, qblocks=None, nthreads=
     With `qblocks` (flat indices (b*Hq+h)*(N/bq)+qb) only those query blocks
     are computed; the other rows of o/lse hold NaN and their mask bytes 0xFE.
     `seed` keys the random numbers of flag 8 (stochastic rounding of the
-    8-bit accumulation).
+    8-bit accumulation).  With `stats`, a fourth element: the statistics
+    words (uint64 [8 + nk + 1], names STAT_NAMES then the histogram) of the
+    computed query blocks.
     """
     q = np.ascontiguousarray(q, dtype=np.uint16)
     k = np.ascontiguousarray(k, dtype=np.uint16)
@@ -290,11 +314,14 @@ def fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, qblocks=None, nthreads=
         qp, nq = _ptr(qbl), qbl.size
     else:
         qp, nq = None, 0
-    rc = lib().lamp_oracle_fwd_seeded(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(causal), int(window),
-                                      bq, bk, nk, float(delta), float(tau), int(flags), int(seed),
-                                      _ptr(o), _ptr(lse), _ptr(mask), qp, nq, nthreads)
+    st = np.zeros(STAT_HIST + nk + 1, dtype=np.uint64)
+    rc = lib().lamp_oracle_fwd_ex(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(causal), int(window),
+                                  bq, bk, nk, float(delta), float(tau), int(flags), int(seed),
+                                  _ptr(o), _ptr(lse), _ptr(mask), qp, nq, nthreads, _ptr(st) if stats else None)
     if rc != 0:
         raise ValueError("lamp_oracle_fwd failed with %d" % rc)
+    if stats:
+        return o, lse, mask, st
     return o, lse, mask
 
 

@@ -34,6 +34,7 @@
 #include "lamp_kernels.h"
 #include "lamp_loops.h"
 #include "lamp_sr.h"
+#include "lamp_stats.h"
 
 #ifndef LAMP_MIN_WAVES
 #define LAMP_MIN_WAVES 2   // minimum waves per SIMD requested from the register allocator
@@ -67,7 +68,8 @@ struct Cfg {
     static constexpr size_t OFF_SP = OFF_CM + (size_t)(NK + 2 * NW) * BQ * 4;   // f64 [2][NW][BQ]
     static constexpr size_t OFF_CO = OFF_SP + (size_t)2 * NW * BQ * 8;   // f64 [NK][BQ]
     static constexpr size_t OFF_ED = OFF_CO + (size_t)NK * BQ * 8;       // f64 [EXPDOC_NK]
-    static constexpr size_t LDS = OFF_ED + (size_t)EXPDOC_NK * 8;
+    static constexpr size_t OFF_ST = OFF_ED + (size_t)EXPDOC_NK * 8;     // u32 [ST_N] statistics
+    static constexpr size_t LDS = OFF_ST + (size_t)ST_N * 4;
     static_assert(BQ == 64 || BQ == 128, "64 or 128 query rows per block");
     static_assert(BK % 16 == 0 && NK <= 4 && NK % NW == 0, "sub-blocks of 16-key chunks, at most 4 per tile");
     static_assert(CPW % 32 == 0, "whole 32-channel tiles per wave");
@@ -76,7 +78,10 @@ struct Cfg {
 
 // SR: the 8-bit logits with stochastic rounding (lamp_sr.h) in place of
 // round-to-nearest.
-template <int D, int BQ, int BK, int NK, bool SR>
+// OBS: the instantiation that also writes the logit observables (p.dbg_y8,
+// p.dbg_y16), kept apart so that the stores do not change the register
+// allocation of the others.
+template <int D, int BQ, int BK, int NK, bool SR, bool OBS>
 __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) void lamp_fwd_kernel(FwdParams p)
 {
     using C = Cfg<D, BQ, BK, NK>;
@@ -96,6 +101,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
     double *spf = sps + NW * BQ;                                       // [NW][BQ] the same over 8-bit sub-blocks
     double *cst_lds = reinterpret_cast<double *>(smem + C::OFF_CO);    // [NK][BQ] stage-2 costs
     double *edk = reinterpret_cast<double *>(smem + C::OFF_ED);        // exp_doc constants
+    uint32_t *stl = reinterpret_cast<uint32_t *>(smem + C::OFF_ST);    // [ST_N] statistics (p.stats)
 
     const int tid = threadIdx.x;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;   // w is wave-uniform
@@ -134,6 +140,13 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
 
     for (int i = tid; i < 256; i += 64 * NW) lut[i] = p.lut8e[i];
     if (tid < EXPDOC_NK) edk[tid] = EXPDOC_K[tid];
+    if (tid < ST_N) stl[tid] = 0u;
+    // logit observables (tests): this query block is observed (uniform)
+    const bool dbg_blk = qb >= p.dbg_qb0 && qb < p.dbg_qb0 + p.dbg_nqb;
+    const bool dbg8 = OBS && p.dbg_y8 != nullptr && dbg_blk, dbg16 = OBS && p.dbg_y16 != nullptr && dbg_blk;
+    auto dbg_off = [&](int s) -> size_t {
+        return ((((size_t)b * p.Hq + h) * p.dbg_nqb + (qb - p.dbg_qb0)) * BQ + row[s]) * (size_t)p.Nk;
+    };
 
     float mu[QPL];     // running maxima (e4m11 or e4m3 values)
     double om[QPL];    // running sums omega
@@ -151,6 +164,46 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
             for (int r = 0; r < 16; ++r) acc[g][t][r] = 0.0f;
 
     auto visible = [&](int s, int key) { return key >= vlo[s] && key <= vhi[s]; };
+
+    // Observables of the 16-bit logits of 2*NWD keys from kc of every slot
+    // (codes two per word): their codes for the tests, and the saturated ones
+    // among the visible keys whose code is the largest e4m11 magnitude (the
+    // FP32 chain rerun for those alone).
+    auto obs16 = [&](int kc, const auto &yc) {
+        constexpr int NWD = sizeof(yc[0]) / sizeof(uint32_t);   // words per slot
+        if (dbg16) {
+#pragma unroll
+            for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                for (int x = 0; x < NWD; ++x) {
+                    const uint32_t lo = visible(s, kc + 2 * x) ? (yc[s][x] & 0xFFFFu) : 0xFFFFu;
+                    const uint32_t hi = visible(s, kc + 2 * x + 1) ? (yc[s][x] >> 16) : 0xFFFFu;
+                    *reinterpret_cast<uint32_t *>(p.dbg_y16 + dbg_off(s) + kc + 2 * x) = lo | (hi << 16);
+                }
+        }
+        if (p.stats) {
+            static_assert(QPL * 2 * NWD <= 32, "one bit per slot and key");
+            uint32_t atmax = 0;   // bit s * 2NWD + i: slot s, key kc + i
+#pragma unroll
+            for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                for (int i = 0; i < 2 * NWD; ++i) {
+                    const uint32_t code = (yc[s][i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+                    atmax |= ((code & 0x7FFFu) == 0x7FFFu && visible(s, kc + i) ? 1u : 0u) << (s * 2 * NWD + i);
+                }
+            if (wave_any(atmax != 0u)) {
+                uint32_t n = 0;
+                for (uint32_t m = atmax; m; m &= m - 1) {
+                    const int bit = __builtin_ctz(m);
+                    const float *qr = qrow[0];
+#pragma unroll
+                    for (int s = 1; s < QPL; ++s) qr = bit / (2 * NWD) == s ? qrow[s] : qr;
+                    n += y16_saturates<D, RowLay<D>>(qr, kt32 + (size_t)(kc + bit % (2 * NWD)) * D) ? 1u : 0u;
+                }
+                if (n) atomicAdd(&stl[ST_SAT16], n);
+            }
+        }
+    };
 
     // 16-bit recompute of sub-block th shared by all waves: wave w takes keys
     // [key0, key0 + KPW) with key0 = k0 + th*BK + w*KPW.  For every 16-key
@@ -215,14 +268,51 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                         const int c16 = th * CPS + ch;
                         const int ck0 = k0 + c16 * 16;
                         if (ck0 > bv_hi || ck0 + 15 < bv_lo) continue;   // nothing visible in the block
-                        uint32_t a8[QPL][8];
+                        uint32_t a8[QPL][8], sat[QPL];
                         if constexpr (SR) {
                             int jq[QPL];
 #pragma unroll
                             for (int s = 0; s < QPL; ++s) jq[s] = q0 + row[s];
-                            sr8_chunk<D, QPL>(qrow, kt32 + (size_t)ck0 * D, p.seed, (uint64_t)bh, jq, ck0, a8);
+                            sr8_chunk<D, QPL>(qrow, kt32 + (size_t)ck0 * D, p.seed, (uint64_t)bh, jq, ck0, a8, sat);
                         } else {
-                            emu8_chunk<D, QPL>(qrow, kt32 + (size_t)ck0 * D, a8);
+                            emu8_chunk<D, QPL>(qrow, kt32 + (size_t)ck0 * D, a8, sat);
+                        }
+                        auto vis16 = [&](int s) {
+                            uint32_t m = 0;
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) m |= (visible(s, ck0 + i) ? 1u : 0u) << i;
+                            return m;
+                        };
+                        if (p.stats) {
+                            uint32_t any = 0;
+#pragma unroll
+                            for (int s = 0; s < QPL; ++s) any |= sat[s];
+                            if (wave_any(any != 0u)) {
+                                uint32_t n = 0;
+#pragma unroll
+                                for (int s = 0; s < QPL; ++s) n += __builtin_popcount(sat[s] & vis16(s));
+                                if (n) atomicAdd(&stl[ST_SAT8], n);
+                            }
+                        }
+                        if (dbg8) {
+#pragma unroll
+                            for (int s = 0; s < QPL; ++s) {
+                                const uint32_t vm = vis16(s);
+                                uint32_t wd[4];
+#pragma unroll
+                                for (int q4 = 0; q4 < 4; ++q4) {
+                                    uint32_t x = 0;
+#pragma unroll
+                                    for (int i = 0; i < 4; ++i) {
+                                        const int key = 4 * q4 + i;
+                                        const uint32_t code = (a8[s][key >> 1] >> (8 * (key & 1))) & 0xFFu;
+                                        x |= ((vm >> key & 1u) ? code : 0xFFu) << (8 * i);
+                                    }
+                                    wd[q4] = x;
+                                }
+                                *reinterpret_cast<u32x4 *>(p.dbg_y8 + dbg_off(s) + ck0) =
+                                    u32x4{wd[0], wd[1], wd[2], wd[3]};
+                            }
                         }
 #pragma unroll
                         for (int s = 0; s < QPL; ++s) {
@@ -282,6 +372,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                         if (ck0 > bv_hi || ck0 + 15 < bv_lo) continue;
                         uint32_t yc[QPL][8];
                         rec16_chunk<D, QPL>(qrow, kt32 + (size_t)ck0 * D, yc);
+                        obs16(ck0, yc);
 #pragma unroll
                         for (int s = 0; s < QPL; ++s) {
 #pragma unroll
@@ -373,6 +464,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                     for (int s = 0; s < QPL; ++s) cm[s] = NEG_INF;
                     shared16(k0, th, [&](int kc, const auto &yc) {
                         constexpr int NWD = sizeof(yc[0]) / sizeof(uint32_t);   // words per slot
+                        obs16(kc, yc);
 #pragma unroll
                         for (int s = 0; s < QPL; ++s) {
 #pragma unroll
@@ -603,6 +695,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
                     for (int s = 0; s < QPL; ++s) ds[s] = 0.0;
                     auto s2fn = [&](int kc, const auto &yc) {
                         constexpr int NWD = sizeof(yc[0]) / sizeof(uint32_t);
+                        obs16(kc, yc);
 #pragma unroll
                         for (int s = 0; s < QPL; ++s) {
                             const uint16_t *src = ycode + row[s] * YP + (kc - k0);
@@ -656,12 +749,24 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
             om[s] = __builtin_fma(lam[s], om[s], S[s]);
             mu[s] = muh[s];
         }
-        if (tid == 0)
+        if (tid == 0) {
 #pragma unroll
             for (int th = 0; th < NK; ++th)
                 mrow[tile * NK + th] = !(active >> th & 1u) ? PREC_INACTIVE
                                      : (prec16 >> th & 1u) ? PREC_S1
                                      : (prec2 >> th & 1u) ? PREC_S2 : PREC_LOW;
+            if (p.stats) {
+                // every recompute of this kernel is one at a time (or after
+                // stage 2), except the all-16-bit mode's own sub-blocks
+                const uint32_t rec = prec16 | prec2;
+                stl[ST_TILES] += 1u;
+                stl[ST_S1] += __builtin_popcount(prec16);
+                stl[ST_S2] += __builtin_popcount(prec2);
+                stl[ST_ACT] += __builtin_popcount(active);
+                stl[ST_LATE] += p.mode == MODE_LAMP ? __builtin_popcount(rec) : 0;
+                stl[ST_HIST + __builtin_popcount(rec)] += 1u;
+            }
+        }
         const uint32_t p16 = prec16 | prec2;
         const int half = lane >> 5, l32 = lane & 31;
         // V^T operands from global memory, one chunk ahead of the matrix-core
@@ -756,20 +861,28 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
             if (t < t_begin || t > t_end)
                 for (int th = 0; th < NK; ++th) mrow[t * NK + th] = PREC_INACTIVE;
     }
+    if (p.stats) flush_stats<NK>(p.stats, stl, (uint32_t)(p.Nk / BK), tid);
 }
 
 // ------------------------------------------------------------------ launcher
-template <int D, int BQ, int BK, int NK, bool SR = false>
-static hipError_t launch_fwd(const FwdParams &p, hipStream_t s)
+template <int D, int BQ, int BK, int NK, bool SR, bool OBS>
+static hipError_t launch_fwd_obs(const FwdParams &p, hipStream_t s)
 {
     using C = Cfg<D, BQ, BK, NK>;
-    auto kern = lamp_fwd_kernel<D, BQ, BK, NK, SR>;
+    auto kern = lamp_fwd_kernel<D, BQ, BK, NK, SR, OBS>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
     if (e != hipSuccess) return e;
     dim3 grid((unsigned)(p.B * p.Hq * (p.Nq / BQ)));
     hipLaunchKernelGGL(kern, grid, dim3(64 * C::NW), C::LDS, s, p);
     return hipGetLastError();
+}
+
+template <int D, int BQ, int BK, int NK, bool SR = false>
+static hipError_t launch_fwd(const FwdParams &p, hipStream_t s)
+{
+    if (p.dbg_y8 || p.dbg_y16) return launch_fwd_obs<D, BQ, BK, NK, SR, true>(p, s);
+    return launch_fwd_obs<D, BQ, BK, NK, SR, false>(p, s);
 }
 
 #define LAMP_FWD_CASE(D_, BQ_, BK_, NK_) \

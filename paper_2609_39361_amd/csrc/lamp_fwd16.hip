@@ -33,6 +33,7 @@
 #include "lamp_device.h"
 #include "lamp_kernels.h"
 #include "lamp_loops.h"
+#include "lamp_stats.h"
 
 #ifndef LAMP_MIN_WAVES
 #define LAMP_MIN_WAVES 2
@@ -47,6 +48,7 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 enum { PREC_LOW = 0, PREC_S1 = 1, PREC_S2 = 2, PREC_INACTIVE = 3 };
+
 
 template <int D, int BQ>
 struct Cfg16 {
@@ -68,7 +70,8 @@ struct Cfg16 {
     static constexpr size_t OFF_SP = OFF_CMF + CMF;                     // f64 [2][NW][BQ]
     static constexpr size_t OFF_ED = OFF_SP + (size_t)2 * NW * BQ * 8;  // f64 [EXPDOC_NK]
     static constexpr size_t OFF_TS = OFF_ED + (size_t)EXPDOC_NK * 8;    // i32 [2][NK] sub-block threats
-    static constexpr size_t LDS = OFF_TS + (size_t)2 * NK * 4;
+    static constexpr size_t OFF_ST = OFF_TS + (size_t)2 * NK * 4;       // u32 [ST_N] statistics
+    static constexpr size_t LDS = OFF_ST + (size_t)ST_N * 4;
     static_assert(BQ == 64 || BQ == 128, "64 or 128 query rows per block");
     static_assert(CPW % 32 == 0, "whole 32-channel tiles per wave");
 };
@@ -146,7 +149,10 @@ __device__ __forceinline__ int wave_max_i32(int v)
 
 } // namespace
 
-template <int D, int BQ, int MODE, bool SIMP>
+// OBS: the instantiation that also writes the logit observables (p.dbg_y8,
+// p.dbg_y16); the same code otherwise, kept apart so that the stores do not
+// change the register allocation of the instantiations that do not.
+template <int D, int BQ, int MODE, bool SIMP, bool OBS>
 __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdParams p)
 {
     using C = Cfg16<D, BQ>;
@@ -166,6 +172,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     double *spf = sps + NW * BQ;                                        // [NW][BQ] over 8-bit sub-blocks
     double *edk = reinterpret_cast<double *>(smem + C::OFF_ED);         // exp_doc constants
     int *tsl = reinterpret_cast<int *>(smem + C::OFF_TS);               // [2][NK] threats of a tile
+    uint32_t *stl = reinterpret_cast<uint32_t *>(smem + C::OFF_ST);    // [ST_N] statistics (p.stats)
 
     const int tid = threadIdx.x;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;   // w is wave-uniform
@@ -229,6 +236,14 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     for (int i = tid; i < 256; i += 256) lut[i] = SIMP ? p.sim8[i] : p.lut8e[i];
     if (tid < EXPDOC_NK) edk[tid] = EXPDOC_K[tid];
     for (int i = tid; i < 2 * NK * BQ; i += 256) cmi2[i] = INT_MIN;
+    if (tid < ST_N) stl[tid] = 0u;
+    // logit observables (tests): this query block is observed (uniform)
+    const bool dbg_blk = qb >= p.dbg_qb0 && qb < p.dbg_qb0 + p.dbg_nqb;
+    const bool dbg8 = OBS && !SIMP && p.dbg_y8 != nullptr && dbg_blk;
+    const bool dbg16 = OBS && !SIMP && p.dbg_y16 != nullptr && dbg_blk;
+    auto dbg_off = [&](int s) -> size_t {
+        return ((((size_t)b * p.Hq + h) * p.dbg_nqb + (qb - p.dbg_qb0)) * BQ + row[s]) * (size_t)p.Nk;
+    };
 
     float mu[QPL];
     double om[QPL];
@@ -271,13 +286,52 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     // 8-bit codes of this wave's sub-block of `tile` into its code buffer, the
     // column maxima over visible keys into m8s (NEG_INF for a sub-block that
     // was not emulated)
-    auto emit8 = [&](int tile, const uint32_t (&a8)[QPL][8], bool done) {
+    auto emit8 = [&](int tile, const uint32_t (&a8)[QPL][8], bool done, const uint32_t (&sat)[QPL]) {
         const int ck0 = tile * KPT + w * BK;
         uint16_t *yc = ycode_of(tile);
         float *m8s = m8s_of(tile);
         bool full = true;
 #pragma unroll
         for (int s = 0; s < QPL; ++s) full &= ck0 >= vlo[s] && ck0 + 15 <= vhi[s];
+        if constexpr (!SIMP) {
+            // visible keys of the 16 in each slot (for the observables)
+            auto vis16 = [&](int s) {
+                uint32_t m = 0;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) m |= (visible(s, ck0 + i) ? 1u : 0u) << i;
+                return m;
+            };
+            if (done && p.stats) {
+                uint32_t any = 0;
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) any |= sat[s];
+                if (wave_any(any != 0u)) {
+                    uint32_t n = 0;
+#pragma unroll
+                    for (int s = 0; s < QPL; ++s) n += __builtin_popcount(sat[s] & vis16(s));
+                    if (n) atomicAdd(&stl[ST_SAT8], n);
+                }
+            }
+            if (done && dbg8) {
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) {
+                    const uint32_t vm = vis16(s);
+                    uint32_t wd[4];
+#pragma unroll
+                    for (int q4 = 0; q4 < 4; ++q4) {
+                        uint32_t x = 0;
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const int key = 4 * q4 + i;
+                            const uint32_t code = (a8[s][key >> 1] >> (8 * (key & 1))) & 0xFFu;
+                            x |= ((vm >> key & 1u) ? code : 0xFFu) << (8 * i);
+                        }
+                        wd[q4] = x;
+                    }
+                    *reinterpret_cast<u32x4 *>(p.dbg_y8 + dbg_off(s) + ck0) = u32x4{wd[0], wd[1], wd[2], wd[3]};
+                }
+            }
+        }
         // FULL: every key of the sub-block visible to every row of the wave
         // (a uniform branch), so no per-key visibility test
         auto run = [&](auto full_c) {
@@ -390,6 +444,48 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
             return bf16_value(eh) + bf16_value(el);   // exact
         }
     };
+    // Observables of the 16-bit logits of 4 keys from key0 of every slot
+    // (codes two per word, as the recomputes leave them): their codes for the
+    // tests, and the saturated ones among the visible keys whose code is the
+    // largest e4m11 magnitude (the FP32 chain rerun for those alone).
+    auto obs16 = [&](int key0, const uint32_t (&yc)[QPL][WPM]) {
+        if constexpr (!SIMP) {
+            if (dbg16) {
+#pragma unroll
+                for (int s = 0; s < QPL; ++s) {
+                    uint32_t wd[2];
+#pragma unroll
+                    for (int x = 0; x < 2; ++x) {
+                        const uint32_t lo = visible(s, key0 + 2 * x) ? (yc[s][x] & 0xFFFFu) : 0xFFFFu;
+                        const uint32_t hi = visible(s, key0 + 2 * x + 1) ? (yc[s][x] >> 16) : 0xFFFFu;
+                        wd[x] = lo | (hi << 16);
+                    }
+                    *reinterpret_cast<uint2 *>(p.dbg_y16 + dbg_off(s) + key0) = make_uint2(wd[0], wd[1]);
+                }
+            }
+            if (p.stats) {
+                uint32_t atmax = 0;   // bit 4s + i: slot s, key key0 + i
+#pragma unroll
+                for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const uint32_t code = (yc[s][i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+                        atmax |= ((code & 0x7FFFu) == 0x7FFFu && visible(s, key0 + i) ? 1u : 0u) << (4 * s + i);
+                    }
+                if (wave_any(atmax != 0u)) {
+                    uint32_t n = 0;
+                    for (uint32_t m = atmax; m; m &= m - 1) {
+                        const int bit = __builtin_ctz(m);
+                        const float *qr = qrow[0];
+#pragma unroll
+                        for (int s = 1; s < QPL; ++s) qr = bit / 4 == s ? qrow[s] : qr;
+                        n += y16_saturates<D, GrpLay>(qr, krow_of(key0 + bit % 4)) ? 1u : 0u;
+                    }
+                    if (n) atomicAdd(&stl[ST_SAT16], n);
+                }
+            }
+        }
+    };
     // SIM profile: the row sum of the tile's exponentials, keys ascending,
     // one fp64 addition at a time, from the values in LDS (hmask: the
     // sub-blocks holding 16-bit exponentials)
@@ -422,9 +518,9 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     uint32_t act = active_of(t);
     if (mode != MODE_ALL16) {
         const bool done = own_emulated(t, act);
-        uint32_t a8[QPL][8];
-        if (done) emu8_any<D, QPL, SIMP, GrpLay>(qrow, kt32 + (size_t)(t * KPT + w * BK) * D, a8);
-        emit8(t, a8, done);
+        uint32_t a8[QPL][8], sat[QPL];
+        if (done) emu8_any<D, QPL, SIMP, GrpLay>(qrow, kt32 + (size_t)(t * KPT + w * BK) * D, a8, sat);
+        emit8(t, a8, done, sat);
     }
     __syncthreads();
     uint32_t F0 = f0_of(t, act);
@@ -451,12 +547,12 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
             const float *krowr = krow_of(k0 + thg * BK + w * 4 + (kk & 3));
             const bool emu = mode != MODE_ALL16 && has_next && own_emulated(t + 1, act_next);
             const float *k32e = kt32 + (size_t)(k0 + KPT + w * BK) * D;   // read only when emu (then below N)
-            uint32_t a8[QPL][8];
+            uint32_t a8[QPL][8], sat8[QPL];
             auto run = [&](auto nkey_c, auto emu_c) {
                 constexpr int NKEY = decltype(nkey_c)::value;
                 constexpr bool EMU = decltype(emu_c)::value;
                 uint32_t c[QPL][y16_words<SIMP>(NKEY)];
-                fused_pass<D, QPL, NKEY, EMU, SIMP, GrpLay>(qrow, k32e, krowr, a8, c);
+                fused_pass<D, QPL, NKEY, EMU, SIMP, GrpLay>(qrow, k32e, krowr, a8, c, sat8);
                 if constexpr (NKEY > 0)
 #pragma unroll
                     for (int s = 0; s < QPL; ++s)
@@ -483,7 +579,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                 default: run(integral_constant<int, 16>(), F_()); break;
                 }
             }
-            if (has_next && mode != MODE_ALL16) emit8(t + 1, a8, emu);
+            if (has_next && mode != MODE_ALL16) emit8(t + 1, a8, emu, sat8);
             // 16-bit column maxima over this wave's 4 keys of every member of F0
             int *cmi = cmi_of(t);
             uint32_t m = F0;
@@ -607,6 +703,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
 #pragma unroll
                     for (int s = 0; s < QPL; ++s) cm[s] = NEG_INF;
                     shared16(k0, th, [&](int kc, const uint32_t (&yc)[QPL][WPM]) {
+                        obs16(kc, yc);
 #pragma unroll
                         for (int s = 0; s < QPL; ++s) {
 #pragma unroll
@@ -791,6 +888,16 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                             else hl[s][i] = p.exp16hl[ue5m11_code(shift_of(muh[s], y))];
                         }
                     const int key0 = k0 + tg[g] * BK + w * 4;
+                    if constexpr (!SIMP) {
+                        if (dbg16 || p.stats) {
+                            uint32_t yc[QPL][WPM];
+#pragma unroll
+                            for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                                for (int x = 0; x < WPM; ++x) yc[s][x] = y16r[s][g * WPM + x];
+                            obs16(key0, yc);
+                        }
+                    }
 #pragma unroll
                     for (int s = 0; s < QPL; ++s) {
                         uint32_t eh[4], el[4];
@@ -932,6 +1039,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
 #pragma unroll
                     for (int s = 0; s < QPL; ++s) ds[s] = 0.0;
                     auto s2fn = [&](int kc, const uint32_t (&yc)[QPL][WPM]) {
+                        obs16(kc, yc);
 #pragma unroll
                         for (int s = 0; s < QPL; ++s) {
                             const uint16_t *src = ycode + row[s] * YP + (kc - k0);
@@ -1033,12 +1141,23 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
             om[s] = __builtin_fma(lam[s], om[s], S[s]);
             mu[s] = muh[s];
         }
-        if (tid == 0)
+        if (tid == 0) {
 #pragma unroll
             for (int th = 0; th < NK; ++th)
                 mrow[t * NK + th] = !(act >> th & 1u) ? PREC_INACTIVE
                                   : (prec16 >> th & 1u) ? PREC_S1
                                   : (prec2 >> th & 1u) ? PREC_S2 : PREC_LOW;
+            if (p.stats && act) {
+                const uint32_t rec = prec16 | prec2;
+                stl[ST_TILES] += 1u;
+                stl[ST_S1] += __builtin_popcount(prec16);
+                stl[ST_S2] += __builtin_popcount(prec2);
+                stl[ST_ACT] += __builtin_popcount(act);
+                stl[ST_UNUSED] += __builtin_popcount(F0 & ~rec);
+                stl[ST_LATE] += __builtin_popcount(rec & ~F0);
+                stl[ST_HIST + __builtin_popcount(rec)] += 1u;
+            }
+        }
         const uint32_t p16 = prec16 | prec2;
         const int half = lane >> 5, l32 = lane & 31;
         // V^T operands from global memory, one chunk ahead of the matrix-core
@@ -1138,20 +1257,29 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
             if (tt < t_begin || tt > t_end)
                 for (int th = 0; th < NK; ++th) mrow[tt * NK + th] = PREC_INACTIVE;
     }
+    if (p.stats) flush_stats<NK>(p.stats, stl, (uint32_t)(p.Nk / BK), tid);
 }
 
 // ------------------------------------------------------------------ launcher
-template <int D, int BQ, int MODE, bool SIMP>
-static hipError_t launch_fwd16_mode(const FwdParams &p, hipStream_t s)
+template <int D, int BQ, int MODE, bool SIMP, bool OBS>
+static hipError_t launch_fwd16_obs(const FwdParams &p, hipStream_t s)
 {
     using C = Cfg16<D, BQ>;
-    auto kern = lamp_fwd16_kernel<D, BQ, MODE, SIMP>;
+    auto kern = lamp_fwd16_kernel<D, BQ, MODE, SIMP, OBS>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
     if (e != hipSuccess) return e;
     dim3 grid((unsigned)(p.B * p.Hq * (p.Nq / BQ)));
     hipLaunchKernelGGL(kern, grid, dim3(256), C::LDS, s, p);
     return hipGetLastError();
+}
+
+template <int D, int BQ, int MODE, bool SIMP>
+static hipError_t launch_fwd16_mode(const FwdParams &p, hipStream_t s)
+{
+    if constexpr (!SIMP)
+        if (p.dbg_y8 || p.dbg_y16) return launch_fwd16_obs<D, BQ, MODE, SIMP, true>(p, s);
+    return launch_fwd16_obs<D, BQ, MODE, SIMP, false>(p, s);
 }
 
 template <int D, int BQ, bool SIMP>

@@ -39,10 +39,9 @@ struct DeviceState {
     uint32_t *exp16hl = nullptr;
     uint16_t *sim8 = nullptr;    // SIM profile tables
     uint32_t *sim16 = nullptr;
-    void *ws = nullptr;
+    void *ws = nullptr;          // the library's workspace of this device (grow-only)
     size_t ws_bytes = 0;
-    void *dws = nullptr;         // decode workspace: pre-scaled queries, 8-bit logit codes
-    size_t dws_bytes = 0;
+    std::vector<void *> retired; // outgrown workspaces, freed by lamp_reserve / lamp_shutdown
 };
 
 std::mutex g_mu;
@@ -111,36 +110,90 @@ float scale_of(int d)
 }
 
 struct Workspace {
+    unsigned *flag;   // non-finite input flag (LAMP_CHECK_FINITE)
     float *qt;
     float *kt32;
-    uint16_t *vt;   // only when asked for (the forward pass)
+    uint16_t *vt;     // only when asked for (the forward pass)
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Grow-only workspace for the pre-scaled Q (Nq rows per head), the fp32 K
-// and (with_vt) the transposed V (Nk keys per head) (lock held).
-int workspace_locked(int dev, int B, int Hq, int Hkv, int Nq, int Nk, int d, Workspace *w, bool with_vt = false)
+// Byte sizes of the prepass workspace: a 256-byte header (the check flag),
+// the pre-scaled Q (Nq rows per head), the fp32 K and (with_vt) the
+// transposed V (Nk keys per head).
+struct WsLayout {
+    size_t qt, k32, vt, total;
+};
+
+WsLayout ws_layout(int B, int Hq, int Hkv, int Nq, int Nk, int d, bool with_vt)
+{
+    const size_t nq = (size_t)B * Hq * Nq * d, nk = (size_t)B * Hkv * Nk * d;
+    WsLayout l;
+    l.qt = align256(nq * 4);
+    l.k32 = align256(nk * 4);
+    l.vt = with_vt ? align256(nk * 2) : 0;
+    l.total = 256 + l.qt + l.k32 + l.vt;
+    return l;
+}
+
+void carve(void *base, const WsLayout &l, Workspace *w)
+{
+    char *c = static_cast<char *>(base);
+    w->flag = reinterpret_cast<unsigned *>(c);
+    w->qt = reinterpret_cast<float *>(c + 256);
+    w->kt32 = reinterpret_cast<float *>(c + 256 + l.qt);
+    w->vt = l.vt ? reinterpret_cast<uint16_t *>(c + 256 + l.qt + l.k32) : nullptr;
+}
+
+bool capturing(hipStream_t s)
+{
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    return hipStreamIsCapturing(s, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone;
+}
+
+// The library's workspace of `dev` with at least `need` bytes (lock held).  A
+// workspace that is too small is retired, not freed: launches already queued
+// may still read it; lamp_reserve and lamp_shutdown free retired ones after
+// waiting for the device.  Growth is refused while `s` is being captured.
+int library_ws_locked(int dev, size_t need, hipStream_t s, void **base)
 {
     DeviceState *st = state_of(dev);
-    size_t nq = (size_t)B * Hq * Nq * d, nk = (size_t)B * Hkv * Nk * d;
-    size_t bq = align256(nq * 4), bk32 = align256(nk * 4), bvt = with_vt ? align256(nk * 2) : 0;
-    size_t need = bq + bk32 + bvt;
     if (need > st->ws_bytes) {
-        if (st->ws) {
-            HIP_TRY(hipDeviceSynchronize());
-            HIP_TRY(hipFree(st->ws));
-            st->ws = nullptr;
-            st->ws_bytes = 0;
-        }
-        HIP_TRY(hipMalloc(&st->ws, need));
-        st->ws_bytes = need;
+        if (capturing(s))
+            return fail(LAMP_ERR_WORKSPACE, "the library workspace holds %zu bytes, the call needs %zu, and the stream "
+                        "is being captured (reserve it with lamp_reserve or pass a workspace)", st->ws_bytes, need);
+        size_t grow = st->ws_bytes + st->ws_bytes / 2;
+        size_t bytes = align256(need > grow ? need : grow);
+        void *p = nullptr;
+        HIP_TRY(hipMalloc(&p, bytes));
+        if (st->ws) st->retired.push_back(st->ws);
+        st->ws = p;
+        st->ws_bytes = bytes;
     }
-    char *base = static_cast<char *>(st->ws);
-    w->qt = reinterpret_cast<float *>(base);
-    w->kt32 = reinterpret_cast<float *>(base + bq);
-    w->vt = with_vt ? reinterpret_cast<uint16_t *>(base + bq + bk32) : nullptr;
+    *base = st->ws;
     return LAMP_OK;
+}
+
+// The workspace of a call: the caller's (extra->workspace) or the library's.
+int call_ws(int dev, const lamp_fwd_extra *extra, size_t need, hipStream_t s, void **base)
+{
+    if (extra && extra->workspace) {
+        if ((reinterpret_cast<uintptr_t>(extra->workspace) & 255u) != 0)
+            return fail(LAMP_ERR_INVALID_ARG, "workspace not aligned to 256 bytes");
+        if (extra->workspace_bytes < need)
+            return fail(LAMP_ERR_WORKSPACE, "workspace of %zu bytes, the call needs %zu", extra->workspace_bytes, need);
+        *base = extra->workspace;
+        return LAMP_OK;
+    }
+    std::lock_guard<std::mutex> lk(g_mu);
+    return library_ws_locked(dev, need, s, base);
+}
+
+// Free the retired workspaces of every device (lock held, after a device sync).
+void free_retired_locked(DeviceState *st)
+{
+    for (void *p : st->retired) (void)hipFree(p);
+    st->retired.clear();
 }
 
 // rows: query rows per (b, h) to compute (N for the prefill form; M for the
@@ -173,7 +226,9 @@ const char *lamp_status_str(int s)
     case LAMP_ERR_INVALID_ARG: return "invalid argument";
     case LAMP_ERR_UNSUPPORTED: return "unsupported configuration";
     case LAMP_ERR_HIP: return "HIP runtime error";
-    case LAMP_ERR_INIT: return "device table initialisation failed";
+    case LAMP_ERR_INIT: return "device tables not built";
+    case LAMP_ERR_NONFINITE_INPUT: return "non-finite input";
+    case LAMP_ERR_WORKSPACE: return "workspace too small";
     default: return "unknown status";
     }
 }
@@ -198,7 +253,7 @@ void lamp_shutdown(void)
     if (hipGetDevice(&prev) != hipSuccess) return;
     for (size_t i = 0; i < g_dev.size(); ++i) {
         DeviceState &st = g_dev[i];
-        if (!st.ready && !st.ws && !st.dws) continue;
+        if (!st.ready && !st.ws && st.retired.empty()) continue;
         if (hipSetDevice((int)i) != hipSuccess) continue;
         (void)hipDeviceSynchronize();
         (void)hipFree(st.lut8);
@@ -208,16 +263,26 @@ void lamp_shutdown(void)
         (void)hipFree(st.sim8);
         (void)hipFree(st.sim16);
         (void)hipFree(st.ws);
-        (void)hipFree(st.dws);
+        free_retired_locked(&st);
         st = DeviceState();
     }
     (void)hipSetDevice(prev);
 }
 
+static size_t fwd_ws_bytes(int B, int Hq, int Hkv, int N, int bq, int bk, int nk, int d)
+{
+    // the workspace holds whole query blocks and whole key tiles (zero padded)
+    const int Nq = (N + bq - 1) / bq * bq, Nk = (N + bk * nk - 1) / (bk * nk) * (bk * nk);
+    return ws_layout(B, Hq, Hkv, Nq, Nk, d, true).total;
+}
+
 // The forward pass; sr: the 8-bit logits rounded stochastically with `seed`.
+// ws_fixed (with ws_fixed_bytes): a workspace that replaces both the caller's
+// and the library's (the allocation-free entry point).
 static int fwd_impl(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B, int Hq, int Hkv, int N, int d,
                     int causal, int window, int bq, int bk, int nk, double delta, double tau, unsigned flags, bool sr,
-                    uint64_t seed, float *o, float *lse, uint8_t *mask, void *stream)
+                    uint64_t seed, float *o, float *lse, uint8_t *mask, const lamp_fwd_extra *extra, void *stream,
+                    void *ws_fixed = nullptr, size_t ws_fixed_bytes = 0)
 {
     int rc = check_common(q, k, B, Hq, Hkv, N, d, causal, window);
     if (rc) return rc;
@@ -225,7 +290,7 @@ static int fwd_impl(const uint16_t *q, const uint16_t *k, const uint16_t *v, int
         return fail(LAMP_ERR_INVALID_ARG, "null pointer among v, o, lse, mask");
     if (!(delta >= 0.0) || std::isinf(delta)) return fail(LAMP_ERR_INVALID_ARG, "delta must be finite and >= 0");
     if (!(tau >= 0.0)) return fail(LAMP_ERR_INVALID_ARG, "tau must be >= 0 (or +inf)");
-    if (flags & ~(unsigned)(LAMP_STAGE1_OFF | LAMP_MU_TRUNC | LAMP_SIM_PROFILE))
+    if (flags & ~(unsigned)(LAMP_STAGE1_OFF | LAMP_MU_TRUNC | LAMP_SIM_PROFILE | LAMP_CHECK_FINITE))
         return fail(LAMP_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
     if (bq <= 0 || bk <= 0 || nk <= 0) return fail(LAMP_ERR_INVALID_ARG, "block sizes must be positive");
     if (!lamp::fwd_supported(d, bq, bk, nk))
@@ -235,34 +300,72 @@ static int fwd_impl(const uint16_t *q, const uint16_t *k, const uint16_t *v, int
     if ((flags & LAMP_SIM_PROFILE) && !(bk == 16 && nk == 4 && (d == 128 || d == 256)))
         return fail(LAMP_ERR_UNSUPPORTED, "the SIM profile is built for bk=16, nk=4, d in {128, 256} (bk=%d, nk=%d, d=%d)",
                     bk, nk, d);
+    const bool dbg = extra && (extra->dbg_y8 || extra->dbg_y16);
+    const int nqb_all = (N + bq - 1) / bq;
+    if (dbg) {
+        if (flags & LAMP_SIM_PROFILE)
+            return fail(LAMP_ERR_UNSUPPORTED, "the logit observables are built for the formats of Sec. 3.3");
+        if (extra->dbg_qb0 < 0 || extra->dbg_nqb <= 0 || extra->dbg_qb0 > nqb_all - extra->dbg_nqb)
+            return fail(LAMP_ERR_INVALID_ARG, "observed query blocks [%d, %d + %d) outside [0, %d)", extra->dbg_qb0,
+                        extra->dbg_qb0, extra->dbg_nqb, nqb_all);
+    }
     if (B == 0 || N == 0) return LAMP_OK;   // nothing to compute
-    // the workspace holds whole query blocks and whole key tiles (zero padded)
-    const int Nq = (N + bq - 1) / bq * bq, Nk = (N + bk * nk - 1) / (bk * nk) * (bk * nk);
+    const int Nq = nqb_all * bq, Nk = (N + bk * nk - 1) / (bk * nk) * (bk * nk);
+    const bool check = (flags & LAMP_CHECK_FINITE) != 0u;
+    flags &= ~(unsigned)LAMP_CHECK_FINITE;
     int dev = 0;
     rc = current_device(&dev);
     if (rc) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (check && capturing(s))
+        return fail(LAMP_ERR_INVALID_ARG, "LAMP_CHECK_FINITE waits for the stream, which is being captured");
     lamp::FwdParams p{};
-    Workspace w{};
     {
         std::lock_guard<std::mutex> lk(g_mu);
-        rc = init_locked(dev);
-        if (rc) return rc;
-        rc = workspace_locked(dev, B, Hq, Hkv, Nq, Nk, d, &w, true);
-        if (rc) return rc;
         DeviceState *st = state_of(dev);
+        if (ws_fixed) {
+            if (!st->ready)
+                return fail(LAMP_ERR_INIT, "the exponential tables of device %d are not built (call lamp_init first)",
+                            dev);
+        } else {
+            rc = init_locked(dev);
+            if (rc) return rc;
+        }
         p.exp16 = st->exp16;
         p.exp16hl = st->exp16hl;
         p.lut8e = st->lut8e;
         p.sim8 = st->sim8;
         p.sim16 = st->sim16;
     }
+    const WsLayout lay = ws_layout(B, Hq, Hkv, Nq, Nk, d, true);
+    void *base = nullptr;
+    if (ws_fixed) {
+        if (lay.total > ws_fixed_bytes)
+            return fail(LAMP_ERR_WORKSPACE, "the call needs %zu bytes of workspace, above the fixed %zu", lay.total,
+                        ws_fixed_bytes);
+        base = ws_fixed;
+    } else {
+        rc = call_ws(dev, extra, lay.total, s, &base);
+        if (rc) return rc;
+    }
+    Workspace w{};
+    carve(base, lay, &w);
     p.qt = w.qt;
     p.kt32 = w.kt32;
     p.vt = w.vt;
     p.o = o;
     p.lse = lse;
     p.mask = mask;
+    p.stats = extra ? extra->stats : nullptr;
+    if (dbg) {
+        p.dbg_y8 = extra->dbg_y8;
+        p.dbg_y16 = extra->dbg_y16;
+        p.dbg_qb0 = extra->dbg_qb0;
+        p.dbg_nqb = extra->dbg_nqb;
+        const size_t n = (size_t)B * Hq * extra->dbg_nqb * bq * Nk;
+        if (p.dbg_y8) HIP_TRY(hipMemsetAsync(p.dbg_y8, 0xFF, n, s));
+        if (p.dbg_y16) HIP_TRY(hipMemsetAsync(p.dbg_y16, 0xFF, n * sizeof(uint16_t), s));
+    }
     p.B = B;
     p.Hq = Hq;
     p.Hkv = Hkv;
@@ -288,9 +391,25 @@ static int fwd_impl(const uint16_t *q, const uint16_t *k, const uint16_t *v, int
         for (int i = 0; i < 3; ++i) HIP_TRY(hipEventCreate(&tc.e[i]));
         HIP_TRY(hipEventRecord(tc.e[0], s));
     }
+    unsigned *bad = nullptr;
+    if (check) {
+        bad = w.flag;
+        HIP_TRY(hipMemsetAsync(bad, 0, sizeof(unsigned), s));
+    }
     HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, Nq, Nk, d, scale_of(d), s,
-                                 !use_sr && lamp::fwd_grouped(d, bq, bk, nk)));
-    HIP_TRY(lamp::launch_transpose_v(v, w.vt, B, Hkv, N, Nk, d, s));
+                                 !use_sr && lamp::fwd_grouped(d, bq, bk, nk), bad));
+    HIP_TRY(lamp::launch_transpose_v(v, w.vt, B, Hkv, N, Nk, d, s, bad));
+    if (check) {
+        unsigned h_bad = 0;
+        HIP_TRY(hipMemcpyAsync(&h_bad, bad, sizeof(unsigned), hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipStreamSynchronize(s));
+        if (h_bad) {
+            if (timed)
+                for (int i = 0; i < 3; ++i) (void)hipEventDestroy(tc.e[i]);
+            return fail(LAMP_ERR_NONFINITE_INPUT, "a NaN or an infinity among the elements of%s%s%s",
+                        (h_bad & 1u) ? " q" : "", (h_bad & 2u) ? " k" : "", (h_bad & 4u) ? " v" : "");
+        }
+    }
     if (timed) HIP_TRY(hipEventRecord(tc.e[1], s));
     bool found = false;
     if (use_sr) HIP_TRY(lamp::dispatch_fwd_sr(d, bq, bk, nk, p, s, &found));
@@ -307,23 +426,76 @@ static int fwd_impl(const uint16_t *q, const uint16_t *k, const uint16_t *v, int
 
 int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B, int Hq, int Hkv, int N, int d,
                   int causal, int window, int bq, int bk, int nk, double delta, double tau, unsigned flags, float *o,
-                  float *lse, uint8_t *mask, void *stream)
+                  float *lse, uint8_t *mask, const lamp_fwd_extra *extra, void *stream)
 {
     return fwd_impl(q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, flags, false, 0, o, lse, mask,
-                    stream);
+                    extra, stream);
 }
 
 int lamp_attn_fwd_sr(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B, int Hq, int Hkv, int N, int d,
                      int causal, int window, int bq, int bk, int nk, double delta, double tau, unsigned flags,
-                     uint64_t seed, float *o, float *lse, uint8_t *mask, void *stream)
+                     uint64_t seed, float *o, float *lse, uint8_t *mask, const lamp_fwd_extra *extra, void *stream)
 {
     return fwd_impl(q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, flags, true, seed, o, lse, mask,
-                    stream);
+                    extra, stream);
+}
+
+size_t lamp_attn_fwd_workspace_size(int B, int Hq, int Hkv, int N, int d, int bq, int bk, int nk)
+{
+    if (B < 0 || Hq <= 0 || Hkv <= 0 || N < 0 || d <= 0 || bq <= 0 || bk <= 0 || nk <= 0) return 0;
+    if (B == 0 || N == 0) return 0;
+    return fwd_ws_bytes(B, Hq, Hkv, N, bq, bk, nk, d);
+}
+
+int lamp_reserve(int device, size_t bytes)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    int prev = 0;
+    HIP_TRY(hipGetDevice(&prev));
+    HIP_TRY(hipSetDevice(device));
+    DeviceState *st = state_of(device);
+    hipError_t e = hipDeviceSynchronize();
+    if (e == hipSuccess) {
+        free_retired_locked(st);
+        void *base = nullptr;
+        int rc = library_ws_locked(device, align256(bytes), nullptr, &base);
+        (void)hipSetDevice(prev);
+        return rc;
+    }
+    (void)hipSetDevice(prev);
+    return fail(LAMP_ERR_HIP, "lamp_reserve: %s", hipGetErrorString(e));
+}
+
+// Byte sizes of the decode workspace: pre-scaled queries, 8-bit codes,
+// exponentials, per-tile factors, partial outputs of the key chunks.
+struct DecLayout {
+    size_t qt, y8, e, f, part, total;
+};
+
+static DecLayout dec_layout(int B, int Hq, int M, int N, int d)
+{
+    const int Np = (N + 63) / 64 * 64, nch = (N + 511) / 512;   // key chunks of the P.V pass
+    const size_t nrows = (size_t)B * Hq * M;
+    DecLayout l;
+    l.qt = align256(nrows * d * 4);
+    l.y8 = align256(nrows * Np);
+    l.e = align256(nrows * Np * 4);
+    l.f = align256(nrows * (Np / 64) * 8);
+    l.part = align256(nrows * nch * d * 4);
+    l.total = l.qt + l.y8 + l.e + l.f + l.part;
+    return l;
+}
+
+size_t lamp_attn_decode_workspace_size(int B, int Hq, int Hkv, int M, int N, int d)
+{
+    if (B < 0 || Hq <= 0 || Hkv <= 0 || M < 0 || M > N || d <= 0) return 0;
+    if (B == 0 || M == 0) return 0;
+    return dec_layout(B, Hq, M, N, d).total;
 }
 
 int lamp_attn_decode(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B, int Hq, int Hkv, int M, int N,
                      int d, int causal, int window, int tk, double delta, double tau, unsigned flags, float *o,
-                     float *lse, uint8_t *mask, void *stream)
+                     float *lse, uint8_t *mask, const lamp_fwd_extra *extra, void *stream)
 {
     if (M < 0 || M > N) return fail(LAMP_ERR_INVALID_ARG, "M=%d query rows must lie in [0, N=%d]", M, N);
     int rc = check_common(q, k, B, Hq, Hkv, N, d, causal, window, M);
@@ -334,12 +506,11 @@ int lamp_attn_decode(const uint16_t *q, const uint16_t *k, const uint16_t *v, in
     if (!(tau >= 0.0)) return fail(LAMP_ERR_INVALID_ARG, "tau must be >= 0 (or +inf)");
     if (flags) return fail(LAMP_ERR_INVALID_ARG, "unknown flags 0x%x (the decode form takes none)", flags);
     if (tk != 64) return fail(LAMP_ERR_UNSUPPORTED, "keys per update tk=%d not built (64)", tk);
+    if (extra && (extra->stats || extra->dbg_y8 || extra->dbg_y16))
+        return fail(LAMP_ERR_UNSUPPORTED, "the decode form takes a workspace only (no stats, no logit observables)");
     if (B == 0 || M == 0) return LAMP_OK;   // nothing to compute
-    const int Np = (N + 63) / 64 * 64, nch = (N + 511) / 512;   // key chunks of the P.V pass
-    const size_t nrows = (size_t)B * Hq * M;
-    const size_t bq = align256(nrows * d * 4), by8 = align256(nrows * Np);
-    const size_t be = align256(nrows * Np * 4), bf = align256(nrows * (Np / 64) * 8);
-    const size_t bpart = align256(nrows * nch * d * 4), need = bq + by8 + be + bf + bpart;
+    const int Np = (N + 63) / 64 * 64;
+    const DecLayout lay = dec_layout(B, Hq, M, N, d);
     int dev = 0;
     rc = current_device(&dev);
     if (rc) return rc;
@@ -350,24 +521,19 @@ int lamp_attn_decode(const uint16_t *q, const uint16_t *k, const uint16_t *v, in
         rc = init_locked(dev);
         if (rc) return rc;
         DeviceState *st = state_of(dev);
-        if (need > st->dws_bytes) {
-            if (st->dws) {
-                HIP_TRY(hipDeviceSynchronize());
-                HIP_TRY(hipFree(st->dws));
-                st->dws = nullptr;
-                st->dws_bytes = 0;
-            }
-            HIP_TRY(hipMalloc(&st->dws, need));
-            st->dws_bytes = need;
-        }
-        char *base = static_cast<char *>(st->dws);
-        p.qt = reinterpret_cast<float *>(base);
-        p.y8 = reinterpret_cast<uint8_t *>(base + bq);
-        p.e = reinterpret_cast<float *>(base + bq + by8);
-        p.f = reinterpret_cast<double *>(base + bq + by8 + be);
-        p.part = reinterpret_cast<float *>(base + bq + by8 + be + bf);
         p.lut8e = st->lut8e;
         p.exp16hl = st->exp16hl;
+    }
+    void *wsb = nullptr;
+    rc = call_ws(dev, extra, lay.total, s, &wsb);
+    if (rc) return rc;
+    {
+        char *base = static_cast<char *>(wsb);
+        p.qt = reinterpret_cast<float *>(base);
+        p.y8 = reinterpret_cast<uint8_t *>(base + lay.qt);
+        p.e = reinterpret_cast<float *>(base + lay.qt + lay.y8);
+        p.f = reinterpret_cast<double *>(base + lay.qt + lay.y8 + lay.e);
+        p.part = reinterpret_cast<float *>(base + lay.qt + lay.y8 + lay.e + lay.f);
     }
     p.k = k;
     p.v = v;
@@ -450,7 +616,8 @@ int lamp_timing_read(int *launches, double *fwd_ms, double *prepass_ms)
 }
 
 static int logits_common(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv, int N, int d, int causal,
-                         int window, int row0, int nrows, void *out, lamp::LogitsParams *p, Workspace *w)
+                         int window, int row0, int nrows, void *out, lamp::LogitsParams *p, Workspace *w,
+                         void *stream)
 {
     int rc = check_common(q, k, B, Hq, Hkv, N, d, causal, window);
     if (rc) return rc;
@@ -464,8 +631,11 @@ static int logits_common(const uint16_t *q, const uint16_t *k, int B, int Hq, in
         std::lock_guard<std::mutex> lk(g_mu);
         rc = init_locked(dev);
         if (rc) return rc;
-        rc = workspace_locked(dev, B, Hq, Hkv, N, N, d, w);
+        const WsLayout lay = ws_layout(B, Hq, Hkv, N, N, d, false);
+        void *base = nullptr;
+        rc = library_ws_locked(dev, lay.total, static_cast<hipStream_t>(stream), &base);
         if (rc) return rc;
+        carve(base, lay, w);
     }
     *p = lamp::LogitsParams{};
     p->qt = w->qt;
@@ -486,7 +656,7 @@ int lamp_attn_logits8(const uint16_t *q, const uint16_t *k, int B, int Hq, int H
 {
     lamp::LogitsParams p;
     Workspace w;
-    int rc = logits_common(q, k, B, Hq, Hkv, N, d, causal, window, row0, nrows, y8, &p, &w);
+    int rc = logits_common(q, k, B, Hq, Hkv, N, d, causal, window, row0, nrows, y8, &p, &w, stream);
     if (rc) return rc;
     p.y8 = y8;
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -500,7 +670,7 @@ int lamp_attn_logits8_sr(const uint16_t *q, const uint16_t *k, int B, int Hq, in
 {
     lamp::LogitsParams p;
     Workspace w;
-    int rc = logits_common(q, k, B, Hq, Hkv, N, d, causal, window, row0, nrows, y8, &p, &w);
+    int rc = logits_common(q, k, B, Hq, Hkv, N, d, causal, window, row0, nrows, y8, &p, &w, stream);
     if (rc) return rc;
     p.y8 = y8;
     p.seed = seed;
@@ -515,7 +685,7 @@ int lamp_attn_logits16(const uint16_t *q, const uint16_t *k, int B, int Hq, int 
 {
     lamp::LogitsParams p;
     Workspace w;
-    int rc = logits_common(q, k, B, Hq, Hkv, N, d, causal, window, row0, nrows, y16, &p, &w);
+    int rc = logits_common(q, k, B, Hq, Hkv, N, d, causal, window, row0, nrows, y16, &p, &w, stream);
     if (rc) return rc;
     p.y16 = y16;
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -529,7 +699,7 @@ int lamp_attn_logits_sim(const uint16_t *q, const uint16_t *k, int B, int Hq, in
 {
     lamp::LogitsParams p;
     Workspace w;
-    int rc = logits_common(q, k, B, Hq, Hkv, N, d, causal, window, row0, nrows, y, &p, &w);
+    int rc = logits_common(q, k, B, Hq, Hkv, N, d, causal, window, row0, nrows, y, &p, &w, stream);
     if (rc) return rc;
     p.ysim = y;
     hipStream_t s = static_cast<hipStream_t>(stream);

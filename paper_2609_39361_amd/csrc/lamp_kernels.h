@@ -32,6 +32,10 @@ struct FwdParams {
     unsigned flags;           // LAMP_SIM_PROFILE; LAMP_STAGE1_OFF | LAMP_MU_TRUNC in the threshold mode
     double delta, tau;
     uint64_t seed;            // key of the stochastic-rounding generator (dispatch_fwd_sr)
+    uint64_t *stats;          // LAMP_STATS_WORDS(NK) counters added to, or null
+    uint8_t *dbg_y8;          // [B][Hq][dbg_nqb*BQ][Nk] 8-bit codes of the observed query blocks, or null
+    uint16_t *dbg_y16;        // the same for the 16-bit codes of recomputed sub-blocks, or null
+    int dbg_qb0, dbg_nqb;     // observed query blocks of every (b, h)
 };
 
 struct LogitsParams {
@@ -71,7 +75,9 @@ hipError_t dispatch_fwd16(int D, int BQ, const FwdParams &p, hipStream_t s, bool
 hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found);
 // the general kernel with stochastically rounded 8-bit logits (row layout)
 hipError_t dispatch_fwd_sr(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found);
-hipError_t launch_transpose_v(const uint16_t *v, uint16_t *vt, int B, int Hkv, int N, int Nk, int D, hipStream_t s);
+// bad (may be null): bit 2 is or-ed into *bad if a V element is not finite.
+hipError_t launch_transpose_v(const uint16_t *v, uint16_t *vt, int B, int Hkv, int N, int Nk, int D, hipStream_t s,
+                              unsigned *bad = nullptr);
 
 // Issue rates of the logit loops' instructions (lamp_rates.hip): ns per
 // wave-instruction (per emulated step for RATE_STEP) per SIMD, into ns[RATE_N].
@@ -79,8 +85,11 @@ enum { RATE_FMAC = 0, RATE_FMAC_DPP = 1, RATE_DECODE = 2, RATE_ENCODE = 3, RATE_
 hipError_t measure_issue_rates(double *ns, hipStream_t s);
 // grouped: the layout of the pipelined kernel (queries in 64-row and keys in
 // 16-row blocks, each block stored [D/4][rows][4]); otherwise [rows][D].
+// bad (may be null): bit 0 (q) or bit 1 (k) is or-ed into *bad if an element
+// is not finite.
 hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float *kt32, int B, int Hq, int Hkv,
-                          int N, int Nq, int Nk, int D, float scale, hipStream_t s, bool grouped = false);
+                          int N, int Nq, int Nk, int D, float scale, hipStream_t s, bool grouped = false,
+                          unsigned *bad = nullptr);
 // whether dispatch_fwd runs the pipelined kernel (which reads the grouped layout)
 bool fwd_grouped(int D, int BQ, int BK, int NK);
 hipError_t launch_logits8(const LogitsParams &p, int D, hipStream_t s, bool sr = false);

@@ -9,7 +9,6 @@
 #include "lamp_kernels.h"
 #include "lamp_loops.h"
 #include "lamp_sr.h"
-#include "lamp_sr.h"
 
 namespace lamp {
 
@@ -38,61 +37,85 @@ __device__ __forceinline__ void rg_of(int u, int G, int blk, int &j, int &g)
 }
 
 // 4 bf16 values (8 bytes) as fp32, times s (s = 1: exact conversion)
-__device__ __forceinline__ float4 bf16x4_scaled(const uint16_t *p, float s)
+__device__ __forceinline__ float4 bf16x4_scaled(const uint2 w, float s)
 {
-    const uint2 w = *reinterpret_cast<const uint2 *>(p);
     return make_float4(bf16_value(w.x & 0xFFFFu) * s, bf16_value(w.x >> 16) * s, bf16_value(w.y & 0xFFFFu) * s,
                        bf16_value(w.y >> 16) * s);
+}
+
+// Nonzero iff one of the bf16 values in a word has an all-ones exponent
+// (an infinity or a NaN).
+__device__ __forceinline__ uint32_t bf16_nonfinite(uint32_t w)
+{
+    return ((w & 0x7F80u) == 0x7F80u) | ((w & 0x7F800000u) == 0x7F800000u);
+}
+
+// Or `bit` into *bad once per wave if any lane saw a non-finite value.
+__device__ __forceinline__ void flag_nonfinite(unsigned *bad, bool seen, unsigned bit)
+{
+    if (__ballot(seen) != 0ull && __lane_id() == (unsigned)__builtin_ctzll(__ballot(seen))) atomicOr(bad, bit);
 }
 
 // Pre-scaled queries q~ = RN32(q * s), rows padded with zeros from N to Nq:
 // qt [BH][Nq][D] from q [BH][N][D] (grouped layout: blk = 64).  Grid: x over
 // the float4 groups of a head, y over heads (both grid-stride).
+// With bad (may be null), bit `bit` is or-ed into *bad if an element of q is
+// not finite.
 __global__ void prescale_q_kernel(const uint16_t *__restrict__ q, float *__restrict__ qt, float s, int N, int Nq,
-                                  int D, int BH, int blk)
+                                  int D, int BH, int blk, unsigned *bad, unsigned bit)
 {
     const int G = D / 4, n4 = Nq * G;
+    bool seen = false;
     for (int bh = blockIdx.y; bh < BH; bh += gridDim.y)
         for (int u = blockIdx.x * blockDim.x + threadIdx.x; u < n4; u += gridDim.x * blockDim.x) {
             int j, g;
             rg_of(u, G, blk, j, g);
-            const float4 v = j < N ? bf16x4_scaled(q + ((size_t)bh * N + j) * D + 4 * g, s)
-                                   : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-            reinterpret_cast<float4 *>(qt + (size_t)bh * Nq * D)[u] = v;
+            const uint2 w = j < N ? *reinterpret_cast<const uint2 *>(q + ((size_t)bh * N + j) * D + 4 * g)
+                                  : make_uint2(0u, 0u);
+            seen |= (bf16_nonfinite(w.x) | bf16_nonfinite(w.y)) != 0u;
+            reinterpret_cast<float4 *>(qt + (size_t)bh * Nq * D)[u] = bf16x4_scaled(w, s);
         }
+    if (bad) flag_nonfinite(bad, seen, bit);
 }
 
 // K in fp32 (bf16 -> fp32 is exact), rows padded with zeros from N to Nk:
 // k32 [BH][Nk][D] from k [BH][N][D] (grouped layout: blk = 16).
 __global__ void convert_k_kernel(const uint16_t *__restrict__ k, float *__restrict__ k32, int N, int Nk, int D,
-                                 int BH, int blk)
+                                 int BH, int blk, unsigned *bad)
 {
     const int G = D / 4, n4 = Nk * G;
+    bool seen = false;
     for (int bh = blockIdx.y; bh < BH; bh += gridDim.y)
         for (int u = blockIdx.x * blockDim.x + threadIdx.x; u < n4; u += gridDim.x * blockDim.x) {
             int j, g;
             rg_of(u, G, blk, j, g);
-            const float4 v = j < N ? bf16x4_scaled(k + ((size_t)bh * N + j) * D + 4 * g, 1.0f)
-                                   : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-            reinterpret_cast<float4 *>(k32 + (size_t)bh * Nk * D)[u] = v;
+            const uint2 w = j < N ? *reinterpret_cast<const uint2 *>(k + ((size_t)bh * N + j) * D + 4 * g)
+                                  : make_uint2(0u, 0u);
+            seen |= (bf16_nonfinite(w.x) | bf16_nonfinite(w.y)) != 0u;
+            reinterpret_cast<float4 *>(k32 + (size_t)bh * Nk * D)[u] = bf16x4_scaled(w, 1.0f);
         }
+    if (bad) flag_nonfinite(bad, seen, 2u);
 }
 
 // V^T [B*Hkv][D][Nk] from V [B*Hkv][N][D] (bf16), keys padded with zeros
 // from N to Nk: 64x64 tiles through LDS.  grid (Nk/64, D/64, B*Hkv); Nk and
 // D are multiples of 64.
 __global__ __launch_bounds__(256) void transpose_v_kernel(const uint16_t *__restrict__ v, uint16_t *__restrict__ vt,
-                                                          int N, int Nk, int D)
+                                                          int N, int Nk, int D, unsigned *bad)
 {
     __shared__ uint16_t tile[64][66];
     const size_t bh = blockIdx.z;
     const int n0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
     const uint16_t *src = v + bh * (size_t)N * D;
     uint16_t *dst = vt + bh * (size_t)D * Nk;
+    bool seen = false;
     for (int e = threadIdx.x; e < 64 * 64; e += 256) {
         const int r = e / 64, c = e % 64;
-        tile[r][c] = n0 + r < N ? src[(size_t)(n0 + r) * D + c0 + c] : (uint16_t)0;
+        const uint16_t x = n0 + r < N ? src[(size_t)(n0 + r) * D + c0 + c] : (uint16_t)0;
+        seen |= (x & 0x7F80u) == 0x7F80u;
+        tile[r][c] = x;
     }
+    if (bad) flag_nonfinite(bad, seen, 4u);
     __syncthreads();
     for (int e = threadIdx.x; e < 64 * 64; e += 256) {
         const int c = e / 64, r = e % 64;
@@ -201,10 +224,10 @@ __global__ __launch_bounds__(64) void logits8_kernel(LogitsParams p)
     for (int g = 0; g < NC; ++g) {
         const int key0 = (blockIdx.y * NC + g) * 16;
         const float *kt = p.kt32 + (((size_t)b * p.Hkv + hk) * p.N + key0) * (size_t)D;
-        uint32_t acc[1][8];
+        uint32_t acc[1][8], sat[1];
         if constexpr (SR) {
             const int jq[1] = {j};
-            sr8_chunk<D, 1>(qrow, kt, p.seed, (uint64_t)bh, jq, key0, acc);
+            sr8_chunk<D, 1>(qrow, kt, p.seed, (uint64_t)bh, jq, key0, acc, sat);
         } else {
             emu8_chunk<D, 1>(qrow, kt, acc);
         }
@@ -324,25 +347,27 @@ static dim3 prepass_grid(int BH, int rows, int D)
 }
 
 hipError_t launch_prepass(const uint16_t *q, const uint16_t *k, float *qt, float *kt32, int B, int Hq, int Hkv,
-                          int N, int Nq, int Nk, int D, float scale, hipStream_t s, bool grouped)
+                          int N, int Nq, int Nk, int D, float scale, hipStream_t s, bool grouped, unsigned *bad)
 {
     hipLaunchKernelGGL(prescale_q_kernel, prepass_grid(B * Hq, Nq, D), dim3(256), 0, s, q, qt, scale, N, Nq, D, B * Hq,
-                       grouped ? 64 : 0);
+                       grouped ? 64 : 0, bad, 1u);
     hipLaunchKernelGGL(convert_k_kernel, prepass_grid(B * Hkv, Nk, D), dim3(256), 0, s, k, kt32, N, Nk, D, B * Hkv,
-                       grouped ? 16 : 0);
+                       grouped ? 16 : 0, bad);
     return hipGetLastError();
 }
 
 hipError_t launch_prescale_q(const uint16_t *q, float *qt, int BH, int rows, int D, float scale, hipStream_t s)
 {
-    hipLaunchKernelGGL(prescale_q_kernel, prepass_grid(BH, rows, D), dim3(256), 0, s, q, qt, scale, rows, rows, D, BH, 0);
+    hipLaunchKernelGGL(prescale_q_kernel, prepass_grid(BH, rows, D), dim3(256), 0, s, q, qt, scale, rows, rows, D, BH, 0,
+                       (unsigned *)nullptr, 0u);
     return hipGetLastError();
 }
 
-hipError_t launch_transpose_v(const uint16_t *v, uint16_t *vt, int B, int Hkv, int N, int Nk, int D, hipStream_t s)
+hipError_t launch_transpose_v(const uint16_t *v, uint16_t *vt, int B, int Hkv, int N, int Nk, int D, hipStream_t s,
+                              unsigned *bad)
 {
     hipLaunchKernelGGL(transpose_v_kernel, dim3((unsigned)(Nk / 64), (unsigned)(D / 64), (unsigned)(B * Hkv)),
-                       dim3(256), 0, s, v, vt, N, Nk, D);
+                       dim3(256), 0, s, v, vt, N, Nk, D, bad);
     return hipGetLastError();
 }
 

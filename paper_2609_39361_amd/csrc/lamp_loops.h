@@ -80,6 +80,15 @@ __device__ __forceinline__ void dpp_guard()
     asm volatile("s_nop 1");
 }
 
+// dpp_guard with a scheduling barrier after it, for loops whose first
+// broadcast FMAs the scheduler would otherwise hoist above the wait states
+// (the FMAs are side-effect-free inline assembly and may move across them).
+__device__ __forceinline__ void dpp_guard_fenced()
+{
+    asm volatile("s_nop 1");
+    __builtin_amdgcn_sched_barrier(0);
+}
+
 // Query rows come either from global memory (const float *) or from LDS
 // (lds_cfptr, so that the loads are ds_read_b128 rather than flat loads).
 typedef const __attribute__((address_space(3))) float *lds_cfptr;
@@ -175,19 +184,53 @@ __device__ __forceinline__ void emu8_pass(const QP (&qrow)[QPL], const float *k3
     run(kb, qb);
 }
 
+// Keys whose 8-bit code is a NaN after the non-saturating pass, one bit per
+// key (bit i: key i of the 16, codes of keys 2p and 2p+1 in word p).  Such a
+// chain overflowed in some step, which is exactly when the saturating
+// recursion clamps to +-448: the two recursions agree up to that step.
+template <int QPL>
+__device__ __forceinline__ void nan_keys(const uint32_t (&acc)[QPL][8], uint32_t (&sat)[QPL])
+{
+#pragma unroll
+    for (int s = 0; s < QPL; ++s) {
+        uint32_t m = 0;
+#pragma unroll
+        for (int p = 0; p < 8; ++p) {
+            const uint32_t r = e4m3_nan_bits(acc[s][p]);
+            m |= ((r >> 7) & 1u) << (2 * p);
+            m |= ((r >> 15) & 1u) << (2 * p + 1);
+        }
+        sat[s] = m;
+    }
+}
+
 // The fast pass uses the non-saturating conversion; if any lane of the wave
 // overflowed somewhere (a NaN code at the end of a chain), the chunk is
-// recomputed with the saturating conversion.
+// recomputed with the saturating conversion.  sat[s] receives the keys of
+// slot s whose accumulation saturated (nan_keys), 0 when none did.
 template <int D, int QPL, class LY = RowLay<D>, class QP>
-__device__ __forceinline__ void emu8_chunk(const QP (&qrow)[QPL], const float *k32, uint32_t (&acc)[QPL][8])
+__device__ __forceinline__ void emu8_chunk(const QP (&qrow)[QPL], const float *k32, uint32_t (&acc)[QPL][8],
+                                           uint32_t (&sat)[QPL])
 {
     emu8_pass<D, QPL, false, LY>(qrow, k32, acc);
     uint32_t nan = 0;
 #pragma unroll
-    for (int s = 0; s < QPL; ++s)
+    for (int s = 0; s < QPL; ++s) {
+        sat[s] = 0u;
 #pragma unroll
         for (int p = 0; p < 8; ++p) nan |= e4m3_nan_bits(acc[s][p]);
-    if (wave_any(nan != 0)) emu8_pass<D, QPL, true, LY>(qrow, k32, acc);
+    }
+    if (wave_any(nan != 0)) {
+        nan_keys<QPL>(acc, sat);
+        emu8_pass<D, QPL, true, LY>(qrow, k32, acc);
+    }
+}
+
+template <int D, int QPL, class LY = RowLay<D>, class QP>
+__device__ __forceinline__ void emu8_chunk(const QP (&qrow)[QPL], const float *k32, uint32_t (&acc)[QPL][8])
+{
+    uint32_t sat[QPL];
+    emu8_chunk<D, QPL, LY>(qrow, k32, acc, sat);
 }
 
 // One channel of the 16-bit accumulation for every key and slot.
@@ -252,14 +295,14 @@ __device__ __forceinline__ void emu8s_pass(const QP (&qrow)[QPL], const float *k
     };
     load_group<QPL, LY>(krow, qrow, 0, ka, qa);
     for (int c = 0; c < D - 8; c += 8) {
-        dpp_guard();
+        dpp_guard_fenced();
         load_group<QPL, LY>(krow, qrow, c + 4, kb, qb);
         run(ka, qa);
         load_group<QPL, LY>(krow, qrow, c + 8, ka, qa);
         run(kb, qb);
     }
     load_group<QPL, LY>(krow, qrow, D - 4, kb, qb);
-    dpp_guard();
+    dpp_guard_fenced();
     run(ka, qa);
     run(kb, qb);
 #pragma unroll
@@ -268,12 +311,19 @@ __device__ __forceinline__ void emu8s_pass(const QP (&qrow)[QPL], const float *k
         for (int p = 0; p < 8; ++p) codes[s][p] = pack_sim8(acc[s][2 * p], acc[s][2 * p + 1]);
 }
 
-// Y8 of a 16-key chunk in either profile.
+// Y8 of a 16-key chunk in either profile (sat as in emu8_chunk; 0 in the
+// SIM profile, which does not saturate).
 template <int D, int QPL, bool SIMP, class LY = RowLay<D>, class QP>
-__device__ __forceinline__ void emu8_any(const QP (&qrow)[QPL], const float *k32, uint32_t (&codes)[QPL][8])
+__device__ __forceinline__ void emu8_any(const QP (&qrow)[QPL], const float *k32, uint32_t (&codes)[QPL][8],
+                                         uint32_t (&sat)[QPL])
 {
-    if constexpr (SIMP) emu8s_pass<D, QPL, LY>(qrow, k32, codes);
-    else emu8_chunk<D, QPL, LY>(qrow, k32, codes);
+    if constexpr (SIMP) {
+        emu8s_pass<D, QPL, LY>(qrow, k32, codes);
+#pragma unroll
+        for (int s = 0; s < QPL; ++s) sat[s] = 0u;
+    } else {
+        emu8_chunk<D, QPL, LY>(qrow, k32, codes, sat);
+    }
 }
 
 // The 16-bit logits of the FP32 chains in acc, encoded: rounded once to e4m11
@@ -305,9 +355,11 @@ __device__ __forceinline__ void encode16(const float (&acc)[QPL][NKEY], uint32_t
 // accumulation of NKEY keys, this lane's key row being krowr (as rec16_keys).
 // The forward kernel uses it to run the 8-bit logits of the next key tile
 // together with the speculative 16-bit recompute of the current one.
+// sat receives the saturated keys of the 8-bit chunk as in emu8_chunk.
 template <int D, int QPL, int NKEY, bool EMU, bool SIMP, class LY = RowLay<D>, class QP>
 __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k32e, const float *krowr,
-                                           uint32_t (&a8)[QPL][8], uint32_t (&c16)[QPL][y16_words<SIMP>(NKEY)])
+                                           uint32_t (&a8)[QPL][8], uint32_t (&c16)[QPL][y16_words<SIMP>(NKEY)],
+                                           uint32_t (&sat)[QPL])
 {
     static_assert(EMU || NKEY > 0, "something to compute");
     static_assert(NKEY == 0 || NKEY == 4 || NKEY == 8 || NKEY == 12 || NKEY == 16, "0, 4, 8, 12 or 16 keys");
@@ -317,6 +369,7 @@ __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k
     float acc[QPL][NA], e8[QPL][NE];
 #pragma unroll
     for (int s = 0; s < QPL; ++s) {
+        sat[s] = 0u;
 #pragma unroll
         for (int p = 0; p < 8; ++p) a8[s][p] = 0u;
 #pragma unroll
@@ -325,6 +378,12 @@ __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k
         for (int i = 0; i < NE; ++i) e8[s][i] = 0.0f;
     }
     const float *krowe = k32e + (size_t)(__lane_id() & 15) * LY::KR;
+    // the SIM profile's loop needs the fenced guard (its schedule hoists
+    // broadcast FMAs above a plain one)
+    auto guard = [] {
+        if constexpr (SIMP) dpp_guard_fenced();
+        else dpp_guard();
+    };
     float4 kea, keb, kra, krb, qa[QPL], qb[QPL];
     auto ld = [&](int c, float4 &ke, float4 &kr, float4 (&q4)[QPL]) {
         if constexpr (EMU) ke = load4(krowe + (c / 4) * LY::KS);
@@ -348,14 +407,14 @@ __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k
     };
     ld(0, kea, kra, qa);
     for (int c = 0; c < D - 8; c += 8) {
-        dpp_guard();
+        guard();
         ld(c + 4, keb, krb, qb);
         run(kea, kra, qa);
         ld(c + 8, kea, kra, qa);
         run(keb, krb, qb);
     }
     ld(D - 4, keb, krb, qb);
-    dpp_guard();
+    guard();
     run(kea, kra, qa);
     run(keb, krb, qb);
     if constexpr (EMU && SIMP) {
@@ -369,7 +428,10 @@ __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k
         for (int s = 0; s < QPL; ++s)
 #pragma unroll
             for (int p = 0; p < 8; ++p) nan |= e4m3_nan_bits(a8[s][p]);
-        if (wave_any(nan != 0)) emu8_pass<D, QPL, true, LY>(qrow, k32e, a8);
+        if (wave_any(nan != 0)) {
+            nan_keys<QPL>(a8, sat);
+            emu8_pass<D, QPL, true, LY>(qrow, k32e, a8);
+        }
     }
     if constexpr (NKEY > 0) encode16<SIMP>(acc, c16);
 }
@@ -429,6 +491,19 @@ __device__ __forceinline__ void rec16_keys(const QP (&qrow)[QPL], const float *k
 #pragma unroll
     for (int r = 0; r < PD; ++r) run(r);   // the last ring, no further loads
     encode16<SIMP>(acc, codes);
+}
+
+// Whether the 16-bit logit of one (query row, key) saturates: its FP32 FMA
+// chain (channels ascending from +0, the recursion rec16_keys runs) rounds
+// beyond 511.875, the largest e4m11 value, i.e. |sum| >= 511.9375 (a tie
+// goes to the even 512).  Used only where a 16-bit code is at that maximum.
+template <int D, class LY>
+__device__ __forceinline__ bool y16_saturates(const float *qrow, const float *krow)
+{
+    float a = 0.0f;
+#pragma unroll 4
+    for (int c = 0; c < D; ++c) a = __builtin_fmaf(qrow[(c / 4) * LY::QS + c % 4], krow[(c / 4) * LY::KS + c % 4], a);
+    return __builtin_fabsf(a) >= 511.9375f;
 }
 
 // Y16 of the 16 keys starting at k32 ([key][D] fp32).

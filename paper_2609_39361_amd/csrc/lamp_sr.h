@@ -62,11 +62,14 @@ __device__ __forceinline__ uint32_t sr_r20(const uint64_t (&w)[4])
 // spacing is 2^-9: the magnitude in units of 2^-29, truncated to an integer
 // (the floor the rounding asks for), takes the same carry step, and the
 // result is converted back (all steps exact).
-__device__ __forceinline__ float sr_e4m3(float t, uint32_t r)
+// amax keeps the largest |t| pattern seen, so that a chain whose steps were
+// clamped (|t| > 448) can be counted.
+__device__ __forceinline__ float sr_e4m3(float t, uint32_t r, uint32_t &amax)
 {
     const uint32_t bits = __builtin_bit_cast(uint32_t, t);
     const uint32_t sign = bits & 0x80000000u;
     uint32_t a = bits & 0x7FFFFFFFu;
+    amax = amax > a ? amax : a;
     a = a < 0x43E00000u ? a : 0x43E00000u;                                 // 448
     const bool sub = a < 0x3C800000u;                                       // below 2^-6
     const uint32_t n = (uint32_t)(__builtin_bit_cast(float, a) * 536870912.0f);   // 2^29 units, floor
@@ -79,9 +82,9 @@ __device__ __forceinline__ float sr_e4m3(float t, uint32_t r)
 // The steps of one row over the channels U... of a group, in order.
 template <int NC, int... U>
 __device__ __forceinline__ float sr8_steps(const float (&qv)[NC], const float (&kv)[NC], const uint64_t (&w)[4],
-                                           float v, std::integer_sequence<int, U...>)
+                                           float v, uint32_t &amax, std::integer_sequence<int, U...>)
 {
-    ((v = sr_e4m3(__builtin_fmaf(qv[U], kv[U], v), sr_r20<U>(w))), ...);
+    ((v = sr_e4m3(__builtin_fmaf(qv[U], kv[U], v), sr_r20<U>(w), amax)), ...);
     return v;
 }
 
@@ -89,7 +92,8 @@ __device__ __forceinline__ float sr8_steps(const float (&qv)[NC], const float (&
 // the NC steps of each row's recursion.
 template <int NC, int QPL>
 __device__ __forceinline__ void sr8_group(const float *const (&qrow)[QPL], const float *krow, int c0, uint64_t seed,
-                                          uint64_t bh, const int (&j)[QPL], uint32_t key, float (&y)[QPL])
+                                          uint64_t bh, const int (&j)[QPL], uint32_t key, float (&y)[QPL],
+                                          uint32_t (&amax)[QPL])
 {
     static_assert(NC % 4 == 0 && NC <= 12, "whole 4-channel loads, at most one call");
     float kv[NC];
@@ -108,7 +112,7 @@ __device__ __forceinline__ void sr8_group(const float *const (&qrow)[QPL], const
         }
         uint64_t w[4] = {(uint64_t)(uint32_t)j[s], (uint64_t)key, bh, (uint64_t)(c0 / 12)};
         philox4x64_10(w, seed, 0);
-        y[s] = sr8_steps(qv, kv, w, y[s], std::make_integer_sequence<int, NC>{});
+        y[s] = sr8_steps(qv, kv, w, y[s], amax[s], std::make_integer_sequence<int, NC>{});
     }
 }
 
@@ -116,30 +120,39 @@ __device__ __forceinline__ void sr8_group(const float *const (&qrow)[QPL], const
 // lane: the key rows k32 + kk*D (fp32, kk = 0..15, the same for every lane),
 // the query rows qrow[s] (fp32, pre-scaled) of query index j[s]; key index
 // i0 + kk; bh = b*Hq + h.  Codes out as in emu8_chunk: acc[s][p] holds the
-// e4m3 codes of keys 2p (bits 7:0) and 2p+1 (bits 15:8).
+// e4m3 codes of keys 2p (bits 7:0) and 2p+1 (bits 15:8); sat[s] bit kk is
+// set when a step of key kk's chain was clamped (|t| > 448).
 template <int D, int QPL>
 __device__ __forceinline__ void sr8_chunk(const float *const (&qrow)[QPL], const float *k32, uint64_t seed,
-                                          uint64_t bh, const int (&j)[QPL], int i0, uint32_t (&acc)[QPL][8])
+                                          uint64_t bh, const int (&j)[QPL], int i0, uint32_t (&acc)[QPL][8],
+                                          uint32_t (&sat)[QPL])
 {
     static_assert(D % 4 == 0, "channel groups of 4");
 #pragma unroll
-    for (int s = 0; s < QPL; ++s)
+    for (int s = 0; s < QPL; ++s) {
+        sat[s] = 0u;
 #pragma unroll
         for (int p = 0; p < 8; ++p) acc[s][p] = 0u;
+    }
     for (int kk = 0; kk < 16; ++kk) {
         const float *krow = k32 + (size_t)kk * D;
         const uint32_t key = (uint32_t)(i0 + kk);
         float y[QPL];
+        uint32_t amax[QPL];
 #pragma unroll
-        for (int s = 0; s < QPL; ++s) y[s] = 0.0f;
-        for (int g = 0; g < D / 12; ++g) sr8_group<12, QPL>(qrow, krow, 12 * g, seed, bh, j, key, y);
-        if constexpr (D % 12 != 0) sr8_group<D % 12, QPL>(qrow, krow, D / 12 * 12, seed, bh, j, key, y);
+        for (int s = 0; s < QPL; ++s) {
+            y[s] = 0.0f;
+            amax[s] = 0u;
+        }
+        for (int g = 0; g < D / 12; ++g) sr8_group<12, QPL>(qrow, krow, 12 * g, seed, bh, j, key, y, amax);
+        if constexpr (D % 12 != 0) sr8_group<D % 12, QPL>(qrow, krow, D / 12 * 12, seed, bh, j, key, y, amax);
         // the code of key kk into its byte (exact: y is an e4m3 value)
 #pragma unroll
         for (int s = 0; s < QPL; ++s) {
             const uint32_t code = pk_e4m3_sat(y[s], 0.0f) & 0xFFu;
 #pragma unroll
             for (int p = 0; p < 8; ++p) acc[s][p] |= (p == (kk >> 1)) ? code << (8 * (kk & 1)) : 0u;
+            sat[s] |= (amax[s] > 0x43E00000u ? 1u : 0u) << kk;
         }
     }
 }

@@ -15,7 +15,25 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "liblamp.so")
 
 LAMP_OK = 0
+LAMP_ERR_NONFINITE_INPUT = 5
+LAMP_ERR_WORKSPACE = 6
 MASK_LOW, MASK_STAGE1, MASK_STAGE2, MASK_INACTIVE = 0, 1, 2, 3
+
+# statistics words (include/lamp.h, LAMP_STAT_*)
+STAT_NAMES = ("tiles", "stage1", "stage2", "inactive", "sat8", "sat16", "spec_unused", "late16")
+STAT_HIST = len(STAT_NAMES)
+
+
+def stats_words(nk):
+    """Number of uint64 statistics words for nk sub-blocks per tile."""
+    return STAT_HIST + nk + 1
+
+
+class FwdExtra(ctypes.Structure):
+    """struct lamp_fwd_extra (include/lamp.h)."""
+    _fields_ = [("stats", ctypes.c_void_p), ("dbg_y8", ctypes.c_void_p), ("dbg_y16", ctypes.c_void_p),
+                ("dbg_qb0", ctypes.c_int), ("dbg_nqb", ctypes.c_int), ("workspace", ctypes.c_void_p),
+                ("workspace_bytes", ctypes.c_size_t)]
 
 
 class LampError(RuntimeError):
@@ -35,23 +53,29 @@ def lib():
             raise RuntimeError("liblamp.so is not built; run `python -m paper_2609_39361_amd.build`")
         L = ctypes.CDLL(LIB_PATH)
         P, i32, f64, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_double, ctypes.c_size_t
-        L.lamp_attn_fwd.argtypes = [P, P, P] + [i32] * 5 + [i32] * 5 + [f64, f64, ctypes.c_uint, P, P, P, P]
+        L.lamp_attn_fwd.argtypes = [P, P, P] + [i32] * 5 + [i32] * 5 + [f64, f64, ctypes.c_uint, P, P, P, P, P]
         L.lamp_attn_fwd.restype = i32
         L.lamp_attn_logits8.argtypes = [P, P] + [i32] * 9 + [P, P]
         L.lamp_attn_logits8.restype = i32
         L.lamp_attn_fwd_sr.argtypes = ([P, P, P] + [i32] * 5 + [i32] * 5 + [f64, f64, ctypes.c_uint, ctypes.c_uint64]
-                                       + [P, P, P, P])
+                                       + [P, P, P, P, P])
         L.lamp_attn_fwd_sr.restype = i32
         L.lamp_attn_logits8_sr.argtypes = [P, P] + [i32] * 9 + [ctypes.c_uint64, P, P]
         L.lamp_attn_logits8_sr.restype = i32
         L.lamp_attn_logits16.argtypes = [P, P] + [i32] * 9 + [P, P]
         L.lamp_attn_logits16.restype = i32
-        L.lamp_attn_decode.argtypes = [P, P, P] + [i32] * 9 + [f64, f64, ctypes.c_uint, P, P, P, P]
+        L.lamp_attn_decode.argtypes = [P, P, P] + [i32] * 9 + [f64, f64, ctypes.c_uint, P, P, P, P, P]
         L.lamp_attn_decode.restype = i32
         L.lamp_attn_logits_sim.argtypes = [P, P] + [i32] * 10 + [P, P]
         L.lamp_attn_logits_sim.restype = i32
         L.lamp_get_sim_tables.argtypes = [i32, P, P]
         L.lamp_get_sim_tables.restype = i32
+        L.lamp_attn_fwd_workspace_size.argtypes = [i32] * 8
+        L.lamp_attn_fwd_workspace_size.restype = sz
+        L.lamp_attn_decode_workspace_size.argtypes = [i32] * 6
+        L.lamp_attn_decode_workspace_size.restype = sz
+        L.lamp_reserve.argtypes = [i32, sz]
+        L.lamp_reserve.restype = i32
         L.lamp_init.argtypes = [i32]
         L.lamp_init.restype = i32
         L.lamp_shutdown.argtypes = []
@@ -109,38 +133,127 @@ def _check_inputs(q, k, v=None):
 STAGE1_OFF = 1   # the first stage disabled: mu_hat from the 8-bit maxima, stage 2 alone recomputes
 MU_TRUNC = 2     # 8-bit shifts against mu_hat truncated to e4m3 (SIM profile: to 3 mantissa bits)
 SIM_PROFILE = 4  # the SIM precision profile (FP32 range, 3 / 11 mantissa bits, no saturation)
+CHECK_FINITE = 8  # check q, k, v for NaN / infinity first (synchronous; LAMP_ERR_NONFINITE_INPUT)
+
+
+def _check_out(t, name, shape, dtype, device):
+    if (not isinstance(t, torch.Tensor) or tuple(t.shape) != tuple(shape) or t.dtype != dtype
+            or t.device != device or not t.is_contiguous()):
+        raise ValueError("%s must be a contiguous %s tensor of shape %s on %s" % (name, dtype, tuple(shape), device))
+
+
+def _extra(stats=None, observe=None, workspace=None, device=None, nk=4):
+    """(FwdExtra or None, tensors kept alive) from the optional arguments."""
+    if stats is None and observe is None and workspace is None:
+        return None, ()
+    e = FwdExtra()
+    keep = []
+    if stats is not None:
+        _check_out(stats, "stats", (stats_words(nk),), torch.int64, device)
+        e.stats = stats.data_ptr()
+        keep.append(stats)
+    if observe is not None:
+        qb0, nqb, y8, y16 = observe
+        e.dbg_qb0, e.dbg_nqb = int(qb0), int(nqb)
+        for t in (y8, y16):
+            if t is not None:
+                if not t.is_contiguous() or t.device != device:
+                    raise ValueError("observable arrays must be contiguous tensors on the inputs' device")
+                keep.append(t)
+        e.dbg_y8 = y8.data_ptr() if y8 is not None else None
+        e.dbg_y16 = y16.data_ptr() if y16 is not None else None
+    if workspace is not None:
+        if workspace.device != device or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous tensor on the inputs' device")
+        e.workspace = workspace.data_ptr()
+        e.workspace_bytes = workspace.numel() * workspace.element_size()
+        keep.append(workspace)
+    return e, tuple(keep)
 
 
 def attn_fwd(q, k, v, causal=True, window=0, bq=128, bk=16, nk=4, delta=2.0 ** -8, tau=0.5, out=None, flags=0,
-             sr_seed=None):
+             sr_seed=None, stats=None, observe=None, workspace=None):
     """LampAttention forward pass.  Returns (o fp32 [B,Hq,N,d], lse fp32
     [B,Hq,N], mask uint8 [B,Hq,ceil(N/bq),ceil(N/(bk*nk))*nk]); N need not be
     a multiple of the block sizes.  `out` may supply those three tensors to
-    write into; `flags` selects the variants STAGE1_OFF, MU_TRUNC and the
-    SIM_PROFILE numerics.  With `sr_seed` (an int below 2^64) the 8-bit
-    accumulation is rounded stochastically with that seed (lamp_attn_fwd_sr)."""
+    write into; `flags` selects the variants STAGE1_OFF, MU_TRUNC, the
+    SIM_PROFILE numerics and the CHECK_FINITE input check.  With `sr_seed` (an
+    int below 2^64) the 8-bit accumulation is rounded stochastically with that
+    seed (lamp_attn_fwd_sr).
+
+    Optional (struct lamp_fwd_extra): `stats`, an int64 tensor of
+    stats_words(nk) elements on the device that the call adds the statistics
+    words to; `observe` = (qb0, nqb, y8, y16), the forward kernel's 8-bit and
+    16-bit logit codes of query blocks [qb0, qb0+nqb) (see observe_logits);
+    `workspace`, a device tensor of at least fwd_workspace_size(...) bytes."""
     B, Hq, Hkv, N, d = _check_inputs(q, k, v)
     dev = q.device
+    mshape = (B, Hq, -(-N // bq), -(-N // (bk * nk)) * nk)
     if out is None:
         o = torch.empty((B, Hq, N, d), dtype=torch.float32, device=dev)
         lse = torch.empty((B, Hq, N), dtype=torch.float32, device=dev)
-        mask = torch.empty((B, Hq, -(-N // bq), -(-N // (bk * nk)) * nk), dtype=torch.uint8, device=dev)
+        mask = torch.empty(mshape, dtype=torch.uint8, device=dev)
     else:
         o, lse, mask = out
+        _check_out(o, "o", (B, Hq, N, d), torch.float32, dev)
+        _check_out(lse, "lse", (B, Hq, N), torch.float32, dev)
+        _check_out(mask, "mask", mshape, torch.uint8, dev)
+    extra, keep = _extra(stats, observe, workspace, dev, nk)
+    ep = ctypes.byref(extra) if extra is not None else None
     with torch.cuda.device(dev):
         if sr_seed is None:
             rc = lib().lamp_attn_fwd(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(causal), int(window),
                                      bq, bk, nk, float(delta), float(tau), int(flags), _ptr(o), _ptr(lse), _ptr(mask),
-                                     _stream(dev))
+                                     ep, _stream(dev))
         else:
             rc = lib().lamp_attn_fwd_sr(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(causal), int(window),
                                         bq, bk, nk, float(delta), float(tau), int(flags), int(sr_seed),
-                                        _ptr(o), _ptr(lse), _ptr(mask), _stream(dev))
+                                        _ptr(o), _ptr(lse), _ptr(mask), ep, _stream(dev))
+    del keep
     _check(rc)
     return o, lse, mask
 
 
-def attn_decode(q, k, v, causal=True, window=0, tk=64, delta=2.0 ** -8, tau=0.5, out=None, flags=0):
+def observe_logits(q, k, v, qb0, nqb, causal=True, window=0, bq=128, bk=16, nk=4, delta=2.0 ** -8, tau=0.5,
+                   flags=0, sr_seed=None, stats=None):
+    """attn_fwd that also returns the forward kernel's own logit codes of the
+    query blocks [qb0, qb0+nqb) of every (b, h): (o, lse, mask, y8, y16),
+    y8 uint8 [B,Hq,nqb*bq,Nt] (e4m3 codes of visible pairs, 0xFF elsewhere)
+    and y16 int16 bit patterns [B,Hq,nqb*bq,Nt] (e4m11 codes of visible pairs
+    in 16-bit sub-blocks, 0xFFFF elsewhere), Nt = ceil(N/(bk*nk))*bk*nk."""
+    B, Hq, Hkv, N, d = _check_inputs(q, k, v)
+    Nt = -(-N // (bk * nk)) * bk * nk
+    y8 = torch.empty((B, Hq, nqb * bq, Nt), dtype=torch.uint8, device=q.device)
+    y16 = torch.empty((B, Hq, nqb * bq, Nt), dtype=torch.int16, device=q.device)
+    o, lse, mask = attn_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, flags=flags, sr_seed=sr_seed,
+                            stats=stats, observe=(qb0, nqb, y8, y16))
+    return o, lse, mask, y8, y16
+
+
+def fwd_workspace_size(B, Hq, Hkv, N, d, bq=128, bk=16, nk=4):
+    """Bytes of workspace one attn_fwd call needs."""
+    return int(lib().lamp_attn_fwd_workspace_size(B, Hq, Hkv, N, d, bq, bk, nk))
+
+
+def decode_workspace_size(B, Hq, Hkv, M, N, d):
+    return int(lib().lamp_attn_decode_workspace_size(B, Hq, Hkv, M, N, d))
+
+
+def reserve(device, nbytes):
+    """Grow the library's workspace of `device` to nbytes now (synchronous)."""
+    _check(lib().lamp_reserve(int(device), int(nbytes)))
+
+
+def stats_dict(stats, nk=4):
+    """The statistics words as a dict (names of STAT_NAMES, 'hist' a list)."""
+    w = [int(x) for x in stats.cpu().tolist()]
+    r = dict(zip(STAT_NAMES, w[:STAT_HIST]))
+    r["hist"] = w[STAT_HIST:STAT_HIST + nk + 1]
+    return r
+
+
+def attn_decode(q, k, v, causal=True, window=0, tk=64, delta=2.0 ** -8, tau=0.5, out=None, flags=0,
+                workspace=None):
     """LampAttention in the vector form (Sec. 2, Eq. (6)) for M query rows per
     (b, h) at positions N-M .. N-1: q [B,Hq,M,d], k / v [B,Hkv,N,d] bf16.
     Returns (o fp32 [B,Hq,M,d], lse fp32 [B,Hq,M], mask uint8
@@ -153,16 +266,25 @@ def attn_decode(q, k, v, causal=True, window=0, tk=64, delta=2.0 ** -8, tau=0.5,
         if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
             raise ValueError("q, k, v must be contiguous bf16 CUDA tensors")
     dev = q.device
+    if q.device != k.device or v.device != k.device:
+        raise ValueError("q, k, v must be on one device")
+    mshape = (B, Hq, M, -(-N // tk) * tk)
     if out is None:
         o = torch.empty((B, Hq, M, d), dtype=torch.float32, device=dev)
         lse = torch.empty((B, Hq, M), dtype=torch.float32, device=dev)
-        mask = torch.empty((B, Hq, M, -(-N // tk) * tk), dtype=torch.uint8, device=dev)
+        mask = torch.empty(mshape, dtype=torch.uint8, device=dev)
     else:
         o, lse, mask = out
+        _check_out(o, "o", (B, Hq, M, d), torch.float32, dev)
+        _check_out(lse, "lse", (B, Hq, M), torch.float32, dev)
+        _check_out(mask, "mask", mshape, torch.uint8, dev)
+    extra, keep = _extra(workspace=workspace, device=dev)
+    ep = ctypes.byref(extra) if extra is not None else None
     with torch.cuda.device(dev):
         rc = lib().lamp_attn_decode(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, M, N, d, int(causal), int(window), tk,
                                     float(delta), float(tau), int(flags), _ptr(o), _ptr(lse), _ptr(mask),
-                                    _stream(dev))
+                                    ep, _stream(dev))
+    del keep
     _check(rc)
     return o, lse, mask
 

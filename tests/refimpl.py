@@ -43,13 +43,26 @@ def rn32_sum(p, c):
     return np.where(go_r2, r2, r)
 
 
-def y8_tile(qt, kf, fmt="e4m3"):
+def _clamped(t, fmt):
+    """Where rounding t to fmt (e4m3 or e4m11) exceeds the largest value, so
+    that the saturating rounding clamps it: the rounding is repeated on a grid
+    without a largest value (same mantissa bits and smallest normal)."""
+    mbits, emin, maxval = M.FMT[fmt][:3]
+    q = M.np_quantum(np.where(t != 0, t, 1.0), fmt)
+    r = np.round(np.abs(t) / q) * q                     # numpy rounds halves to even
+    return (r > maxval) & (t != 0)
+
+
+def y8_tile(qt, kf, fmt="e4m3", sat=None):
     """qt [bq, d] fp32 values (as fp64), kf [T, d] -> Y8 values [T, bq]
-    (fmt "sim3" for the SIM profile)."""
+    (fmt "sim3" for the SIM profile).  sat: an optional bool array [T, bq]
+    or-ed with the chains clamped in some step."""
     acc = np.zeros((kf.shape[0], qt.shape[0]))
     for c in range(qt.shape[1]):
         p = kf[:, c][:, None] * qt[:, c][None, :]          # exact in fp64
         t = rn32_sum(p, acc)
+        if sat is not None and fmt == "e4m3":
+            sat |= _clamped(t, fmt)
         acc = M.np_round(t, fmt)
     return acc
 
@@ -105,9 +118,10 @@ def sr_round(t, r):
     return np.copysign(res, t)
 
 
-def y8_tile_sr(qt, kf, seed, bh, rows, keys):
+def y8_tile_sr(qt, kf, seed, bh, rows, keys, sat=None):
     """Y8 values [T, bq] with stochastic rounding; rows / keys: the query and
-    key indices of qt's rows and kf's rows."""
+    key indices of qt's rows and kf's rows.  sat: as in y8_tile (a step with
+    |t| > 448)."""
     T, bq, d = kf.shape[0], qt.shape[0], qt.shape[1]
     r = np.zeros((d, T, bq))
     for a, i in enumerate(keys):
@@ -119,15 +133,29 @@ def y8_tile_sr(qt, kf, seed, bh, rows, keys):
     acc = np.zeros((T, bq))
     for c in range(d):
         p = kf[:, c][:, None] * qt[:, c][None, :]          # exact in fp64
-        acc = sr_round(rn32_sum(p, acc), r[c])
+        t = rn32_sum(p, acc)
+        if sat is not None:
+            sat |= np.abs(t) > 448.0
+        acc = sr_round(t, r[c])
     return acc
 
 
-def y16_tile(qt, kf, fmt="e4m11"):
+def y16_tile(qt, kf, fmt="e4m11", sat=None, step=False):
+    """Y16 values [T, bq]: the FP32 FMA chain rounded once to fmt, or, with
+    `step`, rounded to fmt after every FMA (e4m11 as the accumulator).  sat:
+    as in y8_tile."""
     acc = np.zeros((kf.shape[0], qt.shape[0]))
     for c in range(qt.shape[1]):
         p = kf[:, c][:, None] * qt[:, c][None, :]           # exact in fp64
         acc = rn32_sum(p, acc)                               # FP32 FMA step
+        if step:
+            if sat is not None and fmt == "e4m11":
+                sat |= _clamped(acc, fmt)
+            acc = M.np_round(acc, fmt)
+    if step:
+        return acc
+    if sat is not None and fmt == "e4m11":
+        sat |= _clamped(acc, fmt)
     return M.np_round(acc, fmt)
 
 
@@ -192,12 +220,14 @@ def _colsum(E):
     return S
 
 
-def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=0, seed=0):
-    """q [B,Hq,N,d], k/v [B,Hkv,N,d] bf16 bit patterns.  Returns o, lse, mask.
-    flags: 1 = first stage disabled, 2 = 8-bit shifts against mu_hat
-    truncated to e4m3 (both only for 0 < tau < inf), 4 = the SIM precision
-    profile (Sec. 4.1) in every mode, 8 = the 8-bit accumulation rounded
-    stochastically with random words keyed by `seed`."""
+def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=0, seed=0, stats=False):
+    """q [B,Hq,N,d], k/v [B,Hkv,N,d] bf16 bit patterns.  Returns o, lse, mask
+    (and, with `stats`, a dict of the statistics: tiles, stage1, stage2,
+    inactive, sat8, sat16, hist).  flags: 1 = first stage disabled, 2 = 8-bit
+    shifts against mu_hat truncated to e4m3 (both only for 0 < tau < inf),
+    4 = the SIM precision profile (Sec. 4.1) in every mode, 8 = the 8-bit
+    accumulation rounded stochastically with random words keyed by `seed`,
+    16 = the 16-bit logits with e4m11 (SIM: 11 bits) as the accumulator."""
     B, Hq, N, d = q.shape
     Hkv = k.shape[1]
     G = Hq // Hkv
@@ -211,7 +241,9 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=
     stage1_off = (not pure8) and (not all16) and bool(flags & 1)
     mu_trunc = (not pure8) and (not all16) and bool(flags & 2)
     sim = bool(flags & 4)
+    step16 = bool(flags & 16)
     f8, f16 = ("sim3", "sim11") if sim else ("e4m3", "e4m11")
+    st = {"tiles": 0, "stage1": 0, "stage2": 0, "inactive": 0, "sat8": 0, "sat16": 0, "hist": [0] * (nk + 1)}
     trunc8 = _trunc_sim3 if sim else _trunc_e4m3
     for b in range(B):
         for h in range(Hq):
@@ -240,19 +272,22 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=
                     kf = kf_all[np.minimum(ii, N - 1)]
                     prec = np.where(act, 0, 3)
                     Y = np.full((T, bq), np.nan)
+                    sat8 = np.zeros((T, bq), dtype=bool)
                     if not all16 and flags & 8:
-                        Y = y8_tile_sr(qt, kf, seed, b * Hq + h, jj, ii)
+                        Y = y8_tile_sr(qt, kf, seed, b * Hq + h, jj, ii, sat=sat8)
                     elif not all16:
-                        Y = y8_tile(qt, kf, f8)
+                        Y = y8_tile(qt, kf, f8, sat=sat8)
+                    st["sat8"] += int((sat8 & vis).sum())
                     Yv = np.where(vis, Y, -np.inf)
                     m8 = np.array([Yv[th * bk:(th + 1) * bk].max(axis=0) for th in range(nk)])
                     muh = mu.copy()
                     Y16 = None
+                    sat16 = np.zeros((T, bq), dtype=bool)
 
                     def y16():
                         nonlocal Y16
                         if Y16 is None:
-                            Y16 = y16_tile(qt, kf, f16)
+                            Y16 = y16_tile(qt, kf, f16, sat=sat16, step=step16)
                         return Y16
 
                     if pure8 or stage1_off:
@@ -336,9 +371,20 @@ def ref_fwd(q, k, v, causal, window, bq, bk, nk, delta, tau, tabs, scale, flags=
                     O = O * lam[:, None] + E.T @ vf_all[np.minimum(ii, N - 1)]
                     mu = muh
                     mask[b, h, qb, t * nk:(t + 1) * nk] = prec
+                    rec = [th for th in range(nk) if prec[th] in (1, 2)]
+                    st["tiles"] += 1
+                    st["stage1"] += int((prec == 1).sum())
+                    st["stage2"] += int((prec == 2).sum())
+                    st["hist"][len(rec)] += 1
+                    for th in rec:
+                        sl = slice(th * bk, (th + 1) * bk)
+                        st["sat16"] += int((sat16[sl] & vis[sl]).sum())
                 with np.errstate(invalid="ignore", divide="ignore"):
                     o[b, h, q0:q0 + nr] = (O / om[:, None])[:nr]
                     lse[b, h, q0:q0 + nr] = (mu + np.log(om))[:nr]
+    st["inactive"] = int((mask == 3).sum())
+    if stats:
+        return o, lse, mask, st
     return o, lse, mask
 
 

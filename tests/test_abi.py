@@ -49,42 +49,42 @@ def test_binding_rejects_bad_arguments_without_gpu():
     lib = ctypes.CDLL(LIB)
     lib.lamp_attn_fwd.restype = ctypes.c_int
     P = ctypes.c_void_p
-    lib.lamp_attn_fwd.argtypes = [P, P, P] + [ctypes.c_int] * 10 + [ctypes.c_double] * 2 + [ctypes.c_uint] + [P, P, P, P]
+    lib.lamp_attn_fwd.argtypes = [P, P, P] + [ctypes.c_int] * 10 + [ctypes.c_double] * 2 + [ctypes.c_uint] + [P, P, P, P, P]
     lib.lamp_last_error.restype = ctypes.c_char_p
     dummy = P(16)
     # Hq not a multiple of Hkv
     rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 3, 2, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 0,
-                           dummy, dummy, dummy, None)
+                           dummy, dummy, dummy, None, None)
     assert rc == 1 and b"multiple" in lib.lamp_last_error()
     # unsupported head dimension
     rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 96, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 0,
-                           dummy, dummy, dummy, None)
+                           dummy, dummy, dummy, None, None)
     assert rc == 2
     # window without causal
     rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 0, 16, 128, 16, 4, 2 ** -8, 0.5, 0,
-                           dummy, dummy, dummy, None)
+                           dummy, dummy, dummy, None, None)
     assert rc == 1
     # negative threshold
     rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, -1.0, 0,
-                           dummy, dummy, dummy, None)
+                           dummy, dummy, dummy, None, None)
     assert rc == 1
     # unknown flag bits
-    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 8,
-                           dummy, dummy, dummy, None)
+    rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 32,
+                           dummy, dummy, dummy, None, None)
     assert rc == 1 and b"flags" in lib.lamp_last_error()
     # the SIM profile is built for 16-key sub-blocks and d >= 128 only
     rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 128, 64, 4, 2 ** -8, 0.5, 4,
-                           dummy, dummy, dummy, None)
+                           dummy, dummy, dummy, None, None)
     assert rc == 2 and b"SIM" in lib.lamp_last_error()
     rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 64, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 4,
-                           dummy, dummy, dummy, None)
+                           dummy, dummy, dummy, None, None)
     assert rc == 2 and b"SIM" in lib.lamp_last_error()
     # block sizes that are not built
     rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 32, 16, 4, 2 ** -8, 0.5, 0,
-                           dummy, dummy, dummy, None)
+                           dummy, dummy, dummy, None, None)
     assert rc == 2 and b"not built" in lib.lamp_last_error()
     rc = lib.lamp_attn_fwd(dummy, dummy, dummy, 1, 2, 1, 256, 128, 1, 0, 128, 32, 4, 2 ** -8, 0.5, 0,
-                           dummy, dummy, dummy, None)
+                           dummy, dummy, dummy, None, None)
     assert rc == 2
 
 
@@ -94,16 +94,16 @@ def test_decode_rejects_bad_arguments_without_gpu():
     lib = ctypes.CDLL(LIB)
     P = ctypes.c_void_p
     lib.lamp_attn_decode.restype = ctypes.c_int
-    lib.lamp_attn_decode.argtypes = [P, P, P] + [ctypes.c_int] * 9 + [ctypes.c_double] * 2 + [ctypes.c_uint] + [P] * 4
+    lib.lamp_attn_decode.argtypes = [P, P, P] + [ctypes.c_int] * 9 + [ctypes.c_double] * 2 + [ctypes.c_uint] + [P] * 5
     lib.lamp_last_error.restype = ctypes.c_char_p
     d = P(16)
     # (B, Hq, Hkv, M, N, d, causal, window, tk)
-    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 128, 1, 0, 32, 2 ** -8, 0.5, 0, d, d, d, None) == 2
+    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 128, 1, 0, 32, 2 ** -8, 0.5, 0, d, d, d, None, None) == 2
     assert b"tk" in lib.lamp_last_error()
-    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 128, 1, 0, 64, 2 ** -8, 0.5, 4, d, d, d, None) == 1
-    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 300, 256, 128, 1, 0, 64, 2 ** -8, 0.5, 0, d, d, d, None) == 1
-    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 96, 1, 0, 64, 2 ** -8, 0.5, 0, d, d, d, None) == 2
-    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 128, 1, 0, 64, 2 ** -8, -1.0, 0, d, d, d, None) == 1
+    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 128, 1, 0, 64, 2 ** -8, 0.5, 4, d, d, d, None, None) == 1
+    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 300, 256, 128, 1, 0, 64, 2 ** -8, 0.5, 0, d, d, d, None, None) == 1
+    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 96, 1, 0, 64, 2 ** -8, 0.5, 0, d, d, d, None, None) == 2
+    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 128, 1, 0, 64, 2 ** -8, -1.0, 0, d, d, d, None, None) == 1
 
 
 def test_timing_read_without_calls():
@@ -137,15 +137,15 @@ def test_fwd_sr_rejects_bad_arguments_without_gpu():
     P = ctypes.c_void_p
     lib.lamp_attn_fwd_sr.restype = ctypes.c_int
     lib.lamp_attn_fwd_sr.argtypes = ([P, P, P] + [ctypes.c_int] * 10 + [ctypes.c_double] * 2 + [ctypes.c_uint]
-                                     + [ctypes.c_uint64] + [P, P, P, P])
+                                     + [ctypes.c_uint64] + [P, P, P, P, P])
     lib.lamp_last_error.restype = ctypes.c_char_p
     d = ctypes.c_void_p(16)
     args = (d, d, d, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5)
-    assert lib.lamp_attn_fwd_sr(*args, 16, 1, d, d, d, None) == 1
-    assert lib.lamp_attn_fwd_sr(*args, 4, 1, d, d, d, None) == 2
+    assert lib.lamp_attn_fwd_sr(*args, 16, 1, d, d, d, None, None) == 1
+    assert lib.lamp_attn_fwd_sr(*args, 4, 1, d, d, d, None, None) == 2
     assert b"SIM" in lib.lamp_last_error()
     assert lib.lamp_attn_fwd_sr(d, d, d, 1, 2, 1, 256, 128, 1, 0, 128, 32, 4, 2 ** -8, 0.5, 0, 2 ** 64 - 1,
-                                d, d, d, None) == 2
+                                d, d, d, None, None) == 2
 
 
 def test_length_limits_without_gpu():
@@ -157,12 +157,77 @@ def test_length_limits_without_gpu():
     lib = ctypes.CDLL(LIB)
     P = ctypes.c_void_p
     lib.lamp_attn_fwd.restype = ctypes.c_int
-    lib.lamp_attn_fwd.argtypes = [P, P, P] + [ctypes.c_int] * 10 + [ctypes.c_double] * 2 + [ctypes.c_uint] + [P, P, P, P]
+    lib.lamp_attn_fwd.argtypes = [P, P, P] + [ctypes.c_int] * 10 + [ctypes.c_double] * 2 + [ctypes.c_uint] + [P, P, P, P, P]
     lib.lamp_last_error.restype = ctypes.c_char_p
     d = ctypes.c_void_p(16)
     assert lib.lamp_attn_fwd(d, d, d, 1, 1, 1, (1 << 20) + 1, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 0,
-                             d, d, d, None) == 2
+                             d, d, d, None, None) == 2
     assert b"2^20" in lib.lamp_last_error()
     assert lib.lamp_attn_fwd(d, d, d, 4096, 1024, 1, 1 << 20, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 0,
-                             d, d, d, None) == 2
+                             d, d, d, None, None) == 2
     assert b"2^31" in lib.lamp_last_error()
+
+
+class _Extra(ctypes.Structure):
+    _fields_ = [("stats", ctypes.c_void_p), ("dbg_y8", ctypes.c_void_p), ("dbg_y16", ctypes.c_void_p),
+                ("dbg_qb0", ctypes.c_int), ("dbg_nqb", ctypes.c_int), ("workspace", ctypes.c_void_p),
+                ("workspace_bytes", ctypes.c_size_t)]
+
+
+def test_extra_arguments_checked_without_gpu():
+    """The optional arguments are validated before any device call: observed
+    query blocks outside the range, observables with the SIM profile, and
+    statistics or observables asked of the decode form."""
+    if not os.path.exists(LIB):
+        pytest.skip("liblamp.so not built")
+    lib = ctypes.CDLL(LIB)
+    P = ctypes.c_void_p
+    lib.lamp_attn_fwd.restype = ctypes.c_int
+    lib.lamp_attn_fwd.argtypes = [P, P, P] + [ctypes.c_int] * 10 + [ctypes.c_double] * 2 + [ctypes.c_uint] + [P] * 5
+    lib.lamp_attn_decode.restype = ctypes.c_int
+    lib.lamp_attn_decode.argtypes = [P, P, P] + [ctypes.c_int] * 9 + [ctypes.c_double] * 2 + [ctypes.c_uint] + [P] * 5
+    lib.lamp_last_error.restype = ctypes.c_char_p
+    d = ctypes.c_void_p(16)
+    e = _Extra()
+    e.dbg_y8 = 16
+    e.dbg_qb0, e.dbg_nqb = 1, 2          # N = 256, bq = 128: two query blocks, [1, 3) is outside
+    assert lib.lamp_attn_fwd(d, d, d, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 0, d, d, d,
+                             ctypes.byref(e), None) == 1
+    assert b"observed" in lib.lamp_last_error()
+    e.dbg_qb0, e.dbg_nqb = 0, 2
+    assert lib.lamp_attn_fwd(d, d, d, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 4, d, d, d,
+                             ctypes.byref(e), None) == 2
+    e2 = _Extra()
+    e2.stats = 16
+    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 128, 1, 0, 64, 2 ** -8, 0.5, 0, d, d, d,
+                                ctypes.byref(e2), None) == 2
+    # unknown flag bits beyond LAMP_CHECK_FINITE
+    assert lib.lamp_attn_fwd(d, d, d, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 16, d, d, d,
+                             None, None) == 1
+
+
+def test_workspace_sizes_without_gpu():
+    """Workspace sizes: a 256-byte header, the pre-scaled queries and the fp32
+    keys of whole blocks and tiles, and V transposed (config 3: 176 MiB)."""
+    if not os.path.exists(LIB):
+        pytest.skip("liblamp.so not built")
+    lib = ctypes.CDLL(LIB)
+    lib.lamp_attn_fwd_workspace_size.restype = ctypes.c_size_t
+    lib.lamp_attn_fwd_workspace_size.argtypes = [ctypes.c_int] * 8
+    lib.lamp_attn_decode_workspace_size.restype = ctypes.c_size_t
+    lib.lamp_attn_decode_workspace_size.argtypes = [ctypes.c_int] * 6
+    n = lib.lamp_attn_fwd_workspace_size(1, 32, 8, 8192, 128, 128, 16, 4)
+    assert n == 256 + 32 * 8192 * 128 * 4 + 8 * 8192 * 128 * 4 + 8 * 8192 * 128 * 2
+    # ragged N: rows padded to whole query blocks, keys to whole tiles, each part 256-aligned
+    def a256(x):
+        return (x + 255) // 256 * 256
+    assert lib.lamp_attn_fwd_workspace_size(1, 2, 1, 300, 128, 128, 16, 4) == \
+        256 + a256(2 * 384 * 128 * 4) + a256(320 * 128 * 4) + a256(320 * 128 * 2)
+    assert lib.lamp_attn_fwd_workspace_size(0, 2, 1, 300, 128, 128, 16, 4) == 0
+    assert lib.lamp_attn_fwd_workspace_size(1, 2, 1, 300, 128, -1, 16, 4) == 0
+    assert lib.lamp_attn_decode_workspace_size(32, 32, 8, 1, 8192, 128) > 0
+    assert lib.lamp_attn_decode_workspace_size(1, 4, 1, 5, 4, 128) == 0    # M > N
+    lib.lamp_status_str.restype = ctypes.c_char_p
+    lib.lamp_status_str.argtypes = [ctypes.c_int]
+    assert lib.lamp_status_str(5) == b"non-finite input"
+    assert lib.lamp_status_str(6) == b"workspace too small"

@@ -9,7 +9,11 @@
   lies within the ue5m11 rounding bound of an fp64 softmax of Y16;
 * threshold 1 never triggers stage 2 (Sec. 4.2);
 * larger safety margins give more stage-1 recomputes (App. C);
-* rows of the attention matrix sum to one, O is a convex combination of V.
+* rows of the attention matrix sum to one, O is a convex combination of V;
+* the statistics words (tile histogram, stage counts, saturated logits)
+  agree with the independent implementation's counts and with the mask;
+* the per-FMA e4m11 reading of the 16-bit logits (flag Y16_STEP) agrees with
+  the independent implementation.
 """
 import math
 
@@ -278,3 +282,80 @@ def test_empty_inputs():
     k = np.zeros((0, 1, 64, 16), dtype=np.uint16)
     o, lse, mask = O.fwd(q, k, k, 1, 0, 32, 8, 4, 2 ** -8, 0.5)
     assert o.size == 0 and mask.shape == (0, 2, 2, 8)
+
+
+STAT_CASES = CASES + [
+    (W.small("sat_d64", N=96, d=64, Hq=1, Hkv=1, bq=32, bk=8, nk=4, causal=1, seed=31, extra={"gain": 8.0}),
+     0.5, 2 ** -8),
+    (W.small("sat_d64_all16", N=64, d=64, Hq=1, Hkv=1, bq=32, bk=8, nk=4, causal=0, seed=32,
+             extra={"gain": 8.0}), 0.0, 2 ** -8),
+    (W.small("sat_d64_pure8", N=64, d=64, Hq=1, Hkv=1, bq=32, bk=8, nk=4, causal=0, seed=33,
+             extra={"gain": 8.0}), math.inf, 2 ** -8),
+]
+
+
+def _stat_vector(st, nk):
+    return [st["tiles"], st["stage1"], st["stage2"], st["inactive"], st["sat8"], st["sat16"], 0, 0] + st["hist"]
+
+
+@pytest.mark.parametrize("w,tau,delta", STAT_CASES, ids=[c[0].name for c in STAT_CASES])
+def test_stats_match_independent_implementation(w, tau, delta, mp_tables):
+    """Every statistics word against the independent implementation's counts
+    (its saturation test repeats the rounding on an unbounded grid), and the
+    mask-derived words against the mask."""
+    q, k, v = _bits(w)
+    o, lse, mask, st = O.fwd(q, k, v, w.causal, w.window, w.bq, w.bk, w.nk, delta, tau, stats=True)
+    ro, rlse, rmask, rst = R.ref_fwd(q, k, v, w.causal, w.window, w.bq, w.bk, w.nk, delta, tau,
+                                     mp_tables, O.scale(w.d), stats=True)
+    assert np.array_equal(mask, rmask)
+    assert st.tolist() == _stat_vector(rst, w.nk)
+    m = mask.reshape(-1, w.nk)
+    act = (m != 3).any(axis=1)
+    assert st[0] == act.sum() and st[1] == (mask == 1).sum() and st[2] == (mask == 2).sum()
+    assert st[3] == (mask == 3).sum()
+    rec = ((m == 1) | (m == 2)).sum(axis=1)[act]
+    assert st[8:].tolist() == np.bincount(rec, minlength=w.nk + 1).tolist()
+    if "gain" in w.extra:
+        assert st[4] > 0 or tau == 0.0
+        assert st[5] > 0 or math.isinf(tau)
+
+
+def test_stats_stochastic_rounding(mp_tables):
+    """With stochastic rounding the 8-bit saturation count is the chains with
+    a step beyond 448 (the rounding clamps |t| there)."""
+    w = W.small("sat_sr", N=64, d=32, Hq=1, Hkv=1, bq=32, bk=8, nk=4, causal=1, seed=34, extra={"gain": 6.0})
+    q, k, v = _bits(w)
+    o, lse, mask, st = O.fwd(q, k, v, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, 0.5, flags=O.SR8, seed=5,
+                             stats=True)
+    ro, rlse, rmask, rst = R.ref_fwd(q, k, v, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, 0.5, mp_tables,
+                                     O.scale(w.d), flags=8, seed=5, stats=True)
+    assert np.array_equal(mask, rmask)
+    assert st.tolist() == _stat_vector(rst, w.nk)
+    assert st[4] > 0
+
+
+def test_stats_of_subset_add_up():
+    """Statistics of query-block subsets add up to those of the full run."""
+    w = W.small("sub", N=128, d=16, Hq=2, Hkv=1, bq=32, bk=8, nk=4, causal=1, seed=35, extra={"gain": 4.0})
+    q, k, v = _bits(w)
+    full = O.fwd(q, k, v, 1, 0, 32, 8, 4, 2 ** -8, 0.5, stats=True)[3]
+    a = O.fwd(q, k, v, 1, 0, 32, 8, 4, 2 ** -8, 0.5, qblocks=[0, 2, 5, 7], stats=True)[3]
+    b = O.fwd(q, k, v, 1, 0, 32, 8, 4, 2 ** -8, 0.5, qblocks=[1, 3, 4, 6], stats=True)[3]
+    assert (a + b).tolist() == full.tolist()
+
+
+Y16_STEP_CASES = [CASES[0], CASES[1], CASES[2], CASES[7], STAT_CASES[-3]]
+
+
+@pytest.mark.parametrize("w,tau,delta", Y16_STEP_CASES, ids=[c[0].name for c in Y16_STEP_CASES])
+def test_y16_step_reading_matches_independent_implementation(w, tau, delta, mp_tables):
+    """The forward pass with the per-FMA e4m11 reading (flag 16) against the
+    independent implementation; O, lse and masks as for the default reading."""
+    q, k, v = _bits(w)
+    o, lse, mask, st = O.fwd(q, k, v, w.causal, w.window, w.bq, w.bk, w.nk, delta, tau, flags=O.Y16_STEP,
+                             stats=True)
+    ro, rlse, rmask, rst = R.ref_fwd(q, k, v, w.causal, w.window, w.bq, w.bk, w.nk, delta, tau,
+                                     mp_tables, O.scale(w.d), flags=16, stats=True)
+    assert np.array_equal(mask, rmask)
+    np.testing.assert_allclose(o, ro, rtol=1e-9, atol=1e-12)
+    assert st.tolist() == _stat_vector(rst, w.nk)

@@ -2,7 +2,8 @@
 
 Y8 (paper Sec. 4.1, Alg. 1): recursive summation with one FP32 FMA per step,
 the running sum rounded to e4m3 after every step, channels ascending.
-Y16: FP32 FMA chain rounded once to e4m11.  Both are re-derived here with
+Y16: FP32 FMA chain rounded once to e4m11; and the alternative reading with
+e4m11 as the accumulator (rounded after every FMA).  All are re-derived here with
 exact rational arithmetic (Python Fractions), a different method from the
 oracle's float code."""
 from fractions import Fraction
@@ -29,6 +30,16 @@ def _frac_y16(qrow_bits, krow_bits, s):
         qt = M.rn32(Fraction(float(M.bf16_to_float(qb))) * Fraction(float(s)))
         acc = M.rn32(qt * Fraction(float(M.bf16_to_float(kb))) + acc)
     return M.frac_fmt(acc, "e4m11")
+
+
+def _frac_y16_step(qrow_bits, krow_bits, s):
+    """The literal Sec. 3.3 reading: e4m11 as the accumulator, every FP32 FMA
+    result rounded to e4m11 (saturating) before the next step."""
+    acc = Fraction(0)
+    for qb, kb in zip(qrow_bits, krow_bits):
+        qt = M.rn32(Fraction(float(M.bf16_to_float(qb))) * Fraction(float(s)))
+        acc = M.frac_fmt(M.rn32(qt * Fraction(float(M.bf16_to_float(kb))) + acc), "e4m11")
+    return acc
 
 
 def _inputs(d, N, seed, gain=1.0, kind="gauss"):
@@ -127,3 +138,24 @@ def test_visibility_conventions():
     # GQA: both query heads read kv head 0
     y1 = O.logits8(qb[:, 1:2].copy(), kb, 1, 0, 0, 32)
     assert np.array_equal(y1[0, 0], yc[0, 1])
+
+
+@pytest.mark.parametrize("d,seed,gain", [(8, 21, 1.0), (64, 22, 1.0), (128, 23, 4.0), (128, 24, 30.0)])
+def test_y16_step_vs_fraction_bruteforce(d, seed, gain):
+    """The per-FMA e4m11 reading (ORACLE_Y16_STEP) against exact rational
+    arithmetic, including inputs large enough to saturate at 511.875; and it
+    differs from the FP32-chain reading somewhere (the readings are distinct)."""
+    N = 12
+    q, k, _ = _inputs(d, N, seed, gain)
+    s = O.scale(d)
+    y = O.logits16_step(q, k, 0, 0, 0, N)
+    val = O.decode_fmt(O.E4M11, y.astype(np.uint32))[0, 0]
+    for j in range(0, N, 2):
+        for i in range(N):
+            ref = _frac_y16_step(q[0, 0, j], k[0, 0, i], s)
+            assert val[j, i] == float(ref), (j, i, val[j, i], float(ref))
+    if d >= 64:
+        chain = O.decode_fmt(O.E4M11, O.logits16(q, k, 0, 0, 0, N).astype(np.uint32))[0, 0]
+        assert np.any(chain != val)
+    if gain >= 30.0:
+        assert np.any(np.abs(val) == 511.875)
