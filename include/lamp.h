@@ -197,6 +197,33 @@ size_t lamp_attn_decode_workspace_size(int B, int Hq, int Hkv, int M, int N, int
  */
 int lamp_reserve(int device, size_t bytes);
 
+/*
+ * lamp_attn_fwd_noalloc -- lamp_attn_fwd for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, outputs and results as
+ * lamp_attn_fwd; it calls no hipMalloc, hipFree or other allocating routine.
+ *
+ * Its workspace is a fixed scratch of 256 MiB (LAMP_NOALLOC_SCRATCH_BYTES)
+ * that the library holds on every device it runs on from load until the
+ * process ends; its device address is taken once per device by lamp_init,
+ * which must have been called for the current device (LAMP_ERR_INIT
+ * otherwise).  A call whose workspace (lamp_attn_fwd_workspace_size) exceeds
+ * the scratch returns LAMP_ERR_WORKSPACE: e.g. the Qwen3-8B-shaped 8K prefill
+ * (176 MiB) fits, four such sequences do not.  extra->workspace must be NULL
+ * (LAMP_ERR_INVALID_ARG) and LAMP_CHECK_FINITE is refused
+ * (LAMP_ERR_UNSUPPORTED); statistics and observables are allowed; kernel
+ * timing (lamp_timing_enable) does not record these calls.  Every call on a
+ * device shares that device's scratch, which keeps the last call's contents:
+ * calls that overlap on one device (other streams, other threads) race.
+ */
+#define LAMP_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
+int lamp_attn_fwd_noalloc(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                          int B, int Hq, int Hkv, int N, int d,
+                          int causal, int window, int bq, int bk, int nk,
+                          double delta, double tau, unsigned flags,
+                          float *o, float *lse, uint8_t *mask,
+                          const struct lamp_fwd_extra *extra, void *stream);
+
 /* Variants of Algorithm 1 (flags of lamp_attn_fwd). */
 enum {
     /* The first stage disabled (the paper's appendix on first-stage

@@ -42,6 +42,7 @@ struct DeviceState {
     void *ws = nullptr;          // the library's workspace of this device (grow-only)
     size_t ws_bytes = 0;
     std::vector<void *> retired; // outgrown workspaces, freed by lamp_reserve / lamp_shutdown
+    void *scratch = nullptr;     // device address of this device's fixed scratch (lamp_attn_fwd_noalloc)
 };
 
 std::mutex g_mu;
@@ -83,6 +84,9 @@ int init_locked(int dev)
     HIP_TRY(hipMemcpy(&h_amb, amb, sizeof(unsigned), hipMemcpyDeviceToHost));
     HIP_TRY(hipFree(amb));
     if (h_amb != 0) return fail(LAMP_ERR_INIT, "%u exponential table entries could not be rounded with certainty", h_amb);
+    // this device's copy of the fixed scratch (the device is current here)
+    HIP_TRY(lamp::noalloc_scratch_address(&st->scratch));
+    if (!st->scratch) return fail(LAMP_ERR_INIT, "no device address for the fixed scratch");
     st->ready = true;
     return LAMP_OK;
 }
@@ -277,12 +281,12 @@ static size_t fwd_ws_bytes(int B, int Hq, int Hkv, int N, int bq, int bk, int nk
 }
 
 // The forward pass; sr: the 8-bit logits rounded stochastically with `seed`.
-// ws_fixed (with ws_fixed_bytes): a workspace that replaces both the caller's
-// and the library's (the allocation-free entry point).
+// fixed: the allocation-free entry point, whose workspace is the device's
+// fixed scratch (the tables must already exist; nothing is allocated).
 static int fwd_impl(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B, int Hq, int Hkv, int N, int d,
                     int causal, int window, int bq, int bk, int nk, double delta, double tau, unsigned flags, bool sr,
                     uint64_t seed, float *o, float *lse, uint8_t *mask, const lamp_fwd_extra *extra, void *stream,
-                    void *ws_fixed = nullptr, size_t ws_fixed_bytes = 0)
+                    bool fixed = false)
 {
     int rc = check_common(q, k, B, Hq, Hkv, N, d, causal, window);
     if (rc) return rc;
@@ -320,13 +324,14 @@ static int fwd_impl(const uint16_t *q, const uint16_t *k, const uint16_t *v, int
     if (check && capturing(s))
         return fail(LAMP_ERR_INVALID_ARG, "LAMP_CHECK_FINITE waits for the stream, which is being captured");
     lamp::FwdParams p{};
+    void *ws_fixed = nullptr;
     {
         std::lock_guard<std::mutex> lk(g_mu);
+        if (fixed && ((size_t)dev >= g_dev.size() || !g_dev[(size_t)dev].ready))
+            return fail(LAMP_ERR_INIT, "device %d is not initialised (call lamp_init first)", dev);
         DeviceState *st = state_of(dev);
-        if (ws_fixed) {
-            if (!st->ready)
-                return fail(LAMP_ERR_INIT, "the exponential tables of device %d are not built (call lamp_init first)",
-                            dev);
+        if (fixed) {
+            ws_fixed = st->scratch;
         } else {
             rc = init_locked(dev);
             if (rc) return rc;
@@ -339,10 +344,10 @@ static int fwd_impl(const uint16_t *q, const uint16_t *k, const uint16_t *v, int
     }
     const WsLayout lay = ws_layout(B, Hq, Hkv, Nq, Nk, d, true);
     void *base = nullptr;
-    if (ws_fixed) {
-        if (lay.total > ws_fixed_bytes)
-            return fail(LAMP_ERR_WORKSPACE, "the call needs %zu bytes of workspace, above the fixed %zu", lay.total,
-                        ws_fixed_bytes);
+    if (fixed) {
+        if (lay.total > lamp::NOALLOC_SCRATCH_BYTES)
+            return fail(LAMP_ERR_WORKSPACE, "the call needs %zu bytes of workspace, above the fixed scratch of %zu",
+                        lay.total, lamp::NOALLOC_SCRATCH_BYTES);
         base = ws_fixed;
     } else {
         rc = call_ws(dev, extra, lay.total, s, &base);
@@ -383,7 +388,7 @@ static int fwd_impl(const uint16_t *q, const uint16_t *k, const uint16_t *v, int
     const bool use_sr = sr && p.mode != lamp::MODE_ALL16;
     bool timed = false;
     TimedCall tc{};
-    {
+    if (!fixed) {   // the allocation-free entry point creates no events
         std::lock_guard<std::mutex> lk(g_tmu);
         timed = g_timing;
     }
@@ -430,6 +435,19 @@ int lamp_attn_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B
 {
     return fwd_impl(q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, flags, false, 0, o, lse, mask,
                     extra, stream);
+}
+
+int lamp_attn_fwd_noalloc(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B, int Hq, int Hkv, int N,
+                          int d, int causal, int window, int bq, int bk, int nk, double delta, double tau,
+                          unsigned flags, float *o, float *lse, uint8_t *mask, const lamp_fwd_extra *extra,
+                          void *stream)
+{
+    if (extra && extra->workspace)
+        return fail(LAMP_ERR_INVALID_ARG, "lamp_attn_fwd_noalloc takes no workspace (it uses its fixed scratch)");
+    if (flags & LAMP_CHECK_FINITE)
+        return fail(LAMP_ERR_UNSUPPORTED, "LAMP_CHECK_FINITE reads a flag back to the host; use lamp_attn_fwd");
+    return fwd_impl(q, k, v, B, Hq, Hkv, N, d, causal, window, bq, bk, nk, delta, tau, flags, false, 0, o, lse, mask,
+                    extra, stream, true);
 }
 
 int lamp_attn_fwd_sr(const uint16_t *q, const uint16_t *k, const uint16_t *v, int B, int Hq, int Hkv, int N, int d,

@@ -68,6 +68,11 @@ struct DecParams {
     double delta, tau;
 };
 
+// The fixed scratch of lamp_attn_fwd_noalloc (lamp_noalloc.hip): its size,
+// and its device address on the current device.
+constexpr size_t NOALLOC_SCRATCH_BYTES = LAMP_NOALLOC_SCRATCH_BYTES;
+hipError_t noalloc_scratch_address(void **ptr);
+
 hipError_t launch_decode(int D, const DecParams &p, hipStream_t s);
 hipError_t launch_prescale_q(const uint16_t *q, float *qt, int BH, int rows, int D, float scale, hipStream_t s);
 bool fwd_supported(int D, int BQ, int BK, int NK);

@@ -60,6 +60,8 @@ def lib():
         L.lamp_attn_fwd_sr.argtypes = ([P, P, P] + [i32] * 5 + [i32] * 5 + [f64, f64, ctypes.c_uint, ctypes.c_uint64]
                                        + [P, P, P, P, P])
         L.lamp_attn_fwd_sr.restype = i32
+        L.lamp_attn_fwd_noalloc.argtypes = [P, P, P] + [i32] * 5 + [i32] * 5 + [f64, f64, ctypes.c_uint, P, P, P, P, P]
+        L.lamp_attn_fwd_noalloc.restype = i32
         L.lamp_attn_logits8_sr.argtypes = [P, P] + [i32] * 9 + [ctypes.c_uint64, P, P]
         L.lamp_attn_logits8_sr.restype = i32
         L.lamp_attn_logits16.argtypes = [P, P] + [i32] * 9 + [P, P]
@@ -209,6 +211,32 @@ def attn_fwd(q, k, v, causal=True, window=0, bq=128, bk=16, nk=4, delta=2.0 ** -
             rc = lib().lamp_attn_fwd_sr(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(causal), int(window),
                                         bq, bk, nk, float(delta), float(tau), int(flags), int(sr_seed),
                                         _ptr(o), _ptr(lse), _ptr(mask), ep, _stream(dev))
+    del keep
+    _check(rc)
+    return o, lse, mask
+
+
+NOALLOC_SCRATCH_BYTES = 256 << 20
+
+
+def attn_fwd_noalloc(q, k, v, out, causal=True, window=0, bq=128, bk=16, nk=4, delta=2.0 ** -8, tau=0.5, flags=0,
+                     stats=None):
+    """attn_fwd through lamp_attn_fwd_noalloc: the library allocates nothing
+    (its workspace is the device's fixed scratch of NOALLOC_SCRATCH_BYTES;
+    init(device) must have been called).  `out` = (o, lse, mask) as for
+    attn_fwd is required, so that nothing is allocated here either."""
+    B, Hq, Hkv, N, d = _check_inputs(q, k, v)
+    dev = q.device
+    o, lse, mask = out
+    _check_out(o, "o", (B, Hq, N, d), torch.float32, dev)
+    _check_out(lse, "lse", (B, Hq, N), torch.float32, dev)
+    _check_out(mask, "mask", (B, Hq, -(-N // bq), -(-N // (bk * nk)) * nk), torch.uint8, dev)
+    extra, keep = _extra(stats=stats, device=dev, nk=nk)
+    ep = ctypes.byref(extra) if extra is not None else None
+    with torch.cuda.device(dev):
+        rc = lib().lamp_attn_fwd_noalloc(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(causal), int(window),
+                                         bq, bk, nk, float(delta), float(tau), int(flags), _ptr(o), _ptr(lse),
+                                         _ptr(mask), ep, _stream(dev))
     del keep
     _check(rc)
     return o, lse, mask
