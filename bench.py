@@ -23,8 +23,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 # MI355X peaks (public figures): 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz of
-# VALU issue (one fp32 FMA or conversion per lane per cycle).
+# VALU issue (one fp32 FMA or conversion per lane per cycle), the unit-count
+# model of one operation per multiply-add; and the published fp32 vector
+# peak, 157.3 TFLOP/s (packed FMAs: 2 flops on 2 values per lane and cycle).
 VALU_LANE_OPS = 256 * 4 * 16 * 2.4e9          # 39.3e12 lane-instructions / s
+FP32_PEAK_FLOPS = 157.3e12
 # Fewest VALU lane-instructions per emulated 8-bit multiply-add on gfx950: one
 # fp32 FMA, half a packed round-to-e4m3 and half a packed decode.
 OPS_PER_MAC8 = 2.0
@@ -39,7 +42,7 @@ SIM_FLAG = 4
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lamp_fwd16_kernel.qwen3-8b-prefill-8k.hbm_traffic.md")
 VALU_FILE = os.path.join(ROOT, "profiles", "lamp_fwd16_kernel.qwen3-8b-prefill-8k.valu_issue.md")
-KERNEL_SOURCES = ["lamp_fwd.hip", "lamp_fwd16.hip", "lamp_loops.h", "lamp_device.h", "lamp_kernels.h"]
+KERNEL_SOURCES = ["lamp_fwd.hip", "lamp_fwd16.hip", "lamp_loops.h", "lamp_device.h", "lamp_kernels.h", "lamp_stats.h"]
 
 
 def kernel_source_hash():
@@ -104,9 +107,11 @@ def visible_in_mask(w, mask):
     return int((rec * cnt[None]).sum())
 
 
-def cpu_baseline(w, tau, q, k, v, budget_s=15.0, seed=0, flags=0, sr_seed=None):
+def cpu_baseline(w, tau, q, k, v, budget_s=15.0, seed=0, flags=0, sr_seed=None, gpu=None):
     """The CPU oracle on a bounded, stated sample of query blocks (with
-    sr_seed: the stochastically rounded 8-bit accumulation)."""
+    sr_seed: the stochastically rounded 8-bit accumulation).  With gpu =
+    (o, lse, mask) numpy arrays of the same run, the sampled blocks are also
+    compared with them: returns (baseline, parity)."""
     from oracle import oracle as O
     rng = np.random.default_rng(seed)
     nqb = w.N // w.bq
@@ -116,14 +121,26 @@ def cpu_baseline(w, tau, q, k, v, budget_s=15.0, seed=0, flags=0, sr_seed=None):
     order = rng.permutation(w.B * w.Hq * nqb)
     picked, spent, flops = [], 0.0, 0.0
     first = True
+    par = {"blocks": 0, "mask_mismatch": 0, "o_err": 0.0, "lse_err": 0.0}
     while spent < budget_s and len(picked) < len(order):
         n = 1 if first else max(1, min(threads, int((budget_s - spent) / max(spent / len(picked), 1e-3))))
         batch = [int(x) for x in order[len(picked):len(picked) + n]]
         t0 = time.perf_counter()
-        O.fwd(qbits, kbits, vbits, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau, qblocks=batch,
-              nthreads=threads, flags=flags | (O.SR8 if sr_seed is not None else 0),
-              seed=sr_seed if sr_seed is not None else 0)
+        ro, rlse, rmask = O.fwd(qbits, kbits, vbits, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau,
+                                qblocks=batch, nthreads=threads, flags=flags | (O.SR8 if sr_seed is not None else 0),
+                                seed=sr_seed if sr_seed is not None else 0)
         spent += time.perf_counter() - t0
+        if gpu is not None:   # the sampled blocks of the GPU outputs of this run, outside the timing
+            go, glse, gmask = gpu
+            for f in batch:
+                bh, qb = divmod(f, nqb)
+                b, h = divmod(bh, w.Hq)
+                rows = slice(qb * w.bq, min((qb + 1) * w.bq, w.N))
+                ref_o = ro[b, h, rows]
+                par["blocks"] += 1
+                par["mask_mismatch"] += int((gmask[b, h, qb] != rmask[b, h, qb]).sum())
+                par["o_err"] = max(par["o_err"], float(np.abs(go[b, h, rows] - ref_o).max() / np.abs(ref_o).max()))
+                par["lse_err"] = max(par["lse_err"], float(np.abs(glse[b, h, rows] - rlse[b, h, rows]).max()))
         for f in batch:
             qb = f % nqb
             vis = 0
@@ -135,7 +152,7 @@ def cpu_baseline(w, tau, q, k, v, budget_s=15.0, seed=0, flags=0, sr_seed=None):
             flops += 4.0 * vis * w.d
         picked += batch
         first = False
-    return {
+    base = {
         "value": flops / spent / 1e12,
         "unit": "TFLOP/s",
         "cores": threads,
@@ -144,6 +161,11 @@ def cpu_baseline(w, tau, q, k, v, budget_s=15.0, seed=0, flags=0, sr_seed=None):
                   "effective FLOP counted over the sampled blocks' visible pairs" % (
                       len(picked), w.B * w.Hq * nqb, spent),
     }
+    if gpu is None:
+        return base
+    par["ok"] = par["mask_mismatch"] == 0 and par["o_err"] <= 2e-3 and par["lse_err"] <= 1e-4
+    par["bar"] = "masks bit-exact, O within 2e-3 of max|O| per block, lse within 1e-4"
+    return base, par
 
 
 HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, public figure
@@ -341,6 +363,13 @@ def run_fwd(args, w, tau, flags, host_inputs, dev_inputs, out, dev):
 
     st = lamp.mask_stats(mask, w.nk)
     mask_np = mask.cpu().numpy()
+    # the statistics words of one more call, outside the timed region
+    # (saturations: how often the accumulations leave the formats' range,
+    # which Sec. 3.3 assumes QK-Norm prevents)
+    stw = torch.zeros(lamp.stats_words(w.nk), dtype=torch.int64, device=dev)
+    lamp.attn_fwd(qd, kd, vd, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau, out=out, flags=flags,
+                  sr_seed=args.sr_seed, stats=stw)
+    stats = lamp.stats_dict(stw, w.nk)
     mac8 = 0 if tau == 0 else w.macs
     mac16 = visible_in_mask(w, mask_np) * w.d
     sim = bool(flags & SIM_FLAG)
@@ -359,8 +388,10 @@ def run_fwd(args, w, tau, flags, host_inputs, dev_inputs, out, dev):
                   % ("SIM profile" if sim else "hardware formats"),
     }
     alg_ops = (OPS_PER_MAC8_SIM if sim else OPS_PER_MAC8) * mac8 + OPS_PER_MAC16 * mac16
-    achieved = alg_ops / (kernel_ms * 1e-3) / 1e12
+    macs_per_s = (mac8 + mac16) / (kernel_ms * 1e-3)
+    achieved = macs_per_s / 1e12
     peak = VALU_LANE_OPS / 1e12
+    fmac_rate = 64.0 / (rates["fmac_f32"] * 1e-9) * simds   # measured lane-FMAs per second
     result = {
         "metric": "effective attention TFLOP/s (4*B*H*N^2*d, halved for causal), 1 GPU",
         "value": w.eff_flops / (ms * 1e-3) / 1e12,
@@ -384,12 +415,17 @@ def run_fwd(args, w, tau, flags, host_inputs, dev_inputs, out, dev):
         "visible_pair_tflops": 4.0 * w.macs / (ms * 1e-3) / 1e12,   # 4*d per visible (query, key) pair
         "recompute_fraction": st["recompute_fraction"],
         "tile_hist": st["tile_hist"],
+        "stats": stats,
         "roofline": {
             "bound": "alu",
             "achieved": achieved,
             "peak": peak,
-            "unit": "T VALU lane-ops/s",
+            "unit": "T multiply-adds/s (one VALU lane-op per 8-bit or 16-bit MAC)",
             "frac": achieved / peak,
+            "frac_2op_per_mac8": alg_ops / (kernel_ms * 1e-3) / VALU_LANE_OPS,
+            "frac_vs_fp32_published": 2.0 * macs_per_s / FP32_PEAK_FLOPS,
+            "frac_vs_measured_fmac_rate": macs_per_s / fmac_rate,
+            "measured_fmac_lane_ops_per_s": fmac_rate,
             "traffic": None if sr else measured_traffic(w.name, tau, flags),
             "kernel": ("lamp_fwd_kernel<%d,%d,%d,%d,SR>" % (w.d, w.bq, w.bk, w.nk)) if sr
                       else ("lamp_fwd16_kernel<%d,%d,%d,%s>" % (w.d, w.bq, _mode_of(tau), "true" if sim else "false"))
@@ -397,18 +433,19 @@ def run_fwd(args, w, tau, flags, host_inputs, dev_inputs, out, dev):
                       else ("lamp_fwd_kernel<%d,%d,%d,%d>" % (w.d, w.bq, w.bk, w.nk)),
             "kernel_ms": kernel_ms,
             "prepass_ms": pre_ms_sum / launches,
-            "ops_per_launch": alg_ops,
-            "ops_per_unit": ("%d per emulated 8-bit MAC, 1 per 16-bit recompute MAC"
-                             % (OPS_PER_MAC8_SIM if sim else OPS_PER_MAC8)),
-            "algorithmic_frac_one_op_per_mac": (mac8 + mac16) / (kernel_ms * 1e-3) / VALU_LANE_OPS,
+            "macs_per_launch": {"mac8": mac8, "mac16": mac16},
+            "ops_per_unit": ("1 per MAC for frac; frac_2op_per_mac8 charges %d per emulated 8-bit MAC "
+                             "(this emulation's cost) and 1 per 16-bit MAC" % (OPS_PER_MAC8_SIM if sim else OPS_PER_MAC8)),
             "valu_issue_frac_counters": None if sr else measured_valu_issue(w.name, tau, flags),
             "issue_floor": issue_floor,
         },
         "wall_s_timed_region": wall,
     }
     if not args.no_cpu:
-        result["cpu_baseline"] = cpu_baseline(w, tau, q, k, v, budget_s=args.cpu_budget, flags=flags,
-                                              sr_seed=args.sr_seed if sr else None)
+        gpu = (o.cpu().numpy(), lse.cpu().numpy(), mask_np)
+        result["cpu_baseline"], result["parity"] = cpu_baseline(w, tau, q, k, v, budget_s=args.cpu_budget,
+                                                                flags=flags, sr_seed=args.sr_seed if sr else None,
+                                                                gpu=gpu)
     print(json.dumps(result), flush=True)
 
 
