@@ -282,6 +282,9 @@ def main():
                          "a comma-separated list sweeps them (outer loop)")
     ap.add_argument("--sr-seed", type=int, default=None,
                     help="round the 8-bit accumulation stochastically with this seed (lamp_attn_fwd_sr)")
+    ap.add_argument("--phase-timer", action="store_true",
+                    help="load liblamp_phase.so (built by `python -m paper_2609_39361_amd.build --phase-timer`) and "
+                         "report the pipelined kernel's share of wave time per phase (instrumented: not a timing)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="before the timed steps, run one plain negating copy of this many MiB "
                          "(fp32 in, fp32 out) to calibrate the HBM byte counters")
@@ -291,6 +294,8 @@ def main():
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
+    if args.phase_timer:
+        os.environ["LAMP_LIBRARY"] = os.path.join(ROOT, "paper_2609_39361_amd", "liblamp_phase.so")
     import torch
     from paper_2609_39361_amd import lamp, workloads as W
 
@@ -345,6 +350,8 @@ def run_fwd(args, w, tau, flags, host_inputs, dev_inputs, out, dev):
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     torch.cuda.synchronize()
     lamp.timing_read()
+    if args.phase_timer:
+        lamp.phase_read(reset=True)
     lamp.timing_enable(True)
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -353,6 +360,13 @@ def run_fwd(args, w, tau, flags, host_inputs, dev_inputs, out, dev):
         ends[i].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    phases = None
+    if args.phase_timer:
+        cyc, waves = lamp.phase_read(reset=True)
+        tot = float(sum(cyc.values()))
+        phases = {"share_of_wave_time": {k: v / tot for k, v in cyc.items()}, "waves": waves,
+                  "note": "instrumented build (liblamp_phase.so): shares of the cycles each wave spends per phase; "
+                          "the kernel time of this run is not the benchmark's"}
     lamp.timing_enable(False)
     launches, fwd_ms_sum, pre_ms_sum = lamp.timing_read()
     if launches != args.steps:
@@ -441,6 +455,8 @@ def run_fwd(args, w, tau, flags, host_inputs, dev_inputs, out, dev):
         },
         "wall_s_timed_region": wall,
     }
+    if phases is not None:
+        result["phases"] = phases
     if not args.no_cpu:
         gpu = (o.cpu().numpy(), lse.cpu().numpy(), mask_np)
         result["cpu_baseline"], result["parity"] = cpu_baseline(w, tau, q, k, v, budget_s=args.cpu_budget,

@@ -389,6 +389,19 @@ int lamp_timing_read(int *launches, double *fwd_ms, double *prepass_ms);
  */
 int lamp_issue_rates(double *ns_per_simd, void *stream);
 
+/*
+ * lamp_phase_read -- the phase timer of the pipelined forward kernel, in a
+ * library built for measurement with -DLAMP_PHASE_TIMER (liblamp_phase.so;
+ * LAMP_ERR_UNSUPPORTED in the normal build).  cycles (HOST memory, 11
+ * entries) receives the shader-clock cycles all waves of the launches since
+ * the last reset spent in each phase of the tile loop -- [0] the fused
+ * 8-bit/16-bit pass, [1] code and maxima emission, [2] barrier B, [3] stage
+ * 1, [4] exponentials, [5] barrier E, [6] rescale and stage 2, [7] P.V and
+ * the next speculative set, [8] barrier I, [9] prologue and epilogue -- and
+ * [10] the number of waves.  reset != 0 clears the sums.  Synchronous.
+ */
+int lamp_phase_read(uint64_t *cycles, int reset);
+
 /* Build the device tables of `device` now (otherwise done by the first call). */
 int lamp_init(int device);
 

@@ -153,9 +153,14 @@ def _compile(src, work, flags, verbose):
     return r.returncode, obj, out
 
 
-def build(verbose=False, extra=()):
+PHASE_LIB = os.path.join(HERE, "liblamp_phase.so")
+
+
+def build(verbose=False, extra=(), out=LIB):
+    """Compile the library into `out` (default liblamp.so).  build_phase()
+    makes the measurement variant with the phase timer."""
     from concurrent.futures import ThreadPoolExecutor
-    tmp = LIB + ".tmp%d" % os.getpid()
+    tmp = out + ".tmp%d" % os.getpid()
     flags = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",
              "-ffp-contract=off", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              "-I", os.path.join(ROOT, "include"), "-I", CSRC,
@@ -167,9 +172,9 @@ def build(verbose=False, extra=()):
         failed = [out for rc, _, out in res if rc != 0]
         if failed:
             raise RuntimeError("hipcc failed:\n" + "\n".join(failed))
-        for _, _, out in res:
-            if verbose and out.strip():
-                print(out)
+        for _, _, msg in res:
+            if verbose and msg.strip():
+                print(msg)
         link = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC"] + [o for _, o, _ in res] + ["-o", tmp]
         if verbose:
             print(" ".join(link), flush=True)
@@ -191,10 +196,19 @@ def build(verbose=False, extra=()):
             os.remove(tmp)
             raise RuntimeError("DPP hazards in the generated code:\n" +
                                "\n".join("%s: %s  (%s)" % b for b in bad[:20]))
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
+
+
+def build_phase(verbose=False):
+    """liblamp_phase.so: the library with the pipelined kernel's phase timer
+    (-DLAMP_PHASE_TIMER), for measurement; load it with LAMP_LIBRARY."""
+    return build(verbose, extra=("-DLAMP_PHASE_TIMER",), out=PHASE_LIB)
 
 
 if __name__ == "__main__":
-    build(verbose=True)
+    if "--phase-timer" in sys.argv:
+        build_phase(verbose=True)
+    else:
+        build(verbose=True)
     sys.exit(0)

@@ -41,6 +41,53 @@
 
 namespace lamp {
 
+// Phase timer (a build with -DLAMP_PHASE_TIMER, for measurement only): every
+// wave adds the shader-clock cycles it spends in each phase of the tile loop
+// to phase_cycles[0..PHASE_N-1] (word PHASE_N counts the waves); read and
+// cleared by lamp_phase_read.  Phases: 0 fused pass, 1 code and maxima
+// emission, 2 barrier B, 3 stage 1, 4 exponentials, 5 barrier E, 6 rescale
+// and stage 2, 7 P.V and the next speculative set, 8 barrier I, 9 prologue
+// and epilogue.
+#ifdef LAMP_PHASE_TIMER
+__device__ unsigned long long phase_cycles[PHASE_N + 1];
+#define LAMP_PH_INIT                                                              \
+    __shared__ uint32_t ph_lds[4 * PHASE_N];                                      \
+    if (lane < PHASE_N) ph_lds[w * PHASE_N + lane] = 0u;                          \
+    uint32_t ph_t = (uint32_t)__builtin_readcyclecounter();
+#define LAMP_PH(i)                                                                \
+    do {                                                                          \
+        const uint32_t ph_n = (uint32_t)__builtin_readcyclecounter();             \
+        if (lane == 0) ph_lds[w * PHASE_N + (i)] += ph_n - ph_t;                  \
+        ph_t = ph_n;                                                              \
+    } while (0)
+#define LAMP_PH_FLUSH                                                             \
+    do {                                                                          \
+        LAMP_PH(9);                                                               \
+        if (lane < PHASE_N) atomicAdd(&phase_cycles[lane], (unsigned long long)ph_lds[w * PHASE_N + lane]); \
+        if (lane == PHASE_N) atomicAdd(&phase_cycles[PHASE_N], 1ull);             \
+    } while (0)
+#else
+#define LAMP_PH_INIT
+#define LAMP_PH(i) ((void)0)
+#define LAMP_PH_FLUSH ((void)0)
+#endif
+
+hipError_t phase_read(unsigned long long *host, bool reset)
+{
+#ifdef LAMP_PHASE_TIMER
+    hipError_t e = hipMemcpyFromSymbol(host, HIP_SYMBOL(phase_cycles), sizeof(phase_cycles));
+    if (e == hipSuccess && reset) {
+        static const unsigned long long zero[PHASE_N + 1] = {};
+        e = hipMemcpyToSymbol(HIP_SYMBOL(phase_cycles), zero, sizeof(phase_cycles));
+    }
+    return e;
+#else
+    (void)host;
+    (void)reset;
+    return hipErrorNotSupported;
+#endif
+}
+
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -176,6 +223,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
 
     const int tid = threadIdx.x;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;   // w is wave-uniform
+    LAMP_PH_INIT
     const int nqb = p.Nq / BQ;   // query blocks per head (the last may be partial)
     // Block order.  Workgroups are handed to the 8 XCDs round-robin (block i to
     // XCD i mod 8), each XCD with its own L2.  When the B*Hkv key/value heads
@@ -579,6 +627,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                 default: run(integral_constant<int, 16>(), F_()); break;
                 }
             }
+            LAMP_PH(0);
             if (has_next && mode != MODE_ALL16) emit8(t + 1, a8, emu, sat8);
             // 16-bit column maxima over this wave's 4 keys of every member of F0
             int *cmi = cmi_of(t);
@@ -603,7 +652,9 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                 }
             }
         }
+        LAMP_PH(1);
         __syncthreads();   // B: codes, m8 of the next tile and the 16-bit maxima are complete
+        LAMP_PH(2);
 
         // ---- C. running maximum mu_hat and stage 1 of tile t
         float muh[QPL];
@@ -738,6 +789,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
         }
 
 
+        LAMP_PH(3);
         // ---- D. exponentials of tile t against mu_hat
         {
             // the 16-bit maxima buffer of tile t+1 was last read in tile t-1
@@ -934,7 +986,9 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                 spf[w * BQ + row[s]] = spF[s];
             }
         }
+        LAMP_PH(4);
         __syncthreads();   // E
+        LAMP_PH(5);
 
         // ---- lambda_hat, omega_hat, stage 2
         double S[QPL], lam[QPL], omh[QPL];
@@ -1135,6 +1189,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
             }
         }
 
+        LAMP_PH(6);
         // ---- G. state update; O^T <- O^T diag(lambda_hat) + V^T E; next F0
 #pragma unroll
         for (int s = 0; s < QPL; ++s) {
@@ -1224,7 +1279,9 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
         F0 = has_next ? f0_of(t + 1, act_next) : 0u;
         if (mode == MODE_LAMP && !stage1_off && has_next) own_threat(t + 1);
         act = act_next;
+        LAMP_PH(7);
         __syncthreads();   // I: this tile's code buffer is rewritten by the pass of tile t+1
+        LAMP_PH(8);
     }
 
     // ---- epilogue: O / omega, lse = mu + ln(omega), mask bytes of skipped tiles
@@ -1258,6 +1315,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                 for (int th = 0; th < NK; ++th) mrow[tt * NK + th] = PREC_INACTIVE;
     }
     if (p.stats) flush_stats<NK>(p.stats, stl, (uint32_t)(p.Nk / BK), tid);
+    LAMP_PH_FLUSH;
 }
 
 // ------------------------------------------------------------------ launcher

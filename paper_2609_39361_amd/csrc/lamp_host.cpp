@@ -599,6 +599,18 @@ int lamp_issue_rates(double *ns_per_simd, void *stream)
     return LAMP_OK;
 }
 
+int lamp_phase_read(uint64_t *cycles, int reset)
+{
+    if (!cycles) return fail(LAMP_ERR_INVALID_ARG, "null pointer");
+    unsigned long long h[lamp::PHASE_N + 1];
+    const hipError_t e = lamp::phase_read(h, reset != 0);
+    if (e == hipErrorNotSupported)
+        return fail(LAMP_ERR_UNSUPPORTED, "this library was built without the phase timer (LAMP_PHASE_TIMER)");
+    if (e != hipSuccess) return fail(LAMP_ERR_HIP, "lamp_phase_read: %s", hipGetErrorString(e));
+    for (int i = 0; i <= lamp::PHASE_N; ++i) cycles[i] = h[i];
+    return LAMP_OK;
+}
+
 int lamp_timing_enable(int on)
 {
     std::lock_guard<std::mutex> lk(g_tmu);

@@ -73,6 +73,11 @@ struct DecParams {
 constexpr size_t NOALLOC_SCRATCH_BYTES = LAMP_NOALLOC_SCRATCH_BYTES;
 hipError_t noalloc_scratch_address(void **ptr);
 
+// Phase timer of the pipelined kernel (a -DLAMP_PHASE_TIMER build): PHASE_N
+// cycle sums and the number of waves; hipErrorNotSupported otherwise.
+constexpr int PHASE_N = 10;
+hipError_t phase_read(unsigned long long *host, bool reset);
+
 hipError_t launch_decode(int D, const DecParams &p, hipStream_t s);
 hipError_t launch_prescale_q(const uint16_t *q, float *qt, int BH, int rows, int D, float scale, hipStream_t s);
 bool fwd_supported(int D, int BQ, int BK, int NK);

@@ -51,6 +51,69 @@ __device__ __forceinline__ void emu8_words(uint32_t &a, uint32_t &b, float kv, f
         : "v248", "v249", "v250", "v251");
 }
 
+// One channel of all eight code words of both query rows (16 keys) in a
+// single statement: the body of emu8_words for word pairs 0..7.  One
+// statement per channel keeps the compiler from placing a wait state between
+// the word pairs, which it does after every separate statement.
+#define LAMP_E8W(A, B, K0, K1)                                                          \
+    "v_cvt_pk_f32_fp8 v[248:249], " A "\n\t"                                           \
+    "v_cvt_pk_f32_fp8 v[250:251], " B "\n\t"                                           \
+    "v_fmac_f32_dpp v248, %16, %17 row_newbcast:" #K0 " row_mask:0xf bank_mask:0xf\n\t" \
+    "v_fmac_f32_dpp v249, %16, %17 row_newbcast:" #K1 " row_mask:0xf bank_mask:0xf\n\t" \
+    "v_fmac_f32_dpp v250, %16, %18 row_newbcast:" #K0 " row_mask:0xf bank_mask:0xf\n\t" \
+    "v_fmac_f32_dpp v251, %16, %18 row_newbcast:" #K1 " row_mask:0xf bank_mask:0xf\n\t" \
+    "v_cvt_pk_fp8_f32 " A ", v248, v249\n\t"                                            \
+    "v_cvt_pk_fp8_f32 " B ", v250, v251\n\t"
+
+__device__ __forceinline__ void emu8_words8(uint32_t (&a)[8], uint32_t (&b)[8], float kv, float qa, float qb)
+{
+    asm(LAMP_E8W("%0", "%8", 0, 1) LAMP_E8W("%1", "%9", 2, 3) LAMP_E8W("%2", "%10", 4, 5)
+        LAMP_E8W("%3", "%11", 6, 7) LAMP_E8W("%4", "%12", 8, 9) LAMP_E8W("%5", "%13", 10, 11)
+        LAMP_E8W("%6", "%14", 12, 13) LAMP_E8W("%7", "%15", 14, 15)
+        : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(a[4]), "+v"(a[5]), "+v"(a[6]), "+v"(a[7]),
+          "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]), "+v"(b[4]), "+v"(b[5]), "+v"(b[6]), "+v"(b[7])
+        : "v"(kv), "v"(qa), "v"(qb)
+        : "v248", "v249", "v250", "v251");
+}
+#undef LAMP_E8W
+
+// One channel of the 16-bit accumulation of one query row for NKEY keys in
+// a single statement: acc[i] += bcast_i(kv) * q, i = 0..NKEY-1.
+#define LAMP_F16(I, ACC) "v_fmac_f32_dpp " ACC ", %[k], %[q] row_newbcast:" #I " row_mask:0xf bank_mask:0xf\n\t"
+template <int NKEY>
+__device__ __forceinline__ void fmac16_row(float (&acc)[NKEY], float kv, float q)
+{
+    static_assert(NKEY == 4 || NKEY == 8 || NKEY == 12 || NKEY == 16, "4, 8, 12 or 16 keys");
+    if constexpr (NKEY == 4) {
+        asm(LAMP_F16(0, "%0") LAMP_F16(1, "%1") LAMP_F16(2, "%2") LAMP_F16(3, "%3")
+            : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3])
+            : [k] "v"(kv), [q] "v"(q));
+    } else if constexpr (NKEY == 8) {
+        asm(LAMP_F16(0, "%0") LAMP_F16(1, "%1") LAMP_F16(2, "%2") LAMP_F16(3, "%3")
+            LAMP_F16(4, "%4") LAMP_F16(5, "%5") LAMP_F16(6, "%6") LAMP_F16(7, "%7")
+            : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3]), "+v"(acc[4]), "+v"(acc[5]), "+v"(acc[6]),
+              "+v"(acc[7])
+            : [k] "v"(kv), [q] "v"(q));
+    } else if constexpr (NKEY == 12) {
+        asm(LAMP_F16(0, "%0") LAMP_F16(1, "%1") LAMP_F16(2, "%2") LAMP_F16(3, "%3")
+            LAMP_F16(4, "%4") LAMP_F16(5, "%5") LAMP_F16(6, "%6") LAMP_F16(7, "%7")
+            LAMP_F16(8, "%8") LAMP_F16(9, "%9") LAMP_F16(10, "%10") LAMP_F16(11, "%11")
+            : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3]), "+v"(acc[4]), "+v"(acc[5]), "+v"(acc[6]),
+              "+v"(acc[7]), "+v"(acc[8]), "+v"(acc[9]), "+v"(acc[10]), "+v"(acc[11])
+            : [k] "v"(kv), [q] "v"(q));
+    } else {
+        asm(LAMP_F16(0, "%0") LAMP_F16(1, "%1") LAMP_F16(2, "%2") LAMP_F16(3, "%3")
+            LAMP_F16(4, "%4") LAMP_F16(5, "%5") LAMP_F16(6, "%6") LAMP_F16(7, "%7")
+            LAMP_F16(8, "%8") LAMP_F16(9, "%9") LAMP_F16(10, "%10") LAMP_F16(11, "%11")
+            LAMP_F16(12, "%12") LAMP_F16(13, "%13") LAMP_F16(14, "%14") LAMP_F16(15, "%15")
+            : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3]), "+v"(acc[4]), "+v"(acc[5]), "+v"(acc[6]),
+              "+v"(acc[7]), "+v"(acc[8]), "+v"(acc[9]), "+v"(acc[10]), "+v"(acc[11]), "+v"(acc[12]),
+              "+v"(acc[13]), "+v"(acc[14]), "+v"(acc[15])
+            : [k] "v"(kv), [q] "v"(q));
+    }
+}
+#undef LAMP_F16
+
 // Where the loops find the fp32 queries and keys.  Row layout ([row][D]): the
 // 4-channel group g of a row is at offset 4g and consecutive keys are D apart.
 // Grouped layout (the pipelined kernel): queries in blocks of 64 rows and keys
@@ -137,7 +200,9 @@ template <int QPL, bool SAT, bool WORDS, int... P>
 __device__ __forceinline__ void emu8_channel(float kv, const float (&q)[QPL], uint32_t (&acc)[QPL][8],
                                              std::integer_sequence<int, P...>)
 {
-    if constexpr (!SAT && WORDS && QPL == 2)
+    if constexpr (!SAT && WORDS && QPL == 2 && sizeof...(P) == 8)
+        emu8_words8(acc[0], acc[1], kv, q[0], q[1]);
+    else if constexpr (!SAT && WORDS && QPL == 2)
         (emu8_words<2 * P, 2 * P + 1, 2 * P, 2 * P + 1>(acc[0][P], acc[1][P], kv, q[0], q[1]), ...);
     else (emu8_pair<QPL, SAT, P>(kv, q, acc), ...);
 }
@@ -442,7 +507,7 @@ __device__ __forceinline__ void rec16_channel(float kv, const float (&q)[QPL], f
                                               std::integer_sequence<int, I...>)
 {
 #pragma unroll
-    for (int s = 0; s < QPL; ++s) ((acc[s][I] = fmac_bc<I>(acc[s][I], kv, q[s])), ...);
+    for (int s = 0; s < QPL; ++s) fmac16_row<NKEY>(acc[s], kv, q[s]);
 }
 
 // Y16 of NKEY keys (NKEY in {4, 8, 12, 16}) for QPL query rows: the FP32 FMA

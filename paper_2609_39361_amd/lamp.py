@@ -12,7 +12,8 @@ import os
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "liblamp.so")
+# LAMP_LIBRARY may name the measurement build liblamp_phase.so (phase timer)
+LIB_PATH = os.environ.get("LAMP_LIBRARY") or os.path.join(HERE, "liblamp.so")
 
 LAMP_OK = 0
 LAMP_ERR_NONFINITE_INPUT = 5
@@ -92,6 +93,8 @@ def lib():
         L.lamp_get_exp16_parts.restype = i32
         L.lamp_issue_rates.argtypes = [P, P]
         L.lamp_issue_rates.restype = i32
+        L.lamp_phase_read.argtypes = [P, i32]
+        L.lamp_phase_read.restype = i32
         L.lamp_timing_enable.argtypes = [i32]
         L.lamp_timing_enable.restype = i32
         L.lamp_timing_read.argtypes = [P, P, P]
@@ -428,6 +431,19 @@ def timing_read():
     n, tf, tp = ctypes.c_int(0), ctypes.c_double(0.0), ctypes.c_double(0.0)
     _check(lib().lamp_timing_read(ctypes.byref(n), ctypes.byref(tf), ctypes.byref(tp)))
     return n.value, tf.value, tp.value
+
+
+PHASE_NAMES = ("fused_pass", "emission", "barrier_B", "stage1", "exponentials", "barrier_E", "rescale_stage2",
+               "pv_next_F0", "barrier_I", "prologue_epilogue")
+
+
+def phase_read(reset=True):
+    """Cycle sums per phase of the pipelined kernel and the wave count (a
+    library built with the phase timer only; LampError otherwise)."""
+    h = (ctypes.c_uint64 * (len(PHASE_NAMES) + 1))()
+    _check(lib().lamp_phase_read(h, 1 if reset else 0))
+    v = list(h)
+    return dict(zip(PHASE_NAMES, v[:-1])), v[-1]
 
 
 ISSUE_RATE_KINDS = ("fmac_f32", "fmac_f32_dpp", "cvt_pk_f32_fp8", "cvt_pk_fp8_f32", "emulated_step",
