@@ -252,7 +252,16 @@ enum {
      * forward kernel if one is found.  The call then waits for its prepass on
      * `stream` (it is synchronous), and refuses a stream being captured into a
      * graph (LAMP_ERR_INVALID_ARG).  Applies in every mode. */
-    LAMP_CHECK_FINITE = 8
+    LAMP_CHECK_FINITE = 8,
+    /* The compact register layout of Sec. 3.3 ("Register layout") as the
+     * kernel's schedule: 8-bit accumulators four per 32-bit register, room
+     * for one 16-bit sub-block in the fused 8-bit pass, and a sequential
+     * 16-bit pass for "disruptive" tiles where two or more sub-blocks are
+     * flagged.  Results are bit-identical to the default (safe) layout.
+     * Applies to the pipelined kernel (b_k = 16, N_k = 4, d >= 128) at
+     * b_q = 128 in the threshold mode with the formats of Sec. 3.3; the flag
+     * has no effect elsewhere. */
+    LAMP_COMPACT = 16
 };
 
 /*

@@ -69,7 +69,8 @@ struct Cfg {
     static constexpr size_t OFF_CO = OFF_SP + (size_t)2 * NW * BQ * 8;   // f64 [NK][BQ]
     static constexpr size_t OFF_ED = OFF_CO + (size_t)NK * BQ * 8;       // f64 [EXPDOC_NK]
     static constexpr size_t OFF_ST = OFF_ED + (size_t)EXPDOC_NK * 8;     // u32 [ST_N] statistics
-    static constexpr size_t LDS = OFF_ST + (size_t)ST_N * 4;
+    static constexpr size_t OFF_PD = OFF_ST + (size_t)ST_N * 4;          // f64 [NW][BQ] pending rescale factors
+    static constexpr size_t LDS = OFF_PD + (size_t)NW * BQ * 8;
     static_assert(BQ == 64 || BQ == 128, "64 or 128 query rows per block");
     static_assert(BK % 16 == 0 && NK <= 4 && NK % NW == 0, "sub-blocks of 16-key chunks, at most 4 per tile");
     static_assert(CPW % 32 == 0, "whole 32-channel tiles per wave");
@@ -102,6 +103,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
     double *cst_lds = reinterpret_cast<double *>(smem + C::OFF_CO);    // [NK][BQ] stage-2 costs
     double *edk = reinterpret_cast<double *>(smem + C::OFF_ED);        // exp_doc constants
     uint32_t *stl = reinterpret_cast<uint32_t *>(smem + C::OFF_ST);    // [ST_N] statistics (p.stats)
+    double *pend = reinterpret_cast<double *>(smem + C::OFF_PD);        // [NW][BQ] pending factors (step 5)
 
     const int tid = threadIdx.x;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;   // w is wave-uniform
@@ -141,6 +143,7 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
     for (int i = tid; i < 256; i += 64 * NW) lut[i] = p.lut8e[i];
     if (tid < EXPDOC_NK) edk[tid] = EXPDOC_K[tid];
     if (tid < ST_N) stl[tid] = 0u;
+    for (int i = tid; i < NW * BQ; i += 64 * NW) pend[i] = 1.0;
     // logit observables (tests): this query block is observed (uniform)
     const bool dbg_blk = qb >= p.dbg_qb0 && qb < p.dbg_qb0 + p.dbg_nqb;
     const bool dbg8 = OBS && p.dbg_y8 != nullptr && dbg_blk, dbg16 = OBS && p.dbg_y16 != nullptr && dbg_blk;
@@ -804,11 +807,26 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
         load_v(0, va);
         {
             // lambda_hat of row 32g + l32 lives in lane (32g + l32) % 64, slot (32g + l32) / 64
+            // A row to which the tile added no mass (S = 0: every exponential
+            // underflowed against a maximum that overshoots) keeps O and omega
+            // in the same ratio, but lambda_hat can lie below fp32's range
+            // while omega, in fp64, stays tiny: O would underflow to 0 and
+            // 0 / omega give NaN.  Such factors are held in pend (fp64) and
+            // applied with the next tile that adds mass, or at the end.  Each
+            // wave keeps its own copy of the rows' factors in LDS.
             float lamf[QPL];
             bool scale = false;
 #pragma unroll
             for (int s = 0; s < QPL; ++s) {
-                lamf[s] = (float)lam[s];
+                double *pd = pend + w * BQ + row[s];
+                const double pv = *pd;
+                if (S[s] > 0.0) {
+                    lamf[s] = (float)(lam[s] * pv);
+                    if (pv != 1.0) *pd = 1.0;
+                } else {
+                    lamf[s] = 1.0f;
+                    *pd = pv * lam[s];
+                }
                 scale |= lamf[s] != 1.0f;
             }
             if (wave_any(scale)) {
@@ -837,7 +855,8 @@ __global__ __launch_bounds__(64 * (NK < D / 32 ? NK : D / 32), LAMP_MIN_WAVES) v
 #pragma unroll
         for (int g = 0; g < QG; ++g) {
             const double og = __shfl(om[g / 2 < QPL ? g / 2 : 0], ((g & 1) << 5) + l32, 64);
-            const float inv = (float)(1.0 / og);
+            const double pg = pend[w * BQ + g * 32 + l32];
+            const float inv = (float)(pg / og);   // pg = 1 unless the last tiles added no mass
             const int jq = q0 + g * 32 + l32;
             if (jq >= p.N) continue;   // beyond N in a partial last block
             float *orow = p.o + (((size_t)b * p.Hq + h) * p.N + jq) * D + w * CPW;

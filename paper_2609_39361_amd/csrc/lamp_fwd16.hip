@@ -118,7 +118,8 @@ struct Cfg16 {
     static constexpr size_t OFF_ED = OFF_SP + (size_t)2 * NW * BQ * 8;  // f64 [EXPDOC_NK]
     static constexpr size_t OFF_TS = OFF_ED + (size_t)EXPDOC_NK * 8;    // i32 [2][NK] sub-block threats
     static constexpr size_t OFF_ST = OFF_TS + (size_t)2 * NK * 4;       // u32 [ST_N] statistics
-    static constexpr size_t LDS = OFF_ST + (size_t)ST_N * 4;
+    static constexpr size_t OFF_PD = OFF_ST + (size_t)ST_N * 4;         // f64 [NW][BQ] pending rescale factors
+    static constexpr size_t LDS = OFF_PD + (size_t)NW * BQ * 8;
     static_assert(BQ == 64 || BQ == 128, "64 or 128 query rows per block");
     static_assert(CPW % 32 == 0, "whole 32-channel tiles per wave");
 };
@@ -199,7 +200,13 @@ __device__ __forceinline__ int wave_max_i32(int v)
 // OBS: the instantiation that also writes the logit observables (p.dbg_y8,
 // p.dbg_y16); the same code otherwise, kept apart so that the stores do not
 // change the register allocation of the instantiations that do not.
-template <int D, int BQ, int MODE, bool SIMP, bool OBS>
+// CMP: the compact register layout (Sec. 3.3, "Register layout"): the fused
+// pass keeps the 8-bit codes four per register and computes the 16-bit logits
+// of at most one speculative sub-block; when two or more are flagged (a
+// "disruptive" tile) the others follow in a sequential 16-bit pass once the
+// 8-bit codes are stored.  A schedule only: the results are those of the safe
+// layout.
+template <int D, int BQ, int MODE, bool SIMP, bool OBS, bool CMP>
 __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdParams p)
 {
     using C = Cfg16<D, BQ>;
@@ -220,6 +227,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     double *edk = reinterpret_cast<double *>(smem + C::OFF_ED);         // exp_doc constants
     int *tsl = reinterpret_cast<int *>(smem + C::OFF_TS);               // [2][NK] threats of a tile
     uint32_t *stl = reinterpret_cast<uint32_t *>(smem + C::OFF_ST);    // [ST_N] statistics (p.stats)
+    double *pend = reinterpret_cast<double *>(smem + C::OFF_PD);        // [NW][BQ] pending factors (G below)
 
     const int tid = threadIdx.x;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;   // w is wave-uniform
@@ -285,6 +293,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     if (tid < EXPDOC_NK) edk[tid] = EXPDOC_K[tid];
     for (int i = tid; i < 2 * NK * BQ; i += 256) cmi2[i] = INT_MIN;
     if (tid < ST_N) stl[tid] = 0u;
+    for (int i = tid; i < NW * BQ; i += 256) pend[i] = 1.0;
     // logit observables (tests): this query block is observed (uniform)
     const bool dbg_blk = qb >= p.dbg_qb0 && qb < p.dbg_qb0 + p.dbg_nqb;
     const bool dbg8 = OBS && !SIMP && p.dbg_y8 != nullptr && dbg_blk;
@@ -584,7 +593,8 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
         // wave), 8-bit logits of this wave's sub-block of the next tile
         uint32_t y16r[QPL][4 * WPM];   // 16-bit logits of keys th*16 + w*4 + {0..3} of the g-th member of F0
         {
-            const int nf = __builtin_popcount(F0);
+            const int nf_all = __builtin_popcount(F0);
+            const int nf = CMP ? (nf_all < 1 ? nf_all : 1) : nf_all;   // members in the fused pass
             const int kk = nf ? (lane & 15) % (4 * nf) : 0;
             int thg = 0;
             if (nf) {
@@ -600,7 +610,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                 constexpr int NKEY = decltype(nkey_c)::value;
                 constexpr bool EMU = decltype(emu_c)::value;
                 uint32_t c[QPL][y16_words<SIMP>(NKEY)];
-                fused_pass<D, QPL, NKEY, EMU, SIMP, GrpLay>(qrow, k32e, krowr, a8, c, sat8);
+                fused_pass<D, QPL, NKEY, EMU, SIMP, GrpLay, CMP>(qrow, k32e, krowr, a8, c, sat8);
                 if constexpr (NKEY > 0)
 #pragma unroll
                     for (int s = 0; s < QPL; ++s)
@@ -629,6 +639,31 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
             }
             LAMP_PH(0);
             if (has_next && mode != MODE_ALL16) emit8(t + 1, a8, emu, sat8);
+            if constexpr (CMP) {
+                // a disruptive tile: the other members of F0 in a sequential
+                // 16-bit pass (4 keys of each per wave, as in the fused pass)
+                if (nf_all >= 2) {
+                    const int nr = nf_all - 1;
+                    const int kb = (lane & 15) % (4 * nr);
+                    uint32_t m = F0 & (F0 - 1u);   // without the member of the fused pass
+                    for (int g = 0; g < kb / 4; ++g) m &= m - 1;
+                    const float *krow = krow_of(k0 + __builtin_ctz(m) * BK + w * 4 + (kb & 3));
+                    auto seq = [&](auto nkey_c) {
+                        constexpr int NKEY = decltype(nkey_c)::value;
+                        uint32_t c[QPL][y16_words<SIMP>(NKEY)];
+                        rec16_keys<D, QPL, NKEY, SIMP, GrpLay>(qrow, krow, c);
+#pragma unroll
+                        for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                            for (int pp = 0; pp < y16_words<SIMP>(NKEY); ++pp) y16r[s][WPM + pp] = c[s][pp];
+                    };
+                    switch (nr) {
+                    case 1: seq(std::integral_constant<int, 4>()); break;
+                    case 2: seq(std::integral_constant<int, 8>()); break;
+                    default: seq(std::integral_constant<int, 12>()); break;
+                    }
+                }
+            }
             // 16-bit column maxima over this wave's 4 keys of every member of F0
             int *cmi = cmi_of(t);
             uint32_t m = F0;
@@ -1250,11 +1285,26 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
         load_v(0, va);
         {
             // lambda_hat of row 32g + l32 lives in lane (32g + l32) % 64, slot (32g + l32) / 64
+            // A row to which the tile added no mass (S = 0: every exponential
+            // underflowed against a maximum that overshoots) keeps O and omega
+            // in the same ratio, but lambda_hat can lie below fp32's range
+            // while omega, in fp64, stays tiny: O would underflow to 0 and
+            // 0 / omega give NaN.  Such factors are held in pend (fp64) and
+            // applied with the next tile that adds mass, or at the end.  Each
+            // wave keeps its own copy of the rows' factors in LDS.
             float lamf[QPL];
             bool scale = false;
 #pragma unroll
             for (int s = 0; s < QPL; ++s) {
-                lamf[s] = (float)lam[s];
+                double *pd = pend + w * BQ + row[s];
+                const double pv = *pd;
+                if (S[s] > 0.0) {
+                    lamf[s] = (float)(lam[s] * pv);
+                    if (pv != 1.0) *pd = 1.0;
+                } else {
+                    lamf[s] = 1.0f;
+                    *pd = pv * lam[s];
+                }
                 scale |= lamf[s] != 1.0f;
             }
             if (wave_any(scale)) {
@@ -1290,7 +1340,8 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
 #pragma unroll
         for (int g = 0; g < QG; ++g) {
             const double og = __shfl(om[g / 2 < QPL ? g / 2 : 0], ((g & 1) << 5) + l32, 64);
-            const float inv = (float)(1.0 / og);
+            const double pg = pend[w * BQ + g * 32 + l32];
+            const float inv = (float)(pg / og);   // pg = 1 unless the last tiles added no mass
             const int jq = q0 + g * 32 + l32;
             if (jq >= p.N) continue;   // beyond N in a partial last block
             float *orow = p.o + (((size_t)b * p.Hq + h) * p.N + jq) * D + w * CPW;
@@ -1319,11 +1370,11 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
 }
 
 // ------------------------------------------------------------------ launcher
-template <int D, int BQ, int MODE, bool SIMP, bool OBS>
+template <int D, int BQ, int MODE, bool SIMP, bool OBS, bool CMP = false>
 static hipError_t launch_fwd16_obs(const FwdParams &p, hipStream_t s)
 {
     using C = Cfg16<D, BQ>;
-    auto kern = lamp_fwd16_kernel<D, BQ, MODE, SIMP, OBS>;
+    auto kern = lamp_fwd16_kernel<D, BQ, MODE, SIMP, OBS, CMP>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
     if (e != hipSuccess) return e;
@@ -1335,8 +1386,14 @@ static hipError_t launch_fwd16_obs(const FwdParams &p, hipStream_t s)
 template <int D, int BQ, int MODE, bool SIMP>
 static hipError_t launch_fwd16_mode(const FwdParams &p, hipStream_t s)
 {
+    const bool obs = p.dbg_y8 || p.dbg_y16;
+    // the compact layout: threshold mode, hardware formats, 128-row blocks
+    if constexpr (MODE == MODE_LAMP && !SIMP && BQ == 128)
+        if (p.flags & LAMP_COMPACT)
+            return obs ? launch_fwd16_obs<D, BQ, MODE, SIMP, true, true>(p, s)
+                       : launch_fwd16_obs<D, BQ, MODE, SIMP, false, true>(p, s);
     if constexpr (!SIMP)
-        if (p.dbg_y8 || p.dbg_y16) return launch_fwd16_obs<D, BQ, MODE, SIMP, true>(p, s);
+        if (obs) return launch_fwd16_obs<D, BQ, MODE, SIMP, true>(p, s);
     return launch_fwd16_obs<D, BQ, MODE, SIMP, false>(p, s);
 }
 

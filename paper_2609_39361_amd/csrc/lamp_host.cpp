@@ -294,7 +294,7 @@ static int fwd_impl(const uint16_t *q, const uint16_t *k, const uint16_t *v, int
         return fail(LAMP_ERR_INVALID_ARG, "null pointer among v, o, lse, mask");
     if (!(delta >= 0.0) || std::isinf(delta)) return fail(LAMP_ERR_INVALID_ARG, "delta must be finite and >= 0");
     if (!(tau >= 0.0)) return fail(LAMP_ERR_INVALID_ARG, "tau must be >= 0 (or +inf)");
-    if (flags & ~(unsigned)(LAMP_STAGE1_OFF | LAMP_MU_TRUNC | LAMP_SIM_PROFILE | LAMP_CHECK_FINITE))
+    if (flags & ~(unsigned)(LAMP_STAGE1_OFF | LAMP_MU_TRUNC | LAMP_SIM_PROFILE | LAMP_CHECK_FINITE | LAMP_COMPACT))
         return fail(LAMP_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
     if (bq <= 0 || bk <= 0 || nk <= 0) return fail(LAMP_ERR_INVALID_ARG, "block sizes must be positive");
     if (!lamp::fwd_supported(d, bq, bk, nk))
@@ -383,6 +383,7 @@ static int fwd_impl(const uint16_t *q, const uint16_t *k, const uint16_t *v, int
     p.tau = tau;
     p.mode = std::isinf(tau) ? lamp::MODE_PURE8 : (tau == 0.0 ? lamp::MODE_ALL16 : lamp::MODE_LAMP);
     p.flags = p.mode == lamp::MODE_LAMP ? flags : (flags & (unsigned)LAMP_SIM_PROFILE);
+    if (sr) p.flags &= ~(unsigned)LAMP_COMPACT;   // a schedule of the pipelined kernel only
     p.seed = seed;
     // the all-16-bit mode computes no 8-bit logit: the rounding mode does not matter there
     const bool use_sr = sr && p.mode != lamp::MODE_ALL16;

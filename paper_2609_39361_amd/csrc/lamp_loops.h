@@ -77,6 +77,40 @@ __device__ __forceinline__ void emu8_words8(uint32_t (&a)[8], uint32_t (&b)[8], 
 }
 #undef LAMP_E8W
 
+// The compact register layout (Sec. 3.3, "Register layout": four 8-bit
+// accumulators per 32-bit register): one channel of both query rows' 16
+// codes held four per word -- keys 4w, 4w+1 in bits [15:0] of word w, keys
+// 4w+2, 4w+3 in bits [31:16] -- in a single statement.  The high halves are
+// decoded with an SDWA word select and written back with op_sel, so the
+// instructions are those of emu8_words8.
+#define LAMP_E8H(A, B, K0, K1, K2, K3)                                                  \
+    "v_cvt_pk_f32_fp8 v[248:249], " A "\n\t"                                           \
+    "v_cvt_pk_f32_fp8 v[250:251], " B "\n\t"                                           \
+    "v_fmac_f32_dpp v248, %8, %9 row_newbcast:" #K0 " row_mask:0xf bank_mask:0xf\n\t"   \
+    "v_fmac_f32_dpp v249, %8, %9 row_newbcast:" #K1 " row_mask:0xf bank_mask:0xf\n\t"   \
+    "v_fmac_f32_dpp v250, %8, %10 row_newbcast:" #K0 " row_mask:0xf bank_mask:0xf\n\t"  \
+    "v_fmac_f32_dpp v251, %8, %10 row_newbcast:" #K1 " row_mask:0xf bank_mask:0xf\n\t"  \
+    "v_cvt_pk_fp8_f32 " A ", v248, v249\n\t"                                            \
+    "v_cvt_pk_fp8_f32 " B ", v250, v251\n\t"                                            \
+    "v_cvt_pk_f32_fp8_sdwa v[248:249], " A " src0_sel:WORD_1\n\t"                       \
+    "v_cvt_pk_f32_fp8_sdwa v[250:251], " B " src0_sel:WORD_1\n\t"                       \
+    "v_fmac_f32_dpp v248, %8, %9 row_newbcast:" #K2 " row_mask:0xf bank_mask:0xf\n\t"   \
+    "v_fmac_f32_dpp v249, %8, %9 row_newbcast:" #K3 " row_mask:0xf bank_mask:0xf\n\t"   \
+    "v_fmac_f32_dpp v250, %8, %10 row_newbcast:" #K2 " row_mask:0xf bank_mask:0xf\n\t"  \
+    "v_fmac_f32_dpp v251, %8, %10 row_newbcast:" #K3 " row_mask:0xf bank_mask:0xf\n\t"  \
+    "v_cvt_pk_fp8_f32 " A ", v248, v249 op_sel:[0,0,1]\n\t"                             \
+    "v_cvt_pk_fp8_f32 " B ", v250, v251 op_sel:[0,0,1]\n\t"
+
+__device__ __forceinline__ void emu8_quads4(uint32_t (&a)[4], uint32_t (&b)[4], float kv, float qa, float qb)
+{
+    asm(LAMP_E8H("%0", "%4", 0, 1, 2, 3) LAMP_E8H("%1", "%5", 4, 5, 6, 7) LAMP_E8H("%2", "%6", 8, 9, 10, 11)
+        LAMP_E8H("%3", "%7", 12, 13, 14, 15)
+        : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3])
+        : "v"(kv), "v"(qa), "v"(qb)
+        : "v248", "v249", "v250", "v251");
+}
+#undef LAMP_E8H
+
 // One channel of the 16-bit accumulation of one query row for NKEY keys in
 // a single statement: acc[i] += bcast_i(kv) * q, i = 0..NKEY-1.
 #define LAMP_F16(I, ACC) "v_fmac_f32_dpp " ACC ", %[k], %[q] row_newbcast:" #I " row_mask:0xf bank_mask:0xf\n\t"
@@ -421,11 +455,17 @@ __device__ __forceinline__ void encode16(const float (&acc)[QPL][NKEY], uint32_t
 // The forward kernel uses it to run the 8-bit logits of the next key tile
 // together with the speculative 16-bit recompute of the current one.
 // sat receives the saturated keys of the 8-bit chunk as in emu8_chunk.
-template <int D, int QPL, int NKEY, bool EMU, bool SIMP, class LY = RowLay<D>, class QP>
+// CMP: the 8-bit codes live four per register during the pass (emu8_quads4;
+// two query rows per lane, the grouped layout); a8 receives them two per word
+// as always.
+template <int D, int QPL, int NKEY, bool EMU, bool SIMP, class LY = RowLay<D>, bool CMP = false, class QP>
 __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k32e, const float *krowr,
                                            uint32_t (&a8)[QPL][8], uint32_t (&c16)[QPL][y16_words<SIMP>(NKEY)],
                                            uint32_t (&sat)[QPL])
 {
+    static_assert(!CMP || (QPL == 2 && !SIMP && LY::WORDS), "compact words: two rows per lane, hardware formats");
+    constexpr bool QUADS = CMP && EMU;
+    uint32_t a8q[QPL][4];   // the compact words (QUADS)
     static_assert(EMU || NKEY > 0, "something to compute");
     static_assert(NKEY == 0 || NKEY == 4 || NKEY == 8 || NKEY == 12 || NKEY == 16, "0, 4, 8, 12 or 16 keys");
     static_assert(D % 8 == 0, "channels in pairs of 4-channel groups");
@@ -437,6 +477,8 @@ __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k
         sat[s] = 0u;
 #pragma unroll
         for (int p = 0; p < 8; ++p) a8[s][p] = 0u;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) a8q[s][p] = 0u;
 #pragma unroll
         for (int i = 0; i < NA; ++i) acc[s][i] = 0.0f;
 #pragma unroll
@@ -464,6 +506,8 @@ __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k
             for (int s = 0; s < QPL; ++s) q[s] = f4_at(q4[s], cc);
             if constexpr (EMU && SIMP)
                 emu8s_channel<QPL>(f4_at(ke, cc), q, e8, std::make_integer_sequence<int, 16>());
+            else if constexpr (QUADS)
+                emu8_quads4(a8q[0], a8q[QPL - 1], f4_at(ke, cc), q[0], q[QPL - 1]);
             else if constexpr (EMU)
                 emu8_channel<QPL, false, LY::WORDS>(f4_at(ke, cc), q, a8, std::make_integer_sequence<int, 8>());
             if constexpr (NKEY > 0)
@@ -488,6 +532,15 @@ __device__ __forceinline__ void fused_pass(const QP (&qrow)[QPL], const float *k
 #pragma unroll
             for (int p = 0; p < 8; ++p) a8[s][p] = pack_sim8(e8[s][2 * p], e8[s][2 * p + 1]);
     } else if constexpr (EMU) {
+        if constexpr (QUADS) {   // back to two codes per word
+#pragma unroll
+            for (int s = 0; s < QPL; ++s)
+#pragma unroll
+                for (int p = 0; p < 4; ++p) {
+                    a8[s][2 * p] = a8q[s][p] & 0xFFFFu;
+                    a8[s][2 * p + 1] = a8q[s][p] >> 16;
+                }
+        }
         uint32_t nan = 0;
 #pragma unroll
         for (int s = 0; s < QPL; ++s)

@@ -139,6 +139,7 @@ STAGE1_OFF = 1   # the first stage disabled: mu_hat from the 8-bit maxima, stage
 MU_TRUNC = 2     # 8-bit shifts against mu_hat truncated to e4m3 (SIM profile: to 3 mantissa bits)
 SIM_PROFILE = 4  # the SIM precision profile (FP32 range, 3 / 11 mantissa bits, no saturation)
 CHECK_FINITE = 8  # check q, k, v for NaN / infinity first (synchronous; LAMP_ERR_NONFINITE_INPUT)
+COMPACT = 16     # the compact register layout of Sec. 3.3 as the kernel's schedule (same results)
 
 
 def _check_out(t, name, shape, dtype, device):

@@ -445,3 +445,32 @@ def test_fwd_sim_config5_sampled(L, tau):
     err, mask = _compare_fwd(L, w, tau, qblocks=qbl, keep=True, flags=O.SIM)
     _say("config 5 SIM tau %s sampled: O err %.2e, mask %s (%.1f s)" % (
         tau, err, np.bincount(mask.ravel(), minlength=4), time.time() - t0))
+
+
+NO_MASS = [
+    W.small("nm_pipelined", N=256, d=128, Hq=1, Hkv=1, bq=128, bk=16, nk=4, causal=1, seed=313, extra={"gain": 8.0}),
+    W.small("nm_general", N=256, d=64, Hq=1, Hkv=1, bq=64, bk=64, nk=4, causal=0, seed=314, extra={"gain": 8.0}),
+    W.small("nm_general_d64_bk16", N=256, d=64, Hq=2, Hkv=1, bq=64, bk=16, nk=4, causal=1, seed=315,
+            extra={"gain": 8.0}),
+]
+
+
+@pytest.mark.parametrize("tau", [0.5, 2.0 ** -5])
+@pytest.mark.parametrize("w", NO_MASS, ids=[w.name for w in NO_MASS])
+def test_fwd_tiles_adding_no_mass(L, w, tau):
+    """First stage off on saturating inputs: the 8-bit maximum can overshoot a
+    row's 16-bit logits so far that a tile adds no mass (every exponential
+    underflows) while the rescale factor is below fp32's range.  O keeps its
+    ratio to omega (O finite wherever the oracle's is; NaN with lse = -inf
+    only for rows that never receive mass)."""
+    qd, kd, vd, qb, kb, vb = _inputs(w)
+    o, lse, mask = [t.cpu().numpy() for t in
+                    L.attn_fwd(qd, kd, vd, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau, flags=1)]
+    ro, rlse, rmask = O.fwd(qb, kb, vb, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, tau, flags=1)
+    assert np.array_equal(mask, rmask)
+    assert np.array_equal(np.isnan(o), np.isnan(ro)), "NaN rows differ"
+    assert np.array_equal(np.isneginf(lse), np.isneginf(rlse))
+    fin = ~np.isnan(ro)
+    assert np.abs(o[fin] - ro[fin]).max() <= O_TOL * np.abs(ro[fin]).max()
+    fl = np.isfinite(rlse)
+    assert np.abs(lse[fl] - rlse[fl]).max() <= LSE_TOL
