@@ -183,10 +183,10 @@ enum {
 #define LAMP_STATS_WORDS(nk) (LAMP_STAT_HIST + (nk) + 1)
 
 /* Bytes of workspace lamp_attn_fwd / lamp_attn_fwd_sr need for these sizes
- * (0 for invalid sizes; B = 0 or N = 0 needs none). */
+ * (0 for sizes or block sizes they refuse; B = 0 or N = 0 needs none). */
 size_t lamp_attn_fwd_workspace_size(int B, int Hq, int Hkv, int N, int d, int bq, int bk, int nk);
 
-/* Bytes of workspace lamp_attn_decode needs (0 for invalid sizes). */
+/* Bytes of workspace lamp_attn_decode needs (0 for sizes it refuses). */
 size_t lamp_attn_decode_workspace_size(int B, int Hq, int Hkv, int M, int N, int d);
 
 /*
@@ -283,7 +283,8 @@ enum {
  * no 8-bit logit and equals lamp_attn_fwd).
  *
  * Arguments, layouts, outputs, extra and workspace as lamp_attn_fwd; flags: 0,
- * LAMP_STAGE1_OFF, LAMP_MU_TRUNC and/or LAMP_CHECK_FINITE; LAMP_SIM_PROFILE gives
+ * LAMP_STAGE1_OFF, LAMP_MU_TRUNC and/or LAMP_CHECK_FINITE (LAMP_COMPACT is
+ * accepted and has no effect here); LAMP_SIM_PROFILE gives
  * LAMP_ERR_UNSUPPORTED.  Built for the configurations lamp_attn_fwd lists for
  * the formats of Sec. 3.3.  The generator costs some hundred VALU operations
  * per 8 multiply-adds: expect this pass to run far slower than
@@ -360,7 +361,8 @@ int lamp_attn_logits16(const uint16_t *q, const uint16_t *k,
 /*
  * lamp_attn_logits_sim -- the logits of the SIM profile (LAMP_SIM_PROFILE):
  * high = 0 the 8-bit recursion (FP32 FMA, then 3 mantissa bits, every step),
- * high = 1 the 16-bit one (FP32 FMA chain, then 11 mantissa bits once).
+ * high = 1 the 16-bit one (FP32 FMA chain, then 11 mantissa bits once); any
+ * other value is LAMP_ERR_INVALID_ARG.
  * Values y [B][Hq][nrows][N] fp32 (device); invisible entries hold a NaN.
  * d in {64, 128, 256}, N a multiple of 16, 0 <= row0, row0 + nrows <= N.
  */

@@ -129,7 +129,7 @@ struct WsLayout {
     size_t qt, k32, vt, total;
 };
 
-WsLayout ws_layout(int B, int Hq, int Hkv, int Nq, int Nk, int d, bool with_vt)
+WsLayout ws_layout(int B, int Hq, int Hkv, int64_t Nq, int64_t Nk, int d, bool with_vt)
 {
     const size_t nq = (size_t)B * Hq * Nq * d, nk = (size_t)B * Hkv * Nk * d;
     WsLayout l;
@@ -219,6 +219,13 @@ int check_common(const void *q, const void *k, int B, int Hq, int Hkv, int N, in
     return LAMP_OK;
 }
 
+// The sizes check_common accepts (d built, N and B*Hq*N within the limits):
+// the workspace sizes of these cannot overflow.
+bool sizes_built(int B, int Hq, int N, int d)
+{
+    return (d == 64 || d == 128 || d == 256) && N <= (1 << 20) && (size_t)B * Hq * (size_t)N <= (size_t)1 << 31;
+}
+
 } // namespace
 
 extern "C" {
@@ -276,7 +283,8 @@ void lamp_shutdown(void)
 static size_t fwd_ws_bytes(int B, int Hq, int Hkv, int N, int bq, int bk, int nk, int d)
 {
     // the workspace holds whole query blocks and whole key tiles (zero padded)
-    const int Nq = (N + bq - 1) / bq * bq, Nk = (N + bk * nk - 1) / (bk * nk) * (bk * nk);
+    const int64_t T = (int64_t)bk * nk;
+    const int64_t Nq = ((int64_t)N + bq - 1) / bq * bq, Nk = ((int64_t)N + T - 1) / T * T;
     return ws_layout(B, Hq, Hkv, Nq, Nk, d, true).total;
 }
 
@@ -463,6 +471,7 @@ size_t lamp_attn_fwd_workspace_size(int B, int Hq, int Hkv, int N, int d, int bq
 {
     if (B < 0 || Hq <= 0 || Hkv <= 0 || N < 0 || d <= 0 || bq <= 0 || bk <= 0 || nk <= 0) return 0;
     if (B == 0 || N == 0) return 0;
+    if (!sizes_built(B, Hq, N, d) || !lamp::fwd_supported(d, bq, bk, nk)) return 0;
     return fwd_ws_bytes(B, Hq, Hkv, N, bq, bk, nk, d);
 }
 
@@ -493,7 +502,7 @@ struct DecLayout {
 
 static DecLayout dec_layout(int B, int Hq, int M, int N, int d)
 {
-    const int Np = (N + 63) / 64 * 64, nch = (N + 511) / 512;   // key chunks of the P.V pass
+    const int64_t Np = ((int64_t)N + 63) / 64 * 64, nch = ((int64_t)N + 511) / 512;   // key chunks of the P.V pass
     const size_t nrows = (size_t)B * Hq * M;
     DecLayout l;
     l.qt = align256(nrows * d * 4);
@@ -509,6 +518,7 @@ size_t lamp_attn_decode_workspace_size(int B, int Hq, int Hkv, int M, int N, int
 {
     if (B < 0 || Hq <= 0 || Hkv <= 0 || M < 0 || M > N || d <= 0) return 0;
     if (B == 0 || M == 0) return 0;
+    if (!sizes_built(B, Hq, N, d)) return 0;
     return dec_layout(B, Hq, M, N, d).total;
 }
 
@@ -654,7 +664,7 @@ static int logits_common(const uint16_t *q, const uint16_t *k, int B, int Hq, in
     if (rc) return rc;
     if (!out) return fail(LAMP_ERR_INVALID_ARG, "null output pointer");
     if (B == 0 || N == 0 || N % 16) return fail(LAMP_ERR_UNSUPPORTED, "N=%d is not a positive multiple of 16 (B=%d)", N, B);
-    if (row0 < 0 || nrows <= 0 || row0 + nrows > N) return fail(LAMP_ERR_INVALID_ARG, "row range outside [0, N)");
+    if (row0 < 0 || nrows <= 0 || nrows > N - row0) return fail(LAMP_ERR_INVALID_ARG, "row range outside [0, N)");
     int dev = 0;
     rc = current_device(&dev);
     if (rc) return rc;
@@ -728,6 +738,7 @@ int lamp_attn_logits16(const uint16_t *q, const uint16_t *k, int B, int Hq, int 
 int lamp_attn_logits_sim(const uint16_t *q, const uint16_t *k, int B, int Hq, int Hkv, int N, int d, int causal,
                          int window, int row0, int nrows, int high, float *y, void *stream)
 {
+    if (high != 0 && high != 1) return fail(LAMP_ERR_INVALID_ARG, "high must be 0 or 1");
     lamp::LogitsParams p;
     Workspace w;
     int rc = logits_common(q, k, B, Hq, Hkv, N, d, causal, window, row0, nrows, y, &p, &w, stream);
@@ -735,7 +746,7 @@ int lamp_attn_logits_sim(const uint16_t *q, const uint16_t *k, int B, int Hq, in
     p.ysim = y;
     hipStream_t s = static_cast<hipStream_t>(stream);
     HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, N, N, d, scale_of(d), s));
-    HIP_TRY(lamp::launch_logits_sim(p, d, high != 0, s));
+    HIP_TRY(lamp::launch_logits_sim(p, d, high, s));
     return LAMP_OK;
 }
 

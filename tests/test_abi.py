@@ -141,7 +141,7 @@ def test_fwd_sr_rejects_bad_arguments_without_gpu():
     lib.lamp_last_error.restype = ctypes.c_char_p
     d = ctypes.c_void_p(16)
     args = (d, d, d, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5)
-    assert lib.lamp_attn_fwd_sr(*args, 16, 1, d, d, d, None, None) == 1
+    assert lib.lamp_attn_fwd_sr(*args, 32, 1, d, d, d, None, None) == 1
     assert lib.lamp_attn_fwd_sr(*args, 4, 1, d, d, d, None, None) == 2
     assert b"SIM" in lib.lamp_last_error()
     assert lib.lamp_attn_fwd_sr(d, d, d, 1, 2, 1, 256, 128, 1, 0, 128, 32, 4, 2 ** -8, 0.5, 0, 2 ** 64 - 1,
@@ -201,8 +201,8 @@ def test_extra_arguments_checked_without_gpu():
     e2.stats = 16
     assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 128, 1, 0, 64, 2 ** -8, 0.5, 0, d, d, d,
                                 ctypes.byref(e2), None) == 2
-    # unknown flag bits beyond LAMP_CHECK_FINITE
-    assert lib.lamp_attn_fwd(d, d, d, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 16, d, d, d,
+    # unknown flag bits beyond LAMP_COMPACT
+    assert lib.lamp_attn_fwd(d, d, d, 1, 2, 1, 256, 128, 1, 0, 128, 16, 4, 2 ** -8, 0.5, 32, d, d, d,
                              None, None) == 1
 
 
@@ -227,6 +227,12 @@ def test_workspace_sizes_without_gpu():
     assert lib.lamp_attn_fwd_workspace_size(1, 2, 1, 300, 128, -1, 16, 4) == 0
     assert lib.lamp_attn_decode_workspace_size(32, 32, 8, 1, 8192, 128) > 0
     assert lib.lamp_attn_decode_workspace_size(1, 4, 1, 5, 4, 128) == 0    # M > N
+    # sizes and block sizes the passes refuse need no workspace (and overflow nothing)
+    assert lib.lamp_attn_fwd_workspace_size(1, 2, 1, 300, 128, 2 ** 31 - 1, 2 ** 31 - 1, 2 ** 31 - 1) == 0
+    assert lib.lamp_attn_fwd_workspace_size(1, 2, 1, 300, 96, 128, 16, 4) == 0
+    assert lib.lamp_attn_fwd_workspace_size(1, 1, 1, (1 << 20) + 1, 128, 128, 16, 4) == 0
+    assert lib.lamp_attn_fwd_workspace_size(2 ** 31 - 1, 2 ** 31 - 1, 1, 1 << 20, 128, 128, 16, 4) == 0
+    assert lib.lamp_attn_decode_workspace_size(1, 4, 1, 1, 2 ** 31 - 1, 128) == 0
     lib.lamp_status_str.restype = ctypes.c_char_p
     lib.lamp_status_str.argtypes = [ctypes.c_int]
     assert lib.lamp_status_str(5) == b"non-finite input"
