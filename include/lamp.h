@@ -317,8 +317,9 @@ int lamp_attn_fwd_sr(const uint16_t *q, const uint16_t *k, const uint16_t *v,
  * recomputed by the look-ahead test -- every key at tau = 0 --, 2 recomputed
  * by the knapsack, 3 invisible).  Built: tk = 64, d in {64, 128, 256};
  * flags must be 0.  B = 0 or M = 0 returns LAMP_OK and writes nothing.  The
- * workspace (the pre-scaled queries, the 8-bit logit codes, the
- * exponentials, per-tile rescale factors and partial outputs:
+ * workspace (the pre-scaled queries, the 8-bit logit codes, the 16-bit
+ * logits of the recomputed keys, per-tile mu_hat and rescale factors, partial
+ * outputs:
  * lamp_attn_decode_workspace_size bytes) comes from extra->workspace or from
  * the library's per-device workspace, as for lamp_attn_fwd; extra->stats and
  * the dbg pointers must be NULL (LAMP_ERR_UNSUPPORTED).

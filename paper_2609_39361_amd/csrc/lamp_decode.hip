@@ -15,18 +15,22 @@
 //   3. omega, O and mu are updated (Sec. 2, online softmax).
 //
 // Four kernels:
-//   dec_logits8_kernel  the 8-bit logits of every (query row, key), which
-//                       depend on no decision: one thread per key, the 4 query
-//                       rows of a group accumulated together, queries read
-//                       from LDS (broadcast), keys staged through LDS from
-//                       coalesced loads of the bf16 cache (no fp32 copy);
+//   dec_logits_kernel   the logits of every (query row, key), which depend on
+//                       no decision, in 8 bits and in 16 bits (codes), and
+//                       the mask code of every key: one thread per key, the 4
+//                       query rows of a group accumulated together, queries
+//                       read from LDS (broadcast), keys staged through LDS
+//                       from coalesced loads of the bf16 cache (no fp32 copy);
 //   dec_lamp_kernel     the decisions, one wave per query row: lane i holds
 //                       key i of the tile; DPP reductions, a bitonic sort of
-//                       the costs and the sequential sum; it writes the
-//                       exponentials and per-tile rescale factors;
+//                       the costs and the sequential sum; runs of up to 8
+//                       tiles that keep the running maximum and pass the
+//                       knapsack's quick acceptance are evaluated together;
+//                       it records mu_hat and the rescale factors per tile
+//                       and the mask codes of the recomputed keys;
 //   dec_pv_kernel       P.V in parallel over key chunks for all query rows of
 //                       a key/value head (fp32 FMAs; every exponential is
-//                       exact in fp32);
+//                       exact in fp32), the weights recomputed from the codes;
 //   dec_reduce_kernel   the sum of the chunks' partial outputs.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -48,28 +52,6 @@ __device__ __forceinline__ void unpack8(const uint4 &w, float (&f)[8])
         f[2 * i] = __builtin_bit_cast(float, x[i] << 16);
         f[2 * i + 1] = __builtin_bit_cast(float, x[i] & 0xFFFF0000u);
     }
-}
-
-// 16-bit logit of this lane's key: the FP32 FMA chain over the channels in
-// ascending order from +0, rounded once to e4m11 (saturating).  The key row's
-// loads are all issued before the chain starts: the decision loop waits for
-// this recompute, so its cost is one memory round trip, not one per group.
-template <int D>
-__device__ __forceinline__ float dec16_chain(const uint16_t *krow, kptr32_t q)
-{
-    uint4 kw[D / 8];
-#pragma unroll
-    for (int g = 0; g < D / 8; ++g) kw[g] = *reinterpret_cast<const uint4 *>(krow + 8 * g);
-    float acc = 0.0f;
-#pragma unroll
-    for (int g = 0; g < D / 8; ++g) {
-        float kf[8];
-        unpack8(kw[g], kf);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc = __builtin_fmaf(q[8 * g + j], kf[j], acc);
-    }
-    uint32_t code;
-    return rn_e4m11((double)acc, &code);
 }
 
 // Wave reductions on the VALU: DPP exchanges within each row of 16 lanes
@@ -141,30 +123,53 @@ __device__ __forceinline__ double wave_sum_f64(double v)
 } // namespace
 
 // ------------------------------------------------------------------ phase 1
+// The logits of every (query row, key), which depend on no decision: the
+// 8-bit ones (the emulated e4m3 recursion) unless every logit is recomputed,
+// and the 16-bit ones (the FP32 FMA chain over the channels in ascending
+// order, rounded once to e4m11) unless none is, with the mask code of every
+// key (0, or 1 when every logit is 16-bit, where visible; 3 elsewhere; the
+// decisions overwrite the recomputed ones).
+//
 // grid (key blocks of 256 from key kb0, B * Hkv * row groups); a row group is
 // 4 consecutive rows of the G*M query rows of one key/value head (row rho is
 // query head hk*G + rho / M, query r = rho % M).  Thread t owns key
 // kb0 + 256 blockIdx.x + t.  The keys reach LDS in stages of 64 channels with
 // coalesced 16-byte loads (8 threads per 128-byte key row), so each global
 // load instruction covers whole cache lines; every thread then reads its own
-// row from LDS (pitch 72 bf16 against bank conflicts).
+// row from LDS (pitch 72 bf16 against bank conflicts).  The next stage's loads
+// are issued before the current stage is computed.
 constexpr int P1_CH = 64, P1_PITCH = P1_CH + 8;
 
-template <int D, bool SAT>
-__device__ __forceinline__ void dec8_staged(const uint16_t *kblk, int nvalid, uint16_t *tile, const float *qs,
-                                            uint32_t (&acc)[2])
+template <int D, int MODE, bool SAT>
+__device__ __forceinline__ void dec_staged(const uint16_t *kblk, int nvalid, uint16_t *tile, const float *qs,
+                                           uint32_t (&acc)[2], float (&acc16)[4])
 {
+    constexpr bool L8 = MODE != MODE_ALL16, L16 = MODE != MODE_PURE8 && !SAT;
     const int tid = threadIdx.x;
     acc[0] = acc[1] = 0u;
-    for (int c0 = 0; c0 < D; c0 += P1_CH) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int x = tid + 256 * j, key = x >> 3, part = x & 7;
-            const int kc = key < nvalid ? key : nvalid - 1;   // rows beyond N repeat the last key (not stored)
-            const uint4 w = *reinterpret_cast<const uint4 *>(kblk + (size_t)kc * D + c0 + part * 8);
-            *reinterpret_cast<uint4 *>(tile + key * P1_PITCH + part * 8) = w;
-        }
+    for (int i = 0; i < 4; ++i) acc16[i] = 0.0f;
+    // this thread's 16-byte pieces of 8 key rows (rows beyond N repeat the
+    // last key, not stored), one stage of 64 channels held in registers
+#define LAMP_P1_ADDR(j) (kblk + (size_t)((tid + 256 * (j)) >> 3 < nvalid ? (tid + 256 * (j)) >> 3 : nvalid - 1) * D + \
+                         ((tid + 256 * (j)) & 7) * 8)
+#define LAMP_P1_LOAD(c0) \
+    w0 = *reinterpret_cast<const uint4 *>(LAMP_P1_ADDR(0) + (c0)); w1 = *reinterpret_cast<const uint4 *>(LAMP_P1_ADDR(1) + (c0)); \
+    w2 = *reinterpret_cast<const uint4 *>(LAMP_P1_ADDR(2) + (c0)); w3 = *reinterpret_cast<const uint4 *>(LAMP_P1_ADDR(3) + (c0)); \
+    w4 = *reinterpret_cast<const uint4 *>(LAMP_P1_ADDR(4) + (c0)); w5 = *reinterpret_cast<const uint4 *>(LAMP_P1_ADDR(5) + (c0)); \
+    w6 = *reinterpret_cast<const uint4 *>(LAMP_P1_ADDR(6) + (c0)); w7 = *reinterpret_cast<const uint4 *>(LAMP_P1_ADDR(7) + (c0));
+#define LAMP_P1_STORE(j, w) *reinterpret_cast<uint4 *>(tile + (((tid + 256 * (j)) >> 3) * P1_PITCH) + ((tid + 256 * (j)) & 7) * 8) = (w);
+    uint4 w0, w1, w2, w3, w4, w5, w6, w7;
+    LAMP_P1_LOAD(0)
+#pragma clang loop unroll(full)
+    for (int c0 = 0; c0 < D; c0 += P1_CH) {
+        __syncthreads();   // the previous stage is no longer read
+        LAMP_P1_STORE(0, w0) LAMP_P1_STORE(1, w1) LAMP_P1_STORE(2, w2) LAMP_P1_STORE(3, w3)
+        LAMP_P1_STORE(4, w4) LAMP_P1_STORE(5, w5) LAMP_P1_STORE(6, w6) LAMP_P1_STORE(7, w7)
         __syncthreads();
+        if (c0 + P1_CH < D) {
+            LAMP_P1_LOAD(c0 + P1_CH)
+        }
 #pragma unroll 2
         for (int c = 0; c < P1_CH; c += 8) {
             float kf[8];
@@ -180,22 +185,31 @@ __device__ __forceinline__ void dec8_staged(const uint16_t *kblk, int nvalid, ui
             }
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
-                const float2 a = unpk_e4m3(acc[0]);
-                const float x = __builtin_fmaf(qv[0][j], kf[j], a.x);
-                const float y = __builtin_fmaf(qv[1][j], kf[j], a.y);
-                acc[0] = SAT ? pk_e4m3_sat(x, y, acc[0]) : pk_e4m3(x, y, acc[0]);
-                const float2 bb = unpk_e4m3(acc[1]);
-                const float z = __builtin_fmaf(qv[2][j], kf[j], bb.x);
-                const float u = __builtin_fmaf(qv[3][j], kf[j], bb.y);
-                acc[1] = SAT ? pk_e4m3_sat(z, u, acc[1]) : pk_e4m3(z, u, acc[1]);
+                if (L8) {
+                    const float2 a = unpk_e4m3(acc[0]);
+                    const float x = __builtin_fmaf(qv[0][j], kf[j], a.x);
+                    const float y = __builtin_fmaf(qv[1][j], kf[j], a.y);
+                    acc[0] = SAT ? pk_e4m3_sat(x, y, acc[0]) : pk_e4m3(x, y, acc[0]);
+                    const float2 bb = unpk_e4m3(acc[1]);
+                    const float z = __builtin_fmaf(qv[2][j], kf[j], bb.x);
+                    const float u = __builtin_fmaf(qv[3][j], kf[j], bb.y);
+                    acc[1] = SAT ? pk_e4m3_sat(z, u, acc[1]) : pk_e4m3(z, u, acc[1]);
+                }
+                if (L16) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) acc16[i] = __builtin_fmaf(qv[i][j], kf[j], acc16[i]);
+                }
             }
         }
-        __syncthreads();   // the tile is overwritten by the next stage
     }
 }
 
-template <int D>
-__global__ __launch_bounds__(256) void dec_logits8_kernel(DecParams p)
+#undef LAMP_P1_ADDR
+#undef LAMP_P1_LOAD
+#undef LAMP_P1_STORE
+
+template <int D, int MODE>
+__global__ __launch_bounds__(256) void dec_logits_kernel(DecParams p)
 {
     __shared__ __align__(16) uint16_t tile[256 * P1_PITCH];
     __shared__ __align__(16) float qs[4 * D];   // the group's 4 pre-scaled query rows
@@ -219,38 +233,71 @@ __global__ __launch_bounds__(256) void dec_logits8_kernel(DecParams p)
     for (int x = (int)threadIdx.x; x < 4 * D; x += 256) qs[x] = p.qt[qrow[x / D] * D + x % D];
     __syncthreads();
     uint32_t acc[2];
-    dec8_staged<D, false>(kblk, nvalid, tile, qs, acc);
-    // an overflow somewhere gives a NaN code at the end of its chain: the
-    // workgroup re-runs its chains with the saturating conversion
-    if (__syncthreads_or((e4m3_nan_bits(acc[0]) | e4m3_nan_bits(acc[1])) != 0u))
-        dec8_staged<D, true>(kblk, nvalid, tile, qs, acc);
-    if (key >= p.N) return;
+    float acc16[4];
+    dec_staged<D, MODE, false>(kblk, nvalid, tile, qs, acc, acc16);
+    // an overflow somewhere gives a NaN code at the end of its 8-bit chain:
+    // the workgroup re-runs those chains with the saturating conversion
+    if (MODE != MODE_ALL16 && __syncthreads_or((e4m3_nan_bits(acc[0]) | e4m3_nan_bits(acc[1])) != 0u)) {
+        float unused[4];
+        dec_staged<D, MODE, true>(kblk, nvalid, tile, qs, acc, unused);
+    }
+    if (key >= p.Np) return;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-        if (grp * 4 + i < rows) p.y8[qrow[i] * (size_t)p.Np + key] = (uint8_t)(acc[i >> 1] >> (8 * (i & 1)));
+    for (int i = 0; i < 4; ++i) {
+        const int rho = grp * 4 + i;
+        if (rho >= rows) continue;
+        const int P = p.N - p.M + rho % p.M;
+        const int vlo = p.window > 0 ? (P - p.window + 1 > 0 ? P - p.window + 1 : 0) : 0;
+        const int vhi = p.causal ? P : p.N - 1;
+        const size_t at = qrow[i] * (size_t)p.Np + key;
+        if (key < p.N) {
+            if (MODE != MODE_ALL16) p.y8[at] = (uint8_t)(acc[i >> 1] >> (8 * (i & 1)));
+            if (MODE != MODE_PURE8) {
+                uint32_t code;
+                (void)rn_e4m11((double)acc16[i], &code);
+                p.y16[at] = (uint16_t)code;
+            }
+        }
+        p.mask[at] = key >= vlo && key <= vhi ? (MODE == MODE_ALL16 ? 1 : 0) : 3;
+    }
 }
 
 // ------------------------------------------------------------------ phase 2
-// The decisions, one wave per query row.  The output does not feed any
-// decision, so this kernel writes the exponentials of every visible key (and
-// 0 for invisible keys of the visited tiles) and, per visited tile, the
-// factor f_t = (prod of lambda_hat of the later tiles) / omega that turns them
-// into the final weights of P.V: O = sum_t f_t sum_{i in t} E_i v_i.  Both are
-// stored with the R = G*M query rows of a key/value head interleaved
-// (e [b][hk][key][rho], f [b][hk][tile][rho]) for the P.V kernel.
+// The decisions, one wave per query row.  Nothing in the output feeds a
+// decision, so this kernel records only what the decisions fixed: per visited
+// tile mu_hat and the factor f_t = (prod of lambda_hat of the later tiles) /
+// omega that turns the tile's exponentials into the final weights of P.V
+// (O = sum_t f_t sum_{i in t} E_i v_i), both with the R = G*M query rows of a
+// key/value head interleaved (mu [b][hk][tile][rho], f likewise); and per
+// recomputed key its 16-bit logit and mask code (1 or 2).  The 8-bit logits'
+// mask codes (0, or 3 where invisible) were written with the codes by phase 1;
+// the all-16-bit mode writes every mask byte and 16-bit logit here.  P.V
+// recomputes each weight from these, with the same tables.
+//
+// The tile loop issues no global store (on gfx950 a wait for a load also
+// waits for every earlier store of the wave, so a store in the loop would
+// cost a store round trip at the next load): mu_hat and lambda_hat of 64
+// tiles at a time are held one per lane and written when the window is
+// complete, and the recomputed keys are collected in LDS and written at the
+// end of the row (or when the list is full).
+constexpr int REC_CAP = 256;   // recomputed keys held in LDS per wave
+
 template <int D, int MODE>
 __global__ __launch_bounds__(256) void dec_lamp_kernel(DecParams p)
 {
     __shared__ uint16_t lut[256];
     __shared__ double edk[EXPDOC_NK];
-    __shared__ __align__(16) uint8_t cbuf[4][16 * TK];   // per wave: the codes of 16 tiles
-    const int tid = threadIdx.x, lane = tid & 63;
+    __shared__ __align__(16) uint8_t cbuf[4][MODE != MODE_ALL16 ? 32 * TK : 1];     // per wave: rings of two
+    __shared__ __align__(16) uint16_t hbuf[4][MODE != MODE_PURE8 ? 32 * TK : 1];    // blocks of 16 tiles' codes
+    __shared__ int rec_key[4][MODE == MODE_LAMP ? REC_CAP : 1];
+    __shared__ uint8_t rec_code[4][MODE == MODE_LAMP ? REC_CAP : 1];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     for (int i = tid; i < 256; i += 256) lut[i] = p.lut8e[i];
     if (tid < EXPDOC_NK) edk[tid] = EXPDOC_K[tid];
     __syncthreads();
 
     const int64_t nrows = (int64_t)p.B * p.Hq * p.M;
-    const int64_t row = (int64_t)blockIdx.x * 4 + (tid >> 6);
+    const int64_t row = (int64_t)blockIdx.x * 4 + wv;
     if (row >= nrows) return;   // whole wave
     const int r = (int)(row % p.M);
     const int h = (int)((row / p.M) % p.Hq);
@@ -262,51 +309,97 @@ __global__ __launch_bounds__(256) void dec_lamp_kernel(DecParams p)
     const int vhi = p.causal ? P : p.N - 1;
     const int t_begin = vlo / TK, t_end = vhi / TK;
     const int ntiles = p.Np / TK;
-    const kptr32_t qv = (kptr32_t)(p.qt + row * D);
-    const uint16_t *kbase = p.k + ((size_t)b * p.Hkv + hk) * (size_t)p.N * D;
     const uint8_t *y8row = p.y8 + row * (size_t)p.Np;
-    float *erow = p.e + ((size_t)b * p.Hkv + hk) * (size_t)p.Np * RR + rho;          // stride RR per key
-    double *frow = p.f + ((size_t)b * p.Hkv + hk) * (size_t)ntiles * RR + rho;       // stride RR per tile
+    const uint16_t *y16row = p.y16 + row * (size_t)p.Np;
+    double *frow = p.f + ((size_t)b * p.Hkv + hk) * (size_t)ntiles * RR + rho;   // stride RR per tile
+    float *murow = p.mut + ((size_t)b * p.Hkv + hk) * (size_t)ntiles * RR + rho;  // stride RR per tile
     uint8_t *mrow = p.mask + row * (size_t)p.Np;
     const float NEG_INF = -__builtin_inff();
     float mu = NEG_INF;
     double om = 0.0;
 
-    // tiles without a visible key
+    // tiles without a visible key (phase 1 wrote the same code for those it covers)
     for (int t = lane; t < ntiles; t += 64)
         if (t < t_begin || t > t_end)
             for (int i = 0; i < TK; ++i) mrow[t * TK + i] = 3;
 
-    // The 8-bit logit codes arrive 16 tiles at a time: one 16-byte load per
-    // lane (keys 16 lane .. 16 lane + 15 of the block), held in registers one
-    // block ahead and passed through this wave's LDS buffer, so no global load
-    // is waited for inside the tile loop (on gfx950 a wait for a load also
-    // waits for every earlier store of the wave).
-    uint8_t *cb = cbuf[tid >> 6];
-    auto load_block = [&](int tb) -> uint4 {
-        const int k = tb * TK + 16 * lane;
-        return (MODE != MODE_ALL16 && tb <= t_end && k + 16 <= p.Np) ? *reinterpret_cast<const uint4 *>(y8row + k)
-                                                                      : make_uint4(0u, 0u, 0u, 0u);
+    // mu_hat and lambda_hat of the tiles t_begin + 64 wcur + lane
+    float w_mu = 0.0f;
+    double w_lam = 0.0;
+    int wcur = 0;
+    auto flush_window = [&]() {
+        const int tt = t_begin + 64 * wcur + lane;
+        if (tt <= t_end) {
+            frow[(size_t)tt * RR] = w_lam;
+            murow[(size_t)tt * RR] = w_mu;
+        }
     };
-    uint4 nxt = load_block(t_begin);
-    for (int t = t_begin; t <= t_end; ++t) {
+    auto record_tile = [&](int tt, float muh, double lam) {
+        if ((tt - t_begin) >> 6 != wcur) {
+            flush_window();
+            wcur = (tt - t_begin) >> 6;
+        }
+        if (lane == ((tt - t_begin) & 63)) {
+            w_mu = muh;
+            w_lam = lam;
+        }
+    };
+    // recomputed keys of this row (LDS list)
+    int nrec = 0;
+    auto flush_rec = [&]() {
+        for (int i = lane; i < nrec; i += 64) mrow[rec_key[wv][i]] = rec_code[wv][i];
+        nrec = 0;
+    };
+
+    // The logit codes arrive 16 tiles (a block) at a time: per lane keys
+    // 16 lane .. 16 lane + 15 of the block (one 16-byte load of 8-bit codes,
+    // two of 16-bit codes), held in registers one block ahead and passed
+    // through this wave's LDS rings of two blocks, so no load is waited for
+    // inside the tile loop.
+    uint8_t *cb = cbuf[wv];
+    uint16_t *hb = hbuf[wv];
+    uint4 nxt8 = make_uint4(0u, 0u, 0u, 0u), nxt16a = nxt8, nxt16b = nxt8;
+    auto load_block = [&](int kb) {
+        const int tb = t_begin + 16 * kb;
+        const int k = tb * TK + 16 * lane;
+        const bool ok = tb <= t_end && k + 16 <= p.Np;
+        if (MODE != MODE_ALL16) nxt8 = ok ? *reinterpret_cast<const uint4 *>(y8row + k) : make_uint4(0u, 0u, 0u, 0u);
+        if (MODE != MODE_PURE8) {
+            nxt16a = ok ? *reinterpret_cast<const uint4 *>(y16row + k) : make_uint4(0u, 0u, 0u, 0u);
+            nxt16b = ok ? *reinterpret_cast<const uint4 *>(y16row + k + 8) : make_uint4(0u, 0u, 0u, 0u);
+        }
+    };
+    load_block(0);
+    int kn = 0;   // blocks below kn are in the rings; the registers hold block kn
+    // make the codes of every tile up to t_hi readable (LDS operations of a
+    // wave stay in order; the ring slot written held a block two behind)
+    auto ensure = [&](int t_hi) {
+        while ((t_hi - t_begin) >> 4 >= kn) {
+            if (MODE != MODE_ALL16) *reinterpret_cast<uint4 *>(cb + (kn & 1) * 16 * TK + 16 * lane) = nxt8;
+            if (MODE != MODE_PURE8) {
+                *reinterpret_cast<uint4 *>(hb + (kn & 1) * 16 * TK + 16 * lane) = nxt16a;
+                *reinterpret_cast<uint4 *>(hb + (kn & 1) * 16 * TK + 16 * lane + 8) = nxt16b;
+            }
+            ++kn;
+            load_block(kn);
+        }
+    };
+    auto code_of = [&](int t) -> uint8_t { return cb[((t - t_begin) & 31) * TK + lane]; };
+    auto y16_of = [&](int t) -> float { return e4m11_value(hb[((t - t_begin) & 31) * TK + lane]); };
+
+    // One tile exactly as the procedure states it: look-ahead test on the
+    // maximizer, exponentials, rescale, knapsack, update.
+    auto tile_exact = [&](int t) {
         const int key = t * TK + lane;
         const bool vis = key >= vlo && key <= vhi;   // vhi < N
-        const int tb = (t - t_begin) & 15;
-        if (MODE != MODE_ALL16 && tb == 0) {
-            *reinterpret_cast<uint4 *>(cb + 16 * lane) = nxt;   // LDS operations of a wave stay in order
-            nxt = load_block(t + 16);
-        }
-        const uint8_t code = MODE != MODE_ALL16 ? cb[tb * TK + lane] : (uint8_t)0;
-        const int keyc = key < p.N ? key : p.N - 1;
-        const uint16_t *krow = kbase + (size_t)keyc * D;
+        const uint8_t code = MODE != MODE_ALL16 ? code_of(t) : (uint8_t)0;
         float y = NEG_INF;   // this key's logit in the precision chosen for it
         uint8_t prec = vis ? 0 : 3;
         bool have16 = false;
         float y16 = 0.0f;
         float muh;
         if (MODE == MODE_ALL16) {
-            y16 = dec16_chain<D>(krow, qv);
+            y16 = y16_of(t);
             have16 = true;
             y = vis ? y16 : NEG_INF;
             prec = vis ? 1 : 3;
@@ -326,7 +419,7 @@ __global__ __launch_bounds__(256) void dec_lamp_kernel(DecParams p)
                     // compute their 16-bit logit (the issue cost of one lane's)
                     const uint64_t at = __ballot(vis && y == mx);
                     const int c = __builtin_ctzll(at);
-                    y16 = dec16_chain<D>(krow, qv);
+                    y16 = y16_of(t);
                     have16 = true;
                     const float yc = __shfl(y16, c, 64);
                     muh = yc > mu ? yc : mu;
@@ -402,7 +495,7 @@ __global__ __launch_bounds__(256) void dec_lamp_kernel(DecParams p)
                 const uint64_t rbits = __ballot(rflag != 0);
                 if (rbits) {
                     if (!have16) {
-                        y16 = dec16_chain<D>(krow, qv);
+                        y16 = y16_of(t);
                         have16 = true;
                     }
                     if (rbits >> lane & 1ull) {
@@ -416,18 +509,123 @@ __global__ __launch_bounds__(256) void dec_lamp_kernel(DecParams p)
         }
         om = __builtin_fma(lam, om, S2);
         mu = muh;
-        erow[(size_t)key * RR] = e;
-        mrow[key] = prec;
-        if (lane == 0) frow[(size_t)t * RR] = lam;
+        record_tile(t, muh, lam);
+        if (MODE == MODE_LAMP) {
+            const bool recd = prec == 1 || prec == 2;
+            const uint64_t rb = __ballot(recd);
+            if (rb) {
+                if (nrec + 64 > REC_CAP) flush_rec();
+                if (recd) {
+                    const int pos = nrec + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(rb >> 32),
+                                                                          __builtin_amdgcn_mbcnt_lo((uint32_t)rb, 0u));
+                    rec_key[wv][pos] = key;
+                    rec_code[wv][pos] = prec;
+                }
+                nrec += __builtin_popcountll(rb);
+            }
+        }
+    };
+
+    // Runs of tiles in which nothing changes precision.  Once mu is finite,
+    // a tile whose maximizer passes the look-ahead test against mu (pure
+    // 8-bit mode: whose maximum does not exceed mu) keeps mu_hat = mu and
+    // lambda_hat = 1, so its exponentials and sum depend on mu alone; the
+    // knapsack then keeps all its logits when the quick acceptance holds
+    // against omega_hat = omega + S.  Up to CH = 8 tiles are evaluated
+    // together on that assumption, 8 lanes per tile and 8 keys per lane
+    // (eight reductions at once over groups of 8 lanes); the omega chain is
+    // then replayed tile by tile in the same order and rounding as above, and
+    // the tiles up to the first one where a test fails are committed; that
+    // tile goes through tile_exact.  Every committed value equals what
+    // tile_exact would have produced: the maximum and the fp64 sum of the
+    // exponentials are exact in any order, and the fp32 sum only feeds a
+    // bound that holds in any order (a tile the bound does not accept here
+    // goes through the exact path, whose greedy then decides).
+    constexpr int CH = 8;
+    const int jl = lane >> 3, sub = lane & 7;   // this lane's tile of the run, its 8 keys
+    int t = t_begin;
+    while (t <= t_end) {
+        if (MODE == MODE_ALL16 || mu == NEG_INF) {
+            ensure(t);
+            tile_exact(t);
+            ++t;
+            continue;
+        }
+        const int nt = t_end - t + 1 < CH ? t_end - t + 1 : CH;
+        ensure(t + nt - 1);
+        const int tj = t + jl;
+        const bool in = jl < nt;
+        const uint2 cw = in ? *reinterpret_cast<const uint2 *>(cb + ((tj - t_begin) & 31) * TK + 8 * sub)
+                            : make_uint2(0u, 0u);
+        const int key0 = tj * TK + 8 * sub;
+        float mxl = NEG_INF, sf = 0.0f;
+        double sl = 0.0;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int key = key0 + k;
+            const bool vis = in && key >= vlo && key <= vhi;
+            const uint8_t code = (uint8_t)((k < 4 ? cw.x : cw.y) >> (8 * (k & 3)));
+            const float y = vis ? e4m3_value(code) : NEG_INF;
+            mxl = y > mxl ? y : mxl;
+            const float e = vis ? bf16_value(lut[ue5m3_code(shift_of(mu, y))]) : 0.0f;
+            sl += (double)e;
+            sf += e;
+        }
+        // reductions over the 8 lanes of each tile (quad neighbours, quad
+        // pairs, half-row mirror)
+        {
+            float o;
+            o = dpp_f32<0xB1>(mxl); mxl = o > mxl ? o : mxl;
+            o = dpp_f32<0x4E>(mxl); mxl = o > mxl ? o : mxl;
+            o = dpp_f32<0x141>(mxl); mxl = o > mxl ? o : mxl;
+            sl += dpp_f64<0xB1>(sl);
+            sl += dpp_f64<0x4E>(sl);
+            sl += dpp_f64<0x141>(sl);
+            if (MODE == MODE_LAMP) {
+                sf += dpp_f32<0xB1>(sf);
+                sf += dpp_f32<0x4E>(sf);
+                sf += dpp_f32<0x141>(sf);
+            }
+        }
+        // the look-ahead test of every tile at once (lane 8j holds tile j's
+        // maximum), then the omega chain and the quick acceptance tile by tile
+        // up to the first failure, without branches
+        const double m = (double)mu;
+        const bool passl = MODE == MODE_PURE8 ? !(mxl > mu) : m > __builtin_fma(__builtin_fabs(m), p.delta, (double)mxl);
+        const uint64_t fails = ~__ballot(passl) & 0x0101010101010101ull & (nt < CH ? (1ull << (8 * nt)) - 1ull : ~0ull);
+        int jc = fails ? __builtin_ctzll(fails) >> 3 : nt;   // tiles committed
+        double omv = om;
+#pragma unroll
+        for (int j = 0; j < CH; ++j) {
+            const double omh = __builtin_fma(1.0, omv, readlane_f64(sl, 8 * j));
+            bool ok = true;
+            if (MODE == MODE_LAMP) {
+                const double SF = (double)readlane_f32(sf, 8 * j) * (1.0 + 0x1p-17);
+                ok = SF <= (p.tau * omh) * (1.0 - 0x1p-38);
+            }
+            jc = (j < jc && !ok) ? j : jc;
+            omv = j < jc ? omh : omv;
+        }
+        om = omv;
+#pragma unroll
+        for (int j = 0; j < CH; ++j)
+            if (j < jc) record_tile(t + j, mu, 1.0);
+        t += jc;
+        if (jc < nt) {
+            tile_exact(t);
+            ++t;
+        }
     }
+    flush_window();
+    if (MODE == MODE_LAMP) flush_rec();
     if (lane == 0) p.lse[row] = (float)((double)mu + ::log(om));
-    __threadfence_block();   // lane 0's rescale factors, read back by every lane below
+    __threadfence_block();   // the rescale factors written above, read back by every lane below
     // f_t = (prod over the later visited tiles of lambda_hat) / omega, from the
     // last tile backwards in chunks of 64 (lane j: tile t_end - 64c - j)
     double carry = 1.0 / om;
     for (int t0 = t_end; t0 >= t_begin; t0 -= 64) {
-        const int t = t0 - lane;
-        const double lam = t >= t_begin ? frow[(size_t)t * RR] : 1.0;
+        const int tt = t0 - lane;
+        const double lam = tt >= t_begin ? frow[(size_t)tt * RR] : 1.0;
         double incl = lam;   // inclusive product over lanes 0..j
 #pragma unroll
         for (int m = 1; m < 64; m <<= 1) {
@@ -436,7 +634,7 @@ __global__ __launch_bounds__(256) void dec_lamp_kernel(DecParams p)
         }
         double excl = __shfl_up(incl, 1, 64);
         if (lane == 0) excl = 1.0;
-        if (t >= t_begin) frow[(size_t)t * RR] = carry * excl;
+        if (tt >= t_begin) frow[(size_t)tt * RR] = carry * excl;
         carry *= __shfl(incl, 63, 64);
     }
 }
@@ -444,11 +642,14 @@ __global__ __launch_bounds__(256) void dec_lamp_kernel(DecParams p)
 // ------------------------------------------------------------------ phase 3
 // P.V: one workgroup per (chunk of PV_CHUNK keys from key kb0, b, key/value
 // head) for NR of the R = G*M query rows of the head.  The chunk's weights
-// E f_t of those rows are first gathered into LDS (coalesced), so the main
-// loop issues one 16-byte load of V (8 channels of one key) per lane and key,
-// feeding 8 FMAs per query row, and reads the key's weights from LDS (one
-// broadcast read).  Partial outputs per chunk go to a workspace; phase 4 adds
-// them up.
+// E f_t of those rows are first formed in LDS: E from the key's mask code and
+// logit (the 8-bit code through the ue5m3 table, or the recomputed 16-bit
+// logit through the ue5m11 table) against the tile's mu_hat, the same
+// computation as in the decisions; then the main loop issues one 16-byte load
+// of V (8 channels of one key) per lane and key, one step ahead of its
+// arithmetic (the first step before the weights), feeding 8 FMAs per query row,
+// and reads the key's weights from LDS (one broadcast read).  Partial outputs
+// per chunk go to a workspace; phase 4 adds them up.
 constexpr int PV_CHUNK = 512, PV_ROWS = 16;
 
 template <int D, int NR>
@@ -457,6 +658,7 @@ __global__ __launch_bounds__(256) void dec_pv_kernel(DecParams p, int rg0)
     constexpr int CC = D / 8, KG = 256 / CC;   // channel chunks; keys per step over the workgroup
     __shared__ __align__(16) float wl[PV_CHUNK][NR];
     __shared__ float red[4][NR][D];
+    __shared__ uint16_t lut[256];
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
     const int cc = tid % CC, kg = tid / CC;
     const int chunk = (int)blockIdx.x;
@@ -466,19 +668,59 @@ __global__ __launch_bounds__(256) void dec_pv_kernel(DecParams p, int rg0)
     const int ntiles = p.Np / TK;
     const int k0 = p.kb0 + chunk * PV_CHUNK;
     const int k_end = k0 + PV_CHUNK < p.N ? k0 + PV_CHUNK : p.N;
-    for (int x = tid; x < PV_CHUNK * NR; x += 256) {
-        const int kl = x / NR, i = x % NR;
-        const int key = k0 + kl, rho = rg0 + i;
-        float wgt = 0.0f;
-        if (key < k_end && rho < RR) {
-            const int P = p.N - p.M + rho % p.M;
-            const int vlo = p.window > 0 ? (P - p.window + 1 > 0 ? P - p.window + 1 : 0) : 0;
-            const int vhi = p.causal ? P : p.N - 1;
-            if (key >= vlo && key <= vhi)
-                wgt = p.e[((size_t)bhk * p.Np + key) * RR + rho] *
-                      (float)p.f[((size_t)bhk * ntiles + key / TK) * RR + rho];
+    for (int i = tid; i < 256; i += 256) lut[i] = p.lut8e[i];
+    // U keys of V per step and lane (8 channels each), the first step's loads
+    // issued before the weights are formed and every later step's one step
+    // ahead of its arithmetic (keys past the chunk read a valid row and have
+    // weight 0)
+    constexpr int U = 4, STEPS = PV_CHUNK / (U * KG);
+    const uint16_t *vbase = p.v + (size_t)bhk * p.N * D + cc * 8;
+    uint4 vbuf[2][U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int key = k0 + kg + u * KG;
+        vbuf[0][u] = *reinterpret_cast<const uint4 *>(vbase + (size_t)(key < k_end ? key : k_end - 1) * D);
+    }
+    __syncthreads();
+    // the weights, 8 per thread at a time with all their loads issued together
+    // (consecutive threads: consecutive keys of one row)
+    constexpr int EB = 8;
+    for (int x0 = tid; x0 < PV_CHUNK * NR; x0 += 256 * EB) {
+        uint32_t mc[EB], c8[EB];
+        float muv[EB];
+        double fv[EB];
+        size_t at[EB];
+#pragma unroll
+        for (int e = 0; e < EB; ++e) {
+            const int x = x0 + 256 * e;
+            const int i = x / PV_CHUNK, kl = x % PV_CHUNK;
+            const int key = k0 + kl, rho = rg0 + i;
+            const bool valid = x < PV_CHUNK * NR && key < k_end && rho < RR;
+            const int64_t rid = ((int64_t)b * p.Hq + hk * G + rho / p.M) * p.M + rho % p.M;
+            at[e] = (size_t)rid * p.Np + key;
+            const size_t tat = ((size_t)bhk * ntiles + key / TK) * RR + rho;
+            mc[e] = valid ? p.mask[at[e]] : 3u;
+            c8[e] = valid ? p.y8[at[e]] : 0u;
+            muv[e] = valid ? p.mut[tat] : 0.0f;
+            fv[e] = valid ? p.f[tat] : 0.0;
         }
-        wl[kl][i] = wgt;
+#pragma unroll
+        for (int e = 0; e < EB; ++e) {
+            const int x = x0 + 256 * e;
+            if (x >= PV_CHUNK * NR) break;
+            float wgt = 0.0f;
+            if (mc[e] != 3u) {
+                float ev;
+                if (mc[e] == 0u) {
+                    ev = bf16_value(lut[ue5m3_code(shift_of(muv[e], e4m3_value(c8[e])))]);
+                } else {
+                    const uint32_t hl = p.exp16hl[ue5m11_code(shift_of(muv[e], e4m11_value(p.y16[at[e]])))];
+                    ev = bf16_value(hl & 0xFFFFu) + bf16_value(hl >> 16);   // exact
+                }
+                wgt = ev * (float)fv[e];
+            }
+            wl[x % PV_CHUNK][x / PV_CHUNK] = wgt;
+        }
     }
     __syncthreads();
     float acc[NR][8];
@@ -486,22 +728,20 @@ __global__ __launch_bounds__(256) void dec_pv_kernel(DecParams p, int rg0)
     for (int i = 0; i < NR; ++i)
 #pragma unroll
         for (int c = 0; c < 8; ++c) acc[i][c] = 0.0f;
-    const uint16_t *vbase = p.v + (size_t)bhk * p.N * D + cc * 8;
-    // U keys per iteration, their loads issued before any arithmetic (keys
-    // past the chunk read a valid row and have weight 0)
-    constexpr int U = 4;
-    for (int kl0 = kg; kl0 < PV_CHUNK; kl0 += U * KG) {
-        uint4 vw[U];
+#pragma clang loop unroll(full)
+    for (int st = 0; st < STEPS; ++st) {
+        if (st + 1 < STEPS) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int key = k0 + kl0 + u * KG;
-            vw[u] = *reinterpret_cast<const uint4 *>(vbase + (size_t)(key < k_end ? key : k_end - 1) * D);
+            for (int u = 0; u < U; ++u) {
+                const int key = k0 + kg + (st + 1) * U * KG + u * KG;
+                vbuf[(st + 1) & 1][u] = *reinterpret_cast<const uint4 *>(vbase + (size_t)(key < k_end ? key : k_end - 1) * D);
+            }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             float vf[8];
-            unpack8(vw[u], vf);
-            const int kl = kl0 + u * KG;
+            unpack8(vbuf[st & 1][u], vf);
+            const int kl = kg + st * U * KG + u * KG;
 #pragma unroll
             for (int i = 0; i < NR; ++i) {
                 const float wgt = wl[kl][i];
@@ -555,10 +795,12 @@ __global__ __launch_bounds__(256) void dec_reduce_kernel(DecParams p)
 template <int D>
 static hipError_t launch_decode_d(const DecParams &p, hipStream_t s)
 {
-    if (p.mode != MODE_ALL16) {   // the all-16-bit mode reads no 8-bit logit
+    {
         const int G = p.Hq / p.Hkv, ngroups = (G * p.M + 3) / 4;
         dim3 g1((unsigned)((p.N - p.kb0 + 255) / 256), (unsigned)(p.B * p.Hkv * ngroups));
-        hipLaunchKernelGGL(dec_logits8_kernel<D>, g1, dim3(256), 0, s, p);
+        if (p.mode == MODE_PURE8) hipLaunchKernelGGL((dec_logits_kernel<D, MODE_PURE8>), g1, dim3(256), 0, s, p);
+        else if (p.mode == MODE_ALL16) hipLaunchKernelGGL((dec_logits_kernel<D, MODE_ALL16>), g1, dim3(256), 0, s, p);
+        else hipLaunchKernelGGL((dec_logits_kernel<D, MODE_LAMP>), g1, dim3(256), 0, s, p);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

@@ -494,10 +494,10 @@ int lamp_reserve(int device, size_t bytes)
     return fail(LAMP_ERR_HIP, "lamp_reserve: %s", hipGetErrorString(e));
 }
 
-// Byte sizes of the decode workspace: pre-scaled queries, 8-bit codes,
-// exponentials, per-tile factors, partial outputs of the key chunks.
+// Byte sizes of the decode workspace: pre-scaled queries, 8-bit and 16-bit
+// logit codes, per-tile factors and mu_hat, partial outputs of the key chunks.
 struct DecLayout {
-    size_t qt, y8, e, f, part, total;
+    size_t qt, y8, y16, f, mu, part, total;
 };
 
 static DecLayout dec_layout(int B, int Hq, int M, int N, int d)
@@ -507,10 +507,11 @@ static DecLayout dec_layout(int B, int Hq, int M, int N, int d)
     DecLayout l;
     l.qt = align256(nrows * d * 4);
     l.y8 = align256(nrows * Np);
-    l.e = align256(nrows * Np * 4);
+    l.y16 = align256(nrows * Np * 2);
     l.f = align256(nrows * (Np / 64) * 8);
+    l.mu = align256(nrows * (Np / 64) * 4);
     l.part = align256(nrows * nch * d * 4);
-    l.total = l.qt + l.y8 + l.e + l.f + l.part;
+    l.total = l.qt + l.y8 + l.y16 + l.f + l.mu + l.part;
     return l;
 }
 
@@ -560,9 +561,10 @@ int lamp_attn_decode(const uint16_t *q, const uint16_t *k, const uint16_t *v, in
         char *base = static_cast<char *>(wsb);
         p.qt = reinterpret_cast<float *>(base);
         p.y8 = reinterpret_cast<uint8_t *>(base + lay.qt);
-        p.e = reinterpret_cast<float *>(base + lay.qt + lay.y8);
-        p.f = reinterpret_cast<double *>(base + lay.qt + lay.y8 + lay.e);
-        p.part = reinterpret_cast<float *>(base + lay.qt + lay.y8 + lay.e + lay.f);
+        p.y16 = reinterpret_cast<uint16_t *>(base + lay.qt + lay.y8);
+        p.f = reinterpret_cast<double *>(base + lay.qt + lay.y8 + lay.y16);
+        p.mut = reinterpret_cast<float *>(base + lay.qt + lay.y8 + lay.y16 + lay.f);
+        p.part = reinterpret_cast<float *>(base + lay.qt + lay.y8 + lay.y16 + lay.f + lay.mu);
     }
     p.k = k;
     p.v = v;

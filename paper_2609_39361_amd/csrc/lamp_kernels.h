@@ -54,7 +54,8 @@ struct DecParams {
     const float *qt;          // [B][Hq][M][D] pre-scaled queries
     const uint16_t *k, *v;    // [B][Hkv][N][D] bf16 cache
     uint8_t *y8;              // [B][Hq][M][Np] 8-bit logit codes (workspace)
-    float *e;                 // [B][Hkv][Np][G*M] exponentials of the visited tiles (workspace)
+    uint16_t *y16;            // [B][Hq][M][Np] e4m11 codes of the 16-bit logits (workspace)
+    float *mut;               // [B][Hkv][Np/64][G*M] mu_hat per visited tile (workspace)
     double *f;                // [B][Hkv][Np/64][G*M] lambda_hat per tile, then the P.V factor (workspace)
     float *part;              // [B][Hq][M][ceil(N/512)][D] partial outputs of the key chunks (workspace)
     const uint16_t *lut8e;    // ue5m3 shift code -> bf16 bits of the ue5m3 exp
