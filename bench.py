@@ -254,8 +254,8 @@ def main_decode(args, w, tau):
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-            "kernel": "dec_logits8_kernel<%d> + dec_lamp_kernel<%d,%d> + dec_pv_kernel<%d,4> + dec_reduce_kernel<%d>"
-                      % (w.d, w.d, _mode_of(tau), w.d, w.d),
+            "kernel": "dec_logits_kernel<%d,%d> + dec_lamp_kernel<%d,%d> + dec_pv_kernel<%d,4> + dec_reduce_kernel<%d>"
+                      % (w.d, _mode_of(tau), w.d, _mode_of(tau), w.d, w.d),
             "kernel_ms": kernel_ms, "prepass_ms": pre_ms_sum / launches,
             "bytes_per_launch": nbytes,
             "valu_frac_algorithmic": (OPS_PER_MAC8 * mac8 + OPS_PER_MAC16 * mac16) / (kernel_ms * 1e-3) / VALU_LANE_OPS,
