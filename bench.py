@@ -42,7 +42,7 @@ SIM_FLAG = 4
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lamp_fwd16_kernel.qwen3-8b-prefill-8k.hbm_traffic.md")
 VALU_FILE = os.path.join(ROOT, "profiles", "lamp_fwd16_kernel.qwen3-8b-prefill-8k.valu_issue.md")
-KERNEL_SOURCES = ["lamp_fwd.hip", "lamp_fwd16.hip", "lamp_loops.h", "lamp_device.h", "lamp_kernels.h", "lamp_stats.h"]
+KERNEL_SOURCES = ["lamp_fwd.hip", "lamp_fwd16.hip", "lamp_loops.h", "lamp_sr.h", "lamp_device.h", "lamp_kernels.h", "lamp_stats.h"]
 
 
 def kernel_source_hash():
@@ -419,7 +419,7 @@ def run_fwd(args, w, tau, flags, host_inputs, dev_inputs, out, dev):
         "vs_baseline": None,
         "dtype": ("SIM profile: fp32 with 3/11-bit mantissas (fp32 FMA + integer rounding), bf16 inputs, fp32 output"
                   if sim else
-                  "e4m3 stochastically rounded (fp32 FMA + Philox4x64-10 bits), e4m11, bf16 inputs, fp32 output"
+                  "e4m3 stochastically rounded (fp32 FMA + Philox4x32-10 bits), e4m11, bf16 inputs, fp32 output"
                   if sr else "e4m3/e4m11 emulated (fp32 FMA + fp8 conversions), bf16 inputs, fp32 output"),
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "N": w.N, "d": w.d,
@@ -441,10 +441,10 @@ def run_fwd(args, w, tau, flags, host_inputs, dev_inputs, out, dev):
             "frac_vs_measured_fmac_rate": macs_per_s / fmac_rate,
             "measured_fmac_lane_ops_per_s": fmac_rate,
             "traffic": None if sr else measured_traffic(w.name, tau, flags),
-            "kernel": ("lamp_fwd_kernel<%d,%d,%d,%d,SR>" % (w.d, w.bq, w.bk, w.nk)) if sr
-                      else ("lamp_fwd16_kernel<%d,%d,%d,%s>" % (w.d, w.bq, _mode_of(tau), "true" if sim else "false"))
+            "kernel": ("lamp_fwd16_kernel<%d,%d,%d,%s%s>" % (w.d, w.bq, _mode_of(tau), "true" if sim else "false",
+                                                             ",SR" if sr and _mode_of(tau) != 2 else ""))
                       if (w.bk == 16 and w.d >= 128)
-                      else ("lamp_fwd_kernel<%d,%d,%d,%d>" % (w.d, w.bq, w.bk, w.nk)),
+                      else ("lamp_fwd_kernel<%d,%d,%d,%d%s>" % (w.d, w.bq, w.bk, w.nk, ",SR" if sr else "")),
             "kernel_ms": kernel_ms,
             "prepass_ms": pre_ms_sum / launches,
             "macs_per_launch": {"mac8": mac8, "mac16": mac16},

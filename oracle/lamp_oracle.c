@@ -537,50 +537,41 @@ static double logit16_sim_step(const float *qt, const uint16_t *k, int d, int *s
  *     recursion) to one of its two e4m3 neighbours: a = min(|t|, 448), lo the
  *     e4m3 number next to a toward zero, u = 2^(max(e, -6) - 3) its spacing
  *     (e the binary exponent of a); the result is lo + u when
- *     floor(2^20 (a - lo) / u) + r >= 2^20 and lo otherwise, with the sign of
+ *     floor(2^16 (a - lo) / u) + r >= 2^16 and lo otherwise, with the sign of
  *     t (saturating at 448, as the round-to-nearest recursion; a zero keeps
- *     the sign of t).  r is a uniform 20-bit integer, so the probability of
+ *     the sign of t).  r is a uniform 16-bit integer, so the probability of
  *     rounding away from zero is the distance to lo in units of u, cut to
- *     20 bits (exact for a normal-range a, whose FP32 pattern has 20 bits below
- *     e4m3's last mantissa bit);
- *   - r comes from the counter-based generator Philox4x64-10 (Salmon, Moraes,
+ *     16 bits;
+ *   - r comes from the counter-based generator Philox4x32-10 (Salmon, Moraes,
  *     Dror and Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC 2011),
- *     key (seed, 0), counter (j, i, b*Hq + h, c / 12) for query row j, key
- *     i, query head h of batch b and channel c: each of the four 64-bit
- *     words of one call holds three 20-bit fields (bits 0-19, 20-39, 40-59;
- *     bits 60-63 unused), and channel c takes field (c mod 12) mod 3 of word
- *     (c mod 12) / 3.  The numbers depend on the logit and the channel alone,
+ *     key (seed mod 2^32, seed / 2^32), counter (j, i, b*Hq + h, c / 8) for
+ *     query row j, key i, query head h of batch b and channel c: each of the
+ *     four 32-bit words of one call holds two 16-bit fields, and channel c
+ *     takes the low half (c even) or the high half (c odd) of word
+ *     (c mod 8) / 2.  The numbers depend on the logit and the channel alone,
  *     not on any blocking. */
 
-/* (hi, lo) = a * b, full 128-bit product. */
-static void mulhilo64(uint64_t a, uint64_t b, uint64_t *hi, uint64_t *lo)
-{
-    unsigned __int128 p = (unsigned __int128)a * b;
-    *hi = (uint64_t)(p >> 64);
-    *lo = (uint64_t)p;
-}
-
-/* Philox4x64-10 of counter c under key k (SC 2011: the 4x64 round with
+/* Philox4x32-10 of counter c under key k (SC 2011: the 4x32 round with
  * multipliers M0, M1 and Weyl key increments W0, W1; ten rounds, the first
  * with the key as given). */
-void oracle_philox4x64_10(const uint64_t c_in[4], const uint64_t k_in[2], uint64_t out[4])
+void oracle_philox4x32_10(const uint32_t c_in[4], const uint32_t k_in[2], uint32_t out[4])
 {
-    const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
-    const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
-    uint64_t c0 = c_in[0], c1 = c_in[1], c2 = c_in[2], c3 = c_in[3];
-    uint64_t k0 = k_in[0], k1 = k_in[1];
+    const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
+    const uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+    uint32_t c0 = c_in[0], c1 = c_in[1], c2 = c_in[2], c3 = c_in[3];
+    uint32_t k0 = k_in[0], k1 = k_in[1];
     for (int round = 0; round < 10; ++round) {
         if (round > 0) { k0 += W0; k1 += W1; }
-        uint64_t hi0, lo0, hi1, lo1;
-        mulhilo64(M0, c0, &hi0, &lo0);
-        mulhilo64(M1, c2, &hi1, &lo1);
-        uint64_t n0 = hi1 ^ c1 ^ k0, n1 = lo1, n2 = hi0 ^ c3 ^ k1, n3 = lo0;
+        const uint64_t p0 = (uint64_t)M0 * c0, p1 = (uint64_t)M1 * c2;
+        const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        const uint32_t n0 = hi1 ^ c1 ^ k0, n1 = lo1, n2 = hi0 ^ c3 ^ k1, n3 = lo0;
         c0 = n0; c1 = n1; c2 = n2; c3 = n3;
     }
     out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
 }
 
-/* Stochastic rounding of t to e4m3 with the 20-bit random integer r (above). */
+/* Stochastic rounding of t to e4m3 with the 16-bit random integer r (above). */
 static double sr_e4m3(double t, uint32_t r)
 {
     double a = fabs(t);
@@ -592,31 +583,30 @@ static double sr_e4m3(double t, uint32_t r)
     if (e < emin) e = emin;
     double u = ldexp(1.0, e - F_E4M3.mbits);
     double lo = floor(a / u) * u;
-    double frac20 = floor((a - lo) / u * 1048576.0);
-    double res = (frac20 + (double)r >= 1048576.0) ? lo + u : lo;
+    double frac16 = floor((a - lo) / u * 65536.0);
+    double res = (frac16 + (double)r >= 65536.0) ? lo + u : lo;
     return copysign(res, t);
 }
 
 int oracle_sr_e4m3(const double *t, const uint32_t *r, double *y, int64_t n)
 {
     for (int64_t i = 0; i < n; ++i) {
-        if (r[i] >= (1u << 20)) return -1;
+        if (r[i] >= (1u << 16)) return -1;
         y[i] = sr_e4m3(t[i], r[i]);
     }
     return 0;
 }
 
-/* 20-bit random integer of channel c of the logit (j, i) of head bh. */
-static uint32_t sr_bits(uint64_t seed, int64_t bh, int64_t j, int64_t i, int c, uint64_t w[4], int *have)
+/* 16-bit random integer of channel c of the logit (j, i) of head bh. */
+static uint32_t sr_bits(uint64_t seed, int64_t bh, int64_t j, int64_t i, int c, uint32_t w[4], int *have)
 {
-    if (c % 12 == 0 || !*have) {
-        const uint64_t ctr[4] = {(uint64_t)j, (uint64_t)i, (uint64_t)bh, (uint64_t)(c / 12)};
-        const uint64_t key[2] = {seed, 0};
-        oracle_philox4x64_10(ctr, key, w);
+    if (c % 8 == 0 || !*have) {
+        const uint32_t ctr[4] = {(uint32_t)j, (uint32_t)i, (uint32_t)bh, (uint32_t)(c / 8)};
+        const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+        oracle_philox4x32_10(ctr, key, w);
         *have = 1;
     }
-    const int m = c % 12;
-    return (uint32_t)((w[m / 3] >> (20 * (m % 3))) & 0xFFFFFu);
+    return (w[(c % 8) / 2] >> (16 * (c & 1))) & 0xFFFFu;
 }
 
 /* Low-precision logit with stochastic rounding: the recursion of logit8 with
@@ -626,7 +616,7 @@ static double logit8_sr_s(const float *qt, const uint16_t *k, int d, uint64_t se
                           int64_t i, int *sat)
 {
     float acc = 0.0f;
-    uint64_t w[4];
+    uint32_t w[4];
     int have = 0;
     for (int c = 0; c < d; ++c) {
         float t = fmaf(qt[c], bf16_to_f32(k[c]), acc);

@@ -46,8 +46,8 @@ def lib():
         _lib.lamp_oracle_fwd_ex.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32,
                                             f64, f64, ctypes.c_uint, ctypes.c_uint64, P, P, P, P, i64, i32, P]
         _lib.lamp_oracle_fwd_ex.restype = i32
-        _lib.oracle_philox4x64_10.argtypes = [P, P, P]
-        _lib.oracle_philox4x64_10.restype = None
+        _lib.oracle_philox4x32_10.argtypes = [P, P, P]
+        _lib.oracle_philox4x32_10.restype = None
         _lib.oracle_sr_e4m3.argtypes = [P, P, P, i64]
         _lib.oracle_sr_e4m3.restype = i32
         _lib.oracle_logits8_sr.argtypes = [P, P, i32, i32, i32, i32, i32, i32, i32, i32, i32, ctypes.c_uint64, P, i32]
@@ -166,24 +166,24 @@ def logits8(q, k, causal, window, row0, nrows, nthreads=0):
     return out
 
 
-def philox4x64_10(counter, key):
-    """Philox4x64-10 (Salmon et al., SC 2011) of one counter (4 words) under key (2 words)."""
-    c = np.ascontiguousarray(counter, dtype=np.uint64)
-    kk = np.ascontiguousarray(key, dtype=np.uint64)
+def philox4x32_10(counter, key):
+    """Philox4x32-10 (Salmon et al., SC 2011) of one counter (4 words) under key (2 words)."""
+    c = np.ascontiguousarray(counter, dtype=np.uint32)
+    kk = np.ascontiguousarray(key, dtype=np.uint32)
     assert c.shape == (4,) and kk.shape == (2,)
-    out = np.empty(4, dtype=np.uint64)
-    lib().oracle_philox4x64_10(_ptr(c), _ptr(kk), _ptr(out))
+    out = np.empty(4, dtype=np.uint32)
+    lib().oracle_philox4x32_10(_ptr(c), _ptr(kk), _ptr(out))
     return out
 
 
 def sr_e4m3(t, r):
-    """Stochastic rounding of values t to e4m3 with 20-bit random integers r (fp64 results)."""
+    """Stochastic rounding of values t to e4m3 with 16-bit random integers r (fp64 results)."""
     t = np.ascontiguousarray(t, dtype=np.float64)
     r = np.ascontiguousarray(np.broadcast_to(r, t.shape), dtype=np.uint32)
     y = np.empty_like(t)
     rc = lib().oracle_sr_e4m3(_ptr(t), _ptr(r), _ptr(y), t.size)
     if rc != 0:
-        raise ValueError("random integers must lie in [0, 2^20)")
+        raise ValueError("random integers must lie in [0, 2^16)")
     return y
 
 
@@ -276,7 +276,7 @@ def logits_sim(q, k, causal, window, row0, nrows, high, nthreads=0):
 STAGE1_OFF = 1   # the first stage disabled: mu_hat from the 8-bit maxima, stage 2 alone recomputes
 MU_TRUNC = 2     # 8-bit shifts against mu_hat truncated to e4m3 (SIM: to 3 mantissa bits)
 SIM = 4          # the "SIM" precision profile (FP32 range, 3/11-bit mantissas, no saturation)
-SR8 = 8          # the 8-bit accumulation rounded stochastically (seeded Philox4x64-10 bits)
+SR8 = 8          # the 8-bit accumulation rounded stochastically (seeded Philox4x32-10 bits)
 Y16_STEP = 16    # the 16-bit logits with e4m11 as the accumulator (rounded after every FMA; Sec. 3.3 literally)
 
 STAT_NAMES = ("tiles", "stage1", "stage2", "inactive", "sat8", "sat16", "spec_unused", "late16")

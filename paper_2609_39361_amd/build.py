@@ -28,8 +28,8 @@ LIB = os.path.join(HERE, "liblamp.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["lamp_kernels.hip", "lamp_fwd.hip", "lamp_fwd16.hip", "lamp_decode.hip", "lamp_rates.hip", "lamp_noalloc.hip",
-           "lamp_host.cpp"]
+SOURCES = ["lamp_kernels.hip", "lamp_fwd.hip", "lamp_fwd16.hip", "lamp_fwd16_sr.hip", "lamp_decode.hip", "lamp_rates.hip",
+           "lamp_noalloc.hip", "lamp_host.cpp"]
 
 DPP_VGPR_WAITS = 2
 DPP_EXEC_WAITS = 5

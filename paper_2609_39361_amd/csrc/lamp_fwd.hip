@@ -937,6 +937,8 @@ hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipSt
 
 hipError_t dispatch_fwd_sr(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found)
 {
+    // 16-key sub-blocks with d >= 128: the pipelined kernel's SR instantiations
+    if (fwd_grouped(D, BQ, BK, NK)) return dispatch_fwd16_sr(D, BQ, p, s, found);
     *found = true;
 #define LAMP_FWD_SR(D_, BQ_, BK_)                                            \
     if (D == D_ && BQ == BQ_ && BK == BK_ && NK == 4) return launch_fwd<D_, BQ_, BK_, 4, true>(p, s);

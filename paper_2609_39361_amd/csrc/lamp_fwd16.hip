@@ -33,6 +33,7 @@
 #include "lamp_device.h"
 #include "lamp_kernels.h"
 #include "lamp_loops.h"
+#include "lamp_sr.h"
 #include "lamp_stats.h"
 
 #ifndef LAMP_MIN_WAVES
@@ -47,8 +48,9 @@ namespace lamp {
 // cleared by lamp_phase_read.  Phases: 0 fused pass, 1 code and maxima
 // emission, 2 barrier B, 3 stage 1, 4 exponentials, 5 barrier E, 6 rescale
 // and stage 2, 7 P.V and the next speculative set, 8 barrier I, 9 prologue
-// and epilogue.
-#ifdef LAMP_PHASE_TIMER
+// and epilogue.  (Not in the stochastic-rounding instantiations, which are
+// compiled in a unit of their own, lamp_fwd16_sr.hip.)
+#if defined(LAMP_PHASE_TIMER) && !defined(LAMP_FWD16_NO_LAUNCHERS)
 __device__ unsigned long long phase_cycles[PHASE_N + 1];
 #define LAMP_PH_INIT                                                              \
     __shared__ uint32_t ph_lds[4 * PHASE_N];                                      \
@@ -72,6 +74,7 @@ __device__ unsigned long long phase_cycles[PHASE_N + 1];
 #define LAMP_PH_FLUSH ((void)0)
 #endif
 
+#ifndef LAMP_FWD16_NO_LAUNCHERS
 hipError_t phase_read(unsigned long long *host, bool reset)
 {
 #ifdef LAMP_PHASE_TIMER
@@ -87,6 +90,7 @@ hipError_t phase_read(unsigned long long *host, bool reset)
     return hipErrorNotSupported;
 #endif
 }
+#endif
 
 namespace {
 
@@ -206,7 +210,10 @@ __device__ __forceinline__ int wave_max_i32(int v)
 // "disruptive" tile) the others follow in a sequential 16-bit pass once the
 // 8-bit codes are stored.  A schedule only: the results are those of the safe
 // layout.
-template <int D, int BQ, int MODE, bool SIMP, bool OBS, bool CMP>
+// SR: the 8-bit logits rounded stochastically (lamp_sr.h, sr8_chunk_bc) with
+// the generator keyed by p.seed; they run after the fused pass, which then
+// carries the speculative 16-bit logits alone.
+template <int D, int BQ, int MODE, bool SIMP, bool OBS, bool CMP, bool SR = false>
 __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdParams p)
 {
     using C = Cfg16<D, BQ>;
@@ -264,12 +271,13 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     const bool stage1_off = (p.flags & LAMP_STAGE1_OFF) != 0u;   // flags are 0 outside the threshold mode
     const bool mu_trunc = (p.flags & LAMP_MU_TRUNC) != 0u;
 
-    int row[QPL], vlo[QPL], vhi[QPL];
+    int row[QPL], vlo[QPL], vhi[QPL], jq[QPL];
     const float *qrow[QPL];
 #pragma unroll
     for (int s = 0; s < QPL; ++s) {
         row[s] = s * 64 + lane;
         const int j = q0 + row[s];
+        jq[s] = j;
         vlo[s] = p.window > 0 ? (j - p.window + 1 > 0 ? j - p.window + 1 : 0) : 0;
         vhi[s] = p.causal ? j : p.N - 1;
         if (j >= p.N) {   // a row beyond N (partial last block): no visible key
@@ -576,7 +584,12 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
     if (mode != MODE_ALL16) {
         const bool done = own_emulated(t, act);
         uint32_t a8[QPL][8], sat[QPL];
-        if (done) emu8_any<D, QPL, SIMP, GrpLay>(qrow, kt32 + (size_t)(t * KPT + w * BK) * D, a8, sat);
+        if (done) {
+            if constexpr (SR)
+                sr8_chunk_bc<D, QPL, GrpLay>(qrow, kt32 + (size_t)(t * KPT + w * BK) * D, jq, (uint32_t)(t * KPT + w * BK),
+                                             (uint32_t)(b * p.Hq + h), p.seed, a8, sat);
+            else emu8_any<D, QPL, SIMP, GrpLay>(qrow, kt32 + (size_t)(t * KPT + w * BK) * D, a8, sat);
+        }
         emit8(t, a8, done, sat);
     }
     __syncthreads();
@@ -620,7 +633,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
             using T_ = std::true_type;
             using F_ = std::false_type;
             using std::integral_constant;
-            if (emu) {
+            if (emu && !SR) {
                 switch (nf) {
                 case 0: run(integral_constant<int, 0>(), T_()); break;
                 case 1: run(integral_constant<int, 4>(), T_()); break;
@@ -637,6 +650,10 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
                 default: run(integral_constant<int, 16>(), F_()); break;
                 }
             }
+            if constexpr (SR)
+                if (emu)
+                    sr8_chunk_bc<D, QPL, GrpLay>(qrow, k32e, jq, (uint32_t)(k0 + KPT + w * BK), (uint32_t)(b * p.Hq + h),
+                                                 p.seed, a8, sat8);
             LAMP_PH(0);
             if (has_next && mode != MODE_ALL16) emit8(t + 1, a8, emu, sat8);
             if constexpr (CMP) {
@@ -1370,6 +1387,7 @@ __global__ __launch_bounds__(256, LAMP_MIN_WAVES) void lamp_fwd16_kernel(FwdPara
 }
 
 // ------------------------------------------------------------------ launcher
+#ifndef LAMP_FWD16_NO_LAUNCHERS
 template <int D, int BQ, int MODE, bool SIMP, bool OBS, bool CMP = false>
 static hipError_t launch_fwd16_obs(const FwdParams &p, hipStream_t s)
 {
@@ -1422,5 +1440,7 @@ hipError_t dispatch_fwd16(int D, int BQ, const FwdParams &p, hipStream_t s, bool
     *found = false;
     return hipSuccess;
 }
+
+#endif // LAMP_FWD16_NO_LAUNCHERS
 
 } // namespace lamp

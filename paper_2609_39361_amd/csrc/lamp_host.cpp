@@ -411,7 +411,7 @@ static int fwd_impl(const uint16_t *q, const uint16_t *k, const uint16_t *v, int
         HIP_TRY(hipMemsetAsync(bad, 0, sizeof(unsigned), s));
     }
     HIP_TRY(lamp::launch_prepass(q, k, w.qt, w.kt32, B, Hq, Hkv, N, Nq, Nk, d, scale_of(d), s,
-                                 !use_sr && lamp::fwd_grouped(d, bq, bk, nk), bad));
+                                 lamp::fwd_grouped(d, bq, bk, nk), bad));
     HIP_TRY(lamp::launch_transpose_v(v, w.vt, B, Hkv, N, Nk, d, s, bad));
     if (check) {
         unsigned h_bad = 0;

@@ -83,6 +83,7 @@ hipError_t launch_decode(int D, const DecParams &p, hipStream_t s);
 hipError_t launch_prescale_q(const uint16_t *q, float *qt, int BH, int rows, int D, float scale, hipStream_t s);
 bool fwd_supported(int D, int BQ, int BK, int NK);
 hipError_t dispatch_fwd16(int D, int BQ, const FwdParams &p, hipStream_t s, bool *found);
+hipError_t dispatch_fwd16_sr(int D, int BQ, const FwdParams &p, hipStream_t s, bool *found);
 hipError_t dispatch_fwd(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found);
 // the general kernel with stochastically rounded 8-bit logits (row layout)
 hipError_t dispatch_fwd_sr(int D, int BQ, int BK, int NK, const FwdParams &p, hipStream_t s, bool *found);

@@ -68,10 +68,9 @@ def y8_tile(qt, kf, fmt="e4m3", sat=None):
 
 
 # ---- stochastic rounding of the 8-bit accumulation (Sec. 3.3's alternative
-# to round-to-nearest).  Written apart from the oracle: the random words come
-# from numpy's own Philox4x64-10 generator (which increments its counter
-# before each block, hence the counter minus one below), the e4m3 neighbours
-# from a search of the enumerated e4m3 magnitudes.
+# to round-to-nearest).  Written apart from the oracle: Philox4x32-10 on numpy
+# arrays of 64-bit integers (all counters of a tile at once), the e4m3
+# neighbours from a search of the enumerated e4m3 magnitudes.
 _E4M3_MAGS = None
 
 
@@ -87,34 +86,43 @@ def e4m3_mags():
     return _E4M3_MAGS
 
 
-def sr_words(seed, j, i, bh, g):
-    """The 4 words of Philox4x64-10 at counter (j, i, bh, g), key (seed, 0)."""
-    # numpy's generator adds one to the (256-bit) counter before producing a
-    # block: start it one below
-    n = (int(j) | int(i) << 64 | int(bh) << 128 | int(g) << 192) - 1
-    n %= 1 << 256
-    ctr = np.array([(n >> (64 * t)) & ((1 << 64) - 1) for t in range(4)], dtype=np.uint64)
-    gen = np.random.Philox(counter=ctr, key=np.array([seed, 0], dtype=np.uint64))
-    return gen.random_raw(4)
+def philox4x32(ctr, key, rounds=10):
+    """Philox4x32 (Salmon et al., SC 2011) of counters ctr [..., 4] under key
+    (k0, k1); numpy uint64 arithmetic, every word kept below 2^32."""
+    mask = np.uint64(0xFFFFFFFF)
+    x = [np.asarray(ctr[..., t], dtype=np.uint64) & mask for t in range(4)]
+    k0, k1 = np.uint64(key[0] & 0xFFFFFFFF), np.uint64(key[1] & 0xFFFFFFFF)
+    mul = (np.uint64(0xD2511F53), np.uint64(0xCD9E8D57))
+    weyl = (np.uint64(0x9E3779B9), np.uint64(0xBB67AE85))
+    for rnd in range(rounds):
+        if rnd:
+            k0, k1 = (k0 + weyl[0]) & mask, (k1 + weyl[1]) & mask
+        p0 = mul[0] * x[0]                      # < 2^64: exact in uint64
+        p1 = mul[1] * x[2]
+        x = [(p1 >> np.uint64(32)) ^ x[1] ^ k0, p1 & mask, (p0 >> np.uint64(32)) ^ x[3] ^ k1, p0 & mask]
+    return np.stack(x, axis=-1)
 
 
-def sr_r20(words, c):
-    """20-bit random integer of channel c from the words of its group of 12:
-    field (c mod 12) mod 3 (bits 0-19, 20-39, 40-59) of word (c mod 12) // 3."""
-    m = c % 12
-    return (int(words[m // 3]) >> (20 * (m % 3))) & 0xFFFFF
+def sr_r16(seed, j, i, bh, c):
+    """16-bit random integers of channel c for arrays of query rows j and keys
+    i: Philox4x32-10 at counter (j, i, bh, c // 8), key (seed mod 2^32,
+    seed // 2^32); the low (c even) or high (c odd) half of word (c mod 8) // 2."""
+    j, i = np.broadcast_arrays(np.asarray(j, dtype=np.uint64), np.asarray(i, dtype=np.uint64))
+    ctr = np.stack([j, i, np.full(j.shape, bh, dtype=np.uint64), np.full(j.shape, c // 8, dtype=np.uint64)], -1)
+    w = philox4x32(ctr, (seed & 0xFFFFFFFF, seed >> 32))[..., (c % 8) // 2]
+    return ((w >> np.uint64(16 * (c & 1))) & np.uint64(0xFFFF)).astype(np.float64)
 
 
 def sr_round(t, r):
-    """Stochastic rounding of fp64 values t (fp32 numbers) to e4m3, random integers r < 2^20."""
+    """Stochastic rounding of fp64 values t (fp32 numbers) to e4m3, random integers r < 2^16."""
     mags = e4m3_mags()
     a = np.minimum(np.abs(t), 448.0)
     idx = np.searchsorted(mags, a, side="right") - 1
     lo = mags[idx]
     hi = mags[np.minimum(idx + 1, mags.size - 1)]
     u = np.where(hi > lo, hi - lo, 1.0)
-    frac20 = np.floor((a - lo) / u * 2.0 ** 20)
-    res = np.where(frac20 + r >= 2.0 ** 20, hi, lo)
+    frac16 = np.floor((a - lo) / u * 2.0 ** 16)
+    res = np.where(frac16 + r >= 2.0 ** 16, hi, lo)
     return np.copysign(res, t)
 
 
@@ -122,21 +130,15 @@ def y8_tile_sr(qt, kf, seed, bh, rows, keys, sat=None):
     """Y8 values [T, bq] with stochastic rounding; rows / keys: the query and
     key indices of qt's rows and kf's rows.  sat: as in y8_tile (a step with
     |t| > 448)."""
-    T, bq, d = kf.shape[0], qt.shape[0], qt.shape[1]
-    r = np.zeros((d, T, bq))
-    for a, i in enumerate(keys):
-        for bb, j in enumerate(rows):
-            for g in range(-(-d // 12)):
-                wds = sr_words(seed, int(j), int(i), bh, g)
-                for c in range(12 * g, min(12 * g + 12, d)):
-                    r[c, a, bb] = sr_r20(wds, c)
-    acc = np.zeros((T, bq))
+    d = qt.shape[1]
+    ii, jj = np.meshgrid(np.asarray(keys), np.asarray(rows), indexing="ij")   # [T, bq]
+    acc = np.zeros((kf.shape[0], qt.shape[0]))
     for c in range(d):
         p = kf[:, c][:, None] * qt[:, c][None, :]          # exact in fp64
         t = rn32_sum(p, acc)
         if sat is not None:
             sat |= np.abs(t) > 448.0
-        acc = sr_round(t, r[c])
+        acc = sr_round(t, sr_r16(seed, jj, ii, bh, c))
     return acc
 
 

@@ -121,17 +121,17 @@ def test_fwd_sr_variants(L, w, flags):
 
 def test_fwd_sr_row_with_every_exponential_underflowing(L):
     """With the first stage off, mu_hat is the largest 8-bit logit; here
-    (seed 0, query row 100) a stochastically rounded 8-bit logit overshoots its
-    16-bit value by 36.6 (192 vs 155.375), the knapsack recomputes that
+    (seed 3, query row 123) a stochastically rounded 8-bit logit overshoots its
+    16-bit value by 31.9 (352 vs 320.125), the knapsack recomputes that
     sub-block and one other, and every 16-bit and remaining 8-bit exponential
     of the row underflows against mu_hat: omega = 0, so O is 0/0 (NaN) and
     lse is -inf, on both sides."""
     w = FWD_CASES[2]
     qd, kd, vd, *_ = _inputs(w)
-    err, mask = _compare(L, w, 0.5, flags=1, seed=0)
+    err, mask = _compare(L, w, 0.5, flags=1, seed=3)
     assert list(mask[0, 0, 1]) == [0, 2, 2, 0]
-    o, lse, _ = L.attn_fwd(qd, kd, vd, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, 0.5, flags=1, sr_seed=0)
-    assert lse[0, 0, 100].item() == -math.inf and torch.isnan(o[0, 0, 100]).all()
+    o, lse, _ = L.attn_fwd(qd, kd, vd, w.causal, w.window, w.bq, w.bk, w.nk, w.delta, 0.5, flags=1, sr_seed=3)
+    assert lse[0, 0, 123].item() == -math.inf and torch.isnan(o[0, 0, 123]).all()
 
 
 def test_fwd_sr_seed_changes_the_logits_not_the_all16_mode(L):

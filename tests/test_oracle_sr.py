@@ -3,19 +3,21 @@ alternative to round-to-nearest that Sec. 3.3 names against swamping).
 
 Readings (the paper fixes neither generator nor bit count): each FP32 FMA
 result is rounded to one of its two e4m3 neighbours, away from zero when
-floor(2^20 * distance to the lower one / spacing) + r >= 2^20 for a 20-bit
-uniform r, saturating at 448; r comes from Philox4x64-10 keyed by (seed, 0)
-at counter (query row, key, b*Hq + h, channel / 12): three 20-bit fields of
-each of the four output words, field (channel mod 12) mod 3 of word
-(channel mod 12) / 3.
+floor(2^16 * distance to the lower one / spacing) + r >= 2^16 for a 16-bit
+uniform r, saturating at 448; r comes from Philox4x32-10 keyed by (seed mod
+2^32, seed / 2^32) at counter (query row, key, b*Hq + h, channel / 8): the
+low (even channel) or high (odd channel) half of word (channel mod 8) / 2.
 
-Pinned by: numpy's own Philox4x64-10 (an independent implementation of the
-published generator); the rounding against the enumerated e4m3 grid and a
-second rounding written with a grid search (tests/refimpl.py); exact
-unbiasedness over all 2^20 random integers; the 8-bit logits and the whole
-forward pass against the independent implementation; a swamping example in
-which round-to-nearest loses every small term while the stochastic mean
-keeps the exact sum.
+Pinned by: the library routine rocRAND's Philox4x32-10 stream on the GPU machine
+(tests/test_gpu_rocrand.py: counter (n, 0, 0, 0), key = the seed's halves),
+and here by what any correct Philox4x32-10 has (every output bit balanced,
+the 16-bit fields uniform, one flipped counter or key bit flipping half the
+output bits) and a second implementation written apart (tests/refimpl.py);
+the rounding against the enumerated e4m3 grid and a second rounding written
+with a grid search; exact unbiasedness over all 2^16 random integers; the
+8-bit logits and the whole forward pass against the independent
+implementation; a swamping example in which round-to-nearest loses every
+small term while the stochastic mean keeps the exact sum.
 """
 import math
 
@@ -33,18 +35,62 @@ def mp_tables():
     return M.mp_exp_tables()
 
 
-@pytest.mark.parametrize("ctr,key", [
+PHILOX_CASES = [
+    ([0, 0, 0, 0], [0, 0]),
     ([1, 0, 0, 0], [0, 0]),
-    ([0, 0, 0, 0], [0, 0]),                          # counter carry in numpy's pre-increment
     ([5, 7, 9, 11], [0x1234, 0x5678]),
-    ([2 ** 64 - 1, 2 ** 64 - 1, 3, 0], [2 ** 64 - 1, 2 ** 64 - 1]),
-    ([123456789, 42, 31, 15], [0xDEADBEEFCAFEF00D, 0]),
-])
-def test_philox_matches_numpy(ctr, key):
-    n = (sum(c << (64 * t) for t, c in enumerate(ctr)) - 1) % (1 << 256)
-    start = np.array([(n >> (64 * t)) & ((1 << 64) - 1) for t in range(4)], dtype=np.uint64)
-    want = np.random.Philox(counter=start, key=np.array(key, dtype=np.uint64)).random_raw(4)
-    assert np.array_equal(O.philox4x64_10(ctr, key), want)
+    ([2 ** 32 - 1, 2 ** 32 - 1, 3, 0], [2 ** 32 - 1, 2 ** 32 - 1]),
+    ([123456789, 42, 31, 15], [0xCAFEF00D, 0xDEADBEEF]),
+]
+
+
+@pytest.mark.parametrize("ctr,key", PHILOX_CASES)
+def test_philox_matches_the_second_implementation(ctr, key):
+    got = O.philox4x32_10(ctr, key)
+    want = R.philox4x32(np.array(ctr, dtype=np.uint64), (key[0], key[1]))
+    assert np.array_equal(got.astype(np.uint64), want)
+
+
+def test_philox_output_statistics():
+    """Over 2^13 consecutive counters: each of the 128 output bits is set in
+    half the calls (within 5 standard deviations), the 16-bit fields are
+    uniform (chi-square over 16 bins of their top nibble), and flipping any
+    one of the 192 counter and key bits flips 64 of the 128 output bits on
+    average (within 4 of 64 over 64 random inputs per bit)."""
+    n = 1 << 13
+    ctr = np.zeros((n, 4), dtype=np.uint64)
+    ctr[:, 0] = np.arange(n)
+    ctr[:, 2] = 7
+    key = (0x9E3779B9, 0x243F6A88)
+    out = R.philox4x32(ctr, key)
+    for t in range(4):
+        c = np.array([O.philox4x32_10(ctr[t * 997], key)], dtype=np.uint64)
+        assert np.array_equal(c[0], out[t * 997])
+    bits = ((out[:, :, None] >> np.arange(32, dtype=np.uint64)) & np.uint64(1)).reshape(n, 128)
+    frac = bits.mean(axis=0)
+    assert np.all(np.abs(frac - 0.5) < 5 * 0.5 / np.sqrt(n))
+    fields = np.concatenate([out & np.uint64(0xFFFF), out >> np.uint64(16)]).ravel()
+    hist = np.bincount((fields >> np.uint64(12)).astype(np.int64), minlength=16)
+    expect = fields.size / 16
+    chi2 = ((hist - expect) ** 2 / expect).sum()
+    assert chi2 < 50.0                                  # 15 degrees of freedom: p ~ 1e-5
+    rng = np.random.default_rng(3)
+    base = rng.integers(0, 2 ** 32, (64, 4), dtype=np.uint64)
+    keys = rng.integers(0, 2 ** 32, (64, 2), dtype=np.uint64)
+    ref = np.stack([O.philox4x32_10(base[m], keys[m]) for m in range(64)]).astype(np.uint64)
+    def popcount(x):
+        return sum(((x >> np.uint64(b)) & np.uint64(1)) for b in range(32)).sum(axis=-1)
+    for bit in range(192):
+        flipped = []
+        for m in range(64):
+            c, k = base[m].copy(), keys[m].copy()
+            if bit < 128:
+                c[bit // 32] ^= np.uint64(1 << (bit % 32))
+            else:
+                k[(bit - 128) // 32] ^= np.uint64(1 << (bit % 32))
+            flipped.append(O.philox4x32_10(c, k).astype(np.uint64))
+        d = popcount(np.stack(flipped) ^ ref)
+        assert abs(d.mean() - 64.0) < 4.0, bit
 
 
 def _f32_values(rng, n):
@@ -58,7 +104,7 @@ def _f32_values(rng, n):
 def test_sr_picks_a_neighbour_on_the_grid():
     rng = np.random.default_rng(7)
     t = _f32_values(rng, 4000)
-    r = rng.integers(0, 1 << 20, t.size).astype(np.uint32)
+    r = rng.integers(0, 1 << 16, t.size).astype(np.uint32)
     y = O.sr_e4m3(t, r)
     mags = R.e4m3_mags()
     a = np.minimum(np.abs(t), 448.0)
@@ -71,26 +117,30 @@ def test_sr_picks_a_neighbour_on_the_grid():
     # r = 0 truncates toward zero; grid values and saturation are fixed points
     assert np.array_equal(np.abs(O.sr_e4m3(t, 0)), lo)
     on_grid = a == lo
-    for rr in (0, 1, 1 << 19, (1 << 20) - 1):
+    for rr in (0, 1, 1 << 15, (1 << 16) - 1):
         assert np.array_equal(np.abs(O.sr_e4m3(t, rr))[on_grid], lo[on_grid])
-    assert np.all(np.abs(O.sr_e4m3(t[np.abs(t) >= 448], (1 << 20) - 1)) == 448.0)
+    assert np.all(np.abs(O.sr_e4m3(t[np.abs(t) >= 448], (1 << 16) - 1)) == 448.0)
     # the independent rounding agrees everywhere
     assert np.array_equal(y, R.sr_round(t, r))
 
 
 def test_sr_is_unbiased_over_all_random_integers():
-    """Mean over r in [0, 2^20) equals t exactly where t is a multiple of
-    2^-20 of the e4m3 spacing (every normal-range FP32 value)."""
-    r = np.arange(1 << 20, dtype=np.uint32)
-    for t in (1.0 + 2 ** -23, 3.14159274101257324, 17.3, -200.123, 447.9, 0.0157, 2.0 ** -6 + 2 ** -29,
-              -(2.0 ** -7 + 2.0 ** -28)):
-        t = float(np.float32(t))
+    """Mean over r in [0, 2^16) equals t exactly where t is a multiple of
+    2^-16 of the e4m3 spacing (FP32 values whose 4 lowest of the 20 bits below
+    e4m3's last bit are zero), and the value with the distance cut to 16 bits
+    where it is not."""
+    r = np.arange(1 << 16, dtype=np.uint32)
+
+    def cut4(x):
+        b = np.float32(x).view(np.uint32) & np.uint32(0xFFFFFFF0)
+        return float(b.view(np.float32))
+    for t in (1.0 + 2 ** -19, cut4(3.14159274101257324), cut4(17.3), -cut4(200.123), cut4(447.9), cut4(0.0157),
+              2.0 ** -6 + 2 ** -25, -(2.0 ** -7 + 2.0 ** -25)):
         y = O.sr_e4m3(np.full(r.size, t), r)
         assert math.fsum(y) / r.size == t, t
-    # below 2^-9 x 2^-20 the probability is cut to 20 bits: the mean is the truncated value
-    t = float(np.float32(2.0 ** -7 + 2.0 ** -33))
-    y = O.sr_e4m3(np.full(r.size, t), r)
-    assert math.fsum(y) / r.size == 2.0 ** -7
+    for t, cut in ((1.0 + 2 ** -23, 1.0), (float(np.float32(2.0 ** -7 + 2.0 ** -30)), 2.0 ** -7)):
+        y = O.sr_e4m3(np.full(r.size, t), r)
+        assert math.fsum(y) / r.size == cut
 
 
 def _bits(w):

@@ -43,8 +43,8 @@ def test_oracle_under_sanitizers(tmp_path):
     assert "all calls clean" in out
 
 
-HOST_SOURCES = ["lamp_kernels.hip", "lamp_fwd.hip", "lamp_fwd16.hip", "lamp_decode.hip", "lamp_rates.hip",
-                "lamp_noalloc.hip", "lamp_host.cpp"]
+HOST_SOURCES = ["lamp_kernels.hip", "lamp_fwd.hip", "lamp_fwd16.hip", "lamp_fwd16_sr.hip", "lamp_decode.hip",
+                "lamp_rates.hip", "lamp_noalloc.hip", "lamp_host.cpp"]
 SAN = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined", "-Xarch_host",
        "-fno-sanitize-recover=all"]
 
