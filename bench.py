@@ -195,8 +195,9 @@ def cpu_baseline_decode(w, tau, q, k, v, budget_s=15.0, seed=0):
                 len(picked), nrows, spent)}
 
 
-def main_decode(args, w, tau):
-    """Bench line of the decode form (vector LAMP, Sec. 2, Eq. (6))."""
+def main_decode(args, w, tau, flags=0):
+    """Bench line of the decode form (vector LAMP, Sec. 2, Eq. (6)); flags: 0 (the key-chunk
+    pipeline) or lamp.DECODE_SERIAL."""
     import torch
     from paper_2609_39361_amd import lamp, workloads as W
     dev = torch.device("cuda:0")
@@ -208,7 +209,7 @@ def main_decode(args, w, tau):
     mask = torch.empty((w.B, w.Hq, w.M, -(-w.N // tk) * tk), dtype=torch.uint8, device=dev)
 
     def step():
-        lamp.attn_decode(qd, kd, vd, w.causal, w.window, tk, w.delta, tau, out=(o, lse, mask))
+        lamp.attn_decode(qd, kd, vd, w.causal, w.window, tk, w.delta, tau, out=(o, lse, mask), flags=flags)
 
     for _ in range(args.warmup):
         step()
@@ -238,6 +239,15 @@ def main_decode(args, w, tau):
     achieved = nbytes / (kernel_ms * 1e-3) / 1e9
     mac8 = 0 if tau == 0 else w.macs
     mac16 = (s1 + s2) * w.d
+    serial = flags == lamp.DECODE_SERIAL
+    md = _mode_of(tau)
+    rows = w.Hq // w.Hkv * w.M
+    if serial or rows > 8:
+        kernels = ["dec_logits_kernel<%d,%d>" % (w.d, md), "dec_lamp_kernel<%d,%d>" % (w.d, md),
+                   "dec_pv_kernel<%d,%d>" % (w.d, 4 if rows <= 4 else 8 if rows <= 8 else 16)]
+    else:
+        kernels = ["dec_stage_kernel<%d,%d,%d>" % (w.d, md, 4 if rows <= 4 else 8)]
+    kernels += ["dec_reduce_kernel<%d>" % w.d]
     result = {
         "metric": "effective attention TFLOP/s (4*d per visible (query, key) pair), decode form, 1 GPU",
         "value": w.eff_flops / (ms * 1e-3) / 1e12,
@@ -247,15 +257,15 @@ def main_decode(args, w, tau):
         "dtype": "e4m3/e4m11 emulated (fp32 FMA + fp8 conversions), bf16 cache, fp32 output",
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "M": w.M, "N": w.N, "d": w.d,
-                   "causal": w.causal, "window": w.window, "tk": tk, "delta": w.delta, "tau": tau},
+                   "causal": w.causal, "window": w.window, "tk": tk, "delta": w.delta, "tau": tau,
+                   "form": "serial" if serial else "pipelined"},
         "tokens_per_s": w.B * w.M / (ms * 1e-3),
         "recompute_fraction": (s1 + s2) / vis,
         "lookahead_recomputes": s1, "knapsack_recomputes": s2,
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-            "kernel": "dec_logits_kernel<%d,%d> + dec_lamp_kernel<%d,%d> + dec_pv_kernel<%d,4> + dec_reduce_kernel<%d>"
-                      % (w.d, _mode_of(tau), w.d, _mode_of(tau), w.d, w.d),
+            "kernel": " + ".join(kernels),
             "kernel_ms": kernel_ms, "prepass_ms": pre_ms_sum / launches,
             "bytes_per_launch": nbytes,
             "valu_frac_algorithmic": (OPS_PER_MAC8 * mac8 + OPS_PER_MAC16 * mac16) / (kernel_ms * 1e-3) / VALU_LANE_OPS,
@@ -303,10 +313,12 @@ def main():
     taus = [w.tau] if args.tau is None else [float(x) for x in args.tau.split(",")]
     flags_list = [int(x) for x in args.flags.split(",")]
     if w.M > 0:
-        if flags_list != [0] or args.sr_seed is not None:
-            raise SystemExit("the decode form takes no flags and no stochastic rounding")
-        for tau in taus:
-            main_decode(args, w, tau)
+        if any(f not in (0, lamp.DECODE_SERIAL) for f in flags_list) or args.sr_seed is not None:
+            raise SystemExit("the decode form takes flags 0 or %d (serial) and no stochastic rounding"
+                             % lamp.DECODE_SERIAL)
+        for flags in flags_list:
+            for tau in taus:
+                main_decode(args, w, tau, flags)
         return
     dev = torch.device("cuda:0")
     q, k, v = W.make_inputs(w)

@@ -316,14 +316,27 @@ int lamp_attn_fwd_sr(const uint16_t *q, const uint16_t *k, const uint16_t *v,
  * [B][Hq][M][ceil(N/tk)*tk] uint8, one code per key (0 8-bit, 1 the maximizer
  * recomputed by the look-ahead test -- every key at tau = 0 --, 2 recomputed
  * by the knapsack, 3 invisible).  Built: tk = 64, d in {64, 128, 256};
- * flags must be 0.  B = 0 or M = 0 returns LAMP_OK and writes nothing.  The
- * workspace (the pre-scaled queries, the 8-bit logit codes, the 16-bit
- * logits of the recomputed keys, per-tile mu_hat and rescale factors, partial
- * outputs:
+ * flags: 0 or LAMP_DECODE_SERIAL.  By default the keys from the first one
+ * any row sees are taken in up to 4 chunks of a multiple of 512 keys (one
+ * when there are at most 2048): the decisions visit the chunks in order,
+ * carrying each row's running maximum and sum, and with at most 8 query rows
+ * per key/value head the logits of chunk c + 1, the decisions of chunk c and
+ * P.V of chunk c - 1 run side by side in one launch.  B = 0 or M = 0 returns
+ * LAMP_OK and writes nothing.  The
+ * workspace (the 8-bit and 16-bit logit codes, per-tile mu_hat and rescale
+ * factors, partial outputs, the row state between key chunks:
  * lamp_attn_decode_workspace_size bytes) comes from extra->workspace or from
  * the library's per-device workspace, as for lamp_attn_fwd; extra->stats and
  * the dbg pointers must be NULL (LAMP_ERR_UNSUPPORTED).
  */
+/* Flags of lamp_attn_decode. */
+enum {
+    /* One key chunk and the three passes (logits, decisions, P.V) one after
+     * another, instead of the default pipeline of key chunks (below); the
+     * same masks and lse, O equal up to the order of its final sums. */
+    LAMP_DECODE_SERIAL = 256
+};
+
 int lamp_attn_decode(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                      int B, int Hq, int Hkv, int M, int N, int d,
                      int causal, int window, int tk, double delta, double tau, unsigned flags,

@@ -208,17 +208,25 @@ __device__ __forceinline__ void dec_staged(const uint16_t *kblk, int nvalid, uin
 #undef LAMP_P1_LOAD
 #undef LAMP_P1_STORE
 
+template <int D>
+struct LogitsLds {
+    uint16_t tile[256 * P1_PITCH];
+    float qs[4 * D];   // the group's 4 pre-scaled query rows
+};
+
+// Workgroup (bx, by) of the logit pass over the launch's key chunk: keys
+// ka + 256 bx .., row group by % ngroups of key/value head by / ngroups.
 template <int D, int MODE>
-__global__ __launch_bounds__(256) void dec_logits_kernel(DecParams p)
+__device__ __forceinline__ void dec_logits_role(const DecParams &p, LogitsLds<D> &sm, int bx, int by)
 {
-    __shared__ __align__(16) uint16_t tile[256 * P1_PITCH];
-    __shared__ __align__(16) float qs[4 * D];   // the group's 4 pre-scaled query rows
+    uint16_t *tile = sm.tile;
+    float *qs = sm.qs;
     const int G = p.Hq / p.Hkv;
     const int rows = G * p.M, ngroups = (rows + 3) / 4;
-    const int grp = (int)(blockIdx.y % (unsigned)ngroups);
-    const int bhk = (int)(blockIdx.y / (unsigned)ngroups);
+    const int grp = by % ngroups;
+    const int bhk = by / ngroups;
     const int b = bhk / p.Hkv, hk = bhk % p.Hkv;
-    const int key0 = p.kb0 + (int)blockIdx.x * 256;
+    const int key0 = p.ka + bx * 256;
     const int key = key0 + (int)threadIdx.x;
     const int nvalid = p.N - key0 < 256 ? p.N - key0 : 256;
     const uint16_t *kblk = p.k + (((size_t)b * p.Hkv + hk) * p.N + key0) * D;
@@ -230,7 +238,9 @@ __global__ __launch_bounds__(256) void dec_logits_kernel(DecParams p)
         const int h = hk * G + rho / p.M, r = rho % p.M;
         qrow[i] = ((size_t)b * p.Hq + h) * p.M + r;
     }
-    for (int x = (int)threadIdx.x; x < 4 * D; x += 256) qs[x] = p.qt[qrow[x / D] * D + x % D];
+    // the group's queries scaled in fp32 (the same product as the forward
+    // pass's prepass: bf16 value times RN32(1/sqrt(d)))
+    for (int x = (int)threadIdx.x; x < 4 * D; x += 256) qs[x] = bf16_value(p.q[qrow[x / D] * D + x % D]) * p.qscale;
     __syncthreads();
     uint32_t acc[2];
     float acc16[4];
@@ -241,7 +251,7 @@ __global__ __launch_bounds__(256) void dec_logits_kernel(DecParams p)
         float unused[4];
         dec_staged<D, MODE, true>(kblk, nvalid, tile, qs, acc, unused);
     }
-    if (key >= p.Np) return;
+    if (key >= p.Np || key >= p.kz) return;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int rho = grp * 4 + i;
@@ -263,92 +273,425 @@ __global__ __launch_bounds__(256) void dec_logits_kernel(DecParams p)
 }
 
 // ------------------------------------------------------------------ phase 2
-// The decisions, one wave per query row.  Nothing in the output feeds a
-// decision, so this kernel records only what the decisions fixed: per visited
-// tile mu_hat and the factor f_t = (prod of lambda_hat of the later tiles) /
-// omega that turns the tile's exponentials into the final weights of P.V
-// (O = sum_t f_t sum_{i in t} E_i v_i), both with the R = G*M query rows of a
-// key/value head interleaved (mu [b][hk][tile][rho], f likewise); and per
-// recomputed key its 16-bit logit and mask code (1 or 2).  The 8-bit logits'
-// mask codes (0, or 3 where invisible) were written with the codes by phase 1;
-// the all-16-bit mode writes every mask byte and 16-bit logit here.  P.V
-// recomputes each weight from these, with the same tables.
+// The decisions of one query row, one wave per row, lane i holding key i of a
+// tile.  Nothing in the output feeds a decision, so the decisions record only
+// what they fixed: per visited tile mu_hat and the factor f_t = (prod of
+// lambda_hat of the later tiles) / omega that turns the tile's exponentials
+// into the final weights of P.V (O = sum_t f_t sum_{i in t} E_i v_i), both
+// with the R = G*M query rows of a key/value head interleaved (mu
+// [b][hk][tile][rho], f likewise); and per recomputed key its mask code (1 or
+// 2), handed to a sink.  P.V recomputes each weight from the mask code, the
+// 8-bit or 16-bit logit code and mu_hat, with the same tables.
 //
-// The tile loop issues no global store (on gfx950 a wait for a load also
-// waits for every earlier store of the wave, so a store in the loop would
-// cost a store round trip at the next load): mu_hat and lambda_hat of 64
-// tiles at a time are held one per lane and written when the window is
-// complete, and the recomputed keys are collected in LDS and written at the
-// end of the row (or when the list is full).
+// No global store is issued per tile (on gfx950 a wait for a load also waits
+// for every earlier store of the wave, so a store in the tile loop would cost
+// a store round trip at the next load): mu_hat and lambda_hat of 64 tiles at
+// a time are held one per lane and written when the window is complete.
+template <int MODE>
+struct RowDecider {
+    const DecParams *p;
+    const uint16_t *lut;   // LDS: ue5m3 shift code -> bf16 bits of the exponential
+    const double *edk;     // LDS: the exp_doc constants
+    double *frow;          // lambda_hat, then the P.V factor, of this row's tiles (stride RR)
+    float *murow;          // mu_hat of this row's tiles (stride RR)
+    int64_t row;
+    int lane, vlo, vhi, t_begin, t_end, RR;
+    int tc_lo, tc_hi;      // this row's tiles in the launch's key chunk
+    int t_rec;             // the tile after the last one recorded
+    float mu;
+    double om;
+    float w_mu;            // mu_hat and lambda_hat of tile tc_lo + 64 wcur + lane
+    double w_lam;
+    int wcur;
+
+    __device__ __forceinline__ void start(const DecParams &pp, const uint16_t *lut_, const double *edk_, int64_t row_,
+                                          int lane_)
+    {
+        p = &pp;
+        lut = lut_;
+        edk = edk_;
+        lane = lane_;
+        row = row_;
+        const int r = (int)(row % pp.M);
+        const int h = (int)((row / pp.M) % pp.Hq);
+        const int b = (int)(row / ((int64_t)pp.M * pp.Hq));
+        const int G = pp.Hq / pp.Hkv, hk = h / G;
+        RR = G * pp.M;
+        const int rho = (h - hk * G) * pp.M + r;   // this row's slot among the rows of the head
+        const int P = pp.N - pp.M + r;              // the query's position
+        vlo = pp.window > 0 ? (P - pp.window + 1 > 0 ? P - pp.window + 1 : 0) : 0;
+        vhi = pp.causal ? P : pp.N - 1;
+        t_begin = vlo / TK;
+        t_end = vhi / TK;
+        tc_lo = t_begin > pp.ka / TK ? t_begin : pp.ka / TK;
+        tc_hi = t_end < pp.kz / TK - 1 ? t_end : pp.kz / TK - 1;
+        t_rec = tc_lo;
+        const int ntiles = pp.Np / TK;
+        frow = pp.f + ((size_t)b * pp.Hkv + hk) * (size_t)ntiles * RR + rho;
+        murow = pp.mut + ((size_t)b * pp.Hkv + hk) * (size_t)ntiles * RR + rho;
+        // the state the earlier chunks left (the first starts empty)
+        mu = pp.chunk > 0 ? pp.mu_st[row] : -__builtin_inff();
+        om = pp.chunk > 0 ? pp.om_st[row] : 0.0;
+        w_mu = 0.0f;
+        w_lam = 0.0;
+        wcur = 0;
+    }
+
+    __device__ __forceinline__ void flush_window()
+    {
+        const int tt = tc_lo + 64 * wcur + lane;
+        if (tt < t_rec) {
+            frow[(size_t)tt * RR] = w_lam;
+            murow[(size_t)tt * RR] = w_mu;
+        }
+    }
+
+    __device__ __forceinline__ void record_tile(int tt, float muh, double lam)
+    {
+        if ((tt - tc_lo) >> 6 != wcur) {
+            flush_window();
+            wcur = (tt - tc_lo) >> 6;
+        }
+        if (lane == ((tt - tc_lo) & 63)) {
+            w_mu = muh;
+            w_lam = lam;
+        }
+        t_rec = tt + 1;
+    }
+
+    __device__ __forceinline__ float e_of(float muh, float yy, bool high) const
+    {
+        if (high) {
+            const uint32_t hl = p->exp16hl[ue5m11_code(shift_of(muh, yy))];
+            return bf16_value(hl & 0xFFFFu) + bf16_value(hl >> 16);   // exact
+        }
+        return bf16_value(lut[ue5m3_code(shift_of(muh, yy))]);
+    }
+
+    // One tile exactly as the procedure states it: look-ahead test on the
+    // maximizer, exponentials, rescale, knapsack, update.  code: this lane's
+    // 8-bit logit code; y16_of(): this lane's 16-bit logit; sink(key, prec)
+    // is called by the lanes of the recomputed keys (mask code 1 or 2; in the
+    // threshold mode only).
+    template <class Y16, class Sink>
+    __device__ __forceinline__ void tile_exact(int t, uint32_t code, Y16 y16_of, Sink sink)
+    {
+        const float NEG_INF = -__builtin_inff();
+        const int key = t * TK + lane;
+        const bool vis = key >= vlo && key <= vhi;   // vhi < N
+        float y = NEG_INF;   // this key's logit in the precision chosen for it
+        uint8_t prec = vis ? 0 : 3;
+        bool have16 = false;
+        float y16 = 0.0f;
+        float muh;
+        if (MODE == MODE_ALL16) {
+            y16 = y16_of();
+            have16 = true;
+            y = vis ? y16 : NEG_INF;
+            prec = vis ? 1 : 3;
+            const float mx = wave_max_f32(y);
+            muh = mx > mu ? mx : mu;
+        } else {
+            y = vis ? e4m3_value(code) : NEG_INF;
+            const float mx = wave_max_f32(y);
+            if (MODE == MODE_PURE8) {
+                muh = mx > mu ? mx : mu;
+            } else {
+                const double m = (double)mu;
+                if (m > __builtin_fma(__builtin_fabs(m), p->delta, (double)mx)) {
+                    muh = mu;
+                } else {
+                    // the first lane holding the maximum; all visible lanes
+                    // compute their 16-bit logit (the issue cost of one lane's)
+                    const uint64_t at = __ballot(vis && y == mx);
+                    const int c = __builtin_ctzll(at);
+                    y16 = y16_of();
+                    have16 = true;
+                    const float yc = __shfl(y16, c, 64);
+                    muh = yc > mu ? yc : mu;
+                    if (lane == c) {
+                        y = y16;
+                        prec = 1;
+                    }
+                }
+            }
+        }
+        float e = vis ? e_of(muh, y, prec == 1) : 0.0f;
+        const double lam = mu == NEG_INF ? 0.0
+                         : (mu == muh ? 1.0 : exp_doc_k((double)mu - (double)muh, [&](int i) { return edk[i]; }));
+        const double S = wave_sum_f64((double)e);
+        const double omh = __builtin_fma(lam, om, S);
+        double S2 = S;
+        if (MODE == MODE_LAMP) {
+            const bool cand = prec == 0;
+            const double ec = cand ? (double)e : 0.0;
+            // quick acceptance of the empty recompute set: every cost is at
+            // most E omega_hat, and the fp64 sorted sum stays below
+            // omega_hat S_F (1 + 2^-45), so S_F <= tau omega_hat (1 - 2^-38)
+            // implies that the exact greedy keeps every logit.  S_F is bounded
+            // from an fp32 sum of its 64 non-negative terms (relative error
+            // below 2^-17).
+            const double SF = (double)wave_sum_f32(cand ? e : 0.0f) * (1.0 + 0x1p-17);
+            if (!(SF <= (p->tau * omh) * (1.0 - 0x1p-38))) {
+                const double tt = omh - ec;
+                double kap = cand ? ec * tt : __builtin_inf();
+                int idx = lane;
+                // bitonic sort of (cost, lane) ascending over the wave
+#pragma unroll
+                for (int k = 2; k <= 64; k <<= 1) {
+#pragma unroll
+                    for (int j = k >> 1; j >= 1; j >>= 1) {
+                        const double ok = __shfl_xor(kap, j, 64);
+                        const int oi = __shfl_xor(idx, j, 64);
+                        const bool mine_less = kap < ok || (kap == ok && idx < oi);
+                        const bool up = (lane & k) == 0;
+                        const bool lower = (lane & j) == 0;
+                        const bool keep = (lower == up) ? mine_less : !mine_less;
+                        if (!keep) {
+                            kap = ok;
+                            idx = oi;
+                        }
+                    }
+                }
+                // the greedy: sorted costs summed one at a time in fp64, in
+                // straight-line code on values read out of their lanes (the
+                // index of the first cost that is infinite or would pass the
+                // limit is the count kept; the sum after it is not used)
+                const double lim = (p->tau * omh) * omh;
+                double xi = 0.0;
+                int nkeep = 64;
+#pragma unroll
+                for (int i = 0; i < 64; ++i) {
+                    const double kk = readlane_f64(kap, i);
+                    const double nx = xi + kk;
+                    const bool ok = kk != __builtin_inf() && nx <= lim;
+                    nkeep = (nkeep == 64 && !ok) ? i : nkeep;
+                    xi = nx;
+                }
+                // sorted position -> key lane: each sorted slot sends its
+                // recompute flag to the lane of its key (idx is a permutation)
+                const int rflag = __builtin_amdgcn_ds_permute(idx << 2, (lane >= nkeep && kap != __builtin_inf()) ? 1 : 0);
+                const uint64_t rbits = __ballot(rflag != 0);
+                if (rbits) {
+                    if (!have16) {
+                        y16 = y16_of();
+                        have16 = true;
+                    }
+                    if (rbits >> lane & 1ull) {
+                        prec = 2;
+                        y = y16;
+                        e = e_of(muh, y, true);
+                    }
+                    S2 = wave_sum_f64((double)e);
+                }
+            }
+        }
+        om = __builtin_fma(lam, om, S2);
+        mu = muh;
+        record_tile(t, muh, lam);
+        if (MODE == MODE_LAMP) sink(key, prec, prec == 1 || prec == 2);
+    }
+
+    // Runs of tiles in which nothing changes precision.  Once mu is finite, a
+    // tile whose maximizer passes the look-ahead test against mu (pure 8-bit
+    // mode: whose maximum does not exceed mu) keeps mu_hat = mu and lambda_hat
+    // = 1, so its exponentials and sum depend on mu alone; the knapsack then
+    // keeps all its logits when the quick acceptance holds against omega_hat
+    // = omega + S.  Up to CH tiles are evaluated together on that assumption,
+    // 64/CH lanes per tile and CH keys per lane (CH reductions at once over
+    // groups of lanes); the omega chain is then replayed tile by tile in the
+    // same order and rounding as in tile_exact, and the tiles up to the first
+    // one where a test fails are committed.  Returns the number committed;
+    // the caller passes the next tile to tile_exact.  Every committed value
+    // equals what tile_exact would have produced: the maximum and the fp64
+    // sum of the exponentials are exact in any order, and the fp32 sum only
+    // feeds a bound that holds in any order (a tile the bound does not accept
+    // here goes through the exact path, whose greedy then decides).
+    // words(j, sub): the CH 8-bit codes of keys CH*sub .. CH*sub + CH-1 of
+    // tile t + j, one per byte (j < nt).
+    template <int CH, class Words>
+    __device__ __forceinline__ int run(int t, int nt, Words words)
+    {
+        static_assert(CH == 4 || CH == 8, "runs of 4 or 8 tiles");
+        constexpr int LPT = TK / CH;   // lanes per tile
+        const float NEG_INF = -__builtin_inff();
+        const int jl = lane / LPT, sub = lane % LPT;
+        const int tj = t + jl;
+        const bool in = jl < nt;
+        const uint64_t cw = in ? words(jl, sub) : 0ull;
+        const int key0 = tj * TK + CH * sub;
+        float mxl = NEG_INF, sf = 0.0f;
+        double sl = 0.0;
+#pragma unroll
+        for (int k = 0; k < CH; ++k) {
+            const int key = key0 + k;
+            const bool vis = in && key >= vlo && key <= vhi;
+            const uint8_t code = (uint8_t)(cw >> (8 * k));
+            const float y = vis ? e4m3_value(code) : NEG_INF;
+            mxl = y > mxl ? y : mxl;
+            const float e = vis ? bf16_value(lut[ue5m3_code(shift_of(mu, y))]) : 0.0f;
+            sl += (double)e;
+            sf += e;
+        }
+        // reductions over the lanes of each tile (quad neighbours, quad
+        // pairs, half-row mirror, and for 16 lanes the row mirror)
+        {
+            float o;
+            o = dpp_f32<0xB1>(mxl); mxl = o > mxl ? o : mxl;
+            o = dpp_f32<0x4E>(mxl); mxl = o > mxl ? o : mxl;
+            o = dpp_f32<0x141>(mxl); mxl = o > mxl ? o : mxl;
+            if (LPT == 16) { o = dpp_f32<0x140>(mxl); mxl = o > mxl ? o : mxl; }
+            sl += dpp_f64<0xB1>(sl);
+            sl += dpp_f64<0x4E>(sl);
+            sl += dpp_f64<0x141>(sl);
+            if (LPT == 16) sl += dpp_f64<0x140>(sl);
+            if (MODE == MODE_LAMP) {
+                sf += dpp_f32<0xB1>(sf);
+                sf += dpp_f32<0x4E>(sf);
+                sf += dpp_f32<0x141>(sf);
+                if (LPT == 16) sf += dpp_f32<0x140>(sf);
+            }
+        }
+        // the look-ahead test of every tile at once (lane LPT j holds tile j's
+        // maximum), then the omega chain and the quick acceptance tile by tile
+        // up to the first failure, without branches
+        const double m = (double)mu;
+        const bool passl = MODE == MODE_PURE8 ? !(mxl > mu) : m > __builtin_fma(__builtin_fabs(m), p->delta, (double)mxl);
+        constexpr uint64_t heads = LPT == 8 ? 0x0101010101010101ull : 0x0001000100010001ull;
+        const uint64_t fails = ~__ballot(passl) & heads & (nt < CH ? (1ull << (LPT * nt)) - 1ull : ~0ull);
+        int jc = fails ? __builtin_ctzll(fails) / LPT : nt;   // tiles committed
+        double omv = om;
+#pragma unroll
+        for (int j = 0; j < CH; ++j) {
+            const double omh = __builtin_fma(1.0, omv, readlane_f64(sl, LPT * j));
+            bool ok = true;
+            if (MODE == MODE_LAMP) {
+                const double SF = (double)readlane_f32(sf, LPT * j) * (1.0 + 0x1p-17);
+                ok = SF <= (p->tau * omh) * (1.0 - 0x1p-38);
+            }
+            jc = (j < jc && !ok) ? j : jc;
+            omv = j < jc ? omh : omv;
+        }
+        om = omv;
+#pragma unroll
+        for (int j = 0; j < CH; ++j)
+            if (j < jc) record_tile(t + j, mu, 1.0);
+        return jc;
+    }
+
+    // After the chunk's last tile: the outstanding window, the row state for
+    // the next chunk, and the P.V factors within the chunk, g_t = the product
+    // of lambda_hat over the chunk's later tiles, from its last tile backwards
+    // in runs of 64 (lane j: tile t_rec - 1 - 64c - j), with their product
+    // over the whole chunk (the reduction over the chunks scales each chunk's
+    // partial output by the product over the later chunks, divided by the
+    // final omega).  After the last chunk also lse.
+    __device__ __forceinline__ void finish(float *lse)
+    {
+        flush_window();
+        __threadfence_block();   // the rescale factors written above, read back by every lane below
+        double carry = 1.0;
+        for (int t0 = t_rec - 1; t0 >= tc_lo; t0 -= 64) {
+            const int tt = t0 - lane;
+            const double lam = tt >= tc_lo ? frow[(size_t)tt * RR] : 1.0;
+            double incl = lam;   // inclusive product over lanes 0..j
+#pragma unroll
+            for (int m = 1; m < 64; m <<= 1) {
+                const double o = __shfl_up(incl, m, 64);
+                if (lane >= m) incl *= o;
+            }
+            double excl = __shfl_up(incl, 1, 64);
+            if (lane == 0) excl = 1.0;
+            if (tt >= tc_lo) frow[(size_t)tt * RR] = carry * excl;
+            carry *= __shfl(incl, 63, 64);
+        }
+        if (lane == 0) {
+            p->lam_c[row * p->nchunks + p->chunk] = carry;
+            p->mu_st[row] = mu;
+            p->om_st[row] = om;
+            if (p->chunk == p->nchunks - 1) *lse = (float)((double)mu + ::log(om));
+        }
+    }
+};
+
+// The split form's decisions: one wave per query row over the codes phase 1
+// wrote.  The 8-bit logits' mask codes (0, or 3 where invisible) were written
+// with the codes by phase 1 (the all-16-bit mode: 1 where visible); this
+// kernel writes 3 over the tiles no key of which is visible and the codes of
+// the recomputed keys.  The recomputed keys are collected in LDS and written
+// at the end of the row (or when the list is full).
 constexpr int REC_CAP = 256;   // recomputed keys held in LDS per wave
 
+template <int MODE>
+struct DecideLds {
+    uint8_t cbuf[4][MODE != MODE_ALL16 ? 32 * TK : 1];    // per wave: rings of two
+    uint16_t hbuf[4][MODE != MODE_PURE8 ? 32 * TK : 1];   // blocks of 16 tiles' codes
+    int rec_key[4][MODE == MODE_LAMP ? REC_CAP : 1];
+    uint8_t rec_code[4][MODE == MODE_LAMP ? REC_CAP : 1];
+    uint16_t lut[256];
+    double edk[EXPDOC_NK];
+};
+
+// Workgroup bx of the decisions over the launch's key chunk: query rows
+// 4 bx .. 4 bx + 3, one wave each.
 template <int D, int MODE>
-__global__ __launch_bounds__(256) void dec_lamp_kernel(DecParams p)
+__device__ __forceinline__ void dec_decide_role(const DecParams &p, DecideLds<MODE> &sm, int bx)
 {
-    __shared__ uint16_t lut[256];
-    __shared__ double edk[EXPDOC_NK];
-    __shared__ __align__(16) uint8_t cbuf[4][MODE != MODE_ALL16 ? 32 * TK : 1];     // per wave: rings of two
-    __shared__ __align__(16) uint16_t hbuf[4][MODE != MODE_PURE8 ? 32 * TK : 1];    // blocks of 16 tiles' codes
-    __shared__ int rec_key[4][MODE == MODE_LAMP ? REC_CAP : 1];
-    __shared__ uint8_t rec_code[4][MODE == MODE_LAMP ? REC_CAP : 1];
+    uint16_t *lut = sm.lut;
+    double *edk = sm.edk;
+    auto &cbuf = sm.cbuf;
+    auto &hbuf = sm.hbuf;
+    auto &rec_key = sm.rec_key;
+    auto &rec_code = sm.rec_code;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     for (int i = tid; i < 256; i += 256) lut[i] = p.lut8e[i];
     if (tid < EXPDOC_NK) edk[tid] = EXPDOC_K[tid];
     __syncthreads();
 
     const int64_t nrows = (int64_t)p.B * p.Hq * p.M;
-    const int64_t row = (int64_t)blockIdx.x * 4 + wv;
+    const int64_t row = (int64_t)bx * 4 + wv;
     if (row >= nrows) return;   // whole wave
-    const int r = (int)(row % p.M);
-    const int h = (int)((row / p.M) % p.Hq);
-    const int b = (int)(row / ((int64_t)p.M * p.Hq));
-    const int G = p.Hq / p.Hkv, hk = h / G;
-    const int RR = G * p.M, rho = (h - hk * G) * p.M + r;   // rows of the head, this row's slot
-    const int P = p.N - p.M + r;   // the query's position
-    const int vlo = p.window > 0 ? (P - p.window + 1 > 0 ? P - p.window + 1 : 0) : 0;
-    const int vhi = p.causal ? P : p.N - 1;
-    const int t_begin = vlo / TK, t_end = vhi / TK;
+    // the decisions are bound by the latency of their dependent chains: a
+    // higher wave priority lets them issue as soon as they are ready beside
+    // the other key chunks' logit and P.V workgroups
+    __builtin_amdgcn_s_setprio(2);
+    RowDecider<MODE> d;
+    d.start(p, lut, edk, row, lane);
+    // this launch's tiles of the row (t_begin, t_end: the chunk's part of the
+    // visible range)
+    const int t_begin = d.tc_lo, t_end = d.tc_hi;
     const int ntiles = p.Np / TK;
     const uint8_t *y8row = p.y8 + row * (size_t)p.Np;
     const uint16_t *y16row = p.y16 + row * (size_t)p.Np;
-    double *frow = p.f + ((size_t)b * p.Hkv + hk) * (size_t)ntiles * RR + rho;   // stride RR per tile
-    float *murow = p.mut + ((size_t)b * p.Hkv + hk) * (size_t)ntiles * RR + rho;  // stride RR per tile
     uint8_t *mrow = p.mask + row * (size_t)p.Np;
-    const float NEG_INF = -__builtin_inff();
-    float mu = NEG_INF;
-    double om = 0.0;
 
-    // tiles without a visible key (phase 1 wrote the same code for those it covers)
-    for (int t = lane; t < ntiles; t += 64)
-        if (t < t_begin || t > t_end)
-            for (int i = 0; i < TK; ++i) mrow[t * TK + i] = 3;
+    // the chunk's tiles without a visible key (phase 1 wrote the same code
+    // for those it covers; the first chunk also covers the keys before kb0)
+    {
+        const int lo = p.chunk == 0 ? 0 : p.ka / TK, hi = p.chunk == p.nchunks - 1 ? ntiles : p.kz / TK;
+        for (int t = lo + lane; t < hi; t += 64)
+            if (t < d.t_begin || t > d.t_end)
+                for (int i = 0; i < TK; ++i) mrow[t * TK + i] = 3;
+    }
 
-    // mu_hat and lambda_hat of the tiles t_begin + 64 wcur + lane
-    float w_mu = 0.0f;
-    double w_lam = 0.0;
-    int wcur = 0;
-    auto flush_window = [&]() {
-        const int tt = t_begin + 64 * wcur + lane;
-        if (tt <= t_end) {
-            frow[(size_t)tt * RR] = w_lam;
-            murow[(size_t)tt * RR] = w_mu;
-        }
-    };
-    auto record_tile = [&](int tt, float muh, double lam) {
-        if ((tt - t_begin) >> 6 != wcur) {
-            flush_window();
-            wcur = (tt - t_begin) >> 6;
-        }
-        if (lane == ((tt - t_begin) & 63)) {
-            w_mu = muh;
-            w_lam = lam;
-        }
-    };
     // recomputed keys of this row (LDS list)
     int nrec = 0;
     auto flush_rec = [&]() {
         for (int i = lane; i < nrec; i += 64) mrow[rec_key[wv][i]] = rec_code[wv][i];
         nrec = 0;
+    };
+    auto sink = [&](int key, uint8_t prec, bool recd) {
+        const uint64_t rb = __ballot(recd);
+        if (rb) {
+            if (nrec + 64 > REC_CAP) flush_rec();
+            if (recd) {
+                const int pos = nrec + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(rb >> 32),
+                                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)rb, 0u));
+                rec_key[wv][pos] = key;
+                rec_code[wv][pos] = prec;
+            }
+            nrec += __builtin_popcountll(rb);
+        }
     };
 
     // The logit codes arrive 16 tiles (a block) at a time: per lane keys
@@ -384,259 +727,33 @@ __global__ __launch_bounds__(256) void dec_lamp_kernel(DecParams p)
             load_block(kn);
         }
     };
-    auto code_of = [&](int t) -> uint8_t { return cb[((t - t_begin) & 31) * TK + lane]; };
-    auto y16_of = [&](int t) -> float { return e4m11_value(hb[((t - t_begin) & 31) * TK + lane]); };
-
-    // One tile exactly as the procedure states it: look-ahead test on the
-    // maximizer, exponentials, rescale, knapsack, update.
-    auto tile_exact = [&](int t) {
-        const int key = t * TK + lane;
-        const bool vis = key >= vlo && key <= vhi;   // vhi < N
-        const uint8_t code = MODE != MODE_ALL16 ? code_of(t) : (uint8_t)0;
-        float y = NEG_INF;   // this key's logit in the precision chosen for it
-        uint8_t prec = vis ? 0 : 3;
-        bool have16 = false;
-        float y16 = 0.0f;
-        float muh;
-        if (MODE == MODE_ALL16) {
-            y16 = y16_of(t);
-            have16 = true;
-            y = vis ? y16 : NEG_INF;
-            prec = vis ? 1 : 3;
-            const float mx = wave_max_f32(y);
-            muh = mx > mu ? mx : mu;
-        } else {
-            y = vis ? e4m3_value(code) : NEG_INF;
-            const float mx = wave_max_f32(y);
-            if (MODE == MODE_PURE8) {
-                muh = mx > mu ? mx : mu;
-            } else {
-                const double m = (double)mu;
-                if (m > __builtin_fma(__builtin_fabs(m), p.delta, (double)mx)) {
-                    muh = mu;
-                } else {
-                    // the first lane holding the maximum; all visible lanes
-                    // compute their 16-bit logit (the issue cost of one lane's)
-                    const uint64_t at = __ballot(vis && y == mx);
-                    const int c = __builtin_ctzll(at);
-                    y16 = y16_of(t);
-                    have16 = true;
-                    const float yc = __shfl(y16, c, 64);
-                    muh = yc > mu ? yc : mu;
-                    if (lane == c) {
-                        y = y16;
-                        prec = 1;
-                    }
-                }
-            }
-        }
-        auto e_of = [&](float yy, bool high) -> float {
-            if (high) {
-                const uint32_t hl = p.exp16hl[ue5m11_code(shift_of(muh, yy))];
-                return bf16_value(hl & 0xFFFFu) + bf16_value(hl >> 16);   // exact
-            }
-            return bf16_value(lut[ue5m3_code(shift_of(muh, yy))]);
-        };
-        float e = vis ? e_of(y, prec == 1) : 0.0f;
-        const double lam = mu == NEG_INF ? 0.0
-                         : (mu == muh ? 1.0 : exp_doc_k((double)mu - (double)muh, [&](int i) { return edk[i]; }));
-        const double S = wave_sum_f64((double)e);
-        const double omh = __builtin_fma(lam, om, S);
-        double S2 = S;
-        if (MODE == MODE_LAMP) {
-            const bool cand = prec == 0;
-            const double ec = cand ? (double)e : 0.0;
-            // quick acceptance of the empty recompute set: every cost is at
-            // most E omega_hat, and the fp64 sorted sum stays below
-            // omega_hat S_F (1 + 2^-45), so S_F <= tau omega_hat (1 - 2^-38)
-            // implies that the exact greedy keeps every logit.  S_F is bounded
-            // from an fp32 sum of its 64 non-negative terms (relative error
-            // below 2^-17).
-            const double SF = (double)wave_sum_f32(cand ? e : 0.0f) * (1.0 + 0x1p-17);
-            if (!(SF <= (p.tau * omh) * (1.0 - 0x1p-38))) {
-                const double tt = omh - ec;
-                double kap = cand ? ec * tt : __builtin_inf();
-                int idx = lane;
-                // bitonic sort of (cost, lane) ascending over the wave
-#pragma unroll
-                for (int k = 2; k <= 64; k <<= 1) {
-#pragma unroll
-                    for (int j = k >> 1; j >= 1; j >>= 1) {
-                        const double ok = __shfl_xor(kap, j, 64);
-                        const int oi = __shfl_xor(idx, j, 64);
-                        const bool mine_less = kap < ok || (kap == ok && idx < oi);
-                        const bool up = (lane & k) == 0;
-                        const bool lower = (lane & j) == 0;
-                        const bool keep = (lower == up) ? mine_less : !mine_less;
-                        if (!keep) {
-                            kap = ok;
-                            idx = oi;
-                        }
-                    }
-                }
-                // the greedy: sorted costs summed one at a time in fp64, in
-                // straight-line code on values read out of their lanes (the
-                // index of the first cost that is infinite or would pass the
-                // limit is the count kept; the sum after it is not used)
-                const double lim = (p.tau * omh) * omh;
-                double xi = 0.0;
-                int nkeep = 64;
-#pragma unroll
-                for (int i = 0; i < 64; ++i) {
-                    const double kk = readlane_f64(kap, i);
-                    const double nx = xi + kk;
-                    const bool ok = kk != __builtin_inf() && nx <= lim;
-                    nkeep = (nkeep == 64 && !ok) ? i : nkeep;
-                    xi = nx;
-                }
-                // sorted position -> key lane: each sorted slot sends its
-                // recompute flag to the lane of its key (idx is a permutation)
-                const int rflag = __builtin_amdgcn_ds_permute(idx << 2, (lane >= nkeep && kap != __builtin_inf()) ? 1 : 0);
-                const uint64_t rbits = __ballot(rflag != 0);
-                if (rbits) {
-                    if (!have16) {
-                        y16 = y16_of(t);
-                        have16 = true;
-                    }
-                    if (rbits >> lane & 1ull) {
-                        prec = 2;
-                        y = y16;
-                        e = e_of(y, true);
-                    }
-                    S2 = wave_sum_f64((double)e);
-                }
-            }
-        }
-        om = __builtin_fma(lam, om, S2);
-        mu = muh;
-        record_tile(t, muh, lam);
-        if (MODE == MODE_LAMP) {
-            const bool recd = prec == 1 || prec == 2;
-            const uint64_t rb = __ballot(recd);
-            if (rb) {
-                if (nrec + 64 > REC_CAP) flush_rec();
-                if (recd) {
-                    const int pos = nrec + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(rb >> 32),
-                                                                          __builtin_amdgcn_mbcnt_lo((uint32_t)rb, 0u));
-                    rec_key[wv][pos] = key;
-                    rec_code[wv][pos] = prec;
-                }
-                nrec += __builtin_popcountll(rb);
-            }
-        }
+    auto exact = [&](int t) {
+        const uint32_t code = MODE != MODE_ALL16 ? cb[((t - t_begin) & 31) * TK + lane] : 0u;
+        d.tile_exact(t, code, [&]() { return e4m11_value(hb[((t - t_begin) & 31) * TK + lane]); }, sink);
     };
-
-    // Runs of tiles in which nothing changes precision.  Once mu is finite,
-    // a tile whose maximizer passes the look-ahead test against mu (pure
-    // 8-bit mode: whose maximum does not exceed mu) keeps mu_hat = mu and
-    // lambda_hat = 1, so its exponentials and sum depend on mu alone; the
-    // knapsack then keeps all its logits when the quick acceptance holds
-    // against omega_hat = omega + S.  Up to CH = 8 tiles are evaluated
-    // together on that assumption, 8 lanes per tile and 8 keys per lane
-    // (eight reductions at once over groups of 8 lanes); the omega chain is
-    // then replayed tile by tile in the same order and rounding as above, and
-    // the tiles up to the first one where a test fails are committed; that
-    // tile goes through tile_exact.  Every committed value equals what
-    // tile_exact would have produced: the maximum and the fp64 sum of the
-    // exponentials are exact in any order, and the fp32 sum only feeds a
-    // bound that holds in any order (a tile the bound does not accept here
-    // goes through the exact path, whose greedy then decides).
     constexpr int CH = 8;
-    const int jl = lane >> 3, sub = lane & 7;   // this lane's tile of the run, its 8 keys
     int t = t_begin;
     while (t <= t_end) {
-        if (MODE == MODE_ALL16 || mu == NEG_INF) {
+        if (MODE == MODE_ALL16 || d.mu == -__builtin_inff()) {
             ensure(t);
-            tile_exact(t);
+            exact(t);
             ++t;
             continue;
         }
         const int nt = t_end - t + 1 < CH ? t_end - t + 1 : CH;
         ensure(t + nt - 1);
-        const int tj = t + jl;
-        const bool in = jl < nt;
-        const uint2 cw = in ? *reinterpret_cast<const uint2 *>(cb + ((tj - t_begin) & 31) * TK + 8 * sub)
-                            : make_uint2(0u, 0u);
-        const int key0 = tj * TK + 8 * sub;
-        float mxl = NEG_INF, sf = 0.0f;
-        double sl = 0.0;
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int key = key0 + k;
-            const bool vis = in && key >= vlo && key <= vhi;
-            const uint8_t code = (uint8_t)((k < 4 ? cw.x : cw.y) >> (8 * (k & 3)));
-            const float y = vis ? e4m3_value(code) : NEG_INF;
-            mxl = y > mxl ? y : mxl;
-            const float e = vis ? bf16_value(lut[ue5m3_code(shift_of(mu, y))]) : 0.0f;
-            sl += (double)e;
-            sf += e;
-        }
-        // reductions over the 8 lanes of each tile (quad neighbours, quad
-        // pairs, half-row mirror)
-        {
-            float o;
-            o = dpp_f32<0xB1>(mxl); mxl = o > mxl ? o : mxl;
-            o = dpp_f32<0x4E>(mxl); mxl = o > mxl ? o : mxl;
-            o = dpp_f32<0x141>(mxl); mxl = o > mxl ? o : mxl;
-            sl += dpp_f64<0xB1>(sl);
-            sl += dpp_f64<0x4E>(sl);
-            sl += dpp_f64<0x141>(sl);
-            if (MODE == MODE_LAMP) {
-                sf += dpp_f32<0xB1>(sf);
-                sf += dpp_f32<0x4E>(sf);
-                sf += dpp_f32<0x141>(sf);
-            }
-        }
-        // the look-ahead test of every tile at once (lane 8j holds tile j's
-        // maximum), then the omega chain and the quick acceptance tile by tile
-        // up to the first failure, without branches
-        const double m = (double)mu;
-        const bool passl = MODE == MODE_PURE8 ? !(mxl > mu) : m > __builtin_fma(__builtin_fabs(m), p.delta, (double)mxl);
-        const uint64_t fails = ~__ballot(passl) & 0x0101010101010101ull & (nt < CH ? (1ull << (8 * nt)) - 1ull : ~0ull);
-        int jc = fails ? __builtin_ctzll(fails) >> 3 : nt;   // tiles committed
-        double omv = om;
-#pragma unroll
-        for (int j = 0; j < CH; ++j) {
-            const double omh = __builtin_fma(1.0, omv, readlane_f64(sl, 8 * j));
-            bool ok = true;
-            if (MODE == MODE_LAMP) {
-                const double SF = (double)readlane_f32(sf, 8 * j) * (1.0 + 0x1p-17);
-                ok = SF <= (p.tau * omh) * (1.0 - 0x1p-38);
-            }
-            jc = (j < jc && !ok) ? j : jc;
-            omv = j < jc ? omh : omv;
-        }
-        om = omv;
-#pragma unroll
-        for (int j = 0; j < CH; ++j)
-            if (j < jc) record_tile(t + j, mu, 1.0);
+        const int jc = d.template run<CH>(t, nt, [&](int j, int sub) -> uint64_t {
+            const uint2 w = *reinterpret_cast<const uint2 *>(cb + ((t + j - t_begin) & 31) * TK + CH * sub);
+            return ((uint64_t)w.y << 32) | w.x;
+        });
         t += jc;
         if (jc < nt) {
-            tile_exact(t);
+            exact(t);
             ++t;
         }
     }
-    flush_window();
     if (MODE == MODE_LAMP) flush_rec();
-    if (lane == 0) p.lse[row] = (float)((double)mu + ::log(om));
-    __threadfence_block();   // the rescale factors written above, read back by every lane below
-    // f_t = (prod over the later visited tiles of lambda_hat) / omega, from the
-    // last tile backwards in chunks of 64 (lane j: tile t_end - 64c - j)
-    double carry = 1.0 / om;
-    for (int t0 = t_end; t0 >= t_begin; t0 -= 64) {
-        const int tt = t0 - lane;
-        const double lam = tt >= t_begin ? frow[(size_t)tt * RR] : 1.0;
-        double incl = lam;   // inclusive product over lanes 0..j
-#pragma unroll
-        for (int m = 1; m < 64; m <<= 1) {
-            const double o = __shfl_up(incl, m, 64);
-            if (lane >= m) incl *= o;
-        }
-        double excl = __shfl_up(incl, 1, 64);
-        if (lane == 0) excl = 1.0;
-        if (tt >= t_begin) frow[(size_t)tt * RR] = carry * excl;
-        carry *= __shfl(incl, 63, 64);
-    }
+    d.finish(p.lse + row);
 }
 
 // ------------------------------------------------------------------ phase 3
@@ -653,21 +770,31 @@ __global__ __launch_bounds__(256) void dec_lamp_kernel(DecParams p)
 constexpr int PV_CHUNK = 512, PV_ROWS = 16;
 
 template <int D, int NR>
-__global__ __launch_bounds__(256) void dec_pv_kernel(DecParams p, int rg0)
+struct PvLds {
+    float wl[PV_CHUNK][NR];
+    float red[4][NR][D];
+    uint16_t lut[256];
+};
+
+// Workgroup (bx, by) of P.V over the launch's key chunk: keys ka + 512 bx ..,
+// key/value head by, its query rows rg0 .. rg0 + NR - 1.
+template <int D, int NR>
+__device__ __forceinline__ void dec_pv_role(const DecParams &p, PvLds<D, NR> &sm, int bx, int by, int rg0)
 {
     constexpr int CC = D / 8, KG = 256 / CC;   // channel chunks; keys per step over the workgroup
-    __shared__ __align__(16) float wl[PV_CHUNK][NR];
-    __shared__ float red[4][NR][D];
-    __shared__ uint16_t lut[256];
+    auto &wl = sm.wl;
+    auto &red = sm.red;
+    uint16_t *lut = sm.lut;
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
     const int cc = tid % CC, kg = tid / CC;
-    const int chunk = (int)blockIdx.x;
-    const int bhk = (int)blockIdx.y;
+    const int chunk = bx;
+    const int bhk = by;
     const int b = bhk / p.Hkv, hk = bhk % p.Hkv;
     const int G = p.Hq / p.Hkv, RR = G * p.M;
     const int ntiles = p.Np / TK;
-    const int k0 = p.kb0 + chunk * PV_CHUNK;
+    const int k0 = p.ka + chunk * PV_CHUNK;
     const int k_end = k0 + PV_CHUNK < p.N ? k0 + PV_CHUNK : p.N;
+    const int pvc = (k0 - p.kb0) / PV_CHUNK;   // this piece among the call's
     for (int i = tid; i < 256; i += 256) lut[i] = p.lut8e[i];
     // U keys of V per step and lane (8 channels each), the first step's loads
     // issued before the weights are formed and every later step's one step
@@ -771,65 +898,220 @@ __global__ __launch_bounds__(256) void dec_pv_kernel(DecParams p, int rg0)
         if (rho >= RR) continue;
         const float v = red[0][i][c] + red[1][i][c] + red[2][i][c] + red[3][i][c];
         const int64_t rid = ((int64_t)b * p.Hq + hk * G + rho / p.M) * p.M + rho % p.M;
-        p.part[((size_t)rid * nch + chunk) * D + c] = v;
+        p.part[((size_t)rid * nch + pvc) * D + c] = v;
+    }
+}
+
+// ------------------------------------------------------------------ kernels
+template <int D, int MODE>
+__global__ __launch_bounds__(256) void dec_logits_kernel(DecParams p)
+{
+    __shared__ __align__(16) LogitsLds<D> sm;
+    dec_logits_role<D, MODE>(p, sm, (int)blockIdx.x, (int)blockIdx.y);
+}
+
+template <int D, int MODE>
+__global__ __launch_bounds__(256) void dec_lamp_kernel(DecParams p)
+{
+    __shared__ __align__(16) DecideLds<MODE> sm;
+    dec_decide_role<D, MODE>(p, sm, (int)blockIdx.x);
+}
+
+template <int D, int NR>
+__global__ __launch_bounds__(256) void dec_pv_kernel(DecParams p, int rg0)
+{
+    __shared__ __align__(16) PvLds<D, NR> sm;
+    dec_pv_role<D, NR>(p, sm, (int)blockIdx.x, (int)blockIdx.y, rg0);
+}
+
+// One stage of the key-chunk pipeline: the decisions of chunk c - 1, the
+// logits of chunk c and P.V of chunk c - 2 in one launch (each part may be
+// empty; pd, pl, pp carry the chunks).  Stages run in order on one stream, so
+// every part finds what it reads complete; within a stage the three overlap:
+// the decisions (bound by the latency of their reductions, at a higher wave
+// priority) take the first nd workgroups, then the logit workgroups (bound by
+// the VALU) and the P.V ones (bound by HBM) are interleaved in proportion.
+// The workgroups share one LDS buffer laid out per part.
+template <int D, int MODE, int NR>
+__global__ __launch_bounds__(256) void dec_stage_kernel(DecParams pd, DecParams pl, DecParams pp, int nd, int nl_x,
+                                                        int nl, int np_x, int np)
+{
+    constexpr size_t A = sizeof(LogitsLds<D>), B = sizeof(DecideLds<MODE>), C = sizeof(PvLds<D, NR>);
+    constexpr size_t AB = A > B ? A : B, ABC = AB > C ? AB : C;
+    __shared__ __align__(16) unsigned char buf[ABC];
+    const int bid = (int)blockIdx.x;
+    if (bid < nd) {
+        dec_decide_role<D, MODE>(pd, *reinterpret_cast<DecideLds<MODE> *>(buf), bid);
+        return;
+    }
+    // the r-th of the other workgroups: logits when floor((r + 1) nl / T)
+    // passes floor(r nl / T) (their index), P.V otherwise
+    const int64_t r = bid - nd, T = (int64_t)nl + np;
+    const int64_t il = r * nl / T;
+    if ((r + 1) * nl / T > il) {
+        dec_logits_role<D, MODE>(pl, *reinterpret_cast<LogitsLds<D> *>(buf), (int)(il % nl_x), (int)(il / nl_x));
+    } else {
+        const int64_t ip = r - il;
+        const int per = np_x * pp.B * pp.Hkv;   // workgroups per group of NR rows
+        const int rg = (int)(ip / per), rem = (int)(ip % per);
+        dec_pv_role<D, NR>(pp, *reinterpret_cast<PvLds<D, NR> *>(buf), rem % np_x, rem / np_x, rg * NR);
     }
 }
 
 // ------------------------------------------------------------------ phase 4
-// O = sum over the key chunks of the partial outputs.
+// O = sum over the key chunks c of F_c times the sum of chunk c's partial
+// outputs, F_c = (product of the later chunks' lambda_hat products) / omega.
+// Thread x: channels 4 (x % (D/4)) .. + 3 of row x / (D/4), the pieces of a
+// chunk read four at a time.
 template <int D>
 __global__ __launch_bounds__(256) void dec_reduce_kernel(DecParams p)
 {
+    constexpr int Q = D / 4;
     const int64_t nrows = (int64_t)p.B * p.Hq * p.M;
-    const int nch = (p.N - p.kb0 + PV_CHUNK - 1) / PV_CHUNK;
+    const int nch = (p.N - p.kb0 + PV_CHUNK - 1) / PV_CHUNK, per = p.ck / PV_CHUNK;
     const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (x >= nrows * D) return;
-    const int64_t row = x / D;
-    const int c = (int)(x % D);
-    float s = 0.0f;
-    for (int ch = 0; ch < nch; ++ch) s += p.part[(row * nch + ch) * D + c];
-    p.o[x] = s;
+    if (x >= nrows * Q) return;
+    const int64_t row = x / Q;
+    const int c4 = (int)(x % Q) * 4;
+    const float4 *part = reinterpret_cast<const float4 *>(p.part + row * nch * D + c4);
+    double fc = 1.0 / p.om_st[row];
+    float4 s = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int cc = p.nchunks - 1; cc >= 0; --cc) {
+        const int a = cc * per, z = (cc + 1) * per < nch ? (cc + 1) * per : nch;
+        float4 sc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll 4
+        for (int ch = a; ch < z; ++ch) {
+            const float4 v = part[(size_t)ch * (D / 4)];
+            sc.x += v.x;
+            sc.y += v.y;
+            sc.z += v.z;
+            sc.w += v.w;
+        }
+        const float f = (float)fc;
+        s.x += f * sc.x;
+        s.y += f * sc.y;
+        s.z += f * sc.z;
+        s.w += f * sc.w;
+        fc *= p.lam_c[row * p.nchunks + cc];
+    }
+    float *o = p.o + row * D + c4;
+    if (((uintptr_t)p.o & 15u) == 0u) {
+        *reinterpret_cast<float4 *>(o) = s;
+    } else {
+        o[0] = s.x;
+        o[1] = s.y;
+        o[2] = s.z;
+        o[3] = s.w;
+    }
 }
 
 // ------------------------------------------------------------------ launchers
 template <int D>
-static hipError_t launch_decode_d(const DecParams &p, hipStream_t s)
+static hipError_t dec_logits_d(const DecParams &p, hipStream_t s)
 {
-    {
-        const int G = p.Hq / p.Hkv, ngroups = (G * p.M + 3) / 4;
-        dim3 g1((unsigned)((p.N - p.kb0 + 255) / 256), (unsigned)(p.B * p.Hkv * ngroups));
-        if (p.mode == MODE_PURE8) hipLaunchKernelGGL((dec_logits_kernel<D, MODE_PURE8>), g1, dim3(256), 0, s, p);
-        else if (p.mode == MODE_ALL16) hipLaunchKernelGGL((dec_logits_kernel<D, MODE_ALL16>), g1, dim3(256), 0, s, p);
-        else hipLaunchKernelGGL((dec_logits_kernel<D, MODE_LAMP>), g1, dim3(256), 0, s, p);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    const int64_t nrows = (int64_t)p.B * p.Hq * p.M;
-    dim3 g2((unsigned)((nrows + 3) / 4));
-    if (p.mode == MODE_PURE8) hipLaunchKernelGGL((dec_lamp_kernel<D, MODE_PURE8>), g2, dim3(256), 0, s, p);
-    else if (p.mode == MODE_ALL16) hipLaunchKernelGGL((dec_lamp_kernel<D, MODE_ALL16>), g2, dim3(256), 0, s, p);
-    else hipLaunchKernelGGL((dec_lamp_kernel<D, MODE_LAMP>), g2, dim3(256), 0, s, p);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    const int rows = (p.Hq / p.Hkv) * p.M;
-    dim3 g3((unsigned)((p.N - p.kb0 + PV_CHUNK - 1) / PV_CHUNK), (unsigned)(p.B * p.Hkv));
-    for (int rg0 = 0; rg0 < rows; rg0 += PV_ROWS) {
-        const int nr = rows - rg0;
-        if (nr <= 4) hipLaunchKernelGGL((dec_pv_kernel<D, 4>), g3, dim3(256), 0, s, p, rg0);
-        else if (nr <= 8) hipLaunchKernelGGL((dec_pv_kernel<D, 8>), g3, dim3(256), 0, s, p, rg0);
-        else hipLaunchKernelGGL((dec_pv_kernel<D, PV_ROWS>), g3, dim3(256), 0, s, p, rg0);
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    hipLaunchKernelGGL(dec_reduce_kernel<D>, dim3((unsigned)((nrows * D + 255) / 256)), dim3(256), 0, s, p);
+    const int G = p.Hq / p.Hkv, ngroups = (G * p.M + 3) / 4;
+    const int kend = p.kz < p.N ? p.kz : p.N;
+    dim3 g((unsigned)((kend - p.ka + 255) / 256), (unsigned)(p.B * p.Hkv * ngroups));
+    if (p.mode == MODE_PURE8) hipLaunchKernelGGL((dec_logits_kernel<D, MODE_PURE8>), g, dim3(256), 0, s, p);
+    else if (p.mode == MODE_ALL16) hipLaunchKernelGGL((dec_logits_kernel<D, MODE_ALL16>), g, dim3(256), 0, s, p);
+    else hipLaunchKernelGGL((dec_logits_kernel<D, MODE_LAMP>), g, dim3(256), 0, s, p);
     return hipGetLastError();
 }
 
-hipError_t launch_decode(int D, const DecParams &p, hipStream_t s)
+template <int D>
+static hipError_t dec_decide_d(const DecParams &p, hipStream_t s)
 {
-    if (D == 64) return launch_decode_d<64>(p, s);
-    if (D == 128) return launch_decode_d<128>(p, s);
-    return launch_decode_d<256>(p, s);
+    const int64_t nrows = (int64_t)p.B * p.Hq * p.M;
+    dim3 g((unsigned)((nrows + 3) / 4));
+    if (p.mode == MODE_PURE8) hipLaunchKernelGGL((dec_lamp_kernel<D, MODE_PURE8>), g, dim3(256), 0, s, p);
+    else if (p.mode == MODE_ALL16) hipLaunchKernelGGL((dec_lamp_kernel<D, MODE_ALL16>), g, dim3(256), 0, s, p);
+    else hipLaunchKernelGGL((dec_lamp_kernel<D, MODE_LAMP>), g, dim3(256), 0, s, p);
+    return hipGetLastError();
 }
+
+template <int D>
+static hipError_t dec_pv_d(const DecParams &p, hipStream_t s)
+{
+    const int rows = (p.Hq / p.Hkv) * p.M;
+    const int kend = p.kz < p.N ? p.kz : p.N;
+    dim3 g((unsigned)((kend - p.ka + PV_CHUNK - 1) / PV_CHUNK), (unsigned)(p.B * p.Hkv));
+    for (int rg0 = 0; rg0 < rows; rg0 += PV_ROWS) {
+        const int nr = rows - rg0;
+        if (nr <= 4) hipLaunchKernelGGL((dec_pv_kernel<D, 4>), g, dim3(256), 0, s, p, rg0);
+        else if (nr <= 8) hipLaunchKernelGGL((dec_pv_kernel<D, 8>), g, dim3(256), 0, s, p, rg0);
+        else hipLaunchKernelGGL((dec_pv_kernel<D, PV_ROWS>), g, dim3(256), 0, s, p, rg0);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+template <int D>
+static hipError_t dec_reduce_d(const DecParams &p, hipStream_t s)
+{
+    const int64_t nrows = (int64_t)p.B * p.Hq * p.M;
+    hipLaunchKernelGGL(dec_reduce_kernel<D>, dim3((unsigned)((nrows * (D / 4) + 255) / 256)), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+// One pipeline stage (dec_stage_kernel); a null part is empty.
+template <int D, int MODE, int NR>
+static hipError_t dec_stage_dmn(const DecParams *pd, const DecParams *pl, const DecParams *pp, hipStream_t s)
+{
+    const DecParams &any = pd ? *pd : pl ? *pl : *pp;
+    const int G = any.Hq / any.Hkv, rows = G * any.M, ngroups = (rows + 3) / 4;
+    const int64_t nrows = (int64_t)any.B * any.Hq * any.M;
+    const int nd = pd ? (int)((nrows + 3) / 4) : 0;
+    int nl_x = 1, nl = 0, np_x = 1, np = 0;
+    if (pl) {
+        const int kend = pl->kz < pl->N ? pl->kz : pl->N;
+        nl_x = (kend - pl->ka + 255) / 256;
+        nl = nl_x * pl->B * pl->Hkv * ngroups;
+    }
+    if (pp) {
+        const int kend = pp->kz < pp->N ? pp->kz : pp->N;
+        np_x = (kend - pp->ka + PV_CHUNK - 1) / PV_CHUNK;
+        np = np_x * pp->B * pp->Hkv * ((rows + NR - 1) / NR);
+    }
+    const DecParams &d0 = pd ? *pd : any, &l0 = pl ? *pl : any, &p0 = pp ? *pp : any;
+    hipLaunchKernelGGL((dec_stage_kernel<D, MODE, NR>), dim3((unsigned)(nd + nl + np)), dim3(256), 0, s, d0, l0, p0, nd,
+                       nl_x, nl, np_x, np);
+    return hipGetLastError();
+}
+
+template <int D, int MODE>
+static hipError_t dec_stage_dm(const DecParams *pd, const DecParams *pl, const DecParams *pp, hipStream_t s)
+{
+    const DecParams &any = pd ? *pd : pl ? *pl : *pp;
+    if ((any.Hq / any.Hkv) * any.M <= 4) return dec_stage_dmn<D, MODE, 4>(pd, pl, pp, s);
+    return dec_stage_dmn<D, MODE, 8>(pd, pl, pp, s);
+}
+
+template <int D>
+static hipError_t dec_stage_d(const DecParams *pd, const DecParams *pl, const DecParams *pp, hipStream_t s)
+{
+    const DecParams &any = pd ? *pd : pl ? *pl : *pp;
+    if (any.mode == MODE_PURE8) return dec_stage_dm<D, MODE_PURE8>(pd, pl, pp, s);
+    if (any.mode == MODE_ALL16) return dec_stage_dm<D, MODE_ALL16>(pd, pl, pp, s);
+    return dec_stage_dm<D, MODE_LAMP>(pd, pl, pp, s);
+}
+
+#define LAMP_DEC_BY_D(fn, ...)                                  \
+    if (D == 64) return fn<64>(__VA_ARGS__);                    \
+    if (D == 128) return fn<128>(__VA_ARGS__);                  \
+    if (D == 256) return fn<256>(__VA_ARGS__);                  \
+    return hipErrorInvalidValue;
+
+hipError_t launch_dec_logits(int D, const DecParams &p, hipStream_t s) { LAMP_DEC_BY_D(dec_logits_d, p, s) }
+hipError_t launch_dec_decide(int D, const DecParams &p, hipStream_t s) { LAMP_DEC_BY_D(dec_decide_d, p, s) }
+hipError_t launch_dec_pv(int D, const DecParams &p, hipStream_t s) { LAMP_DEC_BY_D(dec_pv_d, p, s) }
+hipError_t launch_dec_reduce(int D, const DecParams &p, hipStream_t s) { LAMP_DEC_BY_D(dec_reduce_d, p, s) }
+hipError_t launch_dec_stage(int D, const DecParams *pd, const DecParams *pl, const DecParams *pp, hipStream_t s)
+{
+    if (!pd && !pl && !pp) return hipSuccess;
+    LAMP_DEC_BY_D(dec_stage_d, pd, pl, pp, s)
+}
+
+#undef LAMP_DEC_BY_D
 
 } // namespace lamp

@@ -494,25 +494,45 @@ int lamp_reserve(int device, size_t bytes)
     return fail(LAMP_ERR_HIP, "lamp_reserve: %s", hipGetErrorString(e));
 }
 
-// Byte sizes of the decode workspace: pre-scaled queries, 8-bit and 16-bit
-// logit codes, per-tile factors and mu_hat, partial outputs of the key chunks.
+// Byte sizes of the decode workspace: 8-bit and 16-bit logit codes, per-tile
+// factors and mu_hat, partial outputs of the P.V pieces, and per row the
+// state carried between key chunks and each chunk's product of rescale
+// factors.
 struct DecLayout {
-    size_t qt, y8, y16, f, mu, part, total;
+    size_t y8, y16, f, mu, part, mu_st, om_st, lam_c, total;
 };
 
 static DecLayout dec_layout(int B, int Hq, int M, int N, int d)
 {
-    const int64_t Np = ((int64_t)N + 63) / 64 * 64, nch = ((int64_t)N + 511) / 512;   // key chunks of the P.V pass
+    const int64_t Np = ((int64_t)N + 63) / 64 * 64, nch = ((int64_t)N + 511) / 512;   // 512-key pieces of the P.V pass
     const size_t nrows = (size_t)B * Hq * M;
     DecLayout l;
-    l.qt = align256(nrows * d * 4);
     l.y8 = align256(nrows * Np);
     l.y16 = align256(nrows * Np * 2);
     l.f = align256(nrows * (Np / 64) * 8);
     l.mu = align256(nrows * (Np / 64) * 4);
     l.part = align256(nrows * nch * d * 4);
-    l.total = l.qt + l.y8 + l.y16 + l.f + l.mu + l.part;
+    l.mu_st = align256(nrows * 4);
+    l.om_st = align256(nrows * 8);
+    l.lam_c = align256(nrows * lamp::DEC_MAX_CHUNKS * 8);
+    l.total = l.y8 + l.y16 + l.f + l.mu + l.part + l.mu_st + l.om_st + l.lam_c;
     return l;
+}
+
+// The decode form's key chunks: about DEC_CHUNKS chunks of a multiple of 512
+// keys (one when the keys from kb0 are at most 2048); the last ends at Np.
+static constexpr int DEC_CHUNKS = 2;
+static void dec_chunks(int N, int kb0, int *ck, int *nchunks)
+{
+    const int64_t span = (int64_t)N - kb0;
+    if (span <= 2048) {
+        *ck = (int)((span + 511) / 512 * 512);
+        *nchunks = 1;
+        return;
+    }
+    const int64_t per = (span + DEC_CHUNKS - 1) / DEC_CHUNKS;
+    *ck = (int)((per + 511) / 512 * 512);
+    *nchunks = (int)((span + *ck - 1) / *ck);
 }
 
 size_t lamp_attn_decode_workspace_size(int B, int Hq, int Hkv, int M, int N, int d)
@@ -534,7 +554,8 @@ int lamp_attn_decode(const uint16_t *q, const uint16_t *k, const uint16_t *v, in
         return fail(LAMP_ERR_INVALID_ARG, "null pointer among q, k, v, o, lse, mask");
     if (!(delta >= 0.0) || std::isinf(delta)) return fail(LAMP_ERR_INVALID_ARG, "delta must be finite and >= 0");
     if (!(tau >= 0.0)) return fail(LAMP_ERR_INVALID_ARG, "tau must be >= 0 (or +inf)");
-    if (flags) return fail(LAMP_ERR_INVALID_ARG, "unknown flags 0x%x (the decode form takes none)", flags);
+    if (flags & ~(unsigned)LAMP_DECODE_SERIAL)
+        return fail(LAMP_ERR_INVALID_ARG, "unknown flags 0x%x (the decode form takes LAMP_DECODE_SERIAL)", flags);
     if (tk != 64) return fail(LAMP_ERR_UNSUPPORTED, "keys per update tk=%d not built (64)", tk);
     if (extra && (extra->stats || extra->dbg_y8 || extra->dbg_y16))
         return fail(LAMP_ERR_UNSUPPORTED, "the decode form takes a workspace only (no stats, no logit observables)");
@@ -559,13 +580,21 @@ int lamp_attn_decode(const uint16_t *q, const uint16_t *k, const uint16_t *v, in
     if (rc) return rc;
     {
         char *base = static_cast<char *>(wsb);
-        p.qt = reinterpret_cast<float *>(base);
-        p.y8 = reinterpret_cast<uint8_t *>(base + lay.qt);
-        p.y16 = reinterpret_cast<uint16_t *>(base + lay.qt + lay.y8);
-        p.f = reinterpret_cast<double *>(base + lay.qt + lay.y8 + lay.y16);
-        p.mut = reinterpret_cast<float *>(base + lay.qt + lay.y8 + lay.y16 + lay.f);
-        p.part = reinterpret_cast<float *>(base + lay.qt + lay.y8 + lay.y16 + lay.f + lay.mu);
+        p.y8 = reinterpret_cast<uint8_t *>(base);
+        p.y16 = reinterpret_cast<uint16_t *>(base + lay.y8);
+        p.f = reinterpret_cast<double *>(base + lay.y8 + lay.y16);
+        p.mut = reinterpret_cast<float *>(base + lay.y8 + lay.y16 + lay.f);
+        size_t off = lay.y8 + lay.y16 + lay.f + lay.mu;
+        p.part = reinterpret_cast<float *>(base + off);
+        off += lay.part;
+        p.mu_st = reinterpret_cast<float *>(base + off);
+        off += lay.mu_st;
+        p.om_st = reinterpret_cast<double *>(base + off);
+        off += lay.om_st;
+        p.lam_c = reinterpret_cast<double *>(base + off);
     }
+    p.q = q;
+    p.qscale = scale_of(d);
     p.k = k;
     p.v = v;
     p.o = o;
@@ -594,9 +623,49 @@ int lamp_attn_decode(const uint16_t *q, const uint16_t *k, const uint16_t *v, in
         for (int i = 0; i < 3; ++i) HIP_TRY(hipEventCreate(&tc.e[i]));
         HIP_TRY(hipEventRecord(tc.e[0], s));
     }
-    HIP_TRY(lamp::launch_prescale_q(q, const_cast<float *>(p.qt), B * Hq, M, d, scale_of(d), s));
-    if (timed) HIP_TRY(hipEventRecord(tc.e[1], s));
-    HIP_TRY(lamp::launch_decode(d, p, s));
+    if (timed) HIP_TRY(hipEventRecord(tc.e[1], s));   // no prepass: the logits scale the queries
+    auto chunk_of = [&](int c) {
+        lamp::DecParams pc = p;
+        pc.chunk = c;
+        pc.ka = p.kb0 + c * p.ck;
+        pc.kz = c == p.nchunks - 1 ? Np : pc.ka + p.ck;
+        return pc;
+    };
+    if (flags & LAMP_DECODE_SERIAL) {
+        // one key chunk, the passes one after another
+        p.ck = (N - p.kb0 + 511) / 512 * 512;
+        p.nchunks = 1;
+        const lamp::DecParams pc = chunk_of(0);
+        HIP_TRY(lamp::launch_dec_logits(d, pc, s));
+        HIP_TRY(lamp::launch_dec_decide(d, pc, s));
+        HIP_TRY(lamp::launch_dec_pv(d, pc, s));
+    } else if ((Hq / Hkv) * M <= lamp::DEC_STAGE_MAX_ROWS) {
+        // the key chunks in a pipeline of stage launches on `s`: stage g
+        // runs the logits of chunk g (bound by the VALU), the decisions of
+        // chunk g - 1 (bound by latency; they take the chunks in order, each
+        // continuing the row state of the one before) and P.V of chunk g - 2
+        // (bound by HBM) side by side
+        dec_chunks(N, p.kb0, &p.ck, &p.nchunks);
+        for (int g = 0; g < p.nchunks + 2; ++g) {
+            lamp::DecParams pl, pd, pp;
+            const bool hl = g < p.nchunks, hd = g >= 1 && g - 1 < p.nchunks, hp = g >= 2;
+            if (hl) pl = chunk_of(g);
+            if (hd) pd = chunk_of(g - 1);
+            if (hp) pp = chunk_of(g - 2);
+            HIP_TRY(lamp::launch_dec_stage(d, hd ? &pd : nullptr, hl ? &pl : nullptr, hp ? &pp : nullptr, s));
+        }
+    } else {
+        // more query rows per key/value head than a stage holds: the chunks
+        // one after another
+        dec_chunks(N, p.kb0, &p.ck, &p.nchunks);
+        for (int c = 0; c < p.nchunks; ++c) {
+            const lamp::DecParams pc = chunk_of(c);
+            HIP_TRY(lamp::launch_dec_logits(d, pc, s));
+            HIP_TRY(lamp::launch_dec_decide(d, pc, s));
+            HIP_TRY(lamp::launch_dec_pv(d, pc, s));
+        }
+    }
+    HIP_TRY(lamp::launch_dec_reduce(d, p, s));
     if (timed) {
         HIP_TRY(hipEventRecord(tc.e[2], s));
         std::lock_guard<std::mutex> lk(g_tmu);

@@ -140,6 +140,9 @@ MU_TRUNC = 2     # 8-bit shifts against mu_hat truncated to e4m3 (SIM profile: t
 SIM_PROFILE = 4  # the SIM precision profile (FP32 range, 3 / 11 mantissa bits, no saturation)
 CHECK_FINITE = 8  # check q, k, v for NaN / infinity first (synchronous; LAMP_ERR_NONFINITE_INPUT)
 COMPACT = 16     # the compact register layout of Sec. 3.3 as the kernel's schedule (same results)
+# attn_decode flag: one key chunk and the passes one after another instead of the key-chunk
+# pipeline (same masks and lse; O equal up to the order of its final sums)
+DECODE_SERIAL = 256
 
 
 def _check_out(t, name, shape, dtype, device):

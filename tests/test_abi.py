@@ -104,6 +104,9 @@ def test_decode_rejects_bad_arguments_without_gpu():
     assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 300, 256, 128, 1, 0, 64, 2 ** -8, 0.5, 0, d, d, d, None, None) == 1
     assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 96, 1, 0, 64, 2 ** -8, 0.5, 0, d, d, d, None, None) == 2
     assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 128, 1, 0, 64, 2 ** -8, -1.0, 0, d, d, d, None, None) == 1
+    # flag bits other than LAMP_DECODE_SERIAL
+    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 128, 1, 0, 64, 2 ** -8, 0.5, 512, d, d, d, None, None) == 1
+    assert lib.lamp_attn_decode(d, d, d, 1, 4, 1, 1, 256, 128, 1, 0, 64, 2 ** -8, 0.5, 257, d, d, d, None, None) == 1
 
 
 def test_timing_read_without_calls():

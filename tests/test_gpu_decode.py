@@ -32,9 +32,9 @@ def _say(*a):
     sys.stdout.flush()
 
 
-def _compare(L, w, tau, rows=None):
+def _compare(L, w, tau, rows=None, flags=0):
     q, k, v = W.make_inputs(w)
-    o, lse, mask = L.attn_decode(q.cuda(), k.cuda(), v.cuda(), w.causal, w.window, w.bk, w.delta, tau)
+    o, lse, mask = L.attn_decode(q.cuda(), k.cuda(), v.cuda(), w.causal, w.window, w.bk, w.delta, tau, flags=flags)
     torch.cuda.synchronize()
     ro, rlse, rmask = O.decode(O.bf16_bits(q), O.bf16_bits(k), O.bf16_bits(v), w.causal, w.window, w.bk, w.delta,
                                tau, rows=rows)
@@ -61,10 +61,33 @@ DEC_CASES = [
 ]
 
 
+# the two schedules of the pass: the default pipeline of key chunks and the
+# serial one (one chunk, the passes one after another)
+FORMS = {"pipelined": 0, "serial": 256}
+
+
+@pytest.mark.parametrize("form", sorted(FORMS))
 @pytest.mark.parametrize("tau", [math.inf, 1.0, 0.5, 2.0 ** -5, 0.0])
 @pytest.mark.parametrize("w", DEC_CASES, ids=[w.name for w in DEC_CASES])
-def test_decode_parity_small(L, w, tau):
-    _compare(L, w, tau)
+def test_decode_parity_small(L, w, tau, form):
+    _compare(L, w, tau, flags=FORMS[form])
+
+
+# caches long enough for several key chunks: 3 chunks of 1024 keys with a
+# window (the first visible key past 0) and 6 query rows per key/value head,
+# and 4 chunks of 1536 keys with 12 rows per head (more than a pipeline stage
+# holds: the chunks one after another)
+DEC_CHUNKED = [
+    W.small("dg_chunks_window", B=2, Hq=6, Hkv=1, N=3000, d=128, causal=1, window=2600, seed=431, M=1, bk=64),
+    W.small("dg_chunks_rows12", B=1, Hq=12, Hkv=2, N=6000, d=64, causal=1, seed=432, M=2, bk=64),
+]
+
+
+@pytest.mark.parametrize("form", sorted(FORMS))
+@pytest.mark.parametrize("tau", [math.inf, 0.5, 2.0 ** -5, 0.0])
+@pytest.mark.parametrize("w", DEC_CHUNKED, ids=[w.name for w in DEC_CHUNKED])
+def test_decode_parity_chunked(L, w, tau, form):
+    _compare(L, w, tau, flags=FORMS[form])
 
 
 DEC_DEGENERATE = [
@@ -74,10 +97,11 @@ DEC_DEGENERATE = [
 ]
 
 
+@pytest.mark.parametrize("form", sorted(FORMS))
 @pytest.mark.parametrize("tau", [math.inf, 0.5, 2.0 ** -5, 0.0])
 @pytest.mark.parametrize("w", DEC_DEGENERATE, ids=[w.name for w in DEC_DEGENERATE])
-def test_decode_degenerate(L, w, tau):
-    err, mask = _compare(L, w, tau)
+def test_decode_degenerate(L, w, tau, form):
+    err, mask = _compare(L, w, tau, flags=FORMS[form])
     if "zero_q" in w.extra and 0 < tau < math.inf:
         # every logit is 0, so |mu| delta = 0 and every tile's maximizer fails the test
         assert np.all((mask == 1).sum(axis=-1) == -(-w.N // 64))
@@ -91,23 +115,27 @@ def test_decode_empty(L):
     assert o.numel() == 0 and mask.numel() == 0
 
 
-def test_decode_maximum_cache(L):
+@pytest.mark.parametrize("form", sorted(FORMS))
+def test_decode_maximum_cache(L, form):
     """A cache of N = 2^20 keys, the longest the library accepts, for two
     query rows of four heads; every row checked against the oracle."""
     w = W.small("dg_max_n", B=1, Hq=4, Hkv=1, N=1 << 20, d=128, causal=1, seed=421, M=2, bk=64, kind="gauss")
     t0 = time.time()
-    err, mask = _compare(L, w, 0.5)
-    _say("decode N = 2^20: O err %.2e, mask %s (%.1f s)" % (err, np.bincount(mask.ravel(), minlength=4),
-                                                            time.time() - t0))
+    err, mask = _compare(L, w, 0.5, flags=FORMS[form])
+    _say("decode N = 2^20 (%s): O err %.2e, mask %s (%.1f s)" % (form, err, np.bincount(mask.ravel(), minlength=4),
+                                                                 time.time() - t0))
 
 
+@pytest.mark.parametrize("form", sorted(FORMS))
 @pytest.mark.parametrize("tau", W.TAU_SWEEP)
-def test_decode_config6_sampled(L, tau):
+def test_decode_config6_sampled(L, tau, form):
     """Qwen3-8B-shaped decode (32 sequences, 32/8 heads, 8K cache) at full
-    size; the oracle computes 12 rows spread over sequences and heads."""
+    size, in both schedules; the oracle computes 12 rows spread over
+    sequences and heads."""
     w = W.CONFIGS[6]
     rows = [0, 7, 31, 100, 257, 400, 511, 600, 777, 900, 1000, 1023]
     t0 = time.time()
-    err, mask = _compare(L, w, tau, rows=rows)
-    _say("config 6 tau %s sampled: O err %.2e, mask %s (%.1f s)" % (tau, err, np.bincount(mask.ravel(), minlength=4),
-                                                                   time.time() - t0))
+    err, mask = _compare(L, w, tau, rows=rows, flags=FORMS[form])
+    _say("config 6 tau %s %s sampled: O err %.2e, mask %s (%.1f s)" % (tau, form, err,
+                                                                      np.bincount(mask.ravel(), minlength=4),
+                                                                      time.time() - t0))
