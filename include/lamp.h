@@ -317,8 +317,8 @@ int lamp_attn_fwd_sr(const uint16_t *q, const uint16_t *k, const uint16_t *v,
  * recomputed by the look-ahead test -- every key at tau = 0 --, 2 recomputed
  * by the knapsack, 3 invisible).  Built: tk = 64, d in {64, 128, 256};
  * flags: 0 or LAMP_DECODE_SERIAL.  By default the keys from the first one
- * any row sees are taken in up to 4 chunks of a multiple of 512 keys (one
- * when there are at most 2048): the decisions visit the chunks in order,
+ * any row sees are taken in 2 chunks of a multiple of 512 keys (one when
+ * there are at most 2048): the decisions visit the chunks in order,
  * carrying each row's running maximum and sum, and with at most 8 query rows
  * per key/value head the logits of chunk c + 1, the decisions of chunk c and
  * P.V of chunk c - 1 run side by side in one launch.  B = 0 or M = 0 returns

@@ -35,6 +35,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "lamp_decode.h"
 #include "lamp_device.h"
 #include "lamp_kernels.h"
 
@@ -767,7 +768,7 @@ __device__ __forceinline__ void dec_decide_role(const DecParams &p, DecideLds<MO
 // arithmetic (the first step before the weights), feeding 8 FMAs per query row,
 // and reads the key's weights from LDS (one broadcast read).  Partial outputs
 // per chunk go to a workspace; phase 4 adds them up.
-constexpr int PV_CHUNK = 512, PV_ROWS = 16;
+constexpr int PV_CHUNK = DEC_PV_KEYS, PV_ROWS = 16;
 
 template <int D, int NR>
 struct PvLds {

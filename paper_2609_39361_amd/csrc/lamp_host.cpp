@@ -10,6 +10,7 @@
 #include <vector>
 
 #include "lamp.h"
+#include "lamp_decode.h"
 #include "lamp_kernels.h"
 
 namespace {
@@ -504,7 +505,8 @@ struct DecLayout {
 
 static DecLayout dec_layout(int B, int Hq, int M, int N, int d)
 {
-    const int64_t Np = ((int64_t)N + 63) / 64 * 64, nch = ((int64_t)N + 511) / 512;   // 512-key pieces of the P.V pass
+    const int64_t Np = ((int64_t)N + 63) / 64 * 64;
+    const int64_t nch = ((int64_t)N + lamp::DEC_PV_KEYS - 1) / lamp::DEC_PV_KEYS;   // pieces of the P.V pass
     const size_t nrows = (size_t)B * Hq * M;
     DecLayout l;
     l.y8 = align256(nrows * Np);
@@ -519,19 +521,23 @@ static DecLayout dec_layout(int B, int Hq, int M, int N, int d)
     return l;
 }
 
-// The decode form's key chunks: about DEC_CHUNKS chunks of a multiple of 512
-// keys (one when the keys from kb0 are at most 2048); the last ends at Np.
+// The decode form's key chunks: about DEC_CHUNKS chunks of a multiple of
+// DEC_PV_KEYS keys (one when the keys from kb0 are at most 2048); the last
+// ends at Np.
 static constexpr int DEC_CHUNKS = 2;
+static int64_t round_pv(int64_t x)
+{
+    return (x + lamp::DEC_PV_KEYS - 1) / lamp::DEC_PV_KEYS * lamp::DEC_PV_KEYS;
+}
 static void dec_chunks(int N, int kb0, int *ck, int *nchunks)
 {
     const int64_t span = (int64_t)N - kb0;
     if (span <= 2048) {
-        *ck = (int)((span + 511) / 512 * 512);
+        *ck = (int)round_pv(span);
         *nchunks = 1;
         return;
     }
-    const int64_t per = (span + DEC_CHUNKS - 1) / DEC_CHUNKS;
-    *ck = (int)((per + 511) / 512 * 512);
+    *ck = (int)round_pv((span + DEC_CHUNKS - 1) / DEC_CHUNKS);
     *nchunks = (int)((span + *ck - 1) / *ck);
 }
 
@@ -633,7 +639,7 @@ int lamp_attn_decode(const uint16_t *q, const uint16_t *k, const uint16_t *v, in
     };
     if (flags & LAMP_DECODE_SERIAL) {
         // one key chunk, the passes one after another
-        p.ck = (N - p.kb0 + 511) / 512 * 512;
+        p.ck = (int)round_pv(N - p.kb0);
         p.nchunks = 1;
         const lamp::DecParams pc = chunk_of(0);
         HIP_TRY(lamp::launch_dec_logits(d, pc, s));
