@@ -14,24 +14,28 @@
 //      recomputed in 16 bits against the same mu_hat;
 //   3. omega, O and mu are updated (Sec. 2, online softmax).
 //
-// Four kernels:
-//   dec_logits_kernel   the logits of every (query row, key), which depend on
-//                       no decision, in 8 bits and in 16 bits (codes), and
-//                       the mask code of every key: one thread per key, the 4
-//                       query rows of a group accumulated together, queries
-//                       read from LDS (broadcast), keys staged through LDS
-//                       from coalesced loads of the bf16 cache (no fp32 copy);
-//   dec_lamp_kernel     the decisions, one wave per query row: lane i holds
-//                       key i of the tile; DPP reductions, a bitonic sort of
-//                       the costs and the sequential sum; runs of up to 8
-//                       tiles that keep the running maximum and pass the
-//                       knapsack's quick acceptance are evaluated together;
-//                       it records mu_hat and the rescale factors per tile
-//                       and the mask codes of the recomputed keys;
-//   dec_pv_kernel       P.V in parallel over key chunks for all query rows of
-//                       a key/value head (fp32 FMAs; every exponential is
-//                       exact in fp32), the weights recomputed from the codes;
-//   dec_reduce_kernel   the sum of the chunks' partial outputs.
+// Three passes over a chunk of keys, each a device function (a role) that a
+// workgroup runs:
+//   logits     the logits of every (query row, key), which depend on no
+//              decision, in 8 bits and in 16 bits (codes), and the mask code
+//              of every key: one thread per key, the 4 query rows of a group
+//              accumulated together, queries read from LDS (broadcast), keys
+//              staged through LDS from coalesced loads of the bf16 cache (no
+//              fp32 copy);
+//   decisions  one wave per query row: lane i holds key i of the tile; DPP
+//              reductions, a bitonic sort of the costs and the sequential sum;
+//              runs of up to 8 tiles that keep the running maximum and pass
+//              the knapsack's quick acceptance are evaluated together; the row
+//              state (mu, omega) passes from chunk to chunk, and each chunk
+//              records mu_hat and its rescale factors per tile and the mask
+//              codes of the recomputed keys;
+//   P.V        in parallel over 512-key pieces for all query rows of a
+//              key/value head (fp32 FMAs; every exponential is exact in fp32),
+//              the weights recomputed from the codes.
+// dec_stage_kernel runs the decisions of one chunk, the logits of the next and
+// P.V of the one before in one launch (the chunk pipeline); dec_logits_kernel,
+// dec_lamp_kernel and dec_pv_kernel run one role each (the serial schedule);
+// dec_reduce_kernel combines the pieces' partial outputs over the chunks.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
