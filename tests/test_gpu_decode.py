@@ -77,11 +77,12 @@ def test_decode_parity_small(L, w, tau, form):
 # window (the first visible key past 0) and 6 query rows per key/value head;
 # 2 chunks of 3072 keys with 12 rows per head (more than a pipeline stage
 # holds: the chunks one after another); 2 chunks of 1536 keys at d = 256 with
-# 3 rows per head and a last chunk that ends in a partial tile
+# 2 query positions of 3 heads per key/value head (6 rows, each its own causal
+# end) and a last chunk that ends in a partial tile
 DEC_CHUNKED = [
     W.small("dg_chunks_window", B=2, Hq=6, Hkv=1, N=3000, d=128, causal=1, window=2600, seed=431, M=1, bk=64),
     W.small("dg_chunks_rows12", B=1, Hq=12, Hkv=2, N=6000, d=64, causal=1, seed=432, M=2, bk=64),
-    W.small("dg_chunks_d256", B=1, Hq=3, Hkv=1, N=2999, d=256, causal=1, seed=433, M=1, bk=64),
+    W.small("dg_chunks_d256", B=1, Hq=3, Hkv=1, N=2999, d=256, causal=1, seed=433, M=2, bk=64),
 ]
 
 
