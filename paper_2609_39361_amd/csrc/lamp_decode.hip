@@ -80,6 +80,38 @@ __device__ __forceinline__ double dpp_f64(double v)
     return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
 }
 
+// The value of lane (this lane xor j): within a 16-lane row by DPP (j = 1, 2
+// and 8 one move: quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_ror:8; j = 4
+// two: row_half_mirror then quad_perm [3,2,1,0]), across rows by a lane
+// permute.  j is a constant wherever the callers' loops are unrolled.
+template <int J>
+__device__ __forceinline__ uint32_t xor_dpp(uint32_t v)
+{
+    if constexpr (J == 1) return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, true);
+    if constexpr (J == 2) return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, true);
+    if constexpr (J == 8) return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x128, 0xF, 0xF, true);
+    const int w = __builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, true);
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, w, 0x1B, 0xF, 0xF, true);
+}
+
+__device__ __forceinline__ uint32_t xor_lanes(uint32_t v, int j)
+{
+    switch (j) {
+    case 1: return xor_dpp<1>(v);
+    case 2: return xor_dpp<2>(v);
+    case 4: return xor_dpp<4>(v);
+    case 8: return xor_dpp<8>(v);
+    default: return (uint32_t)__shfl_xor((int)v, j, 64);
+    }
+}
+
+__device__ __forceinline__ double xor_lanes(double v, int j)
+{
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = xor_lanes((uint32_t)u, j), hi = xor_lanes((uint32_t)(u >> 32), j);
+    return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
 __device__ __forceinline__ float readlane_f32(float v, int l)
 {
     return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
@@ -446,8 +478,8 @@ struct RowDecider {
                 for (int k = 2; k <= 64; k <<= 1) {
 #pragma unroll
                     for (int j = k >> 1; j >= 1; j >>= 1) {
-                        const double ok = __shfl_xor(kap, j, 64);
-                        const int oi = __shfl_xor(idx, j, 64);
+                        const double ok = xor_lanes(kap, j);
+                        const int oi = (int)xor_lanes((uint32_t)idx, j);
                         const bool mine_less = kap < ok || (kap == ok && idx < oi);
                         const bool up = (lane & k) == 0;
                         const bool lower = (lane & j) == 0;
