@@ -125,6 +125,21 @@ __device__ __forceinline__ double readlane_f64(double v, int l)
     return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
 }
 
+// Inclusive prefix sum over the wave in fp64: within each 16-lane row by DPP
+// row shifts of 1, 2, 4 and 8 (lanes shifted in from outside the row read 0),
+// then the totals of the rows below added in.
+__device__ __forceinline__ double prefix_sum_f64(double v)
+{
+    v += dpp_f64<0x111>(v);
+    v += dpp_f64<0x112>(v);
+    v += dpp_f64<0x114>(v);
+    v += dpp_f64<0x118>(v);
+    const double t0 = readlane_f64(v, 15), t1 = readlane_f64(v, 31), t2 = readlane_f64(v, 47);
+    const int r = (int)(__lane_id() >> 4);
+    const double off = (r >= 1 ? t0 : 0.0) + ((r >= 2 ? t1 : 0.0) + (r >= 3 ? t2 : 0.0));
+    return v + off;
+}
+
 __device__ __forceinline__ float wave_max_f32(float v)
 {
     float o;
@@ -495,15 +510,32 @@ struct RowDecider {
                 // index of the first cost that is infinite or would pass the
                 // limit is the count kept; the sum after it is not used)
                 const double lim = (p->tau * omh) * omh;
-                double xi = 0.0;
+                // First from a prefix scan of the sorted costs (any
+                // association), whose sums differ from the sequential ones
+                // by less than 70 units of 2^-53 of the prefix: the
+                // sequential sum is monotone, so the crossing is the scan's
+                // when neither neighbour of it lies within 2^-44 of the limit
+                // (infinite costs, last in the order, fail either way).
                 int nkeep = 64;
+                {
+                    const double sc = prefix_sum_f64(kap);
+                    const uint64_t okb = __ballot(kap != __builtin_inf() && sc <= lim);
+                    const int n = okb == ~0ull ? 64 : __builtin_ctzll(~okb);
+                    const bool near = (lane == n - 1 || lane == n) && kap != __builtin_inf() &&
+                                      __builtin_fabs(sc - lim) <= 0x1p-44 * sc;
+                    nkeep = wave_any(near) ? -1 : n;
+                }
+                if (nkeep < 0) {   // too close to call: the greedy itself
+                    double xi = 0.0;
+                    nkeep = 64;
 #pragma unroll
-                for (int i = 0; i < 64; ++i) {
-                    const double kk = readlane_f64(kap, i);
-                    const double nx = xi + kk;
-                    const bool ok = kk != __builtin_inf() && nx <= lim;
-                    nkeep = (nkeep == 64 && !ok) ? i : nkeep;
-                    xi = nx;
+                    for (int i = 0; i < 64; ++i) {
+                        const double kk = readlane_f64(kap, i);
+                        const double nx = xi + kk;
+                        const bool ok = kk != __builtin_inf() && nx <= lim;
+                        nkeep = (nkeep == 64 && !ok) ? i : nkeep;
+                        xi = nx;
+                    }
                 }
                 // sorted position -> key lane: each sorted slot sends its
                 // recompute flag to the lane of its key (idx is a permutation)
