@@ -826,16 +826,17 @@ __device__ __forceinline__ void dec_decide_role(const DecParams &p, DecideLds<MO
 }
 
 // ------------------------------------------------------------------ phase 3
-// P.V: one workgroup per (chunk of PV_CHUNK keys from key kb0, b, key/value
-// head) for NR of the R = G*M query rows of the head.  The chunk's weights
-// E f_t of those rows are first formed in LDS: E from the key's mask code and
-// logit (the 8-bit code through the ue5m3 table, or the recomputed 16-bit
-// logit through the ue5m11 table) against the tile's mu_hat, the same
-// computation as in the decisions; then the main loop issues one 16-byte load
-// of V (8 channels of one key) per lane and key, one step ahead of its
-// arithmetic (the first step before the weights), feeding 8 FMAs per query row,
-// and reads the key's weights from LDS (one broadcast read).  Partial outputs
-// per chunk go to a workspace; phase 4 adds them up.
+// P.V: one workgroup per (piece of PV_CHUNK keys of the launch's key chunk,
+// b, key/value head) for NR of the R = G*M query rows of the head.  The
+// piece's weights E g_t of those rows are first formed in LDS: E from the
+// key's mask code and logit (the 8-bit code through the ue5m3 table, or the
+// recomputed 16-bit logit through the ue5m11 table) against the tile's
+// mu_hat, the same computation as in the decisions, and g_t the tile's factor
+// within its chunk; then the main loop issues one 16-byte load of V (8
+// channels of one key) per lane and key, one step ahead of its arithmetic
+// (the first step before the weights), feeding 8 FMAs per query row, and
+// reads the key's weights from LDS (one broadcast read).  Partial outputs per
+// piece go to a workspace; the reduce kernel combines them over the chunks.
 constexpr int PV_CHUNK = DEC_PV_KEYS, PV_ROWS = 16;
 
 template <int D, int NR>
