@@ -42,13 +42,16 @@ SIM_FLAG = 4
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lamp_fwd16_kernel.qwen3-8b-prefill-8k.hbm_traffic.md")
 VALU_FILE = os.path.join(ROOT, "profiles", "lamp_fwd16_kernel.qwen3-8b-prefill-8k.valu_issue.md")
+DEC_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lamp_decode.qwen3-8b-decode-b32-kv8k.hbm_traffic.md")
 KERNEL_SOURCES = ["lamp_fwd.hip", "lamp_fwd16.hip", "lamp_loops.h", "lamp_sr.h", "lamp_device.h", "lamp_kernels.h", "lamp_stats.h"]
+DEC_SOURCES = ["lamp_decode.hip", "lamp_decode.h", "lamp_device.h", "lamp_loops.h", "lamp_host.cpp"]
 
 
-def kernel_source_hash():
-    """sha256 over the forward kernel's sources, to tie counter readings to them."""
+def kernel_source_hash(sources=None):
+    """sha256 over the forward kernel's sources (or the given ones), to tie
+    counter readings to them."""
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
+    for name in sources or KERNEL_SOURCES:
         with open(os.path.join(ROOT, "paper_2609_39361_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
@@ -59,7 +62,7 @@ def _mode_of(tau):
     return 1 if math.isinf(tau) else (2 if tau == 0 else 0)
 
 
-def _profile_record(path, tag, workload, tau, flags=0):
+def _profile_record(path, tag, workload, tau, flags=0, sources=None):
     """The `tag: {json}` line of a committed profile summary, when it was taken
     on the current kernel sources and on this workload; else None."""
     try:
@@ -70,7 +73,7 @@ def _profile_record(path, tag, workload, tau, flags=0):
     for line in text.splitlines():
         if line.startswith(tag + ": "):
             rec = json.loads(line[len(tag) + 2:])
-            if rec.get("source_sha256") == kernel_source_hash() and rec.get("workload") == workload \
+            if rec.get("source_sha256") == kernel_source_hash(sources) and rec.get("workload") == workload \
                     and rec.get("tau") == tau and rec.get("flags", 0) == flags:
                 return rec
     return None
@@ -80,6 +83,26 @@ def measured_traffic(workload, tau, flags=0):
     """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE runs."""
     rec = _profile_record(TRAFFIC_FILE, "traffic-json", workload, tau, flags)
     return None if rec is None else rec["bytes_per_launch"]
+
+
+def measured_decode_traffic(workload, tau, flags=0):
+    """HBM bytes per decode step (all its kernels) from the committed
+    FETCH_SIZE / WRITE_SIZE runs."""
+    rec = _profile_record(DEC_TRAFFIC_FILE, "traffic-json", workload, tau, flags, DEC_SOURCES)
+    return None if rec is None else rec["bytes_per_step"]
+
+
+def copy_calibration(mib, dev):
+    """One plain negating copy of `mib` MiB of fp32 (reads and writes that many
+    bytes), whose counter readings calibrate the HBM byte counters."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 def measured_valu_issue(workload, tau, flags=0):
@@ -264,7 +287,7 @@ def main_decode(args, w, tau, flags=0):
         "lookahead_recomputes": s1, "knapsack_recomputes": s2,
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+            "frac": achieved / HBM_PEAK_GBS, "traffic": measured_decode_traffic(w.name, tau, flags),
             "kernel": " + ".join(kernels),
             "kernel_ms": kernel_ms, "prepass_ms": pre_ms_sum / launches,
             "bytes_per_launch": nbytes,
@@ -316,6 +339,8 @@ def main():
         if any(f not in (0, lamp.DECODE_SERIAL) for f in flags_list) or args.sr_seed is not None:
             raise SystemExit("the decode form takes flags 0 or %d (serial) and no stochastic rounding"
                              % lamp.DECODE_SERIAL)
+        if args.copy_calib_mib > 0:
+            copy_calibration(args.copy_calib_mib, torch.device("cuda:0"))
         for flags in flags_list:
             for tau in taus:
                 main_decode(args, w, tau, flags)
@@ -328,13 +353,7 @@ def main():
     mask = torch.empty((w.B, w.Hq, -(-w.N // w.bq), -(-w.N // (w.bk * w.nk)) * w.nk), dtype=torch.uint8, device=dev)
     out = (o, lse, mask)
     if args.copy_calib_mib > 0:
-        n = args.copy_calib_mib * (1 << 20) // 4
-        src = torch.ones(n, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        torch.neg(src, out=dst)
-        torch.cuda.synchronize()
-        del src, dst
+        copy_calibration(args.copy_calib_mib, dev)
     for flags in flags_list:
         for tau in taus:
             run_fwd(args, w, tau, flags, (q, k, v), (qd, kd, vd), out, dev)
