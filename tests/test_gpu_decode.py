@@ -83,6 +83,10 @@ DEC_CHUNKED = [
     W.small("dg_chunks_window", B=2, Hq=6, Hkv=1, N=3000, d=128, causal=1, window=2600, seed=431, M=1, bk=64),
     W.small("dg_chunks_rows12", B=1, Hq=12, Hkv=2, N=6000, d=64, causal=1, seed=432, M=2, bk=64),
     W.small("dg_chunks_d256", B=1, Hq=3, Hkv=1, N=2999, d=256, causal=1, seed=433, M=2, bk=64),
+    # d = 64 through the chunk pipeline: 4 rows per key/value head, and 8
+    # rows with every key visible
+    W.small("dg_chunks_d64_r4", B=1, Hq=4, Hkv=2, N=4500, d=64, causal=1, seed=434, M=2, bk=64),
+    W.small("dg_chunks_d64_r8_noncausal", B=1, Hq=4, Hkv=1, N=4100, d=64, causal=0, seed=435, M=2, bk=64),
 ]
 
 
